@@ -1,0 +1,8 @@
+"""CPU oracle for the SKIP routing core (test infrastructure only: imported
+by the test-suite, the package smoke check and the benchmark's CPU baseline,
+never by the product path)."""
+from .skip_oracle import (  # noqa: F401
+    RouteResult, adjacency_to_csr, bipartite_xattn, bsca_attention, bsca_edges,
+    cosine_matrix, edge_budget, gather_rows, mean_pool_question, passage_keys,
+    qvs_logits, qvs_scores, qvs_topk, route,
+)

@@ -1,0 +1,331 @@
+"""Plain CPU oracle for the SKIP sparse cross-modal routing core.
+
+TEST INFRASTRUCTURE ONLY.  This module is the checker the GPU path is held
+against.  Only the test-suite, the package smoke check and the benchmark's CPU
+baseline leg may import or call it; the product path never does, and it
+shares no code with the HIP kernels or their host library.
+
+Everything is written for readability, in float64, one question at a time and
+one kept row at a time, following the paper's definitions in their own order:
+
+* mean-pooled question embedding (Sec. 3.3; App. B.2, Def. B.2);
+* question-guided salience score (App. B.1, Def. B.1; Alg. 1, scoring step)
+  with f_q = mean-pool and f_v = identity, plus the optional content bias;
+* top-k pruning of the visual tokens (Def. B.1; Alg. 1, TopK step);
+* the bipartite graph between kept tokens and passages (App. B.3, Def. B.3,
+  edge rule; Alg. 1, graph step);
+* sparse cross-attention restricted to that graph (Def. B.3, attention rule;
+  Alg. 1, fuse step).
+
+Readings where the paper is silent or inconsistent (each is listed with its
+justification in the design notes of the repository):
+
+* selection ranks the pre-sigmoid logit z (sigmoid is monotone, so the kept
+  set is the paper's; ranking z avoids spurious saturation ties);
+* ties in any top-k go to the lowest index; kept indices are returned in
+  ascending order;
+* an edge joins a kept visual token and a whole passage; the token attends to
+  every token of each neighbour passage;
+* the edge threshold is set per question so that exactly
+  E = min(ceil(avg_degree * k), k * P) edges survive (the paper sets the edge
+  threshold "dynamically" to hold the average degree near 4); ties go to the
+  lower flattened index i * P + j;
+* a passage's key is the mean of its per-token keys over all heads, unless
+  the caller supplies passage keys;
+* a kept token with no edge gets a zero output and log-sum-exp of -inf;
+* all heads share one graph.
+
+Parity pins: every function below is checked in the CPU test-suite against
+worked examples, closed forms, brute force on tiny inputs, library routines
+for the special cases that reduce to them, and invariants.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# Stage 1: question-guided visual salience (Sec. 3.3; App. B.1, Def. B.1)
+# --------------------------------------------------------------------------
+
+def mean_pool_question(Q: np.ndarray) -> np.ndarray:
+    """q_bar = mean of the T question-token rows (Def. B.2 defines q_bar as
+    the mean-pool of Q; Alg. 1 uses it in the difficulty step).  Q: [T, d]."""
+    Q = np.asarray(Q, dtype=np.float64)
+    if Q.ndim != 2 or Q.shape[0] < 1:
+        raise ValueError("need at least one question token")
+    return Q.sum(axis=0) / Q.shape[0]
+
+
+def qvs_logits(V: np.ndarray, q_bar: np.ndarray, w_bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Pre-sigmoid salience z_i = q_bar . v_i / sqrt(d) + w_b . v_i (Def. B.1
+    with f_q = mean-pool, f_v = identity).  V: [N, d] -> z: [N]."""
+    V = np.asarray(V, dtype=np.float64)
+    d = V.shape[1]
+    u = np.asarray(q_bar, dtype=np.float64) / math.sqrt(d)
+    if w_bias is not None:
+        u = u + np.asarray(w_bias, dtype=np.float64)
+    return V @ u
+
+
+def qvs_scores(z: np.ndarray) -> np.ndarray:
+    """s_i = sigma(z_i) in [0, 1] (Def. B.1)."""
+    z = np.asarray(z, dtype=np.float64)
+    return 1.0 / (1.0 + np.exp(-z))
+
+
+def qvs_topk(z: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k largest logits; among equal logits the lower index
+    wins; returned in ascending index order (Def. B.1 keeps ceil(rho L)
+    tokens with the highest score; Alg. 1, TopK step)."""
+    z = np.asarray(z, dtype=np.float64)
+    n = z.shape[0]
+    if not 0 <= k <= n:
+        raise ValueError("k out of range")
+    order = np.lexsort((np.arange(n), -z))     # primary key -z, then index
+    return np.sort(order[:k]).astype(np.int64)
+
+
+def gather_rows(V: np.ndarray, idx: np.ndarray) -> np.ndarray:
+    """V_hat = the rows of V at the kept indices (Alg. 1, TopK step)."""
+    return np.asarray(V)[np.asarray(idx, dtype=np.int64)]
+
+
+# --------------------------------------------------------------------------
+# Stage 2: bipartite graph (App. B.3, Def. B.3, edge rule)
+# --------------------------------------------------------------------------
+
+def passage_keys(Kh: np.ndarray, passage_ranges: Sequence[tuple]) -> np.ndarray:
+    """k_bar_j = mean over the tokens of passage j of that token's keys,
+    flattened over heads.  Kh: [M, H, d_h]; passage_ranges: (start, end)
+    token ranges.  Returns [P, H * d_h]."""
+    Kh = np.asarray(Kh, dtype=np.float64)
+    M = Kh.shape[0]
+    flat = Kh.reshape(M, -1)
+    out = np.zeros((len(passage_ranges), flat.shape[1]))
+    for j, (a, b) in enumerate(passage_ranges):
+        if b <= a:
+            raise ValueError("a passage needs at least one token")
+        out[j] = flat[a:b].sum(axis=0) / (b - a)
+    return out
+
+
+def cosine_matrix(Qrows: np.ndarray, Kbar: np.ndarray) -> np.ndarray:
+    """c_ij = cos(q_i, k_bar_j) = <q_i, k_bar_j> / (|q_i| |k_bar_j|), and 0
+    when either norm is 0 (Def. B.3 edge rule)."""
+    Qrows = np.asarray(Qrows, dtype=np.float64)
+    Kbar = np.asarray(Kbar, dtype=np.float64)
+    c = np.zeros((Qrows.shape[0], Kbar.shape[0]))
+    for i in range(Qrows.shape[0]):
+        nq = math.sqrt(float(Qrows[i] @ Qrows[i]))
+        for j in range(Kbar.shape[0]):
+            nk = math.sqrt(float(Kbar[j] @ Kbar[j]))
+            if nq > 0.0 and nk > 0.0:
+                c[i, j] = float(Qrows[i] @ Kbar[j]) / (nq * nk)
+    return c
+
+
+def edge_budget(k: int, P: int, avg_degree: float) -> int:
+    """E = min(ceil(avg_degree * k), k * P): the number of edges that keeps
+    the average degree of a kept token at avg_degree (Def. B.3 sets the edge
+    threshold so that the average degree stays near 4); avg_degree >= P
+    gives the complete bipartite graph."""
+    return int(min(math.ceil(float(avg_degree) * k), k * P))
+
+
+def bsca_edges(c: np.ndarray, avg_degree: float) -> np.ndarray:
+    """Boolean adjacency [k, P]: the E largest cosines, ties to the lower
+    flattened index i * P + j (Def. B.3 edge rule with a per-question
+    threshold)."""
+    c = np.asarray(c, dtype=np.float64)
+    k, P = c.shape
+    E = edge_budget(k, P, avg_degree)
+    flat = c.reshape(-1)
+    order = np.lexsort((np.arange(flat.size), -flat))
+    adj = np.zeros(flat.size, dtype=bool)
+    adj[order[:E]] = True
+    return adj.reshape(k, P)
+
+
+def adjacency_to_csr(adj: np.ndarray):
+    """CSR (rowptr [k+1], col [E]) with columns ascending within each row."""
+    adj = np.asarray(adj, dtype=bool)
+    rowptr = np.zeros(adj.shape[0] + 1, dtype=np.int64)
+    cols: List[int] = []
+    for i in range(adj.shape[0]):
+        js = np.nonzero(adj[i])[0]
+        cols.extend(int(j) for j in js)
+        rowptr[i + 1] = len(cols)
+    return rowptr, np.asarray(cols, dtype=np.int64)
+
+
+# --------------------------------------------------------------------------
+# Stage 3: sparse cross-attention over the graph (Def. B.3, attention rule)
+# --------------------------------------------------------------------------
+
+def bsca_attention(Qh: np.ndarray, Kh: np.ndarray, Vh: np.ndarray,
+                   passage_ranges: Sequence[tuple], adj: np.ndarray,
+                   sm_scale: float, rows: Optional[Sequence[int]] = None,
+                   return_probs: bool = False):
+    """For every kept row i and head h: e_m = sm_scale * <Qh[i,h], Kh[m,h]>
+    over the tokens m of the passages adjacent to row i (in ascending passage
+    order), O[i,h] = sum_m softmax(e)_m Vh[m,h], LSE[i,h] = log sum_m exp e_m.
+    A row with no neighbour gets O = 0 and LSE = -inf.
+
+    Qh: [k, H, d_h]; Kh, Vh: [M, H, d_h] (this question's tokens);
+    passage_ranges: (start, end) into Kh/Vh per passage; adj: [k, P] bool.
+    ``rows`` restricts the computation to some kept rows (outputs for other
+    rows are left as NaN)."""
+    Qh = np.asarray(Qh, dtype=np.float64)
+    Kh = np.asarray(Kh, dtype=np.float64)
+    Vh = np.asarray(Vh, dtype=np.float64)
+    k, H, d_h = Qh.shape
+    O = np.full((k, H, d_h), np.nan)
+    LSE = np.full((k, H), np.nan)
+    probs = {}
+    for i in (range(k) if rows is None else rows):
+        nbrs = np.nonzero(adj[i])[0]
+        if nbrs.size == 0:
+            O[i] = 0.0
+            LSE[i] = -np.inf
+            continue
+        idx = np.concatenate([np.arange(*passage_ranges[j]) for j in nbrs])
+        for h in range(H):
+            Kg = Kh[idx, h, :]                      # [m, d_h]
+            Vg = Vh[idx, h, :]
+            e = sm_scale * (Kg @ Qh[i, h])          # [m]
+            mx = e.max()
+            w = np.exp(e - mx)
+            den = w.sum()
+            p = w / den
+            O[i, h] = p @ Vg
+            LSE[i, h] = mx + math.log(den)
+            if return_probs:
+                probs[(i, h)] = p
+    if return_probs:
+        return O, LSE, probs
+    return O, LSE
+
+
+# --------------------------------------------------------------------------
+# Whole route for a batch of questions (Alg. 1: scoring, TopK, graph, fuse)
+# --------------------------------------------------------------------------
+
+@dataclass
+class RouteResult:
+    kept_idx: List[np.ndarray]        # per question, ascending
+    z: List[np.ndarray]               # per question logits [N]
+    scores: List[np.ndarray]          # per question sigmoid scores [N]
+    cos: List[np.ndarray]             # per question [k_b, P_b]
+    adj: List[np.ndarray]             # per question [k_b, P_b] bool
+    O: List[np.ndarray]               # per question [k_b, H, d_h]
+    LSE: List[np.ndarray]             # per question [k_b, H]
+
+
+def _f64(x) -> np.ndarray:
+    if hasattr(x, "detach"):          # a torch tensor on the CPU
+        import torch
+        return x.detach().to(torch.float64).numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
+          query_passages, sm_scale: float, avg_degree: float = 4.0,
+          w_bias=None, passage_key_table=None, queries: Optional[Sequence[int]] = None,
+          attn_rows: Optional[dict] = None, with_attention: bool = True) -> RouteResult:
+    """Prune, build the graph and attend, question by question.
+
+    V: [B, N, d]; Qtok: [sum T, d]; Kh, Vh: [sum M, H, d_h]; offsets as in
+    the library interface.  The attention queries of a kept row are that
+    row's visual token viewed as [H, d_h] (identity query projection).
+    ``queries`` restricts the work to some questions; ``attn_rows`` maps a
+    question to the kept rows whose attention output is wanted."""
+    V = _f64(V)
+    Qtok = _f64(Qtok)
+    Kh = _f64(Kh)
+    Vh = _f64(Vh)
+    w = None if w_bias is None else _f64(w_bias)
+    pk = None if passage_key_table is None else _f64(passage_key_table)
+    B, N, d = V.shape
+    H, d_h = Kh.shape[1], Kh.shape[2]
+    res = RouteResult([], [], [], [], [], [], [])
+    for b in (range(B) if queries is None else queries):
+        Q = Qtok[q_offsets[b]:q_offsets[b + 1]]
+        q_bar = mean_pool_question(Q)
+        z = qvs_logits(V[b], q_bar, w)
+        k = int(kept_offsets[b + 1] - kept_offsets[b])
+        idx = qvs_topk(z, k)
+        Vhat = gather_rows(V[b], idx)
+        p0, p1 = int(query_passages[b]), int(query_passages[b + 1])
+        t0 = int(passage_offsets[p0]) if p1 > p0 else 0
+        ranges = [(int(passage_offsets[j]) - t0, int(passage_offsets[j + 1]) - t0)
+                  for j in range(p0, p1)]
+        t1 = int(passage_offsets[p1]) if p1 > p0 else 0
+        Kq, Vq = Kh[t0:t1], Vh[t0:t1]
+        if p1 > p0:
+            Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
+            c = cosine_matrix(Vhat, Kbar)
+            adj = bsca_edges(c, avg_degree)
+        else:
+            c = np.zeros((k, 0))
+            adj = np.zeros((k, 0), dtype=bool)
+        if with_attention:
+            rows = None if attn_rows is None else attn_rows.get(b, [])
+            O, LSE = bsca_attention(Vhat.reshape(k, H, d_h), Kq, Vq, ranges, adj,
+                                    sm_scale, rows=rows)
+        else:
+            O, LSE = None, None
+        res.kept_idx.append(idx)
+        res.z.append(z)
+        res.scores.append(qvs_scores(z))
+        res.cos.append(c)
+        res.adj.append(adj)
+        res.O.append(O)
+        res.LSE.append(LSE)
+    return res
+
+
+def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
+                    sm_scale: float, avg_degree: float = 4.0,
+                    passage_key_table=None, adjacency: Optional[List[np.ndarray]] = None,
+                    attn_rows: Optional[dict] = None):
+    """Graph + attention on caller-given kept-row queries Qh [sum k, H, d_h].
+    ``adjacency`` (per question [k_b, P_b] bool) replaces the cosine rule
+    when the caller brings its own graph.  Returns (cos, adj, O, LSE) lists."""
+    Qh = _f64(Qh)
+    Kh = _f64(Kh)
+    Vh = _f64(Vh)
+    pk = None if passage_key_table is None else _f64(passage_key_table)
+    B = len(kept_offsets) - 1
+    H, d_h = Qh.shape[1], Qh.shape[2]
+    cos_l, adj_l, O_l, L_l = [], [], [], []
+    for b in range(B):
+        r0, r1 = int(kept_offsets[b]), int(kept_offsets[b + 1])
+        k = r1 - r0
+        p0, p1 = int(query_passages[b]), int(query_passages[b + 1])
+        t0 = int(passage_offsets[p0]) if p1 > p0 else 0
+        t1 = int(passage_offsets[p1]) if p1 > p0 else 0
+        ranges = [(int(passage_offsets[j]) - t0, int(passage_offsets[j + 1]) - t0)
+                  for j in range(p0, p1)]
+        Q = Qh[r0:r1]
+        if adjacency is not None:
+            c = None
+            adj = np.asarray(adjacency[b], dtype=bool)
+        elif p1 > p0:
+            Kbar = pk[p0:p1] if pk is not None else passage_keys(Kh[t0:t1], ranges)
+            c = cosine_matrix(Q.reshape(k, H * d_h), Kbar)
+            adj = bsca_edges(c, avg_degree)
+        else:
+            c = np.zeros((k, 0))
+            adj = np.zeros((k, 0), dtype=bool)
+        rows = None if attn_rows is None else attn_rows.get(b, [])
+        O, LSE = bsca_attention(Q, Kh[t0:t1], Vh[t0:t1], ranges, adj, sm_scale, rows=rows)
+        cos_l.append(c)
+        adj_l.append(adj)
+        O_l.append(O)
+        L_l.append(LSE)
+    return cos_l, adj_l, O_l, L_l
