@@ -1,0 +1,214 @@
+"""Benchmark of the SKIP routing core on one MI355X.
+
+One step = one fused route (question pooling -> salience scoring -> top-k
+prune -> passage keys -> edge cosines -> edge selection -> sparse
+cross-attention) over one synthetic batch already resident in HBM.  The
+workload is "highres_bf16": 16 questions, N = 2304 visual tokens of width
+4096, k = 192 kept tokens, 10 passages x 256 tokens, 32 heads x 128, average
+degree 4 (bf16; selection sums in float64).
+
+Prints ONE JSON line.  ``value`` is queries/s of the whole job.  The timed
+steps use the profiled entry point, which records HIP events on the launch
+stream between kernel stages; the roofline of the dominant kernel (the
+attention) divides its algorithmic bytes by its average event-timed duration.
+The CPU baseline times the CPU oracle (single thread) on a few questions of
+the same batch.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "queries/sec + fused route TFLOP/s & HBM GB/s vs MI355X peak, N=2304"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="highres_bf16")
+    ap.add_argument("--seed", type=int, default=2026)
+    ap.add_argument("--cpu-sample", type=int, default=4,
+                    help="questions of the batch the CPU oracle is timed on (0: skip)")
+    ap.add_argument("--pass-keys", action="store_true",
+                    help="hand precomputed passage keys to the library (skips pooling)")
+    return ap.parse_args()
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the routing core runs on a single MI355X; see the sharding notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_25422_amd import accounting as acc
+    from paper_2607_25422_amd import binding as B
+    from paper_2607_25422_amd import workloads as wls
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {args.workload} seed {args.seed}", file=sys.stderr, flush=True)
+    batch = wls.make_batch(args.workload, args.seed, threads=16)
+    wl = batch.wl
+    db = B.to_device(batch)
+    p = db.p
+    elem = 4 if wl.dtype == "f32" else 2
+    pkeys = None
+    if args.pass_keys:
+        # passage keys as a retriever would hand them over (mean of the keys)
+        pk = torch.stack([batch.Kh[a:b].float().reshape(b - a, -1).mean(0) for a, b in
+                          zip(batch.passage_offsets[:-1], batch.passage_offsets[1:])])
+        pkeys = pk.cuda()
+
+    # The graph, once, outside the timed region: realised edges for the FLOP
+    # and byte accounting.
+    idx, _, Vk = B.prune_topk(db, want_scores=False)
+    _, _, rp, col = B.bipartite_xattn(db, Vk.view(-1, p.H, p.d_h), passage_keys=pkeys)
+    torch.cuda.synchronize()
+    rp_h, col_h = rp.cpu().numpy(), col.cpu().numpy()
+    edge_L = acc.edge_lengths_from_csr(rp_h, col_h, batch.kept_offsets, batch.query_passages,
+                                       batch.passage_offsets)
+    touched = acc.touched_passages(rp_h, col_h, batch.kept_offsets, batch.query_passages)
+    L = np.diff(batch.passage_offsets)
+    touched_tokens = int(L[touched].sum()) if touched.size else 0
+    attn_flops = acc.attention_flops(edge_L, p.H, p.d_h)
+    attn_bytes = acc.attention_bytes(p.total_kept, p.d, p.H, touched_tokens, elem, elem)
+    score_bytes = acc.score_bytes(p.B, p.N, p.d, elem)
+    route_bytes = acc.route_bytes(p.B, p.N, p.d, p.total_qtok, p.total_kept, p.H,
+                                  p.total_tokens, touched_tokens, elem, pooled_keys=pkeys is None)
+    del idx, Vk, rp, col
+
+    out = (torch.empty(p.total_kept, dtype=torch.int32, device="cuda"),
+           torch.empty((p.total_kept, p.H, p.d_h), dtype=batch.torch_dtype, device="cuda"),
+           torch.empty((p.total_kept, p.H), dtype=torch.float32, device="cuda"))
+    events = [B.StageEvents() for _ in range(args.steps)]
+    for _ in range(args.warmup):
+        B.route_fused(db, passage_keys=pkeys, out=out)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
+
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        B.route_fused(db, passage_keys=pkeys, out=out, stage_events=events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall = t1 - t0
+    ms_per_step = 1e3 * wall / args.steps
+    qps = p.B * args.steps / wall
+
+    stages = {k: 0.0 for k in B.FUSED_STAGES}
+    for ev in events:
+        for k, v in ev.stage_ms().items():
+            stages[k] += v / args.steps
+    gpu_ms = sum(stages.values())
+
+    attn_ms = stages["attention"]
+    attn_gbs = attn_bytes / (attn_ms * 1e-3) / 1e9
+    score_gbs = score_bytes / (stages["score"] * 1e-3) / 1e9
+    prune_ms = stages["pool_question"] + stages["score"] + stages["topk"]
+
+    res = {
+        "metric": METRIC,
+        "value": round(qps, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": p.B, "N": p.N, "d": p.d, "T": wl.T,
+                   "k": int(batch.k[0]) if len(set(batch.k.tolist())) == 1 else "mixed",
+                   "passages": int(batch.P[0]) if len(set(batch.P.tolist())) == 1 else "mixed",
+                   "L_p": wl.L_p, "H": p.H, "d_h": p.d_h, "avg_degree": wl.avg_degree,
+                   "seed": args.seed, "passage_keys": "given" if pkeys is not None else "pooled"},
+        "roofline": {
+            "kernel": "attn_bf16_kernel" if wl.dtype == "bf16" else "attn_f32_kernel",
+            "bound": "hbm",
+            "achieved": round(attn_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "algorithmic_bytes": attn_bytes,
+            "avg_ms": round(attn_ms, 5),
+        },
+        "attention": {
+            "tflops": round(attn_flops / (attn_ms * 1e-3) / 1e12, 2),
+            "mfma_peak_frac": round(attn_flops / (attn_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "algorithmic_gflop": round(attn_flops / 1e9, 3),
+            "edges": int(rp_h[-1]),
+        },
+        "prune": {
+            "ms": round(prune_ms, 5),
+            "score_ms": round(stages["score"], 5),
+            "score_gbs": round(score_gbs, 1),
+            "score_hbm_frac": round(score_gbs / HBM_PEAK_GBS, 4),
+        },
+        "route": {
+            "gpu_ms": round(gpu_ms, 5),
+            "algorithmic_bytes": route_bytes,
+            "gbs": round(route_bytes / (gpu_ms * 1e-3) / 1e9, 1),
+            "tflops": round(attn_flops / (gpu_ms * 1e-3) / 1e12, 2),
+        },
+        "stages_ms": {k: round(v, 5) for k, v in stages.items()},
+    }
+
+    if args.cpu_sample > 0:
+        from threadpoolctl import threadpool_limits
+
+        import oracle as orc
+        qs = list(range(min(args.cpu_sample, p.B)))
+        print(f"[bench] timing the CPU oracle on {len(qs)} questions", file=sys.stderr,
+              flush=True)
+        with threadpool_limits(1):
+            c0 = time.perf_counter()
+            orc.route(batch.V, batch.Qtok, batch.q_offsets, batch.kept_offsets, batch.Kh,
+                      batch.Vh, batch.passage_offsets, batch.query_passages, wl.scale,
+                      wl.avg_degree, passage_key_table=None if pkeys is None else pkeys.cpu(),
+                      queries=qs)
+            c1 = time.perf_counter()
+        res["cpu_baseline"] = {
+            "value": round(len(qs) / (c1 - c0), 4),
+            "unit": "queries/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": (f"{len(qs)} of {p.B} questions of {wl.name} seed {args.seed}: full route "
+                       f"(pooling, scoring, top-k, graph, attention of every kept row), float64 "
+                       f"numpy, one thread, {c1 - c0:.1f} s, {cpu_model()}"),
+        }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

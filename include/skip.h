@@ -1,0 +1,224 @@
+/*
+ * skip.h -- C ABI of the SKIP sparse cross-modal routing core for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The routing core has two stages (paper: "Salient Knowledge Pathways",
+ * Sec. 3.3 and 3.5; App. B.1 and B.3; Alg. 1, scoring/TopK/graph/fuse steps):
+ *
+ *   1. Question-guided visual pruning (Def. B.1).  For question b with
+ *      question tokens Q_b (T_b rows) and visual tokens V_b (N rows):
+ *        q_bar_b = mean of the rows of Q_b
+ *        z_i     = (q_bar_b / sqrt(d) + w) . v_i        (w: optional content bias)
+ *        s_i     = sigmoid(z_i)
+ *      and the k_b tokens with the largest z are kept (ties: lowest index
+ *      first), reported in ascending index order.
+ *
+ *   2. Bipartite sparse cross-attention (Def. B.3).  Kept row i of question b
+ *      and passage j are joined by an edge when cos(q_i, kbar_j) is among the
+ *      E_b = min(ceil(avg_degree * k_b), k_b * P_b) largest cosines of that
+ *      question (ties: lower flattened index i * P_b + j first).  q_i is the
+ *      row's query vector flattened over heads; kbar_j is the passage key
+ *      (the mean of the passage's per-token keys unless passed in).  Then,
+ *      per head h, row i attends over every token of its neighbour passages:
+ *        e_m = sm_scale * <Qh[i,h], Kh[m,h]>,
+ *        O[i,h] = sum_m softmax(e)_m Vh[m,h],  LSE[i,h] = log sum_m exp(e_m).
+ *      A row without neighbours gets O = 0 and LSE = -inf.
+ *
+ * Selection decisions (the kept set and the edge set) are computed from
+ * float64 accumulations, so they match a float64 reference on any input whose
+ * decisive gap exceeds float64 rounding.  Attention accumulates in float32;
+ * in bf16 mode the softmax weights are rounded to bf16 before the PV product.
+ *
+ * Conventions for every entry point
+ *   - The caller owns all memory.  Every array argument is a DEVICE pointer
+ *     (global memory of the current HIP device); `p` is a HOST pointer.  The
+ *     library allocates no device memory, keeps no state between calls and
+ *     may be called concurrently on different streams with different
+ *     workspaces.  Calls sharing a workspace must be ordered on one stream.
+ *   - Element arrays (V, Qtok, w_bias, Qh, Kh, Vh, O, V_kept) have the element
+ *     type given by p->dtype and must be 16-byte aligned; row widths are
+ *     multiples of 8 elements.
+ *   - Offsets are int32, ascending, starting at 0; offsets arrays are device
+ *     arrays whose last entry must equal the matching total in `p`.
+ *     Kernels clamp every offset into its declared total, so inconsistent
+ *     offsets never cause out-of-bounds access (results are then
+ *     unspecified).
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *     asynchronously; argument checks happen on the host before anything is
+ *     enqueued.  Faults inside kernels surface at the caller's next
+ *     synchronisation, as for any HIP call.
+ *   - Inputs must be finite.  Same inputs give bitwise-identical outputs on
+ *     every call (no floating-point atomics).
+ *
+ * Errors: SKIP_ERR_INVALID_ARG for a NULL required pointer or inconsistent
+ * sizes; SKIP_ERR_UNSUPPORTED for shapes the kernels do not implement (see
+ * skip_problem_t); SKIP_ERR_WORKSPACE when workspace_bytes is below
+ * skip_workspace_bytes(); SKIP_ERR_HIP when a launch fails.  Nothing is
+ * enqueued unless the call returns SKIP_OK.
+ */
+#ifndef SKIP_H
+#define SKIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SKIP_ABI_VERSION 1
+
+typedef enum skip_status {
+  SKIP_OK = 0,
+  SKIP_ERR_INVALID_ARG = 1,
+  SKIP_ERR_UNSUPPORTED = 2,
+  SKIP_ERR_WORKSPACE = 3,
+  SKIP_ERR_HIP = 4
+} skip_status_t;
+
+typedef enum skip_dtype { SKIP_F32 = 0, SKIP_BF16 = 1 } skip_dtype_t;
+
+/*
+ * Host-side description of one batch of B questions (paper Sec. 3.1 problem
+ * statement: visual tokens V, question tokens Q, retrieved passages K).
+ *
+ * Supported shapes: 1 <= B; 1 <= N <= 16384; d a multiple of 8;
+ * H * d_h == d; d_h in {64, 128}; P_max <= 64; k_max * P_max <= 16384
+ * (per-question edge candidates); all totals below 2^31 elements.
+ */
+typedef struct skip_problem {
+  int32_t dtype;           /* skip_dtype_t: element type of all element arrays */
+  int32_t B;               /* questions in the batch                           */
+  int32_t N;               /* visual tokens per question                       */
+  int32_t d;               /* embedding width of V, Qtok, Qh rows              */
+  int32_t H;               /* attention heads                                  */
+  int32_t d_h;             /* head dimension                                   */
+  int32_t total_qtok;      /* sum_b T_b = rows of Qtok                         */
+  int32_t k_max;           /* max_b k_b                                        */
+  int32_t total_kept;      /* sum_b k_b = rows of Qh, O, kept_idx              */
+  int32_t P_max;           /* max_b P_b                                        */
+  int32_t total_passages;  /* sum_b P_b                                        */
+  int32_t total_tokens;    /* sum over passages of their token counts          */
+  int32_t L_max;           /* longest passage, in tokens                       */
+  int32_t total_edges;     /* length of a caller-given edge_col (else 0)       */
+  double avg_degree;       /* target average degree of a kept row (paper: 4)   */
+  float sm_scale;          /* logit scale (paper: 1/sqrt(d_h))                 */
+  int32_t o_f32;           /* 0: O has the element type of dtype; 1: O is float */
+} skip_problem_t;
+
+/* ABI version of the loaded library (SKIP_ABI_VERSION). */
+int32_t skip_abi_version(void);
+
+/* Static, NUL-terminated description of a status code. */
+const char* skip_status_string(skip_status_t s);
+
+/*
+ * Workspace size in bytes that every entry point needs for problem `p`
+ * (host-only, no device access).  Writes *bytes and returns SKIP_OK, or
+ * returns the validation error without writing.
+ */
+skip_status_t skip_workspace_bytes(const skip_problem_t* p, size_t* bytes);
+
+/*
+ * Stage 1: question-guided visual token pruning (Def. B.1; Alg. 1, scoring
+ * and TopK steps).
+ *   V            [B][N][d]      visual tokens
+ *   Qtok         [total_qtok][d] question tokens of all questions
+ *   q_offsets    [B+1]          rows of Qtok per question; T_b >= 1 (a
+ *                               question with no token is pooled as zero)
+ *   w_bias       [d] or NULL    content bias w of Def. B.1
+ *   kept_offsets [B+1]          k_b = kept_offsets[b+1] - kept_offsets[b],
+ *                               0 <= k_b <= N
+ *   kept_idx     out [total_kept] int32 kept token indices in [0, N),
+ *                               ascending within each question
+ *   scores       out [B][N] float sigmoid scores s_i, or NULL
+ *   V_kept       out [total_kept][d] the kept rows of V, or NULL
+ */
+skip_status_t skip_prune_topk(const skip_problem_t* p, const void* V,
+                              const void* Qtok, const int32_t* q_offsets,
+                              const void* w_bias, const int32_t* kept_offsets,
+                              int32_t* kept_idx, float* scores, void* V_kept,
+                              void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/*
+ * Stage 2: bipartite graph + sparse cross-attention (Def. B.3; Alg. 1,
+ * graph and fuse steps) on caller-given kept-row queries.
+ *   Qh              [total_kept][H][d_h] queries of the kept rows
+ *   kept_offsets    [B+1]
+ *   Kh, Vh          [total_tokens][H][d_h] per-token keys and values
+ *   passage_offsets [total_passages+1] token offsets; every passage >= 1 token
+ *   query_passages  [B+1] passages of question b are
+ *                   query_passages[b] .. query_passages[b+1]-1 (P_b may be 0)
+ *   passage_keys    [total_passages][d] float passage keys, or NULL to use the
+ *                   per-passage mean of Kh
+ *   edge_rowptr, edge_col  a caller-given graph (CSR over kept rows, column =
+ *                   passage number within the question, p->total_edges
+ *                   entries), or both NULL to build the graph by the cosine
+ *                   rule; columns outside [0, P_b) are ignored
+ *   O               out [total_kept][H][d_h], element type dtype (float if
+ *                   p->o_f32)
+ *   lse             out [total_kept][H] float natural-log LSE, or NULL
+ *   edge_rowptr_out out [total_kept+1] int32, or NULL
+ *   edge_col_out    out int32, capacity total_kept * P_max, or NULL; with
+ *                   edge_rowptr_out it receives the graph in CSR form
+ *                   (columns ascending within a row).  Both or neither.
+ */
+skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
+                                   const int32_t* kept_offsets, const void* Kh,
+                                   const void* Vh,
+                                   const int32_t* passage_offsets,
+                                   const int32_t* query_passages,
+                                   const float* passage_keys,
+                                   const int32_t* edge_rowptr,
+                                   const int32_t* edge_col, void* O, float* lse,
+                                   int32_t* edge_rowptr_out,
+                                   int32_t* edge_col_out, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/*
+ * Both stages fused (Alg. 1: scoring, TopK, graph, fuse): the kept visual
+ * tokens are the attention queries (Qh = the kept rows of V viewed as
+ * [H][d_h], which requires H * d_h == d) and are read straight from V, never
+ * written out.  Arguments as in the two calls above.
+ */
+skip_status_t skip_route_fused(const skip_problem_t* p, const void* V,
+                               const void* Qtok, const int32_t* q_offsets,
+                               const void* w_bias,
+                               const int32_t* kept_offsets, const void* Kh,
+                               const void* Vh, const int32_t* passage_offsets,
+                               const int32_t* query_passages,
+                               const float* passage_keys, int32_t* kept_idx,
+                               void* O, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* Kernel stages of skip_route_fused, in launch order: question pooling,
+ * salience scoring, top-k, passage keys, edge cosines, edge selection,
+ * attention. */
+#define SKIP_FUSED_STAGES 7
+
+/*
+ * skip_route_fused with per-stage timing, for profiling harnesses.
+ * stage_events holds n_events == SKIP_FUSED_STAGES + 1 hipEvent_t handles
+ * created by the caller (host array of handles); event s is recorded on
+ * `stream` just before stage s is enqueued and the last one after the final
+ * stage, so hipEventElapsedTime(events[s], events[s+1]) is the duration of
+ * stage s.  A stage with nothing to do (passage keys given by the caller)
+ * records its two events back to back.  Other arguments and results as in
+ * skip_route_fused; SKIP_ERR_INVALID_ARG if stage_events is NULL or
+ * n_events is wrong.
+ */
+skip_status_t skip_route_fused_profiled(
+    const skip_problem_t* p, const void* V, const void* Qtok,
+    const int32_t* q_offsets, const void* w_bias, const int32_t* kept_offsets,
+    const void* Kh, const void* Vh, const int32_t* passage_offsets,
+    const int32_t* query_passages, const float* passage_keys,
+    int32_t* kept_idx, void* O, float* lse, void* workspace,
+    size_t workspace_bytes, void* stream, void* const* stage_events,
+    int32_t n_events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SKIP_H */

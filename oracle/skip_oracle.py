@@ -244,28 +244,26 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
     row's visual token viewed as [H, d_h] (identity query projection).
     ``queries`` restricts the work to some questions; ``attn_rows`` maps a
     question to the kept rows whose attention output is wanted."""
-    V = _f64(V)
-    Qtok = _f64(Qtok)
-    Kh = _f64(Kh)
-    Vh = _f64(Vh)
     w = None if w_bias is None else _f64(w_bias)
     pk = None if passage_key_table is None else _f64(passage_key_table)
     B, N, d = V.shape
     H, d_h = Kh.shape[1], Kh.shape[2]
     res = RouteResult([], [], [], [], [], [], [])
     for b in (range(B) if queries is None else queries):
-        Q = Qtok[q_offsets[b]:q_offsets[b + 1]]
+        # inputs are widened to float64 one question at a time
+        Q = _f64(Qtok[int(q_offsets[b]):int(q_offsets[b + 1])])
+        Vb = _f64(V[b])
         q_bar = mean_pool_question(Q)
-        z = qvs_logits(V[b], q_bar, w)
+        z = qvs_logits(Vb, q_bar, w)
         k = int(kept_offsets[b + 1] - kept_offsets[b])
         idx = qvs_topk(z, k)
-        Vhat = gather_rows(V[b], idx)
+        Vhat = gather_rows(Vb, idx)
         p0, p1 = int(query_passages[b]), int(query_passages[b + 1])
         t0 = int(passage_offsets[p0]) if p1 > p0 else 0
         ranges = [(int(passage_offsets[j]) - t0, int(passage_offsets[j + 1]) - t0)
                   for j in range(p0, p1)]
         t1 = int(passage_offsets[p1]) if p1 > p0 else 0
-        Kq, Vq = Kh[t0:t1], Vh[t0:t1]
+        Kq, Vq = _f64(Kh[t0:t1]), _f64(Vh[t0:t1])
         if p1 > p0:
             Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
             c = cosine_matrix(Vhat, Kbar)
@@ -296,9 +294,6 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
     """Graph + attention on caller-given kept-row queries Qh [sum k, H, d_h].
     ``adjacency`` (per question [k_b, P_b] bool) replaces the cosine rule
     when the caller brings its own graph.  Returns (cos, adj, O, LSE) lists."""
-    Qh = _f64(Qh)
-    Kh = _f64(Kh)
-    Vh = _f64(Vh)
     pk = None if passage_key_table is None else _f64(passage_key_table)
     B = len(kept_offsets) - 1
     H, d_h = Qh.shape[1], Qh.shape[2]
@@ -311,19 +306,20 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
         t1 = int(passage_offsets[p1]) if p1 > p0 else 0
         ranges = [(int(passage_offsets[j]) - t0, int(passage_offsets[j + 1]) - t0)
                   for j in range(p0, p1)]
-        Q = Qh[r0:r1]
+        Q = _f64(Qh[r0:r1])
+        Kq, Vq = _f64(Kh[t0:t1]), _f64(Vh[t0:t1])
         if adjacency is not None:
             c = None
             adj = np.asarray(adjacency[b], dtype=bool)
         elif p1 > p0:
-            Kbar = pk[p0:p1] if pk is not None else passage_keys(Kh[t0:t1], ranges)
+            Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
             c = cosine_matrix(Q.reshape(k, H * d_h), Kbar)
             adj = bsca_edges(c, avg_degree)
         else:
             c = np.zeros((k, 0))
             adj = np.zeros((k, 0), dtype=bool)
         rows = None if attn_rows is None else attn_rows.get(b, [])
-        O, LSE = bsca_attention(Q, Kh[t0:t1], Vh[t0:t1], ranges, adj, sm_scale, rows=rows)
+        O, LSE = bsca_attention(Q, Kq, Vq, ranges, adj, sm_scale, rows=rows)
         cos_l.append(c)
         adj_l.append(adj)
         O_l.append(O)

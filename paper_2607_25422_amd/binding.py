@@ -1,0 +1,373 @@
+"""Python binding of libskip.so (ctypes; argument marshalling only).
+
+Every function here checks tensor placement/shape/dtype, reads raw device
+pointers and the current HIP stream from torch, and calls the C entry point
+of the same name.  All arithmetic happens in the library's HIP kernels; there
+is no fallback path.  If the library is missing, importing this module raises.
+
+Offsets arrays are given twice: as host numpy arrays (to fill the problem
+description, which the C ABI takes by value on the host) and as device int32
+tensors (which the kernels read).  ``Offsets.to_device`` makes the pair.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libskip.so")
+
+SKIP_OK, SKIP_ERR_INVALID_ARG, SKIP_ERR_UNSUPPORTED, SKIP_ERR_WORKSPACE, SKIP_ERR_HIP = range(5)
+SKIP_F32, SKIP_BF16 = 0, 1
+
+ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes",
+                "skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused",
+                "skip_route_fused_profiled")
+FUSED_STAGES = ("pool_question", "score", "topk", "passage_keys", "edge_cos", "edge_select",
+                "attention")
+
+
+class SkipError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}")
+
+
+class SkipProblem(ctypes.Structure):
+    _fields_ = [
+        ("dtype", ctypes.c_int32), ("B", ctypes.c_int32), ("N", ctypes.c_int32),
+        ("d", ctypes.c_int32), ("H", ctypes.c_int32), ("d_h", ctypes.c_int32),
+        ("total_qtok", ctypes.c_int32), ("k_max", ctypes.c_int32),
+        ("total_kept", ctypes.c_int32), ("P_max", ctypes.c_int32),
+        ("total_passages", ctypes.c_int32), ("total_tokens", ctypes.c_int32),
+        ("L_max", ctypes.c_int32), ("total_edges", ctypes.c_int32),
+        ("avg_degree", ctypes.c_double), ("sm_scale", ctypes.c_float),
+        ("o_f32", ctypes.c_int32),
+    ]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2607_25422_amd.build` "
+            "(the routing core has no non-HIP implementation)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(SkipProblem)
+    vp, i32p = ctypes.c_void_p, ctypes.c_void_p
+    lib.skip_abi_version.restype = ctypes.c_int32
+    lib.skip_abi_version.argtypes = []
+    lib.skip_status_string.restype = ctypes.c_char_p
+    lib.skip_status_string.argtypes = [ctypes.c_int]
+    lib.skip_workspace_bytes.restype = ctypes.c_int
+    lib.skip_workspace_bytes.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.skip_prune_topk.restype = ctypes.c_int
+    lib.skip_prune_topk.argtypes = [P, vp, vp, i32p, vp, i32p, i32p, vp, vp, vp,
+                                    ctypes.c_size_t, vp]
+    lib.skip_bipartite_xattn.restype = ctypes.c_int
+    lib.skip_bipartite_xattn.argtypes = [P, vp, i32p, vp, vp, i32p, i32p, vp, i32p, i32p,
+                                         vp, vp, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.skip_route_fused.restype = ctypes.c_int
+    lib.skip_route_fused.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p, vp,
+                                     i32p, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.skip_route_fused_profiled.restype = ctypes.c_int
+    lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
+                                              vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
+                                              ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32]
+    return lib
+
+
+LIB = _load()
+
+
+def status_string(status: int) -> str:
+    return LIB.skip_status_string(status).decode()
+
+
+def abi_version() -> int:
+    return LIB.skip_abi_version()
+
+
+def _check(status: int, where: str):
+    if status != SKIP_OK:
+        raise SkipError(status, where)
+
+
+# ---------------------------------------------------------------------------
+# Problem description
+
+def _host_i32(x) -> np.ndarray:
+    if isinstance(x, torch.Tensor):
+        x = x.detach().cpu().numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int64))
+
+
+def make_problem(dtype: str, *, B: int, N: int = 0, d: int, H: int = 0, d_h: int = 0,
+                 q_offsets=None, kept_offsets=None, passage_offsets=None,
+                 query_passages=None, avg_degree: float = 4.0,
+                 sm_scale: Optional[float] = None, total_edges: int = 0,
+                 o_f32: bool = False) -> SkipProblem:
+    """Fill the host-side problem description from host copies of the offsets."""
+    p = SkipProblem()
+    p.dtype = SKIP_F32 if dtype in ("f32", torch.float32) else SKIP_BF16
+    p.B, p.N, p.d, p.H, p.d_h = B, N, d, H, d_h
+    if q_offsets is not None:
+        qo = _host_i32(q_offsets)
+        p.total_qtok = int(qo[-1])
+    if kept_offsets is not None:
+        ko = _host_i32(kept_offsets)
+        p.total_kept = int(ko[-1])
+        p.k_max = int(np.diff(ko).max()) if ko.size > 1 else 0
+    if query_passages is not None:
+        qp = _host_i32(query_passages)
+        p.total_passages = int(qp[-1])
+        p.P_max = int(np.diff(qp).max()) if qp.size > 1 else 0
+    if passage_offsets is not None:
+        po = _host_i32(passage_offsets)
+        p.total_tokens = int(po[-1])
+        p.L_max = int(np.diff(po).max()) if po.size > 1 else 0
+    p.total_edges = int(total_edges)
+    p.avg_degree = float(avg_degree)
+    p.sm_scale = float(sm_scale if sm_scale is not None else (1.0 / math.sqrt(d_h) if d_h else 1.0))
+    p.o_f32 = 1 if o_f32 else 0
+    return p
+
+
+def workspace_bytes(p: SkipProblem) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.skip_workspace_bytes(ctypes.byref(p), ctypes.byref(n)), "skip_workspace_bytes")
+    return int(n.value)
+
+
+def new_workspace(p: SkipProblem, device="cuda") -> torch.Tensor:
+    return torch.empty(max(workspace_bytes(p), 256), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# Pointer helpers
+
+def _elem_dtype(p: SkipProblem) -> torch.dtype:
+    return torch.float32 if p.dtype == SKIP_F32 else torch.bfloat16
+
+
+def _out_dtype(p: SkipProblem) -> torch.dtype:
+    return torch.float32 if (p.dtype == SKIP_F32 or p.o_f32) else torch.bfloat16
+
+
+def _ptr(t: Optional[torch.Tensor], name: str, dtype=None, numel=None) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} needs {numel} elements, has {t.numel()}")
+    if t.numel() and t.data_ptr() % 16:
+        raise ValueError(f"{name} must be 16-byte aligned")
+    return t.data_ptr() if t.numel() else None
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ws(p, workspace):
+    if workspace is None:
+        workspace = new_workspace(p)
+    return workspace, workspace.data_ptr(), workspace.numel()
+
+
+# ---------------------------------------------------------------------------
+# Entry points (low level: caller-provided outputs)
+
+def skip_prune_topk(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, kept_idx,
+                    scores=None, V_kept=None, workspace=None, stream=None):
+    et = _elem_dtype(p)
+    ws, wsp, wsn = _ws(p, workspace)
+    st = LIB.skip_prune_topk(
+        ctypes.byref(p), _ptr(V, "V", et, p.B * p.N * p.d), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
+        _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1), _ptr(w_bias, "w_bias", et, p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept),
+        _ptr(scores, "scores", torch.float32, p.B * p.N),
+        _ptr(V_kept, "V_kept", et, p.total_kept * p.d), wsp, wsn, _stream(stream))
+    _check(st, "skip_prune_topk")
+
+
+def skip_bipartite_xattn(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passage_offsets,
+                         query_passages, O, lse=None, passage_keys=None, edge_rowptr=None,
+                         edge_col=None, edge_rowptr_out=None, edge_col_out=None,
+                         workspace=None, stream=None):
+    et = _elem_dtype(p)
+    ws, wsp, wsn = _ws(p, workspace)
+    st = LIB.skip_bipartite_xattn(
+        ctypes.byref(p), _ptr(Qh, "Qh", et, p.total_kept * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d), _ptr(Vh, "Vh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(edge_rowptr, "edge_rowptr", torch.int32, p.total_kept + 1),
+        _ptr(edge_col, "edge_col", torch.int32, p.total_edges),
+        _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
+        _ptr(lse, "lse", torch.float32, p.total_kept * p.H),
+        _ptr(edge_rowptr_out, "edge_rowptr_out", torch.int32, p.total_kept + 1),
+        _ptr(edge_col_out, "edge_col_out", torch.int32, p.total_kept * p.P_max),
+        wsp, wsn, _stream(stream))
+    _check(st, "skip_bipartite_xattn")
+
+
+def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                     passage_offsets, query_passages, kept_idx, O, lse=None,
+                     passage_keys=None, workspace=None, stream=None, stage_events=None):
+    """``stage_events``: a StageEvents set to time each kernel stage (calls
+    skip_route_fused_profiled)."""
+    et = _elem_dtype(p)
+    ws, wsp, wsn = _ws(p, workspace)
+    if stage_events is None:
+        fn, extra = LIB.skip_route_fused, ()
+    else:
+        fn, extra = LIB.skip_route_fused_profiled, (stage_events.handles, len(stage_events))
+    st = fn(
+        ctypes.byref(p), _ptr(V, "V", et, p.B * p.N * p.d), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
+        _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1), _ptr(w_bias, "w_bias", et, p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d), _ptr(Vh, "Vh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept),
+        _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
+        _ptr(lse, "lse", torch.float32, p.total_kept * p.H), wsp, wsn, _stream(stream), *extra)
+    _check(st, "skip_route_fused")
+
+
+class StageEvents:
+    """SKIP_FUSED_STAGES + 1 timing events for skip_route_fused_profiled.
+    torch events are created (by one record on the current stream) and their
+    raw hipEvent_t handles handed to the library, which records them on the
+    launch stream between its kernel stages."""
+
+    def __init__(self):
+        self.events = [torch.cuda.Event(enable_timing=True) for _ in range(len(FUSED_STAGES) + 1)]
+        for e in self.events:
+            e.record()
+        arr = (ctypes.c_void_p * len(self.events))(*[e.cuda_event for e in self.events])
+        self.handles = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+        self._arr = arr
+
+    def __len__(self):
+        return len(self.events)
+
+    def stage_ms(self):
+        """Per-stage durations in ms (call after the stream has synchronised)."""
+        return {name: self.events[i].elapsed_time(self.events[i + 1])
+                for i, name in enumerate(FUSED_STAGES)}
+
+
+# ---------------------------------------------------------------------------
+# Convenience layer over a generated batch (allocates outputs)
+
+@dataclass
+class DeviceBatch:
+    """A batch's tensors and offsets on the device, plus its problem."""
+    p: SkipProblem
+    V: torch.Tensor
+    Qtok: torch.Tensor
+    q_offsets: torch.Tensor
+    kept_offsets: torch.Tensor
+    Kh: torch.Tensor
+    Vh: torch.Tensor
+    passage_offsets: torch.Tensor
+    query_passages: torch.Tensor
+    w_bias: Optional[torch.Tensor]
+    workspace: torch.Tensor
+
+
+def to_device(batch, device="cuda", avg_degree: Optional[float] = None,
+              sm_scale: Optional[float] = None, o_f32: bool = False) -> DeviceBatch:
+    """Move a generated batch (``workloads.Batch``) to the device."""
+    wl = batch.wl
+    B, N, d = batch.V.shape
+    H, d_h = batch.Kh.shape[1], batch.Kh.shape[2]
+    p = make_problem(wl.dtype, B=B, N=N, d=d, H=H, d_h=d_h, q_offsets=batch.q_offsets,
+                     kept_offsets=batch.kept_offsets, passage_offsets=batch.passage_offsets,
+                     query_passages=batch.query_passages,
+                     avg_degree=wl.avg_degree if avg_degree is None else avg_degree,
+                     sm_scale=wl.scale if sm_scale is None else sm_scale, o_f32=o_f32)
+    i32 = lambda a: torch.from_numpy(np.asarray(a, dtype=np.int32)).to(device)
+    return DeviceBatch(
+        p=p, V=batch.V.to(device), Qtok=batch.Qtok.to(device), q_offsets=i32(batch.q_offsets),
+        kept_offsets=i32(batch.kept_offsets), Kh=batch.Kh.to(device), Vh=batch.Vh.to(device),
+        passage_offsets=i32(batch.passage_offsets), query_passages=i32(batch.query_passages),
+        w_bias=None if batch.w_bias is None else batch.w_bias.to(device),
+        workspace=new_workspace(p, device))
+
+
+def with_f32_output(db: DeviceBatch) -> DeviceBatch:
+    """The same batch (shared tensors) with O written as float32."""
+    q = SkipProblem.from_buffer_copy(db.p)
+    q.o_f32 = 1
+    return DeviceBatch(q, db.V, db.Qtok, db.q_offsets, db.kept_offsets, db.Kh, db.Vh,
+                       db.passage_offsets, db.query_passages, db.w_bias, db.workspace)
+
+
+def prune_topk(db: DeviceBatch, want_scores=True, want_rows=True):
+    p = db.p
+    kept_idx = torch.empty(max(p.total_kept, 1), dtype=torch.int32, device=db.V.device)
+    scores = torch.empty(p.B * p.N, dtype=torch.float32, device=db.V.device) if want_scores else None
+    V_kept = (torch.empty((max(p.total_kept, 1), p.d), dtype=db.V.dtype, device=db.V.device)
+              if want_rows else None)
+    skip_prune_topk(p, db.V, db.Qtok, db.q_offsets, db.w_bias, db.kept_offsets, kept_idx,
+                    scores, V_kept, db.workspace)
+    return (kept_idx[:p.total_kept], None if scores is None else scores.view(p.B, p.N),
+            None if V_kept is None else V_kept[:p.total_kept])
+
+
+def bipartite_xattn(db: DeviceBatch, Qh: torch.Tensor, passage_keys=None, edges=None,
+                    want_edges=True) -> Tuple:
+    """Qh: [total_kept, H, d_h].  ``edges`` = (rowptr, col) device int32 to
+    use a given graph.  Returns (O, lse, rowptr, col)."""
+    p = db.p
+    dev = db.V.device
+    O = torch.empty((max(p.total_kept, 1), p.H, p.d_h), dtype=_out_dtype(p), device=dev)
+    lse = torch.empty((max(p.total_kept, 1), p.H), dtype=torch.float32, device=dev)
+    rp = col = None
+    q = p
+    if edges is not None:
+        q = SkipProblem.from_buffer_copy(p)
+        q.total_edges = int(edges[1].numel())
+    elif want_edges:
+        rp = torch.empty(p.total_kept + 1, dtype=torch.int32, device=dev)
+        col = torch.empty(max(p.total_kept * p.P_max, 1), dtype=torch.int32, device=dev)
+    skip_bipartite_xattn(q, Qh if p.total_kept else None, db.kept_offsets, db.Kh, db.Vh,
+                         db.passage_offsets, db.query_passages, O if p.total_kept else None,
+                         lse if p.total_kept else None, passage_keys,
+                         None if edges is None else edges[0],
+                         None if edges is None else edges[1], rp, col, db.workspace)
+    return O[:p.total_kept], lse[:p.total_kept], rp, col
+
+
+def route_fused(db: DeviceBatch, passage_keys=None, out=None, stage_events=None):
+    """Returns (kept_idx, O, lse).  ``out`` = preallocated (kept_idx, O, lse)."""
+    p = db.p
+    dev = db.V.device
+    if out is None:
+        out = (torch.empty(max(p.total_kept, 1), dtype=torch.int32, device=dev),
+               torch.empty((max(p.total_kept, 1), p.H, p.d_h), dtype=_out_dtype(p), device=dev),
+               torch.empty((max(p.total_kept, 1), p.H), dtype=torch.float32, device=dev))
+    kept_idx, O, lse = out
+    skip_route_fused(p, db.V, db.Qtok, db.q_offsets, db.w_bias, db.kept_offsets, db.Kh, db.Vh,
+                     db.passage_offsets, db.query_passages, kept_idx, O, lse, passage_keys,
+                     db.workspace, stage_events=stage_events)
+    return kept_idx[:p.total_kept], O[:p.total_kept], lse[:p.total_kept]

@@ -1,0 +1,390 @@
+// Bipartite graph between kept visual tokens and retrieved passages
+// (paper App. B.3, Def. B.3 edge rule; Alg. 1, graph step).
+//
+//   passage_keys : kbar_j = mean over the tokens of passage j of Kh[m] (all
+//                  heads flattened), float64 sums
+//   edge_cos     : c_ij = <q_i, kbar_j> / (|q_i| |kbar_j|), float64, 0 when a
+//                  norm is 0
+//   edge_select  : per question, the E_b = min(ceil(avg_degree * k_b),
+//                  k_b * P_b) largest cosines (lower flattened index i*P_b+j
+//                  on ties) -> one 64-bit neighbour mask per kept row, and
+//                  optionally the graph in CSR form
+//   csr_to_mask  : neighbour masks from a caller-given CSR graph
+#include "skip_common.h"
+#include "skip_internal.h"
+#include "skip_select.h"
+
+namespace skip {
+
+template <typename T> struct GVec;
+template <> struct GVec<float> { static constexpr int n = 4; };
+template <> struct GVec<bf16_t> { static constexpr int n = 8; };
+
+template <typename T>
+__device__ __forceinline__ void unpack_f64(const u32x4& x, double* out);
+template <>
+__device__ __forceinline__ void unpack_f64<float>(const u32x4& x, double* out) {
+  out[0] = (double)__uint_as_float(x.x);
+  out[1] = (double)__uint_as_float(x.y);
+  out[2] = (double)__uint_as_float(x.z);
+  out[3] = (double)__uint_as_float(x.w);
+}
+template <>
+__device__ __forceinline__ void unpack_f64<bf16_t>(const u32x4& x, double* out) {
+  out[0] = (double)bf16_to_f32(x.x & 0xffffu);
+  out[1] = (double)bf16_to_f32(x.x >> 16);
+  out[2] = (double)bf16_to_f32(x.y & 0xffffu);
+  out[3] = (double)bf16_to_f32(x.y >> 16);
+  out[4] = (double)bf16_to_f32(x.z & 0xffffu);
+  out[5] = (double)bf16_to_f32(x.z >> 16);
+  out[6] = (double)bf16_to_f32(x.w & 0xffffu);
+  out[7] = (double)bf16_to_f32(x.w >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float elem_f32(const T* p, size_t i);
+template <> __device__ __forceinline__ float elem_f32<float>(const float* p, size_t i) {
+  return p[i];
+}
+template <> __device__ __forceinline__ float elem_f32<bf16_t>(const bf16_t* p, size_t i) {
+  return bf16_to_f32(p[i]);
+}
+
+// ---------------------------------------------------------------------------
+// Passage keys.  Workgroup = (column slice of 64 lanes x 16 bytes, passage);
+// wave w sums tokens w, w+4, ...; the four partial sums are combined in wave
+// order through LDS.
+template <typename T>
+__global__ void __launch_bounds__(256)
+passage_keys_kernel(const T* __restrict__ Kh, const int32_t* __restrict__ passage_offsets,
+                    int d, int total_tokens, double* __restrict__ kbar) {
+  constexpr int VEC = GVec<T>::n;
+  __shared__ double part[4][64][VEC];
+  const int pj = blockIdx.y;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int c = (blockIdx.x * 64 + lane) * VEC;
+  int t0, t1;
+  range_of(passage_offsets, pj, total_tokens, t0, t1);
+  double acc[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) acc[e] = 0.0;
+  if (c < d) {
+    int t = t0 + wave;
+    for (; t + 12 < t1; t += 16) {
+      u32x4 x[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        x[q] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(Kh + (size_t)(t + 4 * q) * d + c));
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        double v[VEC];
+        unpack_f64<T>(x[q], v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+      }
+    }
+    for (; t < t1; t += 4) {
+      u32x4 x = *reinterpret_cast<const u32x4*>(Kh + (size_t)t * d + c);
+      double v[VEC];
+      unpack_f64<T>(x, v);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) part[wave][lane][e] = acc[e];
+  __syncthreads();
+  if (wave == 0 && c < d) {
+    const int L = t1 - t0;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const double s = ((part[0][lane][e] + part[1][lane][e]) + part[2][lane][e]) +
+                       part[3][lane][e];
+      kbar[(size_t)pj * d + c + e] = (L > 0) ? s / (double)L : 0.0;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Edge cosines.  Workgroup = kEdgeRows kept rows of one question against all
+// of its passages.  Columns are processed in chunks of kEdgeCW: the rows'
+// chunk (transposed, float) and the passage keys' chunk (float64) are staged
+// in LDS; thread t accumulates the float64 dot products of the (row, passage)
+// pairs t, t+256, ...
+constexpr int kEdgeRows = 16;
+constexpr int kEdgeCW = 64;
+constexpr int kEdgeMaxPairs = (kEdgeRows * 64 + 255) / 256;
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+edge_cos_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
+                int N, const int32_t* __restrict__ kept_offsets,
+                const int32_t* __restrict__ query_passages,
+                const double* __restrict__ kbar, const float* __restrict__ pkeys,
+                int d, int total_kept, int total_passages, int k_max, int P_max,
+                double* __restrict__ cosv) {
+  extern __shared__ double sm[];
+  double* kb = sm;                                       // [P][kEdgeCW]
+  float* qT = reinterpret_cast<float*>(sm + (size_t)P_max * kEdgeCW);  // [kEdgeCW][kEdgeRows]
+  __shared__ double nq2[kEdgeRows];
+  __shared__ double nk2[64];
+
+  const int b = blockIdx.y;
+  int k0, k1, p0, p1;
+  range_of(kept_offsets, b, total_kept, k0, k1);
+  range_of(query_passages, b, total_passages, p0, p1);
+  const int kb_ = min(k1 - k0, k_max);
+  const int P = min(min(p1 - p0, P_max), 64);
+  const int i0 = blockIdx.x * kEdgeRows;
+  if (i0 >= kb_ || P <= 0) return;
+  const int nrows = min(kEdgeRows, kb_ - i0);
+
+  // Source row of each kept row of this block.
+  __shared__ const T* rowp[kEdgeRows];
+  if (threadIdx.x < kEdgeRows) {
+    const int i = i0 + threadIdx.x;
+    const T* ptr = nullptr;
+    if (threadIdx.x < nrows) {
+      if (kept_idx) {
+        const int src = clampi(kept_idx[k0 + i], 0, N - 1);
+        ptr = qbase + ((size_t)b * N + src) * d;
+      } else {
+        ptr = qbase + (size_t)(k0 + i) * d;
+      }
+    }
+    rowp[threadIdx.x] = ptr;
+  }
+  __syncthreads();
+
+  double acc[kEdgeMaxPairs];
+#pragma unroll
+  for (int q = 0; q < kEdgeMaxPairs; ++q) acc[q] = 0.0;
+  double qq = 0.0, kk = 0.0;
+  const int npairs = kEdgeRows * P;
+
+  for (int cc = 0; cc < d; cc += kEdgeCW) {
+    const int cw = min(kEdgeCW, d - cc);
+    // stage the rows' chunk, transposed
+    for (int e = threadIdx.x; e < kEdgeRows * kEdgeCW; e += blockDim.x) {
+      const int r = e / kEdgeCW, c = e % kEdgeCW;
+      float v = 0.f;
+      if (r < nrows && c < cw) v = elem_f32(rowp[r], (size_t)(cc + c));
+      qT[c * kEdgeRows + r] = v;
+    }
+    // stage the passage keys' chunk
+    for (int e = threadIdx.x; e < P * kEdgeCW; e += blockDim.x) {
+      const int j = e / kEdgeCW, c = e % kEdgeCW;
+      double v = 0.0;
+      if (c < cw) {
+        const size_t off = (size_t)(p0 + j) * d + cc + c;
+        v = pkeys ? (double)pkeys[off] : kbar[off];
+      }
+      kb[j * kEdgeCW + c] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kEdgeMaxPairs; ++q) {
+      const int pr = threadIdx.x + q * 256;
+      if (pr < npairs) {
+        const int i = pr % kEdgeRows, j = pr / kEdgeRows;
+        double s = acc[q];
+        for (int c = 0; c < cw; ++c)
+          s = fma((double)qT[c * kEdgeRows + i], kb[j * kEdgeCW + c], s);
+        acc[q] = s;
+      }
+    }
+    if (threadIdx.x < kEdgeRows) {
+      for (int c = 0; c < cw; ++c) {
+        const double v = (double)qT[c * kEdgeRows + threadIdx.x];
+        qq = fma(v, v, qq);
+      }
+    } else if (threadIdx.x >= 64 && threadIdx.x < 64 + P) {
+      const int j = threadIdx.x - 64;
+      for (int c = 0; c < cw; ++c) {
+        const double v = kb[j * kEdgeCW + c];
+        kk = fma(v, v, kk);
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x < kEdgeRows) nq2[threadIdx.x] = qq;
+  else if (threadIdx.x >= 64 && threadIdx.x < 64 + P) nk2[threadIdx.x - 64] = kk;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kEdgeMaxPairs; ++q) {
+    const int pr = threadIdx.x + q * 256;
+    if (pr < npairs) {
+      const int i = pr % kEdgeRows, j = pr / kEdgeRows;
+      if (i < nrows) {
+        const double nq = sqrt(nq2[i]), nk = sqrt(nk2[j]);
+        const double c = (nq > 0.0 && nk > 0.0) ? acc[q] / (nq * nk) : 0.0;
+        cosv[(size_t)b * k_max * P_max + (size_t)(i0 + i) * P + j] = c;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Edge selection, one workgroup per question.
+constexpr int kGSelThreads = 1024;
+constexpr int kGSelMaxPT = 16;     // k_b * P_b <= 16384
+
+__global__ void __launch_bounds__(kGSelThreads)
+edge_select_kernel(const double* __restrict__ cosv, const int32_t* __restrict__ kept_offsets,
+                   const int32_t* __restrict__ query_passages, int B, int total_kept,
+                   int total_passages, int k_max, int P_max, double avg_degree,
+                   uint64_t* __restrict__ rowmask, int32_t* __restrict__ rowptr_out,
+                   int32_t* __restrict__ col_out) {
+  __shared__ SelectShared sh;
+  __shared__ uint32_t scan_sh[20];
+  __shared__ uint8_t flag[kGSelThreads * kGSelMaxPT];
+  const int b = blockIdx.x;
+  int k0, k1, p0, p1;
+  range_of(kept_offsets, b, total_kept, k0, k1);
+  range_of(query_passages, b, total_passages, p0, p1);
+  const int k = min(k1 - k0, k_max);
+  const int P = min(min(p1 - p0, P_max), 64);
+  const int n = min(k * P, kGSelThreads * kGSelMaxPT);
+  const long long want = (long long)ceil(avg_degree * (double)k);
+  const int E = (int)min((long long)n, max(0ll, want));
+
+  const int C = (n + blockDim.x - 1) / blockDim.x;
+  const int e0 = threadIdx.x * C;
+  const int cnt = max(0, min(C, n - e0));
+  const double* cb = cosv + (size_t)b * k_max * P_max;
+  uint64_t keys[kGSelMaxPT];
+#pragma unroll
+  for (int j = 0; j < kGSelMaxPT; ++j) keys[j] = (j < cnt) ? order_key(cb[e0 + j]) : 0ull;
+  const uint32_t flags = block_select_top<kGSelMaxPT>(keys, cnt, n, E, &sh);
+
+#pragma unroll
+  for (int j = 0; j < kGSelMaxPT; ++j)
+    if (j < cnt) flag[e0 + j] = (flags >> j) & 1u;
+  __syncthreads();
+  for (int i = threadIdx.x; i < k; i += blockDim.x) {
+    uint64_t m = 0;
+    if (P > 0 && (i + 1) * P <= n)
+      for (int j = 0; j < P; ++j) m |= (uint64_t)flag[i * P + j] << j;
+    rowmask[k0 + i] = m;
+  }
+  if (rowptr_out == nullptr || col_out == nullptr) return;
+
+  // CSR: the edges of question b start after those of questions 0..b-1.
+  long long base = 0;
+  for (int bb = 0; bb < b; ++bb) {
+    int a0, a1, q0, q1;
+    range_of(kept_offsets, bb, total_kept, a0, a1);
+    range_of(query_passages, bb, total_passages, q0, q1);
+    const int kq = min(a1 - a0, k_max), Pq = min(min(q1 - q0, P_max), 64);
+    const long long nq = min((long long)kq * Pq, (long long)kGSelThreads * kGSelMaxPT);
+    base += min(nq, max(0ll, (long long)ceil(avg_degree * (double)kq)));
+  }
+  uint32_t total;
+  uint32_t pos = block_exclusive_scan(__popc(flags), scan_sh, &total);
+  const long long cap = (long long)total_kept * P_max;
+#pragma unroll
+  for (int j = 0; j < kGSelMaxPT; ++j) {
+    if (j < cnt) {
+      const int f = e0 + j;
+      if (P > 0 && f % P == 0) {
+        const int i = f / P;
+        if (i < k) rowptr_out[k0 + i] = (int32_t)(base + pos);
+      }
+      if (flags & (1u << j)) {
+        if (base + pos < cap) col_out[base + pos] = f % P;
+        ++pos;
+      }
+    }
+  }
+  // Rows beyond the candidate range (P == 0): they have no edges.
+  if (P == 0)
+    for (int i = threadIdx.x; i < k; i += blockDim.x) rowptr_out[k0 + i] = (int32_t)base;
+  if (b == B - 1 && threadIdx.x == 0) rowptr_out[total_kept] = (int32_t)(base + total);
+}
+
+// ---------------------------------------------------------------------------
+// Neighbour masks from a caller-given CSR graph.
+__global__ void __launch_bounds__(256)
+csr_to_mask_kernel(const int32_t* __restrict__ kept_offsets,
+                   const int32_t* __restrict__ query_passages,
+                   const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+                   int total_kept, int total_passages, int total_edges,
+                   uint64_t* __restrict__ rowmask) {
+  const int b = blockIdx.y;
+  int k0, k1, p0, p1;
+  range_of(kept_offsets, b, total_kept, k0, k1);
+  range_of(query_passages, b, total_passages, p0, p1);
+  const int P = min(p1 - p0, 64);
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k0 + i >= k1) return;
+  int e0, e1;
+  range_of(rowptr, k0 + i, total_edges, e0, e1);
+  uint64_t m = 0;
+  for (int e = e0; e < e1; ++e) {
+    const int j = col[e];
+    if (j >= 0 && j < P) m |= 1ull << j;
+  }
+  rowmask[k0 + i] = m;
+}
+
+// ---------------------------------------------------------------------------
+hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
+                               const int32_t* passage_offsets, double* kbar,
+                               hipStream_t s) {
+  if (p.total_passages <= 0) return hipSuccess;
+  if (p.dtype == SKIP_F32) {
+    dim3 grid((p.d + 255) / 256, p.total_passages);
+    hipLaunchKernelGGL(passage_keys_kernel<float>, grid, dim3(256), 0, s,
+                       (const float*)Kh, passage_offsets, p.d, p.total_tokens, kbar);
+  } else {
+    dim3 grid((p.d + 511) / 512, p.total_passages);
+    hipLaunchKernelGGL(passage_keys_kernel<bf16_t>, grid, dim3(256), 0, s,
+                       (const bf16_t*)Kh, passage_offsets, p.d, p.total_tokens, kbar);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_cos(const skip_problem_t& p, QuerySource q,
+                           const int32_t* kept_offsets, const int32_t* query_passages,
+                           const double* kbar, const float* passage_keys, double* cosv,
+                           hipStream_t s) {
+  if (p.k_max <= 0 || p.P_max <= 0) return hipSuccess;
+  dim3 grid((p.k_max + kEdgeRows - 1) / kEdgeRows, p.B);
+  const size_t lds = (size_t)p.P_max * kEdgeCW * sizeof(double) +
+                     (size_t)kEdgeCW * kEdgeRows * sizeof(float);
+  if (p.dtype == SKIP_F32)
+    hipLaunchKernelGGL(edge_cos_kernel<float>, grid, dim3(256), lds, s,
+                       (const float*)q.base, q.kept_idx, q.N, kept_offsets, query_passages,
+                       kbar, passage_keys, p.d, p.total_kept, p.total_passages, p.k_max,
+                       p.P_max, cosv);
+  else
+    hipLaunchKernelGGL(edge_cos_kernel<bf16_t>, grid, dim3(256), lds, s,
+                       (const bf16_t*)q.base, q.kept_idx, q.N, kept_offsets,
+                       query_passages, kbar, passage_keys, p.d, p.total_kept,
+                       p.total_passages, p.k_max, p.P_max, cosv);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_select(const skip_problem_t& p, const double* cosv,
+                              const int32_t* kept_offsets, const int32_t* query_passages,
+                              uint64_t* rowmask, int32_t* rowptr_out, int32_t* col_out,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(edge_select_kernel, dim3(p.B), dim3(kGSelThreads), 0, s, cosv,
+                     kept_offsets, query_passages, p.B, p.total_kept, p.total_passages,
+                     p.k_max, p.P_max, p.avg_degree, rowmask, rowptr_out, col_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_csr_to_mask(const skip_problem_t& p, const int32_t* kept_offsets,
+                              const int32_t* query_passages, const int32_t* edge_rowptr,
+                              const int32_t* edge_col, uint64_t* rowmask, hipStream_t s) {
+  if (p.k_max <= 0) return hipSuccess;
+  dim3 grid((p.k_max + 255) / 256, p.B);
+  hipLaunchKernelGGL(csr_to_mask_kernel, grid, dim3(256), 0, s, kept_offsets,
+                     query_passages, edge_rowptr, edge_col, p.total_kept,
+                     p.total_passages, p.total_edges, rowmask);
+  return hipGetLastError();
+}
+
+}  // namespace skip

@@ -1,0 +1,264 @@
+// C ABI of libskip.so: argument validation, workspace carving, launches.
+// The public contract (argument meaning, layout, ownership, errors) is in
+// include/skip.h.
+#include <cmath>
+#include <cstdint>
+
+#include "skip.h"
+#include "skip_internal.h"
+
+namespace skip {
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kMaxN = 16384;
+constexpr int kMaxD = 8192;
+constexpr int kMaxCandidates = 16384;   // k_b * P_b per question
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+enum Need { kPrune = 1, kGraph = 2 };
+
+skip_status_t check_common(const skip_problem_t* p) {
+  if (!p) return SKIP_ERR_INVALID_ARG;
+  if (p->o_f32 != 0 && p->o_f32 != 1) return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_F32 && p->dtype != SKIP_BF16) return SKIP_ERR_INVALID_ARG;
+  if (p->B < 1 || p->d < 1 || p->k_max < 0 || p->total_kept < 0) return SKIP_ERR_INVALID_ARG;
+  if ((int64_t)p->total_kept > (int64_t)p->B * p->k_max) return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept < p->k_max) return SKIP_ERR_INVALID_ARG;
+  if (p->d % 8 != 0 || p->d > kMaxD) return SKIP_ERR_UNSUPPORTED;
+  return SKIP_OK;
+}
+
+skip_status_t check(const skip_problem_t* p, int need) {
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (need & kPrune) {
+    if (p->N < 1 || p->total_qtok < p->B) return SKIP_ERR_INVALID_ARG;
+    if (p->k_max > p->N) return SKIP_ERR_INVALID_ARG;
+    if (p->N > kMaxN) return SKIP_ERR_UNSUPPORTED;
+    if ((int64_t)p->B * p->N > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  }
+  if (need & kGraph) {
+    if (p->H < 1 || p->d_h < 1 || (int64_t)p->H * p->d_h != p->d) return SKIP_ERR_INVALID_ARG;
+    if (p->d_h != 64 && p->d_h != 128) return SKIP_ERR_UNSUPPORTED;
+    if (p->P_max < 0 || p->total_passages < p->P_max) return SKIP_ERR_INVALID_ARG;
+    if ((int64_t)p->total_passages > (int64_t)p->B * p->P_max) return SKIP_ERR_INVALID_ARG;
+    if (p->total_tokens < p->total_passages) return SKIP_ERR_INVALID_ARG;
+    if (p->total_passages > 0 && (p->L_max < 1 || p->L_max > p->total_tokens))
+      return SKIP_ERR_INVALID_ARG;
+    if (!std::isfinite(p->avg_degree) || p->avg_degree < 0.0) return SKIP_ERR_INVALID_ARG;
+    if (!std::isfinite(p->sm_scale)) return SKIP_ERR_INVALID_ARG;
+    if (p->total_edges < 0) return SKIP_ERR_INVALID_ARG;
+    if (p->P_max > 64) return SKIP_ERR_UNSUPPORTED;
+    if ((int64_t)p->k_max * p->P_max > kMaxCandidates) return SKIP_ERR_UNSUPPORTED;
+  }
+  return SKIP_OK;
+}
+
+size_t workspace_size(const skip_problem_t& p) {
+  size_t n = 0;
+  n += align_up((size_t)p.B * p.d * sizeof(double));                  // u
+  n += align_up((size_t)p.B * (size_t)p.N * sizeof(double));          // z
+  n += align_up((size_t)p.total_passages * p.d * sizeof(double));     // kbar
+  n += align_up((size_t)p.B * p.k_max * p.P_max * sizeof(double));    // cos
+  n += align_up((size_t)p.total_kept * sizeof(uint64_t));             // rowmask
+  return n;
+}
+
+#define SKIP_TRY(expr)                       \
+  do {                                       \
+    hipError_t e_ = (expr);                  \
+    if (e_ != hipSuccess) return SKIP_ERR_HIP; \
+  } while (0)
+
+}  // namespace
+
+Workspace carve_workspace(const skip_problem_t& p, void* base) {
+  Workspace w{};
+  char* c = static_cast<char*>(base);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* r = c + off;
+    off += align_up(bytes);
+    return r;
+  };
+  w.u = reinterpret_cast<double*>(take((size_t)p.B * p.d * sizeof(double)));
+  w.z = reinterpret_cast<double*>(take((size_t)p.B * (size_t)p.N * sizeof(double)));
+  w.kbar = reinterpret_cast<double*>(take((size_t)p.total_passages * p.d * sizeof(double)));
+  w.cosv = reinterpret_cast<double*>(take((size_t)p.B * p.k_max * p.P_max * sizeof(double)));
+  w.rowmask = reinterpret_cast<uint64_t*>(take((size_t)p.total_kept * sizeof(uint64_t)));
+  w.bytes = off;
+  return w;
+}
+
+}  // namespace skip
+
+using namespace skip;
+
+extern "C" {
+
+int32_t skip_abi_version(void) { return SKIP_ABI_VERSION; }
+
+const char* skip_status_string(skip_status_t s) {
+  switch (s) {
+    case SKIP_OK: return "SKIP_OK";
+    case SKIP_ERR_INVALID_ARG: return "SKIP_ERR_INVALID_ARG: invalid argument";
+    case SKIP_ERR_UNSUPPORTED: return "SKIP_ERR_UNSUPPORTED: shape not implemented";
+    case SKIP_ERR_WORKSPACE: return "SKIP_ERR_WORKSPACE: workspace too small";
+    case SKIP_ERR_HIP: return "SKIP_ERR_HIP: HIP launch failed";
+  }
+  return "SKIP_ERR_UNKNOWN";
+}
+
+skip_status_t skip_workspace_bytes(const skip_problem_t* p, size_t* bytes) {
+  if (!bytes) return SKIP_ERR_INVALID_ARG;
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (p->N < 0 || p->P_max < 0 || p->total_passages < 0) return SKIP_ERR_INVALID_ARG;
+  *bytes = workspace_size(*p);
+  return SKIP_OK;
+}
+
+skip_status_t skip_prune_topk(const skip_problem_t* p, const void* V, const void* Qtok,
+                              const int32_t* q_offsets, const void* w_bias,
+                              const int32_t* kept_offsets, int32_t* kept_idx, float* scores,
+                              void* V_kept, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  skip_status_t st = check(p, kPrune);
+  if (st != SKIP_OK) return st;
+  if (!V || !Qtok || !q_offsets || !kept_offsets || !workspace) return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && !kept_idx) return SKIP_ERR_INVALID_ARG;
+  if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Workspace w = carve_workspace(*p, workspace);
+  SKIP_TRY(launch_pool_question(*p, Qtok, q_offsets, w_bias, w.u, s));
+  SKIP_TRY(launch_score(*p, V, w.u, w.z, scores, s));
+  if (p->total_kept > 0) {
+    SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
+    if (V_kept) SKIP_TRY(launch_gather(*p, V, kept_offsets, kept_idx, V_kept, s));
+  }
+  return SKIP_OK;
+}
+
+skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
+                                   const int32_t* kept_offsets, const void* Kh, const void* Vh,
+                                   const int32_t* passage_offsets,
+                                   const int32_t* query_passages, const float* passage_keys,
+                                   const int32_t* edge_rowptr, const int32_t* edge_col,
+                                   void* O, float* lse, int32_t* edge_rowptr_out,
+                                   int32_t* edge_col_out, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  skip_status_t st = check(p, kGraph);
+  if (st != SKIP_OK) return st;
+  if (!kept_offsets || !query_passages || !passage_offsets || !workspace)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && (!Qh || !O)) return SKIP_ERR_INVALID_ARG;
+  if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
+  const bool given = edge_rowptr || edge_col;
+  if (given && (!edge_rowptr || (!edge_col && p->total_edges > 0))) return SKIP_ERR_INVALID_ARG;
+  if ((edge_rowptr_out == nullptr) != (edge_col_out == nullptr)) return SKIP_ERR_INVALID_ARG;
+  if (given && edge_rowptr_out) return SKIP_ERR_INVALID_ARG;
+  if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Workspace w = carve_workspace(*p, workspace);
+  if (p->total_kept == 0) {
+    // No kept rows: only the (empty) CSR needs its closing offset.
+    if (edge_rowptr_out)
+      SKIP_TRY(launch_edge_select(*p, w.cosv, kept_offsets, query_passages, w.rowmask,
+                                  edge_rowptr_out, edge_col_out, s));
+    return SKIP_OK;
+  }
+  QuerySource q{Qh, nullptr, 0};
+  if (given) {
+    SKIP_TRY(launch_csr_to_mask(*p, kept_offsets, query_passages, edge_rowptr, edge_col,
+                                w.rowmask, s));
+  } else {
+    if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
+    SKIP_TRY(launch_edge_cos(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
+                             w.cosv, s));
+    SKIP_TRY(launch_edge_select(*p, w.cosv, kept_offsets, query_passages, w.rowmask,
+                                edge_rowptr_out, edge_col_out, s));
+  }
+  SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
+                            w.rowmask, O, lse, s));
+  return SKIP_OK;
+}
+
+static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
+                                      const void* Qtok, const int32_t* q_offsets,
+                                      const void* w_bias, const int32_t* kept_offsets,
+                                      const void* Kh, const void* Vh,
+                                      const int32_t* passage_offsets,
+                                      const int32_t* query_passages,
+                                      const float* passage_keys, int32_t* kept_idx, void* O,
+                                      float* lse, void* workspace, size_t workspace_bytes,
+                                      void* stream, void* const* ev) {
+  skip_status_t st = check(p, kPrune | kGraph);
+  if (st != SKIP_OK) return st;
+  if (!V || !Qtok || !q_offsets || !kept_offsets || !query_passages || !passage_offsets ||
+      !workspace)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && (!kept_idx || !O)) return SKIP_ERR_INVALID_ARG;
+  if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
+  if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Workspace w = carve_workspace(*p, workspace);
+  int stage = 0;
+  auto mark = [&]() -> hipError_t {
+    return ev ? hipEventRecord(static_cast<hipEvent_t>(ev[stage++]), s) : hipSuccess;
+  };
+  const bool work = p->total_kept > 0;
+  QuerySource q{V, kept_idx, p->N};
+  SKIP_TRY(mark());
+  if (work) SKIP_TRY(launch_pool_question(*p, Qtok, q_offsets, w_bias, w.u, s));
+  SKIP_TRY(mark());
+  if (work) SKIP_TRY(launch_score(*p, V, w.u, w.z, nullptr, s));
+  SKIP_TRY(mark());
+  if (work) SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
+  SKIP_TRY(mark());
+  if (work && !passage_keys)
+    SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
+  SKIP_TRY(mark());
+  if (work)
+    SKIP_TRY(launch_edge_cos(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
+                             w.cosv, s));
+  SKIP_TRY(mark());
+  if (work)
+    SKIP_TRY(launch_edge_select(*p, w.cosv, kept_offsets, query_passages, w.rowmask, nullptr,
+                                nullptr, s));
+  SKIP_TRY(mark());
+  if (work)
+    SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
+                              w.rowmask, O, lse, s));
+  SKIP_TRY(mark());
+  return SKIP_OK;
+}
+
+skip_status_t skip_route_fused(const skip_problem_t* p, const void* V, const void* Qtok,
+                               const int32_t* q_offsets, const void* w_bias,
+                               const int32_t* kept_offsets, const void* Kh, const void* Vh,
+                               const int32_t* passage_offsets, const int32_t* query_passages,
+                               const float* passage_keys, int32_t* kept_idx, void* O,
+                               float* lse, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  return route_fused_impl(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                          passage_offsets, query_passages, passage_keys, kept_idx, O, lse,
+                          workspace, workspace_bytes, stream, nullptr);
+}
+
+skip_status_t skip_route_fused_profiled(
+    const skip_problem_t* p, const void* V, const void* Qtok, const int32_t* q_offsets,
+    const void* w_bias, const int32_t* kept_offsets, const void* Kh, const void* Vh,
+    const int32_t* passage_offsets, const int32_t* query_passages, const float* passage_keys,
+    int32_t* kept_idx, void* O, float* lse, void* workspace, size_t workspace_bytes,
+    void* stream, void* const* stage_events, int32_t n_events) {
+  if (!stage_events || n_events != SKIP_FUSED_STAGES + 1) return SKIP_ERR_INVALID_ARG;
+  for (int i = 0; i < n_events; ++i)
+    if (!stage_events[i]) return SKIP_ERR_INVALID_ARG;
+  return route_fused_impl(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                          passage_offsets, query_passages, passage_keys, kept_idx, O, lse,
+                          workspace, workspace_bytes, stream, stage_events);
+}
+
+}  // extern "C"

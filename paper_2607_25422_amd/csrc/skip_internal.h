@@ -1,0 +1,70 @@
+// Host-side launchers of the SKIP kernels (internal to libskip.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "skip.h"
+
+namespace skip {
+
+// Workspace carve-up (byte offsets from the workspace base, 256-B aligned).
+struct Workspace {
+  double* u;          // [B][d]        scoring vector q_bar/sqrt(d) + w
+  double* z;          // [B][N]        salience logits
+  double* kbar;       // [total_passages][d] passage keys
+  double* cosv;       // [B][k_max*P_max] cosines, flattened i*P_b + j
+  uint64_t* rowmask;  // [total_kept]  neighbour passages of each kept row
+  size_t bytes;
+};
+
+Workspace carve_workspace(const skip_problem_t& p, void* base);
+
+// Stage 1 ---------------------------------------------------------------
+hipError_t launch_pool_question(const skip_problem_t& p, const void* Qtok,
+                                const int32_t* q_offsets, const void* w_bias,
+                                double* u, hipStream_t s);
+hipError_t launch_score(const skip_problem_t& p, const void* V, const double* u,
+                        double* z, float* scores, hipStream_t s);
+hipError_t launch_topk(const skip_problem_t& p, const double* z,
+                       const int32_t* kept_offsets, int32_t* kept_idx,
+                       hipStream_t s);
+hipError_t launch_gather(const skip_problem_t& p, const void* V,
+                         const int32_t* kept_offsets, const int32_t* kept_idx,
+                         void* V_kept, hipStream_t s);
+
+// Stage 2 ---------------------------------------------------------------
+// Query rows: if kept_idx is non-NULL, row r of question b is
+// V[b][kept_idx[r]] (the fused route); otherwise it is Qh[r].
+struct QuerySource {
+  const void* base;
+  const int32_t* kept_idx;   // NULL for Qh
+  int32_t N;                 // visual tokens per question (fused route)
+};
+
+hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
+                               const int32_t* passage_offsets, double* kbar,
+                               hipStream_t s);
+hipError_t launch_edge_cos(const skip_problem_t& p, QuerySource q,
+                           const int32_t* kept_offsets,
+                           const int32_t* query_passages, const double* kbar,
+                           const float* passage_keys, double* cosv,
+                           hipStream_t s);
+hipError_t launch_edge_select(const skip_problem_t& p, const double* cosv,
+                              const int32_t* kept_offsets,
+                              const int32_t* query_passages, uint64_t* rowmask,
+                              int32_t* rowptr_out, int32_t* col_out,
+                              hipStream_t s);
+hipError_t launch_csr_to_mask(const skip_problem_t& p, const int32_t* kept_offsets,
+                              const int32_t* query_passages,
+                              const int32_t* edge_rowptr, const int32_t* edge_col,
+                              uint64_t* rowmask, hipStream_t s);
+hipError_t launch_attention(const skip_problem_t& p, QuerySource q,
+                            const int32_t* kept_offsets, const void* Kh,
+                            const void* Vh, const int32_t* passage_offsets,
+                            const int32_t* query_passages,
+                            const uint64_t* rowmask, void* O, float* lse,
+                            hipStream_t s);
+
+}  // namespace skip

@@ -1,0 +1,113 @@
+// Block-wide exact top-k selection on 64-bit order-preserving keys.
+//
+// Used for both cuts of the routing core: the kept visual tokens (top k_b
+// logits of a question, Def. B.1) and the graph edges (top E_b cosines of a
+// question, Def. B.3).  The selected set is: every key above the k-th largest
+// key, plus, among keys equal to it, the ones with the lowest element index.
+//
+// Method: MSB-first radix select with 8-bit digits.  Each pass histograms the
+// digits of the keys that still share the chosen prefix, finds the digit at
+// which the running count from the top reaches the number still needed, and
+// narrows the prefix.  It stops early once every key sharing the prefix is
+// needed; after all 8 passes the remaining keys are exactly equal and an
+// ordered prefix count admits the lowest indices.  Counts are integers, so
+// the result does not depend on thread timing.
+//
+// Data layout: thread t holds elements [t*C, t*C + cnt) of the n elements in
+// registers (keys[0..cnt)), C = ceil(n / blockDim.x) <= MAXPT.
+#pragma once
+
+#include "skip_common.h"
+
+namespace skip {
+
+struct SelectShared {
+  uint32_t hist[256];
+  uint32_t misc[4];
+  uint32_t scan[20];
+};
+
+// Returns a bitmask over the thread's elements (bit j = element t*C + j).
+template <int MAXPT>
+__device__ uint32_t block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int n,
+                                     int kk, SelectShared* sh) {
+  static_assert(MAXPT <= 32, "flags are a 32-bit mask");
+  const uint32_t all = (cnt >= 32) ? 0xffffffffu : ((1u << cnt) - 1u);
+  if (kk <= 0) return 0u;
+  if (kk >= n) return all;
+
+  uint64_t prefix = 0, mask = 0;
+  uint32_t need = (uint32_t)kk;
+  bool whole_bucket = false;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[i] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < MAXPT; ++j) {
+      if (j < cnt && (keys[j] & mask) == prefix)
+        atomicAdd(&sh->hist[(uint32_t)(keys[j] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+      const int l = threadIdx.x;
+      const uint32_t h0 = sh->hist[255 - 4 * l], h1 = sh->hist[254 - 4 * l];
+      const uint32_t h2 = sh->hist[253 - 4 * l], h3 = sh->hist[252 - 4 * l];
+      const uint32_t s = h0 + h1 + h2 + h3;
+      uint32_t inc = s;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        uint32_t y = __shfl_up(inc, o, kWave);
+        if (l >= o) inc += y;
+      }
+      const uint32_t exc = inc - s;
+      if (exc < need && need <= inc) {       // exactly one lane
+        uint32_t c = exc;
+        uint32_t bin, inbin;
+        if (c + h0 >= need) {
+          bin = 255 - 4 * l; inbin = h0;
+        } else if (c + h0 + h1 >= need) {
+          c += h0; bin = 254 - 4 * l; inbin = h1;
+        } else if (c + h0 + h1 + h2 >= need) {
+          c += h0 + h1; bin = 253 - 4 * l; inbin = h2;
+        } else {
+          c += h0 + h1 + h2; bin = 252 - 4 * l; inbin = h3;
+        }
+        sh->misc[0] = bin;
+        sh->misc[1] = c;        // candidates with a larger digit: all taken
+        sh->misc[2] = inbin;    // candidates with exactly this digit
+      }
+    }
+    __syncthreads();
+    const uint32_t bin = sh->misc[0], above = sh->misc[1], inbin = sh->misc[2];
+    __syncthreads();
+    need -= above;
+    prefix |= (uint64_t)bin << shift;
+    mask |= 0xffull << shift;
+    if (inbin == need) { whole_bucket = true; break; }
+  }
+
+  uint32_t flags = 0u, inb = 0u;
+#pragma unroll
+  for (int j = 0; j < MAXPT; ++j) {
+    if (j < cnt) {
+      const uint64_t m = keys[j] & mask;
+      if (m > prefix) flags |= 1u << j;
+      else if (m == prefix) inb |= 1u << j;
+    }
+  }
+  if (whole_bucket) return flags | inb;
+  // Exactly equal keys: admit the `need` lowest indices.
+  uint32_t total;
+  uint32_t rank = block_exclusive_scan(__popc(inb), sh->scan, &total);
+#pragma unroll
+  for (int j = 0; j < MAXPT; ++j) {
+    if (inb & (1u << j)) {
+      if (rank < need) flags |= 1u << j;
+      ++rank;
+    }
+  }
+  return flags;
+}
+
+}  // namespace skip

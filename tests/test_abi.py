@@ -1,0 +1,139 @@
+"""The C ABI on the host: the library loads, exports every symbol the header
+declares, and rejects bad arguments before touching any device (no GPU needed:
+every call here fails validation before anything is enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "skip.h")
+
+
+@pytest.fixture(scope="module")
+def b():
+    from paper_2607_25422_amd import binding
+    return binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(skip_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_entry_points():
+    names = declared_functions()
+    for n in ("skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(b):
+    for name in declared_functions():
+        assert hasattr(b.LIB, name), name
+    assert set(b.ENTRY_POINTS) == set(declared_functions())
+
+
+def test_version_and_status_strings(b):
+    assert b.abi_version() == 1
+    for s in range(5):
+        assert b.status_string(s).startswith("SKIP_")
+    assert "UNKNOWN" in b.status_string(99)
+
+
+def test_problem_struct_layout(b):
+    # 14 int32, a double at offset 56, a float and an int32 after it
+    assert ctypes.sizeof(b.SkipProblem) == 72
+    assert b.SkipProblem.avg_degree.offset == 56
+
+
+def _problem(b, **kw):
+    base = dict(B=2, N=576, d=1024, H=16, d_h=64, q_offsets=[0, 3, 7],
+                kept_offsets=[0, 96, 192], passage_offsets=[0, 10, 20, 30],
+                query_passages=[0, 2, 3], sm_scale=0.125)
+    base.update(kw)
+    return b.make_problem("bf16", **base)
+
+
+def test_workspace_bytes(b):
+    p = _problem(b)
+    n = b.workspace_bytes(p)
+    # u + z + kbar + cos + rowmask, each rounded to 256 bytes
+    parts = [2 * 1024 * 8, 2 * 576 * 8, 3 * 1024 * 8, 2 * 96 * 2 * 8, 192 * 8]
+    assert n == sum((x + 255) // 256 * 256 for x in parts)
+    with pytest.raises(b.SkipError):
+        b.workspace_bytes(_problem(b, B=0, q_offsets=[0], kept_offsets=[0], query_passages=[0]))
+
+
+FAKE = 1 << 40   # never dereferenced: every call below fails validation
+
+
+def _prune(b, p, ws_bytes=1 << 30, **ptrs):
+    args = dict(V=FAKE, Qtok=FAKE, q_off=FAKE, w=None, k_off=FAKE, idx=FAKE, scores=None,
+                vk=None, ws=FAKE)
+    args.update(ptrs)
+    return b.LIB.skip_prune_topk(ctypes.byref(p), args["V"], args["Qtok"], args["q_off"],
+                                 args["w"], args["k_off"], args["idx"], args["scores"],
+                                 args["vk"], args["ws"], ws_bytes, None)
+
+
+def test_prune_rejects_bad_arguments(b):
+    p = _problem(b)
+    assert _prune(b, p, V=None) == b.SKIP_ERR_INVALID_ARG
+    assert _prune(b, p, idx=None) == b.SKIP_ERR_INVALID_ARG
+    assert _prune(b, p, ws=None) == b.SKIP_ERR_INVALID_ARG
+    assert _prune(b, p, ws_bytes=16) == b.SKIP_ERR_WORKSPACE
+    assert _prune(b, _problem(b, kept_offsets=[0, 600, 700])) == b.SKIP_ERR_INVALID_ARG  # k > N
+    assert _prune(b, _problem(b, N=20000)) == b.SKIP_ERR_UNSUPPORTED
+    assert _prune(b, _problem(b, d=1020, H=15, d_h=68)) == b.SKIP_ERR_UNSUPPORTED
+    q = _problem(b)
+    q.o_f32 = 2
+    assert _prune(b, q) == b.SKIP_ERR_INVALID_ARG
+    q = _problem(b)
+    q.dtype = 7
+    assert _prune(b, q) == b.SKIP_ERR_INVALID_ARG
+    q = _problem(b)
+    q.total_qtok = 1          # fewer question tokens than questions
+    assert _prune(b, q) == b.SKIP_ERR_INVALID_ARG
+
+
+def _xattn(b, p, ws_bytes=1 << 30, **ptrs):
+    a = dict(Qh=FAKE, k_off=FAKE, Kh=FAKE, Vh=FAKE, p_off=FAKE, qp=FAKE, pk=None, erp=None,
+             ecol=None, O=FAKE, lse=None, rp_out=None, col_out=None, ws=FAKE)
+    a.update(ptrs)
+    return b.LIB.skip_bipartite_xattn(ctypes.byref(p), a["Qh"], a["k_off"], a["Kh"], a["Vh"],
+                                      a["p_off"], a["qp"], a["pk"], a["erp"], a["ecol"], a["O"],
+                                      a["lse"], a["rp_out"], a["col_out"], a["ws"], ws_bytes,
+                                      None)
+
+
+def test_xattn_rejects_bad_arguments(b):
+    p = _problem(b)
+    assert _xattn(b, p, O=None) == b.SKIP_ERR_INVALID_ARG
+    assert _xattn(b, p, Kh=None) == b.SKIP_ERR_INVALID_ARG
+    assert _xattn(b, p, rp_out=FAKE) == b.SKIP_ERR_INVALID_ARG          # one of a pair
+    assert _xattn(b, p, erp=FAKE, rp_out=FAKE, col_out=FAKE) == b.SKIP_ERR_INVALID_ARG
+    assert _xattn(b, p, ws_bytes=0) == b.SKIP_ERR_WORKSPACE
+    assert _xattn(b, _problem(b, d_h=32, H=32)) == b.SKIP_ERR_UNSUPPORTED
+    assert _xattn(b, _problem(b, H=8)) == b.SKIP_ERR_INVALID_ARG          # H*d_h != d
+    many = list(range(0, 70 * 10 + 1, 10))
+    assert _xattn(b, _problem(b, passage_offsets=many, query_passages=[0, 65, 70])) \
+        == b.SKIP_ERR_UNSUPPORTED                                           # P > 64
+    q = _problem(b)
+    q.avg_degree = float("nan")
+    assert _xattn(b, q) == b.SKIP_ERR_INVALID_ARG
+    q = _problem(b)
+    q.total_tokens = 1        # fewer tokens than passages
+    assert _xattn(b, q) == b.SKIP_ERR_INVALID_ARG
+
+
+def test_fused_requires_matching_head_split(b):
+    p = _problem(b, H=8)      # 8 * 64 != 1024
+    st = b.LIB.skip_route_fused(ctypes.byref(p), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None)
+    assert st == b.SKIP_ERR_INVALID_ARG
+    p = _problem(b)
+    st = b.LIB.skip_route_fused(ctypes.byref(p), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, None, None, FAKE, None, FAKE, 1 << 30, None)
+    assert st == b.SKIP_ERR_INVALID_ARG                                   # kept_idx NULL

@@ -1,0 +1,309 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle
+on the same seeded inputs.
+
+Bars: kept-token sets and edge sets identical (selection is decided in
+float64 on both sides); attention outputs within 1e-5 relative (fp32 mode,
+max |y - y_ref| / max(|y_ref|, RMS(y_ref))) or 2e-2 of the output RMS (bf16
+mode); rows without neighbours exactly zero with LSE = -inf.
+
+bf16 mode is checked twice.  With float32 output (o_f32) the raw error must
+be within 2e-2 x RMS.  With bf16 output the one rounding of each stored value
+(at most 2^-8 of its magnitude) is allowed on top of that bar: a correctly
+rounded bf16 value can already differ from the float64 result by more than
+2e-2 x RMS when |O| exceeds a few times the RMS.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2607_25422_amd import workloads as wls
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def B():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    from paper_2607_25422_amd import binding
+    return binding
+
+
+# --------------------------------------------------------------------------- helpers
+
+def f64(t):
+    return t.detach().cpu().to(torch.float64).numpy()
+
+
+def check_attention(O, L, O_ref, L_ref, dtype, tag="", stored_bf16=None):
+    """O, O_ref: [n, H, d_h]; L, L_ref: [n, H] (float64 numpy).  In bf16
+    mode ``stored_bf16`` says whether O was written as bf16 (default) or as
+    float32."""
+    if stored_bf16 is None:
+        stored_bf16 = dtype != "f32"
+    if O_ref.size == 0:
+        return
+    live = np.isfinite(L_ref).all(axis=1)
+    dead = ~live
+    assert np.all(O[dead] == 0), f"{tag}: rows without neighbours must be 0"
+    assert np.all(np.isneginf(L[dead])), f"{tag}: rows without neighbours need LSE = -inf"
+    if not live.any():
+        return
+    y, r = O[live], O_ref[live]
+    rms = math.sqrt(float(np.mean(r * r)))
+    if dtype == "f32":
+        err = np.max(np.abs(y - r) / np.maximum(np.abs(r), rms))
+        assert err <= 1e-5, f"{tag}: fp32 max relative error {err:.3e}"
+        lerr = np.max(np.abs(L[live] - L_ref[live]) / np.maximum(1.0, np.abs(L_ref[live])))
+        assert lerr <= 1e-5, f"{tag}: LSE error {lerr:.3e}"
+    else:
+        allow = (2.0 ** -8) * np.abs(r) if stored_bf16 else 0.0
+        raw = np.max(np.abs(y - r)) / rms
+        err = np.max(np.abs(y - r) - allow) / rms
+        say(f"{tag}: bf16 max error {raw:.3e} x RMS raw, {err:.3e} beyond storage rounding")
+        assert err <= 2e-2, f"{tag}: bf16 max error {err:.3e} x RMS"
+        lerr = np.max(np.abs(L[live] - L_ref[live]) / np.maximum(1.0, np.abs(L_ref[live])))
+        assert lerr <= 1e-3, f"{tag}: LSE error {lerr:.3e}"
+
+
+def oracle_route(batch, **kw):
+    return orc.route(batch.V, batch.Qtok, batch.q_offsets, batch.kept_offsets, batch.Kh,
+                     batch.Vh, batch.passage_offsets, batch.query_passages, batch.wl.scale,
+                     batch.wl.avg_degree, w_bias=batch.w_bias, **kw)
+
+
+def sample_rows(batch, per_q, seed=0):
+    rng = np.random.default_rng(seed)
+    out = {}
+    for b in range(batch.B):
+        k = int(batch.k[b])
+        out[b] = sorted(rng.choice(k, size=min(per_q, k), replace=False).tolist()) if k else []
+    return out
+
+
+def small_batch(dtype, seed, **kw):
+    name = "tiny_fp32" if dtype == "f32" else "llava_bf16"
+    base = dict(B=5, N=300, H=4, d_h=64, T=(1, 3, 8), k=(0, 7, 33, 64, 300),
+                P=(0, 1, 3, 6), L_p=(1, 5, 64, 100))
+    base.update(kw)
+    return wls.make_batch(name, seed, **base)
+
+
+def run_prune(B, batch):
+    db = B.to_device(batch)
+    idx, scores, rows = B.prune_topk(db)
+    torch.cuda.synchronize()
+    return db, idx.cpu().numpy(), scores.cpu().numpy(), rows.cpu()
+
+
+# --------------------------------------------------------------------------- stage 1
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seed", wls.SEEDS)
+def test_prune_small_ragged(B, dtype, seed):
+    batch = small_batch(dtype, seed, with_bias=True)
+    say(f"prune small {dtype} seed={seed} k={batch.k.tolist()}")
+    db, idx, scores, rows = run_prune(B, batch)
+    ref = oracle_route(batch, with_attention=False)
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist(), f"question {b}"
+        np.testing.assert_allclose(scores[b], ref.scores[b], rtol=1e-6, atol=1e-30)
+        assert torch.equal(rows[k0:k1], batch.V[b][torch.from_numpy(ref.kept_idx[b])])
+
+
+def test_prune_ties_lowest_index(B):
+    # identical visual tokens score identically: the lowest indices must win
+    batch = wls.make_batch("llava_bf16", 7, B=3, N=200, H=4, d_h=64, k=(5, 50, 199))
+    V = batch.V.clone()
+    V[:, 100:] = V[:, 0:100]          # every token duplicated 100 positions later
+    V[1, :, :] = V[1, 0, :]           # question 1: all 200 tokens equal
+    batch.V = V
+    db, idx, _, _ = run_prune(B, batch)
+    ref = oracle_route(batch, with_attention=False)
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist()
+    k0, k1 = batch.kept_offsets[1], batch.kept_offsets[2]
+    assert idx[k0:k1].tolist() == list(range(k1 - k0))
+
+
+@pytest.mark.parametrize("name", wls.ORDER)
+def test_prune_named_full_size(B, name):
+    batch = wls.make_batch(name, 2026, threads=16)
+    say(f"prune {name} full size B={batch.B} N={batch.wl.N}")
+    db, idx, scores, rows = run_prune(B, batch)
+    ref = oracle_route(batch, with_attention=False)
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist(), f"{name} question {b}"
+        if batch.planted[b].size:
+            kept = set(idx[k0:k1].tolist())
+            pl = set(batch.planted[b].tolist())
+            assert pl <= kept or kept <= pl, f"{name} q{b}: planted tokens lost"
+    b = batch.B - 1
+    np.testing.assert_allclose(scores[b], ref.scores[b], rtol=1e-6)
+
+
+# --------------------------------------------------------------------------- stage 2
+
+def queries_from_batch(batch):
+    """Kept-row queries for the stand-alone graph + attention call: the first
+    k_b visual tokens of each question viewed as [H, d_h]."""
+    H, d_h = batch.Kh.shape[1], batch.Kh.shape[2]
+    rows = [batch.V[b, :int(batch.k[b])] for b in range(batch.B)]
+    return torch.cat(rows, 0).reshape(-1, H, d_h).contiguous()
+
+
+def check_graph(batch, rp, col, adj_ref):
+    rp = rp.cpu().numpy()
+    col = col.cpu().numpy()
+    for b in range(batch.B):
+        k0 = int(batch.kept_offsets[b])
+        want_rp, want_col = orc.adjacency_to_csr(adj_ref[b])
+        got_rp = rp[k0:k0 + len(want_rp)] - rp[k0]
+        assert got_rp.tolist() == want_rp.tolist(), f"question {b}: row pointers"
+        got_col = col[rp[k0]:rp[k0] + len(want_col)]
+        assert got_col.tolist() == want_col.tolist(), f"question {b}: columns"
+    assert rp[-1] == sum(int(a.sum()) for a in adj_ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seed", wls.SEEDS)
+@pytest.mark.parametrize("deg", [4.0, 1.5])
+def test_xattn_small_ragged(B, dtype, seed, deg):
+    batch = small_batch(dtype, seed, H=2, d_h=128)
+    say(f"xattn small {dtype} seed={seed} deg={deg} P={batch.P.tolist()}")
+    db = B.to_device(batch, avg_degree=deg)
+    Qh = queries_from_batch(batch)
+    O, L, rp, col = B.bipartite_xattn(db, Qh.cuda())
+    torch.cuda.synchronize()
+    cos, adj, O_ref, L_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, deg)
+    check_graph(batch, rp, col, adj)
+    check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_xattn_given_graph_and_keys(B, dtype):
+    batch = small_batch(dtype, 11, B=4, k=(20, 64), P=(3, 7), L_p=(2, 70))
+    H, d_h = batch.Kh.shape[1], batch.Kh.shape[2]
+    db = B.to_device(batch)
+    Qh = queries_from_batch(batch)
+    rng = np.random.default_rng(5)
+    adj = [rng.random((int(k), int(P))) < 0.4 for k, P in zip(batch.k, batch.P)]
+    adj[0][0] = False                     # a row with no neighbour
+    adj[1][1] = True                      # a row adjacent to every passage
+    rp = [0]
+    cols = []
+    for a in adj:
+        for row in a:
+            cols.extend(np.nonzero(row)[0].tolist())
+            rp.append(len(cols))
+    edges = (torch.tensor(rp, dtype=torch.int32, device="cuda"),
+             torch.tensor(cols, dtype=torch.int32, device="cuda"))
+    O, L, _, _ = B.bipartite_xattn(db, Qh.cuda(), edges=edges)
+    _, _, O_ref, L_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, adjacency=adj)
+    check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), dtype, "csr")
+    # caller-given passage keys replace the pooled keys
+    keys = torch.randn(int(batch.query_passages[-1]), H * d_h, generator=torch.Generator().manual_seed(3))
+    O2, L2, rp2, col2 = B.bipartite_xattn(db, Qh.cuda(), passage_keys=keys.cuda())
+    _, adj2, O2_ref, L2_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, passage_key_table=keys.double())
+    check_graph(batch, rp2, col2, adj2)
+    check_attention(f64(O2), f64(L2), np.concatenate(O2_ref), np.concatenate(L2_ref), dtype, "keys")
+
+
+# --------------------------------------------------------------------------- fused
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seed", wls.SEEDS)
+def test_fused_small_ragged(B, dtype, seed):
+    batch = small_batch(dtype, seed, H=4, d_h=64, with_bias=True)
+    say(f"fused small {dtype} seed={seed}")
+    db = B.to_device(batch)
+    idx, O, L = B.route_fused(db)
+    torch.cuda.synchronize()
+    ref = oracle_route(batch)
+    idx = idx.cpu().numpy()
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist()
+    check_attention(f64(O), f64(L), np.concatenate(ref.O), np.concatenate(ref.LSE), dtype)
+
+
+@pytest.mark.parametrize("name", wls.ORDER)
+def test_named_full_size_staged_and_fused(B, name):
+    """Full-size workloads in the launch configuration the benchmark times:
+    exact kept sets and edge sets for every question, attention on sampled
+    rows, and the fused route bitwise equal to the staged calls."""
+    batch = wls.make_batch(name, 2026, threads=16)
+    say(f"full {name}: B={batch.B} N={batch.wl.N} d={batch.wl.d}")
+    db = B.to_device(batch)
+    idx, _, Vk = B.prune_topk(db, want_scores=False)
+    Qh = Vk.view(-1, batch.Kh.shape[1], batch.Kh.shape[2])
+    O, L, rp, col = B.bipartite_xattn(db, Qh)
+    fidx, fO, fL = B.route_fused(db)
+    _, O32, _ = B.route_fused(B.with_f32_output(db))
+    torch.cuda.synchronize()
+    assert torch.equal(idx, fidx)
+    assert torch.equal(O, fO) and torch.equal(L, fL), "fused != staged"
+    per_q = 24 if batch.B <= 16 else 4
+    rows = sample_rows(batch, per_q)
+    ref = oracle_route(batch, attn_rows=rows)
+    idx = idx.cpu().numpy()
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist(), f"{name} q{b} kept set"
+    check_graph(batch, rp, col, ref.adj)
+    Of, Lf, O32f = f64(O), f64(L), f64(O32)
+    got_O, got_O32, got_L, want_O, want_L = [], [], [], [], []
+    for b, rs in rows.items():
+        k0 = int(batch.kept_offsets[b])
+        for r in rs:
+            got_O.append(Of[k0 + r]); got_O32.append(O32f[k0 + r]); got_L.append(Lf[k0 + r])
+            want_O.append(ref.O[b][r]); want_L.append(ref.LSE[b][r])
+    want_O, want_L = np.stack(want_O), np.stack(want_L)
+    check_attention(np.stack(got_O), np.stack(got_L), want_O, want_L, batch.wl.dtype, name)
+    check_attention(np.stack(got_O32), np.stack(got_L), want_O, want_L, batch.wl.dtype,
+                    name + " f32-out", stored_bf16=False)
+
+
+def test_fused_deterministic_and_stream(B):
+    batch = wls.make_batch("llava_bf16", 42)
+    db = B.to_device(batch)
+    a = [t.clone() for t in B.route_fused(db)]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        b = [t.clone() for t in B.route_fused(db)]
+    s.synchronize()
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_degenerate_shapes(B):
+    # every question: one question token; passages of one token; k = N; P = 0
+    batch = wls.make_batch("llava_bf16", 137, B=4, N=64, H=4, d_h=64, T=1, k=(0, 64),
+                           P=(0, 1, 2), L_p=1)
+    say(f"degenerate k={batch.k.tolist()} P={batch.P.tolist()}")
+    db = B.to_device(batch)
+    idx, O, L = B.route_fused(db)
+    torch.cuda.synchronize()
+    ref = oracle_route(batch)
+    idx = idx.cpu().numpy()
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist()
+    check_attention(f64(O), f64(L), np.concatenate(ref.O), np.concatenate(ref.LSE), "bf16")
