@@ -35,9 +35,13 @@ namespace skip {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kAttnRows = 128;   // kept rows per work item
-constexpr int kTile = 64;        // tokens per K/V tile
+constexpr int kWaves = 8;                 // waves per work item
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxRows = 32 * kWaves;     // kept rows per work item
+constexpr int kTile = 64;                 // tokens per K/V tile
+constexpr int kStages = 4;                // K/V tiles resident in LDS
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -46,22 +50,59 @@ __device__ __forceinline__ f32x16_t mfma32(const u32x4& a, const u32x4& b, f32x1
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair, round-to-nearest-even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+  bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
-// Position of token w (0..63) of a tile inside its 16-token block of the
-// transposed V tile: the S^T accumulator gives lane half hh, element e the
-// token 8*(e/4) + 4*hh + e%4 of the block, and that pair is stored at 8*hh + e.
-__device__ __forceinline__ int vt_pos(int w) {
-  const int blk = w >> 4, ww = w & 15;
-  const int hh = (ww >> 2) & 1;
-  const int e = 4 * (ww >> 3) + (ww & 3);
-  return 16 * blk + 8 * hh + e;
+// Wait until at most N of this wave's vector-memory operations are pending
+// (expcnt and lgkmcnt left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// Workgroup barrier without a memory fence: LDS in the loop is written only
+// by direct global->LDS loads, whose completion is awaited explicitly.
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// A wave-uniform 64-bit value moved to scalar registers.
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Transposing LDS read: in each group of 16 lanes, lane j receives element
+// j & 3 of the 8-byte pieces addressed by lanes (j >> 2) + 4e, e = 0..3.
+__device__ __forceinline__ uint2 ds_read_tr16(const bf16_t* p) {
+  s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4_t*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// bf16 path.  Work item = (question b, head h, block of <= 256 kept rows);
+// eight waves, 32 rows each.  K and V tiles of 64 tokens of head h stream
+// through a 4-stage LDS ring filled by direct global->LDS loads (16 bytes a
+// lane), three tiles ahead of the tile being consumed, one barrier per tile.
+// Tiles are stored in natural token-major layout with 16-byte chunks XOR-
+// swizzled by row (conflict-free MFMA operand reads).  Per wave and tile:
+//   S^T (64 tokens x 32 rows) = K_tile . Q^T     (A: K rows, 16-byte LDS reads)
+//   mask rows without an edge to the passage and tokens past its end, online
+//   softmax in fp32 (base-2), P rounded to bf16,
+//   O^T (d_h x 32 rows) += V_tile^T . P^T        (A: V^T via transposing LDS reads)
+// The S^T accumulator layout gives lane half hh, element e of a 16-token
+// block the token 8*(e/4) + 4*hh + e%4; the V^T operand is read in that same
+// token order, so P^T needs no data movement.
 template <int D>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(kThreads)
 attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
                  int N, int qstride, const int32_t* __restrict__ kept_offsets,
                  const bf16_t* __restrict__ Kh, const bf16_t* __restrict__ Vh,
@@ -71,16 +112,19 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
                  int total_passages, int total_tokens, int k_max, int P_max, int RB,
                  int n_items, float scale_log2, void* __restrict__ O, int o_f32,
                  float* __restrict__ lse) {
-  constexpr int KS = D + 8;              // K tile row stride (elements)
-  constexpr int VS = kTile + 8;          // V^T tile row stride (elements)
-  constexpr int KB = D / 16;             // k-blocks of the QK^T product
-  constexpr int DT = D / 32;             // 32-wide feature tiles of O
-  constexpr int CH = kTile * D / 8;      // 16-byte chunks per tile
-  constexpr int CPT = CH / 256;          // chunks per thread
-  static_assert(CH % 256 == 0, "tile chunks must divide over the workgroup");
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[kTile * KS];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[D * VS];
-  __shared__ uint64_t wave_union[4];
+  constexpr int NCH = D / 8;               // 16-byte chunks per token row
+  constexpr int KB = D / 16;               // k-blocks of QK^T
+  constexpr int DT = D / 32;               // 32-wide feature tiles of O
+  constexpr int TILE = kTile * D;          // elements per K (or V) tile
+  constexpr int LPT = 2 * NCH / kWaves;    // direct loads per lane per tile
+  // V chunk swizzle: depends on row % 4 only; keeps the transposing reads of
+  // four consecutive tokens on distinct banks.
+  auto vswz = [](int row) { return (NCH >= 16 ? 4 : 2) * (row & 3); };
+  static_assert(NCH % kWaves == 0, "tile loads must divide over the waves");
+  __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kStages * TILE];
+  __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kStages * TILE];
+  __shared__ uint64_t wave_union[kWaves];
+  __shared__ int p_ts[64], p_te[64];
 
   // XCD-aware decode: consecutive items on one XCD share (b, h).
   const int per_xcd = gridDim.x / 8;
@@ -95,8 +139,11 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   range_of(query_passages, b, total_passages, p0, p1);
   const int kq = min(k1 - k0, k_max);
   const int P = min(min(p1 - p0, P_max), 64);
-  const int row0 = rb * kAttnRows;
-  if (row0 >= kq) return;
+  const int nblk = (kq + kMaxRows - 1) / kMaxRows;
+  if (rb >= nblk) return;
+  const int rpb = ((kq + nblk - 1) / nblk + 31) / 32 * 32;   // rows per block
+  const int row0 = rb * rpb;
+  const int row_end = min(kq, row0 + rpb);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -104,8 +151,14 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   const int col = lane & 31;         // query row within the wave
   const int hh = lane >> 5;          // half wave
   const int r = row0 + wave * 32 + col;
-  const bool row_ok = r < kq;
+  const bool row_ok = r < row_end;
 
+  if (tid < P) {
+    int ts, te;
+    range_of(passage_offsets, p0 + tid, total_tokens, ts, te);
+    p_ts[tid] = ts;
+    p_te[tid] = te;
+  }
   uint64_t mrow = row_ok ? rowmask[k0 + r] : 0ull;
   if (P < 64) mrow &= (1ull << P) - 1ull;
   uint64_t wmask = mrow;
@@ -131,7 +184,58 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
                       : u32x4{0u, 0u, 0u, 0u};
   }
   __syncthreads();
-  const uint64_t U = wave_union[0] | wave_union[1] | wave_union[2] | wave_union[3];
+  uint64_t U = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) U |= wave_union[w];
+  U = uniform64(U);
+  wmask = uniform64(wmask);
+
+  // Tile cursors over (adjacent passage, 64-token block): one for issuing
+  // loads, one for computing.
+  struct Cursor {
+    uint64_t rem;
+    int j, t, te;
+  };
+  auto advance = [&](Cursor& c) -> bool {
+    if (c.j >= 0 && c.t + kTile < c.te) {
+      c.t += kTile;
+      return true;
+    }
+    while (c.rem) {
+      const int j = __builtin_ctzll(c.rem);
+      c.rem &= c.rem - 1ull;
+      const int ts = __builtin_amdgcn_readfirstlane(p_ts[j]);
+      const int te = __builtin_amdgcn_readfirstlane(p_te[j]);
+      if (te > ts) {
+        c.j = j; c.t = ts; c.te = te;
+        return true;
+      }
+    }
+    return false;
+  };
+  // Direct loads of one tile: instruction q fills LDS bytes [q*1024, +1024)
+  // of the stage; lane l's 16 bytes are slot o = q*64 + l = (row, physical
+  // chunk p).  K holds logical chunk p ^ (row % NCH) there, V holds logical
+  // chunk p ^ vswz(row) (a key of row % 4 only, so the transposing reads of
+  // tokens t, t+8, t+16, t+32 differ by constant offsets).  Rows past the
+  // passage end re-read its last token (finite values, masked in the
+  // softmax).
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  auto issue = [&](int stage, int t, int te) {
+    bf16_t* Ks = Kbuf + stage * TILE;
+    bf16_t* Vs = Vbuf + stage * TILE;
+#pragma unroll
+    for (int q = wave_s; q < NCH; q += kWaves) {
+      const int o = q * 64 + lane;
+      const int row = o / NCH, pch = o % NCH;
+      const int ck = pch ^ (row & (NCH - 1));
+      const int cv = pch ^ vswz(row);
+      const int tok = min(t + row, te - 1);
+      const size_t rowoff = ((size_t)tok * H + h) * D;
+      __builtin_amdgcn_global_load_lds(Kh + rowoff + ck * 8, Ks + q * 512, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(Vh + rowoff + cv * 8, Vs + q * 512, 16, 0, 0);
+    }
+  };
 
   f32x16_t acc[DT];
 #pragma unroll
@@ -140,130 +244,117 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Tile walk over (adjacent passage, 64-token block).
-  uint64_t urem = U;
-  int cur_j = -1, cur_t = 0, cur_end = 0;
-  auto advance = [&]() -> bool {
-    if (cur_j >= 0 && cur_t + kTile < cur_end) {
-      cur_t += kTile;
-      return true;
-    }
-    while (urem) {
-      const int j = __builtin_ctzll(urem);
-      urem &= urem - 1ull;
-      int ts, te;
-      range_of(passage_offsets, p0 + j, total_tokens, ts, te);
-      if (te > ts) {
-        cur_j = j; cur_t = ts; cur_end = te;
-        return true;
-      }
-    }
-    return false;
-  };
+  // per-lane constants of the MFMA operand reads: K rows st*32 + col share
+  // the swizzle key col % NCH; V^T reads follow the transposing-read layout
+  const int g16 = lane >> 4, s16 = lane & 15;
+  int koff[KB];                                       // K row col, chunk 2kb+hh
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+    koff[kb] = col * D + (((2 * kb + hh) ^ (col & (NCH - 1))) << 3);
+  // V^T operand: token 4*hh + (s16 >> 2) (+ 16 per k-block, + 8 for the upper
+  // half), feature 32*dt + 16*(g16 & 1) + 4*(s16 & 3)
+  const int tr_tok = 4 * hh + (s16 >> 2);
+  int voff[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    const int d = 32 * dt + 16 * (g16 & 1) + 4 * (s16 & 3);
+    voff[dt] = tr_tok * D + (((d >> 3) ^ vswz(tr_tok)) << 3) + (d & 7);
+  }
 
-  u32x4 kreg[CPT], vreg[CPT];
-  auto load_tile = [&](int t_base, int t_end) {
+  Cursor ci{U, -1, 0, 0}, cc{U, -1, 0, 0};
+  int issued = 0;
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int ch = tid + 256 * c;
-      const int tok = ch / (D / 8), c8 = ch % (D / 8);
-      const int t = t_base + tok;
-      if (t < t_end) {
-        const size_t off = ((size_t)t * H + h) * D + c8 * 8;
-        kreg[c] = *reinterpret_cast<const u32x4*>(Kh + off);
-        vreg[c] = *reinterpret_cast<const u32x4*>(Vh + off);
-      } else {
-        kreg[c] = u32x4{0u, 0u, 0u, 0u};
-        vreg[c] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int ch = tid + 256 * c;
-      const int tok = ch / (D / 8), c8 = ch % (D / 8);
-      *reinterpret_cast<u32x4*>(&Ks[tok * KS + c8 * 8]) = kreg[c];
-      const int pos = vt_pos(tok);
-      const uint32_t w4[4] = {vreg[c].x, vreg[c].y, vreg[c].z, vreg[c].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Vt[(c8 * 8 + 2 * e) * VS + pos] = (bf16_t)(w4[e] & 0xffffu);
-        Vt[(c8 * 8 + 2 * e + 1) * VS + pos] = (bf16_t)(w4[e] >> 16);
-      }
-    }
-  };
+  for (int s = 0; s < kStages - 1; ++s)
+    if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
 
-  bool have = advance();
-  if (have) load_tile(cur_t, cur_end);
-  while (have) {
-    const int j = cur_j, t_base = cur_t, t_end = cur_end;
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    have = advance();
-    if (have) load_tile(cur_t, cur_end);
+  for (int i = 0; advance(cc); ++i) {
+    const int ahead = issued - i - 1;
+    if (ahead >= 2) wait_vmem<2 * LPT>();
+    else if (ahead == 1) wait_vmem<LPT>();
+    else wait_vmem<0>();
+    barrier_nofence();
+    if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
 
-    if ((wmask >> j) & 1ull) {
-      const bool adj = (mrow >> j) & 1ull;
-      f32x16_t s[2];
+    const int j = cc.j;
+    if (!((wmask >> j) & 1ull)) continue;
+    const bf16_t* Ks = Kbuf + (i % kStages) * TILE;
+    const bf16_t* Vs = Vbuf + (i % kStages) * TILE;
+    const int t_base = cc.t, t_end = cc.te;
+    const bool adj = (mrow >> j) & 1ull;
+
+    // two sub-steps of 32 tokens, each a complete online-softmax update
+    const bool full = t_base + kTile <= t_end;
+    const float mbias = adj ? 0.f : -INFINITY;
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
+    for (int st = 0; st < 2; ++st) {
+      // S^T = K . Q^T for 32 tokens
+      u32x4 ka[KB];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[st][v] = 0.f;
+      for (int kb = 0; kb < KB; ++kb)
+        ka[kb] = *reinterpret_cast<const u32x4*>(Ks + st * 32 * D + koff[kb]);
+      f32x16_t sacc;
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          const u32x4 a =
-              *reinterpret_cast<const u32x4*>(&Ks[(st * 32 + col) * KS + kb * 16 + 8 * hh]);
-          s[st] = mfma32(a, qf[kb], s[st]);
-        }
-      }
-      // mask + scale, tile max
-      float mt = -INFINITY;
+      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
+      for (int kb = 0; kb < KB; ++kb) sacc = mfma32(ka[kb], qf[kb], sacc);
+      __builtin_amdgcn_sched_barrier(0);
+
+      // V^T operands of the two 16-token k-blocks, read while the softmax runs
+      u32x4 va[DT][2];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int tok = t_base + st * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          const float x = (adj && tok < t_end) ? s[st][v] * scale_log2 : -INFINITY;
-          s[st][v] = x;
-          mt = fmaxf(mt, x);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      float ls = 0.f;
-      u32x4 pb[4];
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        float pv[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float x = s[st][v];
-          pv[v] = (x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x - m_new);
-          ls += pv[v];
-        }
+      for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
-          pb[2 * st + g] = u32x4{pack2_bf16(pv[8 * g + 0], pv[8 * g + 1]),
-                                 pack2_bf16(pv[8 * g + 2], pv[8 * g + 3]),
-                                 pack2_bf16(pv[8 * g + 4], pv[8 * g + 5]),
-                                 pack2_bf16(pv[8 * g + 6], pv[8 * g + 7])};
+          const bf16_t* vp = Vs + (32 * st + 16 * g) * D + voff[dt];
+          const uint2 lo = ds_read_tr16(vp);
+          const uint2 hi = ds_read_tr16(vp + 8 * D);
+          va[dt][g] = u32x4{lo.x, lo.y, hi.x, hi.y};
         }
+
+      // scale + adjacency mask in one fma; token bound only on a partial tile
+      float mt = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float x = fmaf(sacc[v], scale_log2, mbias);
+        if (!full) {
+          const int tok = t_base + st * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
+          x = (tok < t_end) ? x : -INFINITY;
+        }
+        sacc[v] = x;
+        mt = fmaxf(mt, x);
+      }
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float m_new = fmaxf(m_run, mt);
+      const float mref = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mref);
+      float ls = 0.f;
+      u32x4 pb[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        float pv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pv[e] = __builtin_amdgcn_exp2f(sacc[8 * g + e] - mref);
+          ls += pv[e];
+        }
+        pb[g] = u32x4{pack2_bf16(pv[0], pv[1]), pack2_bf16(pv[2], pv[3]),
+                      pack2_bf16(pv[4], pv[5]), pack2_bf16(pv[6], pv[7])};
       }
       l_run = l_run * alpha + ls;
       m_run = m_new;
+      if (__any(alpha != 1.f)) {
 #pragma unroll
-      for (int t = 0; t < DT; ++t) {
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[t][v] *= alpha;
-#pragma unroll
-        for (int kb2 = 0; kb2 < 4; ++kb2) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(
-              &Vt[(t * 32 + col) * VS + 16 * kb2 + 8 * hh]);
-          acc[t] = mfma32(a, pb[kb2], acc[t]);
-        }
+          for (int v = 0; v < 16; ++v) acc[dt][v] *= alpha;
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        acc[dt] = mfma32(va[dt][0], pb[0], acc[dt]);
+        acc[dt] = mfma32(va[dt][1], pb[1], acc[dt]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -392,12 +483,12 @@ hipError_t launch_attention(const skip_problem_t& p, QuerySource q,
   if (p.k_max <= 0) return hipSuccess;
   const int qstride = p.d;
   if (p.dtype == SKIP_BF16) {
-    const int RB = (p.k_max + kAttnRows - 1) / kAttnRows;
+    const int RB = (p.k_max + kMaxRows - 1) / kMaxRows;
     const int n_items = p.B * p.H * RB;
     const int grid = ((n_items + 7) / 8) * 8;
     const float sl2 = p.sm_scale * kLog2e;
 #define SKIP_ATTN_BF16(DD)                                                                   \
-  hipLaunchKernelGGL(attn_bf16_kernel<DD>, dim3(grid), dim3(256), 0, s,                      \
+  hipLaunchKernelGGL(attn_bf16_kernel<DD>, dim3(grid), dim3(kThreads), 0, s,                 \
                      (const bf16_t*)q.base, q.kept_idx, q.N, qstride, kept_offsets,          \
                      (const bf16_t*)Kh, (const bf16_t*)Vh, passage_offsets, query_passages,  \
                      rowmask, p.H, p.total_kept, p.total_passages, p.total_tokens, p.k_max,  \

@@ -3,8 +3,10 @@
 //
 //   passage_keys : kbar_j = mean over the tokens of passage j of Kh[m] (all
 //                  heads flattened), float64 sums
-//   edge_cos     : c_ij = <q_i, kbar_j> / (|q_i| |kbar_j|), float64, 0 when a
-//                  norm is 0
+//   edge_dot     : float64 partial sums of <q_i, kbar_j>, |q_i|^2, |kbar_j|^2
+//                  over slices of d
+//   (cosine)       c_ij = <q_i, kbar_j> / (|q_i| |kbar_j|), 0 when a norm is 0,
+//                  formed from the partial sums by the selection kernel
 //   edge_select  : per question, the E_b = min(ceil(avg_degree * k_b),
 //                  k_b * P_b) largest cosines (lower flattened index i*P_b+j
 //                  on ties) -> one 64-bit neighbour mask per kept row, and
@@ -107,122 +109,127 @@ passage_keys_kernel(const T* __restrict__ Kh, const int32_t* __restrict__ passag
 }
 
 // ---------------------------------------------------------------------------
-// Edge cosines.  Workgroup = kEdgeRows kept rows of one question against all
-// of its passages.  Columns are processed in chunks of kEdgeCW: the rows'
-// chunk (transposed, float) and the passage keys' chunk (float64) are staged
-// in LDS; thread t accumulates the float64 dot products of the (row, passage)
-// pairs t, t+256, ...
-constexpr int kEdgeRows = 16;
-constexpr int kEdgeCW = 64;
-constexpr int kEdgeMaxPairs = (kEdgeRows * 64 + 255) / 256;
+// Edge dot products, split over d.  Workgroup = (512-column slice, 32 kept
+// rows, question).  Per 256-column chunk, the rows (transposed, float) and 16
+// passage keys at a time (float64) are staged in LDS; thread (i = t%32,
+// g = t/32) accumulates rows i against passages g and g+8 of each group of
+// 16.  Partial dot products and squared norms are written per slice and
+// summed in slice order by the selection kernel (deterministic).
+constexpr int kEdRows = 32;
+constexpr int kEdSlice = 512;
+constexpr int kEdChunk = 256;
+constexpr int kEdPG = 16;
+constexpr int kEdMaxGroups = 64 / kEdPG;
 
 template <typename T>
 __global__ void __launch_bounds__(256)
-edge_cos_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
-                int N, const int32_t* __restrict__ kept_offsets,
-                const int32_t* __restrict__ query_passages,
-                const double* __restrict__ kbar, const float* __restrict__ pkeys,
-                int d, int total_kept, int total_passages, int k_max, int P_max,
-                double* __restrict__ cosv) {
-  extern __shared__ double sm[];
-  double* kb = sm;                                       // [P][kEdgeCW]
-  float* qT = reinterpret_cast<float*>(sm + (size_t)P_max * kEdgeCW);  // [kEdgeCW][kEdgeRows]
-  __shared__ double nq2[kEdgeRows];
-  __shared__ double nk2[64];
+edge_dot_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_idx, int N,
+                const int32_t* __restrict__ kept_offsets,
+                const int32_t* __restrict__ query_passages, const double* __restrict__ kbar,
+                const float* __restrict__ pkeys, int d, int total_kept, int total_passages,
+                int k_max, int P_max, int S, double* __restrict__ part,
+                double* __restrict__ qn2p, double* __restrict__ kn2p) {
+  constexpr int VEC = GVec<T>::n;
+  __shared__ float qT[kEdChunk][kEdRows + 1];
+  __shared__ __attribute__((aligned(16))) double kb[kEdPG][kEdChunk];
+  __shared__ const T* rowp[kEdRows];
 
-  const int b = blockIdx.y;
+  const int s = blockIdx.x, b = blockIdx.z;
   int k0, k1, p0, p1;
   range_of(kept_offsets, b, total_kept, k0, k1);
   range_of(query_passages, b, total_passages, p0, p1);
-  const int kb_ = min(k1 - k0, k_max);
+  const int kq = min(k1 - k0, k_max);
   const int P = min(min(p1 - p0, P_max), 64);
-  const int i0 = blockIdx.x * kEdgeRows;
-  if (i0 >= kb_ || P <= 0) return;
-  const int nrows = min(kEdgeRows, kb_ - i0);
+  const int i0 = blockIdx.y * kEdRows;
+  if (i0 >= kq || P <= 0) return;
+  const int nrows = min(kEdRows, kq - i0);
+  const int c_begin = s * kEdSlice;
+  const int c_end = min(d, c_begin + kEdSlice);
+  const int tid = threadIdx.x;
+  const int i = tid % kEdRows, g = tid / kEdRows;
+  const int ngroups = (P + kEdPG - 1) / kEdPG;
 
-  // Source row of each kept row of this block.
-  __shared__ const T* rowp[kEdgeRows];
-  if (threadIdx.x < kEdgeRows) {
-    const int i = i0 + threadIdx.x;
+  if (tid < kEdRows) {
     const T* ptr = nullptr;
-    if (threadIdx.x < nrows) {
+    if (tid < nrows) {
       if (kept_idx) {
-        const int src = clampi(kept_idx[k0 + i], 0, N - 1);
+        const int src = clampi(kept_idx[k0 + i0 + tid], 0, N - 1);
         ptr = qbase + ((size_t)b * N + src) * d;
       } else {
-        ptr = qbase + (size_t)(k0 + i) * d;
+        ptr = qbase + (size_t)(k0 + i0 + tid) * d;
       }
     }
-    rowp[threadIdx.x] = ptr;
+    rowp[tid] = ptr;
   }
   __syncthreads();
 
-  double acc[kEdgeMaxPairs];
+  double acc[2 * kEdMaxGroups];
 #pragma unroll
-  for (int q = 0; q < kEdgeMaxPairs; ++q) acc[q] = 0.0;
-  double qq = 0.0, kk = 0.0;
-  const int npairs = kEdgeRows * P;
+  for (int q = 0; q < 2 * kEdMaxGroups; ++q) acc[q] = 0.0;
+  double qq = 0.0;
+  double kk[kEdMaxGroups];
+#pragma unroll
+  for (int q = 0; q < kEdMaxGroups; ++q) kk[q] = 0.0;
 
-  for (int cc = 0; cc < d; cc += kEdgeCW) {
-    const int cw = min(kEdgeCW, d - cc);
-    // stage the rows' chunk, transposed
-    for (int e = threadIdx.x; e < kEdgeRows * kEdgeCW; e += blockDim.x) {
-      const int r = e / kEdgeCW, c = e % kEdgeCW;
-      float v = 0.f;
-      if (r < nrows && c < cw) v = elem_f32(rowp[r], (size_t)(cc + c));
-      qT[c * kEdgeRows + r] = v;
-    }
-    // stage the passage keys' chunk
-    for (int e = threadIdx.x; e < P * kEdgeCW; e += blockDim.x) {
-      const int j = e / kEdgeCW, c = e % kEdgeCW;
-      double v = 0.0;
-      if (c < cw) {
-        const size_t off = (size_t)(p0 + j) * d + cc + c;
-        v = pkeys ? (double)pkeys[off] : kbar[off];
-      }
-      kb[j * kEdgeCW + c] = v;
+  for (int cc = c_begin; cc < c_end; cc += kEdChunk) {
+    const int cw = min(kEdChunk, c_end - cc);
+    // rows, transposed: 32 rows x cw columns in 16-byte pieces
+    for (int ch = tid; ch < kEdRows * (kEdChunk / VEC); ch += 256) {
+      const int r = ch / (kEdChunk / VEC), cv = (ch % (kEdChunk / VEC)) * VEC;
+      u32x4 x = u32x4{0u, 0u, 0u, 0u};
+      if (r < nrows && cv < cw) x = *reinterpret_cast<const u32x4*>(rowp[r] + cc + cv);
+      double v[VEC];
+      unpack_f64<T>(x, v);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) qT[cv + e][r] = (float)v[e];
     }
     __syncthreads();
-#pragma unroll
-    for (int q = 0; q < kEdgeMaxPairs; ++q) {
-      const int pr = threadIdx.x + q * 256;
-      if (pr < npairs) {
-        const int i = pr % kEdgeRows, j = pr / kEdgeRows;
-        double s = acc[q];
-        for (int c = 0; c < cw; ++c)
-          s = fma((double)qT[c * kEdgeRows + i], kb[j * kEdgeCW + c], s);
-        acc[q] = s;
-      }
-    }
-    if (threadIdx.x < kEdgeRows) {
+    if (tid < kEdRows)
       for (int c = 0; c < cw; ++c) {
-        const double v = (double)qT[c * kEdgeRows + threadIdx.x];
+        const double v = (double)qT[c][tid];
         qq = fma(v, v, qq);
       }
-    } else if (threadIdx.x >= 64 && threadIdx.x < 64 + P) {
-      const int j = threadIdx.x - 64;
+    for (int pg = 0; pg < ngroups; ++pg) {
+      const int jn = min(kEdPG, P - pg * kEdPG);
+      for (int e = tid; e < kEdPG * kEdChunk; e += 256) {
+        const int jj = e / kEdChunk, c = e % kEdChunk;
+        double v = 0.0;
+        if (jj < jn && c < cw) {
+          const size_t off = (size_t)(p0 + pg * kEdPG + jj) * d + cc + c;
+          v = pkeys ? (double)pkeys[off] : kbar[off];
+        }
+        kb[jj][c] = v;
+      }
+      __syncthreads();
+      double a0 = acc[2 * pg], a1 = acc[2 * pg + 1];
       for (int c = 0; c < cw; ++c) {
-        const double v = kb[j * kEdgeCW + c];
-        kk = fma(v, v, kk);
+        const double qv = (double)qT[c][i];
+        a0 = fma(qv, kb[g][c], a0);
+        a1 = fma(qv, kb[g + 8][c], a1);
       }
+      acc[2 * pg] = a0;
+      acc[2 * pg + 1] = a1;
+      if (blockIdx.y == 0 && tid < kEdPG)
+        for (int c = 0; c < cw; ++c) kk[pg] = fma(kb[tid][c], kb[tid][c], kk[pg]);
+      __syncthreads();
     }
-    __syncthreads();
   }
-  if (threadIdx.x < kEdgeRows) nq2[threadIdx.x] = qq;
-  else if (threadIdx.x >= 64 && threadIdx.x < 64 + P) nk2[threadIdx.x - 64] = kk;
-  __syncthreads();
+  const size_t base = (size_t)b * S + s;
+  if (i < nrows) {
+    for (int pg = 0; pg < ngroups; ++pg) {
 #pragma unroll
-  for (int q = 0; q < kEdgeMaxPairs; ++q) {
-    const int pr = threadIdx.x + q * 256;
-    if (pr < npairs) {
-      const int i = pr % kEdgeRows, j = pr / kEdgeRows;
-      if (i < nrows) {
-        const double nq = sqrt(nq2[i]), nk = sqrt(nk2[j]);
-        const double c = (nq > 0.0 && nk > 0.0) ? acc[q] / (nq * nk) : 0.0;
-        cosv[(size_t)b * k_max * P_max + (size_t)(i0 + i) * P + j] = c;
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int j = pg * kEdPG + g + 8 * h2;
+        if (j < P) part[(base * k_max + i0 + i) * P_max + j] = acc[2 * pg + h2];
       }
     }
+    if (tid < kEdRows) qn2p[base * k_max + i0 + i] = qq;
   }
+  if (blockIdx.y == 0 && tid < kEdPG)
+    for (int pg = 0; pg < ngroups; ++pg) {
+      const int j = pg * kEdPG + tid;
+      if (j < P) kn2p[base * P_max + j] = kk[pg];
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -231,7 +238,9 @@ constexpr int kGSelThreads = 1024;
 constexpr int kGSelMaxPT = 16;     // k_b * P_b <= 16384
 
 __global__ void __launch_bounds__(kGSelThreads)
-edge_select_kernel(const double* __restrict__ cosv, const int32_t* __restrict__ kept_offsets,
+edge_select_kernel(const double* __restrict__ part, const double* __restrict__ qn2p,
+                   const double* __restrict__ kn2p, int S,
+                   const int32_t* __restrict__ kept_offsets,
                    const int32_t* __restrict__ query_passages, int B, int total_kept,
                    int total_passages, int k_max, int P_max, double avg_degree,
                    uint64_t* __restrict__ rowmask, int32_t* __restrict__ rowptr_out,
@@ -252,10 +261,24 @@ edge_select_kernel(const double* __restrict__ cosv, const int32_t* __restrict__ 
   const int C = (n + blockDim.x - 1) / blockDim.x;
   const int e0 = threadIdx.x * C;
   const int cnt = max(0, min(C, n - e0));
-  const double* cb = cosv + (size_t)b * k_max * P_max;
+  // cos(q_i, kbar_j) from the per-slice partial sums, in slice order
   uint64_t keys[kGSelMaxPT];
 #pragma unroll
-  for (int j = 0; j < kGSelMaxPT; ++j) keys[j] = (j < cnt) ? order_key(cb[e0 + j]) : 0ull;
+  for (int jj = 0; jj < kGSelMaxPT; ++jj) {
+    keys[jj] = 0ull;
+    if (jj < cnt) {
+      const int f = e0 + jj, i = f / P, j = f % P;
+      double dot = 0.0, q2 = 0.0, k2 = 0.0;
+      for (int sl = 0; sl < S; ++sl) {
+        const size_t base = (size_t)b * S + sl;
+        dot += part[(base * k_max + i) * P_max + j];
+        q2 += qn2p[base * k_max + i];
+        k2 += kn2p[base * P_max + j];
+      }
+      const double nq = sqrt(q2), nk = sqrt(k2);
+      keys[jj] = order_key((nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0);
+    }
+  }
   const uint32_t flags = block_select_top<kGSelMaxPT>(keys, cnt, n, E, &sh);
 
 #pragma unroll
@@ -345,33 +368,34 @@ hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
   return hipGetLastError();
 }
 
-hipError_t launch_edge_cos(const skip_problem_t& p, QuerySource q,
+int edge_slices(const skip_problem_t& p) { return (p.d + kEdSlice - 1) / kEdSlice; }
+
+hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
                            const int32_t* kept_offsets, const int32_t* query_passages,
-                           const double* kbar, const float* passage_keys, double* cosv,
+                           const double* kbar, const float* passage_keys, EdgePartials ep,
                            hipStream_t s) {
   if (p.k_max <= 0 || p.P_max <= 0) return hipSuccess;
-  dim3 grid((p.k_max + kEdgeRows - 1) / kEdgeRows, p.B);
-  const size_t lds = (size_t)p.P_max * kEdgeCW * sizeof(double) +
-                     (size_t)kEdgeCW * kEdgeRows * sizeof(float);
+  const int S = edge_slices(p);
+  dim3 grid(S, (p.k_max + kEdRows - 1) / kEdRows, p.B);
   if (p.dtype == SKIP_F32)
-    hipLaunchKernelGGL(edge_cos_kernel<float>, grid, dim3(256), lds, s,
+    hipLaunchKernelGGL(edge_dot_kernel<float>, grid, dim3(256), 0, s,
                        (const float*)q.base, q.kept_idx, q.N, kept_offsets, query_passages,
                        kbar, passage_keys, p.d, p.total_kept, p.total_passages, p.k_max,
-                       p.P_max, cosv);
+                       p.P_max, S, ep.part, ep.qn2, ep.kn2);
   else
-    hipLaunchKernelGGL(edge_cos_kernel<bf16_t>, grid, dim3(256), lds, s,
+    hipLaunchKernelGGL(edge_dot_kernel<bf16_t>, grid, dim3(256), 0, s,
                        (const bf16_t*)q.base, q.kept_idx, q.N, kept_offsets,
                        query_passages, kbar, passage_keys, p.d, p.total_kept,
-                       p.total_passages, p.k_max, p.P_max, cosv);
+                       p.total_passages, p.k_max, p.P_max, S, ep.part, ep.qn2, ep.kn2);
   return hipGetLastError();
 }
 
-hipError_t launch_edge_select(const skip_problem_t& p, const double* cosv,
+hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
                               const int32_t* kept_offsets, const int32_t* query_passages,
                               uint64_t* rowmask, int32_t* rowptr_out, int32_t* col_out,
                               hipStream_t s) {
-  hipLaunchKernelGGL(edge_select_kernel, dim3(p.B), dim3(kGSelThreads), 0, s, cosv,
-                     kept_offsets, query_passages, p.B, p.total_kept, p.total_passages,
+  hipLaunchKernelGGL(edge_select_kernel, dim3(p.B), dim3(kGSelThreads), 0, s, ep.part,
+                     ep.qn2, ep.kn2, edge_slices(p), kept_offsets, query_passages, p.B, p.total_kept, p.total_passages,
                      p.k_max, p.P_max, p.avg_degree, rowmask, rowptr_out, col_out);
   return hipGetLastError();
 }

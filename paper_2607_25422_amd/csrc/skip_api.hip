@@ -61,7 +61,10 @@ size_t workspace_size(const skip_problem_t& p) {
   n += align_up((size_t)p.B * p.d * sizeof(double));                  // u
   n += align_up((size_t)p.B * (size_t)p.N * sizeof(double));          // z
   n += align_up((size_t)p.total_passages * p.d * sizeof(double));     // kbar
-  n += align_up((size_t)p.B * p.k_max * p.P_max * sizeof(double));    // cos
+  const size_t S = (size_t)edge_slices(p);
+  n += align_up((size_t)p.B * S * p.k_max * p.P_max * sizeof(double));  // edge partials
+  n += align_up((size_t)p.B * S * p.k_max * sizeof(double));            // row norms
+  n += align_up((size_t)p.B * S * p.P_max * sizeof(double));            // key norms
   n += align_up((size_t)p.total_kept * sizeof(uint64_t));             // rowmask
   return n;
 }
@@ -86,7 +89,10 @@ Workspace carve_workspace(const skip_problem_t& p, void* base) {
   w.u = reinterpret_cast<double*>(take((size_t)p.B * p.d * sizeof(double)));
   w.z = reinterpret_cast<double*>(take((size_t)p.B * (size_t)p.N * sizeof(double)));
   w.kbar = reinterpret_cast<double*>(take((size_t)p.total_passages * p.d * sizeof(double)));
-  w.cosv = reinterpret_cast<double*>(take((size_t)p.B * p.k_max * p.P_max * sizeof(double)));
+  const size_t S = (size_t)edge_slices(p);
+  w.part = reinterpret_cast<double*>(take((size_t)p.B * S * p.k_max * p.P_max * sizeof(double)));
+  w.qn2 = reinterpret_cast<double*>(take((size_t)p.B * S * p.k_max * sizeof(double)));
+  w.kn2 = reinterpret_cast<double*>(take((size_t)p.B * S * p.P_max * sizeof(double)));
   w.rowmask = reinterpret_cast<uint64_t*>(take((size_t)p.total_kept * sizeof(uint64_t)));
   w.bytes = off;
   return w;
@@ -165,7 +171,7 @@ skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
   if (p->total_kept == 0) {
     // No kept rows: only the (empty) CSR needs its closing offset.
     if (edge_rowptr_out)
-      SKIP_TRY(launch_edge_select(*p, w.cosv, kept_offsets, query_passages, w.rowmask,
+      SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets, query_passages, w.rowmask,
                                   edge_rowptr_out, edge_col_out, s));
     return SKIP_OK;
   }
@@ -175,9 +181,9 @@ skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
                                 w.rowmask, s));
   } else {
     if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-    SKIP_TRY(launch_edge_cos(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
-                             w.cosv, s));
-    SKIP_TRY(launch_edge_select(*p, w.cosv, kept_offsets, query_passages, w.rowmask,
+    SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
+                             EdgePartials{w.part, w.qn2, w.kn2}, s));
+    SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets, query_passages, w.rowmask,
                                 edge_rowptr_out, edge_col_out, s));
   }
   SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
@@ -221,11 +227,11 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
     SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
   SKIP_TRY(mark());
   if (work)
-    SKIP_TRY(launch_edge_cos(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
-                             w.cosv, s));
+    SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
+                             EdgePartials{w.part, w.qn2, w.kn2}, s));
   SKIP_TRY(mark());
   if (work)
-    SKIP_TRY(launch_edge_select(*p, w.cosv, kept_offsets, query_passages, w.rowmask, nullptr,
+    SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets, query_passages, w.rowmask, nullptr,
                                 nullptr, s));
   SKIP_TRY(mark());
   if (work)

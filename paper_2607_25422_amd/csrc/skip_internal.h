@@ -14,7 +14,9 @@ struct Workspace {
   double* u;          // [B][d]        scoring vector q_bar/sqrt(d) + w
   double* z;          // [B][N]        salience logits
   double* kbar;       // [total_passages][d] passage keys
-  double* cosv;       // [B][k_max*P_max] cosines, flattened i*P_b + j
+  double* part;       // [B][S][k_max][P_max] partial dot products (S slices of d)
+  double* qn2;        // [B][S][k_max] partial squared row norms
+  double* kn2;        // [B][S][P_max] partial squared passage-key norms
   uint64_t* rowmask;  // [total_kept]  neighbour passages of each kept row
   size_t bytes;
 };
@@ -46,12 +48,17 @@ struct QuerySource {
 hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
                                const int32_t* passage_offsets, double* kbar,
                                hipStream_t s);
-hipError_t launch_edge_cos(const skip_problem_t& p, QuerySource q,
+struct EdgePartials {
+  double* part;
+  double* qn2;
+  double* kn2;
+};
+int edge_slices(const skip_problem_t& p);
+hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
                            const int32_t* kept_offsets,
                            const int32_t* query_passages, const double* kbar,
-                           const float* passage_keys, double* cosv,
-                           hipStream_t s);
-hipError_t launch_edge_select(const skip_problem_t& p, const double* cosv,
+                           const float* passage_keys, EdgePartials ep, hipStream_t s);
+hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
                               const int32_t* kept_offsets,
                               const int32_t* query_passages, uint64_t* rowmask,
                               int32_t* rowptr_out, int32_t* col_out,
