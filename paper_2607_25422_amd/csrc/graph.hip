@@ -109,17 +109,37 @@ passage_keys_kernel(const T* __restrict__ Kh, const int32_t* __restrict__ passag
 }
 
 // ---------------------------------------------------------------------------
-// Edge dot products, split over d.  Workgroup = (512-column slice, 32 kept
-// rows, question).  Per 256-column chunk, the rows (transposed, float) and 16
-// passage keys at a time (float64) are staged in LDS; thread (i = t%32,
-// g = t/32) accumulates rows i against passages g and g+8 of each group of
-// 16.  Partial dot products and squared norms are written per slice and
-// summed in slice order by the selection kernel (deterministic).
-constexpr int kEdRows = 32;
+// Edge dot products on the float64 matrix cores, split over d.
+// Workgroup = (512-column slice, 64 kept rows x 16 passages, question); wave w
+// owns rows 16w..16w+15 of the block.  v_mfma_f64_16x16x4_f64 takes one
+// element of A (rows x 4 columns) and one of B (4 columns x passages) per
+// lane: lane l supplies row/passage l % 16 and column slot l / 16.  The
+// contraction order over columns is free, so column slot kk of MFMA m (m =
+// 0..7 within a 32-column step) is column 8*kk + m: every lane then reads 8
+// consecutive columns of its row (one 16-byte load) and of its passage key,
+// straight from global memory.  Each lane also sums the squares of the values
+// it loads (partial row and key norms).  Results per slice are summed in
+// slice order by the selection kernel.
+constexpr int kEdRows = 64;
+constexpr int kEdPT = 16;
 constexpr int kEdSlice = 512;
-constexpr int kEdChunk = 256;
-constexpr int kEdPG = 16;
-constexpr int kEdMaxGroups = 64 / kEdPG;
+
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+template <typename T>
+__device__ __forceinline__ void load8_f64(const T* p, bool ok, double* out);
+template <>
+__device__ __forceinline__ void load8_f64<bf16_t>(const bf16_t* p, bool ok, double* out) {
+  u32x4 x = ok ? *reinterpret_cast<const u32x4*>(p) : u32x4{0u, 0u, 0u, 0u};
+  unpack_f64<bf16_t>(x, out);
+}
+template <>
+__device__ __forceinline__ void load8_f64<float>(const float* p, bool ok, double* out) {
+  u32x4 x0 = ok ? *reinterpret_cast<const u32x4*>(p) : u32x4{0u, 0u, 0u, 0u};
+  u32x4 x1 = ok ? *reinterpret_cast<const u32x4*>(p + 4) : u32x4{0u, 0u, 0u, 0u};
+  unpack_f64<float>(x0, out);
+  unpack_f64<float>(x1, out + 4);
+}
 
 template <typename T>
 __global__ void __launch_bounds__(256)
@@ -127,109 +147,77 @@ edge_dot_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_id
                 const int32_t* __restrict__ kept_offsets,
                 const int32_t* __restrict__ query_passages, const double* __restrict__ kbar,
                 const float* __restrict__ pkeys, int d, int total_kept, int total_passages,
-                int k_max, int P_max, int S, double* __restrict__ part,
+                int k_max, int P_max, int S, int n_pt, double* __restrict__ part,
                 double* __restrict__ qn2p, double* __restrict__ kn2p) {
-  constexpr int VEC = GVec<T>::n;
-  __shared__ float qT[kEdChunk][kEdRows + 1];
-  __shared__ __attribute__((aligned(16))) double kb[kEdPG][kEdChunk];
-  __shared__ const T* rowp[kEdRows];
-
   const int s = blockIdx.x, b = blockIdx.z;
+  const int rb = blockIdx.y / n_pt, pt = blockIdx.y % n_pt;
   int k0, k1, p0, p1;
   range_of(kept_offsets, b, total_kept, k0, k1);
   range_of(query_passages, b, total_passages, p0, p1);
   const int kq = min(k1 - k0, k_max);
   const int P = min(min(p1 - p0, P_max), 64);
-  const int i0 = blockIdx.y * kEdRows;
-  if (i0 >= kq || P <= 0) return;
-  const int nrows = min(kEdRows, kq - i0);
-  const int c_begin = s * kEdSlice;
-  const int c_end = min(d, c_begin + kEdSlice);
-  const int tid = threadIdx.x;
-  const int i = tid % kEdRows, g = tid / kEdRows;
-  const int ngroups = (P + kEdPG - 1) / kEdPG;
-
-  if (tid < kEdRows) {
-    const T* ptr = nullptr;
-    if (tid < nrows) {
-      if (kept_idx) {
-        const int src = clampi(kept_idx[k0 + i0 + tid], 0, N - 1);
-        ptr = qbase + ((size_t)b * N + src) * d;
-      } else {
-        ptr = qbase + (size_t)(k0 + i0 + tid) * d;
-      }
-    }
-    rowp[tid] = ptr;
-  }
-  __syncthreads();
-
-  double acc[2 * kEdMaxGroups];
-#pragma unroll
-  for (int q = 0; q < 2 * kEdMaxGroups; ++q) acc[q] = 0.0;
-  double qq = 0.0;
-  double kk[kEdMaxGroups];
-#pragma unroll
-  for (int q = 0; q < kEdMaxGroups; ++q) kk[q] = 0.0;
-
-  for (int cc = c_begin; cc < c_end; cc += kEdChunk) {
-    const int cw = min(kEdChunk, c_end - cc);
-    // rows, transposed: 32 rows x cw columns in 16-byte pieces
-    for (int ch = tid; ch < kEdRows * (kEdChunk / VEC); ch += 256) {
-      const int r = ch / (kEdChunk / VEC), cv = (ch % (kEdChunk / VEC)) * VEC;
-      u32x4 x = u32x4{0u, 0u, 0u, 0u};
-      if (r < nrows && cv < cw) x = *reinterpret_cast<const u32x4*>(rowp[r] + cc + cv);
-      double v[VEC];
-      unpack_f64<T>(x, v);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) qT[cv + e][r] = (float)v[e];
-    }
-    __syncthreads();
-    if (tid < kEdRows)
-      for (int c = 0; c < cw; ++c) {
-        const double v = (double)qT[c][tid];
-        qq = fma(v, v, qq);
-      }
-    for (int pg = 0; pg < ngroups; ++pg) {
-      const int jn = min(kEdPG, P - pg * kEdPG);
-      for (int e = tid; e < kEdPG * kEdChunk; e += 256) {
-        const int jj = e / kEdChunk, c = e % kEdChunk;
-        double v = 0.0;
-        if (jj < jn && c < cw) {
-          const size_t off = (size_t)(p0 + pg * kEdPG + jj) * d + cc + c;
-          v = pkeys ? (double)pkeys[off] : kbar[off];
-        }
-        kb[jj][c] = v;
-      }
-      __syncthreads();
-      double a0 = acc[2 * pg], a1 = acc[2 * pg + 1];
-      for (int c = 0; c < cw; ++c) {
-        const double qv = (double)qT[c][i];
-        a0 = fma(qv, kb[g][c], a0);
-        a1 = fma(qv, kb[g + 8][c], a1);
-      }
-      acc[2 * pg] = a0;
-      acc[2 * pg + 1] = a1;
-      if (blockIdx.y == 0 && tid < kEdPG)
-        for (int c = 0; c < cw; ++c) kk[pg] = fma(kb[tid][c], kb[tid][c], kk[pg]);
-      __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rt0 = rb * kEdRows + wave * 16;          // first row of this wave
+  if (rt0 >= kq || pt * kEdPT >= P) return;          // whole wave (no barriers)
+  const int c_begin = s * kEdSlice, c_end = min(d, c_begin + kEdSlice);
+  const int l16 = lane & 15, kk = lane >> 4;
+  const int row = rt0 + l16, pj = pt * kEdPT + l16;
+  const bool row_ok = row < kq, key_ok = pj < P;
+  const T* qrow = qbase;          // never read unless row_ok
+  if (row_ok) {
+    if (kept_idx) {
+      const int src = clampi(kept_idx[k0 + row], 0, N - 1);
+      qrow = qbase + ((size_t)b * N + src) * d;
+    } else {
+      qrow = qbase + (size_t)(k0 + row) * d;
     }
   }
+  const size_t krow = (size_t)(p0 + (key_ok ? pj : 0)) * d;
+
+  f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
+  double qq = 0.0, k2 = 0.0;
+  for (int c0 = c_begin; c0 < c_end; c0 += 32) {
+    const int c = c0 + 8 * kk;
+    const bool in = c < c_end;                 // d is a multiple of 8
+    double qa[8], kv[8];
+    load8_f64<T>(qrow + c, row_ok && in, qa);
+    if (pkeys) {
+      load8_f64<float>(pkeys + krow + c, key_ok && in, kv);
+    } else if (key_ok && in) {
+      const double2* kp = reinterpret_cast<const double2*>(kbar + krow + c);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const double2 t = kp[q];
+        kv[2 * q] = t.x;
+        kv[2 * q + 1] = t.y;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kv[e] = 0.0;
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[m], kv[m], acc, 0, 0, 0);
+      qq = fma(qa[m], qa[m], qq);
+      k2 = fma(kv[m], kv[m], k2);
+    }
+  }
+  // lanes l16, l16+16, l16+32, l16+48 hold the four column slots of one row/key
+  qq += __shfl_xor(qq, 16, 64);
+  qq += __shfl_xor(qq, 32, 64);
+  k2 += __shfl_xor(k2, 16, 64);
+  k2 += __shfl_xor(k2, 32, 64);
   const size_t base = (size_t)b * S + s;
-  if (i < nrows) {
-    for (int pg = 0; pg < ngroups; ++pg) {
+  // D[i][j]: register r of lane l holds row 4*r + l/16, passage column l % 16
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const int j = pg * kEdPG + g + 8 * h2;
-        if (j < P) part[(base * k_max + i0 + i) * P_max + j] = acc[2 * pg + h2];
-      }
-    }
-    if (tid < kEdRows) qn2p[base * k_max + i0 + i] = qq;
+  for (int r = 0; r < 4; ++r) {
+    const int i = rt0 + 4 * r + kk;
+    if (i < kq && key_ok) part[(base * k_max + i) * P_max + pj] = acc[r];
   }
-  if (blockIdx.y == 0 && tid < kEdPG)
-    for (int pg = 0; pg < ngroups; ++pg) {
-      const int j = pg * kEdPG + tid;
-      if (j < P) kn2p[base * P_max + j] = kk[pg];
-    }
+  if (kk == 0) {
+    if (pt == 0 && row_ok) qn2p[base * k_max + row] = qq;
+    if (rb == 0 && wave == 0 && key_ok) kn2p[base * P_max + pj] = k2;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -269,11 +257,18 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
     if (jj < cnt) {
       const int f = e0 + jj, i = f / P, j = f % P;
       double dot = 0.0, q2 = 0.0, k2 = 0.0;
-      for (int sl = 0; sl < S; ++sl) {
-        const size_t base = (size_t)b * S + sl;
-        dot += part[(base * k_max + i) * P_max + j];
-        q2 += qn2p[base * k_max + i];
-        k2 += kn2p[base * P_max + j];
+      for (int sl0 = 0; sl0 < S; sl0 += 8) {
+        double pd[8], pq[8], pk[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const size_t base = (size_t)b * S + min(sl0 + u, S - 1);
+          pd[u] = part[(base * k_max + i) * P_max + j];
+          pq[u] = qn2p[base * k_max + i];
+          pk[u] = kn2p[base * P_max + j];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (sl0 + u < S) { dot += pd[u]; q2 += pq[u]; k2 += pk[u]; }
       }
       const double nq = sqrt(q2), nk = sqrt(k2);
       keys[jj] = order_key((nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0);
@@ -376,17 +371,18 @@ hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
                            hipStream_t s) {
   if (p.k_max <= 0 || p.P_max <= 0) return hipSuccess;
   const int S = edge_slices(p);
-  dim3 grid(S, (p.k_max + kEdRows - 1) / kEdRows, p.B);
+  const int n_pt = (p.P_max + kEdPT - 1) / kEdPT;
+  dim3 grid(S, ((p.k_max + kEdRows - 1) / kEdRows) * n_pt, p.B);
   if (p.dtype == SKIP_F32)
     hipLaunchKernelGGL(edge_dot_kernel<float>, grid, dim3(256), 0, s,
                        (const float*)q.base, q.kept_idx, q.N, kept_offsets, query_passages,
                        kbar, passage_keys, p.d, p.total_kept, p.total_passages, p.k_max,
-                       p.P_max, S, ep.part, ep.qn2, ep.kn2);
+                       p.P_max, S, n_pt, ep.part, ep.qn2, ep.kn2);
   else
     hipLaunchKernelGGL(edge_dot_kernel<bf16_t>, grid, dim3(256), 0, s,
                        (const bf16_t*)q.base, q.kept_idx, q.N, kept_offsets,
                        query_passages, kbar, passage_keys, p.d, p.total_kept,
-                       p.total_passages, p.k_max, p.P_max, S, ep.part, ep.qn2, ep.kn2);
+                       p.total_passages, p.k_max, p.P_max, S, n_pt, ep.part, ep.qn2, ep.kn2);
   return hipGetLastError();
 }
 

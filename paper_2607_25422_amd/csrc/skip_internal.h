@@ -49,9 +49,9 @@ hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
                                const int32_t* passage_offsets, double* kbar,
                                hipStream_t s);
 struct EdgePartials {
-  double* part;
-  double* qn2;
-  double* kn2;
+  double* part;              // per-slice partial dot products
+  double* qn2;               // per-slice partial squared row norms
+  double* kn2;               // per-slice partial squared passage-key norms
 };
 int edge_slices(const skip_problem_t& p);
 hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,

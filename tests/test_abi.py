@@ -59,8 +59,8 @@ def _problem(b, **kw):
 def test_workspace_bytes(b):
     p = _problem(b)
     n = b.workspace_bytes(p)
-    # u + z + kbar + edge partials (2 slices of 512 columns) + row and key
-    # norm partials + rowmask, each rounded to 256 bytes
+    # u + z + kbar + edge partials (2 slices of 512 columns) + row-norm and
+    # key-norm partials + rowmask, each rounded to 256 bytes
     S = 2
     parts = [2 * 1024 * 8, 2 * 576 * 8, 3 * 1024 * 8, 2 * S * 96 * 2 * 8, 2 * S * 96 * 8,
              2 * S * 2 * 8, 192 * 8]
