@@ -82,10 +82,11 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
 
 // Transposing LDS read: in each group of 16 lanes, lane j receives element
 // j & 3 of the 8-byte pieces addressed by lanes (j >> 2) + 4e, e = 0..3.
-__device__ __forceinline__ uint2 ds_read_tr16(const bf16_t* p) {
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2 ds_read_tr16(const bf16_t* p) {
   s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (__attribute__((address_space(3))) s16x4_t*)(p));
-  return __builtin_bit_cast(uint2, v);
+  return __builtin_bit_cast(u32x2, v);
 }
 
 // bf16 path.  Work item = (question b, head h, block of <= 256 kept rows);
@@ -101,7 +102,7 @@ __device__ __forceinline__ uint2 ds_read_tr16(const bf16_t* p) {
 // The S^T accumulator layout gives lane half hh, element e of a 16-token
 // block the token 8*(e/4) + 4*hh + e%4; the V^T operand is read in that same
 // token order, so P^T needs no data movement.
-template <int D>
+template <int D, bool SPLIT_P>
 __global__ void __launch_bounds__(kThreads)
 attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
                  int N, int qstride, const int32_t* __restrict__ kept_offsets,
@@ -116,11 +117,13 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   constexpr int KB = D / 16;               // k-blocks of QK^T
   constexpr int DT = D / 32;               // 32-wide feature tiles of O
   constexpr int TILE = kTile * D;          // elements per K (or V) tile
-  constexpr int LPT = 2 * NCH / kWaves;    // direct loads per lane per tile
+  constexpr int NI = kTile * NCH / 64;     // 1 KiB load instructions per K (or V) tile
+  // direct loads per lane per tile (waves >= NI issue none when NI < kWaves)
+  constexpr int LPT = 2 * ((NI + kWaves - 1) / kWaves);
   // V chunk swizzle: depends on row % 4 only; keeps the transposing reads of
   // four consecutive tokens on distinct banks.
   auto vswz = [](int row) { return (NCH >= 16 ? 4 : 2) * (row & 3); };
-  static_assert(NCH % kWaves == 0, "tile loads must divide over the waves");
+  static_assert(NI % kWaves == 0 || NI < kWaves, "tile loads must divide over the waves");
   __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kStages * TILE];
   __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kStages * TILE];
   __shared__ uint64_t wave_union[kWaves];
@@ -225,7 +228,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     bf16_t* Ks = Kbuf + stage * TILE;
     bf16_t* Vs = Vbuf + stage * TILE;
 #pragma unroll
-    for (int q = wave_s; q < NCH; q += kWaves) {
+    for (int q = wave_s; q < NI; q += kWaves) {
       const int o = q * 64 + lane;
       const int row = o / NCH, pch = o % NCH;
       const int ck = pch ^ (row & (NCH - 1));
@@ -266,95 +269,150 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
 #pragma unroll
   for (int s = 0; s < kStages - 1; ++s)
     if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
-
-  for (int i = 0; advance(cc); ++i) {
-    const int ahead = issued - i - 1;
+  // tile i's loads have landed once at most `ahead` later tiles are pending
+  auto wait_tile = [&](int ahead) {
     if (ahead >= 2) wait_vmem<2 * LPT>();
     else if (ahead == 1) wait_vmem<LPT>();
     else wait_vmem<0>();
-    barrier_nofence();
-    if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+  };
 
-    const int j = cc.j;
-    if (!((wmask >> j) & 1ull)) continue;
-    const bf16_t* Ks = Kbuf + (i % kStages) * TILE;
-    const bf16_t* Vs = Vbuf + (i % kStages) * TILE;
-    const int t_base = cc.t, t_end = cc.te;
-    const bool adj = (mrow >> j) & 1ull;
+  if (wmask == 0) {
+    // A wave without kept rows only helps to stream the tiles.
+    for (int i = 0; advance(cc); ++i) {
+      wait_tile(issued - i - 1);
+      barrier_nofence();
+      if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+    }
+  } else {
+    for (int i = 0; advance(cc); ++i) {
+      wait_tile(issued - i - 1);
+      barrier_nofence();
+      if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
 
-    // two sub-steps of 32 tokens, each a complete online-softmax update
-    const bool full = t_base + kTile <= t_end;
-    const float mbias = adj ? 0.f : -INFINITY;
+      // Every tile is computed; rows not adjacent to its passage are masked
+      // (a wave whose rows all miss the passage contributes nothing).
+      const bf16_t* Ks = Kbuf + (i % kStages) * TILE;
+      const bf16_t* Vs = Vbuf + (i % kStages) * TILE;
+      const bool full = cc.t + kTile <= cc.te;
+      const float mbias = ((mrow >> cc.j) & 1ull) ? 0.f : -INFINITY;
+      // accumulator element v of sub-tile st is token 32*st + 8*(v/4) + v%4
+      // + 4*hh of the tile; it exists if that is below rem
+      const int rem = cc.te - cc.t - 4 * hh;
+
+      // S^T = K . Q^T for the 64 tokens: two independent 32-token chains
+      f32x16_t sacc[2];
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      // S^T = K . Q^T for 32 tokens
-      u32x4 ka[KB];
+      for (int st = 0; st < 2; ++st) {
+        u32x4 ka[KB];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        ka[kb] = *reinterpret_cast<const u32x4*>(Ks + st * 32 * D + koff[kb]);
-      f32x16_t sacc;
+        for (int kb = 0; kb < KB; ++kb)
+          ka[kb] = *reinterpret_cast<const u32x4*>(Ks + st * 32 * D + koff[kb]);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+        for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) sacc = mfma32(ka[kb], qf[kb], sacc);
+        for (int kb = 0; kb < KB; ++kb) sacc[st] = mfma32(ka[kb], qf[kb], sacc[st]);
+      }
       __builtin_amdgcn_sched_barrier(0);
 
-      // V^T operands of the two 16-token k-blocks, read while the softmax runs
+      // V^T operands of k-blocks 0 and 1, read while the softmax runs
       u32x4 va[DT][2];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
-          const bf16_t* vp = Vs + (32 * st + 16 * g) * D + voff[dt];
-          const uint2 lo = ds_read_tr16(vp);
-          const uint2 hi = ds_read_tr16(vp + 8 * D);
-          va[dt][g] = u32x4{lo.x, lo.y, hi.x, hi.y};
+          const bf16_t* vp = Vs + (16 * g) * D + voff[dt];
+          va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
+                                              0, 1, 2, 3);
         }
 
-      // scale + adjacency mask in one fma; token bound only on a partial tile
-      float mt = -INFINITY;
+      // online softmax over the 32 scores of this lane's row
+      float c = scale_log2;
+      if (c < 0.f) {                   // fold a negative scale into the scores
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x = fmaf(sacc[v], scale_log2, mbias);
-        if (!full) {
-          const int tok = t_base + st * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          x = (tok < t_end) ? x : -INFINITY;
-        }
-        sacc[v] = x;
-        mt = fmaxf(mt, x);
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sacc[st][v] = -sacc[st][v];
+        c = -c;
       }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float m_new = fmaxf(m_run, mt);
-      const float mref = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - mref);
-      float ls = 0.f;
-      u32x4 pb[2];
+      if (!full) {                     // tokens past the passage end
 #pragma unroll
-      for (int g = 0; g < 2; ++g) {
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (32 * st + 8 * (v >> 2) + (v & 3) >= rem) sacc[st][v] = -INFINITY;
+      }
+      float sm = sacc[0][0];
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sm = fmaxf(sm, sacc[st][v]);
+      sm = fmaxf(sm, __shfl_xor(sm, 32, 64));
+      const float mt = (sm == -INFINITY) ? -INFINITY : fmaf(sm, c, mbias);
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      const float bias = mbias - ((m_new == -INFINITY) ? 0.f : m_new);
+      m_run = m_new;
+      float ls = 0.f;
+      u32x4 pb[4], pl[4];
+#pragma unroll
+      for (int kb2 = 0; kb2 < 4; ++kb2) {
         float pv[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pv[e] = __builtin_amdgcn_exp2f(sacc[8 * g + e] - mref);
+          // scores are finite on a full tile (a row not adjacent to the
+          // passage has bias -inf); past the passage end the weight is 0
+          const int v = 8 * (kb2 & 1) + e;
+          const float x = sacc[kb2 >> 1][v];
+          pv[e] = __builtin_amdgcn_exp2f(fmaf(x, c, bias));
+          if (!full) pv[e] = (32 * (kb2 >> 1) + 8 * (v >> 2) + (v & 3) < rem) ? pv[e] : 0.f;
           ls += pv[e];
         }
-        pb[g] = u32x4{pack2_bf16(pv[0], pv[1]), pack2_bf16(pv[2], pv[3]),
-                      pack2_bf16(pv[4], pv[5]), pack2_bf16(pv[6], pv[7])};
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = pack2_bf16(pv[2 * q], pv[2 * q + 1]);
+        pb[kb2] = u32x4{w[0], w[1], w[2], w[3]};
+        if (SPLIT_P) {
+          uint32_t wl[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            wl[q] = pack2_bf16(pv[2 * q] - __uint_as_float(w[q] << 16),
+                               pv[2 * q + 1] - __uint_as_float(w[q] & 0xffff0000u));
+          pl[kb2] = u32x4{wl[0], wl[1], wl[2], wl[3]};
+        }
       }
       l_run = l_run * alpha + ls;
-      m_run = m_new;
-      if (__any(alpha != 1.f)) {
+      if (__any(alpha != 1.f)) {       // some row's maximum moved
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
           for (int v = 0; v < 16; ++v) acc[dt][v] *= alpha;
       }
       __builtin_amdgcn_sched_barrier(0);
+
+      // O^T += V^T . P^T, k-blocks 0-1 then 2-3
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        acc[dt] = mfma32(va[dt][0], pb[0], acc[dt]);
-        acc[dt] = mfma32(va[dt][1], pb[1], acc[dt]);
+      for (int half = 0; half < 2; ++half) {
+        if (half == 1) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int g = 0; g < 2; ++g) {
+              const bf16_t* vp = Vs + (32 + 16 * g) * D + voff[dt];
+              va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
+                                                  0, 1, 2, 3);
+            }
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          acc[dt] = mfma32(va[dt][0], pb[2 * half], acc[dt]);
+          acc[dt] = mfma32(va[dt][1], pb[2 * half + 1], acc[dt]);
+          if (SPLIT_P) {
+            acc[dt] = mfma32(va[dt][0], pl[2 * half], acc[dt]);
+            acc[dt] = mfma32(va[dt][1], pl[2 * half + 1], acc[dt]);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -487,14 +545,20 @@ hipError_t launch_attention(const skip_problem_t& p, QuerySource q,
     const int n_items = p.B * p.H * RB;
     const int grid = ((n_items + 7) / 8) * 8;
     const float sl2 = p.sm_scale * kLog2e;
-#define SKIP_ATTN_BF16(DD)                                                                   \
-  hipLaunchKernelGGL(attn_bf16_kernel<DD>, dim3(grid), dim3(kThreads), 0, s,                 \
+#define SKIP_ATTN_BF16(DD, SP)                                                               \
+  hipLaunchKernelGGL((attn_bf16_kernel<DD, SP>), dim3(grid), dim3(kThreads), 0, s,           \
                      (const bf16_t*)q.base, q.kept_idx, q.N, qstride, kept_offsets,          \
                      (const bf16_t*)Kh, (const bf16_t*)Vh, passage_offsets, query_passages,  \
                      rowmask, p.H, p.total_kept, p.total_passages, p.total_tokens, p.k_max,  \
                      p.P_max, RB, n_items, sl2, O, p.o_f32, lse)
-    if (p.d_h == 64) SKIP_ATTN_BF16(64);
-    else SKIP_ATTN_BF16(128);
+    // float32 output: split softmax weights (bf16 hi + lo) for near-fp32 accuracy
+    if (p.d_h == 64) {
+      if (p.o_f32) SKIP_ATTN_BF16(64, true);
+      else SKIP_ATTN_BF16(64, false);
+    } else {
+      if (p.o_f32) SKIP_ATTN_BF16(128, true);
+      else SKIP_ATTN_BF16(128, false);
+    }
 #undef SKIP_ATTN_BF16
   } else {
     dim3 grid((p.k_max * p.H + 3) / 4, p.B);
