@@ -40,11 +40,33 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="highres_bf16")
     ap.add_argument("--seed", type=int, default=2026)
-    ap.add_argument("--cpu-sample", type=int, default=4,
+    ap.add_argument("--cpu-sample", type=int, default=12,
                     help="questions of the batch the CPU oracle is timed on (0: skip)")
     ap.add_argument("--pass-keys", action="store_true",
                     help="hand precomputed passage keys to the library (skips pooling)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="before timing, run an elementwise copy (negation) of MIB MiB of "
+                         "float32 three times, so a hardware-counter pass can scale "
+                         "FETCH_SIZE / WRITE_SIZE by a kernel of known traffic")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel.highres_bf16.traffic.json")
+ATTN_SOURCE = os.path.join(ROOT, "paper_2607_25422_amd", "csrc", "attn.hip")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when it was taken on another workload or an older attention source."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    sha = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+    if rec.get("workload") != workload or rec.get("attn_source_sha256") != sha:
+        return None
+    return rec.get("hbm_bytes_per_launch")
 
 
 def cpu_model() -> str:
@@ -108,6 +130,13 @@ def main():
     out = (torch.empty(p.total_kept, dtype=torch.int32, device="cuda"),
            torch.empty((p.total_kept, p.H, p.d_h), dtype=batch.torch_dtype, device="cuda"),
            torch.empty((p.total_kept, p.H), dtype=torch.float32, device="cuda"))
+    if args.calibrate_copy > 0:
+        src = torch.ones(args.calibrate_copy << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     events = [B.StageEvents() for _ in range(args.steps)]
     for _ in range(args.warmup):
         B.route_fused(db, passage_keys=pkeys, out=out)
@@ -159,7 +188,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(wl.name),
             "algorithmic_bytes": attn_bytes,
             "avg_ms": round(attn_ms, 5),
         },
