@@ -73,11 +73,31 @@ __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
 }
 
+// LDS byte address of a shared-memory pointer, as a wave-uniform value.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
+}
+
 // A wave-uniform 64-bit value moved to scalar registers.
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
   return ((uint64_t)hi << 32) | lo;
+}
+
+// Direct global->LDS load of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l's bytes land at LDS byte address lds + 16 * l (lds wave-uniform).
+// Issued through inline assembly so that the compiler's wait-count pass does
+// not treat it as a write that may alias every later LDS read (it would put
+// a full vmcnt(0) before them and drain the prefetch ring); completion is
+// awaited explicitly with wait_vmem<> before the barrier that publishes a
+// tile.
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(lds)
+               : "memory", "m0");
 }
 
 // Transposing LDS read: in each group of 16 lanes, lane j receives element
@@ -185,6 +205,10 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     for (int kb = 0; kb < KB; ++kb)
       qf[kb] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh)
                       : u32x4{0u, 0u, 0u, 0u};
+    // Settle the query loads here: left pending, the compiler would wait for
+    // them (vmcnt(0)) inside the tile loop, draining the prefetch ring.
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) asm volatile("" ::"v"(qf[kb]));
   }
   __syncthreads();
   uint64_t U = 0;
@@ -235,8 +259,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
       const int cv = pch ^ vswz(row);
       const int tok = min(t + row, te - 1);
       const size_t rowoff = ((size_t)tok * H + h) * D;
-      __builtin_amdgcn_global_load_lds(Kh + rowoff + ck * 8, Ks + q * 512, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(Vh + rowoff + cv * 8, Vs + q * 512, 16, 0, 0);
+      lds_dma16(Kh + rowoff + ck * 8, lds_addr(Ks + q * 512));
+      lds_dma16(Vh + rowoff + cv * 8, lds_addr(Vs + q * 512));
     }
   };
 
