@@ -100,6 +100,13 @@ __device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
                : "memory", "m0");
 }
 
+// Value of lane l ^ 32 (v_permlane32_swap: the two half-waves trade places).
+__device__ __forceinline__ float swap_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return __uint_as_float(__lane_id() < 32 ? r[1] : r[0]);
+}
+
 // Transposing LDS read: in each group of 16 lanes, lane j receives element
 // j & 3 of the 8-byte pieces addressed by lanes (j >> 2) + 4e, e = 0..3.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -139,11 +146,12 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   constexpr int TILE = kTile * D;          // elements per K (or V) tile
   constexpr int NI = kTile * NCH / 64;     // 1 KiB load instructions per K (or V) tile
   // direct loads per lane per tile (waves >= NI issue none when NI < kWaves)
-  constexpr int LPT = 2 * ((NI + kWaves - 1) / kWaves);
+  constexpr int kLoaders = kWaves / 2;    // group A issues every tile load
+  constexpr int LPT = 2 * ((NI + kLoaders - 1) / kLoaders);
   // V chunk swizzle: depends on row % 4 only; keeps the transposing reads of
   // four consecutive tokens on distinct banks.
   auto vswz = [](int row) { return (NCH >= 16 ? 4 : 2) * (row & 3); };
-  static_assert(NI % kWaves == 0 || NI < kWaves, "tile loads must divide over the waves");
+  static_assert(NI % kLoaders == 0, "tile loads must divide over the loading waves");
   __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kStages * TILE];
   __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kStages * TILE];
   __shared__ uint64_t wave_union[kWaves];
@@ -252,7 +260,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     bf16_t* Ks = Kbuf + stage * TILE;
     bf16_t* Vs = Vbuf + stage * TILE;
 #pragma unroll
-    for (int q = wave_s; q < NI; q += kWaves) {
+    for (int q = wave_s; q < NI; q += kLoaders) {
       const int o = q * 64 + lane;
       const int row = o / NCH, pch = o % NCH;
       const int ck = pch ^ (row & (NCH - 1));
@@ -288,160 +296,188 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     voff[dt] = tr_tok * D + (((d >> 3) ^ vswz(tr_tok)) << 3) + (d & 7);
   }
 
+  // Matrix phase: O^T += V^T . P^T for the previous tile (weights pb/pl,
+  // V tile in stage pv_stage), then S^T = K . Q^T for the tile in stage
+  // s_stage into sacc.
+  f32x16_t sacc[2];
+  u32x4 pb[4], pl[4];
+  float acc_scale = 1.f;             // rescale of acc owed by the last softmax
+  auto pv_product = [&](int pv_stage) {
+    __builtin_amdgcn_sched_barrier(0);
+    if (__any(acc_scale != 1.f)) {   // some row's maximum moved
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[dt][v] *= acc_scale;
+    }
+    const bf16_t* Vs = Vbuf + pv_stage * TILE;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      u32x4 va[DT][2];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const bf16_t* vp = Vs + (32 * half + 16 * g) * D + voff[dt];
+          va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
+                                              0, 1, 2, 3);
+        }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        acc[dt] = mfma32(va[dt][0], pb[2 * half], acc[dt]);
+        acc[dt] = mfma32(va[dt][1], pb[2 * half + 1], acc[dt]);
+        if (SPLIT_P) {
+          acc[dt] = mfma32(va[dt][0], pl[2 * half], acc[dt]);
+          acc[dt] = mfma32(va[dt][1], pl[2 * half + 1], acc[dt]);
+        }
+      }
+    }
+  };
+  auto s_product = [&](int s_stage) {
+    __builtin_amdgcn_sched_barrier(0);
+    const bf16_t* Ks = Kbuf + s_stage * TILE;
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      u32x4 ka[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        ka[kb] = *reinterpret_cast<const u32x4*>(Ks + st * 32 * D + koff[kb]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) sacc[st] = mfma32(ka[kb], qf[kb], sacc[st]);
+    }
+  };
+  // Vector phase: online softmax over the 32 scores of this lane's row in
+  // sacc (tile with `full`, `rem`, adjacency bias `mbias`); rescales acc and
+  // leaves the bf16 weights in pb (and their remainders in pl).
+  auto softmax = [&](bool full, int rem, float mbias) {
+    __builtin_amdgcn_sched_barrier(0);
+    float c = scale_log2;
+    if (c < 0.f) {                   // fold a negative scale into the scores
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[st][v] = -sacc[st][v];
+      c = -c;
+    }
+    if (!full) {                     // tokens past the passage end
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (32 * st + 8 * (v >> 2) + (v & 3) >= rem) sacc[st][v] = -INFINITY;
+    }
+    float sm = sacc[0][0];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sm = fmaxf(sm, sacc[st][v]);
+    sm = fmaxf(sm, swap_halves(sm));
+    const float mt = (sm == -INFINITY) ? -INFINITY : fmaf(sm, c, mbias);
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    const float bias = mbias - ((m_new == -INFINITY) ? 0.f : m_new);
+    m_run = m_new;
+    float ls = 0.f;
+#pragma unroll
+    for (int kb2 = 0; kb2 < 4; ++kb2) {
+      float pv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        // scores are finite on a full tile (a row not adjacent to the
+        // passage has bias -inf); past the passage end the weight is 0
+        const int v = 8 * (kb2 & 1) + e;
+        const float x = sacc[kb2 >> 1][v];
+        pv[e] = __builtin_amdgcn_exp2f(fmaf(x, c, bias));
+        if (!full) pv[e] = (32 * (kb2 >> 1) + 8 * (v >> 2) + (v & 3) < rem) ? pv[e] : 0.f;
+        ls += pv[e];
+      }
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = pack2_bf16(pv[2 * q], pv[2 * q + 1]);
+      pb[kb2] = u32x4{w[0], w[1], w[2], w[3]};
+      if (SPLIT_P) {
+        uint32_t wl[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          wl[q] = pack2_bf16(pv[2 * q] - __uint_as_float(w[q] << 16),
+                             pv[2 * q + 1] - __uint_as_float(w[q] & 0xffff0000u));
+        pl[kb2] = u32x4{wl[0], wl[1], wl[2], wl[3]};
+      }
+    }
+    l_run = l_run * alpha + ls;
+    acc_scale = alpha;               // applied before the next PV product
+  };
+
+  // Tile loop, two half-steps per tile separated by barriers: the matrix
+  // phase of tile i (PV of tile i-1, S of tile i), then its softmax.  Group B
+  // (waves 4-7) takes one extra barrier first, so it runs half a step behind
+  // group A (waves 0-3): on each SIMD one wave's matrix work overlaps the
+  // other's vector work.  Group A issues and awaits every tile load; a tile
+  // is awaited before the barrier that precedes its first use by either
+  // group.  Tiles i-1 and i stay in use until group B's step i ends, so loads
+  // run STAGES-2 tiles ahead.
+  const bool group_b = wave >= 4;
+  const bool busy = wmask != 0;
   Cursor ci{U, -1, 0, 0}, cc{U, -1, 0, 0};
   int issued = 0;
+  if (!group_b) {
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s)
-    if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+    for (int s = 0; s < kStages - 2; ++s)
+      if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+  } else {
+    barrier_nofence();
+  }
   // tile i's loads have landed once at most `ahead` later tiles are pending
   auto wait_tile = [&](int ahead) {
     if (ahead >= 2) wait_vmem<2 * LPT>();
     else if (ahead == 1) wait_vmem<LPT>();
     else wait_vmem<0>();
   };
-
-  if (wmask == 0) {
-    // A wave without kept rows only helps to stream the tiles.
+  if (!busy) {
+    // A wave without kept rows only keeps step with the barriers (and, in
+    // group A, streams its share of the tiles).
     for (int i = 0; advance(cc); ++i) {
-      wait_tile(issued - i - 1);
+      if (!group_b) wait_tile(issued - i - 1);
       barrier_nofence();
-      if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+      if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+      barrier_nofence();
     }
   } else {
-    for (int i = 0; advance(cc); ++i) {
-      wait_tile(issued - i - 1);
+    // The first matrix phase adds tile 0's V with zero weights (exactly 0).
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      pb[q] = u32x4{0u, 0u, 0u, 0u};
+      pl[q] = u32x4{0u, 0u, 0u, 0u};
+    }
+    // Step i: PV of tile i-1 (zero weights at i = 0), S and softmax of tile
+    // i; a final step past the last tile does only the PV.
+    int prev_stage = 0;
+    for (int i = 0;; ++i) {
+      const bool more = advance(cc);
+      if (!more && i == 0) break;
+      if (more) {
+        if (!group_b) wait_tile(issued - i - 1);
+        barrier_nofence();
+        if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+      }
+      pv_product(prev_stage);
+      if (!more) break;
+      const int stage = i % kStages;
+      s_product(stage);
       barrier_nofence();
-      if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
-
-      // Every tile is computed; rows not adjacent to its passage are masked
-      // (a wave whose rows all miss the passage contributes nothing).
-      const bf16_t* Ks = Kbuf + (i % kStages) * TILE;
-      const bf16_t* Vs = Vbuf + (i % kStages) * TILE;
-      const bool full = cc.t + kTile <= cc.te;
-      const float mbias = ((mrow >> cc.j) & 1ull) ? 0.f : -INFINITY;
       // accumulator element v of sub-tile st is token 32*st + 8*(v/4) + v%4
       // + 4*hh of the tile; it exists if that is below rem
-      const int rem = cc.te - cc.t - 4 * hh;
-
-      // S^T = K . Q^T for the 64 tokens: two independent 32-token chains
-      f32x16_t sacc[2];
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        u32x4 ka[KB];
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-          ka[kb] = *reinterpret_cast<const u32x4*>(Ks + st * 32 * D + koff[kb]);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) sacc[st] = mfma32(ka[kb], qf[kb], sacc[st]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-
-      // V^T operands of k-blocks 0 and 1, read while the softmax runs
-      u32x4 va[DT][2];
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-          const bf16_t* vp = Vs + (16 * g) * D + voff[dt];
-          va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
-                                              0, 1, 2, 3);
-        }
-
-      // online softmax over the 32 scores of this lane's row
-      float c = scale_log2;
-      if (c < 0.f) {                   // fold a negative scale into the scores
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) sacc[st][v] = -sacc[st][v];
-        c = -c;
-      }
-      if (!full) {                     // tokens past the passage end
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            if (32 * st + 8 * (v >> 2) + (v & 3) >= rem) sacc[st][v] = -INFINITY;
-      }
-      float sm = sacc[0][0];
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sm = fmaxf(sm, sacc[st][v]);
-      sm = fmaxf(sm, __shfl_xor(sm, 32, 64));
-      const float mt = (sm == -INFINITY) ? -INFINITY : fmaf(sm, c, mbias);
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      const float bias = mbias - ((m_new == -INFINITY) ? 0.f : m_new);
-      m_run = m_new;
-      float ls = 0.f;
-      u32x4 pb[4], pl[4];
-#pragma unroll
-      for (int kb2 = 0; kb2 < 4; ++kb2) {
-        float pv[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          // scores are finite on a full tile (a row not adjacent to the
-          // passage has bias -inf); past the passage end the weight is 0
-          const int v = 8 * (kb2 & 1) + e;
-          const float x = sacc[kb2 >> 1][v];
-          pv[e] = __builtin_amdgcn_exp2f(fmaf(x, c, bias));
-          if (!full) pv[e] = (32 * (kb2 >> 1) + 8 * (v >> 2) + (v & 3) < rem) ? pv[e] : 0.f;
-          ls += pv[e];
-        }
-        uint32_t w[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) w[q] = pack2_bf16(pv[2 * q], pv[2 * q + 1]);
-        pb[kb2] = u32x4{w[0], w[1], w[2], w[3]};
-        if (SPLIT_P) {
-          uint32_t wl[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            wl[q] = pack2_bf16(pv[2 * q] - __uint_as_float(w[q] << 16),
-                               pv[2 * q + 1] - __uint_as_float(w[q] & 0xffff0000u));
-          pl[kb2] = u32x4{wl[0], wl[1], wl[2], wl[3]};
-        }
-      }
-      l_run = l_run * alpha + ls;
-      if (__any(alpha != 1.f)) {       // some row's maximum moved
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[dt][v] *= alpha;
-      }
-      __builtin_amdgcn_sched_barrier(0);
-
-      // O^T += V^T . P^T, k-blocks 0-1 then 2-3
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        if (half == 1) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int g = 0; g < 2; ++g) {
-              const bf16_t* vp = Vs + (32 + 16 * g) * D + voff[dt];
-              va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
-                                                  0, 1, 2, 3);
-            }
-        }
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          acc[dt] = mfma32(va[dt][0], pb[2 * half], acc[dt]);
-          acc[dt] = mfma32(va[dt][1], pb[2 * half + 1], acc[dt]);
-          if (SPLIT_P) {
-            acc[dt] = mfma32(va[dt][0], pl[2 * half], acc[dt]);
-            acc[dt] = mfma32(va[dt][1], pl[2 * half + 1], acc[dt]);
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      softmax(cc.t + kTile <= cc.te, cc.te - cc.t - 4 * hh,
+              ((mrow >> cc.j) & 1ull) ? 0.f : -INFINITY);
+      prev_stage = stage;
     }
   }
+  if (!group_b) barrier_nofence();
 
   // finalize
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = l_run + swap_halves(l_run);
   if (!row_ok) return;
   const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
   const size_t obase = ((size_t)(k0 + r) * H + h) * D;
