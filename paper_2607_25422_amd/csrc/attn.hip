@@ -209,9 +209,12 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
         qrow = qbase + (size_t)(k0 + r) * qstride + (size_t)h * D;
       }
     }
+    // a negative scale is folded in here (bf16 sign flips), so the logits
+    // below are always scaled by |scale|
+    const uint32_t neg = (scale_log2 < 0.f) ? 0x80008000u : 0u;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
-      qf[kb] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh)
+      qf[kb] = row_ok ? (*reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh) ^ neg)
                       : u32x4{0u, 0u, 0u, 0u};
     // Settle the query loads here: left pending, the compiler would wait for
     // them (vmcnt(0)) inside the tile loop, draining the prefetch ring.
@@ -353,15 +356,11 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   // leaves the bf16 weights in pb (and their remainders in pl).
   auto softmax = [&](bool full, int rem, float mbias) {
     __builtin_amdgcn_sched_barrier(0);
-    float c = scale_log2;
-    if (c < 0.f) {                   // fold a negative scale into the scores
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[st][v] = -sacc[st][v];
-      c = -c;
-    }
+    // (a negative scale was folded into the query fragments: c > 0)
+    const float c = fabsf(scale_log2);
     if (!full) {                     // tokens past the passage end
+      // kept as a branch: selecting on every tile would cost 64 VALU ops
+      asm volatile("");
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -387,10 +386,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
       for (int e = 0; e < 8; ++e) {
         // scores are finite on a full tile (a row not adjacent to the
         // passage has bias -inf); past the passage end the weight is 0
-        const int v = 8 * (kb2 & 1) + e;
-        const float x = sacc[kb2 >> 1][v];
-        pv[e] = __builtin_amdgcn_exp2f(fmaf(x, c, bias));
-        if (!full) pv[e] = (32 * (kb2 >> 1) + 8 * (v >> 2) + (v & 3) < rem) ? pv[e] : 0.f;
+        const float x = sacc[kb2 >> 1][8 * (kb2 & 1) + e];
+        pv[e] = __builtin_amdgcn_exp2f(fmaf(x, c, bias));   // 0 for a masked token
         ls += pv[e];
       }
       uint32_t w[4];
