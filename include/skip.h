@@ -195,7 +195,7 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V,
 /* Kernel stages of skip_route_fused, in launch order: question pooling,
  * salience scoring, top-k, passage keys, edge cosines, edge selection,
  * attention. */
-#define SKIP_FUSED_STAGES 7
+#define SKIP_FUSED_STAGES 6
 
 /*
  * skip_route_fused with per-stage timing, for profiling harnesses.
@@ -203,8 +203,9 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V,
  * created by the caller (host array of handles); event s is recorded on
  * `stream` just before stage s is enqueued and the last one after the final
  * stage, so hipEventElapsedTime(events[s], events[s+1]) is the duration of
- * stage s.  A stage with nothing to do (passage keys given by the caller)
- * records its two events back to back.  Other arguments and results as in
+ * stage s.  The stages, in order: pooling (the questions and, unless the
+ * caller gives passage keys, the passages), scoring, top-k, edge cosines,
+ * edge selection, attention.  Other arguments and results as in
  * skip_route_fused; SKIP_ERR_INVALID_ARG if stage_events is NULL or
  * n_events is wrong.
  */

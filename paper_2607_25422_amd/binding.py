@@ -29,8 +29,7 @@ SKIP_F32, SKIP_BF16 = 0, 1
 ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes",
                 "skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused",
                 "skip_route_fused_profiled")
-FUSED_STAGES = ("pool_question", "score", "topk", "passage_keys", "edge_cos", "edge_select",
-                "attention")
+FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
 class SkipError(RuntimeError):

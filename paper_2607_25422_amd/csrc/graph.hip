@@ -14,34 +14,10 @@
 //   csr_to_mask  : neighbour masks from a caller-given CSR graph
 #include "skip_common.h"
 #include "skip_internal.h"
+#include "skip_pool.h"
 #include "skip_select.h"
 
 namespace skip {
-
-template <typename T> struct GVec;
-template <> struct GVec<float> { static constexpr int n = 4; };
-template <> struct GVec<bf16_t> { static constexpr int n = 8; };
-
-template <typename T>
-__device__ __forceinline__ void unpack_f64(const u32x4& x, double* out);
-template <>
-__device__ __forceinline__ void unpack_f64<float>(const u32x4& x, double* out) {
-  out[0] = (double)__uint_as_float(x.x);
-  out[1] = (double)__uint_as_float(x.y);
-  out[2] = (double)__uint_as_float(x.z);
-  out[3] = (double)__uint_as_float(x.w);
-}
-template <>
-__device__ __forceinline__ void unpack_f64<bf16_t>(const u32x4& x, double* out) {
-  out[0] = (double)bf16_to_f32(x.x & 0xffffu);
-  out[1] = (double)bf16_to_f32(x.x >> 16);
-  out[2] = (double)bf16_to_f32(x.y & 0xffffu);
-  out[3] = (double)bf16_to_f32(x.y >> 16);
-  out[4] = (double)bf16_to_f32(x.z & 0xffffu);
-  out[5] = (double)bf16_to_f32(x.z >> 16);
-  out[6] = (double)bf16_to_f32(x.w & 0xffffu);
-  out[7] = (double)bf16_to_f32(x.w >> 16);
-}
 
 template <typename T> __device__ __forceinline__ float elem_f32(const T* p, size_t i);
 template <> __device__ __forceinline__ float elem_f32<float>(const float* p, size_t i) {
@@ -49,63 +25,6 @@ template <> __device__ __forceinline__ float elem_f32<float>(const float* p, siz
 }
 template <> __device__ __forceinline__ float elem_f32<bf16_t>(const bf16_t* p, size_t i) {
   return bf16_to_f32(p[i]);
-}
-
-// ---------------------------------------------------------------------------
-// Passage keys.  Workgroup = (column slice of 64 lanes x 16 bytes, passage);
-// wave w sums tokens w, w+4, ...; the four partial sums are combined in wave
-// order through LDS.
-template <typename T>
-__global__ void __launch_bounds__(256)
-passage_keys_kernel(const T* __restrict__ Kh, const int32_t* __restrict__ passage_offsets,
-                    int d, int total_tokens, double* __restrict__ kbar) {
-  constexpr int VEC = GVec<T>::n;
-  __shared__ double part[4][64][VEC];
-  const int pj = blockIdx.y;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int c = (blockIdx.x * 64 + lane) * VEC;
-  int t0, t1;
-  range_of(passage_offsets, pj, total_tokens, t0, t1);
-  double acc[VEC];
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) acc[e] = 0.0;
-  if (c < d) {
-    int t = t0 + wave;
-    for (; t + 12 < t1; t += 16) {
-      u32x4 x[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        x[q] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(Kh + (size_t)(t + 4 * q) * d + c));
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        double v[VEC];
-        unpack_f64<T>(x[q], v);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += v[e];
-      }
-    }
-    for (; t < t1; t += 4) {
-      u32x4 x = *reinterpret_cast<const u32x4*>(Kh + (size_t)t * d + c);
-      double v[VEC];
-      unpack_f64<T>(x, v);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] += v[e];
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) part[wave][lane][e] = acc[e];
-  __syncthreads();
-  if (wave == 0 && c < d) {
-    const int L = t1 - t0;
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      const double s = ((part[0][lane][e] + part[1][lane][e]) + part[2][lane][e]) +
-                       part[3][lane][e];
-      kbar[(size_t)pj * d + c + e] = (L > 0) ? s / (double)L : 0.0;
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -351,16 +270,8 @@ hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
                                const int32_t* passage_offsets, double* kbar,
                                hipStream_t s) {
   if (p.total_passages <= 0) return hipSuccess;
-  if (p.dtype == SKIP_F32) {
-    dim3 grid((p.d + 255) / 256, p.total_passages);
-    hipLaunchKernelGGL(passage_keys_kernel<float>, grid, dim3(256), 0, s,
-                       (const float*)Kh, passage_offsets, p.d, p.total_tokens, kbar);
-  } else {
-    dim3 grid((p.d + 511) / 512, p.total_passages);
-    hipLaunchKernelGGL(passage_keys_kernel<bf16_t>, grid, dim3(256), 0, s,
-                       (const bf16_t*)Kh, passage_offsets, p.d, p.total_tokens, kbar);
-  }
-  return hipGetLastError();
+  return launch_pools(p.dtype, p.d, nullptr, nullptr, 0, 0, nullptr, nullptr, Kh,
+                      passage_offsets, p.total_passages, p.total_tokens, kbar, s);
 }
 
 int edge_slices(const skip_problem_t& p) { return (p.d + kEdSlice - 1) / kEdSlice; }

@@ -1,7 +1,8 @@
 // Stage 1 of the routing core: question-guided visual token pruning
 // (paper App. B.1, Def. B.1; Alg. 1, scoring and TopK steps).
 //
-//   pool_question : u_b = mean(Q_b rows) / sqrt(d) + w          (float64)
+//   pool_question : u_b = mean(Q_b rows) / sqrt(d) + w          (float64,
+//                   the row-range mean kernel shared with the passage keys)
 //   score         : z_{b,i} = <u_b, V[b,i]>, s = sigmoid(z)     (float64 sums)
 //   topk          : the k_b largest z of question b, lowest index on ties,
 //                   written in ascending index order
@@ -12,6 +13,7 @@
 // chunks in flight per lane, against u_b staged once per workgroup in LDS.
 #include "skip_common.h"
 #include "skip_internal.h"
+#include "skip_pool.h"
 #include "skip_select.h"
 
 namespace skip {
@@ -41,48 +43,12 @@ __device__ __forceinline__ void unpack16<bf16_t>(const u32x4& x, double* out) {
   out[7] = (double)bf16_to_f32(x.w >> 16);
 }
 
-template <typename T> __device__ __forceinline__ double elem_f64(const T* p, size_t i);
-template <> __device__ __forceinline__ double elem_f64<float>(const float* p, size_t i) {
-  return (double)p[i];
-}
-template <> __device__ __forceinline__ double elem_f64<bf16_t>(const bf16_t* p, size_t i) {
-  return (double)bf16_to_f32(p[i]);
-}
-
-// ---------------------------------------------------------------------------
-// u_b[c] = (sum_t Q_b[t][c]) / T_b / sqrt(d) + w[c]; one thread per column.
-template <typename T>
-__global__ void __launch_bounds__(256)
-pool_question_kernel(const T* __restrict__ Qtok, const int32_t* __restrict__ q_offsets,
-                     const T* __restrict__ w_bias, int d, int total_qtok,
-                     double* __restrict__ u) {
-  const int b = blockIdx.y;
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= d) return;
-  int t0, t1;
-  range_of(q_offsets, b, total_qtok, t0, t1);
-  double s = 0.0;
-  int t = t0;
-  for (; t + 8 <= t1; t += 8) {        // eight independent loads, summed in order
-    double v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = elem_f64(Qtok, (size_t)(t + u) * d + c);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) s += v[u];
-  }
-  for (; t < t1; ++t) s += elem_f64(Qtok, (size_t)t * d + c);
-  const double qbar = (t1 > t0) ? s / (double)(t1 - t0) : 0.0;
-  double v = qbar / sqrt((double)d);
-  if (w_bias) v += elem_f64(w_bias, (size_t)c);
-  u[(size_t)b * d + c] = v;
-}
-
 // ---------------------------------------------------------------------------
 // Streaming GEMV in float64.  Workgroup = 4 waves = kScoreRows rows of one
 // question; each wave handles kRowsPerWave rows, R at a time, U column chunks
 // (of 64 lanes x 16 bytes) in flight per row.
-constexpr int kScoreRows = 32;
-constexpr int kScoreR = 4;
+constexpr int kScoreRows = 24;
+constexpr int kScoreR = 6;
 constexpr int kScoreU = 4;
 
 template <typename T>
@@ -221,16 +187,8 @@ gather_kernel(const T* __restrict__ V, const int32_t* __restrict__ kept_offsets,
 hipError_t launch_pool_question(const skip_problem_t& p, const void* Qtok,
                                 const int32_t* q_offsets, const void* w_bias,
                                 double* u, hipStream_t s) {
-  dim3 grid((p.d + 255) / 256, p.B);
-  if (p.dtype == SKIP_F32)
-    hipLaunchKernelGGL(pool_question_kernel<float>, grid, dim3(256), 0, s,
-                       (const float*)Qtok, q_offsets, (const float*)w_bias, p.d,
-                       p.total_qtok, u);
-  else
-    hipLaunchKernelGGL(pool_question_kernel<bf16_t>, grid, dim3(256), 0, s,
-                       (const bf16_t*)Qtok, q_offsets, (const bf16_t*)w_bias, p.d,
-                       p.total_qtok, u);
-  return hipGetLastError();
+  return launch_pools(p.dtype, p.d, Qtok, q_offsets, p.B, p.total_qtok, w_bias, u, nullptr,
+                      nullptr, 0, 0, nullptr, s);
 }
 
 hipError_t launch_score(const skip_problem_t& p, const void* V, const double* u,

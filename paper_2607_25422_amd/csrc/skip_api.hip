@@ -6,6 +6,7 @@
 
 #include "skip.h"
 #include "skip_internal.h"
+#include "skip_pool.h"
 
 namespace skip {
 namespace {
@@ -217,14 +218,16 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
   const bool work = p->total_kept > 0;
   QuerySource q{V, kept_idx, p->N};
   SKIP_TRY(mark());
-  if (work) SKIP_TRY(launch_pool_question(*p, Qtok, q_offsets, w_bias, w.u, s));
+  // question pooling and (unless given) passage-key pooling in one launch
+  if (work) {
+    const int np = passage_keys ? 0 : p->total_passages;
+    SKIP_TRY(launch_pools(p->dtype, p->d, Qtok, q_offsets, p->B, p->total_qtok, w_bias, w.u,
+                          Kh, passage_offsets, np, p->total_tokens, w.kbar, s));
+  }
   SKIP_TRY(mark());
   if (work) SKIP_TRY(launch_score(*p, V, w.u, w.z, nullptr, s));
   SKIP_TRY(mark());
   if (work) SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
-  SKIP_TRY(mark());
-  if (work && !passage_keys)
-    SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
   SKIP_TRY(mark());
   if (work)
     SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,

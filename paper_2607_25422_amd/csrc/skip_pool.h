@@ -1,0 +1,167 @@
+// Float64 means of row ranges of a [rows][d] matrix (internal to libskip.so):
+// the mean-pooled question (paper Sec. 3.3, Def. B.2; Def. B.1 scoring
+// vector) and the pooled passage keys (Def. B.3).
+#pragma once
+
+#include "skip_common.h"
+
+namespace skip {
+
+template <typename T> struct GVec;
+template <> struct GVec<float> { static constexpr int n = 4; };
+template <> struct GVec<bf16_t> { static constexpr int n = 8; };
+
+template <typename T>
+__device__ __forceinline__ void unpack_f64(const u32x4& x, double* out);
+template <>
+__device__ __forceinline__ void unpack_f64<float>(const u32x4& x, double* out) {
+  out[0] = (double)__uint_as_float(x.x);
+  out[1] = (double)__uint_as_float(x.y);
+  out[2] = (double)__uint_as_float(x.z);
+  out[3] = (double)__uint_as_float(x.w);
+}
+template <>
+__device__ __forceinline__ void unpack_f64<bf16_t>(const u32x4& x, double* out) {
+  out[0] = (double)bf16_to_f32(x.x & 0xffffu);
+  out[1] = (double)bf16_to_f32(x.x >> 16);
+  out[2] = (double)bf16_to_f32(x.y & 0xffffu);
+  out[3] = (double)bf16_to_f32(x.y >> 16);
+  out[4] = (double)bf16_to_f32(x.z & 0xffffu);
+  out[5] = (double)bf16_to_f32(x.z >> 16);
+  out[6] = (double)bf16_to_f32(x.w & 0xffffu);
+  out[7] = (double)bf16_to_f32(x.w >> 16);
+}
+
+// Workgroup = (column slice of 64 lanes x kPoolChunks x 16 bytes, range);
+// wave w sums rows w, w+4, ... (four rows, two 16-byte chunks each, in flight
+// per lane); the four partial sums are combined in wave order through LDS.
+// One launch serves two independent sets of ranges: the questions (ranges
+// 0..nq-1 of Qtok, written as the scoring vector u = mean / sqrt(d) + w) and
+// the passages (the following ranges of Kh, written as their mean), so the
+// short question pooling runs alongside the passage stream.
+constexpr int kPoolChunks = 2;
+
+template <typename T>
+struct PoolRanges {
+  const T* src;
+  const int32_t* offsets;
+  int n;            // ranges
+  int total;        // rows of src
+  double* out;      // [n][d]
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) {
+  constexpr int VEC = GVec<T>::n;
+  constexpr int CH = kPoolChunks;
+  __shared__ double part[4][64][CH * VEC];
+  const bool question = (int)blockIdx.y < qr.n;
+  const PoolRanges<T> rg = question ? qr : pr;
+  const int j = question ? (int)blockIdx.y : (int)blockIdx.y - qr.n;
+  const T* __restrict__ src = rg.src;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int cc[CH];                            // first column of each chunk
+  bool ok[CH];
+#pragma unroll
+  for (int h = 0; h < CH; ++h) {
+    cc[h] = ((blockIdx.x * CH + h) * 64 + lane) * VEC;
+    ok[h] = cc[h] < d;
+  }
+  int t0, t1;
+  range_of(rg.offsets, j, rg.total, t0, t1);
+  double acc[CH][VEC];
+#pragma unroll
+  for (int h = 0; h < CH; ++h)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[h][e] = 0.0;
+  int t = t0 + wave;
+  for (; t + 12 < t1; t += 16) {
+    u32x4 x[4][CH];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h = 0; h < CH; ++h)
+        x[q][h] = ok[h] ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+                              src + (size_t)(t + 4 * q) * d + cc[h]))
+                        : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h = 0; h < CH; ++h) {
+        double v[VEC];
+        unpack_f64<T>(x[q][h], v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[h][e] += v[e];
+      }
+  }
+  for (; t < t1; t += 4) {
+#pragma unroll
+    for (int h = 0; h < CH; ++h) {
+      if (!ok[h]) continue;
+      u32x4 x = *reinterpret_cast<const u32x4*>(src + (size_t)t * d + cc[h]);
+      double v[VEC];
+      unpack_f64<T>(x, v);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[h][e] += v[e];
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < CH; ++h)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) part[wave][lane][h * VEC + e] = acc[h][e];
+  __syncthreads();
+  if (wave != 0) return;
+  const int L = t1 - t0;
+  const double rsd = 1.0 / sqrt((double)d);
+#pragma unroll
+  for (int h = 0; h < CH; ++h) {
+    if (!ok[h]) continue;
+    double wv[VEC];
+    if (question && w) {
+      unpack_f64<T>(*reinterpret_cast<const u32x4*>(w + cc[h]), wv);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) wv[e] = 0.0;
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int i = h * VEC + e;
+      const double s = ((part[0][lane][i] + part[1][lane][i]) + part[2][lane][i]) +
+                       part[3][lane][i];
+      double m = (L > 0) ? s / (double)L : 0.0;
+      if (question) m = m * rsd + wv[e];
+      rg.out[(size_t)j * d + cc[h] + e] = m;
+    }
+  }
+}
+
+// Questions (Qtok by q_offsets -> u, nq ranges) and passages (Kh by
+// passage_offsets -> kbar, np ranges); either set may be empty.
+inline hipError_t launch_pools(int dtype, int d, const void* Qtok, const int32_t* q_offsets,
+                               int nq, int total_qtok, const void* w, double* u,
+                               const void* Kh, const int32_t* passage_offsets, int np,
+                               int total_tokens, double* kbar, hipStream_t s) {
+  if (nq + np <= 0) return hipSuccess;
+  if (dtype == SKIP_F32) {
+    dim3 grid((d + 256 * kPoolChunks - 1) / (256 * kPoolChunks), nq + np);
+    hipLaunchKernelGGL(pool_kernel<float>, grid, dim3(256), 0, s,
+                       PoolRanges<float>{(const float*)Qtok, q_offsets, nq, total_qtok, u},
+                       (const float*)w,
+                       PoolRanges<float>{(const float*)Kh, passage_offsets, np, total_tokens,
+                                         kbar},
+                       d);
+  } else {
+    dim3 grid((d + 512 * kPoolChunks - 1) / (512 * kPoolChunks), nq + np);
+    hipLaunchKernelGGL(pool_kernel<bf16_t>, grid, dim3(256), 0, s,
+                       PoolRanges<bf16_t>{(const bf16_t*)Qtok, q_offsets, nq, total_qtok, u},
+                       (const bf16_t*)w,
+                       PoolRanges<bf16_t>{(const bf16_t*)Kh, passage_offsets, np,
+                                          total_tokens, kbar},
+                       d);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace skip
