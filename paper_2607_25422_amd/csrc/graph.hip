@@ -42,6 +42,7 @@ template <> __device__ __forceinline__ float elem_f32<bf16_t>(const bf16_t* p, s
 constexpr int kEdRows = 64;
 constexpr int kEdPT = 16;
 constexpr int kEdSlice = 512;
+constexpr int kEdSteps = 4;
 
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
@@ -95,31 +96,38 @@ edge_dot_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_id
 
   f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
   double qq = 0.0, k2 = 0.0;
-  for (int c0 = c_begin; c0 < c_end; c0 += 32) {
-    const int c = c0 + 8 * kk;
-    const bool in = c < c_end;                 // d is a multiple of 8
-    double qa[8], kv[8];
-    load8_f64<T>(qrow + c, row_ok && in, qa);
-    if (pkeys) {
-      load8_f64<float>(pkeys + krow + c, key_ok && in, kv);
-    } else if (key_ok && in) {
-      const double2* kp = reinterpret_cast<const double2*>(kbar + krow + c);
+  // kEdSteps 32-column steps per iteration: every load of the iteration is
+  // issued before the first product, so each wave waits once per 128 columns.
+  for (int c0 = c_begin; c0 < c_end; c0 += 32 * kEdSteps) {
+    double qa[kEdSteps][8], kv[kEdSteps][8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const double2 t = kp[q];
-        kv[2 * q] = t.x;
-        kv[2 * q + 1] = t.y;
+    for (int st = 0; st < kEdSteps; ++st) {
+      const int c = c0 + 32 * st + 8 * kk;
+      const bool in = c < c_end;               // d is a multiple of 8
+      load8_f64<T>(qrow + c, row_ok && in, qa[st]);
+      if (pkeys) {
+        load8_f64<float>(pkeys + krow + c, key_ok && in, kv[st]);
+      } else if (key_ok && in) {
+        const double2* kp = reinterpret_cast<const double2*>(kbar + krow + c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const double2 t = kp[q];
+          kv[st][2 * q] = t.x;
+          kv[st][2 * q + 1] = t.y;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kv[st][e] = 0.0;
       }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kv[e] = 0.0;
     }
 #pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[m], kv[m], acc, 0, 0, 0);
-      qq = fma(qa[m], qa[m], qq);
-      k2 = fma(kv[m], kv[m], k2);
-    }
+    for (int st = 0; st < kEdSteps; ++st)
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[st][m], kv[st][m], acc, 0, 0, 0);
+        qq = fma(qa[st][m], qa[st][m], qq);
+        k2 = fma(kv[st][m], kv[st][m], k2);
+      }
   }
   // lanes l16, l16+16, l16+32, l16+48 hold the four column slots of one row/key
   qq += __shfl_xor(qq, 16, 64);
