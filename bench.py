@@ -44,6 +44,8 @@ def parse():
                     help="questions of the batch the CPU oracle is timed on (0: skip)")
     ap.add_argument("--pass-keys", action="store_true",
                     help="hand precomputed passage keys to the library (skips pooling)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip measuring the box's streaming and GEMM ceilings")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run an elementwise copy (negation) of MIB MiB of "
                          "float32 three times, so a hardware-counter pass can scale "
@@ -53,6 +55,41 @@ def parse():
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel.highres_bf16.traffic.json")
 ATTN_SOURCE = os.path.join(ROOT, "paper_2607_25422_amd", "csrc", "attn.hip")
+
+
+def measure_ceilings(torch) -> dict:
+    """Attainable rates on this GPU, beside the published peaks: an elementwise
+    copy (negation, 1 GiB in and out), a column sum reading 1 GiB of bf16, and
+    a 16384^3 bf16 GEMM (hipBLASLt through torch.matmul)."""
+    def timed(fn, it):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(it):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / it
+    n = 1 << 30
+    a = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    copy = 2 * n / timed(lambda: torch.neg(a, out=b), 10) / 1e9
+    del a, b
+    c = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda").view(-1, 4096)
+    read = n / timed(lambda: c.sum(0, dtype=torch.float32), 10) / 1e9
+    del c
+    m = 16384
+    x = torch.randn(m, m, dtype=torch.bfloat16, device="cuda")
+    y = torch.randn(m, m, dtype=torch.bfloat16, device="cuda")
+    gemm = 2 * m ** 3 / timed(lambda: x @ y, 5) / 1e12
+    del x, y
+    torch.cuda.empty_cache()
+    return {"copy_gbs": round(copy, 1), "read_gbs": round(read, 1),
+            "gemm_bf16_tflops": round(gemm, 1),
+            "what": "negation copy of 1 GiB float32; column sum of 1 GiB bf16; "
+                    "16384^3 bf16 GEMM (torch.matmul)"}
 
 
 def measured_traffic(workload: str):
@@ -213,6 +250,12 @@ def main():
         },
         "stages_ms": {k: round(v, 5) for k, v in stages.items()},
     }
+
+    if not args.no_ceilings:
+        ceil = measure_ceilings(torch)
+        res["ceilings"] = ceil
+        res["roofline"]["frac_of_read_ceiling"] = round(attn_gbs / ceil["read_gbs"], 4)
+        res["prune"]["score_frac_of_read_ceiling"] = round(score_gbs / ceil["read_gbs"], 4)
 
     if args.cpu_sample > 0:
         from threadpoolctl import threadpool_limits
