@@ -200,22 +200,25 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   // Q^T fragments (B operand): row `col`, features kb*16 + 8*hh .. +7.
   u32x4 qf[KB];
   {
-    const bf16_t* qrow = nullptr;
-    if (row_ok) {
-      if (kept_idx) {
-        const int src = clampi(kept_idx[k0 + r], 0, N - 1);
-        qrow = qbase + ((size_t)b * N + src) * qstride + (size_t)h * D;
-      } else {
-        qrow = qbase + (size_t)(k0 + r) * qstride + (size_t)h * D;
-      }
+    // A lane past the block's rows reads the question's first kept row (the
+    // item has at least one) and zeroes it, so all loads issue together.
+    const int rr = row_ok ? r : 0;
+    const bf16_t* qrow;
+    if (kept_idx) {
+      const int src = clampi(kept_idx[k0 + rr], 0, N - 1);
+      qrow = qbase + ((size_t)b * N + src) * qstride + (size_t)h * D;
+    } else {
+      qrow = qbase + (size_t)(k0 + rr) * qstride + (size_t)h * D;
     }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+      qf[kb] = *reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh);
     // a negative scale is folded in here (bf16 sign flips), so the logits
     // below are always scaled by |scale|
     const uint32_t neg = (scale_log2 < 0.f) ? 0x80008000u : 0u;
+    const uint32_t keep = row_ok ? 0xffffffffu : 0u;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-      qf[kb] = row_ok ? (*reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh) ^ neg)
-                      : u32x4{0u, 0u, 0u, 0u};
+    for (int kb = 0; kb < KB; ++kb) qf[kb] = (qf[kb] ^ neg) & keep;
     // Settle the query loads here: left pending, the compiler would wait for
     // them (vmcnt(0)) inside the tile loop, draining the prefetch ring.
 #pragma unroll
