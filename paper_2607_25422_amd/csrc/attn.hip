@@ -5,22 +5,19 @@
 // every passage adjacent to i (one 64-bit neighbour mask per row):
 //   e_m = sm_scale * <Qh[i,h], Kh[m,h]>,  O = softmax(e) . Vh,  LSE = log sum exp e.
 //
-// bf16 path (MFMA).  Work item = (question b, head h, block of 128 kept rows):
-// four waves, 32 rows each.  The item walks the passages adjacent to any of
-// its rows, 64 tokens at a time.  K and V tiles of head h are staged once per
-// item in LDS and shared by all 128 rows; the next tile is prefetched into
-// registers while the current one is consumed.  Per wave:
-//   S^T (64 tokens x 32 rows) = K_tile (64 x d_h) . Q^T   v_mfma_f32_32x32x16_bf16
-//   rows not adjacent to the passage are masked to -inf (a wave with no
-//   adjacent row skips the tile), online softmax in fp32 (base-2 exponent),
-//   P rounded to bf16,
-//   O^T (d_h x 32 rows) += V_tile^T . P^T                v_mfma_f32_32x32x16_bf16
+// bf16 path (MFMA).  Work item = (question b, head h, block of <= 256 kept
+// rows), eight waves.  The item walks the passages adjacent to any of its
+// rows, 64 tokens at a time; K and V tiles of head h are staged once per item
+// in an LDS ring and shared by all rows.  Per wave and tile:
+//   S^T (tokens x 32 rows) = K_tile (tokens x d_h) . Q^T   v_mfma_f32_32x32x16_bf16
+//   rows not adjacent to the passage are masked to -inf, online softmax in
+//   fp32 (base-2 exponent), P rounded to bf16,
+//   O^T (d_h x 32 rows) += V_tile^T . P^T                  v_mfma_f32_32x32x16_bf16
 // Computing the transposed products keeps each query row in one lane column,
 // so row statistics need no cross-lane traffic except between the two half
 // waves, and the S^T accumulator is already the P^T operand of the second
-// product.  V is written to LDS transposed, with tokens permuted inside each
-// 16-token block to match the S^T accumulator layout, so every MFMA operand
-// is one 16-byte LDS read.
+// product.  The V^T operand comes from transposing LDS reads in the token
+// order of the S^T accumulator layout.
 //
 // Work items are laid out so that the row blocks of one (b, h) land on the
 // same XCD (workgroups are dealt round-robin over the 8 XCDs), which keeps
@@ -36,6 +33,10 @@ namespace skip {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
+template <int N>
+struct IntC {                     // a compile-time count passed to a generic lambda
+  static constexpr int value = N;
+};
 
 constexpr int kWaves = 8;                 // waves per work item
 constexpr int kThreads = 64 * kWaves;
@@ -152,6 +153,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   // four consecutive tokens on distinct banks.
   auto vswz = [](int row) { return (NCH >= 16 ? 4 : 2) * (row & 3); };
   static_assert(NI % kLoaders == 0, "tile loads must divide over the loading waves");
+  static_assert(2 * (DT * 16 + 2) * 64 * 4 <= kStages * TILE * 2,
+                "the merge of split blocks reuses the K ring");
   __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kStages * TILE];
   __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kStages * TILE];
   __shared__ uint64_t wave_union[kWaves];
@@ -181,8 +184,26 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
   const int wave = tid >> 6;
   const int col = lane & 31;         // query row within the wave
   const int hh = lane >> 5;          // half wave
-  const int r = row0 + wave * 32 + col;
-  const bool row_ok = r < row_end;
+  // Waves w and w+4 share a SIMD.  A wave takes one 32-row block over whole
+  // tiles, or one 32-token half of every tile of a block (its partner, wave
+  // w^1, takes the other half; the two merge once at the end).  Halves are
+  // used where they even out the rows per SIMD: 5-6 blocks (waves 4-7 split
+  // blocks 4 and 5: 48 rows per SIMD instead of 64) and 1-2 blocks (one
+  // block over two SIMDs).
+  const int nrb = (row_end - row0 + 31) / 32;
+  int wb = wave, half = -1;          // wave's row block; half < 0: whole tiles
+  if (nrb <= 2) {
+    wb = wave >> 1;
+    half = wave & 1;
+  } else if ((nrb == 5 || nrb == 6) && wave >= 4) {
+    wb = 4 + ((wave - 4) >> 1);
+    half = wave & 1;
+  }
+  const bool any_split = nrb <= 2 || nrb == 5 || nrb == 6;   // uniform over the item
+  const bool split = half >= 0;
+  const int sub0 = split ? half : 0;                           // first 32-token sub-tile
+  const int r = row0 + wb * 32 + col;
+  const bool row_ok = wb < nrb && r < row_end;
 
   if (tid < P) {
     int ts, te;
@@ -304,11 +325,13 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
 
   // Matrix phase: O^T += V^T . P^T for the previous tile (weights pb/pl,
   // V tile in stage pv_stage), then S^T = K . Q^T for the tile in stage
-  // s_stage into sacc.
+  // s_stage into sacc.  NST (1 or 2) is the number of 32-token sub-tiles the
+  // wave computes, starting at sub-tile sub0.
   f32x16_t sacc[2];
   u32x4 pb[4], pl[4];
   float acc_scale = 1.f;             // rescale of acc owed by the last softmax
-  auto pv_product = [&](int pv_stage) {
+  auto pv_product = [&](auto nst, int pv_stage) {
+    constexpr int NST = decltype(nst)::value;
     __builtin_amdgcn_sched_barrier(0);
     if (__any(acc_scale != 1.f)) {   // some row's maximum moved
 #pragma unroll
@@ -316,34 +339,52 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[dt][v] *= acc_scale;
     }
-    const bf16_t* Vs = Vbuf + pv_stage * TILE;
+    const bf16_t* Vs = Vbuf + pv_stage * TILE + sub0 * 32 * D;
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
+    for (int hf = 0; hf < NST; ++hf) {
       u32x4 va[DT][2];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
-          const bf16_t* vp = Vs + (32 * half + 16 * g) * D + voff[dt];
+          const bf16_t* vp = Vs + (32 * hf + 16 * g) * D + voff[dt];
           va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
                                               0, 1, 2, 3);
         }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        acc[dt] = mfma32(va[dt][0], pb[2 * half], acc[dt]);
-        acc[dt] = mfma32(va[dt][1], pb[2 * half + 1], acc[dt]);
+        acc[dt] = mfma32(va[dt][0], pb[2 * hf], acc[dt]);
+        acc[dt] = mfma32(va[dt][1], pb[2 * hf + 1], acc[dt]);
         if (SPLIT_P) {
-          acc[dt] = mfma32(va[dt][0], pl[2 * half], acc[dt]);
-          acc[dt] = mfma32(va[dt][1], pl[2 * half + 1], acc[dt]);
+          acc[dt] = mfma32(va[dt][0], pl[2 * hf], acc[dt]);
+          acc[dt] = mfma32(va[dt][1], pl[2 * hf + 1], acc[dt]);
         }
       }
     }
-  };
-  auto s_product = [&](int s_stage) {
-    __builtin_amdgcn_sched_barrier(0);
-    const bf16_t* Ks = Kbuf + s_stage * TILE;
+    // Schedule: sixteen V^T reads ahead, then one MFMA (two with the split
+    // weights) per two reads, so the read latency hides behind the matrix
+    // pipe (left alone, the compiler waits for every operand pair in turn).
+    {
+      constexpr int R = NST * 4 * DT;
+      constexpr int MPS = SPLIT_P ? 2 : 1;
+      constexpr int M = NST * 2 * DT * MPS;
+      constexpr int PRE = R < 16 ? R : 16;
+      constexpr int STEPS = (R - PRE) / 2;
+      __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);   // LDS reads
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+      for (int i = 0; i < STEPS; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, MPS, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, M - STEPS * MPS, 0);
+    }
+  };
+  auto s_product = [&](auto nst, int s_stage) {
+    constexpr int NST = decltype(nst)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    const bf16_t* Ks = Kbuf + s_stage * TILE + sub0 * 32 * D;
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
       u32x4 ka[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
@@ -353,11 +394,25 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) sacc[st] = mfma32(ka[kb], qf[kb], sacc[st]);
     }
+    // Schedule: eight K reads ahead (all of them for one sub-tile at d_h 64),
+    // then one MFMA per read.
+    {
+      constexpr int R = NST * KB;
+      constexpr int PRE = R < 8 ? R : 8;
+      __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);
+#pragma unroll
+      for (int i = 0; i < R - PRE; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, PRE, 0);
+    }
   };
-  // Vector phase: online softmax over the 32 scores of this lane's row in
-  // sacc (tile with `full`, `rem`, adjacency bias `mbias`); rescales acc and
+  // Vector phase: online softmax over the scores of this lane's row in sacc
+  // (sub-tiles with `full`, `rem`, adjacency bias `mbias`); rescales acc and
   // leaves the bf16 weights in pb (and their remainders in pl).
-  auto softmax = [&](bool full, int rem, float mbias) {
+  auto softmax = [&](auto nst, bool full, int rem, float mbias) {
+    constexpr int NST = decltype(nst)::value;
     __builtin_amdgcn_sched_barrier(0);
     // (a negative scale was folded into the query fragments: c > 0)
     const float c = fabsf(scale_log2);
@@ -365,14 +420,14 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
       // kept as a branch: selecting on every tile would cost 64 VALU ops
       asm volatile("");
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
+      for (int st = 0; st < NST; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v)
           if (32 * st + 8 * (v >> 2) + (v & 3) >= rem) sacc[st][v] = -INFINITY;
     }
     float sm = sacc[0][0];
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
+    for (int st = 0; st < NST; ++st)
 #pragma unroll
       for (int v = 0; v < 16; ++v) sm = fmaxf(sm, sacc[st][v]);
     sm = fmaxf(sm, swap_halves(sm));
@@ -383,7 +438,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     m_run = m_new;
     float ls = 0.f;
 #pragma unroll
-    for (int kb2 = 0; kb2 < 4; ++kb2) {
+    for (int kb2 = 0; kb2 < 2 * NST; ++kb2) {
       float pv[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -435,24 +490,15 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
     else if (ahead == 1) wait_vmem<LPT>();
     else wait_vmem<0>();
   };
-  if (!busy) {
-    // A wave without kept rows only keeps step with the barriers (and, in
-    // group A, streams its share of the tiles).
-    for (int i = 0; advance(cc); ++i) {
-      if (!group_b) wait_tile(issued - i - 1);
-      barrier_nofence();
-      if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
-      barrier_nofence();
-    }
-  } else {
+  // Step i: PV of tile i-1 (zero weights at i = 0), S and softmax of tile i;
+  // a final step past the last tile does only the PV.
+  auto busy_loop = [&](auto nst) {
     // The first matrix phase adds tile 0's V with zero weights (exactly 0).
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       pb[q] = u32x4{0u, 0u, 0u, 0u};
       pl[q] = u32x4{0u, 0u, 0u, 0u};
     }
-    // Step i: PV of tile i-1 (zero weights at i = 0), S and softmax of tile
-    // i; a final step past the last tile does only the PV.
     int prev_stage = 0;
     for (int i = 0;; ++i) {
       const bool more = advance(cc);
@@ -462,19 +508,67 @@ attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ k
         barrier_nofence();
         if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
       }
-      pv_product(prev_stage);
+      pv_product(nst, prev_stage);
       if (!more) break;
       const int stage = i % kStages;
-      s_product(stage);
+      s_product(nst, stage);
       barrier_nofence();
       // accumulator element v of sub-tile st is token 32*st + 8*(v/4) + v%4
-      // + 4*hh of the tile; it exists if that is below rem
-      softmax(cc.t + kTile <= cc.te, cc.te - cc.t - 4 * hh,
+      // + 4*hh of the wave's first sub-tile; it exists if that is below rem
+      const int t0 = cc.t + 32 * sub0;
+      softmax(nst, t0 + 32 * decltype(nst)::value <= cc.te, cc.te - t0 - 4 * hh,
               ((mrow >> cc.j) & 1ull) ? 0.f : -INFINITY);
       prev_stage = stage;
     }
+  };
+  if (!busy) {
+    // A wave without kept rows only keeps step with the barriers (and, in
+    // group A, streams its share of the tiles).
+    for (int i = 0; advance(cc); ++i) {
+      if (!group_b) wait_tile(issued - i - 1);
+      barrier_nofence();
+      if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
+      barrier_nofence();
+    }
+  } else if (split) {
+    busy_loop(IntC<1>{});
+  } else {
+    busy_loop(IntC<2>{});
   }
   if (!group_b) barrier_nofence();
+
+  // Merge the two halves of a split block (online-softmax combination):
+  // the upper half's wave hands (acc, m, l) over through the LDS ring.
+  if (any_split) {
+    __syncthreads();                 // every wave is done with the ring
+    // a pair's slot: blocks 0/1 (1-2 blocks) or 4/5 (5-6 blocks) use slots 0/1
+    float* xb = reinterpret_cast<float*>(Kbuf) + (wb & 1) * (DT * 16 + 2) * 64;
+    const bool paired = split && wb < nrb;   // waves past the last block hold no rows
+    if (paired && half == 1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) xb[(dt * 16 + v) * 64 + lane] = acc[dt][v];
+      xb[(DT * 16) * 64 + lane] = m_run;
+      xb[(DT * 16 + 1) * 64 + lane] = l_run;
+    }
+    __syncthreads();
+    if (paired && half == 1) return;
+    if (paired) {
+      const float m1 = xb[(DT * 16) * 64 + lane];
+      const float l1 = xb[(DT * 16 + 1) * 64 + lane];
+      const float M = fmaxf(m_run, m1);
+      const float a0 = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - M);
+      const float a1 = (m1 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          acc[dt][v] = acc[dt][v] * a0 + xb[(dt * 16 + v) * 64 + lane] * a1;
+      l_run = l_run * a0 + l1 * a1;
+      m_run = M;
+    }
+  }
 
   // finalize
   const float l_tot = l_run + swap_halves(l_run);

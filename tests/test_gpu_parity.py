@@ -225,6 +225,32 @@ def test_xattn_given_graph_and_keys(B, dtype):
     check_attention(f64(O2), f64(L2), np.concatenate(O2_ref), np.concatenate(L2_ref), dtype, "keys")
 
 
+# Kept-row counts that give every layout of a work item's rows: 1-8 blocks of
+# 32 rows (the item splits 1-2 and 5-6 blocks into token halves merged at the
+# end), and two items per question above 256 rows.
+ROW_COUNTS = (1, 31, 33, 64, 65, 129, 160, 161, 193, 224, 256, 300, 450, 512)
+
+
+@pytest.mark.parametrize("d_h", [64, 128])
+@pytest.mark.parametrize("k", ROW_COUNTS)
+def test_xattn_row_block_layouts(B, k, d_h):
+    batch = wls.make_batch("llava_bf16", 7, B=3, N=520, H=2, d_h=d_h, T=4, k=(k,),
+                           P=(3, 5), L_p=(40, 64, 100))
+    say(f"xattn layouts k={k} d_h={d_h} P={batch.P.tolist()}")
+    Qh = queries_from_batch(batch)
+    _, adj, O_ref, L_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, 2.0)
+    O_ref, L_ref = np.concatenate(O_ref), np.concatenate(L_ref)
+    for f32_out in (False, True):
+        db = B.to_device(batch, avg_degree=2.0, o_f32=f32_out)
+        O, L, rp, col = B.bipartite_xattn(db, Qh.cuda())
+        torch.cuda.synchronize()
+        check_graph(batch, rp, col, adj)
+        check_attention(f64(O), f64(L), O_ref, L_ref, "bf16", f"k={k} f32out={f32_out}",
+                        stored_bf16=not f32_out)
+
+
 # --------------------------------------------------------------------------- fused
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
