@@ -44,6 +44,12 @@ def parse():
                     help="questions of the batch the CPU oracle is timed on (0: skip)")
     ap.add_argument("--avg-degree", type=float, default=None,
                     help="override the workload's average degree (edges per kept row)")
+    ap.add_argument("--edge-rule", default="question", choices=["question", "row", "fraction"],
+                    help="edge cut: per-question budget (default), per-row top, top fraction")
+    ap.add_argument("--edge-metric", default="cosine", choices=["cosine", "dot"],
+                    help="edge compatibility: cosine (default) or scaled dot product")
+    ap.add_argument("--edge-beta", type=float, default=0.1,
+                    help="kept fraction of the pairs for --edge-rule fraction")
     ap.add_argument("--cold", action="store_true",
                     help="overwrite a 1 GiB buffer before every timed step so that no input "
                          "is left in the on-die cache; value then comes from the event-timed "
@@ -142,7 +148,8 @@ def main():
     print(f"[bench] generating {args.workload} seed {args.seed}", file=sys.stderr, flush=True)
     batch = wls.make_batch(args.workload, args.seed, threads=16)
     wl = batch.wl
-    db = B.to_device(batch, avg_degree=args.avg_degree)
+    db = B.to_device(batch, avg_degree=args.avg_degree, edge_rule=args.edge_rule,
+                     edge_metric=args.edge_metric, edge_beta=args.edge_beta)
     p = db.p
     avg_degree = wl.avg_degree if args.avg_degree is None else args.avg_degree
     elem = 4 if wl.dtype == "f32" else 2
@@ -242,7 +249,9 @@ def main():
                    "passages": int(batch.P[0]) if len(set(batch.P.tolist())) == 1 else "mixed",
                    "L_p": wl.L_p, "H": p.H, "d_h": p.d_h, "avg_degree": avg_degree,
                    "seed": args.seed, "passage_keys": "given" if pkeys is not None else "pooled",
-                   "cache": "cold" if args.cold else "warm"},
+                   "cache": "cold" if args.cold else "warm", "edge_rule": args.edge_rule,
+                   "edge_metric": args.edge_metric,
+                   **({"edge_beta": args.edge_beta} if args.edge_rule == "fraction" else {})},
         "step_gpu_ms": {"p10": round(pct(0.1), 5), "p50": round(pct(0.5), 5),
                         "p90": round(pct(0.9), 5)},
         "roofline": {
@@ -295,7 +304,8 @@ def main():
             orc.route(batch.V, batch.Qtok, batch.q_offsets, batch.kept_offsets, batch.Kh,
                       batch.Vh, batch.passage_offsets, batch.query_passages, wl.scale,
                       avg_degree, passage_key_table=None if pkeys is None else pkeys.cpu(),
-                      queries=qs)
+                      queries=qs, edge_rule=args.edge_rule, edge_metric=args.edge_metric,
+                      edge_beta=args.edge_beta)
             c1 = time.perf_counter()
         res["cpu_baseline"] = {
             "value": round(len(qs) / (c1 - c0), 4),

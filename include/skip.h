@@ -18,7 +18,9 @@
  *      E_b = min(ceil(avg_degree * k_b), k_b * P_b) largest cosines of that
  *      question (ties: lower flattened index i * P_b + j first).  q_i is the
  *      row's query vector flattened over heads; kbar_j is the passage key
- *      (the mean of the passage's per-token keys unless passed in).  Then,
+ *      (the mean of the passage's per-token keys unless passed in).  Two
+ *      other cuts and one other compatibility are selectable per call
+ *      (skip_edge_rule_t, skip_edge_metric_t).  Then,
  *      per head h, row i attends over every token of its neighbour passages:
  *        e_m = sm_scale * <Qh[i,h], Kh[m,h]>,
  *        O[i,h] = sum_m softmax(e)_m Vh[m,h],  LSE[i,h] = log sum_m exp(e_m).
@@ -66,7 +68,7 @@
 extern "C" {
 #endif
 
-#define SKIP_ABI_VERSION 1
+#define SKIP_ABI_VERSION 2
 
 typedef enum skip_status {
   SKIP_OK = 0,
@@ -77,6 +79,39 @@ typedef enum skip_status {
 } skip_status_t;
 
 typedef enum skip_dtype { SKIP_F32 = 0, SKIP_BF16 = 1 } skip_dtype_t;
+
+/*
+ * How the edges of a question's bipartite graph are cut from the k_b x P_b
+ * compatibilities c_ij (all rules: ties go to the lower flattened index
+ * i * P_b + j, i.e. the lower row, then the lower passage).
+ *   SKIP_EDGE_QUESTION_BUDGET  the E_b = min(ceil(avg_degree * k_b), k_b * P_b)
+ *                              largest per question: a per-question threshold
+ *                              that holds the average degree at avg_degree
+ *                              (Def. B.3, threshold set dynamically).
+ *   SKIP_EDGE_ROW_TOP          every row keeps its min(ceil(avg_degree), P_b)
+ *                              largest (a per-row threshold).
+ *   SKIP_EDGE_TOP_FRACTION     the min(ceil(edge_beta * k_b * P_b - 1e-9),
+ *                              k_b * P_b) largest per question: top-beta
+ *                              sparsity (Sec. 3.5, the quantile form of the
+ *                              cut; the 1e-9, in double precision, keeps a
+ *                              decimal beta from rounding a whole product up).
+ */
+typedef enum skip_edge_rule {
+  SKIP_EDGE_QUESTION_BUDGET = 0,
+  SKIP_EDGE_ROW_TOP = 1,
+  SKIP_EDGE_TOP_FRACTION = 2
+} skip_edge_rule_t;
+
+/*
+ * Compatibility of kept row i and passage j (q_i: the row flattened over
+ * heads, width d; kbar_j: the passage key).
+ *   SKIP_EDGE_COSINE  cos(q_i, kbar_j), 0 when either norm is 0 (Def. B.3)
+ *   SKIP_EDGE_DOT     <q_i, kbar_j> / sqrt(d): the argument of the sigmoid
+ *                     of eq. (bsca); the sigmoid is monotone, so cutting on
+ *                     the argument keeps the same edges
+ * Both are formed from float64 sums.
+ */
+typedef enum skip_edge_metric { SKIP_EDGE_COSINE = 0, SKIP_EDGE_DOT = 1 } skip_edge_metric_t;
 
 /*
  * Host-side description of one batch of B questions (paper Sec. 3.1 problem
@@ -104,6 +139,9 @@ typedef struct skip_problem {
   double avg_degree;       /* target average degree of a kept row (paper: 4)   */
   float sm_scale;          /* logit scale (paper: 1/sqrt(d_h))                 */
   int32_t o_f32;           /* 0: O has the element type of dtype; 1: O is float */
+  int32_t edge_rule;       /* skip_edge_rule_t (0: per-question budget)        */
+  int32_t edge_metric;     /* skip_edge_metric_t (0: cosine)                   */
+  double edge_beta;        /* kept fraction for SKIP_EDGE_TOP_FRACTION, (0, 1] */
 } skip_problem_t;
 
 /* ABI version of the loaded library (SKIP_ABI_VERSION). */
@@ -192,9 +230,9 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V,
                                void* O, float* lse, void* workspace,
                                size_t workspace_bytes, void* stream);
 
-/* Kernel stages of skip_route_fused, in launch order: question pooling,
- * salience scoring, top-k, passage keys, edge cosines, edge selection,
- * attention. */
+/* Kernel stages of skip_route_fused, in launch order: pooling (questions
+ * and passage keys), salience scoring, top-k, edge compatibilities, edge
+ * selection, attention. */
 #define SKIP_FUSED_STAGES 6
 
 /*

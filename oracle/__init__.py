@@ -3,6 +3,7 @@ by the test-suite, the package smoke check and the benchmark's CPU baseline,
 never by the product path)."""
 from .skip_oracle import (  # noqa: F401
     RouteResult, adjacency_to_csr, bipartite_xattn, bsca_attention, bsca_edges,
-    cosine_matrix, edge_budget, gather_rows, mean_pool_question, passage_keys,
-    qvs_logits, qvs_scores, qvs_topk, route,
+    compatibility, cosine_matrix, dot_matrix, edge_budget, fraction_budget,
+    gather_rows, mean_pool_question, passage_keys, qvs_logits, qvs_scores, qvs_topk,
+    route, row_budget,
 )

@@ -29,7 +29,11 @@ justification in the design notes of the repository):
 * the edge threshold is set per question so that exactly
   E = min(ceil(avg_degree * k), k * P) edges survive (the paper sets the edge
   threshold "dynamically" to hold the average degree near 4); ties go to the
-  lower flattened index i * P + j;
+  lower flattened index i * P + j.  Two other cuts are available: the top
+  beta fraction of a question's pairs (the quantile form of Sec. 3.5) and a
+  per-row cut keeping min(ceil(avg_degree), P) passages per row; and one
+  other compatibility, the scaled dot product of eq. (bsca) with identity
+  projections;
 * a passage's key is the mean of its per-token keys over all heads, unless
   the caller supplies passage keys;
 * a kept token with no edge gets a zero output and log-sum-exp of -inf;
@@ -129,6 +133,30 @@ def cosine_matrix(Qrows: np.ndarray, Kbar: np.ndarray) -> np.ndarray:
     return c
 
 
+def dot_matrix(Qrows: np.ndarray, Kbar: np.ndarray) -> np.ndarray:
+    """c_ij = <q_i, k_bar_j> / sqrt(D), D the width of q_i: the argument of
+    the sigmoid in the main-text compatibility A_ij (Sec. 3.5, eq. bsca, with
+    the projections W_v, W_k taken as the identity or applied by the caller).
+    The sigmoid is monotone, so any cut on A_ij is the same cut on c_ij."""
+    Qrows = np.asarray(Qrows, dtype=np.float64)
+    Kbar = np.asarray(Kbar, dtype=np.float64)
+    c = np.zeros((Qrows.shape[0], Kbar.shape[0]))
+    scale = 1.0 / math.sqrt(Qrows.shape[1])
+    for i in range(Qrows.shape[0]):
+        for j in range(Kbar.shape[0]):
+            c[i, j] = float(Qrows[i] @ Kbar[j]) * scale
+    return c
+
+
+def compatibility(Qrows: np.ndarray, Kbar: np.ndarray, metric: str = "cosine") -> np.ndarray:
+    """Edge compatibilities by name: "cosine" (Def. B.3) or "dot" (eq. bsca)."""
+    if metric == "cosine":
+        return cosine_matrix(Qrows, Kbar)
+    if metric == "dot":
+        return dot_matrix(Qrows, Kbar)
+    raise ValueError(f"unknown edge metric {metric!r}")
+
+
 def edge_budget(k: int, P: int, avg_degree: float) -> int:
     """E = min(ceil(avg_degree * k), k * P): the number of edges that keeps
     the average degree of a kept token at avg_degree (Def. B.3 sets the edge
@@ -137,13 +165,46 @@ def edge_budget(k: int, P: int, avg_degree: float) -> int:
     return int(min(math.ceil(float(avg_degree) * k), k * P))
 
 
-def bsca_edges(c: np.ndarray, avg_degree: float) -> np.ndarray:
-    """Boolean adjacency [k, P]: the E largest cosines, ties to the lower
-    flattened index i * P + j (Def. B.3 edge rule with a per-question
-    threshold)."""
+def fraction_budget(k: int, P: int, beta: float) -> int:
+    """E = min(ceil(beta * k * P - 1e-9), k * P): top-beta sparsity, the cut
+    at the beta-quantile of the k * P compatibilities (Sec. 3.5).  The 1e-9
+    keeps a decimal beta from rounding up a whole product (0.1 * 1920 is
+    192.00000000000003 in binary floating point)."""
+    return int(min(math.ceil(float(beta) * (k * P) - 1e-9), k * P))
+
+
+def row_budget(P: int, avg_degree: float) -> int:
+    """Edges per row under a per-row cut: min(ceil(avg_degree), P)."""
+    return int(min(math.ceil(float(avg_degree)), P))
+
+
+def bsca_edges(c: np.ndarray, avg_degree: float, rule: str = "question",
+               beta: float = 0.1) -> np.ndarray:
+    """Boolean adjacency [k, P] cut from the compatibilities c (ties to the
+    lower flattened index i * P + j under every rule):
+
+    * "question": the edge_budget(k, P, avg_degree) largest of the question
+      (Def. B.3 edge rule with a per-question threshold that holds the
+      average degree at avg_degree);
+    * "fraction": the fraction_budget(k, P, beta) largest of the question
+      (top-beta sparsity, Sec. 3.5);
+    * "row": each row's row_budget(P, avg_degree) largest (a per-row
+      threshold)."""
     c = np.asarray(c, dtype=np.float64)
     k, P = c.shape
-    E = edge_budget(k, P, avg_degree)
+    if rule == "row":
+        D = row_budget(P, avg_degree)
+        adj = np.zeros((k, P), dtype=bool)
+        for i in range(k):
+            order = np.lexsort((np.arange(P), -c[i]))
+            adj[i, order[:D]] = True
+        return adj
+    if rule == "question":
+        E = edge_budget(k, P, avg_degree)
+    elif rule == "fraction":
+        E = fraction_budget(k, P, beta)
+    else:
+        raise ValueError(f"unknown edge rule {rule!r}")
     flat = c.reshape(-1)
     order = np.lexsort((np.arange(flat.size), -flat))
     adj = np.zeros(flat.size, dtype=bool)
@@ -236,7 +297,9 @@ def _f64(x) -> np.ndarray:
 def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
           query_passages, sm_scale: float, avg_degree: float = 4.0,
           w_bias=None, passage_key_table=None, queries: Optional[Sequence[int]] = None,
-          attn_rows: Optional[dict] = None, with_attention: bool = True) -> RouteResult:
+          attn_rows: Optional[dict] = None, with_attention: bool = True,
+          edge_rule: str = "question", edge_metric: str = "cosine",
+          edge_beta: float = 0.1) -> RouteResult:
     """Prune, build the graph and attend, question by question.
 
     V: [B, N, d]; Qtok: [sum T, d]; Kh, Vh: [sum M, H, d_h]; offsets as in
@@ -266,8 +329,8 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
         Kq, Vq = _f64(Kh[t0:t1]), _f64(Vh[t0:t1])
         if p1 > p0:
             Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
-            c = cosine_matrix(Vhat, Kbar)
-            adj = bsca_edges(c, avg_degree)
+            c = compatibility(Vhat, Kbar, edge_metric)
+            adj = bsca_edges(c, avg_degree, edge_rule, edge_beta)
         else:
             c = np.zeros((k, 0))
             adj = np.zeros((k, 0), dtype=bool)
@@ -290,7 +353,8 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
 def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
                     sm_scale: float, avg_degree: float = 4.0,
                     passage_key_table=None, adjacency: Optional[List[np.ndarray]] = None,
-                    attn_rows: Optional[dict] = None):
+                    attn_rows: Optional[dict] = None, edge_rule: str = "question",
+                    edge_metric: str = "cosine", edge_beta: float = 0.1):
     """Graph + attention on caller-given kept-row queries Qh [sum k, H, d_h].
     ``adjacency`` (per question [k_b, P_b] bool) replaces the cosine rule
     when the caller brings its own graph.  Returns (cos, adj, O, LSE) lists."""
@@ -313,8 +377,8 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
             adj = np.asarray(adjacency[b], dtype=bool)
         elif p1 > p0:
             Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
-            c = cosine_matrix(Q.reshape(k, H * d_h), Kbar)
-            adj = bsca_edges(c, avg_degree)
+            c = compatibility(Q.reshape(k, H * d_h), Kbar, edge_metric)
+            adj = bsca_edges(c, avg_degree, edge_rule, edge_beta)
         else:
             c = np.zeros((k, 0))
             adj = np.zeros((k, 0), dtype=bool)

@@ -47,8 +47,14 @@ class SkipProblem(ctypes.Structure):
         ("total_passages", ctypes.c_int32), ("total_tokens", ctypes.c_int32),
         ("L_max", ctypes.c_int32), ("total_edges", ctypes.c_int32),
         ("avg_degree", ctypes.c_double), ("sm_scale", ctypes.c_float),
-        ("o_f32", ctypes.c_int32),
+        ("o_f32", ctypes.c_int32), ("edge_rule", ctypes.c_int32),
+        ("edge_metric", ctypes.c_int32), ("edge_beta", ctypes.c_double),
     ]
+
+
+# skip_edge_rule_t and skip_edge_metric_t, by the names the oracle uses
+EDGE_RULES = {"question": 0, "row": 1, "fraction": 2}
+EDGE_METRICS = {"cosine": 0, "dot": 1}
 
 
 def _load() -> ctypes.CDLL:
@@ -110,7 +116,8 @@ def make_problem(dtype: str, *, B: int, N: int = 0, d: int, H: int = 0, d_h: int
                  q_offsets=None, kept_offsets=None, passage_offsets=None,
                  query_passages=None, avg_degree: float = 4.0,
                  sm_scale: Optional[float] = None, total_edges: int = 0,
-                 o_f32: bool = False) -> SkipProblem:
+                 o_f32: bool = False, edge_rule: str = "question",
+                 edge_metric: str = "cosine", edge_beta: float = 0.1) -> SkipProblem:
     """Fill the host-side problem description from host copies of the offsets."""
     p = SkipProblem()
     p.dtype = SKIP_F32 if dtype in ("f32", torch.float32) else SKIP_BF16
@@ -134,6 +141,9 @@ def make_problem(dtype: str, *, B: int, N: int = 0, d: int, H: int = 0, d_h: int
     p.avg_degree = float(avg_degree)
     p.sm_scale = float(sm_scale if sm_scale is not None else (1.0 / math.sqrt(d_h) if d_h else 1.0))
     p.o_f32 = 1 if o_f32 else 0
+    p.edge_rule = EDGE_RULES[edge_rule]
+    p.edge_metric = EDGE_METRICS[edge_metric]
+    p.edge_beta = float(edge_beta)
     return p
 
 
@@ -294,7 +304,9 @@ class DeviceBatch:
 
 
 def to_device(batch, device="cuda", avg_degree: Optional[float] = None,
-              sm_scale: Optional[float] = None, o_f32: bool = False) -> DeviceBatch:
+              sm_scale: Optional[float] = None, o_f32: bool = False,
+              edge_rule: str = "question", edge_metric: str = "cosine",
+              edge_beta: float = 0.1) -> DeviceBatch:
     """Move a generated batch (``workloads.Batch``) to the device."""
     wl = batch.wl
     B, N, d = batch.V.shape
@@ -303,7 +315,8 @@ def to_device(batch, device="cuda", avg_degree: Optional[float] = None,
                      kept_offsets=batch.kept_offsets, passage_offsets=batch.passage_offsets,
                      query_passages=batch.query_passages,
                      avg_degree=wl.avg_degree if avg_degree is None else avg_degree,
-                     sm_scale=wl.scale if sm_scale is None else sm_scale, o_f32=o_f32)
+                     sm_scale=wl.scale if sm_scale is None else sm_scale, o_f32=o_f32,
+                     edge_rule=edge_rule, edge_metric=edge_metric, edge_beta=edge_beta)
     i32 = lambda a: torch.from_numpy(np.asarray(a, dtype=np.int32)).to(device)
     return DeviceBatch(
         p=p, V=batch.V.to(device), Qtok=batch.Qtok.to(device), q_offsets=i32(batch.q_offsets),

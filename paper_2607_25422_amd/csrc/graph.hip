@@ -10,7 +10,10 @@
 //   edge_select  : per question, the E_b = min(ceil(avg_degree * k_b),
 //                  k_b * P_b) largest cosines (lower flattened index i*P_b+j
 //                  on ties) -> one 64-bit neighbour mask per kept row, and
-//                  optionally the graph in CSR form
+//                  optionally the graph in CSR form.  Also selectable: the
+//                  scaled dot product of eq. (bsca) instead of the cosine,
+//                  the top-beta fraction of the pairs (Sec. 3.5) or a
+//                  per-row cut instead of the per-question budget
 //   csr_to_mask  : neighbour masks from a caller-given CSR graph
 #include "skip_common.h"
 #include "skip_internal.h"
@@ -152,17 +155,30 @@ edge_dot_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_id
 constexpr int kGSelThreads = 1024;
 constexpr int kGSelMaxPT = 16;     // k_b * P_b <= 16384
 
+// Edges a question keeps under each cut (the same arithmetic on every side).
+__device__ __forceinline__ long long edges_of_question(int k, int P, int rule,
+                                                       double avg_degree, double beta) {
+  const long long n = min((long long)k * P, (long long)kGSelThreads * kGSelMaxPT);
+  if (rule == SKIP_EDGE_ROW_TOP)
+    return (long long)k * (long long)fmin((double)P, ceil(avg_degree));
+  const double want = (rule == SKIP_EDGE_TOP_FRACTION) ? ceil(beta * (double)n - 1e-9)
+                                                       : ceil(avg_degree * (double)k);
+  return (long long)fmin((double)n, fmax(0.0, want));
+}
+
 __global__ void __launch_bounds__(kGSelThreads)
 edge_select_kernel(const double* __restrict__ part, const double* __restrict__ qn2p,
                    const double* __restrict__ kn2p, int S,
                    const int32_t* __restrict__ kept_offsets,
                    const int32_t* __restrict__ query_passages, int B, int total_kept,
-                   int total_passages, int k_max, int P_max, double avg_degree,
+                   int total_passages, int k_max, int P_max, int d, double avg_degree,
+                   int rule, int metric, double beta,
                    uint64_t* __restrict__ rowmask, int32_t* __restrict__ rowptr_out,
                    int32_t* __restrict__ col_out) {
   __shared__ SelectShared sh;
   __shared__ uint32_t scan_sh[20];
   __shared__ uint8_t flag[kGSelThreads * kGSelMaxPT];
+  __shared__ uint64_t rkeys[kGSelThreads * kGSelMaxPT];   // per-row cut only
   const int b = blockIdx.x;
   int k0, k1, p0, p1;
   range_of(kept_offsets, b, total_kept, k0, k1);
@@ -170,13 +186,13 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
   const int k = min(k1 - k0, k_max);
   const int P = min(min(p1 - p0, P_max), 64);
   const int n = min(k * P, kGSelThreads * kGSelMaxPT);
-  const long long want = (long long)ceil(avg_degree * (double)k);
-  const int E = (int)min((long long)n, max(0ll, want));
+  const int E = (int)edges_of_question(k, P, rule, avg_degree, beta);
+  const double inv_sqrt_d = 1.0 / sqrt((double)d);
 
   const int C = (n + blockDim.x - 1) / blockDim.x;
   const int e0 = threadIdx.x * C;
   const int cnt = max(0, min(C, n - e0));
-  // cos(q_i, kbar_j) from the per-slice partial sums, in slice order
+  // compatibility of (i, j) from the per-slice partial sums, in slice order
   uint64_t keys[kGSelMaxPT];
 #pragma unroll
   for (int jj = 0; jj < kGSelMaxPT; ++jj) {
@@ -197,16 +213,48 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
         for (int u = 0; u < 8; ++u)
           if (sl0 + u < S) { dot += pd[u]; q2 += pq[u]; k2 += pk[u]; }
       }
-      const double nq = sqrt(q2), nk = sqrt(k2);
-      keys[jj] = order_key((nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0);
+      double c;
+      if (metric == SKIP_EDGE_DOT) {
+        c = dot * inv_sqrt_d;
+      } else {
+        const double nq = sqrt(q2), nk = sqrt(k2);
+        c = (nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0;
+      }
+      keys[jj] = order_key(c);
     }
   }
-  const uint32_t flags = block_select_top<kGSelMaxPT>(keys, cnt, n, E, &sh);
-
+  uint32_t flags;
+  if (rule == SKIP_EDGE_ROW_TOP) {
+    // every row keeps its D largest (lower passage first on ties)
 #pragma unroll
-  for (int j = 0; j < kGSelMaxPT; ++j)
-    if (j < cnt) flag[e0 + j] = (flags >> j) & 1u;
-  __syncthreads();
+    for (int jj = 0; jj < kGSelMaxPT; ++jj)
+      if (jj < cnt) rkeys[e0 + jj] = keys[jj];
+    __syncthreads();
+    const int D = (int)fmin((double)P, ceil(avg_degree));
+    for (int i = threadIdx.x; i < k && (i + 1) * P <= n; i += blockDim.x) {
+      const uint64_t* rk = rkeys + i * P;
+      for (int j = 0; j < P; ++j) {
+        const uint64_t kj = rk[j];
+        int rank = 0;
+        for (int t = 0; t < P; ++t) {
+          const uint64_t kt = rk[t];
+          rank += (kt > kj || (kt == kj && t < j)) ? 1 : 0;
+        }
+        flag[i * P + j] = rank < D ? 1u : 0u;
+      }
+    }
+    __syncthreads();
+    flags = 0u;
+#pragma unroll
+    for (int jj = 0; jj < kGSelMaxPT; ++jj)
+      if (jj < cnt && flag[e0 + jj]) flags |= 1u << jj;
+  } else {
+    flags = block_select_top<kGSelMaxPT>(keys, cnt, n, E, &sh);
+#pragma unroll
+    for (int j = 0; j < kGSelMaxPT; ++j)
+      if (j < cnt) flag[e0 + j] = (flags >> j) & 1u;
+    __syncthreads();
+  }
   for (int i = threadIdx.x; i < k; i += blockDim.x) {
     uint64_t m = 0;
     if (P > 0 && (i + 1) * P <= n)
@@ -222,8 +270,7 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
     range_of(kept_offsets, bb, total_kept, a0, a1);
     range_of(query_passages, bb, total_passages, q0, q1);
     const int kq = min(a1 - a0, k_max), Pq = min(min(q1 - q0, P_max), 64);
-    const long long nq = min((long long)kq * Pq, (long long)kGSelThreads * kGSelMaxPT);
-    base += min(nq, max(0ll, (long long)ceil(avg_degree * (double)kq)));
+    base += edges_of_question(kq, Pq, rule, avg_degree, beta);
   }
   uint32_t total;
   uint32_t pos = block_exclusive_scan(__popc(flags), scan_sh, &total);
@@ -310,8 +357,9 @@ hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
                               uint64_t* rowmask, int32_t* rowptr_out, int32_t* col_out,
                               hipStream_t s) {
   hipLaunchKernelGGL(edge_select_kernel, dim3(p.B), dim3(kGSelThreads), 0, s, ep.part,
-                     ep.qn2, ep.kn2, edge_slices(p), kept_offsets, query_passages, p.B, p.total_kept, p.total_passages,
-                     p.k_max, p.P_max, p.avg_degree, rowmask, rowptr_out, col_out);
+                     ep.qn2, ep.kn2, edge_slices(p), kept_offsets, query_passages, p.B,
+                     p.total_kept, p.total_passages, p.k_max, p.P_max, p.d, p.avg_degree,
+                     p.edge_rule, p.edge_metric, p.edge_beta, rowmask, rowptr_out, col_out);
   return hipGetLastError();
 }
 

@@ -31,6 +31,11 @@ skip_status_t check_common(const skip_problem_t* p) {
   return SKIP_OK;
 }
 
+static_assert(sizeof(skip_problem_t) == 88 && offsetof(skip_problem_t, avg_degree) == 56 &&
+                  offsetof(skip_problem_t, edge_rule) == 72 &&
+                  offsetof(skip_problem_t, edge_beta) == 80,
+              "skip_problem_t layout is part of the ABI");
+
 skip_status_t check(const skip_problem_t* p, int need) {
   skip_status_t st = check_common(p);
   if (st != SKIP_OK) return st;
@@ -49,6 +54,14 @@ skip_status_t check(const skip_problem_t* p, int need) {
     if (p->total_passages > 0 && (p->L_max < 1 || p->L_max > p->total_tokens))
       return SKIP_ERR_INVALID_ARG;
     if (!std::isfinite(p->avg_degree) || p->avg_degree < 0.0) return SKIP_ERR_INVALID_ARG;
+    if (p->edge_rule != SKIP_EDGE_QUESTION_BUDGET && p->edge_rule != SKIP_EDGE_ROW_TOP &&
+        p->edge_rule != SKIP_EDGE_TOP_FRACTION)
+      return SKIP_ERR_INVALID_ARG;
+    if (p->edge_metric != SKIP_EDGE_COSINE && p->edge_metric != SKIP_EDGE_DOT)
+      return SKIP_ERR_INVALID_ARG;
+    if (p->edge_rule == SKIP_EDGE_TOP_FRACTION &&
+        !(p->edge_beta > 0.0 && p->edge_beta <= 1.0))
+      return SKIP_ERR_INVALID_ARG;
     if (!std::isfinite(p->sm_scale)) return SKIP_ERR_INVALID_ARG;
     if (p->total_edges < 0) return SKIP_ERR_INVALID_ARG;
     if (p->P_max > 64) return SKIP_ERR_UNSUPPORTED;

@@ -36,16 +36,20 @@ def test_library_exports_every_declared_symbol(b):
 
 
 def test_version_and_status_strings(b):
-    assert b.abi_version() == 1
+    assert b.abi_version() == 2
     for s in range(5):
         assert b.status_string(s).startswith("SKIP_")
     assert "UNKNOWN" in b.status_string(99)
 
 
 def test_problem_struct_layout(b):
-    # 14 int32, a double at offset 56, a float and an int32 after it
-    assert ctypes.sizeof(b.SkipProblem) == 72
+    # 14 int32, a double at offset 56, a float and three int32 after it, a
+    # double at 80 (the library asserts the same layout at compile time)
+    assert ctypes.sizeof(b.SkipProblem) == 88
     assert b.SkipProblem.avg_degree.offset == 56
+    assert b.SkipProblem.edge_rule.offset == 72
+    assert b.SkipProblem.edge_metric.offset == 76
+    assert b.SkipProblem.edge_beta.offset == 80
 
 
 def _problem(b, **kw):
@@ -129,6 +133,15 @@ def test_xattn_rejects_bad_arguments(b):
     q = _problem(b)
     q.total_tokens = 1        # fewer tokens than passages
     assert _xattn(b, q) == b.SKIP_ERR_INVALID_ARG
+    for field, value in (("edge_rule", 3), ("edge_rule", -1), ("edge_metric", 2)):
+        q = _problem(b)
+        setattr(q, field, value)
+        assert _xattn(b, q) == b.SKIP_ERR_INVALID_ARG, (field, value)
+    for beta in (0.0, -0.5, 1.5, float("nan")):
+        q = _problem(b, edge_rule="fraction", edge_beta=beta)
+        assert _xattn(b, q) == b.SKIP_ERR_INVALID_ARG, beta
+    q = _problem(b, edge_rule="question", edge_beta=0.0)    # beta unused: accepted
+    assert _xattn(b, q, ws_bytes=0) == b.SKIP_ERR_WORKSPACE
 
 
 def test_fused_requires_matching_head_split(b):

@@ -251,6 +251,59 @@ def test_xattn_row_block_layouts(B, k, d_h):
                         stored_bf16=not f32_out)
 
 
+EDGE_VARIANTS = [("question", "dot", 0.1), ("row", "cosine", 0.1), ("row", "dot", 0.1),
+                 ("fraction", "cosine", 0.1), ("fraction", "dot", 0.35)]
+
+
+@pytest.mark.parametrize("rule,metric,beta", EDGE_VARIANTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_xattn_edge_rules_and_metrics(B, rule, metric, beta, dtype):
+    """The other edge cuts (per-row top, top fraction) and the scaled-dot
+    compatibility: identical graphs, attention to the usual bar."""
+    batch = small_batch(dtype, 42, H=2, d_h=128)
+    say(f"xattn edges {rule}/{metric} beta={beta} {dtype} P={batch.P.tolist()} k={batch.k.tolist()}")
+    db = B.to_device(batch, avg_degree=2.5, edge_rule=rule, edge_metric=metric, edge_beta=beta)
+    Qh = queries_from_batch(batch)
+    O, L, rp, col = B.bipartite_xattn(db, Qh.cuda())
+    torch.cuda.synchronize()
+    _, adj, O_ref, L_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, 2.5, edge_rule=rule, edge_metric=metric,
+        edge_beta=beta)
+    check_graph(batch, rp, col, adj)
+    check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), dtype)
+
+
+@pytest.mark.parametrize("rule,metric,beta", [("row", "cosine", 0.1), ("fraction", "dot", 0.1)])
+def test_fused_edge_rules_full_size(B, rule, metric, beta):
+    """highres_bf16 through the fused route under the other cuts: kept sets
+    and graphs exact for every question, attention on sampled rows."""
+    batch = wls.make_batch("highres_bf16", 2026, threads=16)
+    say(f"fused highres {rule}/{metric} beta={beta}")
+    db = B.to_device(batch, edge_rule=rule, edge_metric=metric, edge_beta=beta)
+    idx, _, Vk = B.prune_topk(db, want_scores=False)
+    Qh = Vk.view(-1, batch.Kh.shape[1], batch.Kh.shape[2])
+    _, _, rp, col = B.bipartite_xattn(db, Qh)
+    fidx, fO, fL = B.route_fused(db)
+    torch.cuda.synchronize()
+    rows = sample_rows(batch, 8)
+    ref = oracle_route(batch, attn_rows=rows, edge_rule=rule, edge_metric=metric, edge_beta=beta)
+    idx = fidx.cpu().numpy()
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist(), f"q{b} kept set"
+    check_graph(batch, rp, col, ref.adj)
+    Of, Lf = f64(fO), f64(fL)
+    got_O, got_L, want_O, want_L = [], [], [], []
+    for b, rs in rows.items():
+        k0 = int(batch.kept_offsets[b])
+        for r in rs:
+            got_O.append(Of[k0 + r]); got_L.append(Lf[k0 + r])
+            want_O.append(ref.O[b][r]); want_L.append(ref.LSE[b][r])
+    check_attention(np.stack(got_O), np.stack(got_L), np.stack(want_O), np.stack(want_L),
+                    "bf16", f"highres {rule}/{metric}")
+
+
 # --------------------------------------------------------------------------- fused
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

@@ -173,6 +173,72 @@ def test_edges_permutation_equivariance():
     assert np.array_equal(adj_p, adj[pr][:, pc])
 
 
+def test_dot_metric_worked_example_and_cosine_special_case():
+    # q = (3, 4), keys (1, 0) and (0, 2), D = 2: <q, k> / sqrt(2)
+    c = orc.dot_matrix(np.array([[3.0, 4.0]]), np.array([[1.0, 0.0], [0.0, 2.0]]))
+    np.testing.assert_allclose(c, [[3.0 / math.sqrt(2.0), 8.0 / math.sqrt(2.0)]], rtol=1e-15)
+    # unit rows and keys: the scaled dot product is the cosine over sqrt(D)
+    rng = np.random.default_rng(21)
+    Q = rng.standard_normal((5, 7))
+    K = rng.standard_normal((3, 7))
+    Q /= np.linalg.norm(Q, axis=1, keepdims=True)
+    K /= np.linalg.norm(K, axis=1, keepdims=True)
+    np.testing.assert_allclose(orc.dot_matrix(Q, K) * math.sqrt(7.0),
+                               orc.cosine_matrix(Q, K), rtol=1e-12, atol=1e-15)
+    # ranking on the argument equals ranking on the sigmoid of eq. (bsca)
+    c = orc.dot_matrix(rng.standard_normal((6, 7)), rng.standard_normal((4, 7)))
+    sig = 1.0 / (1.0 + np.exp(-c))
+    assert np.array_equal(orc.bsca_edges(c, 2.0), orc.bsca_edges(sig, 2.0))
+    with pytest.raises(ValueError):
+        orc.compatibility(Q, K, "l2")
+
+
+def test_fraction_rule_budget_and_brute_force():
+    assert orc.fraction_budget(192, 10, 0.1) == 192
+    assert orc.fraction_budget(7, 3, 0.1) == 3          # ceil(2.1)
+    assert orc.fraction_budget(4, 5, 1.0) == 20
+    rng = np.random.default_rng(22)
+    for trial in range(30):
+        k = int(rng.integers(1, 4))
+        P = int(rng.integers(1, 4))
+        beta = float(rng.choice([0.1, 0.25, 0.5, 0.9]))
+        c = rng.uniform(-1, 1, size=(k, P))
+        E = orc.fraction_budget(k, P, beta)
+        pairs = [(i, j) for i in range(k) for j in range(P)]
+        best = max(itertools.combinations(pairs, E), key=lambda t: sum(c[q] for q in t))
+        adj = orc.bsca_edges(c, 4.0, "fraction", beta)
+        assert adj.sum() == E
+        assert sorted(zip(*np.nonzero(adj))) == sorted(best)
+    # top-beta is the per-question budget at avg_degree = beta * P
+    c = rng.uniform(-1, 1, size=(12, 5))
+    assert np.array_equal(orc.bsca_edges(c, 4.0, "fraction", 0.2),
+                          orc.bsca_edges(c, 0.2 * 5, "question"))
+    with pytest.raises(ValueError):
+        orc.bsca_edges(c, 4.0, "nearest")
+
+
+def test_row_rule_brute_force_ties_and_degree():
+    rng = np.random.default_rng(23)
+    for trial in range(30):
+        k = int(rng.integers(1, 5))
+        P = int(rng.integers(1, 6))
+        deg = float(rng.choice([0.5, 1.0, 1.5, 2.0, 7.0]))
+        c = rng.uniform(-1, 1, size=(k, P))
+        adj = orc.bsca_edges(c, deg, "row")
+        D = min(math.ceil(deg), P)
+        assert orc.row_budget(P, deg) == D
+        for i in range(k):
+            best = max(itertools.combinations(range(P), D), key=lambda t: sum(c[i, j] for j in t))
+            assert sorted(np.nonzero(adj[i])[0].tolist()) == sorted(best)
+    # ties: the lower passage wins; every row gets exactly its budget
+    adj = orc.bsca_edges(np.zeros((3, 4)), 2.0, "row")
+    assert adj.tolist() == [[True, True, False, False]] * 3
+    # a per-row cut can differ from the per-question cut on the same budget
+    c = np.array([[0.9, 0.8, 0.7], [0.1, 0.0, -0.1]])
+    assert orc.bsca_edges(c, 1.0, "question").tolist() == [[True, True, False], [False, False, False]]
+    assert orc.bsca_edges(c, 1.0, "row").tolist() == [[True, False, False], [True, False, False]]
+
+
 def test_csr_from_adjacency():
     adj = np.array([[False, True, True], [False, False, False], [True, False, True]])
     rowptr, col = orc.adjacency_to_csr(adj)
