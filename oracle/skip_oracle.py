@@ -11,6 +11,8 @@ one kept row at a time, following the paper's definitions in their own order:
 * mean-pooled question embedding (Sec. 3.3; App. B.2, Def. B.2);
 * question-guided salience score (App. B.1, Def. B.1; Alg. 1, scoring step)
   with f_q = mean-pool and f_v = identity, plus the optional content bias;
+  or the main-text scorer, a two-layer perceptron on [v; q_bar; v * q_bar]
+  (Sec. 3.3, eq. qvs) with ReLU and bfloat16 inputs;
 * top-k pruning of the visual tokens (Def. B.1; Alg. 1, TopK step);
 * the bipartite graph between kept tokens and passages (App. B.3, Def. B.3,
   edge rule; Alg. 1, graph step);
@@ -80,6 +82,42 @@ def qvs_scores(z: np.ndarray) -> np.ndarray:
     """s_i = sigma(z_i) in [0, 1] (Def. B.1)."""
     z = np.asarray(z, dtype=np.float64)
     return 1.0 / (1.0 + np.exp(-z))
+
+
+def round_bf16(x) -> np.ndarray:
+    """Round to the nearest bfloat16 (ties to even) after a first rounding to
+    float32; returned as float64.  bfloat16 keeps the top 16 bits of a float32,
+    so rounding adds 0x7fff plus the lowest kept bit and clears the low half
+    (inputs are finite)."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float64).astype(np.float32))
+    bits = f.view(np.uint32).astype(np.uint64)
+    bits = (bits + 0x7FFF + ((bits >> 16) & 1)) & 0xFFFF0000
+    return bits.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def qvs_mlp_scores(V: np.ndarray, q_bar: np.ndarray, W1: np.ndarray, b1, w2: np.ndarray,
+                   b2: float) -> np.ndarray:
+    """Main-text salience scorer (Sec. 3.3, eq. qvs): s_i = MLP(v_i || q_bar ||
+    v_i * q_bar), a two-layer perceptron with hidden width h:
+
+        a_i = W1 x_i + b1,   s_i = w2 . relu(a_i) + b2,   W1: [h, 3d].
+
+    The model runs in bfloat16 (the paper's mixed precision), so its inputs are
+    bfloat16 values: q_bar is rounded once (through float32) and the Hadamard
+    term is the bfloat16 rounding of the exact product of two bfloat16 values;
+    everything after that is exact here (float64).  V: [N, d] -> s: [N]."""
+    V = np.asarray(V, dtype=np.float64)
+    N, d = V.shape
+    W1 = np.asarray(W1, dtype=np.float64)
+    if W1.shape[1] != 3 * d:
+        raise ValueError("W1 must be [h, 3d]")
+    q = round_bf16(q_bar)                      # [d]
+    X3 = round_bf16(V * q[None, :])            # [N, d]
+    Wa, Wb, Wc = W1[:, :d], W1[:, d:2 * d], W1[:, 2 * d:]
+    A = V @ Wa.T + X3 @ Wc.T + (Wb @ q)[None, :]
+    if b1 is not None:
+        A = A + np.asarray(b1, dtype=np.float64)[None, :]
+    return np.maximum(A, 0.0) @ np.asarray(w2, dtype=np.float64) + float(b2)
 
 
 def qvs_topk(z: np.ndarray, k: int) -> np.ndarray:
@@ -299,14 +337,17 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
           w_bias=None, passage_key_table=None, queries: Optional[Sequence[int]] = None,
           attn_rows: Optional[dict] = None, with_attention: bool = True,
           edge_rule: str = "question", edge_metric: str = "cosine",
-          edge_beta: float = 0.1) -> RouteResult:
+          edge_beta: float = 0.1, mlp: Optional[dict] = None) -> RouteResult:
     """Prune, build the graph and attend, question by question.
 
     V: [B, N, d]; Qtok: [sum T, d]; Kh, Vh: [sum M, H, d_h]; offsets as in
     the library interface.  The attention queries of a kept row are that
     row's visual token viewed as [H, d_h] (identity query projection).
     ``queries`` restricts the work to some questions; ``attn_rows`` maps a
-    question to the kept rows whose attention output is wanted."""
+    question to the kept rows whose attention output is wanted.  With
+    ``mlp`` (keys W1, b1, w2, b2) the tokens are ranked by the main-text
+    scorer instead of the linear logit; the ``z`` and ``scores`` of the
+    result are then both the scorer's s."""
     w = None if w_bias is None else _f64(w_bias)
     pk = None if passage_key_table is None else _f64(passage_key_table)
     B, N, d = V.shape
@@ -317,7 +358,10 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
         Q = _f64(Qtok[int(q_offsets[b]):int(q_offsets[b + 1])])
         Vb = _f64(V[b])
         q_bar = mean_pool_question(Q)
-        z = qvs_logits(Vb, q_bar, w)
+        if mlp is None:
+            z = qvs_logits(Vb, q_bar, w)
+        else:
+            z = qvs_mlp_scores(Vb, q_bar, mlp["W1"], mlp.get("b1"), mlp["w2"], mlp["b2"])
         k = int(kept_offsets[b + 1] - kept_offsets[b])
         idx = qvs_topk(z, k)
         Vhat = gather_rows(Vb, idx)
@@ -342,7 +386,7 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
             O, LSE = None, None
         res.kept_idx.append(idx)
         res.z.append(z)
-        res.scores.append(qvs_scores(z))
+        res.scores.append(qvs_scores(z) if mlp is None else z)
         res.cos.append(c)
         res.adj.append(adj)
         res.O.append(O)

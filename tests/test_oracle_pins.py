@@ -70,6 +70,75 @@ def test_scores_are_library_sigmoid():
 
 # ---------------------------------------------------------------- top-k
 
+def test_bf16_rounding_matches_library_cast():
+    rng = np.random.default_rng(31)
+    x = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-6, 6, 4000),
+                        [0.0, -0.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8)]])
+    want = torch.from_numpy(x).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(orc.round_bf16(x), want)
+    # ties to even, by hand: 1 + 2^-8 is halfway between 1 and 1 + 2^-7
+    assert orc.round_bf16(np.array([1.0 + 2 ** -8]))[0] == 1.0
+    assert orc.round_bf16(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+
+
+def test_mlp_scorer_worked_example():
+    # d = 2, h = 2; bf16-exact inputs so every rounding is the identity
+    V = np.array([[1.0, 2.0], [-1.0, 0.5]])
+    q = np.array([0.5, -1.0])
+    W1 = np.array([[1.0, 0.0, 0.0, 1.0, 2.0, 0.0],     # v1 + q2 + 2 (v*q)1
+                   [0.0, -1.0, 1.0, 0.0, 0.0, 1.0]])   # -v2 + q1 + (v*q)2
+    b1, w2, b2 = np.array([0.5, 0.0]), np.array([1.0, -2.0]), 0.25
+    # token 0: x = (1, 2 | 0.5, -1 | 0.5, -2): a = (1 - 1 + 1 + 0.5, -2 + 0.5 - 2) = (1.5, -3.5)
+    #          s = 1 * 1.5 - 2 * relu(-3.5) + 0.25 = 1.75
+    # token 1: x = (-1, 0.5 | 0.5, -1 | -0.5, -0.5): a = (-1 - 1 - 1 + 0.5, -0.5 + 0.5 - 0.5)
+    #          = (-2.5, -0.5): both clipped, s = 0.25
+    s = orc.qvs_mlp_scores(V, q, W1, b1, w2, b2)
+    np.testing.assert_allclose(s, [1.75, 0.25], rtol=0, atol=1e-15)
+
+
+def test_mlp_scorer_reduces_to_linear_logit_and_folds():
+    rng = np.random.default_rng(32)
+    N, d = 50, 16
+    V = orc.round_bf16(rng.standard_normal((N, d)))
+    q_bar = rng.standard_normal(d)
+    u = rng.standard_normal(d)
+    # one hidden unit that weighs only v, a bias keeping it positive: s = u.v + b1 + b2
+    W1 = np.zeros((1, 3 * d))
+    W1[0, :d] = u
+    s = orc.qvs_mlp_scores(V, q_bar, W1, np.array([1e6]), np.array([1.0]), -1e6 + 0.5)
+    np.testing.assert_allclose(s, V @ u + 0.5, rtol=1e-9, atol=1e-6)
+    # Hadamard weights only, q_bar a power of two: v * q is exact in bfloat16,
+    # so the first layer is (Wc diag(q)) v
+    Wc = rng.standard_normal((3, d))
+    W1 = np.concatenate([np.zeros((3, 2 * d)), Wc], axis=1)
+    w2 = np.array([1.0, -0.5, 2.0])
+    qp = np.full(d, 0.25)
+    A = V @ (Wc * qp[None, :]).T
+    np.testing.assert_allclose(orc.qvs_mlp_scores(V, qp, W1, None, w2, 0.0),
+                               np.maximum(A, 0.0) @ w2, rtol=1e-12, atol=1e-12)
+    # all pre-activations negative: the output is the last bias
+    W1 = -np.abs(rng.standard_normal((4, 3 * d)))
+    s = orc.qvs_mlp_scores(np.abs(V), np.abs(q_bar), W1, -np.ones(4), rng.standard_normal(4), 3.0)
+    np.testing.assert_array_equal(s, np.full(N, 3.0))
+    with pytest.raises(ValueError):
+        orc.qvs_mlp_scores(V, q_bar, np.zeros((2, 2 * d)), None, np.zeros(2), 0.0)
+
+
+def test_mlp_scorer_rounds_the_hadamard_term():
+    # v = q = 1 + 2^-7 (both bfloat16-exact): v * q = 1 + 2^-6 + 2^-14, whose
+    # bfloat16 rounding drops the 2^-14; the scorer must see the rounded value
+    V = np.array([[1.0 + 2 ** -7]])
+    q = np.array([1.0 + 2 ** -7])
+    W1 = np.array([[0.0, 0.0, 1.0]])
+    s = orc.qvs_mlp_scores(V, q, W1, None, np.array([1.0]), 0.0)
+    assert s[0] == 1.0 + 2 ** -6
+    assert s[0] != (1.0 + 2 ** -7) ** 2
+    # and q_bar itself enters rounded: 1 + 2^-8 is a tie and goes to even (1)
+    s = orc.qvs_mlp_scores(np.array([[1.0]]), np.array([1.0 + 2 ** -8]),
+                           np.array([[0.0, 1.0, 0.0]]), None, np.array([1.0]), 0.0)
+    assert s[0] == 1.0
+
+
 def test_topk_ties_go_to_lowest_index():
     z = np.array([1.0, 3.0, 3.0, 2.0, 3.0])
     assert orc.qvs_topk(z, 2).tolist() == [1, 2]
