@@ -50,6 +50,10 @@ def parse():
                     help="edge compatibility: cosine (default) or scaled dot product")
     ap.add_argument("--edge-beta", type=float, default=0.1,
                     help="kept fraction of the pairs for --edge-rule fraction")
+    ap.add_argument("--scorer", default="linear", choices=["linear", "mlp"],
+                    help="mlp: time the prune stage with the main-text scorer instead of "
+                         "the fused route (a record line, not the headline)")
+    ap.add_argument("--hidden", type=int, default=512, help="hidden width of the mlp scorer")
     ap.add_argument("--cold", action="store_true",
                     help="overwrite a 1 GiB buffer before every timed step so that no input "
                          "is left in the on-die cache; value then comes from the event-timed "
@@ -128,6 +132,62 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
+def bench_mlp_scorer(args):
+    """Prune stage (pooling, main-text scorer, top-k, gather) on a workload's
+    visual tokens: queries/s of the stage and the scorer's first-layer
+    TFLOP/s over the whole stage time (event-timed on the launch stream)."""
+    import torch
+
+    from paper_2607_25422_amd import binding as B
+    from paper_2607_25422_amd import workloads as wls
+
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {args.workload} seed {args.seed} (scorer h={args.hidden})",
+          file=sys.stderr, flush=True)
+    batch = wls.make_batch(args.workload, args.seed, threads=16)
+    wl = batch.wl
+    w = wls.make_scorer_weights(wl, args.hidden, args.seed)
+    db = B.to_device(batch)
+    p = db.p
+    mlp = B.QvsMlp(w.W1.cuda(), w.b1.cuda(), w.w2.cuda(), w.b2)
+    ws = torch.empty(B.workspace_bytes_mlp(p, args.hidden), dtype=torch.uint8, device="cuda")
+    for _ in range(args.warmup):
+        B.prune_topk_mlp(db, mlp, want_scores=False, workspace=ws)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(args.steps):
+        B.prune_topk_mlp(db, mlp, want_scores=False, workspace=ws)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    avg_ms = sum(step_ms) / len(step_ms)
+    flops = 2.0 * p.B * p.N * (2 * p.d) * args.hidden + 2.0 * p.B * args.hidden * p.d
+    tf = flops / (avg_ms * 1e-3) / 1e12
+    res = {
+        "metric": "queries/sec (prune stage with the main-text scorer) + scorer TFLOP/s vs "
+                  "MI355X bf16 MFMA peak",
+        "value": round(p.B * args.steps / wall, 1),
+        "unit": "queries/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "B": p.B, "N": p.N, "d": p.d, "k": int(batch.k[0]),
+                   "scorer": "mlp", "hidden": args.hidden, "seed": args.seed},
+        "step_gpu_ms": {"p10": round(step_ms[len(step_ms) // 10], 5),
+                        "p50": round(step_ms[len(step_ms) // 2], 5),
+                        "p90": round(step_ms[min(len(step_ms) - 1, 9 * len(step_ms) // 10)], 5)},
+        "roofline": {"kernel": "mlp_score_kernel (over the whole stage)", "bound": "mfma",
+                     "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "algorithmic_gflop": round(flops / 1e9, 2), "avg_ms": round(avg_ms, 5)},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -135,6 +195,9 @@ def main():
               "(the routing core runs on a single MI355X; see the sharding notes)",
               file=sys.stderr)
         sys.exit(2)
+    if args.scorer == "mlp":
+        bench_mlp_scorer(args)
+        return
 
     import numpy as np
     import torch

@@ -180,6 +180,56 @@ skip_status_t skip_prune_topk(const skip_problem_t* p, const void* V,
                               void* stream);
 
 /*
+ * Main-text salience scorer (Sec. 3.3, eq. qvs): a two-layer perceptron on
+ * x_i = [v_i ; q_bar ; v_i (*) q_bar] (width 3d),
+ *   a_i = W1 x_i + b1,   s_i = w2 . relu(a_i) + b2,
+ * evaluated as the paper's bf16 model would: q_bar enters rounded to bf16
+ * (round-to-nearest-even, through float32), the Hadamard term is the bf16
+ * rounding of the exact product, products accumulate in float32 (bf16
+ * matrix cores) and the second layer sums in float32 then float64.
+ *   hidden  h: a multiple of 256, at most 4096
+ *   W1      [h][3d] bf16, row j = the weights of hidden unit j: columns
+ *           [0, d) weigh v_i, [d, 2d) q_bar, [2d, 3d) v_i (*) q_bar
+ *   b1      [h] float, or NULL for zeros
+ *   w2      [h] float
+ *   b2      output bias
+ * The activation is ReLU (the paper does not name one).
+ */
+typedef struct skip_qvs_mlp {
+  int32_t hidden;
+  int32_t reserved;        /* must be 0 */
+  const void* W1;
+  const float* b1;
+  const float* w2;
+  double b2;
+} skip_qvs_mlp_t;
+
+/*
+ * Workspace of skip_prune_topk_mlp for problem `p` and hidden width `hidden`
+ * (host-only).  Writes *bytes and returns SKIP_OK, or the validation error.
+ */
+skip_status_t skip_workspace_bytes_mlp(const skip_problem_t* p, int32_t hidden,
+                                       size_t* bytes);
+
+/*
+ * Stage 1 with the main-text scorer (Sec. 3.3, eq. qvs; Alg. 1, scoring and
+ * TopK steps): q_bar pooled as in skip_prune_topk, every visual token scored
+ * by the perceptron `mlp` (a HOST pointer to the description; its arrays are
+ * device arrays), the k_b tokens of largest s kept (ties: lowest index),
+ * reported ascending.  bf16 only (p->dtype == SKIP_BF16, else
+ * SKIP_ERR_UNSUPPORTED); d a multiple of 32.
+ *   scores   out [B][N] float: the perceptron outputs s_i, or NULL
+ * Other arguments as in skip_prune_topk (no content bias: it is a term of the
+ * first layer here).  The workspace must hold skip_workspace_bytes_mlp().
+ */
+skip_status_t skip_prune_topk_mlp(const skip_problem_t* p, const skip_qvs_mlp_t* mlp,
+                                  const void* V, const void* Qtok,
+                                  const int32_t* q_offsets,
+                                  const int32_t* kept_offsets, int32_t* kept_idx,
+                                  float* scores, void* V_kept, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/*
  * Stage 2: bipartite graph + sparse cross-attention (Def. B.3; Alg. 1,
  * graph and fuse steps) on caller-given kept-row queries.
  *   Qh              [total_kept][H][d_h] queries of the kept rows

@@ -28,7 +28,8 @@ SKIP_F32, SKIP_BF16 = 0, 1
 
 ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes",
                 "skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused",
-                "skip_route_fused_profiled")
+                "skip_route_fused_profiled", "skip_workspace_bytes_mlp",
+                "skip_prune_topk_mlp")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -49,6 +50,15 @@ class SkipProblem(ctypes.Structure):
         ("avg_degree", ctypes.c_double), ("sm_scale", ctypes.c_float),
         ("o_f32", ctypes.c_int32), ("edge_rule", ctypes.c_int32),
         ("edge_metric", ctypes.c_int32), ("edge_beta", ctypes.c_double),
+    ]
+
+
+class SkipQvsMlp(ctypes.Structure):
+    """skip_qvs_mlp_t: the main-text scorer's weights (device pointers)."""
+    _fields_ = [
+        ("hidden", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+        ("b2", ctypes.c_double),
     ]
 
 
@@ -80,6 +90,12 @@ def _load() -> ctypes.CDLL:
     lib.skip_route_fused.restype = ctypes.c_int
     lib.skip_route_fused.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p, vp,
                                      i32p, vp, vp, vp, ctypes.c_size_t, vp]
+    M = ctypes.POINTER(SkipQvsMlp)
+    lib.skip_workspace_bytes_mlp.restype = ctypes.c_int
+    lib.skip_workspace_bytes_mlp.argtypes = [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.skip_prune_topk_mlp.restype = ctypes.c_int
+    lib.skip_prune_topk_mlp.argtypes = [P, M, vp, vp, i32p, i32p, i32p, vp, vp, vp,
+                                        ctypes.c_size_t, vp]
     lib.skip_route_fused_profiled.restype = ctypes.c_int
     lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                               vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
@@ -157,6 +173,13 @@ def new_workspace(p: SkipProblem, device="cuda") -> torch.Tensor:
     return torch.empty(max(workspace_bytes(p), 256), dtype=torch.uint8, device=device)
 
 
+def workspace_bytes_mlp(p: SkipProblem, hidden: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.skip_workspace_bytes_mlp(ctypes.byref(p), int(hidden), ctypes.byref(n)),
+           "skip_workspace_bytes_mlp")
+    return int(n.value)
+
+
 # ---------------------------------------------------------------------------
 # Pointer helpers
 
@@ -211,6 +234,26 @@ def skip_prune_topk(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, ke
         _ptr(scores, "scores", torch.float32, p.B * p.N),
         _ptr(V_kept, "V_kept", et, p.total_kept * p.d), wsp, wsn, _stream(stream))
     _check(st, "skip_prune_topk")
+
+
+def skip_prune_topk_mlp(p: SkipProblem, mlp: "QvsMlp", V, Qtok, q_offsets, kept_offsets,
+                        kept_idx, scores=None, V_kept=None, workspace=None, stream=None):
+    et = _elem_dtype(p)
+    h = mlp.hidden
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes_mlp(p, h), dtype=torch.uint8, device=V.device)
+    m = SkipQvsMlp(h, 0, _ptr(mlp.W1, "W1", et, h * 3 * p.d), _ptr(mlp.b1, "b1", torch.float32, h),
+                   _ptr(mlp.w2, "w2", torch.float32, h), float(mlp.b2))
+    st = LIB.skip_prune_topk_mlp(
+        ctypes.byref(p), ctypes.byref(m), _ptr(V, "V", et, p.B * p.N * p.d),
+        _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
+        _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept),
+        _ptr(scores, "scores", torch.float32, p.B * p.N),
+        _ptr(V_kept, "V_kept", et, p.total_kept * p.d), workspace.data_ptr(), workspace.numel(),
+        _stream(stream))
+    _check(st, "skip_prune_topk_mlp")
 
 
 def skip_bipartite_xattn(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passage_offsets,
@@ -342,6 +385,35 @@ def prune_topk(db: DeviceBatch, want_scores=True, want_rows=True):
               if want_rows else None)
     skip_prune_topk(p, db.V, db.Qtok, db.q_offsets, db.w_bias, db.kept_offsets, kept_idx,
                     scores, V_kept, db.workspace)
+    return (kept_idx[:p.total_kept], None if scores is None else scores.view(p.B, p.N),
+            None if V_kept is None else V_kept[:p.total_kept])
+
+
+@dataclass
+class QvsMlp:
+    """Device tensors of the main-text scorer: W1 [h, 3d] (element type of V),
+    b1 [h] float32 or None, w2 [h] float32, and the scalar b2."""
+    W1: torch.Tensor
+    b1: Optional[torch.Tensor]
+    w2: torch.Tensor
+    b2: float
+
+    @property
+    def hidden(self) -> int:
+        return int(self.W1.shape[0])
+
+
+def prune_topk_mlp(db: DeviceBatch, mlp: QvsMlp, want_scores=True, want_rows=True,
+                   workspace=None):
+    """Stage 1 with the main-text scorer.  Returns (kept_idx, scores, V_kept)."""
+    p = db.p
+    dev = db.V.device
+    kept_idx = torch.empty(max(p.total_kept, 1), dtype=torch.int32, device=dev)
+    scores = torch.empty(p.B * p.N, dtype=torch.float32, device=dev) if want_scores else None
+    V_kept = (torch.empty((max(p.total_kept, 1), p.d), dtype=db.V.dtype, device=dev)
+              if want_rows else None)
+    skip_prune_topk_mlp(p, mlp, db.V, db.Qtok, db.q_offsets, db.kept_offsets, kept_idx,
+                        scores, V_kept, workspace)
     return (kept_idx[:p.total_kept], None if scores is None else scores.view(p.B, p.N),
             None if V_kept is None else V_kept[:p.total_kept])
 

@@ -1,0 +1,395 @@
+// Main-text salience scorer (paper Sec. 3.3, eq. qvs): a two-layer
+// perceptron on the concatenation [v_i ; q_bar ; v_i * q_bar],
+//
+//   a_i = W1 x_i + b1,   s_i = w2 . relu(a_i) + b2,   W1: [h][3d] bf16.
+//
+// The model runs in bf16: q_bar enters rounded to bf16 (through float32) and
+// the Hadamard term is the bf16 rounding of the exact product of two bf16
+// values.  Split by where the work is:
+//   mlp_prep_kernel  : q_bar' = bf16(q_bar) per question and the per-question
+//                      constant c_b = W1[:, d:2d] q_bar' + b1 (float32 sums of
+//                      exact products)
+//   mlp_score_kernel : per question the GEMM [v_i | bf16(v_i * q_bar')] x
+//                      [W1[:, 0:d] | W1[:, 2d:3d]]^T on v_mfma_f32_32x32x16_bf16
+//                      (the Hadamard operand is formed in registers from the
+//                      staged v tile), with relu(. + c_b) . w2 folded into the
+//                      epilogue: one float partial of s_i per 256 hidden units
+//   mlp_sum_kernel   : s_i = sum of the partials (fixed order) + b2, as the
+//                      float64 ranking key of the top-k and as the output score
+#include "skip_common.h"
+#include "skip_internal.h"
+
+namespace skip {
+
+namespace {
+
+typedef __bf16 mbf16x8_t __attribute__((ext_vector_type(8)));
+typedef float mf32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ mf32x16_t mfma_bf16(const u32x4& a, const u32x4& b, mf32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(mbf16x8_t, a),
+                                                 __builtin_bit_cast(mbf16x8_t, b), c, 0, 0, 0);
+}
+
+// Direct global->LDS load of 16 bytes per lane (lane l's bytes land at
+// lds + 16 * l); completion is awaited with an explicit vmcnt wait.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(lds)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ void barrier_nf() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+typedef __bf16 mbf16x2_t __attribute__((ext_vector_type(2)));
+
+// bf16(a * q) for the 8 bf16 values of a (q: 8 floats); a product of two
+// bf16 values is exact in float32, so the pair conversion (round to nearest
+// even, v_cvt_pk_bf16_f32) is the one rounding of the model.
+__device__ __forceinline__ u32x4 hadamard8(const u32x4& a, const float* q) {
+  u32x4 r;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t x = a[w];
+    const mbf16x2_t p = {(__bf16)(__uint_as_float(x << 16) * q[2 * w]),
+                         (__bf16)(__uint_as_float(x & 0xffff0000u) * q[2 * w + 1])};
+    r[w] = __builtin_bit_cast(uint32_t, p);
+  }
+  return r;
+}
+
+__device__ __forceinline__ void unpack8(const u32x4& x, float* out) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    out[2 * w] = __uint_as_float(x[w] << 16);
+    out[2 * w + 1] = __uint_as_float(x[w] & 0xffff0000u);
+  }
+}
+
+}  // namespace
+
+constexpr int kMlpMT = 128;      // tokens per tile
+constexpr int kMlpKS = 32;       // columns of d per step (v part and v*q part)
+constexpr int kMlpThreads = 512;
+constexpr int kMlpPartial = 128; // hidden units per partial score (the narrowest tile)
+
+// ---------------------------------------------------------------------------
+// q_bar' and the per-question constant of the first layer.  Block (jt, b):
+// q_bar_b rounded to bf16 (through float32) is staged in LDS as floats; wave
+// w then forms c_b[j] = sum_c W1[j][d + c] q_bar'_b[c] + b1[j] for the
+// kMlpPrepJ / 4 hidden units j = jt * kMlpPrepJ + w * (kMlpPrepJ / 4) + t
+// (products of two bf16 values are exact in float32; float32 sums).  Blocks
+// with jt == 0 also write q_bar'_b for the score kernel.
+constexpr int kMlpPrepJ = 32;
+constexpr int kMlpMaxD = 8192;
+
+__global__ void __launch_bounds__(256)
+mlp_prep_kernel(const double* __restrict__ qbar, const bf16_t* __restrict__ W1,
+                const float* __restrict__ b1, int B, int d, int h,
+                bf16_t* __restrict__ qbf, float* __restrict__ cvec) {
+  __shared__ float qs[kMlpMaxD];
+  const int jt = blockIdx.x, b = blockIdx.y;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    const uint32_t r = f32_to_bf16((float)qbar[(size_t)b * d + c]);
+    qs[c] = bf16_to_f32(r);
+    if (jt == 0) qbf[(size_t)b * d + c] = (bf16_t)r;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int JW = kMlpPrepJ / 4;
+  for (int t = 0; t < JW; ++t) {
+    const int j = jt * kMlpPrepJ + wave * JW + t;
+    const bf16_t* wrow = W1 + (size_t)j * 3 * d + d;      // the q_bar block of row j
+    float acc = 0.f;
+    for (int c = lane * 8; c < d; c += 64 * 8) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(wrow + c);
+      float wf[8];
+      unpack8(w, wf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc = fmaf(wf[e], qs[c + e], acc);
+    }
+    acc = wave_sum_f32(acc);
+    if (lane == 0) cvec[(size_t)b * h + j] = acc + (b1 ? b1[j] : 0.f);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// W1's v block and Hadamard block, repacked in the order the score kernel's
+// waves read them: for hidden tile nt (256 units), wave w (32 units), step s
+// (32 columns), block x (0: v, 1: Hadamard), k16 sub-step kk and lane l, the
+// 16 bytes W1[256 nt + 32 w + l % 32][x * 2d + 32 s + 8 (2 kk + l / 32) ...+7].
+// One 1 KiB run per (nt, w, s, x, kk): every fragment load of the score kernel
+// is one fully coalesced wave-wide load.
+constexpr int kMlpNT = 256;
+
+__global__ void __launch_bounds__(256)
+mlp_pack_kernel(const bf16_t* __restrict__ W1, int d, int h, u32x4* __restrict__ Wp) {
+  const size_t total = (size_t)h * d / 4;            // 16-byte units of both blocks
+  const int ksteps = d / kMlpKS;
+  for (size_t u = (size_t)blockIdx.x * blockDim.x + threadIdx.x; u < total;
+       u += (size_t)gridDim.x * blockDim.x) {
+    const int l = (int)(u % 64);
+    size_t r = u / 64;
+    const int kk = (int)(r % 2); r /= 2;
+    const int x = (int)(r % 2); r /= 2;
+    const int s = (int)(r % ksteps); r /= ksteps;
+    const int w = (int)(r % 8);
+    const int nt = (int)(r / 8);
+    const int j = nt * kMlpNT + w * 32 + (l & 31);
+    const int col = x * 2 * d + s * kMlpKS + (2 * kk + (l >> 5)) * 8;
+    Wp[u] = *reinterpret_cast<const u32x4*>(W1 + (size_t)j * 3 * d + col);
+  }
+}
+
+// Work item = (question b, 128-token tile, 256-hidden tile); wave w of 8 owns
+// hidden units 32 w .. 32 w + 31 of the tile for all 128 tokens (4 blocks of
+// 32 x 32, v_mfma_f32_32x32x16_bf16).  Per 32-column step s:
+//   * the v tile V[tile rows, 32 s : 32 s + 32] arrives in a 4-slot LDS ring
+//     by direct global->LDS loads issued 3 steps ahead (16-byte chunks
+//     XOR-swizzled by (row/2) % 4: operand reads of 8 consecutive rows hit
+//     distinct banks);
+//   * the workgroup forms the Hadamard tile bf16(v * q_bar') of step s+1 once,
+//     into one of two LDS buffers, while it multiplies step s;
+//   * each wave's W1 fragments come straight from the repacked weights into
+//     registers, two steps ahead.
+// The epilogue folds relu(a + c_b) . w2 and writes one partial of s_i per
+// 128 hidden units.
+constexpr int kMlpRing = 4;
+constexpr int kMlpAhead = 3;
+
+__global__ void __launch_bounds__(kMlpThreads)
+mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
+                 const u32x4* __restrict__ Wp, int h, const bf16_t* __restrict__ qbf,
+                 const float* __restrict__ cvec, const float* __restrict__ w2,
+                 float* __restrict__ sp, int n_items) {
+  constexpr int A_ELEMS = kMlpMT * kMlpKS;       // 4096 (8 KiB)
+  __shared__ __attribute__((aligned(1024))) bf16_t Ar[kMlpRing * A_ELEMS];
+  __shared__ __attribute__((aligned(1024))) bf16_t Hd[2 * A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[kMlpMaxD];   // q_bar'_b
+
+  const int per_xcd = gridDim.x / 8;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= n_items) return;
+  const int NTL = h / kMlpNT;
+  const int MTL = (N + kMlpMT - 1) / kMlpMT;
+  const int nt = item % NTL;
+  const int mt = (item / NTL) % MTL;
+  const int b = item / (NTL * MTL);
+  const int i0 = mt * kMlpMT, j0 = nt * kMlpNT;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ksteps = d / kMlpKS;
+  const int hh = lane >> 5, r32 = lane & 31;
+
+  // the direct load of this thread's 16 bytes of a v tile: row tid/4,
+  // physical chunk tid%4 holding logical chunk lc_t
+  const int trow = tid >> 2;
+  const int lc_t = (tid & 3) ^ ((trow >> 1) & 3);
+  const bf16_t* vsrc = V + ((size_t)b * N + min(i0 + trow, N - 1)) * d + lc_t * 8;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t ar_lds = lds_u32(Ar) + (uint32_t)(wave_s * 1024);
+  auto issue_v = [&](int s) {
+    dma16(vsrc + s * kMlpKS, __builtin_amdgcn_readfirstlane(
+                                 ar_lds + (uint32_t)((s % kMlpRing) * A_ELEMS * 2)));
+  };
+  // Hadamard tile of step s (this thread's 8 values, same swizzled position;
+  // q_bar' comes from LDS so that no vector-memory load joins the counted
+  // queue of tile loads)
+  auto hadamard_tile = [&](int s) {
+    const u32x4 a = *reinterpret_cast<const u32x4*>(Ar + (s % kMlpRing) * A_ELEMS + tid * 8);
+    float q[8];
+    unpack8(*reinterpret_cast<const u32x4*>(Qs + s * kMlpKS + lc_t * 8), q);
+    *reinterpret_cast<u32x4*>(Hd + (s & 1) * A_ELEMS + tid * 8) = hadamard8(a, q);
+  };
+  // W1 fragments of step s: [x][kk], x = 0 the v block, 1 the Hadamard block
+  const u32x4* wsrc = Wp + ((size_t)(nt * 8 + wave) * ksteps) * 256 + lane;
+  auto load_w = [&](int s, u32x4 (&w)[2][2]) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) w[x][kk] = wsrc[(size_t)s * 256 + (x * 2 + kk) * 64];
+  };
+
+  mf32x16_t acc[4];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[mb][v] = 0.f;
+
+  // A operand offsets (elements) within a tile: block mb, k16 sub-step kk
+  int aoff[2][4];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const int row = mb * 32 + r32;
+      aoff[kk][mb] = row * kMlpKS + (((2 * kk + hh) ^ ((row >> 1) & 3)) << 3);
+    }
+
+  auto mma_step = [&](int s, const u32x4 (&w)[2][2]) {
+    const bf16_t* At = Ar + (s % kMlpRing) * A_ELEMS;
+    const bf16_t* Ht = Hd + (s & 1) * A_ELEMS;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      u32x4 a1[4], a3[4];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        a1[mb] = *reinterpret_cast<const u32x4*>(At + aoff[kk][mb]);
+        a3[mb] = *reinterpret_cast<const u32x4*>(Ht + aoff[kk][mb]);
+      }
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        acc[mb] = mfma_bf16(a1[mb], w[0][kk], acc[mb]);
+        acc[mb] = mfma_bf16(a3[mb], w[1][kk], acc[mb]);
+      }
+    }
+  };
+
+  // prologue: q_bar'_b into LDS, v tiles of steps 0..2, W1 of steps 0 and 1,
+  // Hadamard of step 0
+  for (int c = tid * 8; c < d; c += kMlpThreads * 8)
+    *reinterpret_cast<u32x4*>(Qs + c) =
+        *reinterpret_cast<const u32x4*>(qbf + (size_t)b * d + c);
+#pragma unroll
+  for (int a = 0; a < kMlpAhead; ++a)
+    if (a < ksteps) issue_v(a);
+  u32x4 wA[2][2], wB[2][2];
+  load_w(0, wA);
+  load_w(min(1, ksteps - 1), wB);
+  wait_vm<0>();
+  barrier_nf();
+  hadamard_tile(0);
+
+  // Step s: wait for the v tile of step s+1 (the Hadamard pass reads it),
+  // barrier (publishes it and the Hadamard tile of step s), load the v tile
+  // of step s+3 into the slot step s-1 left, form the Hadamard tile of step
+  // s+1, multiply step s, load the W1 fragments of step s+2.
+  auto step = [&](int s, u32x4 (&w)[2][2]) {
+    // outstanding per wave after this wait: the v tile of step s+2 (one
+    // load, while there is one) and the W1 fragments of step s+1 (four loads)
+    if (s + 2 < ksteps) wait_vm<5>();
+    else wait_vm<4>();
+    barrier_nf();
+    if (s + kMlpAhead < ksteps) issue_v(s + kMlpAhead);
+    if (s + 1 < ksteps) hadamard_tile(s + 1);
+    mma_step(s, w);
+    // unconditional (the last steps reload the final step's fragments): a
+    // conditional load would make the compiler drain the whole queue before
+    // the next use of w
+    load_w(min(s + 2, ksteps - 1), w);
+  };
+  int s = 0;
+  for (; s + 1 < ksteps; s += 2) {
+    step(s, wA);
+    step(s + 1, wB);
+  }
+  if (s < ksteps) step(s, wA);
+
+  // Epilogue: relu(a + c) * w2 for this lane's hidden unit, summed over the
+  // 32 units of the wave, then over the four waves of each 128-unit part in
+  // wave order.  Accumulator element v of block mb: token mb*32 + 8*(v/4) +
+  // 4*hh + v%4; hidden unit j0 + 32*wave + r32.
+  const int j = j0 + wave * 32 + r32;
+  const float c = cvec[(size_t)b * h + j];
+  const float wv = w2[j];
+  float rs[4][16];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = fmaxf(acc[mb][v] + c, 0.f) * wv;
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) x += __shfl_xor(x, o, kWave);
+      rs[mb][v] = x;
+    }
+  __syncthreads();                                   // the ring is free again
+  float* red = reinterpret_cast<float*>(Ar);         // [8][128]
+  if (r32 == 0) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        red[wave * kMlpMT + mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3)] = rs[mb][v];
+  }
+  __syncthreads();
+  if (tid < 2 * kMlpMT) {
+    const int pp = tid / kMlpMT, row = tid % kMlpMT;
+    if (i0 + row < N) {
+      const float* rp = red + pp * 4 * kMlpMT + row;
+      const float sum = ((rp[0] + rp[kMlpMT]) + rp[2 * kMlpMT]) + rp[3 * kMlpMT];
+      sp[((size_t)(nt * 2 + pp) * B + b) * N + i0 + row] = sum;
+    }
+  }
+}
+
+// s_i = sum over hidden tiles of the partials (tile order) + b2.
+__global__ void __launch_bounds__(256)
+mlp_sum_kernel(const float* __restrict__ sp, int NTL, int B, int N, double b2,
+               double* __restrict__ z, float* __restrict__ scores) {
+  const int b = blockIdx.y;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  double s = 0.0;
+  for (int t = 0; t < NTL; ++t) s += (double)sp[((size_t)t * B + b) * N + i];
+  s += b2;
+  z[(size_t)b * N + i] = s;
+  if (scores) scores[(size_t)b * N + i] = (float)s;
+}
+
+static size_t mlp_align(size_t n) { return (n + 255) & ~(size_t)255; }
+
+size_t mlp_scratch_bytes(const skip_problem_t& p, int hidden) {
+  return mlp_align((size_t)p.B * p.d * sizeof(bf16_t)) +
+         mlp_align((size_t)p.B * hidden * sizeof(float)) +
+         mlp_align((size_t)(hidden / kMlpPartial) * p.B * (size_t)p.N * sizeof(float)) +
+         mlp_align((size_t)hidden * 2 * p.d * sizeof(bf16_t));
+}
+
+MlpScratch carve_mlp_scratch(const skip_problem_t& p, int hidden, void* base) {
+  char* c = static_cast<char*>(base);
+  MlpScratch m;
+  m.qbf = reinterpret_cast<bf16_t*>(c);
+  c += mlp_align((size_t)p.B * p.d * sizeof(bf16_t));
+  m.cvec = reinterpret_cast<float*>(c);
+  c += mlp_align((size_t)p.B * hidden * sizeof(float));
+  m.sp = reinterpret_cast<float*>(c);
+  c += mlp_align((size_t)(hidden / kMlpPartial) * p.B * (size_t)p.N * sizeof(float));
+  m.wpack = reinterpret_cast<u32x4*>(c);
+  return m;
+}
+
+hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, const void* V,
+                             const double* qbar, MlpScratch ms, double* z, float* scores,
+                             hipStream_t s) {
+  const int h = m.hidden;
+  hipLaunchKernelGGL(mlp_prep_kernel, dim3(h / kMlpPrepJ, p.B), dim3(256), 0, s, qbar,
+                     (const bf16_t*)m.W1, m.b1, p.B, p.d, h, ms.qbf, ms.cvec);
+  hipLaunchKernelGGL(mlp_pack_kernel, dim3(1024), dim3(256), 0, s, (const bf16_t*)m.W1, p.d, h,
+                     ms.wpack);
+  const int MTL = (p.N + kMlpMT - 1) / kMlpMT;
+  const int n_items = p.B * MTL * (h / kMlpNT);
+  const int grid = ((n_items + 7) / 8) * 8;
+  hipLaunchKernelGGL(mlp_score_kernel, dim3(grid), dim3(kMlpThreads), 0, s, (const bf16_t*)V,
+                     p.N, p.d, p.B, (const u32x4*)ms.wpack, h, (const bf16_t*)ms.qbf, ms.cvec,
+                     m.w2, ms.sp, n_items);
+  hipLaunchKernelGGL(mlp_sum_kernel, dim3((p.N + 255) / 256, p.B), dim3(256), 0, s, ms.sp,
+                     h / kMlpPartial, p.B, p.N, m.b2, z, scores);
+  return hipGetLastError();
+}
+
+}  // namespace skip

@@ -161,6 +161,55 @@ skip_status_t skip_prune_topk(const skip_problem_t* p, const void* V, const void
   return SKIP_OK;
 }
 
+static_assert(sizeof(skip_qvs_mlp_t) == 40 && offsetof(skip_qvs_mlp_t, b2) == 32,
+              "skip_qvs_mlp_t layout is part of the ABI");
+
+static bool mlp_shape_ok(const skip_qvs_mlp_t* m) {
+  return m->hidden > 0 && m->hidden % 256 == 0 && m->hidden <= 4096;
+}
+
+skip_status_t skip_workspace_bytes_mlp(const skip_problem_t* p, int32_t hidden, size_t* bytes) {
+  if (!bytes) return SKIP_ERR_INVALID_ARG;
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (p->N < 0 || p->P_max < 0 || p->total_passages < 0) return SKIP_ERR_INVALID_ARG;
+  if (hidden <= 0) return SKIP_ERR_INVALID_ARG;
+  if (hidden % 256 != 0 || hidden > 4096) return SKIP_ERR_UNSUPPORTED;
+  *bytes = workspace_size(*p) + mlp_scratch_bytes(*p, hidden);
+  return SKIP_OK;
+}
+
+skip_status_t skip_prune_topk_mlp(const skip_problem_t* p, const skip_qvs_mlp_t* mlp,
+                                  const void* V, const void* Qtok, const int32_t* q_offsets,
+                                  const int32_t* kept_offsets, int32_t* kept_idx,
+                                  float* scores, void* V_kept, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  skip_status_t st = check(p, kPrune);
+  if (st != SKIP_OK) return st;
+  if (!mlp || !V || !Qtok || !q_offsets || !kept_offsets || !workspace)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && !kept_idx) return SKIP_ERR_INVALID_ARG;
+  if (mlp->reserved != 0 || !mlp->W1 || !mlp->w2 || mlp->hidden <= 0 ||
+      !std::isfinite(mlp->b2))
+    return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || !mlp_shape_ok(mlp)) return SKIP_ERR_UNSUPPORTED;
+  if ((int64_t)mlp->hidden * 3 * p->d > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  const size_t need = workspace_size(*p) + mlp_scratch_bytes(*p, mlp->hidden);
+  if (workspace_bytes < need) return SKIP_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Workspace w = carve_workspace(*p, workspace);
+  MlpScratch ms = carve_mlp_scratch(*p, mlp->hidden, static_cast<char*>(workspace) + w.bytes);
+  // q_bar itself (the plain mean of the question tokens) into u
+  SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, Qtok,
+                        q_offsets, p->B, p->total_qtok, w.u, s));
+  SKIP_TRY(launch_mlp_scores(*p, *mlp, V, w.u, ms, w.z, scores, s));
+  if (p->total_kept > 0) {
+    SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
+    if (V_kept) SKIP_TRY(launch_gather(*p, V, kept_offsets, kept_idx, V_kept, s));
+  }
+  return SKIP_OK;
+}
+
 skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
                                    const int32_t* kept_offsets, const void* Kh, const void* Vh,
                                    const int32_t* passage_offsets,

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "skip.h"
+#include "skip_common.h"
 
 namespace skip {
 
@@ -35,6 +36,19 @@ hipError_t launch_topk(const skip_problem_t& p, const double* z,
 hipError_t launch_gather(const skip_problem_t& p, const void* V,
                          const int32_t* kept_offsets, const int32_t* kept_idx,
                          void* V_kept, hipStream_t s);
+
+// Main-text scorer (two-layer perceptron) -------------------------------
+struct MlpScratch {
+  bf16_t* qbf;       // [B][d]         q_bar rounded to bf16
+  float* cvec;       // [B][h]         W1[:, d:2d] q_bar' + b1
+  float* sp;         // [h/128][B][N]  partial scores per 128 hidden units
+  u32x4* wpack;      // [h][2d] bf16   W1's v and Hadamard blocks in fragment order
+};
+size_t mlp_scratch_bytes(const skip_problem_t& p, int hidden);
+MlpScratch carve_mlp_scratch(const skip_problem_t& p, int hidden, void* base);
+hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, const void* V,
+                             const double* qbar, MlpScratch ms, double* z, float* scores,
+                             hipStream_t s);
 
 // Stage 2 ---------------------------------------------------------------
 // Query rows: if kept_idx is non-NULL, row r of question b is

@@ -286,3 +286,47 @@ def make_batch(wl: Workload | str, seed: int = 2026, *, B: Optional[int] = None,
                  q_offsets=q_offsets, kept_offsets=kept_offsets, Kh=Kh, Vh=Vh,
                  passage_offsets=passage_offsets, query_passages=query_passages,
                  w_bias=w_bias, planted=[p[7] for p in parts])
+
+
+@dataclass
+class ScorerWeights:
+    """Synthetic weights of the main-text salience scorer, a two-layer
+    perceptron on [v; q_bar; v * q_bar] (CPU tensors): W1 [h, 3d] bfloat16,
+    b1 [h] and w2 [h] float32, b2 a float."""
+
+    W1: torch.Tensor
+    b1: torch.Tensor
+    w2: torch.Tensor
+    b2: float
+
+    @property
+    def hidden(self) -> int:
+        return int(self.W1.shape[0])
+
+    def as_dict(self) -> dict:
+        return {"W1": self.W1, "b1": self.b1, "w2": self.w2, "b2": self.b2}
+
+
+def make_scorer_weights(wl: Workload | str, hidden: int = 512, seed: int = 2026) -> ScorerWeights:
+    """Gaussian weights scaled so that each of the three input blocks adds a
+    term of order one to a hidden pre-activation for this workload's token
+    distribution: the v block ~ N(0, 1/(d s_v^2)), the q_bar block ~ N(0, T/(d
+    s_v^2)) (q_bar averages T tokens), the product block ~ N(0, T/(d s_v^4));
+    s_v is the per-coordinate scale of a visual token (1 or 1/sqrt(d)).  b1 is
+    a small Gaussian, so about half the hidden units are active; w2 ~ N(0,
+    1/h).  No trained weights exist for the paper's scorer; the hidden width
+    is not stated there (512 here)."""
+    if isinstance(wl, str):
+        wl = WORKLOADS[wl]
+    d = wl.d
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, wl.wid, 7919])))
+    sv2 = 1.0 if wl.visual == "unit" else 1.0 / d
+    Wa = rng.standard_normal((hidden, d)) * math.sqrt(1.0 / (d * sv2))
+    Wb = rng.standard_normal((hidden, d)) * math.sqrt(wl.T / (d * sv2))
+    Wc = rng.standard_normal((hidden, d)) * math.sqrt(wl.T / (d * sv2 * sv2))
+    W1 = np.concatenate([Wa, Wb, Wc], axis=1)
+    b1 = rng.standard_normal(hidden) * 0.1
+    w2 = rng.standard_normal(hidden) / math.sqrt(hidden)
+    return ScorerWeights(W1=_round(W1, "bf16"), b1=torch.from_numpy(b1.astype(np.float32)),
+                         w2=torch.from_numpy(w2.astype(np.float32)),
+                         b2=float(rng.standard_normal()))

@@ -115,6 +115,37 @@ def _xattn(b, p, ws_bytes=1 << 30, **ptrs):
                                       None)
 
 
+def test_mlp_scorer_struct_and_validation(b):
+    assert ctypes.sizeof(b.SkipQvsMlp) == 40
+    assert b.SkipQvsMlp.b2.offset == 32
+    p = _problem(b)
+    n = b.workspace_bytes_mlp(p, 512)
+    assert n > b.workspace_bytes(p)
+    assert b.workspace_bytes_mlp(p, 1024) > n
+
+    def call(q, m=None, ws_bytes=1 << 30, **kw):
+        m = m if m is not None else b.SkipQvsMlp(512, 0, FAKE, None, FAKE, 0.5)
+        args = dict(V=FAKE, Qtok=FAKE, qo=FAKE, ko=FAKE, idx=FAKE)
+        args.update(kw)
+        return b.LIB.skip_prune_topk_mlp(ctypes.byref(q), ctypes.byref(m) if m is not False else None,
+                                         args["V"], args["Qtok"], args["qo"], args["ko"],
+                                         args["idx"], None, None, FAKE, ws_bytes, None)
+    assert call(p, m=False) == b.SKIP_ERR_INVALID_ARG                      # no scorer
+    assert call(p, V=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, m=b.SkipQvsMlp(512, 1, FAKE, None, FAKE, 0.0)) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, m=b.SkipQvsMlp(512, 0, None, None, FAKE, 0.0)) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, m=b.SkipQvsMlp(512, 0, FAKE, None, FAKE, float("inf"))) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, m=b.SkipQvsMlp(384, 0, FAKE, None, FAKE, 0.0)) == b.SKIP_ERR_UNSUPPORTED
+    assert call(p, m=b.SkipQvsMlp(8192, 0, FAKE, None, FAKE, 0.0)) == b.SKIP_ERR_UNSUPPORTED
+    q = b.make_problem("f32", B=2, N=576, d=1024, q_offsets=[0, 3, 7], kept_offsets=[0, 96, 192])
+    assert call(q) == b.SKIP_ERR_UNSUPPORTED                              # bf16 only
+    q = b.make_problem("bf16", B=2, N=576, d=1000, q_offsets=[0, 3, 7], kept_offsets=[0, 96, 192])
+    assert call(q) == b.SKIP_ERR_UNSUPPORTED                              # d % 32
+    assert call(p, ws_bytes=n - 1) == b.SKIP_ERR_WORKSPACE
+    with pytest.raises(b.SkipError):
+        b.workspace_bytes_mlp(p, 100)
+
+
 def test_xattn_rejects_bad_arguments(b):
     p = _problem(b)
     assert _xattn(b, p, O=None) == b.SKIP_ERR_INVALID_ARG

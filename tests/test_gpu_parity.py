@@ -304,6 +304,92 @@ def test_fused_edge_rules_full_size(B, rule, metric, beta):
                     "bf16", f"highres {rule}/{metric}")
 
 
+# --------------------------------------------------------------------------- main-text scorer
+
+def mlp_device(B, w):
+    return B.QvsMlp(w.W1.cuda(), w.b1.cuda(), w.w2.cuda(), w.b2)
+
+
+def check_mlp_prune(batch, w, idx, scores, Vk, questions=None, tag=""):
+    """Scores within a float32-accumulation bound of the float64 oracle; the
+    kept set a valid top-k of the GPU's own scores; any difference from the
+    oracle's kept set inside the tie band (reported, never silent); kept rows
+    bitwise equal to V."""
+    idx = idx.cpu().numpy()
+    s_gpu = scores.cpu().double().numpy()
+    Vk = Vk.cpu() if Vk is not None else None
+    W1, b1, w2 = w.W1.double().numpy(), w.b1.double().numpy(), w.w2.double().numpy()
+    events = 0
+    for b in (range(batch.B) if questions is None else questions):
+        Q = batch.Qtok[int(batch.q_offsets[b]):int(batch.q_offsets[b + 1])].double().numpy()
+        s_ref = orc.qvs_mlp_scores(batch.V[b].double().numpy(), orc.mean_pool_question(Q),
+                                   W1, b1, w2, w.b2)
+        err = float(np.max(np.abs(s_gpu[b] - s_ref)))
+        tol = 2e-5 * (1.0 + float(np.max(np.abs(s_ref))))
+        assert err <= tol, f"{tag} q{b}: score error {err:.3e} > {tol:.3e}"
+        k0, k1 = int(batch.kept_offsets[b]), int(batch.kept_offsets[b + 1])
+        k = k1 - k0
+        got = idx[k0:k1]
+        assert got.tolist() == sorted(got.tolist()), f"{tag} q{b}: not ascending"
+        if Vk is not None:
+            assert torch.equal(Vk[k0:k1], batch.V[b][torch.from_numpy(got.astype(np.int64))])
+        if k == 0 or k == batch.wl.N:
+            assert got.tolist() == list(range(k))
+            continue
+        rest = np.setdiff1d(np.arange(batch.wl.N), got)
+        assert s_gpu[b][got].min() >= s_gpu[b][rest].max(), f"{tag} q{b}: not a top-k of its scores"
+        want = orc.qvs_topk(s_ref, k)
+        if got.tolist() != want.tolist():
+            srt = np.sort(s_ref)[::-1]
+            cut = 0.5 * (srt[k - 1] + srt[k])
+            diff = np.setxor1d(got, want)
+            band = np.abs(s_ref[diff] - cut)
+            say(f"{tag} q{b}: tie-band event, tokens {diff.tolist()} at {band.max():.2e} "
+                f"from the cut (score error {err:.2e})")
+            assert band.max() <= 2 * err, f"{tag} q{b}: kept set differs outside the tie band"
+            events += 1
+    return events
+
+
+@pytest.mark.parametrize("hidden", [256, 512])
+@pytest.mark.parametrize("seed", wls.SEEDS)
+def test_prune_mlp_small_ragged(B, hidden, seed):
+    batch = wls.make_batch("llava_bf16", seed, B=4, N=300, H=4, d_h=64, T=(1, 3, 8),
+                           k=(0, 7, 33, 64, 300))
+    w = wls.make_scorer_weights(batch.wl, hidden, seed)
+    say(f"mlp scorer small h={hidden} seed={seed} k={batch.k.tolist()}")
+    db = B.to_device(batch)
+    idx, scores, Vk = B.prune_topk_mlp(db, mlp_device(B, w))
+    torch.cuda.synchronize()
+    check_mlp_prune(batch, w, idx, scores, Vk, tag=f"h{hidden}")
+
+
+def test_prune_mlp_without_b1_and_repeatable(B):
+    batch = wls.make_batch("llava_bf16", 11, B=3, N=260, H=2, d_h=128, T=(2, 5), k=(1, 50))
+    w = wls.make_scorer_weights(batch.wl, 256, 11)
+    w0 = wls.ScorerWeights(w.W1, torch.zeros_like(w.b1), w.w2, w.b2)
+    db = B.to_device(batch)
+    m = B.QvsMlp(w.W1.cuda(), None, w.w2.cuda(), w.b2)
+    a = B.prune_topk_mlp(db, m)
+    b = B.prune_topk_mlp(db, m)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    check_mlp_prune(batch, w0, *a, tag="no b1")
+
+
+def test_prune_mlp_full_size(B):
+    """highres_bf16 (N = 2304, d = 4096) with a 512-unit scorer, in the launch
+    configuration the benchmark times; the oracle checks three questions."""
+    batch = wls.make_batch("highres_bf16", 2026, threads=16)
+    w = wls.make_scorer_weights(batch.wl, 512, 2026)
+    say("mlp scorer full size highres_bf16 h=512")
+    db = B.to_device(batch)
+    idx, scores, Vk = B.prune_topk_mlp(db, mlp_device(B, w))
+    torch.cuda.synchronize()
+    check_mlp_prune(batch, w, idx, scores, Vk, questions=[0, 7, 15], tag="highres")
+
+
 # --------------------------------------------------------------------------- fused
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
