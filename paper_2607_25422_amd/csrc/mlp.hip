@@ -89,43 +89,72 @@ constexpr int kMlpThreads = 512;
 constexpr int kMlpPartial = 128; // hidden units per partial score (the narrowest tile)
 
 // ---------------------------------------------------------------------------
-// q_bar' and the per-question constant of the first layer.  Block (jt, b):
-// q_bar_b rounded to bf16 (through float32) is staged in LDS as floats; wave
-// w then forms c_b[j] = sum_c W1[j][d + c] q_bar'_b[c] + b1[j] for the
-// kMlpPrepJ / 4 hidden units j = jt * kMlpPrepJ + w * (kMlpPrepJ / 4) + t
-// (products of two bf16 values are exact in float32; float32 sums).  Blocks
-// with jt == 0 also write q_bar'_b for the score kernel.
-constexpr int kMlpPrepJ = 32;
+// The per-question constant of the first layer.  Block (jt, qt): q_bar' of
+// the questions qt*4 .. qt*4+3 is staged in LDS; wave w forms c_b[j] = sum_c W1[j][d + c] q_bar'_b[c] + b1[j]
+// for its two hidden units j = 8*jt + 2*w + {0, 1} and the block's questions
+// (products of two bf16 values are exact in float32; float32 sums).  The
+// row loads of a 4096-column group are all issued before the products.
+constexpr int kMlpPrepJ = 8;
+constexpr int kMlpPrepQ = 4;
 constexpr int kMlpMaxD = 8192;
 
 __global__ void __launch_bounds__(256)
-mlp_prep_kernel(const double* __restrict__ qbar, const bf16_t* __restrict__ W1,
-                const float* __restrict__ b1, int B, int d, int h,
-                bf16_t* __restrict__ qbf, float* __restrict__ cvec) {
-  __shared__ float qs[kMlpMaxD];
-  const int jt = blockIdx.x, b = blockIdx.y;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    const uint32_t r = f32_to_bf16((float)qbar[(size_t)b * d + c]);
-    qs[c] = bf16_to_f32(r);
-    if (jt == 0) qbf[(size_t)b * d + c] = (bf16_t)r;
-  }
+mlp_prep_kernel(const bf16_t* __restrict__ qbf, const bf16_t* __restrict__ W1,
+                const float* __restrict__ b1, int B, int d, int h, float* __restrict__ cvec) {
+  __shared__ __attribute__((aligned(16))) bf16_t qs[kMlpPrepQ][kMlpMaxD];
+  const int jt = blockIdx.x, q0 = blockIdx.y * kMlpPrepQ;
+  const int nq = min(kMlpPrepQ, B - q0);
+  for (int i = threadIdx.x * 8; i < nq * d; i += blockDim.x * 8)
+    *reinterpret_cast<u32x4*>(&qs[0][0] + (i / d) * kMlpMaxD + i % d) =
+        *reinterpret_cast<const u32x4*>(qbf + (size_t)q0 * d + i);
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int JW = kMlpPrepJ / 4;
-  for (int t = 0; t < JW; ++t) {
-    const int j = jt * kMlpPrepJ + wave * JW + t;
-    const bf16_t* wrow = W1 + (size_t)j * 3 * d + d;      // the q_bar block of row j
-    float acc = 0.f;
-    for (int c = lane * 8; c < d; c += 64 * 8) {
-      const u32x4 w = *reinterpret_cast<const u32x4*>(wrow + c);
-      float wf[8];
-      unpack8(w, wf);
+  const int j0 = jt * kMlpPrepJ + wave * 2;
+  const bf16_t* wr0 = W1 + (size_t)j0 * 3 * d + d;     // the q_bar block of row j0
+  const bf16_t* wr1 = wr0 + (size_t)3 * d;
+  float acc[2][kMlpPrepQ];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc = fmaf(wf[e], qs[c + e], acc);
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int qq = 0; qq < kMlpPrepQ; ++qq) acc[u][qq] = 0.f;
+  for (int g = 0; g < d; g += 4096) {
+    constexpr int CH = 4096 / 512;                     // 16-byte chunks per lane per group
+    u32x4 w[2][CH];
+#pragma unroll
+    for (int t = 0; t < CH; ++t) {
+      const int c = g + (t * 64 + lane) * 8;
+      const bool ok = c < d;
+      w[0][t] = ok ? *reinterpret_cast<const u32x4*>(wr0 + c) : u32x4{0u, 0u, 0u, 0u};
+      w[1][t] = ok ? *reinterpret_cast<const u32x4*>(wr1 + c) : u32x4{0u, 0u, 0u, 0u};
     }
-    acc = wave_sum_f32(acc);
-    if (lane == 0) cvec[(size_t)b * h + j] = acc + (b1 ? b1[j] : 0.f);
+#pragma unroll
+    for (int t = 0; t < CH; ++t) {
+      const int c = g + (t * 64 + lane) * 8;
+      if (c >= d) continue;
+      float w0[8], w1[8];
+      unpack8(w[0][t], w0);
+      unpack8(w[1][t], w1);
+#pragma unroll
+      for (int qq = 0; qq < kMlpPrepQ; ++qq) {
+        if (qq >= nq) continue;
+        float qv[8];
+        unpack8(*reinterpret_cast<const u32x4*>(&qs[qq][c]), qv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          acc[0][qq] = fmaf(w0[e], qv[e], acc[0][qq]);
+          acc[1][qq] = fmaf(w1[e], qv[e], acc[1][qq]);
+        }
+      }
+    }
   }
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int qq = 0; qq < kMlpPrepQ; ++qq) {
+      const float v = wave_sum_f32(acc[u][qq]);
+      if (lane == 0 && qq < nq)
+        cvec[(size_t)(q0 + qq) * h + j0 + u] = v + (b1 ? b1[j0 + u] : 0.f);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -137,12 +166,22 @@ mlp_prep_kernel(const double* __restrict__ qbar, const bf16_t* __restrict__ W1,
 // is one fully coalesced wave-wide load.
 constexpr int kMlpNT = 256;
 
+constexpr int kMlpPackBlocks = 1024;
+
 __global__ void __launch_bounds__(256)
-mlp_pack_kernel(const bf16_t* __restrict__ W1, int d, int h, u32x4* __restrict__ Wp) {
+mlp_pack_kernel(const bf16_t* __restrict__ W1, int d, int h, u32x4* __restrict__ Wp,
+                const double* __restrict__ qbar, bf16_t* __restrict__ qbf) {
+  if ((int)blockIdx.x >= kMlpPackBlocks) {
+    // q_bar' = bf16(float(q_bar)) of question blockIdx.x - kMlpPackBlocks
+    const int b = blockIdx.x - kMlpPackBlocks;
+    for (int c = threadIdx.x; c < d; c += blockDim.x)
+      qbf[(size_t)b * d + c] = (bf16_t)f32_to_bf16((float)qbar[(size_t)b * d + c]);
+    return;
+  }
   const size_t total = (size_t)h * d / 4;            // 16-byte units of both blocks
   const int ksteps = d / kMlpKS;
   for (size_t u = (size_t)blockIdx.x * blockDim.x + threadIdx.x; u < total;
-       u += (size_t)gridDim.x * blockDim.x) {
+       u += (size_t)kMlpPackBlocks * blockDim.x) {
     const int l = (int)(u % 64);
     size_t r = u / 64;
     const int kk = (int)(r % 2); r /= 2;
@@ -242,22 +281,34 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
     }
 
   auto mma_step = [&](int s, const u32x4 (&w)[2][2]) {
+    __builtin_amdgcn_sched_barrier(0);
     const bf16_t* At = Ar + (s % kMlpRing) * A_ELEMS;
     const bf16_t* Ht = Hd + (s & 1) * A_ELEMS;
+    u32x4 a1[2][4], a3[2][4];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      u32x4 a1[4], a3[4];
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        a1[mb] = *reinterpret_cast<const u32x4*>(At + aoff[kk][mb]);
-        a3[mb] = *reinterpret_cast<const u32x4*>(Ht + aoff[kk][mb]);
-      }
+    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb) {
-        acc[mb] = mfma_bf16(a1[mb], w[0][kk], acc[mb]);
-        acc[mb] = mfma_bf16(a3[mb], w[1][kk], acc[mb]);
+        a1[kk][mb] = *reinterpret_cast<const u32x4*>(At + aoff[kk][mb]);
+        a3[kk][mb] = *reinterpret_cast<const u32x4*>(Ht + aoff[kk][mb]);
       }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        acc[mb] = mfma_bf16(a1[kk][mb], w[0][kk], acc[mb]);
+        acc[mb] = mfma_bf16(a3[kk][mb], w[1][kk], acc[mb]);
+      }
+    // Schedule: eight operand reads ahead, then one MFMA per read, so the
+    // read latency hides behind the matrix pipe.
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   // prologue: q_bar'_b into LDS, v tiles of steps 0..2, W1 of steps 0 and 1,
@@ -286,8 +337,8 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
     else wait_vm<4>();
     barrier_nf();
     if (s + kMlpAhead < ksteps) issue_v(s + kMlpAhead);
-    if (s + 1 < ksteps) hadamard_tile(s + 1);
     mma_step(s, w);
+    if (s + 1 < ksteps) hadamard_tile(s + 1);
     // unconditional (the last steps reload the final step's fragments): a
     // conditional load would make the compiler drain the whole queue before
     // the next use of w
@@ -377,10 +428,12 @@ hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, c
                              const double* qbar, MlpScratch ms, double* z, float* scores,
                              hipStream_t s) {
   const int h = m.hidden;
-  hipLaunchKernelGGL(mlp_prep_kernel, dim3(h / kMlpPrepJ, p.B), dim3(256), 0, s, qbar,
-                     (const bf16_t*)m.W1, m.b1, p.B, p.d, h, ms.qbf, ms.cvec);
-  hipLaunchKernelGGL(mlp_pack_kernel, dim3(1024), dim3(256), 0, s, (const bf16_t*)m.W1, p.d, h,
-                     ms.wpack);
+  // repacked weights and q_bar' (one launch), then the per-question constant
+  hipLaunchKernelGGL(mlp_pack_kernel, dim3(kMlpPackBlocks + p.B), dim3(256), 0, s,
+                     (const bf16_t*)m.W1, p.d, h, ms.wpack, qbar, ms.qbf);
+  hipLaunchKernelGGL(mlp_prep_kernel, dim3(h / kMlpPrepJ, (p.B + kMlpPrepQ - 1) / kMlpPrepQ),
+                     dim3(256), 0, s, (const bf16_t*)ms.qbf, (const bf16_t*)m.W1, m.b1, p.B,
+                     p.d, h, ms.cvec);
   const int MTL = (p.N + kMlpMT - 1) / kMlpMT;
   const int n_items = p.B * MTL * (h / kMlpNT);
   const int grid = ((n_items + 7) / 8) * 8;
