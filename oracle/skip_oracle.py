@@ -195,6 +195,50 @@ def compatibility(Qrows: np.ndarray, Kbar: np.ndarray, metric: str = "cosine") -
     raise ValueError(f"unknown edge metric {metric!r}")
 
 
+def skv_logits(q_bar: np.ndarray, v_bar: np.ndarray, E: np.ndarray, W: np.ndarray, b1,
+               w2: np.ndarray, b2: float) -> np.ndarray:
+    """Passage verification (App. B.4, Def. B.4): nu_j = sigma(h(x_j)) with
+    x_j = [q_bar; v_bar; e_j; e_j * q_bar; |e_j - q_bar|] and h a two-layer
+    perceptron, h(x) = w2 . relu(W x + b1) + b2, W: [h, 5d].  Returns the
+    logits h(x_j) (nu is monotone in them).  As for the main-text scorer the
+    model takes bfloat16 inputs: q_bar, v_bar and e_j are rounded once (through
+    float32), e_j * q_bar is the rounding of the exact product of the rounded
+    values and |e_j - q_bar| the rounding of their float32 difference.
+    E: [P, d] passage embeddings."""
+    E = np.asarray(E, dtype=np.float64)
+    P, d = E.shape
+    W = np.asarray(W, dtype=np.float64)
+    if W.shape[1] != 5 * d:
+        raise ValueError("W must be [h, 5d]")
+    q = round_bf16(q_bar)
+    v = round_bf16(v_bar)
+    e = round_bf16(E)
+    had = round_bf16(e * q[None, :])
+    dif = round_bf16(np.abs(e.astype(np.float32) - q.astype(np.float32)[None, :]))
+    X = np.concatenate([np.broadcast_to(q, (P, d)), np.broadcast_to(v, (P, d)), e, had, dif],
+                       axis=1)
+    A = X @ W.T
+    if b1 is not None:
+        A = A + np.asarray(b1, dtype=np.float64)[None, :]
+    return np.maximum(A, 0.0) @ np.asarray(w2, dtype=np.float64) + float(b2)
+
+
+def skv_keep(logits: np.ndarray, tau: float, rho: float) -> np.ndarray:
+    """Verified passages (Alg. 1, verify step): among the passages with
+    nu_j = sigma(logit_j) >= tau, the ceil(rho * P) largest nu (ties to the
+    lower index).  sigma is monotone, so nu >= tau is logit >= log(tau / (1 -
+    tau)).  Returns a boolean mask [P]."""
+    z = np.asarray(logits, dtype=np.float64)
+    P = z.shape[0]
+    t = math.log(tau) - math.log1p(-tau)
+    cap = int(math.ceil(float(rho) * P - 1e-9))
+    cand = [j for j in range(P) if z[j] >= t]
+    cand.sort(key=lambda j: (-z[j], j))
+    keep = np.zeros(P, dtype=bool)
+    keep[cand[:cap]] = True
+    return keep
+
+
 def edge_budget(k: int, P: int, avg_degree: float) -> int:
     """E = min(ceil(avg_degree * k), k * P): the number of edges that keeps
     the average degree of a kept token at avg_degree (Def. B.3 sets the edge
@@ -217,7 +261,7 @@ def row_budget(P: int, avg_degree: float) -> int:
 
 
 def bsca_edges(c: np.ndarray, avg_degree: float, rule: str = "question",
-               beta: float = 0.1) -> np.ndarray:
+               beta: float = 0.1, passage_keep: Optional[np.ndarray] = None) -> np.ndarray:
     """Boolean adjacency [k, P] cut from the compatibilities c (ties to the
     lower flattened index i * P + j under every rule):
 
@@ -227,8 +271,19 @@ def bsca_edges(c: np.ndarray, avg_degree: float, rule: str = "question",
     * "fraction": the fraction_budget(k, P, beta) largest of the question
       (top-beta sparsity, Sec. 3.5);
     * "row": each row's row_budget(P, avg_degree) largest (a per-row
-      threshold)."""
+      threshold).
+
+    With ``passage_keep`` (the verified passages, Alg. 1 verify step) the
+    graph is built on the kept passages only: the others get no edge and P
+    in every budget counts kept passages."""
     c = np.asarray(c, dtype=np.float64)
+    if passage_keep is not None:
+        keep = np.asarray(passage_keep, dtype=bool)
+        idx = np.nonzero(keep)[0]
+        sub = bsca_edges(c[:, idx], avg_degree, rule, beta)
+        adj = np.zeros(c.shape, dtype=bool)
+        adj[:, idx] = sub
+        return adj
     k, P = c.shape
     if rule == "row":
         D = row_budget(P, avg_degree)
@@ -398,7 +453,8 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
                     sm_scale: float, avg_degree: float = 4.0,
                     passage_key_table=None, adjacency: Optional[List[np.ndarray]] = None,
                     attn_rows: Optional[dict] = None, edge_rule: str = "question",
-                    edge_metric: str = "cosine", edge_beta: float = 0.1):
+                    edge_metric: str = "cosine", edge_beta: float = 0.1,
+                    passage_keep: Optional[np.ndarray] = None):
     """Graph + attention on caller-given kept-row queries Qh [sum k, H, d_h].
     ``adjacency`` (per question [k_b, P_b] bool) replaces the cosine rule
     when the caller brings its own graph.  Returns (cos, adj, O, LSE) lists."""
@@ -422,7 +478,8 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
         elif p1 > p0:
             Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
             c = compatibility(Q.reshape(k, H * d_h), Kbar, edge_metric)
-            adj = bsca_edges(c, avg_degree, edge_rule, edge_beta)
+            adj = bsca_edges(c, avg_degree, edge_rule, edge_beta,
+                             None if passage_keep is None else passage_keep[p0:p1])
         else:
             c = np.zeros((k, 0))
             adj = np.zeros((k, 0), dtype=bool)

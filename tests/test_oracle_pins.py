@@ -308,6 +308,85 @@ def test_row_rule_brute_force_ties_and_degree():
     assert orc.bsca_edges(c, 1.0, "row").tolist() == [[True, False, False], [True, False, False]]
 
 
+def test_skv_logits_worked_example():
+    # d = 1, h = 2; bf16-exact inputs.  q = 0.5, v = 2, e = (1, -1)
+    # x_0 = [0.5, 2, 1, 0.5, 0.5], x_1 = [0.5, 2, -1, -0.5, 1.5]
+    W = np.array([[1.0, 0.0, 1.0, 0.0, 0.0],     # q + e
+                  [0.0, 0.5, 0.0, 2.0, -1.0]])   # v/2 + 2 e*q - |e - q|
+    b1, w2, b2 = np.array([0.0, 0.25]), np.array([1.0, 1.0]), -1.0
+    # a_0 = (1.5, 1 + 1 - 0.5 + 0.25) = (1.5, 1.75) -> 3.25 - 1 = 2.25
+    # a_1 = (-0.5, 1 - 1 - 1.5 + 0.25) = (-0.5, -1.25) -> 0 - 1 = -1
+    z = orc.skv_logits(np.array([0.5]), np.array([2.0]), np.array([[1.0], [-1.0]]),
+                       W, b1, w2, b2)
+    np.testing.assert_allclose(z, [2.25, -1.0], rtol=0, atol=1e-15)
+    with pytest.raises(ValueError):
+        orc.skv_logits(np.zeros(2), np.zeros(2), np.zeros((3, 2)), np.zeros((1, 8)), None,
+                       np.zeros(1), 0.0)
+
+
+def test_skv_logits_blocks_and_rounding():
+    rng = np.random.default_rng(41)
+    d, P = 8, 5
+    q, v = rng.standard_normal(d), rng.standard_normal(d)
+    E = rng.standard_normal((P, d))
+    # only the e block: a linear function of the rounded embeddings
+    u = rng.standard_normal(d)
+    W = np.zeros((1, 5 * d))
+    W[0, 2 * d:3 * d] = u
+    z = orc.skv_logits(q, v, E, W, np.array([1e6]), np.array([1.0]), -1e6)
+    np.testing.assert_allclose(z, orc.round_bf16(E) @ u, rtol=1e-9, atol=1e-6)
+    # the |e - q| block is symmetric in e and q once both are rounded
+    W = np.zeros((1, 5 * d))
+    W[0, 4 * d:] = np.abs(rng.standard_normal(d))
+    qr = orc.round_bf16(q)
+    er = orc.round_bf16(E[0])
+    z1 = orc.skv_logits(qr, v, er[None, :], W, None, np.array([1.0]), 0.0)
+    z2 = orc.skv_logits(er, v, qr[None, :], W, None, np.array([1.0]), 0.0)
+    assert z1[0] == z2[0]
+    # q_bar and v_bar blocks add the same constant to every passage
+    W = np.zeros((1, 5 * d))
+    W[0, :2 * d] = rng.standard_normal(2 * d)
+    z = orc.skv_logits(q, v, E, W, np.array([1e6]), np.array([1.0]), -1e6)
+    assert np.ptp(z) < 1e-9
+
+
+def test_skv_keep_threshold_cap_and_ties():
+    z = np.array([0.3, -0.1, 2.0, 0.3, 0.0, -5.0])
+    # tau = 0.5: logit >= 0 -> {0, 2, 3, 4}; rho = 0.5 -> cap 3: 2, then 0 and 3 (tie, lower first)
+    assert orc.skv_keep(z, 0.5, 0.5).tolist() == [True, False, True, True, False, False]
+    assert orc.skv_keep(z, 0.5, 1.0).tolist() == [True, False, True, True, True, False]
+    # a stricter tau: sigma(z) >= 0.8 <=> z >= log 4
+    assert orc.skv_keep(z, 0.8, 1.0).tolist() == [False, False, True, False, False, False]
+    assert not orc.skv_keep(z, 0.999, 1.0).any()
+    # brute force against sigma directly
+    rng = np.random.default_rng(42)
+    for trial in range(50):
+        z = rng.standard_normal(int(rng.integers(1, 9)))
+        tau, rho = float(rng.uniform(0.2, 0.8)), float(rng.choice([0.25, 0.5, 1.0]))
+        nu = 1.0 / (1.0 + np.exp(-z))
+        ok = [j for j in range(len(z)) if nu[j] >= tau]
+        ok.sort(key=lambda j: (-nu[j], j))
+        want = np.zeros(len(z), dtype=bool)
+        want[ok[:math.ceil(rho * len(z) - 1e-9)]] = True
+        assert np.array_equal(orc.skv_keep(z, tau, rho), want)
+
+
+def test_edges_on_kept_passages_only():
+    rng = np.random.default_rng(43)
+    c = rng.uniform(-1, 1, (7, 6))
+    keep = np.array([True, False, True, True, False, True])
+    for rule in ("question", "row", "fraction"):
+        adj = orc.bsca_edges(c, 2.0, rule, 0.3, passage_keep=keep)
+        assert not adj[:, ~keep].any()
+        assert np.array_equal(adj[:, keep], orc.bsca_edges(c[:, keep], 2.0, rule, 0.3))
+        assert np.array_equal(orc.bsca_edges(c, 2.0, rule, 0.3, passage_keep=np.ones(6, bool)),
+                              orc.bsca_edges(c, 2.0, rule, 0.3))
+    # the budget counts kept passages: E = min(ceil(2 * 7), 7 * 4) = 14
+    assert orc.bsca_edges(c, 2.0, passage_keep=keep).sum() == 14
+    assert orc.bsca_edges(c, 9.0, passage_keep=keep).sum() == 28
+    assert not orc.bsca_edges(c, 2.0, passage_keep=np.zeros(6, bool)).any()
+
+
 def test_csr_from_adjacency():
     adj = np.array([[False, True, True], [False, False, False], [True, False, True]])
     rowptr, col = orc.adjacency_to_csr(adj)
