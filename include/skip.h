@@ -230,6 +230,57 @@ skip_status_t skip_prune_topk_mlp(const skip_problem_t* p, const skip_qvs_mlp_t*
                                   size_t workspace_bytes, void* stream);
 
 /*
+ * Passage verification gate (App. B.4, Def. B.4; Alg. 1, verify step).  For
+ * passage j of question b with embedding e_j (the passage key: the mean of its
+ * per-token keys, or passage_keys),
+ *   x_j = [q_bar ; v_bar ; e_j ; e_j (*) q_bar ; |e_j - q_bar|]   (width 5d),
+ *   logit_j = w2 . relu(W x_j + b1) + b2,   nu_j = sigmoid(logit_j),
+ * v_bar the mean of the question's kept visual rows (0 when it has none).
+ * Inputs enter as bf16 (q_bar, v_bar, e_j rounded through float32; the
+ * product rounded from its exact value; the difference rounded from its
+ * float32 value); products accumulate in float32.  The question keeps, among its passages with
+ * nu_j >= tau, the ceil(rho * P_b - 1e-9) largest nu (ties: lower index).
+ *   hidden  h: a multiple of 64, at most 4096
+ *   W       [h][5d] bf16 (blocks in the order of x)
+ *   b1      [h] float or NULL;  w2 [h] float;  b2 the output bias
+ *   tau     threshold on nu, in (0, 1) (paper: 0.5)
+ *   rho     kept fraction of a question's passages, in (0, 1]
+ * The activation is ReLU (the paper does not name one).
+ */
+typedef struct skip_skv_gate {
+  int32_t hidden;
+  int32_t reserved;        /* must be 0 */
+  const void* W;
+  const float* b1;
+  const float* w2;
+  double b2;
+  double tau;
+  double rho;
+} skip_skv_gate_t;
+
+/* Workspace of skip_skv_gate for problem `p` and hidden width `hidden`. */
+skip_status_t skip_workspace_bytes_gate(const skip_problem_t* p, int32_t hidden,
+                                        size_t* bytes);
+
+/*
+ * The gate.  V_kept [total_kept][d] are the kept visual rows (as written by
+ * skip_prune_topk), Qtok/q_offsets the question tokens, Kh/passage_offsets/
+ * query_passages/passage_keys as in skip_bipartite_xattn (passage_keys NULL:
+ * pooled from Kh; Kh may then not be NULL).
+ *   logits  out [total_passages] float: logit_j, or NULL
+ *   keep    out [total_passages] uint8: 1 for a kept passage, else 0; the
+ *           cut is taken on the float logits (the values written to logits)
+ * bf16 only (SKIP_ERR_UNSUPPORTED otherwise); d a multiple of 32.
+ */
+skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate,
+                            const void* Qtok, const int32_t* q_offsets,
+                            const void* V_kept, const int32_t* kept_offsets,
+                            const void* Kh, const int32_t* passage_offsets,
+                            const int32_t* query_passages, const float* passage_keys,
+                            float* logits, uint8_t* keep, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
  * Stage 2: bipartite graph + sparse cross-attention (Def. B.3; Alg. 1,
  * graph and fuse steps) on caller-given kept-row queries.
  *   Qh              [total_kept][H][d_h] queries of the kept rows
@@ -263,6 +314,25 @@ skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
                                    int32_t* edge_rowptr_out,
                                    int32_t* edge_col_out, void* workspace,
                                    size_t workspace_bytes, void* stream);
+
+/*
+ * skip_bipartite_xattn on the verified passages only (Alg. 1: the graph is
+ * built over the passages the gate keeps).  passage_keep [total_passages]
+ * uint8 (0: dropped) as written by skip_skv_gate: a dropped passage gets no
+ * edge, and P_b in every edge budget counts the kept passages of question b.
+ * Requires the graph to be built here (edge_rowptr and edge_col NULL).  Other
+ * arguments and results as in skip_bipartite_xattn.
+ */
+skip_status_t skip_bipartite_xattn_masked(const skip_problem_t* p, const void* Qh,
+                                          const int32_t* kept_offsets, const void* Kh,
+                                          const void* Vh,
+                                          const int32_t* passage_offsets,
+                                          const int32_t* query_passages,
+                                          const float* passage_keys,
+                                          const uint8_t* passage_keep, void* O,
+                                          float* lse, int32_t* edge_rowptr_out,
+                                          int32_t* edge_col_out, void* workspace,
+                                          size_t workspace_bytes, void* stream);
 
 /*
  * Both stages fused (Alg. 1: scoring, TopK, graph, fuse): the kept visual

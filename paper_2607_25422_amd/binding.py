@@ -29,7 +29,8 @@ SKIP_F32, SKIP_BF16 = 0, 1
 ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes",
                 "skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused",
                 "skip_route_fused_profiled", "skip_workspace_bytes_mlp",
-                "skip_prune_topk_mlp")
+                "skip_prune_topk_mlp", "skip_workspace_bytes_gate", "skip_skv_gate",
+                "skip_bipartite_xattn_masked")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -59,6 +60,15 @@ class SkipQvsMlp(ctypes.Structure):
         ("hidden", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
         ("b2", ctypes.c_double),
+    ]
+
+
+class SkipSkvGate(ctypes.Structure):
+    """skip_skv_gate_t: the passage gate's weights (device pointers) and cuts."""
+    _fields_ = [
+        ("hidden", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("W", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+        ("b2", ctypes.c_double), ("tau", ctypes.c_double), ("rho", ctypes.c_double),
     ]
 
 
@@ -96,6 +106,16 @@ def _load() -> ctypes.CDLL:
     lib.skip_prune_topk_mlp.restype = ctypes.c_int
     lib.skip_prune_topk_mlp.argtypes = [P, M, vp, vp, i32p, i32p, i32p, vp, vp, vp,
                                         ctypes.c_size_t, vp]
+    G = ctypes.POINTER(SkipSkvGate)
+    lib.skip_workspace_bytes_gate.restype = ctypes.c_int
+    lib.skip_workspace_bytes_gate.argtypes = [P, ctypes.c_int32,
+                                              ctypes.POINTER(ctypes.c_size_t)]
+    lib.skip_skv_gate.restype = ctypes.c_int
+    lib.skip_skv_gate.argtypes = [P, G, vp, i32p, vp, i32p, vp, i32p, i32p, vp, vp, vp, vp,
+                                  ctypes.c_size_t, vp]
+    lib.skip_bipartite_xattn_masked.restype = ctypes.c_int
+    lib.skip_bipartite_xattn_masked.argtypes = [P, vp, i32p, vp, vp, i32p, i32p, vp, vp, vp,
+                                                vp, i32p, i32p, vp, ctypes.c_size_t, vp]
     lib.skip_route_fused_profiled.restype = ctypes.c_int
     lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                               vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
@@ -177,6 +197,13 @@ def workspace_bytes_mlp(p: SkipProblem, hidden: int) -> int:
     n = ctypes.c_size_t(0)
     _check(LIB.skip_workspace_bytes_mlp(ctypes.byref(p), int(hidden), ctypes.byref(n)),
            "skip_workspace_bytes_mlp")
+    return int(n.value)
+
+
+def workspace_bytes_gate(p: SkipProblem, hidden: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.skip_workspace_bytes_gate(ctypes.byref(p), int(hidden), ctypes.byref(n)),
+           "skip_workspace_bytes_gate")
     return int(n.value)
 
 
@@ -277,6 +304,54 @@ def skip_bipartite_xattn(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passage_offse
         _ptr(edge_col_out, "edge_col_out", torch.int32, p.total_kept * p.P_max),
         wsp, wsn, _stream(stream))
     _check(st, "skip_bipartite_xattn")
+
+
+def skip_skv_gate(p: SkipProblem, gate: "SkvGate", Qtok, q_offsets, V_kept, kept_offsets,
+                  Kh, passage_offsets, query_passages, keep, logits=None, passage_keys=None,
+                  workspace=None, stream=None):
+    et = _elem_dtype(p)
+    h = gate.hidden
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes_gate(p, h), dtype=torch.uint8,
+                                device=Qtok.device)
+    g = SkipSkvGate(h, 0, _ptr(gate.W, "W", et, h * 5 * p.d),
+                    _ptr(gate.b1, "b1", torch.float32, h), _ptr(gate.w2, "w2", torch.float32, h),
+                    float(gate.b2), float(gate.tau), float(gate.rho))
+    st = LIB.skip_skv_gate(
+        ctypes.byref(p), ctypes.byref(g), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
+        _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1),
+        _ptr(V_kept, "V_kept", et, p.total_kept * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(logits, "logits", torch.float32, p.total_passages),
+        _ptr(keep, "keep", torch.uint8, p.total_passages), workspace.data_ptr(),
+        workspace.numel(), _stream(stream))
+    _check(st, "skip_skv_gate")
+
+
+def skip_bipartite_xattn_masked(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passage_offsets,
+                                query_passages, passage_keep, O, lse=None, passage_keys=None,
+                                edge_rowptr_out=None, edge_col_out=None, workspace=None,
+                                stream=None):
+    et = _elem_dtype(p)
+    ws, wsp, wsn = _ws(p, workspace)
+    st = LIB.skip_bipartite_xattn_masked(
+        ctypes.byref(p), _ptr(Qh, "Qh", et, p.total_kept * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d), _ptr(Vh, "Vh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(passage_keep, "passage_keep", torch.uint8, p.total_passages),
+        _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
+        _ptr(lse, "lse", torch.float32, p.total_kept * p.H),
+        _ptr(edge_rowptr_out, "edge_rowptr_out", torch.int32, p.total_kept + 1),
+        _ptr(edge_col_out, "edge_col_out", torch.int32, p.total_kept * p.P_max),
+        wsp, wsn, _stream(stream))
+    _check(st, "skip_bipartite_xattn_masked")
 
 
 def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
@@ -439,6 +514,56 @@ def bipartite_xattn(db: DeviceBatch, Qh: torch.Tensor, passage_keys=None, edges=
                          lse if p.total_kept else None, passage_keys,
                          None if edges is None else edges[0],
                          None if edges is None else edges[1], rp, col, db.workspace)
+    return O[:p.total_kept], lse[:p.total_kept], rp, col
+
+
+@dataclass
+class SkvGate:
+    """Device tensors of the passage gate: W [h, 5d] (element type of V), b1
+    [h] float32 or None, w2 [h] float32; scalars b2, tau (threshold on the
+    gate probability) and rho (kept fraction of a question's passages)."""
+    W: torch.Tensor
+    b1: Optional[torch.Tensor]
+    w2: torch.Tensor
+    b2: float
+    tau: float = 0.5
+    rho: float = 0.5
+
+    @property
+    def hidden(self) -> int:
+        return int(self.W.shape[0])
+
+
+def skv_gate(db: DeviceBatch, gate: SkvGate, V_kept: torch.Tensor, passage_keys=None,
+             workspace=None):
+    """The passage gate on the kept rows V_kept [total_kept, d].  Returns
+    (keep [total_passages] uint8, logits [total_passages] float32)."""
+    p = db.p
+    dev = db.V.device
+    keep = torch.empty(max(p.total_passages, 1), dtype=torch.uint8, device=dev)
+    logits = torch.empty(max(p.total_passages, 1), dtype=torch.float32, device=dev)
+    skip_skv_gate(p, gate, db.Qtok, db.q_offsets, V_kept if p.total_kept else None,
+                  db.kept_offsets, db.Kh, db.passage_offsets, db.query_passages, keep, logits,
+                  passage_keys, workspace)
+    return keep[:p.total_passages], logits[:p.total_passages]
+
+
+def bipartite_xattn_masked(db: DeviceBatch, Qh: torch.Tensor, passage_keep: torch.Tensor,
+                           passage_keys=None, want_edges=True) -> Tuple:
+    """bipartite_xattn over the passages with passage_keep != 0.  Returns
+    (O, lse, rowptr, col)."""
+    p = db.p
+    dev = db.V.device
+    O = torch.empty((max(p.total_kept, 1), p.H, p.d_h), dtype=_out_dtype(p), device=dev)
+    lse = torch.empty((max(p.total_kept, 1), p.H), dtype=torch.float32, device=dev)
+    rp = col = None
+    if want_edges:
+        rp = torch.empty(p.total_kept + 1, dtype=torch.int32, device=dev)
+        col = torch.empty(max(p.total_kept * p.P_max, 1), dtype=torch.int32, device=dev)
+    skip_bipartite_xattn_masked(p, Qh if p.total_kept else None, db.kept_offsets, db.Kh, db.Vh,
+                                db.passage_offsets, db.query_passages, passage_keep,
+                                O if p.total_kept else None, lse if p.total_kept else None,
+                                passage_keys, rp, col, db.workspace)
     return O[:p.total_kept], lse[:p.total_kept], rp, col
 
 

@@ -172,7 +172,7 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
                    const int32_t* __restrict__ kept_offsets,
                    const int32_t* __restrict__ query_passages, int B, int total_kept,
                    int total_passages, int k_max, int P_max, int d, double avg_degree,
-                   int rule, int metric, double beta,
+                   int rule, int metric, double beta, const uint8_t* __restrict__ keep,
                    uint64_t* __restrict__ rowmask, int32_t* __restrict__ rowptr_out,
                    int32_t* __restrict__ col_out) {
   __shared__ SelectShared sh;
@@ -186,7 +186,15 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
   const int k = min(k1 - k0, k_max);
   const int P = min(min(p1 - p0, P_max), 64);
   const int n = min(k * P, kGSelThreads * kGSelMaxPT);
-  const int E = (int)edges_of_question(k, P, rule, avg_degree, beta);
+  // passages the verification gate dropped take no edge and do not count in
+  // the budget: their candidates get the lowest key
+  uint64_t pkeep = (P >= 64) ? ~0ull : ((1ull << P) - 1ull);
+  if (keep) {
+    pkeep = 0ull;
+    for (int j = 0; j < P; ++j) pkeep |= (keep[p0 + j] ? 1ull : 0ull) << j;
+  }
+  const int Pk = __popcll(pkeep);
+  const int E = (int)edges_of_question(k, Pk, rule, avg_degree, beta);
   const double inv_sqrt_d = 1.0 / sqrt((double)d);
 
   const int C = (n + blockDim.x - 1) / blockDim.x;
@@ -220,7 +228,7 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
         const double nq = sqrt(q2), nk = sqrt(k2);
         c = (nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0;
       }
-      keys[jj] = order_key(c);
+      keys[jj] = ((pkeep >> j) & 1ull) ? order_key(c) : 0ull;
     }
   }
   uint32_t flags;
@@ -230,7 +238,7 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
     for (int jj = 0; jj < kGSelMaxPT; ++jj)
       if (jj < cnt) rkeys[e0 + jj] = keys[jj];
     __syncthreads();
-    const int D = (int)fmin((double)P, ceil(avg_degree));
+    const int D = (int)fmin((double)Pk, ceil(avg_degree));
     for (int i = threadIdx.x; i < k && (i + 1) * P <= n; i += blockDim.x) {
       const uint64_t* rk = rkeys + i * P;
       for (int j = 0; j < P; ++j) {
@@ -270,7 +278,12 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
     range_of(kept_offsets, bb, total_kept, a0, a1);
     range_of(query_passages, bb, total_passages, q0, q1);
     const int kq = min(a1 - a0, k_max), Pq = min(min(q1 - q0, P_max), 64);
-    base += edges_of_question(kq, Pq, rule, avg_degree, beta);
+    int Pkq = Pq;
+    if (keep) {
+      Pkq = 0;
+      for (int j = 0; j < Pq; ++j) Pkq += keep[q0 + j] ? 1 : 0;
+    }
+    base += edges_of_question(kq, Pkq, rule, avg_degree, beta);
   }
   uint32_t total;
   uint32_t pos = block_exclusive_scan(__popc(flags), scan_sh, &total);
@@ -355,11 +368,12 @@ hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
 hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
                               const int32_t* kept_offsets, const int32_t* query_passages,
                               uint64_t* rowmask, int32_t* rowptr_out, int32_t* col_out,
-                              hipStream_t s) {
+                              hipStream_t s, const uint8_t* passage_keep) {
   hipLaunchKernelGGL(edge_select_kernel, dim3(p.B), dim3(kGSelThreads), 0, s, ep.part,
                      ep.qn2, ep.kn2, edge_slices(p), kept_offsets, query_passages, p.B,
                      p.total_kept, p.total_passages, p.k_max, p.P_max, p.d, p.avg_degree,
-                     p.edge_rule, p.edge_metric, p.edge_beta, rowmask, rowptr_out, col_out);
+                     p.edge_rule, p.edge_metric, p.edge_beta, passage_keep, rowmask,
+                     rowptr_out, col_out);
   return hipGetLastError();
 }
 

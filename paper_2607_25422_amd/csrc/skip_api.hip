@@ -210,14 +210,13 @@ skip_status_t skip_prune_topk_mlp(const skip_problem_t* p, const skip_qvs_mlp_t*
   return SKIP_OK;
 }
 
-skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
-                                   const int32_t* kept_offsets, const void* Kh, const void* Vh,
-                                   const int32_t* passage_offsets,
-                                   const int32_t* query_passages, const float* passage_keys,
-                                   const int32_t* edge_rowptr, const int32_t* edge_col,
-                                   void* O, float* lse, int32_t* edge_rowptr_out,
-                                   int32_t* edge_col_out, void* workspace,
-                                   size_t workspace_bytes, void* stream) {
+static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh,
+                                const int32_t* kept_offsets, const void* Kh, const void* Vh,
+                                const int32_t* passage_offsets, const int32_t* query_passages,
+                                const float* passage_keys, const int32_t* edge_rowptr,
+                                const int32_t* edge_col, const uint8_t* passage_keep, void* O,
+                                float* lse, int32_t* edge_rowptr_out, int32_t* edge_col_out,
+                                void* workspace, size_t workspace_bytes, void* stream) {
   skip_status_t st = check(p, kGraph);
   if (st != SKIP_OK) return st;
   if (!kept_offsets || !query_passages || !passage_offsets || !workspace)
@@ -231,11 +230,12 @@ skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
   if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Workspace w = carve_workspace(*p, workspace);
+  const EdgePartials ep{w.part, w.qn2, w.kn2};
   if (p->total_kept == 0) {
     // No kept rows: only the (empty) CSR needs its closing offset.
     if (edge_rowptr_out)
-      SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets, query_passages, w.rowmask,
-                                  edge_rowptr_out, edge_col_out, s));
+      SKIP_TRY(launch_edge_select(*p, ep, kept_offsets, query_passages, w.rowmask,
+                                  edge_rowptr_out, edge_col_out, s, passage_keep));
     return SKIP_OK;
   }
   QuerySource q{Qh, nullptr, 0};
@@ -244,13 +244,99 @@ skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
                                 w.rowmask, s));
   } else {
     if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-    SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
-                             EdgePartials{w.part, w.qn2, w.kn2}, s));
-    SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets, query_passages, w.rowmask,
-                                edge_rowptr_out, edge_col_out, s));
+    SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys, ep, s));
+    SKIP_TRY(launch_edge_select(*p, ep, kept_offsets, query_passages, w.rowmask,
+                                edge_rowptr_out, edge_col_out, s, passage_keep));
   }
   SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
                             w.rowmask, O, lse, s));
+  return SKIP_OK;
+}
+
+skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
+                                   const int32_t* kept_offsets, const void* Kh, const void* Vh,
+                                   const int32_t* passage_offsets,
+                                   const int32_t* query_passages, const float* passage_keys,
+                                   const int32_t* edge_rowptr, const int32_t* edge_col,
+                                   void* O, float* lse, int32_t* edge_rowptr_out,
+                                   int32_t* edge_col_out, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  return xattn_impl(p, Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages, passage_keys,
+                    edge_rowptr, edge_col, nullptr, O, lse, edge_rowptr_out, edge_col_out,
+                    workspace, workspace_bytes, stream);
+}
+
+skip_status_t skip_bipartite_xattn_masked(const skip_problem_t* p, const void* Qh,
+                                          const int32_t* kept_offsets, const void* Kh,
+                                          const void* Vh, const int32_t* passage_offsets,
+                                          const int32_t* query_passages,
+                                          const float* passage_keys,
+                                          const uint8_t* passage_keep, void* O, float* lse,
+                                          int32_t* edge_rowptr_out, int32_t* edge_col_out,
+                                          void* workspace, size_t workspace_bytes,
+                                          void* stream) {
+  if (!passage_keep && p && p->total_passages > 0) return SKIP_ERR_INVALID_ARG;
+  return xattn_impl(p, Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages, passage_keys,
+                    nullptr, nullptr, passage_keep, O, lse, edge_rowptr_out, edge_col_out,
+                    workspace, workspace_bytes, stream);
+}
+
+static_assert(sizeof(skip_skv_gate_t) == 56 && offsetof(skip_skv_gate_t, b2) == 32 &&
+                  offsetof(skip_skv_gate_t, rho) == 48,
+              "skip_skv_gate_t layout is part of the ABI");
+
+static bool gate_hidden_ok(int32_t hidden) {
+  return hidden % 64 == 0 && hidden <= 4096;
+}
+
+skip_status_t skip_workspace_bytes_gate(const skip_problem_t* p, int32_t hidden, size_t* bytes) {
+  if (!bytes) return SKIP_ERR_INVALID_ARG;
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (p->N < 0 || p->P_max < 0 || p->total_passages < 0) return SKIP_ERR_INVALID_ARG;
+  if (hidden <= 0) return SKIP_ERR_INVALID_ARG;
+  if (!gate_hidden_ok(hidden)) return SKIP_ERR_UNSUPPORTED;
+  *bytes = workspace_size(*p) + gate_scratch_bytes(*p, hidden);
+  return SKIP_OK;
+}
+
+skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate,
+                            const void* Qtok, const int32_t* q_offsets, const void* V_kept,
+                            const int32_t* kept_offsets, const void* Kh,
+                            const int32_t* passage_offsets, const int32_t* query_passages,
+                            const float* passage_keys, float* logits, uint8_t* keep,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  skip_status_t st = check(p, kGraph);
+  if (st != SKIP_OK) return st;
+  if (!gate || !Qtok || !q_offsets || !kept_offsets || !query_passages || !workspace)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->total_qtok < p->B) return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && !V_kept) return SKIP_ERR_INVALID_ARG;
+  if (p->total_passages > 0 && !keep) return SKIP_ERR_INVALID_ARG;
+  if (!passage_keys && p->total_passages > 0 && (!Kh || !passage_offsets))
+    return SKIP_ERR_INVALID_ARG;
+  if (gate->reserved != 0 || !gate->W || !gate->w2 || gate->hidden <= 0 ||
+      !std::isfinite(gate->b2) || !(gate->tau > 0.0 && gate->tau < 1.0) ||
+      !(gate->rho > 0.0 && gate->rho <= 1.0))
+    return SKIP_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(gate->W) % 16 != 0) return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || !gate_hidden_ok(gate->hidden))
+    return SKIP_ERR_UNSUPPORTED;
+  if ((int64_t)gate->hidden * 5 * p->d > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  const size_t need = workspace_size(*p) + gate_scratch_bytes(*p, gate->hidden);
+  if (workspace_bytes < need) return SKIP_ERR_WORKSPACE;
+  if (p->total_passages == 0) return SKIP_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Workspace w = carve_workspace(*p, workspace);
+  GateScratch g = carve_gate_scratch(*p, gate->hidden, static_cast<char*>(workspace) + w.bytes);
+  // plain means: q_bar (question tokens) into u, v_bar (kept rows) into g.vbar,
+  // and the passage keys when they are not given
+  SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, Qtok,
+                        q_offsets, p->B, p->total_qtok, w.u, s));
+  SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, V_kept,
+                        kept_offsets, p->B, p->total_kept, g.vbar, s));
+  if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
+  SKIP_TRY(launch_gate(*p, *gate, w.u, w.kbar, passage_keys, query_passages, g, logits, keep, s));
   return SKIP_OK;
 }
 

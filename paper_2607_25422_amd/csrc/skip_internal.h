@@ -50,6 +50,24 @@ hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, c
                              const double* qbar, MlpScratch ms, double* z, float* scores,
                              hipStream_t s);
 
+// Passage verification gate ---------------------------------------------
+struct GateScratch {
+  double* vbar;      // [B][d]         mean of the kept visual rows
+  bf16_t* X;         // [T][3d]        passage part of the gate input
+  bf16_t* QV;        // [B][2d]        question part [q_bar' ; v_bar']
+  float* cvec;       // [B][h]         W[:, 0:2d] [q_bar' ; v_bar'] + b1
+  float* part;       // [h/64][T]      partial logits per 64 hidden units
+  int32_t* pq;       // [T]            question of each passage
+};
+size_t gate_scratch_bytes(const skip_problem_t& p, int hidden);
+GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base);
+// qbar: plain question means; kbar: pooled passage keys (unused when
+// passage_keys is given); g.vbar must hold the kept-row means.
+hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* qbar,
+                       const double* kbar, const float* passage_keys,
+                       const int32_t* query_passages, GateScratch g, float* logits,
+                       uint8_t* keep, hipStream_t s);
+
 // Stage 2 ---------------------------------------------------------------
 // Query rows: if kept_idx is non-NULL, row r of question b is
 // V[b][kept_idx[r]] (the fused route); otherwise it is Qh[r].
@@ -76,7 +94,7 @@ hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
                               const int32_t* kept_offsets,
                               const int32_t* query_passages, uint64_t* rowmask,
                               int32_t* rowptr_out, int32_t* col_out,
-                              hipStream_t s);
+                              hipStream_t s, const uint8_t* passage_keep = nullptr);
 hipError_t launch_csr_to_mask(const skip_problem_t& p, const int32_t* kept_offsets,
                               const int32_t* query_passages,
                               const int32_t* edge_rowptr, const int32_t* edge_col,

@@ -330,3 +330,45 @@ def make_scorer_weights(wl: Workload | str, hidden: int = 512, seed: int = 2026)
     return ScorerWeights(W1=_round(W1, "bf16"), b1=torch.from_numpy(b1.astype(np.float32)),
                          w2=torch.from_numpy(w2.astype(np.float32)),
                          b2=float(rng.standard_normal()))
+
+
+@dataclass
+class GateWeights:
+    """Synthetic weights of the passage verification gate, a two-layer
+    perceptron on [q_bar; v_bar; e; e * q_bar; |e - q_bar|] (CPU tensors):
+    W [h, 5d] bfloat16, b1 [h] and w2 [h] float32, b2 a float."""
+
+    W: torch.Tensor
+    b1: torch.Tensor
+    w2: torch.Tensor
+    b2: float
+
+    @property
+    def hidden(self) -> int:
+        return int(self.W.shape[0])
+
+
+def make_gate_weights(wl: Workload | str, hidden: int = 512, seed: int = 2026) -> GateWeights:
+    """Gaussian weights scaled so that each of the five input blocks adds a
+    term of order one to a hidden pre-activation for this workload's
+    distributions: with s_v the per-coordinate scale of a visual or question
+    token (1 or 1/sqrt(d)) and 0.5 that of a passage key, the block standard
+    deviations are sqrt(T)/(sqrt(d) s_v) for q_bar (a mean of T tokens),
+    1/(sqrt(d) s_v) for v_bar, 2/sqrt(d) for e and |e - q_bar|, and
+    2 sqrt(T)/(sqrt(d) s_v) for the product.  b1 is a small Gaussian, w2 ~
+    N(0, 1/h) and b2 = 0, so a threshold of 1/2 on the gate probability
+    passes about half of the passages.  No trained gate exists; the paper does
+    not state its hidden width (512 here)."""
+    if isinstance(wl, str):
+        wl = WORKLOADS[wl]
+    d = wl.d
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, wl.wid, 104729])))
+    sv = 1.0 if wl.visual == "unit" else 1.0 / math.sqrt(d)
+    rd = 1.0 / math.sqrt(d)
+    sds = (math.sqrt(wl.T) * rd / sv, rd / sv, 2.0 * rd, 2.0 * math.sqrt(wl.T) * rd / sv,
+           2.0 * rd)
+    W = np.concatenate([rng.standard_normal((hidden, d)) * s for s in sds], axis=1)
+    b1 = rng.standard_normal(hidden) * 0.1
+    w2 = rng.standard_normal(hidden) / math.sqrt(hidden)
+    return GateWeights(W=_round(W, "bf16"), b1=torch.from_numpy(b1.astype(np.float32)),
+                       w2=torch.from_numpy(w2.astype(np.float32)), b2=0.0)

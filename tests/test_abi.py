@@ -184,3 +184,63 @@ def test_fused_requires_matching_head_split(b):
     st = b.LIB.skip_route_fused(ctypes.byref(p), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
                                 FAKE, FAKE, None, None, FAKE, None, FAKE, 1 << 30, None)
     assert st == b.SKIP_ERR_INVALID_ARG                                   # kept_idx NULL
+
+
+def test_gate_struct_and_validation(b):
+    assert ctypes.sizeof(b.SkipSkvGate) == 56
+    assert b.SkipSkvGate.b2.offset == 32
+    assert b.SkipSkvGate.rho.offset == 48
+    p = _problem(b)
+    n = b.workspace_bytes_gate(p, 256)
+    assert n > b.workspace_bytes(p)
+    assert b.workspace_bytes_gate(p, 512) > n
+
+    def gate(h=256, reserved=0, W=FAKE, w2=FAKE, b2=0.0, tau=0.5, rho=0.5):
+        return b.SkipSkvGate(h, reserved, W, None, w2, b2, tau, rho)
+
+    def call(q, g=None, ws_bytes=1 << 30, **kw):
+        g = g if g is not None else gate()
+        a = dict(Qtok=FAKE, qo=FAKE, Vk=FAKE, ko=FAKE, Kh=FAKE, po=FAKE, qp=FAKE, pk=None,
+                 logits=None, keep=FAKE)
+        a.update(kw)
+        return b.LIB.skip_skv_gate(ctypes.byref(q), ctypes.byref(g) if g is not False else None,
+                                   a["Qtok"], a["qo"], a["Vk"], a["ko"], a["Kh"], a["po"],
+                                   a["qp"], a["pk"], a["logits"], a["keep"], FAKE, ws_bytes,
+                                   None)
+    # every call fails validation (the last ones on the workspace size)
+    assert call(p, g=False) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, Qtok=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, keep=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, Vk=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, Kh=None) == b.SKIP_ERR_INVALID_ARG        # keys neither given nor poolable
+    assert call(p, g=gate(reserved=1)) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, g=gate(W=None)) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, g=gate(W=FAKE + 8)) == b.SKIP_ERR_INVALID_ARG        # 16-byte alignment
+    assert call(p, g=gate(b2=float("nan"))) == b.SKIP_ERR_INVALID_ARG
+    for tau in (0.0, 1.0, -0.1, float("nan")):
+        assert call(p, g=gate(tau=tau)) == b.SKIP_ERR_INVALID_ARG, tau
+    for rho in (0.0, 1.5, float("nan")):
+        assert call(p, g=gate(rho=rho)) == b.SKIP_ERR_INVALID_ARG, rho
+    assert call(p, g=gate(h=96)) == b.SKIP_ERR_UNSUPPORTED
+    assert call(p, g=gate(h=8192)) == b.SKIP_ERR_UNSUPPORTED
+    q = b.make_problem("f32", B=2, N=576, d=1024, H=16, d_h=64, q_offsets=[0, 3, 7],
+                       kept_offsets=[0, 96, 192], passage_offsets=[0, 10, 20, 30],
+                       query_passages=[0, 2, 3], sm_scale=0.125)
+    assert call(q) == b.SKIP_ERR_UNSUPPORTED                              # bf16 only
+    assert call(p, ws_bytes=b.workspace_bytes_gate(p, 256) - 1) == b.SKIP_ERR_WORKSPACE
+    assert call(p, Kh=None, pk=FAKE, ws_bytes=0) == b.SKIP_ERR_WORKSPACE  # given keys: no Kh
+    with pytest.raises(b.SkipError):
+        b.workspace_bytes_gate(p, 100)
+
+
+def test_masked_xattn_validation(b):
+    p = _problem(b)
+
+    def call(q, keep=FAKE, ws_bytes=1 << 30, O=FAKE):
+        return b.LIB.skip_bipartite_xattn_masked(ctypes.byref(q), FAKE, FAKE, FAKE, FAKE, FAKE,
+                                                 FAKE, None, keep, O, None, None, None, FAKE,
+                                                 ws_bytes, None)
+    assert call(p, keep=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, O=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, ws_bytes=0) == b.SKIP_ERR_WORKSPACE
+    assert call(_problem(b, H=8)) == b.SKIP_ERR_INVALID_ARG
