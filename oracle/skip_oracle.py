@@ -48,7 +48,7 @@ for the special cases that reduce to them, and invariants.
 from __future__ import annotations
 
 import math
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -378,6 +378,8 @@ class RouteResult:
     adj: List[np.ndarray]             # per question [k_b, P_b] bool
     O: List[np.ndarray]               # per question [k_b, H, d_h]
     LSE: List[np.ndarray]             # per question [k_b, H]
+    gate_logits: List[np.ndarray] = field(default_factory=list)   # per question [P_b]
+    keep: List[np.ndarray] = field(default_factory=list)          # per question [P_b] bool
 
 
 def _f64(x) -> np.ndarray:
@@ -392,7 +394,8 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
           w_bias=None, passage_key_table=None, queries: Optional[Sequence[int]] = None,
           attn_rows: Optional[dict] = None, with_attention: bool = True,
           edge_rule: str = "question", edge_metric: str = "cosine",
-          edge_beta: float = 0.1, mlp: Optional[dict] = None) -> RouteResult:
+          edge_beta: float = 0.1, mlp: Optional[dict] = None,
+          gate: Optional[dict] = None) -> RouteResult:
     """Prune, build the graph and attend, question by question.
 
     V: [B, N, d]; Qtok: [sum T, d]; Kh, Vh: [sum M, H, d_h]; offsets as in
@@ -402,7 +405,10 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
     question to the kept rows whose attention output is wanted.  With
     ``mlp`` (keys W1, b1, w2, b2) the tokens are ranked by the main-text
     scorer instead of the linear logit; the ``z`` and ``scores`` of the
-    result are then both the scorer's s."""
+    result are then both the scorer's s.  With ``gate`` (keys W, b1, w2,
+    b2, tau, rho) the verification step of Alg. 1 runs between the top-k and
+    the graph: v_bar is the mean of the kept rows (0 when there are none),
+    e_j the passage keys, and the graph is built on the kept passages only."""
     w = None if w_bias is None else _f64(w_bias)
     pk = None if passage_key_table is None else _f64(passage_key_table)
     B, N, d = V.shape
@@ -426,13 +432,24 @@ def route(V, Qtok, q_offsets, kept_offsets, Kh, Vh, passage_offsets,
                   for j in range(p0, p1)]
         t1 = int(passage_offsets[p1]) if p1 > p0 else 0
         Kq, Vq = _f64(Kh[t0:t1]), _f64(Vh[t0:t1])
+        keep = None
         if p1 > p0:
             Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
+            if gate is not None:
+                v_bar = Vhat.sum(axis=0) / k if k > 0 else np.zeros(d)
+                gl = skv_logits(q_bar, v_bar, Kbar, gate["W"], gate.get("b1"), gate["w2"],
+                                gate["b2"])
+                keep = skv_keep(gl, gate["tau"], gate["rho"])
+                res.gate_logits.append(gl)
+                res.keep.append(keep)
             c = compatibility(Vhat, Kbar, edge_metric)
-            adj = bsca_edges(c, avg_degree, edge_rule, edge_beta)
+            adj = bsca_edges(c, avg_degree, edge_rule, edge_beta, keep)
         else:
             c = np.zeros((k, 0))
             adj = np.zeros((k, 0), dtype=bool)
+            if gate is not None:
+                res.gate_logits.append(np.zeros(0))
+                res.keep.append(np.zeros(0, dtype=bool))
         if with_attention:
             rows = None if attn_rows is None else attn_rows.get(b, [])
             O, LSE = bsca_attention(Vhat.reshape(k, H, d_h), Kq, Vq, ranges, adj,

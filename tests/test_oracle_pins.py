@@ -580,3 +580,59 @@ def test_route_small_ragged_properties(seed):
         empty = ~r.adj[q].any(axis=1) if P else np.ones(k, dtype=bool)
         assert np.all(r.O[q][empty] == 0)
         assert np.all(r.LSE[q][empty] == -np.inf)
+
+
+def _gate_dict(d, h, b2, rng, tau=0.5, rho=1.0):
+    return dict(W=rng.standard_normal((h, 5 * d)) / math.sqrt(5 * d), b1=None,
+                w2=rng.standard_normal(h) / math.sqrt(h), b2=b2, tau=tau, rho=rho)
+
+
+def test_route_with_gate_limits():
+    """A gate that passes everything (large b2, rho = 1) leaves the route as
+    it was; one that passes nothing leaves every kept row without neighbours."""
+    b = wls.make_batch("mixed_bf16", 5, B=3, N=200, H=4, d_h=16, T=(2, 5), k=(9, 30),
+                       P=(1, 4, 6), L_p=(3, 7))
+    rng = np.random.default_rng(5)
+    plain = _route(b)
+    open_ = _route(b, gate=_gate_dict(64, 32, 1e3, rng))
+    shut = _route(b, gate=_gate_dict(64, 32, -1e3, rng))
+    for q in range(b.B):
+        assert open_.keep[q].all() and not shut.keep[q].any()
+        assert np.array_equal(open_.adj[q], plain.adj[q])
+        np.testing.assert_array_equal(open_.O[q], plain.O[q])
+        assert not shut.adj[q].any()
+        assert np.all(shut.O[q] == 0) and np.all(shut.LSE[q] == -np.inf)
+
+
+def test_route_gate_sees_the_mean_of_the_kept_rows():
+    """A gate whose only weight reads coordinate c of the v_bar block: its
+    logit is relu of the bfloat16 rounding of the mean of the kept rows'
+    coordinate c (the rows named by the route's own top-k)."""
+    b = wls.make_batch("mixed_bf16", 9, B=2, N=150, H=4, d_h=16, T=(3,), k=(1, 17),
+                       P=(2, 3), L_p=(4,))
+    d = 64
+    for c in (0, 37):
+        W = np.zeros((1, 5 * d))
+        W[0, d + c] = 1.0
+        g = dict(W=W, b1=None, w2=np.ones(1), b2=0.0, tau=0.5, rho=1.0)
+        r = _route(b, gate=g)
+        for q in range(b.B):
+            rows = b.V[q].double().numpy()[r.kept_idx[q]]
+            want = max(float(orc.round_bf16(np.array([rows[:, c].mean()]))[0]), 0.0)
+            assert np.allclose(r.gate_logits[q], want, rtol=0, atol=0)
+            assert r.keep[q].tolist() == [want >= 0.0] * int(b.P[q])
+
+
+def test_route_gate_drops_passages_from_the_graph():
+    b = wls.make_batch("mixed_bf16", 13, B=4, N=200, H=4, d_h=16, T=(2,), k=(12, 40),
+                       P=(3, 6), L_p=(5,))
+    rng = np.random.default_rng(13)
+    g = _gate_dict(64, 64, 0.0, rng, tau=0.5, rho=0.5)
+    r = _route(b, gate=g)
+    for q in range(b.B):
+        P, k = int(b.P[q]), int(b.k[q])
+        keep = r.keep[q]
+        assert keep.sum() <= math.ceil(0.5 * P - 1e-9)
+        assert np.array_equal(keep, orc.skv_keep(r.gate_logits[q], 0.5, 0.5))
+        assert not r.adj[q][:, ~keep].any()
+        assert r.adj[q].sum() == min(math.ceil(4.0 * k), k * int(keep.sum()))
