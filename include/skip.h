@@ -258,7 +258,8 @@ typedef struct skip_skv_gate {
   double rho;
 } skip_skv_gate_t;
 
-/* Workspace of skip_skv_gate for problem `p` and hidden width `hidden`. */
+/* Workspace of skip_skv_gate and skip_route_fused_gated for problem `p` and
+ * hidden width `hidden`. */
 skip_status_t skip_workspace_bytes_gate(const skip_problem_t* p, int32_t hidden,
                                         size_t* bytes);
 
@@ -375,6 +376,29 @@ skip_status_t skip_route_fused_profiled(
     int32_t* kept_idx, void* O, float* lse, void* workspace,
     size_t workspace_bytes, void* stream, void* const* stage_events,
     int32_t n_events);
+
+/*
+ * The fused route with the verification step (Alg. 1: scoring, TopK, verify,
+ * graph, fuse): skip_route_fused in which the passage gate of skip_skv_gate
+ * runs between the top-k and the graph (v_bar the mean of the kept rows of V,
+ * read through kept_idx; e_j the passage keys the graph uses) and the graph
+ * is built on the verified passages only, as in skip_bipartite_xattn_masked.
+ * Workspace: skip_workspace_bytes_gate(p, gate->hidden).
+ *   passage_keep out [total_passages] uint8, as written by skip_skv_gate
+ *   gate_logits  out [total_passages] float, or NULL
+ * bf16 only (SKIP_ERR_UNSUPPORTED otherwise); d a multiple of 32; gate
+ * fields as in skip_skv_gate.  Other arguments as in skip_route_fused.
+ */
+skip_status_t skip_route_fused_gated(const skip_problem_t* p, const skip_skv_gate_t* gate,
+                                     const void* V, const void* Qtok,
+                                     const int32_t* q_offsets, const void* w_bias,
+                                     const int32_t* kept_offsets, const void* Kh,
+                                     const void* Vh, const int32_t* passage_offsets,
+                                     const int32_t* query_passages,
+                                     const float* passage_keys, int32_t* kept_idx,
+                                     uint8_t* passage_keep, float* gate_logits, void* O,
+                                     float* lse, void* workspace, size_t workspace_bytes,
+                                     void* stream);
 
 #ifdef __cplusplus
 }

@@ -30,7 +30,7 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused",
                 "skip_route_fused_profiled", "skip_workspace_bytes_mlp",
                 "skip_prune_topk_mlp", "skip_workspace_bytes_gate", "skip_skv_gate",
-                "skip_bipartite_xattn_masked")
+                "skip_bipartite_xattn_masked", "skip_route_fused_gated")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -116,6 +116,9 @@ def _load() -> ctypes.CDLL:
     lib.skip_bipartite_xattn_masked.restype = ctypes.c_int
     lib.skip_bipartite_xattn_masked.argtypes = [P, vp, i32p, vp, vp, i32p, i32p, vp, vp, vp,
                                                 vp, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.skip_route_fused_gated.restype = ctypes.c_int
+    lib.skip_route_fused_gated.argtypes = [P, G, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
+                                           vp, i32p, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.skip_route_fused_profiled.restype = ctypes.c_int
     lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                               vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
@@ -314,9 +317,7 @@ def skip_skv_gate(p: SkipProblem, gate: "SkvGate", Qtok, q_offsets, V_kept, kept
     if workspace is None:
         workspace = torch.empty(workspace_bytes_gate(p, h), dtype=torch.uint8,
                                 device=Qtok.device)
-    g = SkipSkvGate(h, 0, _ptr(gate.W, "W", et, h * 5 * p.d),
-                    _ptr(gate.b1, "b1", torch.float32, h), _ptr(gate.w2, "w2", torch.float32, h),
-                    float(gate.b2), float(gate.tau), float(gate.rho))
+    g = _gate_struct(p, gate)
     st = LIB.skip_skv_gate(
         ctypes.byref(p), ctypes.byref(g), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
         _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1),
@@ -352,6 +353,40 @@ def skip_bipartite_xattn_masked(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passag
         _ptr(edge_col_out, "edge_col_out", torch.int32, p.total_kept * p.P_max),
         wsp, wsn, _stream(stream))
     _check(st, "skip_bipartite_xattn_masked")
+
+
+def _gate_struct(p: SkipProblem, gate: "SkvGate") -> SkipSkvGate:
+    h = gate.hidden
+    return SkipSkvGate(h, 0, _ptr(gate.W, "W", _elem_dtype(p), h * 5 * p.d),
+                       _ptr(gate.b1, "b1", torch.float32, h), _ptr(gate.w2, "w2", torch.float32, h),
+                       float(gate.b2), float(gate.tau), float(gate.rho))
+
+
+def skip_route_fused_gated(p: SkipProblem, gate: "SkvGate", V, Qtok, q_offsets, w_bias,
+                           kept_offsets, Kh, Vh, passage_offsets, query_passages, kept_idx,
+                           passage_keep, O, lse=None, gate_logits=None, passage_keys=None,
+                           workspace=None, stream=None):
+    et = _elem_dtype(p)
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes_gate(p, gate.hidden), dtype=torch.uint8,
+                                device=V.device)
+    g = _gate_struct(p, gate)
+    st = LIB.skip_route_fused_gated(
+        ctypes.byref(p), ctypes.byref(g), _ptr(V, "V", et, p.B * p.N * p.d),
+        _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
+        _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1), _ptr(w_bias, "w_bias", et, p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d), _ptr(Vh, "Vh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept),
+        _ptr(passage_keep, "passage_keep", torch.uint8, p.total_passages),
+        _ptr(gate_logits, "gate_logits", torch.float32, p.total_passages),
+        _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
+        _ptr(lse, "lse", torch.float32, p.total_kept * p.H), workspace.data_ptr(),
+        workspace.numel(), _stream(stream))
+    _check(st, "skip_route_fused_gated")
 
 
 def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
@@ -565,6 +600,27 @@ def bipartite_xattn_masked(db: DeviceBatch, Qh: torch.Tensor, passage_keep: torc
                                 O if p.total_kept else None, lse if p.total_kept else None,
                                 passage_keys, rp, col, db.workspace)
     return O[:p.total_kept], lse[:p.total_kept], rp, col
+
+
+def route_fused_gated(db: DeviceBatch, gate: SkvGate, passage_keys=None, out=None,
+                      workspace=None):
+    """The fused route with the verification step.  Returns (kept_idx,
+    passage_keep, gate_logits, O, lse).  ``out`` = preallocated tensors of
+    the same five."""
+    p = db.p
+    dev = db.V.device
+    if out is None:
+        out = (torch.empty(max(p.total_kept, 1), dtype=torch.int32, device=dev),
+               torch.empty(max(p.total_passages, 1), dtype=torch.uint8, device=dev),
+               torch.empty(max(p.total_passages, 1), dtype=torch.float32, device=dev),
+               torch.empty((max(p.total_kept, 1), p.H, p.d_h), dtype=_out_dtype(p), device=dev),
+               torch.empty((max(p.total_kept, 1), p.H), dtype=torch.float32, device=dev))
+    kept_idx, keep, logits, O, lse = out
+    skip_route_fused_gated(p, gate, db.V, db.Qtok, db.q_offsets, db.w_bias, db.kept_offsets,
+                           db.Kh, db.Vh, db.passage_offsets, db.query_passages, kept_idx, keep,
+                           O, lse, logits, passage_keys, workspace)
+    return (kept_idx[:p.total_kept], keep[:p.total_passages], logits[:p.total_passages],
+            O[:p.total_kept], lse[:p.total_kept])
 
 
 def route_fused(db: DeviceBatch, passage_keys=None, out=None, stage_events=None):

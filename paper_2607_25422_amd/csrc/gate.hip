@@ -256,11 +256,59 @@ gate_select_kernel(const float* __restrict__ part, int NT, int T, int B,
   keep[p0 + lane] = (ver[lane] && rank < cap) ? 1u : 0u;
 }
 
+// v_bar of the fused route: the mean of V[b][kept_idx[r]] over the kept rows r
+// of question b (0 when it has none).  Workgroup (512-column slice, question);
+// wave w sums rows w, w+4, ... in float64, 16 bytes a lane; the four partial
+// sums are combined in wave order through LDS.
+__global__ void __launch_bounds__(256)
+gate_vbar_kernel(const bf16_t* __restrict__ V, int N, int d, const int32_t* __restrict__ kept_offsets,
+                 const int32_t* __restrict__ kept_idx, int total_kept,
+                 double* __restrict__ vbar) {
+  __shared__ double part[4][64][8];
+  const int b = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = (blockIdx.x * 64 + lane) * 8;
+  int r0, r1;
+  range_of(kept_offsets, b, total_kept, r0, r1);
+  double acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+  if (c < d) {
+    const bf16_t* base = V + (size_t)b * N * d + c;
+    for (int r = r0 + wave; r < r1; r += 4) {
+      const int i = clampi(kept_idx[r], 0, N - 1);
+      float x[8];
+      gunpack8(*reinterpret_cast<const u32x4*>(base + (size_t)i * d), x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += (double)x[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[wave][lane][e] = acc[e];
+  __syncthreads();
+  if (wave != 0 || c >= d) return;
+  const int L = r1 - r0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const double sum = ((part[0][lane][e] + part[1][lane][e]) + part[2][lane][e]) +
+                       part[3][lane][e];
+    vbar[(size_t)b * d + c + e] = L > 0 ? sum / (double)L : 0.0;
+  }
+}
+
+hipError_t launch_gate_vbar(const skip_problem_t& p, const void* V,
+                            const int32_t* kept_offsets, const int32_t* kept_idx,
+                            GateScratch g, hipStream_t s) {
+  hipLaunchKernelGGL(gate_vbar_kernel, dim3((p.d + 511) / 512, p.B), dim3(256), 0, s,
+                     (const bf16_t*)V, p.N, p.d, kept_offsets, kept_idx, p.total_kept, g.vbar);
+  return hipGetLastError();
+}
+
 static size_t galign(size_t n) { return (n + 255) & ~(size_t)255; }
 
 size_t gate_scratch_bytes(const skip_problem_t& p, int hidden) {
   const size_t T = (size_t)p.total_passages;
   return galign((size_t)p.B * p.d * sizeof(double)) +        // vbar
+         galign((size_t)p.B * p.d * sizeof(double)) +        // qbar
          galign(T * 3 * p.d * sizeof(bf16_t)) +               // X
          galign((size_t)p.B * 2 * p.d * sizeof(bf16_t)) +     // QV
          galign((size_t)p.B * hidden * sizeof(float)) +       // cvec
@@ -273,6 +321,8 @@ GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base) 
   char* c = static_cast<char*>(base);
   GateScratch g;
   g.vbar = reinterpret_cast<double*>(c);
+  c += galign((size_t)p.B * p.d * sizeof(double));
+  g.qbar = reinterpret_cast<double*>(c);
   c += galign((size_t)p.B * p.d * sizeof(double));
   g.X = reinterpret_cast<bf16_t*>(c);
   c += galign(T * 3 * p.d * sizeof(bf16_t));

@@ -289,6 +289,19 @@ static bool gate_hidden_ok(int32_t hidden) {
   return hidden % 64 == 0 && hidden <= 4096;
 }
 
+// gate fields and the shapes the gate kernels take (p already checked)
+static skip_status_t check_gate(const skip_problem_t* p, const skip_skv_gate_t* gate) {
+  if (gate->reserved != 0 || !gate->W || !gate->w2 || gate->hidden <= 0 ||
+      !std::isfinite(gate->b2) || !(gate->tau > 0.0 && gate->tau < 1.0) ||
+      !(gate->rho > 0.0 && gate->rho <= 1.0))
+    return SKIP_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(gate->W) % 16 != 0) return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || !gate_hidden_ok(gate->hidden))
+    return SKIP_ERR_UNSUPPORTED;
+  if ((int64_t)gate->hidden * 5 * p->d > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  return SKIP_OK;
+}
+
 skip_status_t skip_workspace_bytes_gate(const skip_problem_t* p, int32_t hidden, size_t* bytes) {
   if (!bytes) return SKIP_ERR_INVALID_ARG;
   skip_status_t st = check_common(p);
@@ -315,14 +328,8 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
   if (p->total_passages > 0 && !keep) return SKIP_ERR_INVALID_ARG;
   if (!passage_keys && p->total_passages > 0 && (!Kh || !passage_offsets))
     return SKIP_ERR_INVALID_ARG;
-  if (gate->reserved != 0 || !gate->W || !gate->w2 || gate->hidden <= 0 ||
-      !std::isfinite(gate->b2) || !(gate->tau > 0.0 && gate->tau < 1.0) ||
-      !(gate->rho > 0.0 && gate->rho <= 1.0))
-    return SKIP_ERR_INVALID_ARG;
-  if (reinterpret_cast<uintptr_t>(gate->W) % 16 != 0) return SKIP_ERR_INVALID_ARG;
-  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || !gate_hidden_ok(gate->hidden))
-    return SKIP_ERR_UNSUPPORTED;
-  if ((int64_t)gate->hidden * 5 * p->d > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  st = check_gate(p, gate);
+  if (st != SKIP_OK) return st;
   const size_t need = workspace_size(*p) + gate_scratch_bytes(*p, gate->hidden);
   if (workspace_bytes < need) return SKIP_ERR_WORKSPACE;
   if (p->total_passages == 0) return SKIP_OK;
@@ -348,7 +355,10 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
                                       const int32_t* query_passages,
                                       const float* passage_keys, int32_t* kept_idx, void* O,
                                       float* lse, void* workspace, size_t workspace_bytes,
-                                      void* stream, void* const* ev) {
+                                      void* stream, void* const* ev,
+                                      const skip_skv_gate_t* gate = nullptr,
+                                      uint8_t* passage_keep = nullptr,
+                                      float* gate_logits = nullptr) {
   skip_status_t st = check(p, kPrune | kGraph);
   if (st != SKIP_OK) return st;
   if (!V || !Qtok || !q_offsets || !kept_offsets || !query_passages || !passage_offsets ||
@@ -356,7 +366,14 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
     return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && (!kept_idx || !O)) return SKIP_ERR_INVALID_ARG;
   if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
-  if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
+  size_t need = workspace_size(*p);
+  if (gate) {
+    st = check_gate(p, gate);
+    if (st != SKIP_OK) return st;
+    if (p->total_passages > 0 && !passage_keep) return SKIP_ERR_INVALID_ARG;
+    need += gate_scratch_bytes(*p, gate->hidden);
+  }
+  if (workspace_bytes < need) return SKIP_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Workspace w = carve_workspace(*p, workspace);
   int stage = 0;
@@ -377,13 +394,26 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
   SKIP_TRY(mark());
   if (work) SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
   SKIP_TRY(mark());
+  if (gate && p->total_passages > 0) {
+    // verify step: plain question means, kept-row means, then the gate on the
+    // passage keys pooled above
+    GateScratch g = carve_gate_scratch(*p, gate->hidden, static_cast<char*>(workspace) + w.bytes);
+    SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, Qtok,
+                          q_offsets, p->B, p->total_qtok, g.qbar, s));
+    SKIP_TRY(launch_gate_vbar(*p, V, kept_offsets, kept_idx, g, s));
+    if (!work && !passage_keys)
+      SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
+    SKIP_TRY(launch_gate(*p, *gate, g.qbar, w.kbar, passage_keys, query_passages, g,
+                         gate_logits, passage_keep, s));
+  }
   if (work)
     SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
                              EdgePartials{w.part, w.qn2, w.kn2}, s));
   SKIP_TRY(mark());
   if (work)
-    SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets, query_passages, w.rowmask, nullptr,
-                                nullptr, s));
+    SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets,
+                                query_passages, w.rowmask, nullptr, nullptr, s,
+                                gate ? passage_keep : nullptr));
   SKIP_TRY(mark());
   if (work)
     SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
@@ -402,6 +432,23 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V, const voi
   return route_fused_impl(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
                           passage_offsets, query_passages, passage_keys, kept_idx, O, lse,
                           workspace, workspace_bytes, stream, nullptr);
+}
+
+skip_status_t skip_route_fused_gated(const skip_problem_t* p, const skip_skv_gate_t* gate,
+                                     const void* V, const void* Qtok,
+                                     const int32_t* q_offsets, const void* w_bias,
+                                     const int32_t* kept_offsets, const void* Kh,
+                                     const void* Vh, const int32_t* passage_offsets,
+                                     const int32_t* query_passages,
+                                     const float* passage_keys, int32_t* kept_idx,
+                                     uint8_t* passage_keep, float* gate_logits, void* O,
+                                     float* lse, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  if (!gate) return SKIP_ERR_INVALID_ARG;
+  return route_fused_impl(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                          passage_offsets, query_passages, passage_keys, kept_idx, O, lse,
+                          workspace, workspace_bytes, stream, nullptr, gate, passage_keep,
+                          gate_logits);
 }
 
 skip_status_t skip_route_fused_profiled(

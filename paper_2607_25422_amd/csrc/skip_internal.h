@@ -53,6 +53,7 @@ hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, c
 // Passage verification gate ---------------------------------------------
 struct GateScratch {
   double* vbar;      // [B][d]         mean of the kept visual rows
+  double* qbar;      // [B][d]         mean of the question tokens
   bf16_t* X;         // [T][3d]        passage part of the gate input
   bf16_t* QV;        // [B][2d]        question part [q_bar' ; v_bar']
   float* cvec;       // [B][h]         W[:, 0:2d] [q_bar' ; v_bar'] + b1
@@ -63,6 +64,10 @@ size_t gate_scratch_bytes(const skip_problem_t& p, int hidden);
 GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base);
 // qbar: plain question means; kbar: pooled passage keys (unused when
 // passage_keys is given); g.vbar must hold the kept-row means.
+// g.vbar from the kept rows of V named by kept_idx (the fused route)
+hipError_t launch_gate_vbar(const skip_problem_t& p, const void* V,
+                            const int32_t* kept_offsets, const int32_t* kept_idx,
+                            GateScratch g, hipStream_t s);
 hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* qbar,
                        const double* kbar, const float* passage_keys,
                        const int32_t* query_passages, GateScratch g, float* logits,
