@@ -53,7 +53,14 @@ def parse():
     ap.add_argument("--scorer", default="linear", choices=["linear", "mlp"],
                     help="mlp: time the prune stage with the main-text scorer instead of "
                          "the fused route (a record line, not the headline)")
-    ap.add_argument("--hidden", type=int, default=512, help="hidden width of the mlp scorer")
+    ap.add_argument("--hidden", type=int, default=512,
+                    help="hidden width of the mlp scorer or of the passage gate")
+    ap.add_argument("--gate", action="store_true",
+                    help="time the fused route with the passage verification gate (and the "
+                         "route without it, interleaved) instead of the plain fused route")
+    ap.add_argument("--gate-tau", type=float, default=0.5, help="gate threshold on nu")
+    ap.add_argument("--gate-rho", type=float, default=0.5,
+                    help="kept fraction of a question's passages after the gate")
     ap.add_argument("--cold", action="store_true",
                     help="overwrite a 1 GiB buffer before every timed step so that no input "
                          "is left in the on-die cache; value then comes from the event-timed "
@@ -188,6 +195,97 @@ def bench_mlp_scorer(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_gated_route(args):
+    """The fused route with the verification step (score, top-k, gate, graph
+    on the verified passages, attention) against the plain fused route,
+    alternating step by step on the same batch, plus the gate call alone on
+    the gathered rows with the passage keys handed over as float32 (its
+    algorithmic bytes: question tokens, kept rows, the gate weights and the
+    keys, each read once)."""
+    import torch
+
+    from paper_2607_25422_amd import binding as B
+    from paper_2607_25422_amd import workloads as wls
+
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {args.workload} seed {args.seed} (gate h={args.hidden})",
+          file=sys.stderr, flush=True)
+    batch = wls.make_batch(args.workload, args.seed, threads=16)
+    wl = batch.wl
+    w = wls.make_gate_weights(wl, args.hidden, args.seed)
+    db = B.to_device(batch)
+    p = db.p
+    g = B.SkvGate(w.W.cuda(), w.b1.cuda(), w.w2.cuda(), w.b2, args.gate_tau, args.gate_rho)
+    ws = torch.empty(B.workspace_bytes_gate(p, args.hidden), dtype=torch.uint8, device="cuda")
+    dev = "cuda"
+    gout = (torch.empty(p.total_kept, dtype=torch.int32, device=dev),
+            torch.empty(p.total_passages, dtype=torch.uint8, device=dev),
+            torch.empty(p.total_passages, dtype=torch.float32, device=dev),
+            torch.empty((p.total_kept, p.H, p.d_h), dtype=batch.torch_dtype, device=dev),
+            torch.empty((p.total_kept, p.H), dtype=torch.float32, device=dev))
+    pout = (gout[0], gout[3], gout[4])
+    _, _, Vk = B.prune_topk(db, want_scores=False)
+    pk = torch.stack([batch.Kh[a:b].float().reshape(b - a, -1).mean(0) for a, b in
+                      zip(batch.passage_offsets[:-1], batch.passage_offsets[1:])]).cuda()
+    for _ in range(args.warmup):
+        B.route_fused_gated(db, g, out=gout, workspace=ws)
+        B.route_fused(db, out=pout)
+        B.skv_gate(db, g, Vk, passage_keys=pk, workspace=ws)
+    torch.cuda.synchronize()
+    kept = int(gout[1].sum())
+    n = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
+    t_gated = 0.0
+    for i in range(n):
+        ev[i][0].record()
+        B.route_fused_gated(db, g, out=gout, workspace=ws)
+        ev[i][1].record()
+        B.route_fused(db, out=pout)
+        ev[i][2].record()
+        B.skv_gate(db, g, Vk, passage_keys=pk, workspace=ws)
+        ev[i][3].record()
+    torch.cuda.synchronize()
+    gated = sorted(e[0].elapsed_time(e[1]) for e in ev)
+    plain = sorted(e[1].elapsed_time(e[2]) for e in ev)
+    gate_only = sorted(e[2].elapsed_time(e[3]) for e in ev)
+    mean = lambda xs: sum(xs) / len(xs)   # noqa: E731
+    # wall-clock throughput of the gated route alone
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(n):
+        B.route_fused_gated(db, g, out=gout, workspace=ws)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    h, d = args.hidden, p.d
+    gate_bytes = (p.total_qtok * d * 2 + p.total_kept * d * 2 + h * 5 * d * 2
+                  + p.total_passages * d * 4 + 4 * h * 2 + p.total_passages * 5)
+    gate_flops = 2.0 * p.total_passages * h * 3 * d + 2.0 * p.B * h * 2 * d
+    gms = mean(gate_only)
+    gbs = gate_bytes / (gms * 1e-3) / 1e9
+    res = {
+        "metric": "queries/sec (fused route with the passage verification gate) + gate-call "
+                  "HBM GB/s vs MI355X peak",
+        "value": round(p.B * n / wall, 1),
+        "unit": "queries/s",
+        "n_gpus": 1, "steps": n, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall / n, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "B": p.B, "N": p.N, "d": p.d,
+                   "passages": int(batch.P[0]), "gate_hidden": h, "tau": args.gate_tau,
+                   "rho": args.gate_rho, "seed": args.seed},
+        "gated_route_gpu_ms": {"p50": round(gated[n // 2], 5), "mean": round(mean(gated), 5)},
+        "plain_route_gpu_ms": {"p50": round(plain[n // 2], 5), "mean": round(mean(plain), 5)},
+        "passages_kept": kept, "passages": p.total_passages,
+        "roofline": {"kernel": "skip_skv_gate call (6 kernels, keys given)", "bound": "hbm",
+                     "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes": gate_bytes, "avg_ms": round(gms, 5),
+                     "gflop": round(gate_flops / 1e9, 3)},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -197,6 +295,9 @@ def main():
         sys.exit(2)
     if args.scorer == "mlp":
         bench_mlp_scorer(args)
+        return
+    if args.gate:
+        bench_gated_route(args)
         return
 
     import numpy as np

@@ -6,17 +6,18 @@
 // ceil(rho * P_b) with the largest nu.  The model takes bf16 inputs (q_bar,
 // v_bar, e_j rounded through float32; the product rounded from its exact
 // value; the difference rounded from its float32 value).
-//   gate_x_kernel      : the passage part of x_j, [e' ; (e' q')' ; |e' - q'|'],
-//                        bf16, and the question part [q' ; v'] per question
-//   gate_c_kernel      : c_b = W[:, 0:2d] [q'_b ; v'_b] + b1 (float32 sums of
-//                        exact products)
-//   gate_score_kernel  : W[:, 2d:5d] x_j on v_mfma_f32_32x32x16_bf16 for
-//                        32 passages x 64 hidden units a workgroup (the four
-//                        waves split the 3d columns), then relu(. + c_b) . w2
-//                        summed over the 64 units: one partial logit per
-//                        64-unit tile
-//   gate_select_kernel : logit_j = sum of the partials + b2; threshold and
-//                        top fraction per question (one wave a question)
+//   gate_mean_kernel  : q_bar (question tokens) and v_bar (kept rows, given as
+//                       rows or through kept_idx) in float64, 8 waves a
+//                       workgroup with four rows a wave in flight
+//   gate_x_kernel     : the bf16 gate input x_j of every passage, [T][5d]
+//   gate_score_kernel : W x_j on v_mfma_f32_32x32x16_bf16, tiles of 32
+//                       passages x 64 hidden units, the 5d columns split into
+//                       S chunks (split-K, so the launch fills the chip at a
+//                       few hundred passages); one float32 partial per chunk
+//   gate_fin_kernel   : one workgroup a passage: the chunk partials summed in
+//                       chunk order, + b1, relu, . w2, + b2 -> logit_j; the
+//                       last workgroup of a question to finish (a counter in
+//                       the workspace) takes the question's cut
 #include <cmath>
 
 #include "skip_common.h"
@@ -42,6 +43,10 @@ __device__ __forceinline__ void gunpack8(const u32x4& x, float* out) {
   }
 }
 
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
 // question of global passage index j (query_passages ascending)
 __device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, int j) {
   int lo = 0, hi = B;                      // answer in [0, B)
@@ -55,147 +60,225 @@ __device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, 
 
 }  // namespace
 
-constexpr int kGateMT = 32;       // passages per score tile
-constexpr int kGateNT = 64;       // hidden units per score tile
-constexpr int kGateCJ = 8;        // hidden units per c block (2 per wave)
-constexpr int kGateCQ = 4;        // questions per c block (at most; LDS holds qpb x 2d bf16)
+constexpr int kGateMT = 32;        // passages per score tile
+constexpr int kGateNT = 64;        // hidden units per score tile
+constexpr int kGateMeanWaves = 8;  // waves per mean workgroup (512 columns)
+constexpr int kGateTargetWG = 640; // score workgroups aimed for when choosing S
 
-// Blocks [0, T): passage j = block: X[j] = [e' ; (e' q')' ; |e' - q'|'] and
-// pq[j] = its question.  Blocks [T, T + B): QV[b] = [q'_b ; v'_b].
+// Workgroup (512-column slice, y): y < B is q_bar_y over the question tokens,
+// y >= B is v_bar_{y-B} over the kept rows (rows[kept_offsets range], or
+// V[b][kept_idx[r]] when kept_idx is given).  Wave w sums the rows w, w+8, ...
+// in float64 (16 bytes a lane, four rows in flight); the eight partial sums
+// are added in wave order; an empty range gives 0.
+__global__ void __launch_bounds__(512)
+gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_offsets,
+                 int total_qtok, const bf16_t* __restrict__ rows,
+                 const int32_t* __restrict__ kept_offsets, const int32_t* __restrict__ kept_idx,
+                 int N, int total_kept, int B, int d, double* __restrict__ qbar,
+                 double* __restrict__ vbar) {
+  __shared__ double part[kGateMeanWaves][64][8];
+  const bool isq = (int)blockIdx.y < B;
+  const int b = isq ? (int)blockIdx.y : (int)blockIdx.y - B;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = (blockIdx.x * 64 + lane) * 8;
+  int r0, r1;
+  if (isq) range_of(q_offsets, b, total_qtok, r0, r1);
+  else range_of(kept_offsets, b, total_kept, r0, r1);
+  const bf16_t* src = isq ? Qtok : rows;
+  const bool indexed = !isq && kept_idx != nullptr;
+  // indexed rows: lane i holds the index of the wave's i-th row (rows w,
+  // w+8, ... up to 64 of them a pass), read once before the row loads
+  int my_idx = 0, base_r = r0 + wave;
+  auto fetch_idx = [&](int rb) {
+    const int r = rb + kGateMeanWaves * lane;
+    my_idx = (indexed && r < r1) ? clampi(kept_idx[r], 0, N - 1) : 0;
+    base_r = rb;
+  };
+  // the row loop is wave-uniform (every lane shuffles); lanes past the last
+  // column load nothing
+  const bool cok = c < d;
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  auto load_row = [&](int r) -> u32x4 {
+    size_t off = (size_t)r * d;
+    if (indexed) {
+      const int i = __shfl(my_idx, (r - base_r) / kGateMeanWaves, kWave);
+      off = ((size_t)b * N + i) * d;
+    }
+    return cok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + off + c))
+               : zero;
+  };
+  double acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+  constexpr int U = 4;
+  int r = r0 + wave;
+  fetch_idx(r);
+  for (; r + kGateMeanWaves * (U - 1) < r1; r += kGateMeanWaves * U) {
+    if (r + kGateMeanWaves * (U - 1) >= base_r + kGateMeanWaves * 64) fetch_idx(r);
+    u32x4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = load_row(r + kGateMeanWaves * u);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float f[8];
+      gunpack8(x[u], f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
+    }
+  }
+  for (; r < r1; r += kGateMeanWaves) {
+    if (r >= base_r + kGateMeanWaves * 64) fetch_idx(r);
+    float f[8];
+    gunpack8(load_row(r), f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[wave][lane][e] = acc[e];
+  __syncthreads();
+  if (wave != 0 || c >= d) return;
+  const int L = r1 - r0;
+  double* out = (isq ? qbar : vbar) + (size_t)b * d + c;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    double s = part[0][lane][e];
+#pragma unroll
+    for (int w = 1; w < kGateMeanWaves; ++w) s += part[w][lane][e];
+    out[e] = L > 0 ? s / (double)L : 0.0;
+  }
+}
+
+// Block j (passage): X[j] = [q' ; v' ; e' ; (e' q')' ; |e' - q'|'] (x' the
+// bf16 rounding), pq[j] = its question; the first passage of a question also
+// clears that question's finish counter.  Thread t fills 8-column groups t,
+// t+256, ... of every block of X.
 __global__ void __launch_bounds__(256)
 gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
               const double* __restrict__ kbar, const float* __restrict__ pkeys,
               const int32_t* __restrict__ query_passages, int B, int T, int d,
-              bf16_t* __restrict__ X, bf16_t* __restrict__ QV, int32_t* __restrict__ pq) {
-  const int blk = blockIdx.x;
-  if (blk >= T) {
-    const int b = blk - T;
-    for (int c = threadIdx.x; c < d; c += blockDim.x) {
-      QV[(size_t)b * 2 * d + c] = (bf16_t)f32_to_bf16((float)qbar[(size_t)b * d + c]);
-      QV[(size_t)b * 2 * d + d + c] = (bf16_t)f32_to_bf16((float)vbar[(size_t)b * d + c]);
-    }
-    return;
-  }
-  const int j = blk;
+              bf16_t* __restrict__ X, int32_t* __restrict__ pq, int32_t* __restrict__ done) {
+  const int j = blockIdx.x;
   const int b = question_of(query_passages, B, T, j);
-  if (threadIdx.x == 0) pq[j] = b;
-  bf16_t* xr = X + (size_t)j * 3 * d;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    const float ev = pkeys ? pkeys[(size_t)j * d + c] : (float)kbar[(size_t)j * d + c];
-    const float e = bf16_to_f32(f32_to_bf16(ev));
-    const float q = bf16_to_f32(f32_to_bf16((float)qbar[(size_t)b * d + c]));
-    xr[c] = (bf16_t)f32_to_bf16(e);
-    xr[d + c] = (bf16_t)f32_to_bf16(e * q);            // exact product, one rounding
-    xr[2 * d + c] = (bf16_t)f32_to_bf16(fabsf(e - q));  // float32 difference, one rounding
+  if (threadIdx.x == 0) {
+    pq[j] = b;
+    if (clampi(query_passages[b], 0, T) == j) done[b] = 0;
   }
-}
-
-// c_b[j] = W[j, 0:2d] . QV_b + b1[j] for hidden units j = 8*jt + 2*w + {0,1}
-// and questions qpb*qt .. qpb*qt + qpb-1 (QV staged in LDS; float32 sums).
-__global__ void __launch_bounds__(256)
-gate_c_kernel(const bf16_t* __restrict__ QV, const bf16_t* __restrict__ W,
-              const float* __restrict__ b1, int B, int d, int h, int qpb,
-              float* __restrict__ cvec) {
-  extern __shared__ __attribute__((aligned(16))) bf16_t qs[];   // [qpb][2d]
-  const int jt = blockIdx.x, q0 = blockIdx.y * qpb;
-  const int nq = min(qpb, B - q0);
-  const int K = 2 * d;
-  for (int i = threadIdx.x * 8; i < nq * K; i += blockDim.x * 8)
-    *reinterpret_cast<u32x4*>(qs + i) = *reinterpret_cast<const u32x4*>(QV + (size_t)q0 * K + i);
-  __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int j0 = jt * kGateCJ + wave * 2;
-  const bf16_t* wr0 = W + (size_t)j0 * 5 * d;
-  const bf16_t* wr1 = wr0 + (size_t)5 * d;
-  float acc[2][kGateCQ];
+  bf16_t* xr = X + (size_t)j * 5 * d;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float e[8], q[8], v[8];
+    if (pkeys) {
+      const float4 a = *reinterpret_cast<const float4*>(pkeys + (size_t)j * d + c);
+      const float4 a2 = *reinterpret_cast<const float4*>(pkeys + (size_t)j * d + c + 4);
+      e[0] = a.x; e[1] = a.y; e[2] = a.z; e[3] = a.w;
+      e[4] = a2.x; e[5] = a2.y; e[6] = a2.z; e[7] = a2.w;
+    } else {
+      const double2* kp = reinterpret_cast<const double2*>(kbar + (size_t)j * d + c);
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int qq = 0; qq < kGateCQ; ++qq) acc[u][qq] = 0.f;
-  for (int g = 0; g < K; g += 4096) {
-    constexpr int CH = 4096 / 512;
-    u32x4 w[2][CH];
-#pragma unroll
-    for (int t = 0; t < CH; ++t) {
-      const int c = g + (t * 64 + lane) * 8;
-      const bool ok = c < K;
-      w[0][t] = ok ? *reinterpret_cast<const u32x4*>(wr0 + c) : u32x4{0u, 0u, 0u, 0u};
-      w[1][t] = ok ? *reinterpret_cast<const u32x4*>(wr1 + c) : u32x4{0u, 0u, 0u, 0u};
-    }
-#pragma unroll
-    for (int t = 0; t < CH; ++t) {
-      const int c = g + (t * 64 + lane) * 8;
-      if (c >= K) continue;
-      float w0[8], w1[8];
-      gunpack8(w[0][t], w0);
-      gunpack8(w[1][t], w1);
-#pragma unroll
-      for (int qq = 0; qq < kGateCQ; ++qq) {
-        if (qq >= nq) continue;
-        float qv[8];
-        gunpack8(*reinterpret_cast<const u32x4*>(qs + qq * K + c), qv);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          acc[0][qq] = fmaf(w0[e], qv[e], acc[0][qq]);
-          acc[1][qq] = fmaf(w1[e], qv[e], acc[1][qq]);
-        }
+      for (int t = 0; t < 4; ++t) {
+        const double2 x = kp[t];
+        e[2 * t] = (float)x.x;
+        e[2 * t + 1] = (float)x.y;
       }
     }
-  }
+    const double2* qp2 = reinterpret_cast<const double2*>(qbar + (size_t)b * d + c);
+    const double2* vp2 = reinterpret_cast<const double2*>(vbar + (size_t)b * d + c);
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int qq = 0; qq < kGateCQ; ++qq) {
-      const float v = wave_sum_f32(acc[u][qq]);
-      if (lane == 0 && qq < nq)
-        cvec[(size_t)(q0 + qq) * h + j0 + u] = v + (b1 ? b1[j0 + u] : 0.f);
+    for (int t = 0; t < 4; ++t) {
+      const double2 x = qp2[t], y = vp2[t];
+      q[2 * t] = (float)x.x;
+      q[2 * t + 1] = (float)x.y;
+      v[2 * t] = (float)y.x;
+      v[2 * t + 1] = (float)y.y;
     }
+    u32x4 oq, ov, oe, oh, od;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const float e0 = bf16_to_f32(f32_to_bf16(e[2 * t]));
+      const float e1 = bf16_to_f32(f32_to_bf16(e[2 * t + 1]));
+      const float q0 = bf16_to_f32(f32_to_bf16(q[2 * t]));
+      const float q1 = bf16_to_f32(f32_to_bf16(q[2 * t + 1]));
+      oq[t] = bf16_pair(q0, q1);
+      ov[t] = bf16_pair(v[2 * t], v[2 * t + 1]);
+      oe[t] = bf16_pair(e0, e1);
+      oh[t] = bf16_pair(e0 * q0, e1 * q1);              // exact product, one rounding
+      od[t] = bf16_pair(fabsf(e0 - q0), fabsf(e1 - q1)); // float32 difference, one rounding
+    }
+    *reinterpret_cast<u32x4*>(xr + c) = oq;
+    *reinterpret_cast<u32x4*>(xr + d + c) = ov;
+    *reinterpret_cast<u32x4*>(xr + 2 * d + c) = oe;
+    *reinterpret_cast<u32x4*>(xr + 3 * d + c) = oh;
+    *reinterpret_cast<u32x4*>(xr + 4 * d + c) = od;
+  }
 }
 
-// Tile (32 passages from 32*pt, 64 hidden units from 64*ht); the 3d passage
-// columns are 3d/16 MFMA steps of 16 and wave w takes the steps w, w+4, ...
-// Operands straight from global memory: A = X rows (lane: passage l%32, 8
-// columns), B = W rows (lane: hidden unit l%32, 8 columns), four steps in
-// flight per wave.
+// Tile (32 passages from 32*blockIdx.x, 64 hidden units from 64*blockIdx.y),
+// chunk z of the 5d columns, in groups of 64 columns: groups [z*ch, min((z+1)*
+// ch, ceil(5d/64))), wave w taking the groups w, w+4, ...  In a group the lane
+// pair (passage or unit l%32, half hh) reads the row's 128 contiguous bytes,
+// 64 a lane as four 16-byte pieces, and piece u feeds MFMA step u: step u sums
+// the columns 8u..8u+7 and 32+8u..32+8u+7 of the group (A and B take the same
+// columns, so the product over the group is complete).  Two groups (eight
+// steps) are in flight per wave.  A half group at the end of the columns
+// (5d/32 odd) reads zeros for its second half.  The four waves' sums are added
+// in wave order and written as part[z][passage][unit].
+//
+// Tiles go to XCDs by chunk: the hardware deals workgroup ids round-robin over
+// the 8 XCDs, and id L takes chunk z = 8 * zl + L % 8 with (zl, ht, pt) the
+// (L / 8)-th entry of that XCD's list, pt fastest.  Every tile of a chunk then
+// runs on one XCD, whose L2 holds the chunk's columns of X and W (about 1.7 MB
+// at 160 passages x 512 units x 4096), so each is read from memory once.
+// Ids whose chunk is past the last one exit at once.
 __global__ void __launch_bounds__(256)
 gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int T, int d,
-                  int h, const int32_t* __restrict__ pq, const float* __restrict__ cvec,
-                  const float* __restrict__ w2, float* __restrict__ part) {
+                  int h, int ch, int S, float* __restrict__ part) {
   __shared__ float red[4][kGateMT][kGateNT + 1];
-  const int pt = blockIdx.x, ht = blockIdx.y;
+  const int n_pt = (T + kGateMT - 1) / kGateMT, n_ht = h / kGateNT;
+  const int L = blockIdx.x, xcd = L & 7, jl = L >> 3;
+  const int pt = jl % n_pt, ht = (jl / n_pt) % n_ht, zl = jl / (n_pt * n_ht);
+  const int z = zl * 8 + xcd;
+  if (z >= S) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int hh = lane >> 5, r32 = lane & 31;
-  const int K = 3 * d;
-  const int nsteps = K / 16;
+  const int K = 5 * d;
+  const int ngroups = (K + 63) / 64;
+  const int g1 = min((z + 1) * ch, ngroups);
   const int prow = min(pt * kGateMT + r32, T - 1);
-  const bf16_t* xa = X + (size_t)prow * K + 8 * hh;
-  const bf16_t* wb0 = W + (size_t)(ht * kGateNT + r32) * 5 * d + 2 * d + 8 * hh;
-  const bf16_t* wb1 = wb0 + (size_t)32 * 5 * d;
+  const bf16_t* xa = X + (size_t)prow * K + 32 * hh;
+  const bf16_t* wb0 = W + (size_t)(ht * kGateNT + r32) * K + 32 * hh;
+  const bf16_t* wb1 = wb0 + (size_t)32 * K;
   gf32x16_t acc[2];
 #pragma unroll
   for (int v = 0; v < 16; ++v) { acc[0][v] = 0.f; acc[1][v] = 0.f; }
-  constexpr int U = 4;
-  int st = wave;
-  for (; st + 4 * (U - 1) < nsteps; st += 4 * U) {
-    u32x4 a[U], b0[U], b1[U];
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  auto load_group = [&](int g, u32x4* a, u32x4* b0, u32x4* b1) {
+    const int c = 64 * g;
+    const bool ok = c + 32 * hh < K;        // K is a multiple of 32
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = 16 * (st + 4 * u);
-      a[u] = *reinterpret_cast<const u32x4*>(xa + k);
-      b0[u] = *reinterpret_cast<const u32x4*>(wb0 + k);
-      b1[u] = *reinterpret_cast<const u32x4*>(wb1 + k);
+    for (int u = 0; u < 4; ++u) {
+      a[u] = ok ? *reinterpret_cast<const u32x4*>(xa + c + 8 * u) : zero;
+      b0[u] = ok ? *reinterpret_cast<const u32x4*>(wb0 + c + 8 * u) : zero;
+      b1[u] = ok ? *reinterpret_cast<const u32x4*>(wb1 + c + 8 * u) : zero;
     }
+  };
+  int g = z * ch + wave;
+  for (; g + 4 < g1; g += 8) {
+    u32x4 a[8], b0[8], b1[8];
+    load_group(g, a, b0, b1);
+    load_group(g + 4, a + 4, b0 + 4, b1 + 4);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < 8; ++u) {
       acc[0] = gmfma(a[u], b0[u], acc[0]);
       acc[1] = gmfma(a[u], b1[u], acc[1]);
     }
   }
-  for (; st < nsteps; st += 4) {
-    const int k = 16 * st;
-    const u32x4 a = *reinterpret_cast<const u32x4*>(xa + k);
-    acc[0] = gmfma(a, *reinterpret_cast<const u32x4*>(wb0 + k), acc[0]);
-    acc[1] = gmfma(a, *reinterpret_cast<const u32x4*>(wb1 + k), acc[1]);
+  if (g < g1) {
+    u32x4 a[4], b0[4], b1[4];
+    load_group(g, a, b0, b1);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc[0] = gmfma(a[u], b0[u], acc[0]);
+      acc[1] = gmfma(a[u], b1[u], acc[1]);
+    }
   }
   // D layout: element v of block nb is passage 8*(v/4) + 4*hh + v%4, hidden
   // unit nb*32 + r32 of the tile
@@ -208,153 +291,163 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, in
   // thread t: passage t / 8, hidden units 8 * (t % 8) .. + 7
   const int m = threadIdx.x >> 3, n0 = (threadIdx.x & 7) * 8;
   const int p = pt * kGateMT + m;
-  float s = 0.f;
-  if (p < T) {
-    const int b = pq[p];
+  if (p >= T) return;
+  float o[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int n = n0 + e, j = ht * kGateNT + n;
-      const float a = ((red[0][m][n] + red[1][m][n]) + red[2][m][n]) + red[3][m][n];
-      s += fmaxf(a + cvec[(size_t)b * h + j], 0.f) * w2[j];
-    }
+  for (int e = 0; e < 8; ++e) {
+    const int n = n0 + e;
+    o[e] = ((red[0][m][n] + red[1][m][n]) + red[2][m][n]) + red[3][m][n];
   }
-  // sum over the 8 threads of a passage (consecutive lanes), fixed order
-#pragma unroll
-  for (int o = 1; o < 8; o <<= 1) s += __shfl_xor(s, o, kWave);
-  if ((threadIdx.x & 7) == 0 && p < T) part[(size_t)ht * T + p] = s;
+  float4* dst = reinterpret_cast<float4*>(part + ((size_t)z * T + p) * h + ht * kGateNT + n0);
+  dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+  dst[1] = make_float4(o[4], o[5], o[6], o[7]);
 }
 
-// One wave per question: logit_j = the float32 rounding of (the sum of the
-// tile partials, in tile order, + b2); kept = verified (logit >= t) and among
-// the cap largest verified logits (ties: lower index).  The cut is taken on
-// the stored float32 logits, so it can be re-derived from them exactly.
-__global__ void __launch_bounds__(64)
-gate_select_kernel(const float* __restrict__ part, int NT, int T, int B,
-                   const int32_t* __restrict__ query_passages, double b2, double t,
-                   double rho, float* __restrict__ logits, uint8_t* __restrict__ keep) {
-  __shared__ float z[64];
-  __shared__ int ver[64];
-  const int b = blockIdx.x, lane = threadIdx.x;
+// Block p (passage, 256 threads): pre-activation of unit j = the S chunk
+// partials in chunk order + b1[j]; thread t sums relu(.) * w2[j] over its
+// units j = t, t+256, ... in order; the four waves' sums (wave shuffles, then
+// wave order) plus b2, rounded to float32, are logit_p.  The block then bumps
+// its question's counter; the block that completes it (P_b blocks in all)
+// takes the cut: kept = logit >= t and among the cap largest verified logits
+// (ties: lower index), on the float32 logits.
+__global__ void __launch_bounds__(256)
+gate_fin_kernel(const float* __restrict__ part, int S, int T, int h,
+                const float* __restrict__ b1, const float* __restrict__ w2, double b2,
+                const int32_t* __restrict__ pq, const int32_t* __restrict__ query_passages,
+                double t, double rho, float* __restrict__ zbuf, int32_t* __restrict__ done,
+                float* __restrict__ logits, uint8_t* __restrict__ keep) {
+  __shared__ float wsum[4];
+  __shared__ int last;
+  const int p = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float s = 0.f;
+  const size_t zs = (size_t)T * h;
+  for (int j = threadIdx.x; j < h; j += blockDim.x) {
+    const float* src = part + (size_t)p * h + j;
+    float a = 0.f;
+    int zc = 0;
+    for (; zc + 8 <= S; zc += 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = src[(size_t)(zc + e) * zs];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a += v[e];
+    }
+    for (; zc < S; ++zc) a += src[(size_t)zc * zs];
+    a += b1 ? b1[j] : 0.f;
+    s = fmaf(fmaxf(a, 0.f), w2[j], s);
+  }
+  s = wave_sum_f32(s);
+  if (lane == 0) wsum[wave] = s;
+  __syncthreads();
+  const int b = pq[p];
   int p0, p1;
   range_of(query_passages, b, T, p0, p1);
   const int P = min(p1 - p0, 64);
-  float zl = 0.f;
-  if (lane < P) {
-    double acc = 0.0;
-    for (int u = 0; u < NT; ++u) acc += (double)part[(size_t)u * T + p0 + lane];
-    zl = (float)(acc + b2);
-    if (logits) logits[p0 + lane] = zl;
+  if (threadIdx.x == 0) {
+    const double tot = (((double)wsum[0] + (double)wsum[1]) + (double)wsum[2]) +
+                       (double)wsum[3] + b2;
+    const float zl = (float)tot;
+    zbuf[p] = zl;
+    if (logits) logits[p] = zl;
+    __threadfence();
+    const int prev = atomicAdd(&done[b], 1);
+    last = (prev == p1 - p0 - 1) ? 1 : 0;       // every block of the question is done
   }
-  z[lane] = zl;
-  ver[lane] = (lane < P && (double)zl >= t) ? 1 : 0;
   __syncthreads();
-  if (lane >= P) return;
+  if (!last || wave != 0) return;
+  // wave 0 of the question's last block: every logit of the question is
+  // written; the cut is taken with wave shuffles
+  __threadfence();
+  float zl = 0.f;
+  if (lane < P)
+    zl = __hip_atomic_load(&zbuf[p0 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int verified = (lane < P && (double)zl >= t) ? 1 : 0;
   const int cap = (int)ceil(rho * (double)P - 1e-9);
   int rank = 0;
-  for (int u = 0; u < P; ++u)
-    if (ver[u] && (z[u] > zl || (z[u] == zl && u < lane))) ++rank;
-  keep[p0 + lane] = (ver[lane] && rank < cap) ? 1u : 0u;
-}
-
-// v_bar of the fused route: the mean of V[b][kept_idx[r]] over the kept rows r
-// of question b (0 when it has none).  Workgroup (512-column slice, question);
-// wave w sums rows w, w+4, ... in float64, 16 bytes a lane; the four partial
-// sums are combined in wave order through LDS.
-__global__ void __launch_bounds__(256)
-gate_vbar_kernel(const bf16_t* __restrict__ V, int N, int d, const int32_t* __restrict__ kept_offsets,
-                 const int32_t* __restrict__ kept_idx, int total_kept,
-                 double* __restrict__ vbar) {
-  __shared__ double part[4][64][8];
-  const int b = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = (blockIdx.x * 64 + lane) * 8;
-  int r0, r1;
-  range_of(kept_offsets, b, total_kept, r0, r1);
-  double acc[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-  if (c < d) {
-    const bf16_t* base = V + (size_t)b * N * d + c;
-    for (int r = r0 + wave; r < r1; r += 4) {
-      const int i = clampi(kept_idx[r], 0, N - 1);
-      float x[8];
-      gunpack8(*reinterpret_cast<const u32x4*>(base + (size_t)i * d), x);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (double)x[e];
-    }
+  for (int u = 0; u < P; ++u) {
+    const float zu = __shfl(zl, u, kWave);
+    const int vu = __shfl(verified, u, kWave);
+    if (vu && (zu > zl || (zu == zl && u < lane))) ++rank;
   }
-#pragma unroll
-  for (int e = 0; e < 8; ++e) part[wave][lane][e] = acc[e];
-  __syncthreads();
-  if (wave != 0 || c >= d) return;
-  const int L = r1 - r0;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const double sum = ((part[0][lane][e] + part[1][lane][e]) + part[2][lane][e]) +
-                       part[3][lane][e];
-    vbar[(size_t)b * d + c + e] = L > 0 ? sum / (double)L : 0.0;
-  }
-}
-
-hipError_t launch_gate_vbar(const skip_problem_t& p, const void* V,
-                            const int32_t* kept_offsets, const int32_t* kept_idx,
-                            GateScratch g, hipStream_t s) {
-  hipLaunchKernelGGL(gate_vbar_kernel, dim3((p.d + 511) / 512, p.B), dim3(256), 0, s,
-                     (const bf16_t*)V, p.N, p.d, kept_offsets, kept_idx, p.total_kept, g.vbar);
-  return hipGetLastError();
+  if (lane < P) keep[p0 + lane] = (verified && rank < cap) ? 1u : 0u;
 }
 
 static size_t galign(size_t n) { return (n + 255) & ~(size_t)255; }
 
+// chunk length (64-column groups) and count S of the split over the 5d columns
+static void gate_split(int T, int h, int d, int* ch, int* S) {
+  const int tiles = ((T + kGateMT - 1) / kGateMT) * (h / kGateNT);
+  const int groups = (5 * d + 63) / 64;
+  int s = (kGateTargetWG + tiles - 1) / tiles;
+  const int smax = groups / 4 > 0 ? groups / 4 : 1;   // at least one group a wave
+  s = s < 1 ? 1 : (s > smax ? smax : s);
+  const int c = (groups + s - 1) / s;
+  *ch = c;
+  *S = (groups + c - 1) / c;
+}
+
 size_t gate_scratch_bytes(const skip_problem_t& p, int hidden) {
   const size_t T = (size_t)p.total_passages;
-  return galign((size_t)p.B * p.d * sizeof(double)) +        // vbar
-         galign((size_t)p.B * p.d * sizeof(double)) +        // qbar
-         galign(T * 3 * p.d * sizeof(bf16_t)) +               // X
-         galign((size_t)p.B * 2 * p.d * sizeof(bf16_t)) +     // QV
-         galign((size_t)p.B * hidden * sizeof(float)) +       // cvec
-         galign((size_t)(hidden / kGateNT) * T * sizeof(float)) +   // partial logits
-         galign(T * sizeof(int32_t));                         // question of each passage
+  int ch = 1, S = 1;
+  if (T > 0) gate_split((int)T, hidden, p.d, &ch, &S);
+  return 2 * galign((size_t)p.B * p.d * sizeof(double)) +          // qbar, vbar
+         galign(T * 5 * p.d * sizeof(bf16_t)) +                     // X
+         galign((size_t)S * T * hidden * sizeof(float)) +           // chunk partials
+         galign(T * sizeof(float)) +                                // logits
+         galign(T * sizeof(int32_t)) +                              // question of each passage
+         galign((size_t)p.B * sizeof(int32_t));                     // finish counters
 }
 
 GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base) {
   const size_t T = (size_t)p.total_passages;
+  int ch = 1, S = 1;
+  if (T > 0) gate_split((int)T, hidden, p.d, &ch, &S);
   char* c = static_cast<char*>(base);
   GateScratch g;
-  g.vbar = reinterpret_cast<double*>(c);
-  c += galign((size_t)p.B * p.d * sizeof(double));
   g.qbar = reinterpret_cast<double*>(c);
   c += galign((size_t)p.B * p.d * sizeof(double));
+  g.vbar = reinterpret_cast<double*>(c);
+  c += galign((size_t)p.B * p.d * sizeof(double));
   g.X = reinterpret_cast<bf16_t*>(c);
-  c += galign(T * 3 * p.d * sizeof(bf16_t));
-  g.QV = reinterpret_cast<bf16_t*>(c);
-  c += galign((size_t)p.B * 2 * p.d * sizeof(bf16_t));
-  g.cvec = reinterpret_cast<float*>(c);
-  c += galign((size_t)p.B * hidden * sizeof(float));
+  c += galign(T * 5 * p.d * sizeof(bf16_t));
   g.part = reinterpret_cast<float*>(c);
-  c += galign((size_t)(hidden / kGateNT) * T * sizeof(float));
+  c += galign((size_t)S * T * hidden * sizeof(float));
+  g.z = reinterpret_cast<float*>(c);
+  c += galign(T * sizeof(float));
   g.pq = reinterpret_cast<int32_t*>(c);
+  c += galign(T * sizeof(int32_t));
+  g.done = reinterpret_cast<int32_t*>(c);
   return g;
 }
 
-hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* qbar,
-                       const double* kbar, const float* passage_keys,
-                       const int32_t* query_passages, GateScratch g, float* logits,
-                       uint8_t* keep, hipStream_t s) {
+hipError_t launch_gate_means(const skip_problem_t& p, const void* Qtok,
+                             const int32_t* q_offsets, const void* rows,
+                             const int32_t* kept_offsets, const int32_t* kept_idx,
+                             GateScratch g, hipStream_t s) {
+  hipLaunchKernelGGL(gate_mean_kernel, dim3((p.d + 511) / 512, 2 * p.B), dim3(512), 0, s,
+                     (const bf16_t*)Qtok, q_offsets, p.total_qtok, (const bf16_t*)rows,
+                     kept_offsets, kept_idx, p.N, p.total_kept, p.B, p.d, g.qbar, g.vbar);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* kbar,
+                       const float* passage_keys, const int32_t* query_passages,
+                       GateScratch g, float* logits, uint8_t* keep, hipStream_t s) {
   const int T = p.total_passages, h = gt.hidden;
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gate_x_kernel, dim3(T + p.B), dim3(256), 0, s, qbar, g.vbar, kbar,
-                     passage_keys, query_passages, p.B, T, p.d, g.X, g.QV, g.pq);
-  const int qpb = p.d <= 4096 ? kGateCQ : kGateCQ / 2;   // LDS at most 64 KiB
-  const size_t lds = (size_t)qpb * 2 * p.d * sizeof(bf16_t);
-  hipLaunchKernelGGL(gate_c_kernel, dim3(h / kGateCJ, (p.B + qpb - 1) / qpb), dim3(256), lds,
-                     s, (const bf16_t*)g.QV, (const bf16_t*)gt.W, gt.b1, p.B, p.d, h, qpb,
-                     g.cvec);
-  hipLaunchKernelGGL(gate_score_kernel, dim3((T + kGateMT - 1) / kGateMT, h / kGateNT),
-                     dim3(256), 0, s, (const bf16_t*)g.X, (const bf16_t*)gt.W, T, p.d, h,
-                     (const int32_t*)g.pq, (const float*)g.cvec, gt.w2, g.part);
+  int ch = 1, S = 1;
+  gate_split(T, h, p.d, &ch, &S);
+  hipLaunchKernelGGL(gate_x_kernel, dim3(T), dim3(256), 0, s, (const double*)g.qbar,
+                     (const double*)g.vbar, kbar, passage_keys, query_passages, p.B, T, p.d,
+                     g.X, g.pq, g.done);
+  const int n_tiles = ((T + kGateMT - 1) / kGateMT) * (h / kGateNT);
+  hipLaunchKernelGGL(gate_score_kernel, dim3(8 * ((S + 7) / 8) * n_tiles), dim3(256), 0, s,
+                     (const bf16_t*)g.X, (const bf16_t*)gt.W, T, p.d, h, ch, S, g.part);
   const double t = std::log(gt.tau) - std::log1p(-gt.tau);
-  hipLaunchKernelGGL(gate_select_kernel, dim3(p.B), dim3(64), 0, s, (const float*)g.part,
-                     h / kGateNT, T, p.B, query_passages, gt.b2, t, gt.rho, logits, keep);
+  hipLaunchKernelGGL(gate_fin_kernel, dim3(T), dim3(256), 0, s, (const float*)g.part, S, T, h,
+                     gt.b1, gt.w2, gt.b2, (const int32_t*)g.pq, query_passages, t, gt.rho, g.z,
+                     g.done, logits, keep);
   return hipGetLastError();
 }
 

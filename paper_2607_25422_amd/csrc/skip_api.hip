@@ -336,14 +336,10 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
   hipStream_t s = static_cast<hipStream_t>(stream);
   Workspace w = carve_workspace(*p, workspace);
   GateScratch g = carve_gate_scratch(*p, gate->hidden, static_cast<char*>(workspace) + w.bytes);
-  // plain means: q_bar (question tokens) into u, v_bar (kept rows) into g.vbar,
-  // and the passage keys when they are not given
-  SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, Qtok,
-                        q_offsets, p->B, p->total_qtok, w.u, s));
-  SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, V_kept,
-                        kept_offsets, p->B, p->total_kept, g.vbar, s));
+  // q_bar and v_bar, the passage keys when they are not given, the gate
+  SKIP_TRY(launch_gate_means(*p, Qtok, q_offsets, V_kept, kept_offsets, nullptr, g, s));
   if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-  SKIP_TRY(launch_gate(*p, *gate, w.u, w.kbar, passage_keys, query_passages, g, logits, keep, s));
+  SKIP_TRY(launch_gate(*p, *gate, w.kbar, passage_keys, query_passages, g, logits, keep, s));
   return SKIP_OK;
 }
 
@@ -395,16 +391,14 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
   if (work) SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
   SKIP_TRY(mark());
   if (gate && p->total_passages > 0) {
-    // verify step: plain question means, kept-row means, then the gate on the
-    // passage keys pooled above
+    // verify step: question and kept-row means, then the gate on the passage
+    // keys pooled above
     GateScratch g = carve_gate_scratch(*p, gate->hidden, static_cast<char*>(workspace) + w.bytes);
-    SKIP_TRY(launch_pools(p->dtype, p->d, nullptr, nullptr, 0, 0, nullptr, nullptr, Qtok,
-                          q_offsets, p->B, p->total_qtok, g.qbar, s));
-    SKIP_TRY(launch_gate_vbar(*p, V, kept_offsets, kept_idx, g, s));
+    SKIP_TRY(launch_gate_means(*p, Qtok, q_offsets, V, kept_offsets, kept_idx, g, s));
     if (!work && !passage_keys)
       SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-    SKIP_TRY(launch_gate(*p, *gate, g.qbar, w.kbar, passage_keys, query_passages, g,
-                         gate_logits, passage_keep, s));
+    SKIP_TRY(launch_gate(*p, *gate, w.kbar, passage_keys, query_passages, g, gate_logits,
+                         passage_keep, s));
   }
   if (work)
     SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,

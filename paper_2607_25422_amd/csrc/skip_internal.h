@@ -52,26 +52,26 @@ hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, c
 
 // Passage verification gate ---------------------------------------------
 struct GateScratch {
-  double* vbar;      // [B][d]         mean of the kept visual rows
   double* qbar;      // [B][d]         mean of the question tokens
-  bf16_t* X;         // [T][3d]        passage part of the gate input
-  bf16_t* QV;        // [B][2d]        question part [q_bar' ; v_bar']
-  float* cvec;       // [B][h]         W[:, 0:2d] [q_bar' ; v_bar'] + b1
-  float* part;       // [h/64][T]      partial logits per 64 hidden units
+  double* vbar;      // [B][d]         mean of the kept visual rows
+  bf16_t* X;         // [T][5d]        gate inputs
+  float* part;       // [S][T][h]      chunk partials of W x
+  float* z;          // [T]            logits
   int32_t* pq;       // [T]            question of each passage
+  int32_t* done;     // [B]            finished passages per question
 };
 size_t gate_scratch_bytes(const skip_problem_t& p, int hidden);
 GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base);
-// qbar: plain question means; kbar: pooled passage keys (unused when
-// passage_keys is given); g.vbar must hold the kept-row means.
-// g.vbar from the kept rows of V named by kept_idx (the fused route)
-hipError_t launch_gate_vbar(const skip_problem_t& p, const void* V,
-                            const int32_t* kept_offsets, const int32_t* kept_idx,
-                            GateScratch g, hipStream_t s);
-hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* qbar,
-                       const double* kbar, const float* passage_keys,
-                       const int32_t* query_passages, GateScratch g, float* logits,
-                       uint8_t* keep, hipStream_t s);
+// g.qbar, g.vbar from the question tokens and the kept rows: rows[kept
+// range] when kept_idx is NULL, else V[b][kept_idx[r]] (rows = V)
+hipError_t launch_gate_means(const skip_problem_t& p, const void* Qtok,
+                             const int32_t* q_offsets, const void* rows,
+                             const int32_t* kept_offsets, const int32_t* kept_idx,
+                             GateScratch g, hipStream_t s);
+// the gate on g's means and the passage keys (kbar, or passage_keys if given)
+hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* kbar,
+                       const float* passage_keys, const int32_t* query_passages,
+                       GateScratch g, float* logits, uint8_t* keep, hipStream_t s);
 
 // Stage 2 ---------------------------------------------------------------
 // Query rows: if kept_idx is non-NULL, row r of question b is
