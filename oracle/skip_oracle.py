@@ -17,7 +17,11 @@ one kept row at a time, following the paper's definitions in their own order:
 * the bipartite graph between kept tokens and passages (App. B.3, Def. B.3,
   edge rule; Alg. 1, graph step);
 * sparse cross-attention restricted to that graph (Def. B.3, attention rule;
-  Alg. 1, fuse step).
+  Alg. 1, fuse step);
+* the passage verification gate (App. B.4, Def. B.4; Alg. 1, verify step);
+* the regions of the kept tokens, an approximate k-means of them into
+  R = min(V'/4, 8) regions (Sec. 3.4, the clustering that feeds per-region
+  retrieval; the retrieval itself is not part of this path).
 
 Readings where the paper is silent or inconsistent (each is listed with its
 justification in the design notes of the repository):
@@ -135,6 +139,53 @@ def qvs_topk(z: np.ndarray, k: int) -> np.ndarray:
 def gather_rows(V: np.ndarray, idx: np.ndarray) -> np.ndarray:
     """V_hat = the rows of V at the kept indices (Alg. 1, TopK step)."""
     return np.asarray(V)[np.asarray(idx, dtype=np.int64)]
+
+
+# --------------------------------------------------------------------------
+# Regions of the kept tokens (Sec. 3.4, region-conditional retrieval)
+# --------------------------------------------------------------------------
+
+def region_count(k: int, r_max: int = 8) -> int:
+    """R = min(V'/4, 8) regions for V' = k kept tokens (Sec. 3.4), V'/4 taken
+    down to a whole number, at least one region when any token is kept and
+    none when none is; r_max replaces the 8."""
+    if k <= 0:
+        return 0
+    return max(1, min(k // 4, int(r_max)))
+
+
+def region_kmeans(Vhat: np.ndarray, R: int, n_iter: int):
+    """Approximate k-means of the kept rows in embedding space (Sec. 3.4):
+    a fixed number of Lloyd iterations from a fixed start.
+
+    * start: centroid r is the kept row at position floor((2r+1) k / (2R)) of
+      the kept list, the middle of the r-th of R equal runs of it (the list is
+      in ascending token order, so the runs are spread over the image);
+    * iteration: every row goes to the centroid at the least squared
+      Euclidean distance (ties to the lower region), then every centroid
+      becomes the mean of its rows; a region left without rows keeps its
+      centroid.
+
+    Vhat: [k, d].  Returns (assignment [k] int, centroids [R, d] float64,
+    sizes [R] int) after n_iter iterations."""
+    X = np.asarray(Vhat, dtype=np.float64)
+    k = X.shape[0]
+    if R < 1 or R > k:
+        raise ValueError("need 1 <= R <= k")
+    if n_iter < 1:
+        raise ValueError("need at least one iteration")
+    C = np.stack([X[((2 * r + 1) * k) // (2 * R)] for r in range(R)])
+    assign = np.zeros(k, dtype=np.int64)
+    for _ in range(n_iter):
+        for i in range(k):
+            dist = ((X[i][None, :] - C) ** 2).sum(axis=1)
+            assign[i] = int(np.argmin(dist))        # first minimum: the lower region
+        for r in range(R):
+            members = X[assign == r]
+            if members.shape[0] > 0:
+                C[r] = members.sum(axis=0) / members.shape[0]
+    sizes = np.array([int((assign == r).sum()) for r in range(R)], dtype=np.int64)
+    return assign, C, sizes
 
 
 # --------------------------------------------------------------------------

@@ -636,3 +636,93 @@ def test_route_gate_drops_passages_from_the_graph():
         assert np.array_equal(keep, orc.skv_keep(r.gate_logits[q], 0.5, 0.5))
         assert not r.adj[q][:, ~keep].any()
         assert r.adj[q].sum() == min(math.ceil(4.0 * k), k * int(keep.sum()))
+
+
+# ---------------------------------------------------------------- regions (k-means)
+
+def test_region_count_rule():
+    # R = min(V'/4, 8), whole regions, at least one when anything is kept
+    want = {0: 0, 1: 1, 3: 1, 4: 1, 7: 1, 8: 2, 31: 7, 32: 8, 33: 8, 192: 8, 384: 8}
+    for k, r in want.items():
+        assert orc.region_count(k) == r, k
+    assert orc.region_count(192, r_max=4) == 4
+    assert orc.region_count(9, r_max=16) == 2
+
+
+def test_region_kmeans_worked_example():
+    """Six points on a line, two regions, iterated by hand: the start is rows
+    1 and 4 (1 and 7); the second iteration meets an exact tie (5 is 4.5 from
+    both 0.5 and 9.5) that goes to the lower region."""
+    X = np.array([0.0, 1.0, 5.0, 6.0, 7.0, 20.0])[:, None]
+    by_hand = {1: ([0, 0, 1, 1, 1, 1], [0.5, 9.5]), 2: ([0, 0, 0, 1, 1, 1], [2.0, 11.0]),
+               3: ([0, 0, 0, 0, 1, 1], [3.0, 13.5]), 4: ([0, 0, 0, 0, 0, 1], [3.8, 20.0]),
+               10: ([0, 0, 0, 0, 0, 1], [3.8, 20.0])}
+    for n, (a, c) in by_hand.items():
+        got_a, got_c, sizes = orc.region_kmeans(X, 2, n)
+        assert got_a.tolist() == a, n
+        np.testing.assert_allclose(got_c[:, 0], c, rtol=1e-15)
+        assert sizes.tolist() == [a.count(0), a.count(1)]
+    # the same points in three dimensions, the line along the second axis
+    X3 = np.zeros((6, 3))
+    X3[:, 1] = X[:, 0]
+    a3, c3, _ = orc.region_kmeans(X3, 2, 3)
+    assert a3.tolist() == by_hand[3][0]
+    np.testing.assert_allclose(c3[:, 1], by_hand[3][1], rtol=1e-15)
+    assert np.all(c3[:, [0, 2]] == 0)
+
+
+def test_region_kmeans_empty_region_keeps_its_centroid():
+    # both starting centroids are the point 0: every distance ties, so every
+    # row goes to region 0 and region 1 stays where it started ...
+    X = np.array([0.0, 0.0, 0.0, 0.0, 10.0])[:, None]
+    a, c, sizes = orc.region_kmeans(X, 2, 1)
+    assert a.tolist() == [0, 0, 0, 0, 0]
+    assert c[:, 0].tolist() == [2.0, 0.0]
+    assert sizes.tolist() == [5, 0]
+    # ... and the next iteration gives it the four zeros (0 from it, 4 from 2)
+    a, c, sizes = orc.region_kmeans(X, 2, 3)
+    assert a.tolist() == [1, 1, 1, 1, 0]
+    assert c[:, 0].tolist() == [10.0, 0.0]
+    assert sizes.tolist() == [1, 4]
+
+
+def test_region_kmeans_recovers_separated_blobs():
+    """Eight far-apart blobs, rows listed blob by blob: the start takes one row
+    of each blob, so one iteration labels every row by its blob and every
+    centroid is its blob's mean."""
+    rng = np.random.default_rng(3)
+    d, per = 16, 12
+    centres = rng.standard_normal((8, d)) * 100.0
+    X = np.concatenate([c + rng.standard_normal((per, d)) for c in centres])
+    a, C, sizes = orc.region_kmeans(X, 8, 1)
+    assert a.tolist() == [r for r in range(8) for _ in range(per)]
+    for r in range(8):
+        np.testing.assert_allclose(C[r], X[r * per:(r + 1) * per].mean(axis=0), rtol=1e-13)
+    assert sizes.tolist() == [per] * 8
+
+
+def _sse(X, a, C):
+    return float(((X - C[a]) ** 2).sum())
+
+
+def test_region_kmeans_lloyd_properties():
+    """Lloyd iterations: the within-region sum of squares never grows, and at
+    a fixed point every row sits at its nearest centroid (brute force) and
+    every non-empty centroid is its rows' mean."""
+    rng = np.random.default_rng(11)
+    X = np.concatenate([rng.standard_normal((30, 8)) + 4.0 * rng.standard_normal(8)
+                        for _ in range(5)])
+    last = np.inf
+    for n in range(1, 9):
+        a, C, _ = orc.region_kmeans(X, 6, n)
+        # the assignment of iteration n against the centroids before it is at
+        # least as good as any other; after the centroid step the SSE drops
+        sse = _sse(X, a, C)
+        assert sse <= last + 1e-9
+        last = sse
+    a, C, sizes = orc.region_kmeans(X, 6, 100)
+    D = ((X[:, None, :] - C[None, :, :]) ** 2).sum(axis=2)
+    assert np.array_equal(a, D.argmin(axis=1))
+    for r in range(6):
+        if sizes[r]:
+            np.testing.assert_allclose(C[r], X[a == r].mean(axis=0), rtol=1e-12)
