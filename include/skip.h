@@ -282,6 +282,37 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
                             size_t workspace_bytes, void* stream);
 
 /*
+ * Regions of the kept tokens (Sec. 3.4: the approximate k-means with which
+ * region-conditional retrieval groups the kept tokens before issuing one
+ * retrieval query per region centroid; the retrieval is not part of this
+ * library).  Question b with k_b kept rows gets R_b = min(floor(k_b / 4),
+ * r_max) regions, at least 1 when k_b >= 1 and none when k_b = 0.  Start:
+ * centroid r = the kept row at position floor((2r+1) k_b / (2 R_b)) of the
+ * question's kept list.  Then n_iter Lloyd iterations in float64: every row to
+ * the centroid at the least squared Euclidean distance (ties to the lower
+ * region), every centroid to the mean of its rows (a region left without rows
+ * keeps its centroid).
+ *   rows      kept_idx NULL: the kept rows, [total_kept][d] (as written by
+ *             skip_prune_topk); else V [B][N][d], row r of question b being
+ *             V[b][kept_idx[r]] (as in the fused route)
+ *   r_max     1..16 (paper: 8);  n_iter  1..1000
+ *   region    out [total_kept] int32: the region of each kept row after the
+ *             last iteration
+ *   centroids out [B][r_max][d] float: the centroids after the last
+ *             iteration, rounded to float (rows r >= R_b are 0)
+ *   sizes     out [B][r_max] int32 rows per region, or NULL
+ * Distances are compared as |c_r|^2 - 2 v.c_r (the row's own |v|^2 is common
+ * to all regions).  Workspace: skip_workspace_bytes_regions.
+ */
+skip_status_t skip_workspace_bytes_regions(const skip_problem_t* p, int32_t r_max,
+                                           size_t* bytes);
+skip_status_t skip_region_kmeans(const skip_problem_t* p, const void* rows,
+                                 const int32_t* kept_offsets, const int32_t* kept_idx,
+                                 int32_t r_max, int32_t n_iter, int32_t* region,
+                                 float* centroids, int32_t* sizes, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/*
  * Stage 2: bipartite graph + sparse cross-attention (Def. B.3; Alg. 1,
  * graph and fuse steps) on caller-given kept-row queries.
  *   Qh              [total_kept][H][d_h] queries of the kept rows

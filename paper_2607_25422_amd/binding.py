@@ -30,7 +30,8 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_prune_topk", "skip_bipartite_xattn", "skip_route_fused",
                 "skip_route_fused_profiled", "skip_workspace_bytes_mlp",
                 "skip_prune_topk_mlp", "skip_workspace_bytes_gate", "skip_skv_gate",
-                "skip_bipartite_xattn_masked", "skip_route_fused_gated")
+                "skip_bipartite_xattn_masked", "skip_route_fused_gated",
+                "skip_workspace_bytes_regions", "skip_region_kmeans")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -119,6 +120,12 @@ def _load() -> ctypes.CDLL:
     lib.skip_route_fused_gated.restype = ctypes.c_int
     lib.skip_route_fused_gated.argtypes = [P, G, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                            vp, i32p, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.skip_workspace_bytes_regions.restype = ctypes.c_int
+    lib.skip_workspace_bytes_regions.argtypes = [P, ctypes.c_int32,
+                                                 ctypes.POINTER(ctypes.c_size_t)]
+    lib.skip_region_kmeans.restype = ctypes.c_int
+    lib.skip_region_kmeans.argtypes = [P, vp, i32p, i32p, ctypes.c_int32, ctypes.c_int32, i32p,
+                                       vp, i32p, vp, ctypes.c_size_t, vp]
     lib.skip_route_fused_profiled.restype = ctypes.c_int
     lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                               vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
@@ -207,6 +214,13 @@ def workspace_bytes_gate(p: SkipProblem, hidden: int) -> int:
     n = ctypes.c_size_t(0)
     _check(LIB.skip_workspace_bytes_gate(ctypes.byref(p), int(hidden), ctypes.byref(n)),
            "skip_workspace_bytes_gate")
+    return int(n.value)
+
+
+def workspace_bytes_regions(p: SkipProblem, r_max: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.skip_workspace_bytes_regions(ctypes.byref(p), int(r_max), ctypes.byref(n)),
+           "skip_workspace_bytes_regions")
     return int(n.value)
 
 
@@ -387,6 +401,24 @@ def skip_route_fused_gated(p: SkipProblem, gate: "SkvGate", V, Qtok, q_offsets, 
         _ptr(lse, "lse", torch.float32, p.total_kept * p.H), workspace.data_ptr(),
         workspace.numel(), _stream(stream))
     _check(st, "skip_route_fused_gated")
+
+
+def skip_region_kmeans(p: SkipProblem, rows, kept_offsets, kept_idx, r_max, n_iter, region,
+                       centroids, sizes=None, workspace=None, stream=None):
+    et = _elem_dtype(p)
+    if workspace is None:
+        workspace = torch.empty(max(workspace_bytes_regions(p, r_max), 256), dtype=torch.uint8,
+                                device=centroids.device)
+    n_rows = p.B * p.N if kept_idx is not None else p.total_kept
+    st = LIB.skip_region_kmeans(
+        ctypes.byref(p), _ptr(rows, "rows", et, n_rows * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept), int(r_max), int(n_iter),
+        _ptr(region, "region", torch.int32, p.total_kept),
+        _ptr(centroids, "centroids", torch.float32, p.B * r_max * p.d),
+        _ptr(sizes, "sizes", torch.int32, p.B * r_max), workspace.data_ptr(), workspace.numel(),
+        _stream(stream))
+    _check(st, "skip_region_kmeans")
 
 
 def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
@@ -621,6 +653,21 @@ def route_fused_gated(db: DeviceBatch, gate: SkvGate, passage_keys=None, out=Non
                            O, lse, logits, passage_keys, workspace)
     return (kept_idx[:p.total_kept], keep[:p.total_passages], logits[:p.total_passages],
             O[:p.total_kept], lse[:p.total_kept])
+
+
+def region_kmeans(db: DeviceBatch, rows: torch.Tensor, kept_idx=None, r_max: int = 8,
+                  n_iter: int = 10, workspace=None):
+    """Regions of the kept tokens.  ``rows``: the kept rows [total_kept, d], or
+    db.V with ``kept_idx``.  Returns (region [total_kept] int32, centroids
+    [B, r_max, d] float32, sizes [B, r_max] int32)."""
+    p = db.p
+    dev = db.V.device
+    region = torch.empty(max(p.total_kept, 1), dtype=torch.int32, device=dev)
+    cent = torch.empty((p.B, r_max, p.d), dtype=torch.float32, device=dev)
+    sizes = torch.empty((p.B, r_max), dtype=torch.int32, device=dev)
+    skip_region_kmeans(p, rows if p.total_kept else None, db.kept_offsets, kept_idx, r_max,
+                       n_iter, region if p.total_kept else None, cent, sizes, workspace)
+    return region[:p.total_kept], cent, sizes
 
 
 def route_fused(db: DeviceBatch, passage_keys=None, out=None, stage_events=None):

@@ -1,0 +1,292 @@
+// Regions of the kept tokens (paper Sec. 3.4: region-conditional retrieval
+// clusters the kept visual tokens into R = min(V'/4, 8) regions by an
+// approximate k-means in embedding space; each region's centroid then seeds a
+// retrieval query).  Lloyd iterations from a fixed start, float64 throughout:
+//   start       centroid r = kept row floor((2r+1) k / (2R))
+//   iteration   each row to the nearest centroid (squared distance, ties to
+//               the lower region); each centroid to the mean of its rows, a
+//               region without rows keeping its centroid
+// Launches: one clear of the per-question counters, then n_iter + 1 steps of
+// region_step_kernel over (column slice, question) workgroups:
+//   step 0          start centroids; partial products for the first assignment
+//   step t (< n)    centroids from assignment t; partial products for t + 1
+//   step n          centroids from assignment n; outputs
+// In a step the slice workgroups of a question write their partial dot
+// products v_i . c_r and squared norms |c_r|^2 over their columns; the last
+// of them to finish (a counter) sums the partials in slice order and assigns
+// every row by argmin_r |c_r|^2 - 2 v_i . c_r, which is |v_i - c_r|^2 less the
+// row's own |v_i|^2.
+#include "skip_common.h"
+#include "skip_internal.h"
+
+namespace skip {
+
+constexpr int kRegCols = 256;     // columns per slice = threads per workgroup
+constexpr int kRegMax = 16;       // largest r_max
+
+namespace {
+
+template <typename T> __device__ __forceinline__ double reg_load1(const T* p);
+template <> __device__ __forceinline__ double reg_load1<float>(const float* p) {
+  return (double)*p;
+}
+template <> __device__ __forceinline__ double reg_load1<bf16_t>(const bf16_t* p) {
+  return (double)bf16_to_f32(*p);
+}
+
+// eight consecutive elements as doubles (16-byte aligned for bf16, 32 for f32)
+template <typename T> __device__ __forceinline__ void reg_load8(const T* p, double* o);
+template <> __device__ __forceinline__ void reg_load8<float>(const float* p, double* o) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+template <> __device__ __forceinline__ void reg_load8<bf16_t>(const bf16_t* p, double* o) {
+  const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    o[2 * w] = (double)__uint_as_float(x[w] << 16);
+    o[2 * w + 1] = (double)__uint_as_float(x[w] & 0xffff0000u);
+  }
+}
+
+__device__ __forceinline__ int regions_of(int k, int r_max) {
+  if (k <= 0) return 0;
+  const int r = k / 4;
+  return r < 1 ? 1 : (r > r_max ? r_max : r);
+}
+
+}  // namespace
+
+__global__ void region_clear_kernel(int32_t* __restrict__ done, int B) {
+  for (int b = threadIdx.x; b < B; b += blockDim.x) done[b] = 0;
+}
+
+struct RegionArgs {
+  const int32_t* kept_offsets;
+  const int32_t* kept_idx;     // NULL: rows are the kept rows themselves
+  int N, total_kept, B, d, k_max, r_max, S, t, n_iter;
+  double* C;                   // [B][r_max][d]      centroids of the last step
+  double* P;                   // [B][S][k_max][r_max] partial v_i . c_r
+  double* CN;                  // [B][S][r_max]       partial |c_r|^2
+  uint8_t* asg;                // [total_kept]        current assignment
+  int32_t* sizes;              // [B][r_max]          rows per region
+  int32_t* done;               // [B]                 finished slices
+  int32_t* region_out;         // [total_kept]
+  float* cent_out;             // [B][r_max][d]
+  int32_t* sizes_out;          // [B][r_max] or NULL
+};
+
+template <typename T>
+__global__ void __launch_bounds__(kRegCols)
+region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
+  __shared__ double cs[kRegMax][kRegCols];
+  __shared__ int last;
+  __shared__ int cnt[kRegMax];
+  const int s = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  int k0, k1;
+  range_of(a.kept_offsets, b, a.total_kept, k0, k1);
+  const int k = min(k1 - k0, a.k_max);
+  const int R = regions_of(k, a.r_max);
+  const int c0 = s * kRegCols, c = c0 + tid;
+  const int ncol = min(kRegCols, a.d - c0);
+  const bool cok = tid < ncol;
+  auto row_of = [&](int i) -> const T* {
+    if (a.kept_idx) {
+      const int src = clampi(a.kept_idx[k0 + i], 0, a.N - 1);
+      return rows + ((size_t)b * a.N + src) * a.d;
+    }
+    return rows + (size_t)(k0 + i) * a.d;
+  };
+  const bool final_step = a.t == a.n_iter;
+
+  if (R == 0) {
+    if (final_step) {
+      for (int r = 0; r < a.r_max; ++r)
+        if (cok) a.cent_out[((size_t)b * a.r_max + r) * a.d + c] = 0.f;
+      if (s == 0 && a.sizes_out && tid < a.r_max) a.sizes_out[b * a.r_max + tid] = 0;
+    }
+    return;
+  }
+
+  // ---- centroids of this step, this slice's columns
+  if (a.t == 0) {
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) {
+      if (r >= R) break;
+      const int pos = ((2 * r + 1) * k) / (2 * R);
+      cs[r][tid] = cok ? reg_load1<T>(row_of(pos) + c) : 0.0;
+    }
+  } else {
+    double acc[kRegMax];
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) acc[r] = 0.0;
+    for (int i = 0; i < k; ++i) {
+      const int ai = a.asg[k0 + i];
+      const double v = cok ? reg_load1<T>(row_of(i) + c) : 0.0;
+#pragma unroll
+      for (int r = 0; r < kRegMax; ++r) {
+        if (r >= R) break;
+        acc[r] += (r == ai) ? v : 0.0;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) {
+      if (r >= R) break;
+      const int n = a.sizes[b * a.r_max + r];
+      const double old = cok ? a.C[((size_t)b * a.r_max + r) * a.d + c] : 0.0;
+      cs[r][tid] = n > 0 ? acc[r] / (double)n : old;
+    }
+  }
+  if (!final_step && cok) {
+    for (int r = 0; r < R; ++r) a.C[((size_t)b * a.r_max + r) * a.d + c] = cs[r][tid];
+  }
+  __syncthreads();
+
+  if (final_step) {
+    for (int r = 0; r < a.r_max; ++r)
+      if (cok)
+        a.cent_out[((size_t)b * a.r_max + r) * a.d + c] = r < R ? (float)cs[r][tid] : 0.f;
+    if (s == 0) {
+      for (int i = tid; i < k; i += blockDim.x) a.region_out[k0 + i] = a.asg[k0 + i];
+      if (a.sizes_out && tid < a.r_max)
+        a.sizes_out[b * a.r_max + tid] = tid < R ? a.sizes[b * a.r_max + tid] : 0;
+    }
+    return;
+  }
+
+  // ---- partial products over this slice: row i per thread, centroids from LDS
+  double* P = a.P + ((size_t)b * a.S + s) * a.k_max * a.r_max;
+  for (int i = tid; i < k; i += blockDim.x) {
+    const T* v = row_of(i) + c0;
+    double dot[kRegMax];
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) dot[r] = 0.0;
+    for (int j = 0; j < ncol; j += 8) {         // d is a multiple of 8
+      double x[8];
+      reg_load8<T>(v + j, x);
+#pragma unroll
+      for (int r = 0; r < kRegMax; ++r) {
+        if (r >= R) break;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dot[r] = fma(x[e], cs[r][j + e], dot[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) {
+      if (r >= R) break;
+      P[(size_t)i * a.r_max + r] = dot[r];
+    }
+  }
+  if (tid < 64) {
+    // |c_r|^2 over the slice: lane l takes the columns l, l+64, ... in order,
+    // then a fixed shuffle tree
+    for (int r = 0; r < R; ++r) {
+      double q = 0.0;
+      for (int j = tid; j < ncol; j += 64) q = fma(cs[r][j], cs[r][j], q);
+      q = wave_sum_f64(q);
+      if (tid == 0) a.CN[((size_t)b * a.S + s) * a.r_max + r] = q;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    __threadfence();
+    const int prev = atomicAdd(&a.done[b], 1);
+    last = (prev == a.S - 1) ? 1 : 0;
+  }
+  if (tid < kRegMax) cnt[tid] = 0;
+  __syncthreads();
+  if (!last) return;
+
+  // ---- the question's last slice: assignment for the next step
+  __threadfence();
+  const double* Pb = a.P + (size_t)b * a.S * a.k_max * a.r_max;
+  const double* CNb = a.CN + (size_t)b * a.S * a.r_max;
+  double cn[kRegMax];
+#pragma unroll
+  for (int r = 0; r < kRegMax; ++r) {
+    cn[r] = 0.0;
+    if (r < R)
+      for (int z = 0; z < a.S; ++z) cn[r] += CNb[z * a.r_max + r];
+  }
+  for (int i = tid; i < k; i += blockDim.x) {
+    int best = 0;
+    double bd = 0.0;
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) {
+      if (r >= R) break;
+      double dot = 0.0;
+      for (int z = 0; z < a.S; ++z) dot += Pb[((size_t)z * a.k_max + i) * a.r_max + r];
+      const double dist = cn[r] - 2.0 * dot;
+      if (r == 0 || dist < bd) {
+        bd = dist;
+        best = r;
+      }
+    }
+    a.asg[k0 + i] = (uint8_t)best;
+    atomicAdd(&cnt[best], 1);
+  }
+  __syncthreads();
+  if (tid < R) a.sizes[b * a.r_max + tid] = cnt[tid];
+  if (tid == 0) a.done[b] = 0;
+}
+
+static size_t ralign(size_t n) { return (n + 255) & ~(size_t)255; }
+
+int region_slices(const skip_problem_t& p) { return (p.d + kRegCols - 1) / kRegCols; }
+
+size_t region_scratch_bytes(const skip_problem_t& p, int r_max) {
+  const size_t S = (size_t)region_slices(p);
+  return ralign((size_t)p.B * r_max * p.d * sizeof(double)) +
+         ralign((size_t)p.B * S * p.k_max * r_max * sizeof(double)) +
+         ralign((size_t)p.B * S * r_max * sizeof(double)) +
+         ralign((size_t)p.total_kept) +
+         ralign((size_t)p.B * r_max * sizeof(int32_t)) +
+         ralign((size_t)p.B * sizeof(int32_t));
+}
+
+hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
+                          const int32_t* kept_idx, int r_max, int n_iter, int32_t* region,
+                          float* centroids, int32_t* sizes, void* scratch, hipStream_t s) {
+  const int S = region_slices(p);
+  char* c = static_cast<char*>(scratch);
+  RegionArgs a;
+  a.kept_offsets = kept_offsets;
+  a.kept_idx = kept_idx;
+  a.N = p.N;
+  a.total_kept = p.total_kept;
+  a.B = p.B;
+  a.d = p.d;
+  a.k_max = p.k_max;
+  a.r_max = r_max;
+  a.S = S;
+  a.n_iter = n_iter;
+  a.C = reinterpret_cast<double*>(c);
+  c += ralign((size_t)p.B * r_max * p.d * sizeof(double));
+  a.P = reinterpret_cast<double*>(c);
+  c += ralign((size_t)p.B * S * p.k_max * r_max * sizeof(double));
+  a.CN = reinterpret_cast<double*>(c);
+  c += ralign((size_t)p.B * S * r_max * sizeof(double));
+  a.asg = reinterpret_cast<uint8_t*>(c);
+  c += ralign((size_t)p.total_kept);
+  a.sizes = reinterpret_cast<int32_t*>(c);
+  c += ralign((size_t)p.B * r_max * sizeof(int32_t));
+  a.done = reinterpret_cast<int32_t*>(c);
+  a.region_out = region;
+  a.cent_out = centroids;
+  a.sizes_out = sizes;
+  hipLaunchKernelGGL(region_clear_kernel, dim3(1), dim3(256), 0, s, a.done, p.B);
+  for (int t = 0; t <= n_iter; ++t) {
+    a.t = t;
+    if (p.dtype == SKIP_F32)
+      hipLaunchKernelGGL(region_step_kernel<float>, dim3(S, p.B), dim3(kRegCols), 0, s,
+                         (const float*)rows, a);
+    else
+      hipLaunchKernelGGL(region_step_kernel<bf16_t>, dim3(S, p.B), dim3(kRegCols), 0, s,
+                         (const bf16_t*)rows, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace skip

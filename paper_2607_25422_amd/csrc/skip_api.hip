@@ -428,6 +428,37 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V, const voi
                           workspace, workspace_bytes, stream, nullptr);
 }
 
+skip_status_t skip_workspace_bytes_regions(const skip_problem_t* p, int32_t r_max,
+                                           size_t* bytes) {
+  if (!bytes) return SKIP_ERR_INVALID_ARG;
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (r_max < 1 || r_max > 16) return SKIP_ERR_INVALID_ARG;
+  *bytes = region_scratch_bytes(*p, r_max);
+  return SKIP_OK;
+}
+
+skip_status_t skip_region_kmeans(const skip_problem_t* p, const void* rows,
+                                 const int32_t* kept_offsets, const int32_t* kept_idx,
+                                 int32_t r_max, int32_t n_iter, int32_t* region,
+                                 float* centroids, int32_t* sizes, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (!kept_offsets || !centroids || !workspace) return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && (!rows || !region)) return SKIP_ERR_INVALID_ARG;
+  if (r_max < 1 || r_max > 16 || n_iter < 1 || n_iter > 1000) return SKIP_ERR_INVALID_ARG;
+  if (kept_idx) {
+    if (p->N < 1 || p->k_max > p->N) return SKIP_ERR_INVALID_ARG;
+    if ((int64_t)p->B * p->N > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  }
+  if (workspace_bytes < region_scratch_bytes(*p, r_max)) return SKIP_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SKIP_TRY(launch_regions(*p, rows, kept_offsets, kept_idx, r_max, n_iter, region, centroids,
+                          sizes, workspace, s));
+  return SKIP_OK;
+}
+
 skip_status_t skip_route_fused_gated(const skip_problem_t* p, const skip_skv_gate_t* gate,
                                      const void* V, const void* Qtok,
                                      const int32_t* q_offsets, const void* w_bias,

@@ -73,6 +73,14 @@ hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const
                        const float* passage_keys, const int32_t* query_passages,
                        GateScratch g, float* logits, uint8_t* keep, hipStream_t s);
 
+// Regions of the kept tokens (k-means) ------------------------------------
+int region_slices(const skip_problem_t& p);
+size_t region_scratch_bytes(const skip_problem_t& p, int r_max);
+// rows: the kept rows (kept_idx NULL) or V read through kept_idx
+hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
+                          const int32_t* kept_idx, int r_max, int n_iter, int32_t* region,
+                          float* centroids, int32_t* sizes, void* scratch, hipStream_t s);
+
 // Stage 2 ---------------------------------------------------------------
 // Query rows: if kept_idx is non-NULL, row r of question b is
 // V[b][kept_idx[r]] (the fused route); otherwise it is Qh[r].

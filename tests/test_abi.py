@@ -244,3 +244,33 @@ def test_masked_xattn_validation(b):
     assert call(p, O=None) == b.SKIP_ERR_INVALID_ARG
     assert call(p, ws_bytes=0) == b.SKIP_ERR_WORKSPACE
     assert call(_problem(b, H=8)) == b.SKIP_ERR_INVALID_ARG
+
+
+def test_region_kmeans_validation(b):
+    p = _problem(b)
+    n = b.workspace_bytes_regions(p, 8)
+    assert n > 0 and b.workspace_bytes_regions(p, 16) > n
+    with pytest.raises(b.SkipError):
+        b.workspace_bytes_regions(p, 0)
+    with pytest.raises(b.SkipError):
+        b.workspace_bytes_regions(p, 17)
+
+    def call(q, rows=FAKE, ko=FAKE, idx=None, r_max=8, n_iter=10, region=FAKE, cent=FAKE,
+             ws=FAKE, ws_bytes=1 << 30):
+        return b.LIB.skip_region_kmeans(ctypes.byref(q), rows, ko, idx, r_max, n_iter, region,
+                                        cent, None, ws, ws_bytes, None)
+    # every call fails validation
+    assert call(p, rows=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, ko=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, region=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, cent=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, ws=None) == b.SKIP_ERR_INVALID_ARG
+    for r_max in (0, 17, -1):
+        assert call(p, r_max=r_max) == b.SKIP_ERR_INVALID_ARG, r_max
+    for n_iter in (0, 1001):
+        assert call(p, n_iter=n_iter) == b.SKIP_ERR_INVALID_ARG, n_iter
+    q = _problem(b)
+    q.k_max = 600             # kept rows read through kept_idx need k_max <= N
+    q.total_kept = 1200
+    assert call(q, idx=FAKE) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, ws_bytes=n - 1) == b.SKIP_ERR_WORKSPACE
