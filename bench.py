@@ -58,6 +58,11 @@ def parse():
     ap.add_argument("--gate", action="store_true",
                     help="time the fused route with the passage verification gate (and the "
                          "route without it, interleaved) instead of the plain fused route")
+    ap.add_argument("--regions", action="store_true",
+                    help="time the regions of the kept tokens (k-means of the kept rows, read "
+                         "in place through the kept indices) instead of the fused route")
+    ap.add_argument("--r-max", type=int, default=8, help="most regions per question")
+    ap.add_argument("--kmeans-iter", type=int, default=10, help="Lloyd iterations")
     ap.add_argument("--gate-tau", type=float, default=0.5, help="gate threshold on nu")
     ap.add_argument("--gate-rho", type=float, default=0.5,
                     help="kept fraction of a question's passages after the gate")
@@ -286,6 +291,69 @@ def bench_gated_route(args):
     print(json.dumps(res), flush=True)
 
 
+FP64_PEAK_TFLOPS = 78.6
+
+
+def bench_regions(args):
+    """Regions of the kept tokens: k-means of each question's kept rows (read
+    in place through the kept indices of a prune call made beforehand),
+    event-timed on the launch stream.  The floor is the float64 arithmetic of
+    the assignment: 2 * k * R * d FLOP per question and iteration."""
+    import torch
+
+    from paper_2607_25422_amd import binding as B
+    from paper_2607_25422_amd import workloads as wls
+
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {args.workload} seed {args.seed} (regions)", file=sys.stderr,
+          flush=True)
+    batch = wls.make_batch(args.workload, args.seed, threads=16)
+    wl = batch.wl
+    db = B.to_device(batch)
+    p = db.p
+    idx, _, _ = B.prune_topk(db, want_scores=False, want_rows=False)
+    ws = torch.empty(B.workspace_bytes_regions(p, args.r_max), dtype=torch.uint8, device="cuda")
+    for _ in range(args.warmup):
+        B.region_kmeans(db, db.V, kept_idx=idx, r_max=args.r_max, n_iter=args.kmeans_iter,
+                        workspace=ws)
+    torch.cuda.synchronize()
+    n = args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(n):
+        B.region_kmeans(db, db.V, kept_idx=idx, r_max=args.r_max, n_iter=args.kmeans_iter,
+                        workspace=ws)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(n))
+    avg = sum(ms) / n
+    R = [max(1, min(int(k) // 4, args.r_max)) if k > 0 else 0 for k in batch.k]
+    flops = sum(2.0 * int(k) * r * p.d for k, r in zip(batch.k, R)) * args.kmeans_iter
+    tf = flops / (avg * 1e-3) / 1e12
+    res = {
+        "metric": "queries/sec (regions of the kept tokens, k-means) + float64 TFLOP/s vs "
+                  "MI355X fp64 peak",
+        "value": round(p.B * n / wall, 1),
+        "unit": "queries/s",
+        "n_gpus": 1, "steps": n, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall / n, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": wl.name, "B": p.B, "d": p.d,
+                   "k": int(batch.k[0]) if len(set(batch.k.tolist())) == 1 else "mixed",
+                   "r_max": args.r_max, "iterations": args.kmeans_iter, "seed": args.seed},
+        "step_gpu_ms": {"p10": round(ms[n // 10], 5), "p50": round(ms[n // 2], 5),
+                        "p90": round(ms[min(n - 1, 9 * n // 10)], 5)},
+        "roofline": {"kernel": "region_step_kernel (over the whole call)", "bound": "alu",
+                     "achieved": round(tf, 2), "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / FP64_PEAK_TFLOPS, 4), "traffic": None,
+                     "algorithmic_gflop": round(flops / 1e9, 3), "avg_ms": round(avg, 5)},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -298,6 +366,9 @@ def main():
         return
     if args.gate:
         bench_gated_route(args)
+        return
+    if args.regions:
+        bench_regions(args)
         return
 
     import numpy as np

@@ -23,6 +23,7 @@ namespace skip {
 
 constexpr int kRegCols = 256;     // columns per slice = threads per workgroup
 constexpr int kRegMax = 16;       // largest r_max
+constexpr int kRegMaxRows = 16384; // largest k_max
 
 namespace {
 
@@ -71,6 +72,7 @@ struct RegionArgs {
   double* P;                   // [B][S][k_max][r_max] partial v_i . c_r
   double* CN;                  // [B][S][r_max]       partial |c_r|^2
   uint8_t* asg;                // [total_kept]        current assignment
+  int32_t* perm;               // [total_kept]        row ids sorted by region (stable)
   int32_t* sizes;              // [B][r_max]          rows per region
   int32_t* done;               // [B]                 finished slices
   int32_t* region_out;         // [total_kept]
@@ -78,12 +80,44 @@ struct RegionArgs {
   int32_t* sizes_out;          // [B][r_max] or NULL
 };
 
-template <typename T>
+// 8 consecutive elements of a row (16-byte aligned for bf16, 32 for f32) as
+// raw words, converted when used
+template <typename T> struct RegChunk;
+template <> struct RegChunk<bf16_t> {
+  u32x4 w;
+  __device__ __forceinline__ void load(const bf16_t* p) { w = *reinterpret_cast<const u32x4*>(p); }
+  __device__ __forceinline__ double at(int e) const {
+    const uint32_t x = w[e >> 1];
+    return (double)__uint_as_float((e & 1) ? (x & 0xffff0000u) : (x << 16));
+  }
+};
+template <> struct RegChunk<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ double at(int e) const {
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    return (double)v[e];
+  }
+};
+
+constexpr int kRegRowBatch = 32;   // rows whose loads are issued together (update)
+// columns of a row slice loaded at once (dots): the whole bf16 slice, half of
+// an f32 one
+template <typename T> struct RegLoadCols { static constexpr int n = 128; };
+template <> struct RegLoadCols<bf16_t> { static constexpr int n = 256; };
+constexpr int kRegPairs = 4;       // (row, region) sums per thread at once (assignment)
+
+template <typename T, bool IDX>
 __global__ void __launch_bounds__(kRegCols)
 region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
-  __shared__ double cs[kRegMax][kRegCols];
+  __shared__ double cs[kRegMax][kRegCols];      // this step's centroids, this slice
+  __shared__ double dl[kRegCols * kRegMax];     // distances of a block of rows (last slice)
   __shared__ int last;
   __shared__ int cnt[kRegMax];
+  __shared__ uint8_t asl[kRegMaxRows];          // the question's assignment (last slice)
   const int s = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   int k0, k1;
   range_of(a.kept_offsets, b, a.total_kept, k0, k1);
@@ -92,13 +126,12 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   const int c0 = s * kRegCols, c = c0 + tid;
   const int ncol = min(kRegCols, a.d - c0);
   const bool cok = tid < ncol;
-  auto row_of = [&](int i) -> const T* {
-    if (a.kept_idx) {
-      const int src = clampi(a.kept_idx[k0 + i], 0, a.N - 1);
-      return rows + ((size_t)b * a.N + src) * a.d;
-    }
-    return rows + (size_t)(k0 + i) * a.d;
+  // row i of the question: V[b][kept_idx[k0+i]] (IDX) or rows[k0+i]
+  auto row_id = [&](int i) -> size_t {
+    if (IDX) return (size_t)b * a.N + clampi(a.kept_idx[k0 + i], 0, a.N - 1);
+    return (size_t)(k0 + i);
   };
+  auto row_of = [&](int i) -> const T* { return rows + row_id(i) * a.d; };
   const bool final_step = a.t == a.n_iter;
 
   if (R == 0) {
@@ -110,7 +143,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     return;
   }
 
-  // ---- centroids of this step, this slice's columns
+  // ---- centroids of this step, this slice's columns (thread = column)
   if (a.t == 0) {
 #pragma unroll
     for (int r = 0; r < kRegMax; ++r) {
@@ -119,25 +152,52 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       cs[r][tid] = cok ? reg_load1<T>(row_of(pos) + c) : 0.0;
     }
   } else {
-    double acc[kRegMax];
+    // the rows sorted by region (perm: row ids, ascending within a region)
+    // are summed in one pass: each thread keeps its column's running sum in a
+    // register and closes a region where its run ends (sizes give the runs).
+    // The row ids are staged in LDS (the distance buffer, unused here) 8192 at
+    // a time; 32 row loads are issued together, positions and columns clamped
+    // into range so that every load is unconditional.
+    for (int r = tid; r < R; r += blockDim.x) cnt[r] = a.sizes[b * a.r_max + r];
+    int* ids = reinterpret_cast<int*>(dl);
+    constexpr int kIds = (int)(sizeof(dl) / (sizeof(int)));
+    const int cc = cok ? c : c0;
+    int r = 0;
+    int end = 0;
+    double acc = 0.0;
+    auto close = [&]() {
+      const int n = cnt[r];
+      if (n > 0) {
+        cs[r][tid] = cok ? acc / (double)n : 0.0;
+      } else {
+        cs[r][tid] = cok ? a.C[((size_t)b * a.r_max + r) * a.d + c] : 0.0;
+      }
+      acc = 0.0;
+      ++r;
+      end += (r < R) ? cnt[r] : 0;
+    };
+    for (int g0 = 0; g0 < k; g0 += kIds) {
+      const int ng = min(kIds, k - g0);
+      __syncthreads();                 // the previous group's ids are consumed
+      for (int j = tid; j < ng; j += blockDim.x) ids[j] = a.perm[k0 + g0 + j];
+      __syncthreads();
+      if (g0 == 0) end = cnt[0];
+      for (int j0 = 0; j0 < ng; j0 += kRegRowBatch) {
+        double v[kRegRowBatch];
 #pragma unroll
-    for (int r = 0; r < kRegMax; ++r) acc[r] = 0.0;
-    for (int i = 0; i < k; ++i) {
-      const int ai = a.asg[k0 + i];
-      const double v = cok ? reg_load1<T>(row_of(i) + c) : 0.0;
+        for (int u = 0; u < kRegRowBatch; ++u)
+          v[u] = reg_load1<T>(rows + (size_t)ids[min(j0 + u, ng - 1)] * a.d + cc);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int r = 0; r < kRegMax; ++r) {
-        if (r >= R) break;
-        acc[r] += (r == ai) ? v : 0.0;
+        for (int u = 0; u < kRegRowBatch; ++u) {
+          if (j0 + u >= ng) break;
+          while (r < R && g0 + j0 + u == end) close();
+          acc += v[u];
+        }
       }
     }
-#pragma unroll
-    for (int r = 0; r < kRegMax; ++r) {
-      if (r >= R) break;
-      const int n = a.sizes[b * a.r_max + r];
-      const double old = cok ? a.C[((size_t)b * a.r_max + r) * a.d + c] : 0.0;
-      cs[r][tid] = n > 0 ? acc[r] / (double)n : old;
-    }
+    while (r < R) close();
+    __syncthreads();        // cnt and the distance buffer are reused below
   }
   if (!final_step && cok) {
     for (int r = 0; r < R; ++r) a.C[((size_t)b * a.r_max + r) * a.d + c] = cs[r][tid];
@@ -156,21 +216,29 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     return;
   }
 
-  // ---- partial products over this slice: row i per thread, centroids from LDS
+  // ---- partial products over this slice: thread = row; each 128-column half
+  // of the row's slice is loaded whole before its products
   double* P = a.P + ((size_t)b * a.S + s) * a.k_max * a.r_max;
   for (int i = tid; i < k; i += blockDim.x) {
     const T* v = row_of(i) + c0;
     double dot[kRegMax];
 #pragma unroll
     for (int r = 0; r < kRegMax; ++r) dot[r] = 0.0;
-    for (int j = 0; j < ncol; j += 8) {         // d is a multiple of 8
-      double x[8];
-      reg_load8<T>(v + j, x);
+    constexpr int kHalf = RegLoadCols<T>::n;
+    for (int h0 = 0; h0 < ncol; h0 += kHalf) {
+      RegChunk<T> ch[kHalf / 8];
 #pragma unroll
-      for (int r = 0; r < kRegMax; ++r) {
-        if (r >= R) break;
+      for (int q = 0; q < kHalf / 8; ++q)             // ncol is a multiple of 8
+        ch[q].load(v + min(h0 + 8 * q, ncol - 8));   // past the end: a repeat, unused
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dot[r] = fma(x[e], cs[r][j + e], dot[r]);
+      for (int q = 0; q < kHalf / 8; ++q) {
+        if (h0 + 8 * q >= ncol) break;
+#pragma unroll
+        for (int r = 0; r < kRegMax; ++r) {
+          if (r >= R) break;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) dot[r] = fma(ch[q].at(e), cs[r][h0 + 8 * q + e], dot[r]);
+        }
       }
     }
 #pragma unroll
@@ -199,36 +267,101 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   __syncthreads();
   if (!last) return;
 
-  // ---- the question's last slice: assignment for the next step
+  // ---- the question's last slice: assignment for the next step.  Rows in
+  // blocks of 256: the (row, region) sums over the slices, four pairs and
+  // eight slices of loads in flight per thread, in slice order; then one row
+  // per thread takes its argmin.
   __threadfence();
   const double* Pb = a.P + (size_t)b * a.S * a.k_max * a.r_max;
   const double* CNb = a.CN + (size_t)b * a.S * a.r_max;
-  double cn[kRegMax];
-#pragma unroll
-  for (int r = 0; r < kRegMax; ++r) {
-    cn[r] = 0.0;
-    if (r < R)
-      for (int z = 0; z < a.S; ++z) cn[r] += CNb[z * a.r_max + r];
+  __shared__ double cn[kRegMax];
+  if (tid < R) {
+    double q = 0.0;
+    for (int z = 0; z < a.S; ++z) q += CNb[z * a.r_max + tid];
+    cn[tid] = q;
   }
-  for (int i = tid; i < k; i += blockDim.x) {
-    int best = 0;
-    double bd = 0.0;
+  __syncthreads();
+  const size_t zs = (size_t)a.k_max * a.r_max;      // one slice's partials
+  for (int i0 = 0; i0 < k; i0 += kRegCols) {
+    const int rows_here = min(kRegCols, k - i0);
+    const int npair = rows_here * a.r_max;
+    for (int f0 = tid; f0 < npair; f0 += kRegPairs * kRegCols) {
+      double acc[kRegPairs];
+      size_t off[kRegPairs];
+      bool on[kRegPairs];
+#pragma unroll
+      for (int j = 0; j < kRegPairs; ++j) {
+        const int f = f0 + j * kRegCols;
+        on[j] = f < npair && (f % a.r_max) < R;
+        off[j] = on[j] ? (size_t)i0 * a.r_max + f : 0;   // a valid slot when unused
+        acc[j] = 0.0;
+      }
+      int z = 0;
+      for (; z + 8 <= a.S; z += 8) {
+        double x[8][kRegPairs];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int j = 0; j < kRegPairs; ++j) x[u][j] = Pb[(size_t)(z + u) * zs + off[j]];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int j = 0; j < kRegPairs; ++j) acc[j] += x[u][j];
+      }
+      for (; z < a.S; ++z)
+#pragma unroll
+        for (int j = 0; j < kRegPairs; ++j) acc[j] += Pb[(size_t)z * zs + off[j]];
+#pragma unroll
+      for (int j = 0; j < kRegPairs; ++j) {
+        const int f = f0 + j * kRegCols;
+        if (on[j]) dl[f] = cn[f % a.r_max] - 2.0 * acc[j];
+      }
+    }
+    __syncthreads();
+    if (tid < rows_here) {
+      const int i = i0 + tid;
+      int best = 0;
+      double bd = dl[tid * a.r_max];
+      for (int r = 1; r < R; ++r) {
+        const double dist = dl[tid * a.r_max + r];
+        if (dist < bd) {
+          bd = dist;
+          best = r;
+        }
+      }
+      a.asg[k0 + i] = (uint8_t)best;
+      asl[i] = (uint8_t)best;
+      atomicAdd(&cnt[best], 1);
+    }
+    __syncthreads();
+  }
+  if (tid < R) a.sizes[b * a.r_max + tid] = cnt[tid];
+  // row ids sorted by region, ascending within a region: region r starts at
+  // the sizes of the smaller regions; a block scan per region and block of
+  // 256 rows places each row after the earlier rows of its region
+  __shared__ uint32_t scan_sh[kRegCols / 64 + 1];
+  int base[kRegMax];                           // next slot of each region (same in every thread)
+  {
+    int o = 0;
+#pragma unroll
+    for (int r = 0; r < kRegMax; ++r) {
+      base[r] = o;
+      if (r < R) o += cnt[r];
+    }
+  }
+  for (int i0 = 0; i0 < k; i0 += kRegCols) {
+    const int i = i0 + tid;
+    const int ai = i < k ? (int)asl[i] : -1;
+    const int id = i < k ? (int)row_id(i) : 0;
 #pragma unroll
     for (int r = 0; r < kRegMax; ++r) {
       if (r >= R) break;
-      double dot = 0.0;
-      for (int z = 0; z < a.S; ++z) dot += Pb[((size_t)z * a.k_max + i) * a.r_max + r];
-      const double dist = cn[r] - 2.0 * dot;
-      if (r == 0 || dist < bd) {
-        bd = dist;
-        best = r;
-      }
+      uint32_t tot;
+      const uint32_t pos = block_exclusive_scan(ai == r ? 1u : 0u, scan_sh, &tot);
+      if (ai == r) a.perm[k0 + base[r] + (int)pos] = id;
+      base[r] += (int)tot;
     }
-    a.asg[k0 + i] = (uint8_t)best;
-    atomicAdd(&cnt[best], 1);
   }
-  __syncthreads();
-  if (tid < R) a.sizes[b * a.r_max + tid] = cnt[tid];
   if (tid == 0) a.done[b] = 0;
 }
 
@@ -242,6 +375,7 @@ size_t region_scratch_bytes(const skip_problem_t& p, int r_max) {
          ralign((size_t)p.B * S * p.k_max * r_max * sizeof(double)) +
          ralign((size_t)p.B * S * r_max * sizeof(double)) +
          ralign((size_t)p.total_kept) +
+         ralign((size_t)p.total_kept * sizeof(int32_t)) +
          ralign((size_t)p.B * r_max * sizeof(int32_t)) +
          ralign((size_t)p.B * sizeof(int32_t));
 }
@@ -270,6 +404,8 @@ hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32
   c += ralign((size_t)p.B * S * r_max * sizeof(double));
   a.asg = reinterpret_cast<uint8_t*>(c);
   c += ralign((size_t)p.total_kept);
+  a.perm = reinterpret_cast<int32_t*>(c);
+  c += ralign((size_t)p.total_kept * sizeof(int32_t));
   a.sizes = reinterpret_cast<int32_t*>(c);
   c += ralign((size_t)p.B * r_max * sizeof(int32_t));
   a.done = reinterpret_cast<int32_t*>(c);
@@ -277,14 +413,25 @@ hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32
   a.cent_out = centroids;
   a.sizes_out = sizes;
   hipLaunchKernelGGL(region_clear_kernel, dim3(1), dim3(256), 0, s, a.done, p.B);
+  const bool idx = kept_idx != nullptr;
   for (int t = 0; t <= n_iter; ++t) {
     a.t = t;
-    if (p.dtype == SKIP_F32)
-      hipLaunchKernelGGL(region_step_kernel<float>, dim3(S, p.B), dim3(kRegCols), 0, s,
-                         (const float*)rows, a);
-    else
-      hipLaunchKernelGGL(region_step_kernel<bf16_t>, dim3(S, p.B), dim3(kRegCols), 0, s,
-                         (const bf16_t*)rows, a);
+    const dim3 grid(S, p.B), block(kRegCols);
+    if (p.dtype == SKIP_F32) {
+      if (idx)
+        hipLaunchKernelGGL((region_step_kernel<float, true>), grid, block, 0, s,
+                           (const float*)rows, a);
+      else
+        hipLaunchKernelGGL((region_step_kernel<float, false>), grid, block, 0, s,
+                           (const float*)rows, a);
+    } else {
+      if (idx)
+        hipLaunchKernelGGL((region_step_kernel<bf16_t, true>), grid, block, 0, s,
+                           (const bf16_t*)rows, a);
+      else
+        hipLaunchKernelGGL((region_step_kernel<bf16_t, false>), grid, block, 0, s,
+                           (const bf16_t*)rows, a);
+    }
   }
   return hipGetLastError();
 }
