@@ -141,6 +141,18 @@ def gather_rows(V: np.ndarray, idx: np.ndarray) -> np.ndarray:
     return np.asarray(V)[np.asarray(idx, dtype=np.int64)]
 
 
+def project_rows(X: np.ndarray, W: np.ndarray) -> np.ndarray:
+    """Learned projection of rows, y_i = W x_i (eq. bsca applies W_v to a
+    kept token and W_k to a chunk before their inner product; Def. B.3 names
+    them h_v and h_k; the attention query is W_Q v).  X: [n, d], W: [d_out,
+    d] -> [n, d_out], float64."""
+    X = np.asarray(X, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    if X.shape[1] != W.shape[1]:
+        raise ValueError("W must be [d_out, d]")
+    return X @ W.T
+
+
 # --------------------------------------------------------------------------
 # Regions of the kept tokens (Sec. 3.4, region-conditional retrieval)
 # --------------------------------------------------------------------------
@@ -522,10 +534,14 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
                     passage_key_table=None, adjacency: Optional[List[np.ndarray]] = None,
                     attn_rows: Optional[dict] = None, edge_rule: str = "question",
                     edge_metric: str = "cosine", edge_beta: float = 0.1,
-                    passage_keep: Optional[np.ndarray] = None):
+                    passage_keep: Optional[np.ndarray] = None,
+                    edge_rows=None):
     """Graph + attention on caller-given kept-row queries Qh [sum k, H, d_h].
     ``adjacency`` (per question [k_b, P_b] bool) replaces the cosine rule
-    when the caller brings its own graph.  Returns (cos, adj, O, LSE) lists."""
+    when the caller brings its own graph.  ``edge_rows`` [sum k, D] (for
+    instance W_v v_i, eq. bsca) are the rows the edge compatibilities are
+    taken on when they differ from the queries (then the passage keys must
+    be given in the same space).  Returns (cos, adj, O, LSE) lists."""
     pk = None if passage_key_table is None else _f64(passage_key_table)
     B = len(kept_offsets) - 1
     H, d_h = Qh.shape[1], Qh.shape[2]
@@ -539,13 +555,14 @@ def bipartite_xattn(Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages,
         ranges = [(int(passage_offsets[j]) - t0, int(passage_offsets[j + 1]) - t0)
                   for j in range(p0, p1)]
         Q = _f64(Qh[r0:r1])
+        Erows = Q.reshape(k, H * d_h) if edge_rows is None else _f64(edge_rows[r0:r1])
         Kq, Vq = _f64(Kh[t0:t1]), _f64(Vh[t0:t1])
         if adjacency is not None:
             c = None
             adj = np.asarray(adjacency[b], dtype=bool)
         elif p1 > p0:
             Kbar = pk[p0:p1] if pk is not None else passage_keys(Kq, ranges)
-            c = compatibility(Q.reshape(k, H * d_h), Kbar, edge_metric)
+            c = compatibility(Erows, Kbar, edge_metric)
             adj = bsca_edges(c, avg_degree, edge_rule, edge_beta,
                              None if passage_keep is None else passage_keep[p0:p1])
         else:

@@ -726,3 +726,64 @@ def test_region_kmeans_lloyd_properties():
     for r in range(6):
         if sizes[r]:
             np.testing.assert_allclose(C[r], X[a == r].mean(axis=0), rtol=1e-12)
+
+
+# ---------------------------------------------------------------- learned projections
+
+def test_project_rows_worked_example_and_special_matrices():
+    X = np.array([[1.0, 2.0, 3.0], [-1.0, 0.5, 4.0]])
+    W = np.array([[1.0, 0.0, -1.0], [2.0, 1.0, 0.0]])
+    # by hand: row 0 -> (1 - 3, 2 + 2) = (-2, 4); row 1 -> (-1 - 4, -2 + 0.5)
+    np.testing.assert_array_equal(orc.project_rows(X, W), [[-2.0, 4.0], [-5.0, -1.5]])
+    rng = np.random.default_rng(1)
+    Y = rng.standard_normal((5, 7))
+    np.testing.assert_array_equal(orc.project_rows(Y, np.eye(7)), Y)
+    perm = rng.permutation(7)
+    np.testing.assert_array_equal(orc.project_rows(Y, np.eye(7)[perm]), Y[:, perm])
+    with pytest.raises(ValueError):
+        orc.project_rows(Y, np.eye(6))
+
+
+def test_edge_rows_under_an_orthogonal_projection_keep_the_graph():
+    """Cosines are invariant under an orthogonal map, so projecting the edge
+    rows and the passage keys by the same orthogonal W leaves every edge
+    where it was; attention (on the unprojected queries) is unchanged."""
+    b = wls.make_batch("mixed_bf16", 21, B=3, N=200, H=4, d_h=16, T=(2,), k=(6, 20),
+                       P=(2, 5), L_p=(3, 9))
+    Qh = np.concatenate([b.V[q, :int(b.k[q])].double().numpy() for q in range(b.B)])
+    Qh = Qh.reshape(-1, 4, 16)
+    keys = []
+    for j in range(int(b.P.sum())):
+        a, e = int(b.passage_offsets[j]), int(b.passage_offsets[j + 1])
+        keys.append(b.Kh[a:e].double().numpy().reshape(e - a, -1).mean(axis=0))
+    keys = np.stack(keys)
+    Wo, _ = np.linalg.qr(np.random.default_rng(21).standard_normal((64, 64)))
+    args = (Qh, b.kept_offsets, b.Kh, b.Vh, b.passage_offsets, b.query_passages, 0.25, 2.0)
+    _, adj0, O0, L0 = orc.bipartite_xattn(*args, passage_key_table=keys)
+    _, adj1, O1, L1 = orc.bipartite_xattn(*args, passage_key_table=orc.project_rows(keys, Wo),
+                                          edge_rows=orc.project_rows(Qh.reshape(-1, 64), Wo))
+    for q in range(b.B):
+        assert np.array_equal(adj0[q], adj1[q])
+        np.testing.assert_array_equal(O0[q], O1[q])
+
+
+def test_edge_rows_decide_the_edges():
+    """Edge rows equal to one passage key each: under the per-row cut with one
+    edge a row, row i's only edge is the passage its edge row copies."""
+    b = wls.make_batch("mixed_bf16", 22, B=2, N=120, H=4, d_h=16, T=(2,), k=(9,),
+                       P=(3,), L_p=(4,))
+    rng = np.random.default_rng(22)
+    keys = rng.standard_normal((int(b.P.sum()), 64))
+    Qh = rng.standard_normal((int(b.k.sum()), 4, 16))
+    want, rows = [], []
+    for q in range(b.B):
+        p0 = int(b.query_passages[q])
+        for i in range(int(b.k[q])):
+            j = (5 * i + q) % 3
+            want.append((q, i, j))
+            rows.append(keys[p0 + j] * (1.0 + i))      # a positive multiple: cosine 1
+    _, adj, _, _ = orc.bipartite_xattn(Qh, b.kept_offsets, b.Kh, b.Vh, b.passage_offsets,
+                                       b.query_passages, 0.25, 1.0, passage_key_table=keys,
+                                       edge_rule="row", edge_rows=np.stack(rows))
+    for q, i, j in want:
+        assert adj[q][i].tolist() == [jj == j for jj in range(3)]
