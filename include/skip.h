@@ -282,6 +282,27 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
                             size_t workspace_bytes, void* stream);
 
 /*
+ * Learned projection of the kept rows (eq. bsca applies W_v to a kept token
+ * and W_k to a chunk before their inner product; Def. B.3 calls them h_v and
+ * h_k; the attention query is W_Q v): Y[r] = W x_r for every kept row x_r,
+ * gathered as it is read.  bf16 rows and weights, float32 sums on the matrix
+ * cores; Y stored as bf16 (round to nearest even) or float.
+ *   rows     kept_idx NULL: the kept rows [total_kept][d]; else V [B][N][d],
+ *            row r of question b being V[b][kept_idx[r]]
+ *   W        [d_out][d] bf16, 16-byte aligned
+ *   d_out    a multiple of 256, at most 65536;  d a multiple of 32
+ *   Y        out [total_kept][d_out], bf16 (out_f32 = 0) or float (1)
+ * bf16 problems only (SKIP_ERR_UNSUPPORTED otherwise).  The workspace holds
+ * W repacked for the matrix cores: skip_workspace_bytes_project.
+ */
+skip_status_t skip_workspace_bytes_project(const skip_problem_t* p, int32_t d_out,
+                                           size_t* bytes);
+skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
+                                  const int32_t* kept_offsets, const int32_t* kept_idx,
+                                  const void* W, int32_t d_out, void* Y, int32_t out_f32,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Regions of the kept tokens (Sec. 3.4: the approximate k-means with which
  * region-conditional retrieval groups the kept tokens before issuing one
  * retrieval query per region centroid; the retrieval is not part of this
@@ -295,7 +316,7 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
  *   rows      kept_idx NULL: the kept rows, [total_kept][d] (as written by
  *             skip_prune_topk); else V [B][N][d], row r of question b being
  *             V[b][kept_idx[r]] (as in the fused route)
- *   r_max     1..16 (paper: 8);  n_iter  1..1000
+ *   r_max     1..16 (paper: 8);  n_iter  1..1000;  k_max at most 16384
  *   region    out [total_kept] int32: the region of each kept row after the
  *             last iteration
  *   centroids out [B][r_max][d] float: the centroids after the last
@@ -365,6 +386,30 @@ skip_status_t skip_bipartite_xattn_masked(const skip_problem_t* p, const void* Q
                                           float* lse, int32_t* edge_rowptr_out,
                                           int32_t* edge_col_out, void* workspace,
                                           size_t workspace_bytes, void* stream);
+
+/*
+ * skip_bipartite_xattn with the graph cut on separate edge rows (eq. bsca:
+ * the compatibility of W_v v_i and W_k k_j, while the attention queries are
+ * W_Q v_i): the compatibilities are taken between edge_rows and the given
+ * passage keys, attention runs on Qh.
+ *   edge_rows     [total_kept][d] in the problem's element type (e.g. the
+ *                 output of skip_gather_project with W_v)
+ *   passage_keys  [total_passages][d] float, required (the keys in the same
+ *                 space, e.g. W_k applied to the pooled keys)
+ *   passage_keep  NULL or a gate's mask as in skip_bipartite_xattn_masked
+ * The graph is built here.  Other arguments and results as in
+ * skip_bipartite_xattn.
+ */
+skip_status_t skip_bipartite_xattn_proj(const skip_problem_t* p, const void* Qh,
+                                        const void* edge_rows, const int32_t* kept_offsets,
+                                        const void* Kh, const void* Vh,
+                                        const int32_t* passage_offsets,
+                                        const int32_t* query_passages,
+                                        const float* passage_keys,
+                                        const uint8_t* passage_keep, void* O, float* lse,
+                                        int32_t* edge_rowptr_out, int32_t* edge_col_out,
+                                        void* workspace, size_t workspace_bytes,
+                                        void* stream);
 
 /*
  * Both stages fused (Alg. 1: scoring, TopK, graph, fuse): the kept visual

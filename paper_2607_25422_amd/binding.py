@@ -31,7 +31,9 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_route_fused_profiled", "skip_workspace_bytes_mlp",
                 "skip_prune_topk_mlp", "skip_workspace_bytes_gate", "skip_skv_gate",
                 "skip_bipartite_xattn_masked", "skip_route_fused_gated",
-                "skip_workspace_bytes_regions", "skip_region_kmeans")
+                "skip_workspace_bytes_regions", "skip_region_kmeans",
+                "skip_workspace_bytes_project", "skip_gather_project",
+                "skip_bipartite_xattn_proj")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -126,6 +128,15 @@ def _load() -> ctypes.CDLL:
     lib.skip_region_kmeans.restype = ctypes.c_int
     lib.skip_region_kmeans.argtypes = [P, vp, i32p, i32p, ctypes.c_int32, ctypes.c_int32, i32p,
                                        vp, i32p, vp, ctypes.c_size_t, vp]
+    lib.skip_workspace_bytes_project.restype = ctypes.c_int
+    lib.skip_workspace_bytes_project.argtypes = [P, ctypes.c_int32,
+                                                 ctypes.POINTER(ctypes.c_size_t)]
+    lib.skip_gather_project.restype = ctypes.c_int
+    lib.skip_gather_project.argtypes = [P, vp, i32p, i32p, vp, ctypes.c_int32, vp,
+                                        ctypes.c_int32, vp, ctypes.c_size_t, vp]
+    lib.skip_bipartite_xattn_proj.restype = ctypes.c_int
+    lib.skip_bipartite_xattn_proj.argtypes = [P, vp, vp, i32p, vp, vp, i32p, i32p, vp, vp, vp,
+                                              vp, i32p, i32p, vp, ctypes.c_size_t, vp]
     lib.skip_route_fused_profiled.restype = ctypes.c_int
     lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                               vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
@@ -221,6 +232,13 @@ def workspace_bytes_regions(p: SkipProblem, r_max: int) -> int:
     n = ctypes.c_size_t(0)
     _check(LIB.skip_workspace_bytes_regions(ctypes.byref(p), int(r_max), ctypes.byref(n)),
            "skip_workspace_bytes_regions")
+    return int(n.value)
+
+
+def workspace_bytes_project(p: SkipProblem, d_out: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.skip_workspace_bytes_project(ctypes.byref(p), int(d_out), ctypes.byref(n)),
+           "skip_workspace_bytes_project")
     return int(n.value)
 
 
@@ -419,6 +437,46 @@ def skip_region_kmeans(p: SkipProblem, rows, kept_offsets, kept_idx, r_max, n_it
         _ptr(sizes, "sizes", torch.int32, p.B * r_max), workspace.data_ptr(), workspace.numel(),
         _stream(stream))
     _check(st, "skip_region_kmeans")
+
+
+def skip_gather_project(p: SkipProblem, rows, kept_offsets, kept_idx, W, Y, out_f32=False,
+                        workspace=None, stream=None):
+    et = _elem_dtype(p)
+    d_out = int(W.shape[0])
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes_project(p, d_out), dtype=torch.uint8,
+                                device=W.device)
+    n_rows = p.B * p.N if kept_idx is not None else p.total_kept
+    st = LIB.skip_gather_project(
+        ctypes.byref(p), _ptr(rows, "rows", et, n_rows * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept), _ptr(W, "W", et, d_out * p.d),
+        d_out, _ptr(Y, "Y", torch.float32 if out_f32 else et, p.total_kept * d_out),
+        1 if out_f32 else 0, workspace.data_ptr(), workspace.numel(), _stream(stream))
+    _check(st, "skip_gather_project")
+
+
+def skip_bipartite_xattn_proj(p: SkipProblem, Qh, edge_rows, kept_offsets, Kh, Vh,
+                              passage_offsets, query_passages, passage_keys, O, lse=None,
+                              passage_keep=None, edge_rowptr_out=None, edge_col_out=None,
+                              workspace=None, stream=None):
+    et = _elem_dtype(p)
+    ws, wsp, wsn = _ws(p, workspace)
+    st = LIB.skip_bipartite_xattn_proj(
+        ctypes.byref(p), _ptr(Qh, "Qh", et, p.total_kept * p.d),
+        _ptr(edge_rows, "edge_rows", et, p.total_kept * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d), _ptr(Vh, "Vh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(passage_keep, "passage_keep", torch.uint8, p.total_passages),
+        _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
+        _ptr(lse, "lse", torch.float32, p.total_kept * p.H),
+        _ptr(edge_rowptr_out, "edge_rowptr_out", torch.int32, p.total_kept + 1),
+        _ptr(edge_col_out, "edge_col_out", torch.int32, p.total_kept * p.P_max),
+        wsp, wsn, _stream(stream))
+    _check(st, "skip_bipartite_xattn_proj")
 
 
 def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
@@ -668,6 +726,38 @@ def region_kmeans(db: DeviceBatch, rows: torch.Tensor, kept_idx=None, r_max: int
     skip_region_kmeans(p, rows if p.total_kept else None, db.kept_offsets, kept_idx, r_max,
                        n_iter, region if p.total_kept else None, cent, sizes, workspace)
     return region[:p.total_kept], cent, sizes
+
+
+def gather_project(db: DeviceBatch, rows: torch.Tensor, W: torch.Tensor, kept_idx=None,
+                   out_f32=False, workspace=None):
+    """Y = W x_r for every kept row (``rows`` the kept rows, or db.V with
+    ``kept_idx``).  Returns Y [total_kept, d_out] (bf16, or float32)."""
+    p = db.p
+    Y = torch.empty((max(p.total_kept, 1), int(W.shape[0])),
+                    dtype=torch.float32 if out_f32 else db.V.dtype, device=db.V.device)
+    skip_gather_project(p, rows if p.total_kept else None, db.kept_offsets, kept_idx, W,
+                        Y if p.total_kept else None, out_f32, workspace)
+    return Y[:p.total_kept]
+
+
+def bipartite_xattn_proj(db: DeviceBatch, Qh: torch.Tensor, edge_rows: torch.Tensor,
+                         passage_keys: torch.Tensor, passage_keep=None, want_edges=True):
+    """Graph cut on ``edge_rows`` against ``passage_keys``, attention on Qh.
+    Returns (O, lse, rowptr, col)."""
+    p = db.p
+    dev = db.V.device
+    O = torch.empty((max(p.total_kept, 1), p.H, p.d_h), dtype=_out_dtype(p), device=dev)
+    lse = torch.empty((max(p.total_kept, 1), p.H), dtype=torch.float32, device=dev)
+    rp = col = None
+    if want_edges:
+        rp = torch.empty(p.total_kept + 1, dtype=torch.int32, device=dev)
+        col = torch.empty(max(p.total_kept * p.P_max, 1), dtype=torch.int32, device=dev)
+    skip_bipartite_xattn_proj(p, Qh if p.total_kept else None,
+                              edge_rows if p.total_kept else None, db.kept_offsets, db.Kh,
+                              db.Vh, db.passage_offsets, db.query_passages, passage_keys,
+                              O if p.total_kept else None, lse if p.total_kept else None,
+                              passage_keep, rp, col, db.workspace)
+    return O[:p.total_kept], lse[:p.total_kept], rp, col
 
 
 def route_fused(db: DeviceBatch, passage_keys=None, out=None, stage_events=None):

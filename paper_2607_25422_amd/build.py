@@ -24,7 +24,7 @@ LIB = os.path.join(LIBDIR, "libskip.so")
 BUILD = os.path.join(ROOT, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["skip_api.hip", "prune.hip", "graph.hip", "attn.hip", "mlp.hip", "gate.hip", "regions.hip"]
+SOURCES = ["skip_api.hip", "prune.hip", "graph.hip", "attn.hip", "mlp.hip", "gate.hip", "regions.hip", "proj.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

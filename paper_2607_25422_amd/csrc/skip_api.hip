@@ -210,7 +210,7 @@ skip_status_t skip_prune_topk_mlp(const skip_problem_t* p, const skip_qvs_mlp_t*
   return SKIP_OK;
 }
 
-static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh,
+static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh, const void* edge_rows,
                                 const int32_t* kept_offsets, const void* Kh, const void* Vh,
                                 const int32_t* passage_offsets, const int32_t* query_passages,
                                 const float* passage_keys, const int32_t* edge_rowptr,
@@ -244,7 +244,8 @@ static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh,
                                 w.rowmask, s));
   } else {
     if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-    SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys, ep, s));
+    const QuerySource e{edge_rows ? edge_rows : Qh, nullptr, 0};
+    SKIP_TRY(launch_edge_dot(*p, e, kept_offsets, query_passages, w.kbar, passage_keys, ep, s));
     SKIP_TRY(launch_edge_select(*p, ep, kept_offsets, query_passages, w.rowmask,
                                 edge_rowptr_out, edge_col_out, s, passage_keep));
   }
@@ -261,9 +262,9 @@ skip_status_t skip_bipartite_xattn(const skip_problem_t* p, const void* Qh,
                                    void* O, float* lse, int32_t* edge_rowptr_out,
                                    int32_t* edge_col_out, void* workspace,
                                    size_t workspace_bytes, void* stream) {
-  return xattn_impl(p, Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages, passage_keys,
-                    edge_rowptr, edge_col, nullptr, O, lse, edge_rowptr_out, edge_col_out,
-                    workspace, workspace_bytes, stream);
+  return xattn_impl(p, Qh, nullptr, kept_offsets, Kh, Vh, passage_offsets, query_passages,
+                    passage_keys, edge_rowptr, edge_col, nullptr, O, lse, edge_rowptr_out,
+                    edge_col_out, workspace, workspace_bytes, stream);
 }
 
 skip_status_t skip_bipartite_xattn_masked(const skip_problem_t* p, const void* Qh,
@@ -276,9 +277,62 @@ skip_status_t skip_bipartite_xattn_masked(const skip_problem_t* p, const void* Q
                                           void* workspace, size_t workspace_bytes,
                                           void* stream) {
   if (!passage_keep && p && p->total_passages > 0) return SKIP_ERR_INVALID_ARG;
-  return xattn_impl(p, Qh, kept_offsets, Kh, Vh, passage_offsets, query_passages, passage_keys,
-                    nullptr, nullptr, passage_keep, O, lse, edge_rowptr_out, edge_col_out,
-                    workspace, workspace_bytes, stream);
+  return xattn_impl(p, Qh, nullptr, kept_offsets, Kh, Vh, passage_offsets, query_passages,
+                    passage_keys, nullptr, nullptr, passage_keep, O, lse, edge_rowptr_out,
+                    edge_col_out, workspace, workspace_bytes, stream);
+}
+
+skip_status_t skip_bipartite_xattn_proj(const skip_problem_t* p, const void* Qh,
+                                        const void* edge_rows, const int32_t* kept_offsets,
+                                        const void* Kh, const void* Vh,
+                                        const int32_t* passage_offsets,
+                                        const int32_t* query_passages,
+                                        const float* passage_keys,
+                                        const uint8_t* passage_keep, void* O, float* lse,
+                                        int32_t* edge_rowptr_out, int32_t* edge_col_out,
+                                        void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+  if (!p) return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && !edge_rows) return SKIP_ERR_INVALID_ARG;
+  if (p->total_passages > 0 && !passage_keys) return SKIP_ERR_INVALID_ARG;
+  return xattn_impl(p, Qh, edge_rows, kept_offsets, Kh, Vh, passage_offsets, query_passages,
+                    passage_keys, nullptr, nullptr, passage_keep, O, lse, edge_rowptr_out,
+                    edge_col_out, workspace, workspace_bytes, stream);
+}
+
+skip_status_t skip_workspace_bytes_project(const skip_problem_t* p, int32_t d_out,
+                                           size_t* bytes) {
+  if (!bytes) return SKIP_ERR_INVALID_ARG;
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (d_out <= 0) return SKIP_ERR_INVALID_ARG;
+  if (d_out % 256 != 0 || d_out > 65536) return SKIP_ERR_UNSUPPORTED;
+  *bytes = proj_scratch_bytes(p->d, d_out);
+  return SKIP_OK;
+}
+
+skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
+                                  const int32_t* kept_offsets, const int32_t* kept_idx,
+                                  const void* W, int32_t d_out, void* Y, int32_t out_f32,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (!W || !workspace || (out_f32 != 0 && out_f32 != 1) || d_out <= 0)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && (!rows || !Y)) return SKIP_ERR_INVALID_ARG;
+  if (kept_idx && !kept_offsets) return SKIP_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(W) % 16 != 0 || reinterpret_cast<uintptr_t>(rows) % 16 != 0)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || d_out % 256 != 0 || d_out > 65536)
+    return SKIP_ERR_UNSUPPORTED;
+  if (kept_idx) {
+    if (p->N < 1 || p->k_max > p->N) return SKIP_ERR_INVALID_ARG;
+    if ((int64_t)p->B * p->N > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
+  }
+  if (workspace_bytes < proj_scratch_bytes(p->d, d_out)) return SKIP_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SKIP_TRY(launch_project(*p, rows, kept_offsets, kept_idx, W, d_out, Y, out_f32, workspace, s));
+  return SKIP_OK;
 }
 
 static_assert(sizeof(skip_skv_gate_t) == 56 && offsetof(skip_skv_gate_t, b2) == 32 &&

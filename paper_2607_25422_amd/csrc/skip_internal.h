@@ -73,6 +73,12 @@ hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const
                        const float* passage_keys, const int32_t* query_passages,
                        GateScratch g, float* logits, uint8_t* keep, hipStream_t s);
 
+// Learned projection of the kept rows --------------------------------------
+size_t proj_scratch_bytes(int d, int d_out);
+hipError_t launch_project(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
+                          const int32_t* kept_idx, const void* W, int d_out, void* Y,
+                          int out_f32, void* scratch, hipStream_t s);
+
 // Regions of the kept tokens (k-means) ------------------------------------
 int region_slices(const skip_problem_t& p);
 size_t region_scratch_bytes(const skip_problem_t& p, int r_max);

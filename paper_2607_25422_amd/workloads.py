@@ -372,3 +372,11 @@ def make_gate_weights(wl: Workload | str, hidden: int = 512, seed: int = 2026) -
     w2 = rng.standard_normal(hidden) / math.sqrt(hidden)
     return GateWeights(W=_round(W, "bf16"), b1=torch.from_numpy(b1.astype(np.float32)),
                        w2=torch.from_numpy(w2.astype(np.float32)), b2=0.0)
+
+
+def make_projection(d_out: int, d: int, seed: int = 2026) -> torch.Tensor:
+    """A synthetic learned projection W [d_out, d] in bfloat16, N(0, 1/d)
+    entries, so that W x keeps the scale of x.  No trained projections exist
+    for this path."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, d_out, d, 31337])))
+    return _round(rng.standard_normal((d_out, d)) / math.sqrt(d), "bf16")

@@ -274,3 +274,34 @@ def test_region_kmeans_validation(b):
     q.total_kept = 1200
     assert call(q, idx=FAKE) == b.SKIP_ERR_INVALID_ARG
     assert call(p, ws_bytes=n - 1) == b.SKIP_ERR_WORKSPACE
+
+
+def test_projection_and_edge_rows_validation(b):
+    p = _problem(b)
+    n = b.workspace_bytes_project(p, 256)
+    assert n == 256 * 1024 * 2
+    with pytest.raises(b.SkipError):
+        b.workspace_bytes_project(p, 100)
+
+    def proj(q, rows=FAKE, W=FAKE, d_out=256, Y=FAKE, f32=0, idx=None, ws_bytes=1 << 30):
+        return b.LIB.skip_gather_project(ctypes.byref(q), rows, FAKE, idx, W, d_out, Y, f32,
+                                         FAKE, ws_bytes, None)
+    # every call fails validation
+    assert proj(p, rows=None) == b.SKIP_ERR_INVALID_ARG
+    assert proj(p, W=None) == b.SKIP_ERR_INVALID_ARG
+    assert proj(p, Y=None) == b.SKIP_ERR_INVALID_ARG
+    assert proj(p, f32=2) == b.SKIP_ERR_INVALID_ARG
+    assert proj(p, W=FAKE + 8) == b.SKIP_ERR_INVALID_ARG
+    assert proj(p, d_out=300) == b.SKIP_ERR_UNSUPPORTED
+    assert proj(p, d_out=0) == b.SKIP_ERR_INVALID_ARG
+    q = b.make_problem("f32", B=2, N=576, d=1024, q_offsets=[0, 3, 7], kept_offsets=[0, 96, 192])
+    assert proj(q) == b.SKIP_ERR_UNSUPPORTED
+    assert proj(p, ws_bytes=n - 1) == b.SKIP_ERR_WORKSPACE
+
+    def xp(q, edge=FAKE, keys=FAKE, ws_bytes=0):
+        return b.LIB.skip_bipartite_xattn_proj(ctypes.byref(q), FAKE, edge, FAKE, FAKE, FAKE,
+                                               FAKE, FAKE, keys, None, FAKE, None, None, None,
+                                               FAKE, ws_bytes, None)
+    assert xp(p, edge=None) == b.SKIP_ERR_INVALID_ARG
+    assert xp(p, keys=None) == b.SKIP_ERR_INVALID_ARG
+    assert xp(p) == b.SKIP_ERR_WORKSPACE
