@@ -61,6 +61,11 @@ def parse():
     ap.add_argument("--regions", action="store_true",
                     help="time the regions of the kept tokens (k-means of the kept rows, read "
                          "in place through the kept indices) instead of the fused route")
+    ap.add_argument("--project", action="store_true",
+                    help="time the learned projection of the kept rows (gathered GEMM, rows "
+                         "read in place through the kept indices) instead of the fused route")
+    ap.add_argument("--proj-out", type=int, default=0,
+                    help="output width of the projection (default: d)")
     ap.add_argument("--r-max", type=int, default=8, help="most regions per question")
     ap.add_argument("--kmeans-iter", type=int, default=10, help="Lloyd iterations")
     ap.add_argument("--gate-tau", type=float, default=0.5, help="gate threshold on nu")
@@ -294,6 +299,68 @@ def bench_gated_route(args):
 FP64_PEAK_TFLOPS = 78.6
 
 
+def bench_project(args):
+    """Learned projection Y = W x_r of every kept row (rows read in place
+    through the kept indices of a prune call made beforehand; W repacked
+    inside the call), event-timed on the launch stream: 2 * M * d * d_out
+    FLOP per call against the bf16 matrix peak."""
+    import torch
+
+    from paper_2607_25422_amd import binding as B
+    from paper_2607_25422_amd import workloads as wls
+
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {args.workload} seed {args.seed} (projection)", file=sys.stderr,
+          flush=True)
+    batch = wls.make_batch(args.workload, args.seed, threads=16)
+    wl = batch.wl
+    db = B.to_device(batch)
+    p = db.p
+    d_out = args.proj_out or p.d
+    W = wls.make_projection(d_out, p.d, args.seed).cuda()
+    idx, _, _ = B.prune_topk(db, want_scores=False, want_rows=False)
+    ws = torch.empty(B.workspace_bytes_project(p, d_out), dtype=torch.uint8, device="cuda")
+    Y = torch.empty((p.total_kept, d_out), dtype=torch.bfloat16, device="cuda")
+    run = lambda: B.skip_gather_project(p, db.V, db.kept_offsets, idx, W, Y,  # noqa: E731
+                                        workspace=ws)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    n = args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(n):
+        run()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(n))
+    avg = sum(ms) / n
+    flops = 2.0 * p.total_kept * p.d * d_out
+    tf = flops / (avg * 1e-3) / 1e12
+    res = {
+        "metric": "queries/sec (learned projection of the kept rows) + bf16 TFLOP/s vs MI355X "
+                  "bf16 MFMA peak",
+        "value": round(p.B * n / wall, 1),
+        "unit": "queries/s",
+        "n_gpus": 1, "steps": n, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall / n, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "B": p.B, "rows": p.total_kept, "d": p.d,
+                   "d_out": d_out, "seed": args.seed},
+        "step_gpu_ms": {"p10": round(ms[n // 10], 5), "p50": round(ms[n // 2], 5),
+                        "p90": round(ms[min(n - 1, 9 * n // 10)], 5)},
+        "roofline": {"kernel": "proj_gemm_kernel + proj_pack_kernel (the whole call)",
+                     "bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "algorithmic_gflop": round(flops / 1e9, 2),
+                     "avg_ms": round(avg, 5)},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def bench_regions(args):
     """Regions of the kept tokens: k-means of each question's kept rows (read
     in place through the kept indices of a prune call made beforehand),
@@ -369,6 +436,9 @@ def main():
         return
     if args.regions:
         bench_regions(args)
+        return
+    if args.project:
+        bench_project(args)
         return
 
     import numpy as np
