@@ -348,20 +348,14 @@ gate_fin_kernel(const float* __restrict__ part, int S, int T, int h,
     const double tot = (((double)wsum[0] + (double)wsum[1]) + (double)wsum[2]) +
                        (double)wsum[3] + b2;
     const float zl = (float)tot;
-    zbuf[p] = zl;
+    store_shared(&zbuf[p], zl);                   // read by the question's last block
     if (logits) logits[p] = zl;
-    __threadfence();
-    const int prev = atomicAdd(&done[b], 1);
-    last = (prev == p1 - p0 - 1) ? 1 : 0;       // every block of the question is done
   }
-  __syncthreads();
-  if (!last || wave != 0) return;
-  // wave 0 of the question's last block: every logit of the question is
-  // written; the cut is taken with wave shuffles
-  __threadfence();
+  // every block of the question done: the last one takes the cut
+  if (!finish_and_check_last(&done[b], p1 - p0, &last) || wave != 0) return;
+  // wave 0 of the question's last block: the cut with wave shuffles
   float zl = 0.f;
-  if (lane < P)
-    zl = __hip_atomic_load(&zbuf[p0 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (lane < P) zl = load_shared(&zbuf[p0 + lane]);
   const int verified = (lane < P && (double)zl >= t) ? 1 : 0;
   const int cap = (int)ceil(rho * (double)P - 1e-9);
   int rank = 0;

@@ -12,8 +12,9 @@
 //   step t (< n)    centroids from assignment t; partial products for t + 1
 //   step n          centroids from assignment n; outputs
 // In a step the slice workgroups of a question write their partial dot
-// products v_i . c_r and squared norms |c_r|^2 over their columns; the last
-// of them to finish (a counter) sums the partials in slice order and assigns
+// products v_i . c_r and squared norms |c_r|^2 over their columns (coherent
+// stores); the last of them to finish (a counter) sums the partials in slice
+// order and assigns
 // every row by argmin_r |c_r|^2 - 2 v_i . c_r, which is |v_i - c_r|^2 less the
 // row's own |v_i|^2.
 #include "skip_common.h"
@@ -244,7 +245,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 #pragma unroll
     for (int r = 0; r < kRegMax; ++r) {
       if (r >= R) break;
-      P[(size_t)i * a.r_max + r] = dot[r];
+      store_shared(&P[(size_t)i * a.r_max + r], dot[r]);   // read by the last slice
     }
   }
   if (tid < 64) {
@@ -254,30 +255,22 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       double q = 0.0;
       for (int j = tid; j < ncol; j += 64) q = fma(cs[r][j], cs[r][j], q);
       q = wave_sum_f64(q);
-      if (tid == 0) a.CN[((size_t)b * a.S + s) * a.r_max + r] = q;
+      if (tid == 0) store_shared(&a.CN[((size_t)b * a.S + s) * a.r_max + r], q);
     }
   }
-  __syncthreads();
-  if (tid == 0) {
-    __threadfence();
-    const int prev = atomicAdd(&a.done[b], 1);
-    last = (prev == a.S - 1) ? 1 : 0;
-  }
   if (tid < kRegMax) cnt[tid] = 0;
-  __syncthreads();
-  if (!last) return;
+  if (!finish_and_check_last(&a.done[b], a.S, &last)) return;
 
   // ---- the question's last slice: assignment for the next step.  Rows in
   // blocks of 256: the (row, region) sums over the slices, four pairs and
   // eight slices of loads in flight per thread, in slice order; then one row
   // per thread takes its argmin.
-  __threadfence();
   const double* Pb = a.P + (size_t)b * a.S * a.k_max * a.r_max;
   const double* CNb = a.CN + (size_t)b * a.S * a.r_max;
   __shared__ double cn[kRegMax];
   if (tid < R) {
     double q = 0.0;
-    for (int z = 0; z < a.S; ++z) q += CNb[z * a.r_max + tid];
+    for (int z = 0; z < a.S; ++z) q += load_shared(&CNb[z * a.r_max + tid]);
     cn[tid] = q;
   }
   __syncthreads();
@@ -302,7 +295,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u)
 #pragma unroll
-          for (int j = 0; j < kRegPairs; ++j) x[u][j] = Pb[(size_t)(z + u) * zs + off[j]];
+          for (int j = 0; j < kRegPairs; ++j) x[u][j] = load_shared(&Pb[(size_t)(z + u) * zs + off[j]]);
 #pragma unroll
         for (int u = 0; u < 8; ++u)
 #pragma unroll
@@ -310,7 +303,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       }
       for (; z < a.S; ++z)
 #pragma unroll
-        for (int j = 0; j < kRegPairs; ++j) acc[j] += Pb[(size_t)z * zs + off[j]];
+        for (int j = 0; j < kRegPairs; ++j) acc[j] += load_shared(&Pb[(size_t)z * zs + off[j]]);
 #pragma unroll
       for (int j = 0; j < kRegPairs; ++j) {
         const int f = f0 + j * kRegCols;

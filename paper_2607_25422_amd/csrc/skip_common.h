@@ -42,6 +42,37 @@ __device__ __forceinline__ void range_of(const int32_t* off, int i, int total,
   b = clampi(off[i + 1], a, total);
 }
 
+// Publishing data to other workgroups of the same launch (a "last workgroup
+// finishes" counter).  The L2 caches of the XCDs are not coherent with each
+// other within a kernel, and an agent-scope fence writes back and invalidates
+// the whole L2 of the XCD (costly for every other workgroup there).  Instead
+// the shared values are written and read with agent-scope atomic accesses
+// (coherent, sc1), each writer waits for its stores to be acknowledged before
+// the workgroup barrier, and one thread then bumps the counter.
+template <typename T>
+__device__ __forceinline__ void store_shared(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T load_shared(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// every vector memory access of this wave (loads and stores) has completed
+__device__ __forceinline__ void wait_all_vmem() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);            // vmcnt(0), expcnt and lgkmcnt untouched
+}
+// Called by every thread of the workgroup after its shared stores; returns
+// true in every thread of the workgroup that completes `counter` to `total`.
+__device__ __forceinline__ bool finish_and_check_last(int32_t* counter, int total, int* flag) {
+  wait_all_vmem();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *flag = (__hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             total - 1) ? 1 : 0;
+  __syncthreads();
+  return *flag != 0;
+}
+
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s, kWave);
