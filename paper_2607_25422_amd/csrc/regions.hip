@@ -74,6 +74,7 @@ struct RegionArgs {
   double* CN;                  // [B][S][r_max]       partial |c_r|^2
   uint8_t* asg;                // [total_kept]        current assignment
   int32_t* perm;               // [total_kept]        row ids sorted by region (stable)
+  uint8_t* sreg;               // [total_kept]        region of each sorted position
   int32_t* sizes;              // [B][r_max]          rows per region
   int32_t* done;               // [B]                 finished slices
   int32_t* region_out;         // [total_kept]
@@ -111,15 +112,26 @@ template <typename T> struct RegLoadCols { static constexpr int n = 128; };
 template <> struct RegLoadCols<bf16_t> { static constexpr int n = 256; };
 constexpr int kRegPairs = 4;       // (row, region) sums per thread at once (assignment)
 
-template <typename T, bool IDX>
+// RM: a compile-time bound on the regions (4, 8 or 16), so that every loop
+// over the regions unrolls and the per-region sums stay in fixed registers
+// (a run-time bound made the compiler index the register file, one
+// instruction at a time).
+template <typename T, bool IDX, int RM>
 __global__ void __launch_bounds__(kRegCols)
 region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   __shared__ double cs[kRegMax][kRegCols];      // this step's centroids, this slice
-  __shared__ double dl[kRegCols * kRegMax];     // distances of a block of rows (last slice)
+  __shared__ __align__(16) double dl[kRegCols * kRegMax];     // distances of a block of rows (last slice)
   __shared__ int last;
   __shared__ int cnt[kRegMax];
-  __shared__ uint8_t asl[kRegMaxRows];          // the question's assignment (last slice)
-  const int s = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  __shared__ __align__(16) uint8_t asl[kRegMaxRows];          // assignment (last slice) / sorted regions (update)
+  // All slices of a question run on one XCD (workgroup id L goes to XCD
+  // L % 8): its L2 then holds the question's whole kept rows across the
+  // steps.  With slices spread over the XCDs instead, every XCD would hold
+  // the same few column slices of all questions, and rows 8 KiB apart map
+  // those slices onto a small fraction of the L2 sets.
+  const int L = blockIdx.x, xcd = L & 7, jl = L >> 3;
+  const int s = jl % a.S, b = xcd + 8 * (jl / a.S), tid = threadIdx.x;
+  if (b >= a.B) return;
   int k0, k1;
   range_of(a.kept_offsets, b, a.total_kept, k0, k1);
   const int k = min(k1 - k0, a.k_max);
@@ -147,58 +159,79 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   // ---- centroids of this step, this slice's columns (thread = column)
   if (a.t == 0) {
 #pragma unroll
-    for (int r = 0; r < kRegMax; ++r) {
-      if (r >= R) break;
-      const int pos = ((2 * r + 1) * k) / (2 * R);
-      cs[r][tid] = cok ? reg_load1<T>(row_of(pos) + c) : 0.0;
+    for (int r = 0; r < RM; ++r) {
+      if (r < R) {
+        const int pos = ((2 * r + 1) * k) / (2 * R);
+        cs[r][tid] = cok ? reg_load1<T>(row_of(pos) + c) : 0.0;
+      }
     }
   } else {
-    // the rows sorted by region (perm: row ids, ascending within a region)
-    // are summed in one pass: each thread keeps its column's running sum in a
-    // register and closes a region where its run ends (sizes give the runs).
-    // The row ids are staged in LDS (the distance buffer, unused here) 8192 at
-    // a time; 32 row loads are issued together, positions and columns clamped
-    // into range so that every load is unconditional.
+    // the rows sorted by region (perm: row ids, ascending within a region;
+    // sreg: the region of each sorted position) are summed in one pass:
+    // each thread keeps its column's running sum in a register and hands it
+    // to LDS where the region changes (a uniform test).  Row ids and regions
+    // are staged in LDS 8192 at a time; 32 row loads are issued together
+    // (positions and columns clamped into range, so every load is
+    // unconditional).  Regions without rows keep their centroid.
     for (int r = tid; r < R; r += blockDim.x) cnt[r] = a.sizes[b * a.r_max + r];
     int* ids = reinterpret_cast<int*>(dl);
     constexpr int kIds = (int)(sizeof(dl) / (sizeof(int)));
     const int cc = cok ? c : c0;
-    int r = 0;
-    int end = 0;
+    int cur = -1;
     double acc = 0.0;
-    auto close = [&]() {
-      const int n = cnt[r];
-      if (n > 0) {
-        cs[r][tid] = cok ? acc / (double)n : 0.0;
-      } else {
-        cs[r][tid] = cok ? a.C[((size_t)b * a.r_max + r) * a.d + c] : 0.0;
-      }
-      acc = 0.0;
-      ++r;
-      end += (r < R) ? cnt[r] : 0;
-    };
     for (int g0 = 0; g0 < k; g0 += kIds) {
       const int ng = min(kIds, k - g0);
-      __syncthreads();                 // the previous group's ids are consumed
-      for (int j = tid; j < ng; j += blockDim.x) ids[j] = a.perm[k0 + g0 + j];
+      const int ng32 = (ng + kRegRowBatch - 1) / kRegRowBatch * kRegRowBatch;
+      __syncthreads();                 // the previous group is consumed
+      // Padding up to a whole batch repeats the last row id (an in-range
+      // load) and marks its region 0xff (skipped).
+      for (int j = tid; j < ng32; j += blockDim.x) {
+        const int jj = min(j, ng - 1);
+        ids[j] = a.perm[k0 + g0 + jj];
+        asl[j] = (j < ng) ? a.sreg[k0 + g0 + jj] : (uint8_t)0xff;
+      }
       __syncthreads();
-      if (g0 == 0) end = cnt[0];
       for (int j0 = 0; j0 < ng; j0 += kRegRowBatch) {
         double v[kRegRowBatch];
+        int4 id4[kRegRowBatch / 4];
+        uint32_t rg4[kRegRowBatch / 4];
 #pragma unroll
-        for (int u = 0; u < kRegRowBatch; ++u)
-          v[u] = reg_load1<T>(rows + (size_t)ids[min(j0 + u, ng - 1)] * a.d + cc);
+        for (int q = 0; q < kRegRowBatch / 4; ++q) {
+          id4[q] = *reinterpret_cast<const int4*>(&ids[j0 + 4 * q]);
+          rg4[q] = *reinterpret_cast<const uint32_t*>(&asl[j0 + 4 * q]);
+        }
+#pragma unroll
+        for (int q = 0; q < kRegRowBatch / 4; ++q) {
+          v[4 * q + 0] = reg_load1<T>(rows + (size_t)id4[q].x * a.d + cc);
+          v[4 * q + 1] = reg_load1<T>(rows + (size_t)id4[q].y * a.d + cc);
+          v[4 * q + 2] = reg_load1<T>(rows + (size_t)id4[q].z * a.d + cc);
+          v[4 * q + 3] = reg_load1<T>(rows + (size_t)id4[q].w * a.d + cc);
+        }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < kRegRowBatch; ++u) {
-          if (j0 + u >= ng) break;
-          while (r < R && g0 + j0 + u == end) close();
-          acc += v[u];
+          const int rg = (int)((rg4[u / 4] >> (8 * (u % 4))) & 0xffu);
+          if (rg != 0xff) {
+            if (rg != cur) {
+              if (cur >= 0) cs[cur][tid] = acc;
+              acc = 0.0;
+              cur = rg;
+            }
+            acc += v[u];
+          }
         }
       }
     }
-    while (r < R) close();
-    __syncthreads();        // cnt and the distance buffer are reused below
+    if (cur >= 0) cs[cur][tid] = acc;
+#pragma unroll
+    for (int r = 0; r < RM; ++r) {
+      if (r < R) {
+        const int n = cnt[r];
+        if (n > 0) cs[r][tid] = cok ? cs[r][tid] / (double)n : 0.0;
+        else cs[r][tid] = cok ? a.C[((size_t)b * a.r_max + r) * a.d + c] : 0.0;
+      }
+    }
+    __syncthreads();        // cnt and the LDS staging buffers are reused below
   }
   if (!final_step && cok) {
     for (int r = 0; r < R; ++r) a.C[((size_t)b * a.r_max + r) * a.d + c] = cs[r][tid];
@@ -222,31 +255,32 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   double* P = a.P + ((size_t)b * a.S + s) * a.k_max * a.r_max;
   for (int i = tid; i < k; i += blockDim.x) {
     const T* v = row_of(i) + c0;
-    double dot[kRegMax];
+    double dot[RM];
 #pragma unroll
-    for (int r = 0; r < kRegMax; ++r) dot[r] = 0.0;
+    for (int r = 0; r < RM; ++r) dot[r] = 0.0;
     constexpr int kHalf = RegLoadCols<T>::n;
     for (int h0 = 0; h0 < ncol; h0 += kHalf) {
       RegChunk<T> ch[kHalf / 8];
 #pragma unroll
       for (int q = 0; q < kHalf / 8; ++q)             // ncol is a multiple of 8
         ch[q].load(v + min(h0 + 8 * q, ncol - 8));   // past the end: a repeat, unused
+      // (regions past R multiply unset LDS rows; their sums are never stored)
 #pragma unroll
       for (int q = 0; q < kHalf / 8; ++q) {
-        if (h0 + 8 * q >= ncol) break;
+        if (h0 + 8 * q < ncol) {
+          double x[8];
 #pragma unroll
-        for (int r = 0; r < kRegMax; ++r) {
-          if (r >= R) break;
+          for (int e = 0; e < 8; ++e) x[e] = ch[q].at(e);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) dot[r] = fma(ch[q].at(e), cs[r][h0 + 8 * q + e], dot[r]);
+          for (int r = 0; r < RM; ++r)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dot[r] = fma(x[e], cs[r][h0 + 8 * q + e], dot[r]);
         }
       }
     }
 #pragma unroll
-    for (int r = 0; r < kRegMax; ++r) {
-      if (r >= R) break;
-      store_shared(&P[(size_t)i * a.r_max + r], dot[r]);   // read by the last slice
-    }
+    for (int r = 0; r < RM; ++r)
+      if (r < R) store_shared(&P[(size_t)i * a.r_max + r], dot[r]);   // read by the last slice
   }
   if (tid < 64) {
     // |c_r|^2 over the slice: lane l takes the columns l, l+64, ... in order,
@@ -333,11 +367,11 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   // the sizes of the smaller regions; a block scan per region and block of
   // 256 rows places each row after the earlier rows of its region
   __shared__ uint32_t scan_sh[kRegCols / 64 + 1];
-  int base[kRegMax];                           // next slot of each region (same in every thread)
+  int base[RM];                                // next slot of each region (same in every thread)
   {
     int o = 0;
 #pragma unroll
-    for (int r = 0; r < kRegMax; ++r) {
+    for (int r = 0; r < RM; ++r) {
       base[r] = o;
       if (r < R) o += cnt[r];
     }
@@ -347,12 +381,16 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     const int ai = i < k ? (int)asl[i] : -1;
     const int id = i < k ? (int)row_id(i) : 0;
 #pragma unroll
-    for (int r = 0; r < kRegMax; ++r) {
-      if (r >= R) break;
-      uint32_t tot;
-      const uint32_t pos = block_exclusive_scan(ai == r ? 1u : 0u, scan_sh, &tot);
-      if (ai == r) a.perm[k0 + base[r] + (int)pos] = id;
-      base[r] += (int)tot;
+    for (int r = 0; r < RM; ++r) {
+      if (r < R) {
+        uint32_t tot;
+        const uint32_t pos = block_exclusive_scan(ai == r ? 1u : 0u, scan_sh, &tot);
+        if (ai == r) {
+          a.perm[k0 + base[r] + (int)pos] = id;
+          a.sreg[k0 + base[r] + (int)pos] = (uint8_t)r;
+        }
+        base[r] += (int)tot;
+      }
     }
   }
   if (tid == 0) a.done[b] = 0;
@@ -369,8 +407,20 @@ size_t region_scratch_bytes(const skip_problem_t& p, int r_max) {
          ralign((size_t)p.B * S * r_max * sizeof(double)) +
          ralign((size_t)p.total_kept) +
          ralign((size_t)p.total_kept * sizeof(int32_t)) +
+         ralign((size_t)p.total_kept) +
          ralign((size_t)p.B * r_max * sizeof(int32_t)) +
          ralign((size_t)p.B * sizeof(int32_t));
+}
+
+template <typename T, bool IDX>
+static void launch_step(int r_max, dim3 grid, dim3 block, hipStream_t s, const T* rows,
+                        const RegionArgs& a) {
+  if (r_max <= 4)
+    hipLaunchKernelGGL((region_step_kernel<T, IDX, 4>), grid, block, 0, s, rows, a);
+  else if (r_max <= 8)
+    hipLaunchKernelGGL((region_step_kernel<T, IDX, 8>), grid, block, 0, s, rows, a);
+  else
+    hipLaunchKernelGGL((region_step_kernel<T, IDX, 16>), grid, block, 0, s, rows, a);
 }
 
 hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
@@ -399,6 +449,8 @@ hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32
   c += ralign((size_t)p.total_kept);
   a.perm = reinterpret_cast<int32_t*>(c);
   c += ralign((size_t)p.total_kept * sizeof(int32_t));
+  a.sreg = reinterpret_cast<uint8_t*>(c);
+  c += ralign((size_t)p.total_kept);
   a.sizes = reinterpret_cast<int32_t*>(c);
   c += ralign((size_t)p.B * r_max * sizeof(int32_t));
   a.done = reinterpret_cast<int32_t*>(c);
@@ -407,23 +459,15 @@ hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32
   a.sizes_out = sizes;
   hipLaunchKernelGGL(region_clear_kernel, dim3(1), dim3(256), 0, s, a.done, p.B);
   const bool idx = kept_idx != nullptr;
+  const dim3 grid(8 * ((p.B + 7) / 8) * S), block(kRegCols);
   for (int t = 0; t <= n_iter; ++t) {
     a.t = t;
-    const dim3 grid(S, p.B), block(kRegCols);
     if (p.dtype == SKIP_F32) {
-      if (idx)
-        hipLaunchKernelGGL((region_step_kernel<float, true>), grid, block, 0, s,
-                           (const float*)rows, a);
-      else
-        hipLaunchKernelGGL((region_step_kernel<float, false>), grid, block, 0, s,
-                           (const float*)rows, a);
+      if (idx) launch_step<float, true>(r_max, grid, block, s, (const float*)rows, a);
+      else launch_step<float, false>(r_max, grid, block, s, (const float*)rows, a);
     } else {
-      if (idx)
-        hipLaunchKernelGGL((region_step_kernel<bf16_t, true>), grid, block, 0, s,
-                           (const bf16_t*)rows, a);
-      else
-        hipLaunchKernelGGL((region_step_kernel<bf16_t, false>), grid, block, 0, s,
-                           (const bf16_t*)rows, a);
+      if (idx) launch_step<bf16_t, true>(r_max, grid, block, s, (const bf16_t*)rows, a);
+      else launch_step<bf16_t, false>(r_max, grid, block, s, (const bf16_t*)rows, a);
     }
   }
   return hipGetLastError();
