@@ -315,7 +315,7 @@ skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
  * keeps its centroid).
  *   rows      kept_idx NULL: the kept rows, [total_kept][d] (as written by
  *             skip_prune_topk); else V [B][N][d], row r of question b being
- *             V[b][kept_idx[r]] (as in the fused route)
+ *             V[b][kept_idx[r]] (as in the fused route); 16-byte aligned
  *   r_max     1..16 (paper: 8);  n_iter  1..1000;  k_max at most 16384
  *   region    out [total_kept] int32: the region of each kept row after the
  *             last iteration

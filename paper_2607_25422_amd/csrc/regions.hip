@@ -36,22 +36,40 @@ template <> __device__ __forceinline__ double reg_load1<bf16_t>(const bf16_t* p)
   return (double)bf16_to_f32(*p);
 }
 
-// eight consecutive elements as doubles (16-byte aligned for bf16, 32 for f32)
-template <typename T> __device__ __forceinline__ void reg_load8(const T* p, double* o);
-template <> __device__ __forceinline__ void reg_load8<float>(const float* p, double* o) {
-  const float4 a = *reinterpret_cast<const float4*>(p);
-  const float4 b = *reinterpret_cast<const float4*>(p + 4);
-  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
-  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+// Direct global->LDS load of 16 bytes per lane (lane l's bytes land at
+// lds + 16 * l); completion is awaited with an explicit vmcnt wait, since the
+// compiler does not count these loads.
+__device__ __forceinline__ void reg_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(lds)
+               : "memory", "m0");
 }
-template <> __device__ __forceinline__ void reg_load8<bf16_t>(const bf16_t* p, double* o) {
-  const u32x4 x = *reinterpret_cast<const u32x4*>(p);
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    o[2 * w] = (double)__uint_as_float(x[w] << 16);
-    o[2 * w + 1] = (double)__uint_as_float(x[w] & 0xffff0000u);
+__device__ __forceinline__ void reg_wait_dma() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ uint32_t reg_lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16 bytes of a row held in LDS: 8 bf16 or 4 f32 elements, as doubles
+template <typename T> struct RegLds;
+template <> struct RegLds<bf16_t> {
+  static constexpr int n = 8;
+  u32x4 w;
+  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const u32x4*>(p); }
+  __device__ __forceinline__ double at(int e) const {
+    const uint32_t x = w[e >> 1];
+    return (double)__uint_as_float((e & 1) ? (x & 0xffff0000u) : (x << 16));
   }
-}
+};
+template <> struct RegLds<float> {
+  static constexpr int n = 4;
+  u32x4 w;
+  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const u32x4*>(p); }
+  __device__ __forceinline__ double at(int e) const { return (double)__uint_as_float(w[e]); }
+};
 
 __device__ __forceinline__ int regions_of(int k, int r_max) {
   if (k <= 0) return 0;
@@ -70,7 +88,7 @@ struct RegionArgs {
   const int32_t* kept_idx;     // NULL: rows are the kept rows themselves
   int N, total_kept, B, d, k_max, r_max, S, t, n_iter;
   double* C;                   // [B][r_max][d]      centroids of the last step
-  double* P;                   // [B][S][k_max][r_max] partial v_i . c_r
+  double* P;                   // [B][S][r_max][k_max] partial v_i . c_r
   double* CN;                  // [B][S][r_max]       partial |c_r|^2
   uint8_t* asg;                // [total_kept]        current assignment
   int32_t* perm;               // [total_kept]        row ids sorted by region (stable)
@@ -82,35 +100,16 @@ struct RegionArgs {
   int32_t* sizes_out;          // [B][r_max] or NULL
 };
 
-// 8 consecutive elements of a row (16-byte aligned for bf16, 32 for f32) as
-// raw words, converted when used
-template <typename T> struct RegChunk;
-template <> struct RegChunk<bf16_t> {
-  u32x4 w;
-  __device__ __forceinline__ void load(const bf16_t* p) { w = *reinterpret_cast<const u32x4*>(p); }
-  __device__ __forceinline__ double at(int e) const {
-    const uint32_t x = w[e >> 1];
-    return (double)__uint_as_float((e & 1) ? (x & 0xffff0000u) : (x << 16));
-  }
-};
-template <> struct RegChunk<float> {
-  float4 a, b;
-  __device__ __forceinline__ void load(const float* p) {
-    a = *reinterpret_cast<const float4*>(p);
-    b = *reinterpret_cast<const float4*>(p + 4);
-  }
-  __device__ __forceinline__ double at(int e) const {
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    return (double)v[e];
-  }
-};
-
 constexpr int kRegRowBatch = 32;   // rows whose loads are issued together (update)
-// columns of a row slice loaded at once (dots): the whole bf16 slice, half of
-// an f32 one
-template <typename T> struct RegLoadCols { static constexpr int n = 128; };
-template <> struct RegLoadCols<bf16_t> { static constexpr int n = 256; };
-constexpr int kRegPairs = 4;       // (row, region) sums per thread at once (assignment)
+constexpr int kRegPairs = 8;       // (row, region) sums per thread at once (assignment)
+constexpr int kRegBufferFlags = 0x00020000;   // buffer resource word 3 (gfx9 raw buffer)
+constexpr int kRegSc1 = 16;                   // buffer load cache policy: sc1
+
+// Rows per lane in a block of rows of the dot products (each lane's share of
+// a centroid value read from LDS); the block is staged whole in LDS.
+template <int RM> struct RegDotRows { static constexpr int n = RM > 8 ? 2 : 3; };
+constexpr int kRegPoolBytes = 4 * 3 * 64 * 128;   // LDS shared by the phases (96 KiB)
+constexpr int kRegIds = 8192;                       // sorted rows staged at once (update)
 
 // RM: a compile-time bound on the regions (4, 8 or 16), so that every loop
 // over the regions unrolls and the per-region sums stay in fixed registers
@@ -119,11 +118,17 @@ constexpr int kRegPairs = 4;       // (row, region) sums per thread at once (ass
 template <typename T, bool IDX, int RM>
 __global__ void __launch_bounds__(kRegCols)
 region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
-  __shared__ double cs[kRegMax][kRegCols];      // this step's centroids, this slice
-  __shared__ __align__(16) double dl[kRegCols * kRegMax];     // distances of a block of rows (last slice)
+  __shared__ __align__(16) double cs[kRegMax][kRegCols];    // this step's centroids, this slice
+  // One pool, carved per phase:
+  //   update       row ids [kRegIds] int32, then their regions [kRegIds] uint8
+  //   dots         the block of rows, per wave [RPL * 64][128 bytes], later
+  //                the sums of waves 1-3 [3][RPL * RM][64] double
+  //   last slice   distances [256][16] double, then the assignment [k] uint8
+  __shared__ __align__(16) uint8_t pool[kRegPoolBytes];
+  static_assert(kRegIds * 5 <= kRegPoolBytes, "update staging fits the pool");
+  static_assert(kRegCols * kRegMax * 8 + kRegMaxRows <= kRegPoolBytes, "assignment fits the pool");
   __shared__ int last;
   __shared__ int cnt[kRegMax];
-  __shared__ __align__(16) uint8_t asl[kRegMaxRows];          // assignment (last slice) / sorted regions (update)
   // All slices of a question run on one XCD (workgroup id L goes to XCD
   // L % 8): its L2 then holds the question's whole kept rows across the
   // steps.  With slices spread over the XCDs instead, every XCD would hold
@@ -174,8 +179,9 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     // (positions and columns clamped into range, so every load is
     // unconditional).  Regions without rows keep their centroid.
     for (int r = tid; r < R; r += blockDim.x) cnt[r] = a.sizes[b * a.r_max + r];
-    int* ids = reinterpret_cast<int*>(dl);
-    constexpr int kIds = (int)(sizeof(dl) / (sizeof(int)));
+    int* ids = reinterpret_cast<int*>(pool);
+    uint8_t* srg = pool + kRegIds * sizeof(int);
+    constexpr int kIds = kRegIds;
     const int cc = cok ? c : c0;
     int cur = -1;
     double acc = 0.0;
@@ -188,7 +194,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       for (int j = tid; j < ng32; j += blockDim.x) {
         const int jj = min(j, ng - 1);
         ids[j] = a.perm[k0 + g0 + jj];
-        asl[j] = (j < ng) ? a.sreg[k0 + g0 + jj] : (uint8_t)0xff;
+        srg[j] = (j < ng) ? a.sreg[k0 + g0 + jj] : (uint8_t)0xff;
       }
       __syncthreads();
       for (int j0 = 0; j0 < ng; j0 += kRegRowBatch) {
@@ -198,7 +204,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 #pragma unroll
         for (int q = 0; q < kRegRowBatch / 4; ++q) {
           id4[q] = *reinterpret_cast<const int4*>(&ids[j0 + 4 * q]);
-          rg4[q] = *reinterpret_cast<const uint32_t*>(&asl[j0 + 4 * q]);
+          rg4[q] = *reinterpret_cast<const uint32_t*>(&srg[j0 + 4 * q]);
         }
 #pragma unroll
         for (int q = 0; q < kRegRowBatch / 4; ++q) {
@@ -250,58 +256,141 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     return;
   }
 
-  // ---- partial products over this slice: thread = row; each 128-column half
-  // of the row's slice is loaded whole before its products
+  // ---- partial products over this slice.  Wave w takes the slice's columns
+  // [64w, 64w + 64) and lane l the rows l, l + 64, ... of a block of rows
+  // (RPL rows per lane), so that each centroid value read from LDS (one
+  // address for the whole wave) feeds RPL rows.  A wave first copies its
+  // part of the block into LDS with direct loads, 128 bytes of a row per pass
+  // (64 bf16 or 32 f32 columns): eight lanes fetch one row's line, so every
+  // load instruction reads whole lines.  Chunk q of local row j sits at slot
+  // q ^ (j & 7) of the row's 128 bytes, so that the lanes' reads of one chunk
+  // of their own rows fall on distinct LDS banks.  Waves 1-3 then hand their
+  // sums to wave 0 through LDS, which adds them in wave order and stores them.
+  constexpr int RPL = RegDotRows<RM>::n;
+  constexpr int EPC = RegLds<T>::n;                // columns per 16-byte chunk
+  constexpr int NP = 64 / (8 * EPC);               // passes over the wave's columns
+  constexpr int NV = RPL * RM;
+  static_assert(4 * RPL * 64 * 128 <= kRegPoolBytes, "row block fits the pool");
+  static_assert(3 * NV * 64 * (int)sizeof(double) <= kRegPoolBytes, "wave sums fit the pool");
+  const int w = tid >> 6, lane = tid & 63;
   double* P = a.P + ((size_t)b * a.S + s) * a.k_max * a.r_max;
-  for (int i = tid; i < k; i += blockDim.x) {
-    const T* v = row_of(i) + c0;
-    double dot[RM];
+  uint8_t* wrows = pool + w * (RPL * 64 * 128);     // this wave's rows
+  const uint32_t wlds = __builtin_amdgcn_readfirstlane(reg_lds_addr(wrows));
+  double* red = reinterpret_cast<double*>(pool);   // [3][NV][64] sums of waves 1-3
+  for (int blk0 = 0; blk0 < k; blk0 += 64 * RPL) {
+    double dot[RPL][RM];
 #pragma unroll
-    for (int r = 0; r < RM; ++r) dot[r] = 0.0;
-    constexpr int kHalf = RegLoadCols<T>::n;
-    for (int h0 = 0; h0 < ncol; h0 += kHalf) {
-      RegChunk<T> ch[kHalf / 8];
+    for (int rr = 0; rr < RPL; ++rr)
 #pragma unroll
-      for (int q = 0; q < kHalf / 8; ++q)             // ncol is a multiple of 8
-        ch[q].load(v + min(h0 + 8 * q, ncol - 8));   // past the end: a repeat, unused
-      // (regions past R multiply unset LDS rows; their sums are never stored)
+      for (int r = 0; r < RM; ++r) dot[rr][r] = 0.0;
 #pragma unroll
-      for (int q = 0; q < kHalf / 8; ++q) {
-        if (h0 + 8 * q < ncol) {
-          double x[8];
+    for (int pass = 0; pass < NP; ++pass) {
+      // lane l fetches chunk (l & 7) ^ (l >> 3) of local row 8j + (l >> 3);
+      // rows past the question repeat its last row, columns past the slice
+      // its first chunk (their centroid values are 0)
+      // (the row addresses are all computed before the first load: the loads
+      // are opaque to the compiler, which would otherwise wait for each one
+      // before reading the next row index)
+      {
+        const int q = (lane & 7) ^ (lane >> 3);
+        const int col = 64 * w + pass * 8 * EPC + q * EPC;
+        const int colc = col < ncol ? col : 0;
+        int rid[8 * RPL];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = ch[q].at(e);
+        for (int j = 0; j < 8 * RPL; ++j) {
+          const int i = min(blk0 + 8 * j + (lane >> 3), k - 1);
+          rid[j] = IDX ? a.kept_idx[k0 + i] : k0 + i;
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int r = 0; r < RM; ++r)
+        for (int j = 0; j < 8 * RPL; ++j) {
+          const size_t row = IDX ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1) : (size_t)rid[j];
+          reg_dma16(rows + row * a.d + c0 + colc, wlds + j * 1024);
+        }
+      }
+      reg_wait_dma();
 #pragma unroll
-            for (int e = 0; e < 8; ++e) dot[r] = fma(x[e], cs[r][h0 + 8 * q + e], dot[r]);
+      for (int q = 0; q < 8; ++q) {
+        RegLds<T> x[RPL];
+#pragma unroll
+        for (int rr = 0; rr < RPL; ++rr)
+          x[rr].load(wrows + (rr * 64 + lane) * 128 + ((q ^ (lane & 7)) * 16));
+        const int col = 64 * w + pass * 8 * EPC + q * EPC;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+          double xv[RPL];
+#pragma unroll
+          for (int rr = 0; rr < RPL; ++rr) xv[rr] = x[rr].at(e);
+          // (regions past R multiply unset LDS rows; their sums are never stored)
+#pragma unroll
+          for (int r = 0; r < RM; ++r) {
+            const double cv = cs[r][col + e];
+#pragma unroll
+            for (int rr = 0; rr < RPL; ++rr) dot[rr][r] = fma(xv[rr], cv, dot[rr][r]);
+          }
+        }
+      }
+      asm volatile("" ::: "memory");      // the reads above precede the next pass's loads
+      __builtin_amdgcn_s_waitcnt(0xC07F); // lgkmcnt(0)
+    }
+    __syncthreads();                      // every wave is done with its rows
+    if (w > 0) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) red[((w - 1) * NV + v) * 64 + lane] = dot[v / RM][v % RM];
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int rr = 0; rr < RPL; ++rr) {
+        const int i = blk0 + rr * 64 + lane;
+#pragma unroll
+        for (int r = 0; r < RM; ++r) {
+          const int v = rr * RM + r;
+          const double sum = ((dot[rr][r] + red[v * 64 + lane]) + red[(NV + v) * 64 + lane]) +
+                             red[(2 * NV + v) * 64 + lane];
+          if (r < R && i < k) store_shared(&P[(size_t)r * a.k_max + i], sum);   // read by the last slice
         }
       }
     }
-#pragma unroll
-    for (int r = 0; r < RM; ++r)
-      if (r < R) store_shared(&P[(size_t)i * a.r_max + r], dot[r]);   // read by the last slice
+    __syncthreads();                      // the sums are read before the pool is reused
   }
-  if (tid < 64) {
-    // |c_r|^2 over the slice: lane l takes the columns l, l+64, ... in order,
-    // then a fixed shuffle tree
-    for (int r = 0; r < R; ++r) {
-      double q = 0.0;
-      for (int j = tid; j < ncol; j += 64) q = fma(cs[r][j], cs[r][j], q);
-      q = wave_sum_f64(q);
-      if (tid == 0) store_shared(&a.CN[((size_t)b * a.S + s) * a.r_max + r], q);
+  {
+    // |c_r|^2 over the slice: wave w takes the regions w, w + 4, ..., lane l
+    // the columns l, l + 64, l + 128, l + 192 in order (columns past the
+    // slice hold 0), then a fixed shuffle tree over all of the wave's regions
+    // at once
+    constexpr int RW = (RM + 3) / 4;
+    double q[RW];
+#pragma unroll
+    for (int u = 0; u < RW; ++u) {
+      const int r = min(w + 4 * u, RM - 1);
+      q[u] = 0.0;
+#pragma unroll
+      for (int j = 0; j < kRegCols / 64; ++j) q[u] = fma(cs[r][lane + 64 * j], cs[r][lane + 64 * j], q[u]);
+    }
+#pragma unroll
+    for (int sh = 32; sh >= 1; sh >>= 1)
+#pragma unroll
+      for (int u = 0; u < RW; ++u) q[u] += __shfl_xor(q[u], sh, kWave);
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < RW; ++u)
+        if (w + 4 * u < R) store_shared(&a.CN[((size_t)b * a.S + s) * a.r_max + w + 4 * u], q[u]);
     }
   }
   if (tid < kRegMax) cnt[tid] = 0;
   if (!finish_and_check_last(&a.done[b], a.S, &last)) return;
 
   // ---- the question's last slice: assignment for the next step.  Rows in
-  // blocks of 256: the (row, region) sums over the slices, four pairs and
+  // blocks of 256: the (row, region) sums over the slices, eight pairs and
   // eight slices of loads in flight per thread, in slice order; then one row
-  // per thread takes its argmin.
+  // per thread takes its argmin, and each wave counts its rows per region.
+  double* dl = reinterpret_cast<double*>(pool);                 // [256][r_max]
+  uint8_t* asl = pool + kRegCols * kRegMax * sizeof(double);    // [k]
   const double* Pb = a.P + (size_t)b * a.S * a.k_max * a.r_max;
   const double* CNb = a.CN + (size_t)b * a.S * a.r_max;
   __shared__ double cn[kRegMax];
+  __shared__ int cw[kRegCols / 64][kRegMax];
   if (tid < R) {
     double q = 0.0;
     for (int z = 0; z < a.S; ++z) q += load_shared(&CNb[z * a.r_max + tid]);
@@ -309,27 +398,38 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   }
   __syncthreads();
   const size_t zs = (size_t)a.k_max * a.r_max;      // one slice's partials
+  const auto prsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<double*>(Pb), 0, (int)(a.S * zs * sizeof(double)), kRegBufferFlags);
   for (int i0 = 0; i0 < k; i0 += kRegCols) {
     const int rows_here = min(kRegCols, k - i0);
-    const int npair = rows_here * a.r_max;
+    const int npair = rows_here * R;
     for (int f0 = tid; f0 < npair; f0 += kRegPairs * kRegCols) {
+      // pair f = (region f / rows_here, row f % rows_here of the block)
       double acc[kRegPairs];
-      size_t off[kRegPairs];
-      bool on[kRegPairs];
+      uint32_t off[kRegPairs];
 #pragma unroll
       for (int j = 0; j < kRegPairs; ++j) {
-        const int f = f0 + j * kRegCols;
-        on[j] = f < npair && (f % a.r_max) < R;
-        off[j] = on[j] ? (size_t)i0 * a.r_max + f : 0;   // a valid slot when unused
+        const int f = min(f0 + j * kRegCols, npair - 1);        // past the end: a repeat, unused
+        const int r = f / rows_here;
+        off[j] = (uint32_t)(r * a.k_max + i0 + (f - r * rows_here)) * (uint32_t)sizeof(double);
         acc[j] = 0.0;
       }
+      // Buffer loads: the question's partials as one resource, the slice as
+      // a scalar offset, the pair as a 32-bit byte offset (a 64-bit address
+      // per load would take two registers each).  Cache policy sc1, as for
+      // the other reads of values the slices published.
+      auto part = [&](int z, int j) -> double {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(
+            prsrc, off[j], (int)((size_t)z * zs * sizeof(double)), kRegSc1);
+        return __builtin_bit_cast(double, v);
+      };
       int z = 0;
       for (; z + 8 <= a.S; z += 8) {
         double x[8][kRegPairs];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
 #pragma unroll
-          for (int j = 0; j < kRegPairs; ++j) x[u][j] = load_shared(&Pb[(size_t)(z + u) * zs + off[j]]);
+          for (int j = 0; j < kRegPairs; ++j) x[u][j] = part(z + u, j);
 #pragma unroll
         for (int u = 0; u < 8; ++u)
 #pragma unroll
@@ -337,17 +437,21 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       }
       for (; z < a.S; ++z)
 #pragma unroll
-        for (int j = 0; j < kRegPairs; ++j) acc[j] += load_shared(&Pb[(size_t)z * zs + off[j]]);
+        for (int j = 0; j < kRegPairs; ++j) acc[j] += part(z, j);
 #pragma unroll
       for (int j = 0; j < kRegPairs; ++j) {
         const int f = f0 + j * kRegCols;
-        if (on[j]) dl[f] = cn[f % a.r_max] - 2.0 * acc[j];
+        if (f < npair) {
+          const int r = f / rows_here;
+          dl[(f - r * rows_here) * a.r_max + r] = cn[r] - 2.0 * acc[j];
+        }
       }
     }
     __syncthreads();
+    int best = -1;
     if (tid < rows_here) {
       const int i = i0 + tid;
-      int best = 0;
+      best = 0;
       double bd = dl[tid * a.r_max];
       for (int r = 1; r < R; ++r) {
         const double dist = dl[tid * a.r_max + r];
@@ -358,15 +462,21 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       }
       a.asg[k0 + i] = (uint8_t)best;
       asl[i] = (uint8_t)best;
-      atomicAdd(&cnt[best], 1);
+    }
+#pragma unroll
+    for (int r = 0; r < RM; ++r) {
+      if (r < R) {
+        const uint64_t m = __ballot(best == r);
+        if (lane == 0 && m != 0) atomicAdd(&cnt[r], (int)__popcll(m));
+      }
     }
     __syncthreads();
   }
   if (tid < R) a.sizes[b * a.r_max + tid] = cnt[tid];
   // row ids sorted by region, ascending within a region: region r starts at
-  // the sizes of the smaller regions; a block scan per region and block of
-  // 256 rows places each row after the earlier rows of its region
-  __shared__ uint32_t scan_sh[kRegCols / 64 + 1];
+  // the sizes of the smaller regions; within a block of 256 rows a row goes
+  // after the block's earlier rows of its region (the counts of the earlier
+  // waves, then the lanes below it in its wave's ballot)
   int base[RM];                                // next slot of each region (same in every thread)
   {
     int o = 0;
@@ -376,22 +486,34 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       if (r < R) o += cnt[r];
     }
   }
+  const uint64_t below = (1ull << lane) - 1ull;
   for (int i0 = 0; i0 < k; i0 += kRegCols) {
     const int i = i0 + tid;
     const int ai = i < k ? (int)asl[i] : -1;
-    const int id = i < k ? (int)row_id(i) : 0;
+    uint64_t mine = 0;
+    int off = 0;
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
       if (r < R) {
-        uint32_t tot;
-        const uint32_t pos = block_exclusive_scan(ai == r ? 1u : 0u, scan_sh, &tot);
+        const uint64_t m = __ballot(ai == r);
+        if (lane == 0) cw[w][r] = (int)__popcll(m);
         if (ai == r) {
-          a.perm[k0 + base[r] + (int)pos] = id;
-          a.sreg[k0 + base[r] + (int)pos] = (uint8_t)r;
+          mine = m;
+          off = base[r];
         }
-        base[r] += (int)tot;
       }
     }
+    __syncthreads();
+    if (ai >= 0) {
+      for (int v = 0; v < w; ++v) off += cw[v][ai];
+      off += (int)__popcll(mine & below);
+      a.perm[k0 + off] = (int32_t)row_id(i);
+      a.sreg[k0 + off] = (uint8_t)ai;
+    }
+#pragma unroll
+    for (int r = 0; r < RM; ++r)
+      if (r < R) base[r] += cw[0][r] + cw[1][r] + cw[2][r] + cw[3][r];
+    __syncthreads();                             // the counts are reused
   }
   if (tid == 0) a.done[b] = 0;
 }

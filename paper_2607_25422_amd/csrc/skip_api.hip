@@ -502,6 +502,7 @@ skip_status_t skip_region_kmeans(const skip_problem_t* p, const void* rows,
   if (!kept_offsets || !centroids || !workspace) return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && (!rows || !region)) return SKIP_ERR_INVALID_ARG;
   if (r_max < 1 || r_max > 16 || n_iter < 1 || n_iter > 1000) return SKIP_ERR_INVALID_ARG;
+  if (((uintptr_t)rows & 15) != 0) return SKIP_ERR_INVALID_ARG;
   if (p->k_max > kMaxN) return SKIP_ERR_UNSUPPORTED;
   if (kept_idx) {
     if (p->N < 1 || p->k_max > p->N) return SKIP_ERR_INVALID_ARG;

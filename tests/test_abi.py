@@ -269,6 +269,7 @@ def test_region_kmeans_validation(b):
         assert call(p, r_max=r_max) == b.SKIP_ERR_INVALID_ARG, r_max
     for n_iter in (0, 1001):
         assert call(p, n_iter=n_iter) == b.SKIP_ERR_INVALID_ARG, n_iter
+    assert call(p, rows=FAKE + 8) == b.SKIP_ERR_INVALID_ARG     # rows 16-byte aligned
     q = _problem(b)
     q.k_max = 600             # kept rows read through kept_idx need k_max <= N
     q.total_kept = 1200

@@ -84,6 +84,21 @@ def test_regions_small_ragged(B, seed, r_max, n_iter):
     check_regions(batch, kept, region, cent, sizes, r_max, n_iter, f"seed={seed}")
 
 
+@pytest.mark.parametrize("wl,H,d_h,r_max", [("llava_bf16", 5, 64, 4), ("tiny_fp32", 5, 40, 16),
+                                              ("llava_bf16", 10, 40, 8)])
+def test_regions_ragged_slice(B, wl, H, d_h, r_max):
+    """d = 320, 200 or 400: the last 256-column slice is partly empty (64,
+    200 or 144 columns), so some waves of it own no columns at all."""
+    batch = wls.make_batch(wl, 11, B=4, N=400, H=H, d_h=d_h, T=(2, 5), k=(5, 70, 200, 400))
+    say(f"regions ragged slice {wl} d={H * d_h} r_max={r_max} k={batch.k.tolist()}")
+    kept = kept_oracle(batch)
+    db = B.to_device(batch)
+    idx = torch.from_numpy(np.concatenate(kept).astype(np.int32)).cuda()
+    region, cent, sizes = B.region_kmeans(db, db.V, kept_idx=idx, r_max=r_max, n_iter=6)
+    torch.cuda.synchronize()
+    check_regions(batch, kept, region, cent, sizes, r_max, 6, f"{wl} d={H * d_h}")
+
+
 def test_regions_fp32_and_repeatable(B):
     batch = wls.make_batch("tiny_fp32", 5, B=3, N=200, k=(4, 40, 120))
     kept = kept_oracle(batch)
