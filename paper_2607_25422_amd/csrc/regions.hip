@@ -91,7 +91,7 @@ struct RegionArgs {
   double* P;                   // [B][S][r_max][k_max] partial v_i . c_r
   double* CN;                  // [B][S][r_max]       partial |c_r|^2
   uint8_t* asg;                // [total_kept]        current assignment
-  int32_t* perm;               // [total_kept]        row ids sorted by region (stable)
+  int32_t* perm;               // [total_kept]        positions in the question sorted by region (stable)
   uint8_t* sreg;               // [total_kept]        region of each sorted position
   int32_t* sizes;              // [B][r_max]          rows per region
   int32_t* done;               // [B]                 finished slices
@@ -110,6 +110,7 @@ constexpr int kRegSc1 = 16;                   // buffer load cache policy: sc1
 template <int RM> struct RegDotRows { static constexpr int n = RM > 8 ? 2 : 3; };
 constexpr int kRegPoolBytes = 4 * 3 * 64 * 128;   // LDS shared by the phases (96 KiB)
 constexpr int kRegIds = 8192;                       // sorted rows staged at once (update)
+constexpr int kRegResidentRows = 3 * 64;            // largest resident block (RPL = 3)
 
 // RM: a compile-time bound on the regions (4, 8 or 16), so that every loop
 // over the regions unrolls and the per-region sums stay in fixed registers
@@ -129,6 +130,8 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   static_assert(kRegCols * kRegMax * 8 + kRegMaxRows <= kRegPoolBytes, "assignment fits the pool");
   __shared__ int last;
   __shared__ int cnt[kRegMax];
+  // LDS addresses of the sorted positions, when the rows are resident
+  __shared__ __align__(16) int spos[kRegResidentRows + 8];
   // All slices of a question run on one XCD (workgroup id L goes to XCD
   // L % 8): its L2 then holds the question's whole kept rows across the
   // steps.  With slices spread over the XCDs instead, every XCD would hold
@@ -161,70 +164,158 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     return;
   }
 
+  // ---- rows of the question in LDS.  Wave w holds the slice's columns
+  // [64w, 64w + 64) of a block of 64 RPL rows, 128 bytes of a row per pass
+  // (64 bf16 or 32 f32 columns), copied with direct loads: eight lanes fetch
+  // one row's line, so every load instruction reads whole lines.  Chunk q of
+  // local row j sits at slot q ^ (j & 7) of the row's 128 bytes, so that the
+  // lanes' reads of one chunk of their own rows fall on distinct LDS banks.
+  // When a bf16 question fits one block its rows stay resident for the whole
+  // step: loaded once here, read by the centroid update and the products.
+  constexpr int RPL = RegDotRows<RM>::n;
+  constexpr int EPC = RegLds<T>::n;                // columns per 16-byte chunk
+  constexpr int NP = 64 / (8 * EPC);               // passes over the wave's columns
+  static_assert(4 * RPL * 64 * 128 <= kRegPoolBytes, "row block fits the pool");
+  static_assert(64 * RPL <= kRegResidentRows, "resident positions fit");
+  const int w = tid >> 6, lane = tid & 63;
+  uint8_t* wrows = pool + w * (RPL * 64 * 128);     // this wave's rows
+  const uint32_t wlds = __builtin_amdgcn_readfirstlane(reg_lds_addr(wrows));
+  const bool resident = NP == 1 && k <= 64 * RPL;
+  auto stage_rows = [&](int blk0, int pass) {
+    // lane l fetches chunk (l & 7) ^ (l >> 3) of local row 8j + (l >> 3);
+    // rows past the question repeat its last row, columns past the slice its
+    // first chunk (their centroid values are 0).  The row indices are all
+    // read before the first copy: the copies are opaque to the compiler,
+    // which would otherwise wait for each one before the next index.
+    const int q = (lane & 7) ^ (lane >> 3);
+    const int col = 64 * w + pass * 8 * EPC + q * EPC;
+    const int colc = col < ncol ? col : 0;
+    int rid[8 * RPL];
+#pragma unroll
+    for (int j = 0; j < 8 * RPL; ++j) {
+      const int i = min(blk0 + 8 * j + (lane >> 3), k - 1);
+      rid[j] = IDX ? a.kept_idx[k0 + i] : k0 + i;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < 8 * RPL; ++j) {
+      const size_t row = IDX ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1) : (size_t)rid[j];
+      reg_dma16(rows + row * a.d + c0 + colc, wlds + j * 1024);
+    }
+  };
+  // element (local row lr, slice column tid) of a resident block
+  auto resident_at = [&](int lr) -> double {
+    const uint8_t* e = wrows + lr * 128 + (((lane >> 3) ^ (lr & 7)) * 16) + (lane & 7) * sizeof(T);
+    return reg_load1<T>(reinterpret_cast<const T*>(e));
+  };
+  if (resident) stage_rows(0, 0);
+
   // ---- centroids of this step, this slice's columns (thread = column)
   if (a.t == 0) {
+    if (resident) reg_wait_dma();                  // a wave reads only rows it copied
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
       if (r < R) {
         const int pos = ((2 * r + 1) * k) / (2 * R);
-        cs[r][tid] = cok ? reg_load1<T>(row_of(pos) + c) : 0.0;
+        cs[r][tid] = cok ? (resident ? resident_at(pos) : reg_load1<T>(row_of(pos) + c)) : 0.0;
       }
     }
   } else {
-    // the rows sorted by region (perm: row ids, ascending within a region;
-    // sreg: the region of each sorted position) are summed in one pass:
-    // each thread keeps its column's running sum in a register and hands it
-    // to LDS where the region changes (a uniform test).  Row ids and regions
-    // are staged in LDS 8192 at a time; 32 row loads are issued together
-    // (positions and columns clamped into range, so every load is
-    // unconditional).  Regions without rows keep their centroid.
+    // the rows sorted by region (perm: positions in the question, ascending
+    // within a region; sreg: the region of each sorted position) are summed
+    // in one pass: each thread keeps its column's running sum in a register
+    // and hands it to LDS where the region changes (a uniform test).  32
+    // values are read together, positions and columns clamped into range
+    // (padding repeats the last position, marked region 0xff: skipped).
+    // Regions without rows keep their centroid.
     for (int r = tid; r < R; r += blockDim.x) cnt[r] = a.sizes[b * a.r_max + r];
-    int* ids = reinterpret_cast<int*>(pool);
-    uint8_t* srg = pool + kRegIds * sizeof(int);
-    constexpr int kIds = kRegIds;
     const int cc = cok ? c : c0;
     int cur = -1;
     double acc = 0.0;
-    for (int g0 = 0; g0 < k; g0 += kIds) {
-      const int ng = min(kIds, k - g0);
-      const int ng32 = (ng + kRegRowBatch - 1) / kRegRowBatch * kRegRowBatch;
-      __syncthreads();                 // the previous group is consumed
-      // Padding up to a whole batch repeats the last row id (an in-range
-      // load) and marks its region 0xff (skipped).
-      for (int j = tid; j < ng32; j += blockDim.x) {
-        const int jj = min(j, ng - 1);
-        ids[j] = a.perm[k0 + g0 + jj];
-        srg[j] = (j < ng) ? a.sreg[k0 + g0 + jj] : (uint8_t)0xff;
-      }
-      __syncthreads();
-      for (int j0 = 0; j0 < ng; j0 += kRegRowBatch) {
-        double v[kRegRowBatch];
-        int4 id4[kRegRowBatch / 4];
-        uint32_t rg4[kRegRowBatch / 4];
+    auto take = [&](const double (&v)[kRegRowBatch], const uint32_t (&rg4)[kRegRowBatch / 4]) {
 #pragma unroll
-        for (int q = 0; q < kRegRowBatch / 4; ++q) {
-          id4[q] = *reinterpret_cast<const int4*>(&ids[j0 + 4 * q]);
-          rg4[q] = *reinterpret_cast<const uint32_t*>(&srg[j0 + 4 * q]);
-        }
-#pragma unroll
-        for (int q = 0; q < kRegRowBatch / 4; ++q) {
-          v[4 * q + 0] = reg_load1<T>(rows + (size_t)id4[q].x * a.d + cc);
-          v[4 * q + 1] = reg_load1<T>(rows + (size_t)id4[q].y * a.d + cc);
-          v[4 * q + 2] = reg_load1<T>(rows + (size_t)id4[q].z * a.d + cc);
-          v[4 * q + 3] = reg_load1<T>(rows + (size_t)id4[q].w * a.d + cc);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int u = 0; u < kRegRowBatch; ++u) {
-          const int rg = (int)((rg4[u / 4] >> (8 * (u % 4))) & 0xffu);
-          if (rg != 0xff) {
-            if (rg != cur) {
-              if (cur >= 0) cs[cur][tid] = acc;
-              acc = 0.0;
-              cur = rg;
-            }
-            acc += v[u];
+      for (int u = 0; u < kRegRowBatch; ++u) {
+        const int rg = (int)((rg4[u / 4] >> (8 * (u % 4))) & 0xffu);
+        if (rg != 0xff) {
+          if (rg != cur) {
+            if (cur >= 0) cs[cur][tid] = acc;
+            acc = 0.0;
+            cur = rg;
           }
+          acc += v[u];
+        }
+      }
+    };
+    if (resident) {
+      // Region by region (sizes give the runs of the sorted order), eight
+      // values at a time, ascending positions.  For sorted position j the
+      // staged word is the lane-independent part of its LDS address,
+      // 128 lr + 16 (lr & 7) for row lr: the lane's element is then at
+      // (word ^ 16 (l >> 3)) + 2 (l & 7) past the wave's rows.  Past the end
+      // of a run the values are replaced by 0 (the positions there are valid).
+      const int k8 = k + 8;
+      for (int j = tid; j < k8; j += blockDim.x) {
+        const int lr = clampi(a.perm[k0 + min(j, k - 1)], 0, k - 1);
+        spos[j] = lr * 128 + ((lr & 7) << 4);
+      }
+      reg_wait_dma();
+      __syncthreads();
+      const uint32_t lsw = (uint32_t)((lane >> 3) << 4);
+      const uint8_t* wl = wrows + (lane & 7) * sizeof(T);
+      int st = 0;
+#pragma unroll
+      for (int r = 0; r < RM; ++r) {
+        if (r < R) {
+          const int n = cnt[r];
+          double racc = 0.0;
+          for (int j0 = 0; j0 < n; j0 += 8) {
+            int pw[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) pw[u] = spos[st + j0 + u];   // a run starts anywhere
+            double v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+              v[u] = reg_load1<T>(reinterpret_cast<const T*>(wl + (((uint32_t)pw[u]) ^ lsw)));
+#pragma unroll
+            for (int u = 0; u < 8; ++u) racc += (j0 + u < n) ? v[u] : 0.0;
+          }
+          if (n > 0) cs[r][tid] = racc;
+          st += n;
+        }
+      }
+    } else {
+      // row indices and regions staged in LDS 8192 at a time
+      int* ids = reinterpret_cast<int*>(pool);
+      uint8_t* srg = pool + kRegIds * sizeof(int);
+      constexpr int kIds = kRegIds;
+      for (int g0 = 0; g0 < k; g0 += kIds) {
+        const int ng = min(kIds, k - g0);
+        const int ng32 = (ng + kRegRowBatch - 1) / kRegRowBatch * kRegRowBatch;
+        __syncthreads();                 // the previous group is consumed
+        for (int j = tid; j < ng32; j += blockDim.x) {
+          const int jj = min(j, ng - 1);
+          ids[j] = (int)row_id(clampi(a.perm[k0 + g0 + jj], 0, k - 1));
+          srg[j] = (j < ng) ? a.sreg[k0 + g0 + jj] : (uint8_t)0xff;
+        }
+        __syncthreads();
+        for (int j0 = 0; j0 < ng; j0 += kRegRowBatch) {
+          double v[kRegRowBatch];
+          int4 id4[kRegRowBatch / 4];
+          uint32_t rg4[kRegRowBatch / 4];
+#pragma unroll
+          for (int q = 0; q < kRegRowBatch / 4; ++q) {
+            id4[q] = *reinterpret_cast<const int4*>(&ids[j0 + 4 * q]);
+            rg4[q] = *reinterpret_cast<const uint32_t*>(&srg[j0 + 4 * q]);
+          }
+#pragma unroll
+          for (int q = 0; q < kRegRowBatch / 4; ++q) {
+            v[4 * q + 0] = reg_load1<T>(rows + (size_t)id4[q].x * a.d + cc);
+            v[4 * q + 1] = reg_load1<T>(rows + (size_t)id4[q].y * a.d + cc);
+            v[4 * q + 2] = reg_load1<T>(rows + (size_t)id4[q].z * a.d + cc);
+            v[4 * q + 3] = reg_load1<T>(rows + (size_t)id4[q].w * a.d + cc);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          take(v, rg4);
         }
       }
     }
@@ -258,24 +349,13 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 
   // ---- partial products over this slice.  Wave w takes the slice's columns
   // [64w, 64w + 64) and lane l the rows l, l + 64, ... of a block of rows
-  // (RPL rows per lane), so that each centroid value read from LDS (one
-  // address for the whole wave) feeds RPL rows.  A wave first copies its
-  // part of the block into LDS with direct loads, 128 bytes of a row per pass
-  // (64 bf16 or 32 f32 columns): eight lanes fetch one row's line, so every
-  // load instruction reads whole lines.  Chunk q of local row j sits at slot
-  // q ^ (j & 7) of the row's 128 bytes, so that the lanes' reads of one chunk
-  // of their own rows fall on distinct LDS banks.  Waves 1-3 then hand their
-  // sums to wave 0 through LDS, which adds them in wave order and stores them.
-  constexpr int RPL = RegDotRows<RM>::n;
-  constexpr int EPC = RegLds<T>::n;                // columns per 16-byte chunk
-  constexpr int NP = 64 / (8 * EPC);               // passes over the wave's columns
+  // (RPL rows per lane, staged in LDS as described above), so that each
+  // centroid value read from LDS (one address for the whole wave) feeds RPL
+  // rows.  Waves 1-3 then hand their sums to wave 0 through LDS, which adds
+  // them in wave order and stores them.
   constexpr int NV = RPL * RM;
-  static_assert(4 * RPL * 64 * 128 <= kRegPoolBytes, "row block fits the pool");
   static_assert(3 * NV * 64 * (int)sizeof(double) <= kRegPoolBytes, "wave sums fit the pool");
-  const int w = tid >> 6, lane = tid & 63;
   double* P = a.P + ((size_t)b * a.S + s) * a.k_max * a.r_max;
-  uint8_t* wrows = pool + w * (RPL * 64 * 128);     // this wave's rows
-  const uint32_t wlds = __builtin_amdgcn_readfirstlane(reg_lds_addr(wrows));
   double* red = reinterpret_cast<double*>(pool);   // [3][NV][64] sums of waves 1-3
   for (int blk0 = 0; blk0 < k; blk0 += 64 * RPL) {
     double dot[RPL][RM];
@@ -285,30 +365,10 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       for (int r = 0; r < RM; ++r) dot[rr][r] = 0.0;
 #pragma unroll
     for (int pass = 0; pass < NP; ++pass) {
-      // lane l fetches chunk (l & 7) ^ (l >> 3) of local row 8j + (l >> 3);
-      // rows past the question repeat its last row, columns past the slice
-      // its first chunk (their centroid values are 0)
-      // (the row addresses are all computed before the first load: the loads
-      // are opaque to the compiler, which would otherwise wait for each one
-      // before reading the next row index)
-      {
-        const int q = (lane & 7) ^ (lane >> 3);
-        const int col = 64 * w + pass * 8 * EPC + q * EPC;
-        const int colc = col < ncol ? col : 0;
-        int rid[8 * RPL];
-#pragma unroll
-        for (int j = 0; j < 8 * RPL; ++j) {
-          const int i = min(blk0 + 8 * j + (lane >> 3), k - 1);
-          rid[j] = IDX ? a.kept_idx[k0 + i] : k0 + i;
-        }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int j = 0; j < 8 * RPL; ++j) {
-          const size_t row = IDX ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1) : (size_t)rid[j];
-          reg_dma16(rows + row * a.d + c0 + colc, wlds + j * 1024);
-        }
+      if (!resident) {
+        stage_rows(blk0, pass);
+        reg_wait_dma();
       }
-      reg_wait_dma();
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         RegLds<T> x[RPL];
@@ -507,7 +567,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     if (ai >= 0) {
       for (int v = 0; v < w; ++v) off += cw[v][ai];
       off += (int)__popcll(mine & below);
-      a.perm[k0 + off] = (int32_t)row_id(i);
+      a.perm[k0 + off] = i;
       a.sreg[k0 + off] = (uint8_t)ai;
     }
 #pragma unroll
