@@ -88,8 +88,8 @@ struct RegionArgs {
   const int32_t* kept_idx;     // NULL: rows are the kept rows themselves
   int N, total_kept, B, d, k_max, r_max, S, t, n_iter;
   double* C;                   // [B][r_max][d]      centroids of the last step
-  double* P;                   // [B][S][r_max][k_max] partial v_i . c_r
-  double* CN;                  // [B][S][r_max]       partial |c_r|^2
+  double* P;                   // [B][S][r_max][k_max + 1] partial v_i . c_r, then |c_r|^2
+  int PK;                      // k_max + 1: the region stride of P
   uint8_t* asg;                // [total_kept]        current assignment
   int32_t* perm;               // [total_kept]        positions in the question sorted by region (stable)
   uint8_t* sreg;               // [total_kept]        region of each sorted position
@@ -355,7 +355,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   // them in wave order and stores them.
   constexpr int NV = RPL * RM;
   static_assert(3 * NV * 64 * (int)sizeof(double) <= kRegPoolBytes, "wave sums fit the pool");
-  double* P = a.P + ((size_t)b * a.S + s) * a.k_max * a.r_max;
+  double* P = a.P + ((size_t)b * a.S + s) * a.PK * a.r_max;
   double* red = reinterpret_cast<double*>(pool);   // [3][NV][64] sums of waves 1-3
   for (int blk0 = 0; blk0 < k; blk0 += 64 * RPL) {
     double dot[RPL][RM];
@@ -408,7 +408,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
           const int v = rr * RM + r;
           const double sum = ((dot[rr][r] + red[v * 64 + lane]) + red[(NV + v) * 64 + lane]) +
                              red[(2 * NV + v) * 64 + lane];
-          if (r < R && i < k) store_shared(&P[(size_t)r * a.k_max + i], sum);   // read by the last slice
+          if (r < R && i < k) store_shared(&P[(size_t)r * a.PK + i], sum);   // read by the last slice
         }
       }
     }
@@ -435,43 +435,45 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     if (lane == 0) {
 #pragma unroll
       for (int u = 0; u < RW; ++u)
-        if (w + 4 * u < R) store_shared(&a.CN[((size_t)b * a.S + s) * a.r_max + w + 4 * u], q[u]);
+        if (w + 4 * u < R) store_shared(&P[(size_t)(w + 4 * u) * a.PK + a.k_max], q[u]);
     }
   }
   if (tid < kRegMax) cnt[tid] = 0;
   if (!finish_and_check_last(&a.done[b], a.S, &last)) return;
 
   // ---- the question's last slice: assignment for the next step.  Rows in
-  // blocks of 256: the (row, region) sums over the slices, eight pairs and
-  // eight slices of loads in flight per thread, in slice order; then one row
-  // per thread takes its argmin, and each wave counts its rows per region.
-  double* dl = reinterpret_cast<double*>(pool);                 // [256][r_max]
+  // blocks of 256: the (row, region) sums over the slices, with the regions'
+  // |c_r|^2 as R more pairs of the first block, eight pairs and eight slices
+  // of loads in flight per thread, in slice order; then one row per thread
+  // takes its argmin, and each wave counts its rows per region.
+  double* dl = reinterpret_cast<double*>(pool);                 // [256][r_max] v_i . c_r
   uint8_t* asl = pool + kRegCols * kRegMax * sizeof(double);    // [k]
-  const double* Pb = a.P + (size_t)b * a.S * a.k_max * a.r_max;
-  const double* CNb = a.CN + (size_t)b * a.S * a.r_max;
+  const double* Pb = a.P + (size_t)b * a.S * a.PK * a.r_max;
   __shared__ double cn[kRegMax];
   __shared__ int cw[kRegCols / 64][kRegMax];
-  if (tid < R) {
-    double q = 0.0;
-    for (int z = 0; z < a.S; ++z) q += load_shared(&CNb[z * a.r_max + tid]);
-    cn[tid] = q;
-  }
-  __syncthreads();
-  const size_t zs = (size_t)a.k_max * a.r_max;      // one slice's partials
+  const size_t zs = (size_t)a.PK * a.r_max;         // one slice's partials
   const auto prsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<double*>(Pb), 0, (int)(a.S * zs * sizeof(double)), kRegBufferFlags);
   for (int i0 = 0; i0 < k; i0 += kRegCols) {
     const int rows_here = min(kRegCols, k - i0);
-    const int npair = rows_here * R;
+    const int nrow_pairs = rows_here * R;
+    const int npair = nrow_pairs + (i0 == 0 ? R : 0);
     for (int f0 = tid; f0 < npair; f0 += kRegPairs * kRegCols) {
-      // pair f = (region f / rows_here, row f % rows_here of the block)
+      // pair f < nrow_pairs: (region f / rows_here, row f % rows_here of the
+      // block); past them: |c_r|^2 of region f - nrow_pairs
       double acc[kRegPairs];
       uint32_t off[kRegPairs];
 #pragma unroll
       for (int j = 0; j < kRegPairs; ++j) {
         const int f = min(f0 + j * kRegCols, npair - 1);        // past the end: a repeat, unused
-        const int r = f / rows_here;
-        off[j] = (uint32_t)(r * a.k_max + i0 + (f - r * rows_here)) * (uint32_t)sizeof(double);
+        int slot;
+        if (f < nrow_pairs) {
+          const int r = f / rows_here;
+          slot = r * a.PK + i0 + (f - r * rows_here);
+        } else {
+          slot = (f - nrow_pairs) * a.PK + a.k_max;
+        }
+        off[j] = (uint32_t)slot * (uint32_t)sizeof(double);
         acc[j] = 0.0;
       }
       // Buffer loads: the question's partials as one resource, the slice as
@@ -501,9 +503,11 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 #pragma unroll
       for (int j = 0; j < kRegPairs; ++j) {
         const int f = f0 + j * kRegCols;
-        if (f < npair) {
+        if (f < nrow_pairs) {
           const int r = f / rows_here;
-          dl[(f - r * rows_here) * a.r_max + r] = cn[r] - 2.0 * acc[j];
+          dl[(f - r * rows_here) * a.r_max + r] = acc[j];
+        } else if (f < npair) {
+          cn[f - nrow_pairs] = acc[j];
         }
       }
     }
@@ -512,9 +516,9 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     if (tid < rows_here) {
       const int i = i0 + tid;
       best = 0;
-      double bd = dl[tid * a.r_max];
+      double bd = cn[0] - 2.0 * dl[tid * a.r_max];
       for (int r = 1; r < R; ++r) {
-        const double dist = dl[tid * a.r_max + r];
+        const double dist = cn[r] - 2.0 * dl[tid * a.r_max + r];
         if (dist < bd) {
           bd = dist;
           best = r;
@@ -585,8 +589,7 @@ int region_slices(const skip_problem_t& p) { return (p.d + kRegCols - 1) / kRegC
 size_t region_scratch_bytes(const skip_problem_t& p, int r_max) {
   const size_t S = (size_t)region_slices(p);
   return ralign((size_t)p.B * r_max * p.d * sizeof(double)) +
-         ralign((size_t)p.B * S * p.k_max * r_max * sizeof(double)) +
-         ralign((size_t)p.B * S * r_max * sizeof(double)) +
+         ralign((size_t)p.B * S * (p.k_max + 1) * r_max * sizeof(double)) +
          ralign((size_t)p.total_kept) +
          ralign((size_t)p.total_kept * sizeof(int32_t)) +
          ralign((size_t)p.total_kept) +
@@ -624,9 +627,8 @@ hipError_t launch_regions(const skip_problem_t& p, const void* rows, const int32
   a.C = reinterpret_cast<double*>(c);
   c += ralign((size_t)p.B * r_max * p.d * sizeof(double));
   a.P = reinterpret_cast<double*>(c);
-  c += ralign((size_t)p.B * S * p.k_max * r_max * sizeof(double));
-  a.CN = reinterpret_cast<double*>(c);
-  c += ralign((size_t)p.B * S * r_max * sizeof(double));
+  a.PK = p.k_max + 1;
+  c += ralign((size_t)p.B * S * (p.k_max + 1) * r_max * sizeof(double));
   a.asg = reinterpret_cast<uint8_t*>(c);
   c += ralign((size_t)p.total_kept);
   a.perm = reinterpret_cast<int32_t*>(c);
