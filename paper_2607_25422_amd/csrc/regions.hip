@@ -108,9 +108,12 @@ constexpr int kRegSc1 = 16;                   // buffer load cache policy: sc1
 // Rows per lane in a block of rows of the dot products (each lane's share of
 // a centroid value read from LDS); the block is staged whole in LDS.
 template <int RM> struct RegDotRows { static constexpr int n = RM > 8 ? 2 : 3; };
-constexpr int kRegPoolBytes = 4 * 3 * 64 * 128;   // LDS shared by the phases (96 KiB)
+// LDS shared by the phases: per wave a block of up to 3 x 64 rows of 128
+// bytes and one zero row
+constexpr int kRegPoolBytes = 4 * (3 * 64 + 1) * 128;
 constexpr int kRegIds = 8192;                       // sorted rows staged at once (update)
 constexpr int kRegResidentRows = 3 * 64;            // largest resident block (RPL = 3)
+constexpr int kRegUpdBatch = 16;                     // resident values read at once (update)
 
 // RM: a compile-time bound on the regions (4, 8 or 16), so that every loop
 // over the regions unrolls and the per-region sums stay in fixed registers
@@ -131,7 +134,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   __shared__ int last;
   __shared__ int cnt[kRegMax];
   // LDS addresses of the sorted positions, when the rows are resident
-  __shared__ __align__(16) int spos[kRegResidentRows + 8];
+  __shared__ __align__(16) int spos[kRegResidentRows + (kRegMax + 1) * kRegUpdBatch];
   // All slices of a question run on one XCD (workgroup id L goes to XCD
   // L % 8): its L2 then holds the question's whole kept rows across the
   // steps.  With slices spread over the XCDs instead, every XCD would hold
@@ -175,10 +178,11 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   constexpr int RPL = RegDotRows<RM>::n;
   constexpr int EPC = RegLds<T>::n;                // columns per 16-byte chunk
   constexpr int NP = 64 / (8 * EPC);               // passes over the wave's columns
-  static_assert(4 * RPL * 64 * 128 <= kRegPoolBytes, "row block fits the pool");
+  constexpr int WROWS = RPL * 64 + 1;              // rows of a wave's block, the last one zero
+  static_assert(4 * WROWS * 128 <= kRegPoolBytes, "row block fits the pool");
   static_assert(64 * RPL <= kRegResidentRows, "resident positions fit");
   const int w = tid >> 6, lane = tid & 63;
-  uint8_t* wrows = pool + w * (RPL * 64 * 128);     // this wave's rows
+  uint8_t* wrows = pool + w * (WROWS * 128);        // this wave's rows
   const uint32_t wlds = __builtin_amdgcn_readfirstlane(reg_lds_addr(wrows));
   const bool resident = NP == 1 && k <= 64 * RPL;
   auto stage_rows = [&](int blk0, int pass) {
@@ -247,40 +251,71 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
       }
     };
     if (resident) {
-      // Region by region (sizes give the runs of the sorted order), eight
-      // values at a time, ascending positions.  For sorted position j the
-      // staged word is the lane-independent part of its LDS address,
-      // 128 lr + 16 (lr & 7) for row lr: the lane's element is then at
-      // (word ^ 16 (l >> 3)) + 2 (l & 7) past the wave's rows.  Past the end
-      // of a run the values are replaced by 0 (the positions there are valid).
-      const int k8 = k + 8;
-      for (int j = tid; j < k8; j += blockDim.x) {
-        const int lr = clampi(a.perm[k0 + min(j, k - 1)], 0, k - 1);
-        spos[j] = lr * 128 + ((lr & 7) << 4);
+      // Region by region (sizes give the runs of the sorted order), sixteen
+      // values at a time into four running sums (value u of a batch into sum
+      // u % 4; the sums are added pairwise at the end of the region).  The
+      // staged words give the lane-independent part of each value's LDS
+      // address, 128 lr + 16 (lr & 7) for row lr: the lane's element is then
+      // at (word ^ 16 (l >> 3)) + 2 (l & 7) past the wave's rows.  Each run is
+      // padded to a whole batch with the word of the wave's zero row, and the
+      // next batch's words are read before the current batch's values.
+      uint32_t* zrow = reinterpret_cast<uint32_t*>(wrows + (WROWS - 1) * 128);
+      if (lane < 32) zrow[lane] = 0u;
+      const int zword = (WROWS - 1) * 128;         // (WROWS - 1) is a multiple of 8
+      __syncthreads();                             // cnt
+      int pst[RM], rst[RM], np_all = 0;
+      {
+        int o = 0;
+#pragma unroll
+        for (int r = 0; r < RM; ++r) {
+          const int n = r < R ? cnt[r] : 0;
+          pst[r] = np_all;
+          rst[r] = o;
+          np_all += (n + kRegUpdBatch - 1) / kRegUpdBatch * kRegUpdBatch;
+          o += n;
+        }
+      }
+      for (int p = tid; p < np_all + kRegUpdBatch; p += blockDim.x) {
+        int r = 0;
+#pragma unroll
+        for (int q = 1; q < RM; ++q)
+          if (q < R && p >= pst[q]) r = q;
+        const int i = p - pst[r];
+        int word = zword;
+        if (p < np_all && i < cnt[r]) {
+          const int lr = clampi(a.perm[k0 + rst[r] + i], 0, k - 1);
+          word = lr * 128 + ((lr & 7) << 4);
+        }
+        spos[p] = word;
       }
       reg_wait_dma();
       __syncthreads();
       const uint32_t lsw = (uint32_t)((lane >> 3) << 4);
       const uint8_t* wl = wrows + (lane & 7) * sizeof(T);
-      int st = 0;
+      int pwn[kRegUpdBatch];
+#pragma unroll
+      for (int u = 0; u < kRegUpdBatch; ++u) pwn[u] = spos[u];
 #pragma unroll
       for (int r = 0; r < RM; ++r) {
         if (r < R) {
           const int n = cnt[r];
-          double racc = 0.0;
-          for (int j0 = 0; j0 < n; j0 += 8) {
-            int pw[8];
+          const int np = (n + kRegUpdBatch - 1) / kRegUpdBatch * kRegUpdBatch;
+          double racc[4] = {0.0, 0.0, 0.0, 0.0};
+          for (int j0 = 0; j0 < np; j0 += kRegUpdBatch) {
+            int pw[kRegUpdBatch];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) pw[u] = spos[st + j0 + u];   // a run starts anywhere
-            double v[8];
+            for (int u = 0; u < kRegUpdBatch; ++u) {
+              pw[u] = pwn[u];
+              pwn[u] = spos[pst[r] + j0 + kRegUpdBatch + u];
+            }
+            double v[kRegUpdBatch];
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
+            for (int u = 0; u < kRegUpdBatch; ++u)
               v[u] = reg_load1<T>(reinterpret_cast<const T*>(wl + (((uint32_t)pw[u]) ^ lsw)));
 #pragma unroll
-            for (int u = 0; u < 8; ++u) racc += (j0 + u < n) ? v[u] : 0.0;
+            for (int u = 0; u < kRegUpdBatch; ++u) racc[u & 3] += v[u];
           }
-          if (n > 0) cs[r][tid] = racc;
-          st += n;
+          if (n > 0) cs[r][tid] = (racc[0] + racc[1]) + (racc[2] + racc[3]);
         }
       }
     } else {
