@@ -274,6 +274,26 @@ def test_xattn_edge_rules_and_metrics(B, rule, metric, beta, dtype):
     check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), dtype)
 
 
+@pytest.mark.parametrize("dtype,H,d_h,P", [("bf16", 5, 64, (2, 9)), ("f32", 3, 128, (4, 7)),
+                                          ("bf16", 2, 128, (17, 20)), ("f32", 4, 64, (18,))])
+def test_graph_ragged_slices_and_passage_groups(B, dtype, H, d_h, P):
+    """The edge dot products work on 256-column slices and at most 16 passages
+    at a time: d = 320 and 384 leave the last slice partly empty, 17-20
+    passages take two passage groups.  Graphs exact, attention to the usual
+    bar."""
+    batch = small_batch(dtype, 9, H=H, d_h=d_h, P=P, L_p=(3, 40), k=(1, 30, 200, 260))
+    say(f"graph ragged {dtype} d={H * d_h} P={batch.P.tolist()} k={batch.k.tolist()}")
+    db = B.to_device(batch, avg_degree=3.0)
+    Qh = queries_from_batch(batch)
+    O, L, rp, col = B.bipartite_xattn(db, Qh.cuda())
+    torch.cuda.synchronize()
+    _, adj, O_ref, L_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, 3.0)
+    check_graph(batch, rp, col, adj)
+    check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), dtype)
+
+
 @pytest.mark.parametrize("rule,metric,beta", [("row", "cosine", 0.1), ("fraction", "dot", 0.1)])
 def test_fused_edge_rules_full_size(B, rule, metric, beta):
     """highres_bf16 through the fused route under the other cuts: kept sets
