@@ -277,9 +277,9 @@ def test_xattn_edge_rules_and_metrics(B, rule, metric, beta, dtype):
 @pytest.mark.parametrize("dtype,H,d_h,P", [("bf16", 5, 64, (2, 9)), ("f32", 3, 128, (4, 7)),
                                           ("bf16", 2, 128, (17, 20)), ("f32", 4, 64, (18,))])
 def test_graph_ragged_slices_and_passage_groups(B, dtype, H, d_h, P):
-    """The edge dot products work on 256-column slices and at most 16 passages
-    at a time: d = 320 and 384 leave the last slice partly empty, 17-20
-    passages take two passage groups.  Graphs exact, attention to the usual
+    """The edge dot products work on column slices of 512 and on tiles of at
+    most 16 passages: d = 320 and 384 leave a slice partly empty, 17-20
+    passages take two passage tiles.  Graphs exact, attention to the usual
     bar."""
     batch = small_batch(dtype, 9, H=H, d_h=d_h, P=P, L_p=(3, 40), k=(1, 30, 200, 260))
     say(f"graph ragged {dtype} d={H * d_h} P={batch.P.tolist()} k={batch.k.tolist()}")
