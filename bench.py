@@ -493,42 +493,62 @@ def main():
             torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
-    events = [B.StageEvents() for _ in range(args.steps)]
     for _ in range(args.warmup):
         B.route_fused(db, passage_keys=pkeys, out=out)
     torch.cuda.synchronize()
     print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
 
+    # Timed region: exactly `steps` fused routes and nothing else on the
+    # stream.  With --cold a 1 GiB fill overwrites the last-level cache before
+    # every step; it is not part of a step, so each step is then bracketed by
+    # its own pair of events and the median step gives the rate.
     flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda") if args.cold else None
+    cold_ev = ([(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(args.steps)] if args.cold else None)
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         if flush is not None:
             flush.fill_(float(i))
-        B.route_fused(db, passage_keys=pkeys, out=out, stage_events=events[i])
+            cold_ev[i][0].record()
+        B.route_fused(db, passage_keys=pkeys, out=out)
+        if flush is not None:
+            cold_ev[i][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     wall = t1 - t0
+    if args.cold:
+        cold_ms = sorted(a.elapsed_time(b) for a, b in cold_ev)
+        ms_per_step = cold_ms[len(cold_ms) // 2]
+        qps = p.B / (ms_per_step * 1e-3)
+    else:
+        ms_per_step = 1e3 * wall / args.steps
+        qps = p.B * args.steps / wall
 
+    # Profiled pass, after the timed region and not part of it: the same
+    # routes with an event between every two kernel stages (the stage split,
+    # the attention time of the roofline, per-step percentiles).  Each event
+    # on the stream costs a few microseconds, so these steps run longer than
+    # the timed ones.
+    n_prof = min(args.steps, 50)
+    events = [B.StageEvents() for _ in range(n_prof)]
+    for i in range(n_prof):
+        if flush is not None:
+            flush.fill_(float(i))
+        B.route_fused(db, passage_keys=pkeys, out=out, stage_events=events[i])
+    torch.cuda.synchronize()
     stages = {k: 0.0 for k in B.FUSED_STAGES}
     step_ms = []
     for ev in events:
         sm = ev.stage_ms()
         step_ms.append(sum(sm.values()))
         for k, v in sm.items():
-            stages[k] += v / args.steps
+            stages[k] += v / n_prof
     gpu_ms = sum(stages.values())
     step_sorted = sorted(step_ms)
 
     def pct(q):
         return step_sorted[min(len(step_sorted) - 1, int(q * len(step_sorted)))]
-
-    if args.cold:
-        # the cache flush between steps is not part of a step
-        ms_per_step = pct(0.5)
-        qps = p.B / (ms_per_step * 1e-3)
-    else:
-        ms_per_step = 1e3 * wall / args.steps
-        qps = p.B * args.steps / wall
 
     attn_ms = stages["attention"]
     attn_gbs = attn_bytes / (attn_ms * 1e-3) / 1e9
@@ -558,7 +578,8 @@ def main():
                    "edge_metric": args.edge_metric,
                    **({"edge_beta": args.edge_beta} if args.edge_rule == "fraction" else {})},
         "step_gpu_ms": {"p10": round(pct(0.1), 5), "p50": round(pct(0.5), 5),
-                        "p90": round(pct(0.9), 5)},
+                        "p90": round(pct(0.9), 5), "steps": n_prof,
+                        "what": "profiled pass: stage events on the stream, after the timed steps"},
         "roofline": {
             "kernel": "attn_bf16_kernel" if wl.dtype == "bf16" else "attn_f32_kernel",
             "bound": "hbm",
