@@ -32,121 +32,228 @@ template <> __device__ __forceinline__ float elem_f32<bf16_t>(const bf16_t* p, s
 
 // ---------------------------------------------------------------------------
 // Edge dot products on the float64 matrix cores, split over d.
-// Workgroup = (512-column slice, 64 kept rows x 16 passages, question); wave w
-// owns rows 16w..16w+15 of the block.  v_mfma_f64_16x16x4_f64 takes one
-// element of A (rows x 4 columns) and one of B (4 columns x passages) per
-// lane: lane l supplies row/passage l % 16 and column slot l / 16.  The
-// contraction order over columns is free, so column slot kk of MFMA m (m =
-// 0..7 within a 32-column step) is column 8*kk + m: every lane then reads 8
-// consecutive columns of its row (one 16-byte load) and of its passage key,
-// straight from global memory.  Each lane also sums the squares of the values
-// it loads (partial row and key norms).  Results per slice are summed in
-// slice order by the selection kernel.
-constexpr int kEdRows = 64;
-constexpr int kEdPT = 16;
-constexpr int kEdSlice = 512;
-constexpr int kEdSteps = 4;
+// Workgroup = (256-column slice, question), one workgroup per CU over the
+// chip for the usual shapes; the slices of a question run on one XCD
+// (workgroup id L goes to XCD L % 8).  v_mfma_f64_16x16x4_f64 takes one
+// element of A (16 rows x 4 columns) and one of B (4 columns x 16 passages)
+// per lane: lane l supplies row/passage l % 16 and column slot l / 16.  The
+// contraction order over columns is free, so column slot kk of MFMA m within
+// a group of 4·E columns (E = 8 bf16 or 4 f32 per 16-byte chunk) is column
+// E*kk + m: a lane then reads one 16-byte chunk of its row and E consecutive
+// key values per group.
+//   * The kept rows come into LDS in blocks of 192 (16-row tiles; wave w
+//     takes tiles w, w + 4, w + 8) by direct loads of whole 512-byte row
+//     slices (f32 rows in two 128-column passes); chunk c of row r sits at
+//     slot c ^ (r & 7), so that the lanes' reads of one chunk group fall on
+//     distinct banks.  Chunks past the slice are cleared.
+//   * The passage keys of the slice sit in LDS as float64, 16 passages at a
+//     time, read by all four waves.
+// Each lane also sums the squares of its row values (partial row norms); the
+// key norms come from the keys in LDS.  Results per slice are summed in slice
+// order by the selection kernel.
+constexpr int kEdCols = 256;               // columns per slice
+constexpr int kEdBlockRows = 192;          // rows per LDS block (12 tiles)
+constexpr int kEdPT = 16;                  // passages per tile
+constexpr int kEdKeyStride = kEdCols + 2;  // doubles per key row in LDS (bank spread)
 
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
-template <typename T>
-__device__ __forceinline__ void load8_f64(const T* p, bool ok, double* out);
-template <>
-__device__ __forceinline__ void load8_f64<bf16_t>(const bf16_t* p, bool ok, double* out) {
-  u32x4 x = ok ? *reinterpret_cast<const u32x4*>(p) : u32x4{0u, 0u, 0u, 0u};
-  unpack_f64<bf16_t>(x, out);
+__device__ __forceinline__ void ed_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(lds)
+               : "memory", "m0");
 }
-template <>
-__device__ __forceinline__ void load8_f64<float>(const float* p, bool ok, double* out) {
-  u32x4 x0 = ok ? *reinterpret_cast<const u32x4*>(p) : u32x4{0u, 0u, 0u, 0u};
-  u32x4 x1 = ok ? *reinterpret_cast<const u32x4*>(p + 4) : u32x4{0u, 0u, 0u, 0u};
-  unpack_f64<float>(x0, out);
-  unpack_f64<float>(x1, out + 4);
+__device__ __forceinline__ void ed_wait_dma() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
+  asm volatile("" ::: "memory");
 }
+__device__ __forceinline__ uint32_t ed_lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+struct EdgeDotArgs {
+  const int32_t* kept_idx;     // NULL: rows are [total_kept][d]; else V [B][N][d]
+  int N;
+  const int32_t* kept_offsets;
+  const int32_t* query_passages;
+  const double* kbar;          // [total_passages][d] float64 keys, or
+  const float* pkeys;          // [total_passages][d] caller-given keys
+  int d, total_kept, total_passages, k_max, P_max, B, S;
+  double* part;                // [B][S][k_max][P_max] partial <q_i, k̄_j>
+  double* qn2p;                // [B][S][k_max]        partial |q_i|^2
+  double* kn2p;                // [B][S][P_max]        partial |k̄_j|^2
+};
 
 template <typename T>
 __global__ void __launch_bounds__(256)
-edge_dot_kernel(const T* __restrict__ qbase, const int32_t* __restrict__ kept_idx, int N,
-                const int32_t* __restrict__ kept_offsets,
-                const int32_t* __restrict__ query_passages, const double* __restrict__ kbar,
-                const float* __restrict__ pkeys, int d, int total_kept, int total_passages,
-                int k_max, int P_max, int S, int n_pt, double* __restrict__ part,
-                double* __restrict__ qn2p, double* __restrict__ kn2p) {
-  const int s = blockIdx.x, b = blockIdx.z;
-  const int rb = blockIdx.y / n_pt, pt = blockIdx.y % n_pt;
+edge_dot_kernel(const T* __restrict__ rows, EdgeDotArgs a) {
+  constexpr int E = 16 / (int)sizeof(T);          // columns per 16-byte chunk
+  constexpr int CPP = 32 * E;                      // columns per pass (512 bytes of a row)
+  constexpr int NP = kEdCols / CPP;                // passes per slice
+  __shared__ __align__(16) uint8_t rbuf[kEdBlockRows * 512];
+  __shared__ __align__(16) double ks[kEdPT * kEdKeyStride];
+  const int L = blockIdx.x, xcd = L & 7, jl = L >> 3;
+  const int s = jl % a.S, b = xcd + 8 * (jl / a.S), tid = threadIdx.x;
+  if (b >= a.B) return;
   int k0, k1, p0, p1;
-  range_of(kept_offsets, b, total_kept, k0, k1);
-  range_of(query_passages, b, total_passages, p0, p1);
-  const int kq = min(k1 - k0, k_max);
-  const int P = min(min(p1 - p0, P_max), 64);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt0 = rb * kEdRows + wave * 16;          // first row of this wave
-  if (rt0 >= kq || pt * kEdPT >= P) return;          // whole wave (no barriers)
-  const int c_begin = s * kEdSlice, c_end = min(d, c_begin + kEdSlice);
-  const int l16 = lane & 15, kk = lane >> 4;
-  const int row = rt0 + l16, pj = pt * kEdPT + l16;
-  const bool row_ok = row < kq, key_ok = pj < P;
-  const T* qrow = qbase;          // never read unless row_ok
-  if (row_ok) {
-    if (kept_idx) {
-      const int src = clampi(kept_idx[k0 + row], 0, N - 1);
-      qrow = qbase + ((size_t)b * N + src) * d;
-    } else {
-      qrow = qbase + (size_t)(k0 + row) * d;
-    }
-  }
-  const size_t krow = (size_t)(p0 + (key_ok ? pj : 0)) * d;
+  range_of(a.kept_offsets, b, a.total_kept, k0, k1);
+  range_of(a.query_passages, b, a.total_passages, p0, p1);
+  const int k = min(k1 - k0, a.k_max);
+  const int P = min(min(p1 - p0, a.P_max), 64);
+  if (k <= 0 || P <= 0) return;                  // nothing of this question is read
+  const int c0 = s * kEdCols, ncol = min(kEdCols, a.d - c0);
+  const int w = tid >> 6, lane = tid & 63, l16 = lane & 15, kk = lane >> 4;
+  const uint32_t rlds = __builtin_amdgcn_readfirstlane(ed_lds_addr(rbuf));
+  const size_t zs = (size_t)b * a.S + s;
 
-  f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
-  double qq = 0.0, k2 = 0.0;
-  // kEdSteps 32-column steps per iteration: every load of the iteration is
-  // issued before the first product, so each wave waits once per 128 columns.
-  for (int c0 = c_begin; c0 < c_end; c0 += 32 * kEdSteps) {
-    double qa[kEdSteps][8], kv[kEdSteps][8];
+  // Copy rows blk0 .. blk0 + 191, columns [pass·CPP, pass·CPP + CPP) of the
+  // slice, into rbuf.  Wave w copies rows 48w .. 48w + 47, two per load
+  // instruction: lane l writes slot l % 32 of row 2j + l / 32, which holds
+  // chunk (l % 32) ^ (row & 7).  Rows past the question repeat its last row;
+  // chunks past the slice read its first chunk (cleared afterwards).  The
+  // row indices are all read before the first copy: the copies are opaque to
+  // the compiler, which would otherwise wait for each one before the next.
+  auto stage_rows = [&](int blk0, int pass) {
+    const int half = lane >> 5, slot = lane & 31;
+    int rid[24];
 #pragma unroll
-    for (int st = 0; st < kEdSteps; ++st) {
-      const int c = c0 + 32 * st + 8 * kk;
-      const bool in = c < c_end;               // d is a multiple of 8
-      load8_f64<T>(qrow + c, row_ok && in, qa[st]);
-      if (pkeys) {
-        load8_f64<float>(pkeys + krow + c, key_ok && in, kv[st]);
-      } else if (key_ok && in) {
-        const double2* kp = reinterpret_cast<const double2*>(kbar + krow + c);
+    for (int j = 0; j < 24; ++j) {
+      const int i = min(blk0 + 48 * w + 2 * j + half, k - 1);
+      rid[j] = a.kept_idx ? a.kept_idx[k0 + i] : k0 + i;
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const double2 t = kp[q];
-          kv[st][2 * q] = t.x;
-          kv[st][2 * q + 1] = t.y;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kv[st][e] = 0.0;
+    for (int j = 0; j < 24; ++j) {
+      const int r = 48 * w + 2 * j + half;         // row within the block
+      const int col = pass * CPP + (slot ^ (r & 7)) * E;
+      const int colc = col < ncol ? col : 0;
+      const size_t row = a.kept_idx ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1)
+                                    : (size_t)rid[j];
+      ed_dma16(rows + row * a.d + c0 + colc,
+               __builtin_amdgcn_readfirstlane(rlds + (uint32_t)(48 * w + 2 * j) * 512u));
+    }
+  };
+  // after the copies of a pass have landed: clear the chunks past the slice
+  // (each wave its own rows; every wave waits for its copies first)
+  auto finish_rows = [&](int pass) {
+    ed_wait_dma();
+    if (pass * CPP + CPP > ncol) {
+      for (int t = lane; t < 48 * 32; t += 64) {
+        const int r = 48 * w + (t >> 5), sl = t & 31;
+        if (pass * CPP + (sl ^ (r & 7)) * E >= ncol)
+          *reinterpret_cast<u32x4*>(rbuf + r * 512 + sl * 16) = u32x4{0u, 0u, 0u, 0u};
       }
     }
+    __syncthreads();                               // rows of every wave are in
+  };
+
+  for (int blk0 = 0; blk0 < k; blk0 += kEdBlockRows) {
+    for (int pt0 = 0; pt0 < P; pt0 += kEdPT) {
+      // two accumulators per tile (even and odd MFMA of a group), added at
+      // the end: six independent chains keep the matrix pipeline busy
+      double qq[3] = {0.0, 0.0, 0.0};
+      f64x4_t acc[3][2];
 #pragma unroll
-    for (int st = 0; st < kEdSteps; ++st)
+      for (int t = 0; t < 3; ++t) acc[t][0] = acc[t][1] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+      for (int pass = 0; pass < NP; ++pass) {
+        __syncthreads();                           // the previous rows and keys are read
+        stage_rows(blk0, pass);
+        // keys of passages pt0 .. pt0 + 15 over this pass's columns (0 past P
+        // or the slice), under the row copies
+        // (every load unconditional, passages and columns clamped into range
+        // and the value replaced by 0 afterwards, so that they all issue
+        // before the first wait)
+        {
+          constexpr int KPT = kEdPT * CPP / 256;   // key values per thread
+          double kvv[KPT];
 #pragma unroll
-      for (int m = 0; m < 8; ++m) {
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[st][m], kv[st][m], acc, 0, 0, 0);
-        qq = fma(qa[st][m], qa[st][m], qq);
-        k2 = fma(kv[st][m], kv[st][m], k2);
+          for (int u = 0; u < KPT; ++u) {
+            const int t = tid + 256 * u, n = t / CPP, c = pass * CPP + t % CPP;
+            const size_t o = (size_t)(p0 + min(pt0 + n, P - 1)) * a.d + c0 + min(c, ncol - 1);
+            kvv[u] = a.pkeys ? (double)a.pkeys[o] : a.kbar[o];
+          }
+#pragma unroll
+          for (int u = 0; u < KPT; ++u) {
+            const int t = tid + 256 * u, n = t / CPP, c = pass * CPP + t % CPP;
+            ks[n * kEdKeyStride + c] = (pt0 + n < P && c < ncol) ? kvv[u] : 0.0;
+          }
+        }
+        finish_rows(pass);
+        if (blk0 == 0) {
+          // |k̄_j|^2 over the pass's columns: wave w takes passages w, w + 4,
+          // w + 8, w + 12, lane l the columns l, l + 64, ... in order, then a
+          // fixed shuffle tree; added to the partial of the previous pass
+          double q2[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const double* kr = ks + (w + 4 * u) * kEdKeyStride + pass * CPP;
+            q2[u] = 0.0;
+            for (int c = lane; c < CPP; c += 64) q2[u] = fma(kr[c], kr[c], q2[u]);
+          }
+#pragma unroll
+          for (int sh = 32; sh >= 1; sh >>= 1)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) q2[u] += __shfl_xor(q2[u], sh, kWave);
+          if (lane == 0) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int j = pt0 + w + 4 * u;
+              if (j < P) {
+                double* o = a.kn2p + zs * a.P_max + j;
+                *o = (pass == 0 ? 0.0 : *o) + q2[u];
+              }
+            }
+          }
+        }
+        // products: per group of 4 chunks, one key read (E values) feeds the
+        // three row tiles of the wave
+        const double* kp = ks + l16 * kEdKeyStride + pass * CPP + kk * E;
+#pragma unroll 2
+        for (int g = 0; g < 8; ++g) {
+          double kv[E];
+#pragma unroll
+          for (int m = 0; m < E; ++m) kv[m] = kp[g * 4 * E + m];
+          double qa[3][8];
+#pragma unroll
+          for (int t = 0; t < 3; ++t) {
+            const int r = 16 * (w + 4 * t) + l16;          // row within the block
+            const u32x4 x = *reinterpret_cast<const u32x4*>(
+                rbuf + r * 512 + (((4 * g + kk) ^ (r & 7)) * 16));
+            unpack_f64<T>(x, qa[t]);
+          }
+#pragma unroll
+          for (int m = 0; m < E; ++m)
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+              acc[t][m & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[t][m], kv[m], acc[t][m & 1], 0, 0, 0);
+          if (pt0 == 0) {
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+#pragma unroll
+              for (int m = 0; m < E; ++m) qq[t] = fma(qa[t][m], qa[t][m], qq[t]);
+          }
+        }
       }
-  }
-  // lanes l16, l16+16, l16+32, l16+48 hold the four column slots of one row/key
-  qq += __shfl_xor(qq, 16, 64);
-  qq += __shfl_xor(qq, 32, 64);
-  k2 += __shfl_xor(k2, 16, 64);
-  k2 += __shfl_xor(k2, 32, 64);
-  const size_t base = (size_t)b * S + s;
-  // D[i][j]: register r of lane l holds row 4*r + l/16, passage column l % 16
+      // D[i][j]: register v of lane l holds row 4v + l/16 of the tile, passage l % 16
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int i = rt0 + 4 * r + kk;
-    if (i < kq && key_ok) part[(base * k_max + i) * P_max + pj] = acc[r];
-  }
-  if (kk == 0) {
-    if (pt == 0 && row_ok) qn2p[base * k_max + row] = qq;
-    if (rb == 0 && wave == 0 && key_ok) kn2p[base * P_max + pj] = k2;
+      for (int t = 0; t < 3; ++t) {
+        const int tile0 = blk0 + 16 * (w + 4 * t);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int i = tile0 + 4 * v + kk, j = pt0 + l16;
+          if (i < k && j < P) a.part[(zs * a.k_max + i) * a.P_max + j] = acc[t][0][v] + acc[t][1][v];
+        }
+        if (pt0 == 0) {
+          // lanes l16, l16 + 16, l16 + 32, l16 + 48 hold the four column slots of row l16
+          double q = qq[t];
+          q += __shfl_xor(q, 16, kWave);
+          q += __shfl_xor(q, 32, kWave);
+          const int i = tile0 + l16;
+          if (kk == 0 && i < k) a.qn2p[zs * a.k_max + i] = q;
+        }
+      }
+    }
   }
 }
 
@@ -178,7 +285,10 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
   __shared__ SelectShared sh;
   __shared__ uint32_t scan_sh[20];
   __shared__ uint8_t flag[kGSelThreads * kGSelMaxPT];
-  __shared__ uint64_t rkeys[kGSelThreads * kGSelMaxPT];   // per-row cut only
+  // row norms while the keys are formed, then the keys of the per-row cut
+  __shared__ __align__(16) uint64_t rkeys[kGSelThreads * kGSelMaxPT];
+  __shared__ double knorm[64];
+  double* qnorm = reinterpret_cast<double*>(rkeys);
   const int b = blockIdx.x;
   int k0, k1, p0, p1;
   range_of(kept_offsets, b, total_kept, k0, k1);
@@ -200,37 +310,76 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
   const int C = (n + blockDim.x - 1) / blockDim.x;
   const int e0 = threadIdx.x * C;
   const int cnt = max(0, min(C, n - e0));
-  // compatibility of (i, j) from the per-slice partial sums, in slice order
+  // Norms |q_i| and |k̄_j| first: square roots of the slice partials summed
+  // in slice order (slices clamped into range, so every load of a batch is
+  // unconditional), kept in LDS.
+  auto slice_sum = [&](const double* base, size_t stride) -> double {
+    double acc = 0.0;
+    for (int sl0 = 0; sl0 < S; sl0 += 16) {
+      double x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = base[(size_t)min(sl0 + u, S - 1) * stride];
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (sl0 + u < S) acc += x[u];
+    }
+    return acc;
+  };
+  if (metric != SKIP_EDGE_DOT) {
+    const int kr = min(k, kGSelThreads * kGSelMaxPT);   // rows that have candidates
+    for (int t = threadIdx.x; t < kr + P; t += blockDim.x) {
+      if (t < kr) qnorm[t] = sqrt(slice_sum(qn2p + (size_t)b * S * k_max + t, (size_t)k_max));
+      else knorm[t - kr] = sqrt(slice_sum(kn2p + (size_t)b * S * P_max + (t - kr), (size_t)P_max));
+    }
+    __syncthreads();
+  }
+  // compatibility of (i, j) from the per-slice partial products, in slice
+  // order; two candidates at a time, sixteen slices of their loads in flight
   uint64_t keys[kGSelMaxPT];
 #pragma unroll
-  for (int jj = 0; jj < kGSelMaxPT; ++jj) {
-    keys[jj] = 0ull;
-    if (jj < cnt) {
-      const int f = e0 + jj, i = f / P, j = f % P;
-      double dot = 0.0, q2 = 0.0, k2 = 0.0;
-      for (int sl0 = 0; sl0 < S; sl0 += 8) {
-        double pd[8], pq[8], pk[8];
+  for (int jj = 0; jj < kGSelMaxPT; ++jj) keys[jj] = 0ull;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+  for (int jj = 0; jj < kGSelMaxPT; jj += 2) {
+    if (jj < cnt) {
+      int ii[2], pj[2];
+      double dot[2] = {0.0, 0.0};
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int f = min(e0 + jj + h, n - 1);
+        ii[h] = f / P;
+        pj[h] = f - ii[h] * P;
+      }
+      for (int sl0 = 0; sl0 < S; sl0 += 16) {
+        double pd[2][16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
           const size_t base = (size_t)b * S + min(sl0 + u, S - 1);
-          pd[u] = part[(base * k_max + i) * P_max + j];
-          pq[u] = qn2p[base * k_max + i];
-          pk[u] = kn2p[base * P_max + j];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) pd[h][u] = part[(base * k_max + ii[h]) * P_max + pj[h]];
         }
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (sl0 + u < S) { dot += pd[u]; q2 += pq[u]; k2 += pk[u]; }
+        for (int u = 0; u < 16; ++u)
+          if (sl0 + u < S) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) dot[h] += pd[h][u];
+          }
       }
-      double c;
-      if (metric == SKIP_EDGE_DOT) {
-        c = dot * inv_sqrt_d;
-      } else {
-        const double nq = sqrt(q2), nk = sqrt(k2);
-        c = (nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (jj + h < cnt) {
+          double c;
+          if (metric == SKIP_EDGE_DOT) {
+            c = dot[h] * inv_sqrt_d;
+          } else {
+            const double nq = qnorm[ii[h]], nk = knorm[pj[h]];
+            c = (nq > 0.0 && nk > 0.0) ? dot[h] / (nq * nk) : 0.0;
+          }
+          keys[jj + h] = ((pkeep >> pj[h]) & 1ull) ? order_key(c) : 0ull;
+        }
       }
-      keys[jj] = ((pkeep >> j) & 1ull) ? order_key(c) : 0ull;
     }
   }
+  __syncthreads();                 // the row norms are read before rkeys is written
   uint32_t flags;
   if (rule == SKIP_EDGE_ROW_TOP) {
     // every row keeps its D largest (lower passage first on ties)
@@ -342,26 +491,35 @@ hipError_t launch_passage_keys(const skip_problem_t& p, const void* Kh,
                       passage_offsets, p.total_passages, p.total_tokens, kbar, s);
 }
 
-int edge_slices(const skip_problem_t& p) { return (p.d + kEdSlice - 1) / kEdSlice; }
+int edge_slices(const skip_problem_t& p) { return (p.d + kEdCols - 1) / kEdCols; }
 
 hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
                            const int32_t* kept_offsets, const int32_t* query_passages,
                            const double* kbar, const float* passage_keys, EdgePartials ep,
                            hipStream_t s) {
   if (p.k_max <= 0 || p.P_max <= 0) return hipSuccess;
-  const int S = edge_slices(p);
-  const int n_pt = (p.P_max + kEdPT - 1) / kEdPT;
-  dim3 grid(S, ((p.k_max + kEdRows - 1) / kEdRows) * n_pt, p.B);
+  EdgeDotArgs a;
+  a.kept_idx = q.kept_idx;
+  a.N = q.N;
+  a.kept_offsets = kept_offsets;
+  a.query_passages = query_passages;
+  a.kbar = kbar;
+  a.pkeys = passage_keys;
+  a.d = p.d;
+  a.total_kept = p.total_kept;
+  a.total_passages = p.total_passages;
+  a.k_max = p.k_max;
+  a.P_max = p.P_max;
+  a.B = p.B;
+  a.S = edge_slices(p);
+  a.part = ep.part;
+  a.qn2p = ep.qn2;
+  a.kn2p = ep.kn2;
+  dim3 grid(8 * ((p.B + 7) / 8) * a.S);
   if (p.dtype == SKIP_F32)
-    hipLaunchKernelGGL(edge_dot_kernel<float>, grid, dim3(256), 0, s,
-                       (const float*)q.base, q.kept_idx, q.N, kept_offsets, query_passages,
-                       kbar, passage_keys, p.d, p.total_kept, p.total_passages, p.k_max,
-                       p.P_max, S, n_pt, ep.part, ep.qn2, ep.kn2);
+    hipLaunchKernelGGL(edge_dot_kernel<float>, grid, dim3(256), 0, s, (const float*)q.base, a);
   else
-    hipLaunchKernelGGL(edge_dot_kernel<bf16_t>, grid, dim3(256), 0, s,
-                       (const bf16_t*)q.base, q.kept_idx, q.N, kept_offsets,
-                       query_passages, kbar, passage_keys, p.d, p.total_kept,
-                       p.total_passages, p.k_max, p.P_max, S, n_pt, ep.part, ep.qn2, ep.kn2);
+    hipLaunchKernelGGL(edge_dot_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)q.base, a);
   return hipGetLastError();
 }
 
