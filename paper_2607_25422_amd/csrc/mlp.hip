@@ -83,7 +83,10 @@ __device__ __forceinline__ void unpack8(const u32x4& x, float* out) {
 
 }  // namespace
 
-constexpr int kMlpMT = 128;      // tokens per tile
+// tokens per tile: 3 blocks of 32 (2304 tokens of a question make 24 tiles,
+// so 16 questions x 24 tiles x 2 hidden tiles fill 256 CUs three times over)
+constexpr int kMlpMT = 96;
+constexpr int kMlpMB = kMlpMT / 32;   // 32-token blocks per tile
 constexpr int kMlpKS = 32;       // columns of d per step (v part and v*q part)
 constexpr int kMlpThreads = 512;
 constexpr int kMlpPartial = 128; // hidden units per partial score (the narrowest tile)
@@ -195,8 +198,8 @@ mlp_pack_kernel(const bf16_t* __restrict__ W1, int d, int h, u32x4* __restrict__
   }
 }
 
-// Work item = (question b, 128-token tile, 256-hidden tile); wave w of 8 owns
-// hidden units 32 w .. 32 w + 31 of the tile for all 128 tokens (4 blocks of
+// Work item = (question b, 96-token tile, 256-hidden tile); wave w of 8 owns
+// hidden units 32 w .. 32 w + 31 of the tile for all 96 tokens (3 blocks of
 // 32 x 32, v_mfma_f32_32x32x16_bf16).  Per 32-column step s:
 //   * the v tile V[tile rows, 32 s : 32 s + 32] arrives in a 4-slot LDS ring
 //     by direct global->LDS loads issued 3 steps ahead (16-byte chunks
@@ -216,7 +219,7 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
                  const u32x4* __restrict__ Wp, int h, const bf16_t* __restrict__ qbf,
                  const float* __restrict__ cvec, const float* __restrict__ w2,
                  float* __restrict__ sp, int n_items) {
-  constexpr int A_ELEMS = kMlpMT * kMlpKS;       // 4096 (8 KiB)
+  constexpr int A_ELEMS = kMlpMT * kMlpKS;       // 3072 (6 KiB)
   __shared__ __attribute__((aligned(1024))) bf16_t Ar[kMlpRing * A_ELEMS];
   __shared__ __attribute__((aligned(1024))) bf16_t Hd[2 * A_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t Qs[kMlpMaxD];   // q_bar'_b
@@ -242,14 +245,18 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
   const bf16_t* vsrc = V + ((size_t)b * N + min(i0 + trow, N - 1)) * d + lc_t * 8;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t ar_lds = lds_u32(Ar) + (uint32_t)(wave_s * 1024);
+  // (waves past the tile's rows, 4 * kMlpMT threads and up, copy nothing)
+  const bool v_loader = tid < 4 * kMlpMT;
   auto issue_v = [&](int s) {
-    dma16(vsrc + s * kMlpKS, __builtin_amdgcn_readfirstlane(
-                                 ar_lds + (uint32_t)((s % kMlpRing) * A_ELEMS * 2)));
+    if (v_loader)
+      dma16(vsrc + s * kMlpKS, __builtin_amdgcn_readfirstlane(
+                                   ar_lds + (uint32_t)((s % kMlpRing) * A_ELEMS * 2)));
   };
   // Hadamard tile of step s (this thread's 8 values, same swizzled position;
   // q_bar' comes from LDS so that no vector-memory load joins the counted
   // queue of tile loads)
   auto hadamard_tile = [&](int s) {
+    if (!v_loader) return;
     const u32x4 a = *reinterpret_cast<const u32x4*>(Ar + (s % kMlpRing) * A_ELEMS + tid * 8);
     float q[8];
     unpack8(*reinterpret_cast<const u32x4*>(Qs + s * kMlpKS + lc_t * 8), q);
@@ -264,18 +271,18 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
       for (int kk = 0; kk < 2; ++kk) w[x][kk] = wsrc[(size_t)s * 256 + (x * 2 + kk) * 64];
   };
 
-  mf32x16_t acc[4];
+  mf32x16_t acc[kMlpMB];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < kMlpMB; ++mb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[mb][v] = 0.f;
 
   // A operand offsets (elements) within a tile: block mb, k16 sub-step kk
-  int aoff[2][4];
+  int aoff[2][kMlpMB];
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
+    for (int mb = 0; mb < kMlpMB; ++mb) {
       const int row = mb * 32 + r32;
       aoff[kk][mb] = row * kMlpKS + (((2 * kk + hh) ^ ((row >> 1) & 3)) << 3);
     }
@@ -284,30 +291,31 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
     __builtin_amdgcn_sched_barrier(0);
     const bf16_t* At = Ar + (s % kMlpRing) * A_ELEMS;
     const bf16_t* Ht = Hd + (s & 1) * A_ELEMS;
-    u32x4 a1[2][4], a3[2][4];
+    u32x4 a1[2][kMlpMB], a3[2][kMlpMB];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
+      for (int mb = 0; mb < kMlpMB; ++mb) {
         a1[kk][mb] = *reinterpret_cast<const u32x4*>(At + aoff[kk][mb]);
         a3[kk][mb] = *reinterpret_cast<const u32x4*>(Ht + aoff[kk][mb]);
       }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
+      for (int mb = 0; mb < kMlpMB; ++mb) {
         acc[mb] = mfma_bf16(a1[kk][mb], w[0][kk], acc[mb]);
         acc[mb] = mfma_bf16(a3[kk][mb], w[1][kk], acc[mb]);
       }
-    // Schedule: eight operand reads ahead, then one MFMA per read, so the
+    // Schedule: half the operand reads ahead, then one MFMA per read, so the
     // read latency hides behind the matrix pipe.
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    constexpr int NR = 4 * kMlpMB;             // operand reads (= MFMAs / 2)
+    __builtin_amdgcn_sched_group_barrier(0x100, NR / 2, 0);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < NR / 2; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 3 * NR / 2, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -358,9 +366,9 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
   const int j = j0 + wave * 32 + r32;
   const float c = cvec[(size_t)b * h + j];
   const float wv = w2[j];
-  float rs[4][16];
+  float rs[kMlpMB][16];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < kMlpMB; ++mb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       float x = fmaxf(acc[mb][v] + c, 0.f) * wv;
@@ -372,7 +380,7 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
   float* red = reinterpret_cast<float*>(Ar);         // [8][128]
   if (r32 == 0) {
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
+    for (int mb = 0; mb < kMlpMB; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
         red[wave * kMlpMT + mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3)] = rs[mb][v];
