@@ -12,7 +12,7 @@
 //                      gathered through kept_idx as they are loaded; each
 //                      wave's weight fragments come straight from the packed
 //                      copy into registers two steps ahead; 8 waves of 32
-//                      output columns x 128 rows (4 blocks of 32 x 32)
+//                      output columns x 96 rows (3 blocks of 32 x 32)
 #include "skip_common.h"
 #include "skip_internal.h"
 
@@ -55,7 +55,10 @@ __device__ __forceinline__ void pbarrier() {
 
 }  // namespace
 
-constexpr int kProjMT = 128;       // rows per tile
+// rows per tile: 3 blocks of 32 (3072 kept rows make 32 tiles, so with 16
+// column tiles 512 items fill 256 CUs twice over)
+constexpr int kProjMT = 96;
+constexpr int kProjMB = kProjMT / 32;     // 32-row blocks per tile
 constexpr int kProjNT = 256;       // output columns per tile (8 waves x 32)
 constexpr int kProjKS = 32;        // columns of d per step
 constexpr int kProjThreads = 512;
@@ -91,7 +94,7 @@ __global__ void __launch_bounds__(kProjThreads)
 proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ kept_offsets,
                  const int32_t* __restrict__ kept_idx, int B, int N, int M, int d, int d_out,
                  const u32x4* __restrict__ Wp, void* __restrict__ Y, int n_items) {
-  constexpr int A_ELEMS = kProjMT * kProjKS;          // 4096 (8 KiB)
+  constexpr int A_ELEMS = kProjMT * kProjKS;          // 3072 (6 KiB)
   __shared__ __attribute__((aligned(1024))) bf16_t Ar[kProjRing * A_ELEMS];
 
   const int per_xcd = gridDim.x / 8;
@@ -125,9 +128,12 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
   const bf16_t* asrc = rows + rid * d + lc * 8;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t ar_lds = plds_u32(Ar) + (uint32_t)(wave_s * 1024);
+  // (waves past the tile's rows, 4 * kProjMT threads and up, copy nothing)
+  const bool a_loader = tid < 4 * kProjMT;
   auto issue_a = [&](int s) {
-    pdma16(asrc + s * kProjKS, __builtin_amdgcn_readfirstlane(
-                                   ar_lds + (uint32_t)((s % kProjRing) * A_ELEMS * 2)));
+    if (a_loader)
+      pdma16(asrc + s * kProjKS, __builtin_amdgcn_readfirstlane(
+                                     ar_lds + (uint32_t)((s % kProjRing) * A_ELEMS * 2)));
   };
   const u32x4* wsrc = Wp + ((size_t)(nt * 8 + wave) * ksteps) * 128 + lane;
   auto load_w = [&](int s, u32x4 (&w)[2]) {
@@ -135,17 +141,17 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
     for (int kk = 0; kk < 2; ++kk) w[kk] = wsrc[(size_t)s * 128 + kk * 64];
   };
 
-  pf32x16_t acc[4];
+  pf32x16_t acc[kProjMB];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < kProjMB; ++mb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[mb][v] = 0.f;
 
-  int aoff[2][4];
+  int aoff[2][kProjMB];
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
+    for (int mb = 0; mb < kProjMB; ++mb) {
       const int row = mb * 32 + r32;
       aoff[kk][mb] = row * kProjKS + (((2 * kk + hh) ^ ((row >> 1) & 3)) << 3);
     }
@@ -153,23 +159,24 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
   auto mma_step = [&](int s, const u32x4 (&w)[2]) {
     __builtin_amdgcn_sched_barrier(0);
     const bf16_t* At = Ar + (s % kProjRing) * A_ELEMS;
-    u32x4 a[2][4];
+    u32x4 a[2][kProjMB];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) a[kk][mb] = *reinterpret_cast<const u32x4*>(At + aoff[kk][mb]);
+      for (int mb = 0; mb < kProjMB; ++mb) a[kk][mb] = *reinterpret_cast<const u32x4*>(At + aoff[kk][mb]);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) acc[mb] = pmfma(a[kk][mb], w[kk], acc[mb]);
-    // four operand reads ahead, then one MFMA per read
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+      for (int mb = 0; mb < kProjMB; ++mb) acc[mb] = pmfma(a[kk][mb], w[kk], acc[mb]);
+    // half the operand reads ahead, then one MFMA per read
+    constexpr int NR = 2 * kProjMB;          // operand reads (= MFMAs)
+    __builtin_amdgcn_sched_group_barrier(0x100, NR / 2, 0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NR / 2; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NR / 2, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -207,7 +214,7 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
   // column j0 + 32*wave + r32.
   const int j = j0 + wave * 32 + r32;
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < kProjMB; ++mb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int row = i0 + mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
