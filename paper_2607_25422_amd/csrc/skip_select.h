@@ -21,9 +21,13 @@
 
 namespace skip {
 
+// Histograms and pass results alternate between two copies, so that a pass
+// takes two barriers: the next pass's histogram is cleared while this one is
+// filled (its last reader, the previous pass's scan, is past a barrier), and
+// a pass's result is not overwritten until two passes later.
 struct SelectShared {
-  uint32_t hist[256];
-  uint32_t misc[4];
+  uint32_t hist[2][256];
+  uint32_t misc[2][4];
   uint32_t scan[20];
 };
 
@@ -36,23 +40,26 @@ __device__ uint32_t block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int
   if (kk <= 0) return 0u;
   if (kk >= n) return all;
 
+  for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[0][i] = 0u;
+  __syncthreads();
   uint64_t prefix = 0, mask = 0;
   uint32_t need = (uint32_t)kk;
   bool whole_bucket = false;
   for (int pass = 0; pass < 8; ++pass) {
     const int shift = 56 - 8 * pass;
-    for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[i] = 0u;
-    __syncthreads();
+    uint32_t* hist = sh->hist[pass & 1];
+    uint32_t* misc = sh->misc[pass & 1];
 #pragma unroll
     for (int j = 0; j < MAXPT; ++j) {
       if (j < cnt && (keys[j] & mask) == prefix)
-        atomicAdd(&sh->hist[(uint32_t)(keys[j] >> shift) & 255u], 1u);
+        atomicAdd(&hist[(uint32_t)(keys[j] >> shift) & 255u], 1u);
     }
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[(pass + 1) & 1][i] = 0u;
     __syncthreads();
     if (threadIdx.x < kWave) {
       const int l = threadIdx.x;
-      const uint32_t h0 = sh->hist[255 - 4 * l], h1 = sh->hist[254 - 4 * l];
-      const uint32_t h2 = sh->hist[253 - 4 * l], h3 = sh->hist[252 - 4 * l];
+      const uint32_t h0 = hist[255 - 4 * l], h1 = hist[254 - 4 * l];
+      const uint32_t h2 = hist[253 - 4 * l], h3 = hist[252 - 4 * l];
       const uint32_t s = h0 + h1 + h2 + h3;
       uint32_t inc = s;
 #pragma unroll
@@ -73,14 +80,13 @@ __device__ uint32_t block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int
         } else {
           c += h0 + h1 + h2; bin = 252 - 4 * l; inbin = h3;
         }
-        sh->misc[0] = bin;
-        sh->misc[1] = c;        // candidates with a larger digit: all taken
-        sh->misc[2] = inbin;    // candidates with exactly this digit
+        misc[0] = bin;
+        misc[1] = c;        // candidates with a larger digit: all taken
+        misc[2] = inbin;    // candidates with exactly this digit
       }
     }
     __syncthreads();
-    const uint32_t bin = sh->misc[0], above = sh->misc[1], inbin = sh->misc[2];
-    __syncthreads();
+    const uint32_t bin = misc[0], above = misc[1], inbin = misc[2];
     need -= above;
     prefix |= (uint64_t)bin << shift;
     mask |= 0xffull << shift;
