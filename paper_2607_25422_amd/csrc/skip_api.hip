@@ -31,6 +31,11 @@ skip_status_t check_common(const skip_problem_t* p) {
   return SKIP_OK;
 }
 
+// Element arrays are read with 16-byte vector and direct-to-LDS loads: a
+// misaligned array is an argument error (NULL passes; required pointers are
+// checked separately).
+static bool al16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
+
 static_assert(sizeof(skip_problem_t) == 88 && offsetof(skip_problem_t, avg_degree) == 56 &&
                   offsetof(skip_problem_t, edge_rule) == 72 &&
                   offsetof(skip_problem_t, edge_beta) == 80,
@@ -149,6 +154,7 @@ skip_status_t skip_prune_topk(const skip_problem_t* p, const void* V, const void
   if (st != SKIP_OK) return st;
   if (!V || !Qtok || !q_offsets || !kept_offsets || !workspace) return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && !kept_idx) return SKIP_ERR_INVALID_ARG;
+  if (!al16(V) || !al16(Qtok) || !al16(w_bias) || !al16(V_kept)) return SKIP_ERR_INVALID_ARG;
   if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Workspace w = carve_workspace(*p, workspace);
@@ -192,6 +198,7 @@ skip_status_t skip_prune_topk_mlp(const skip_problem_t* p, const skip_qvs_mlp_t*
   if (mlp->reserved != 0 || !mlp->W1 || !mlp->w2 || mlp->hidden <= 0 ||
       !std::isfinite(mlp->b2))
     return SKIP_ERR_INVALID_ARG;
+  if (!al16(V) || !al16(Qtok) || !al16(V_kept) || !al16(mlp->W1)) return SKIP_ERR_INVALID_ARG;
   if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || !mlp_shape_ok(mlp)) return SKIP_ERR_UNSUPPORTED;
   if ((int64_t)mlp->hidden * 3 * p->d > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
   const size_t need = workspace_size(*p) + mlp_scratch_bytes(*p, mlp->hidden);
@@ -223,6 +230,8 @@ static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh, const v
     return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && (!Qh || !O)) return SKIP_ERR_INVALID_ARG;
   if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
+  if (!al16(Qh) || !al16(edge_rows) || !al16(Kh) || !al16(Vh) || !al16(O))
+    return SKIP_ERR_INVALID_ARG;
   const bool given = edge_rowptr || edge_col;
   if (given && (!edge_rowptr || (!edge_col && p->total_edges > 0))) return SKIP_ERR_INVALID_ARG;
   if ((edge_rowptr_out == nullptr) != (edge_col_out == nullptr)) return SKIP_ERR_INVALID_ARG;
@@ -380,6 +389,7 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
   if (p->total_qtok < p->B) return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && !V_kept) return SKIP_ERR_INVALID_ARG;
   if (p->total_passages > 0 && !keep) return SKIP_ERR_INVALID_ARG;
+  if (!al16(Qtok) || !al16(V_kept) || !al16(Kh)) return SKIP_ERR_INVALID_ARG;
   if (!passage_keys && p->total_passages > 0 && (!Kh || !passage_offsets))
     return SKIP_ERR_INVALID_ARG;
   st = check_gate(p, gate);
@@ -416,6 +426,8 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
     return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && (!kept_idx || !O)) return SKIP_ERR_INVALID_ARG;
   if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
+  if (!al16(V) || !al16(Qtok) || !al16(w_bias) || !al16(Kh) || !al16(Vh) || !al16(O))
+    return SKIP_ERR_INVALID_ARG;
   size_t need = workspace_size(*p);
   if (gate) {
     st = check_gate(p, gate);

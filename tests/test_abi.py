@@ -63,9 +63,9 @@ def _problem(b, **kw):
 def test_workspace_bytes(b):
     p = _problem(b)
     n = b.workspace_bytes(p)
-    # u + z + kbar + edge partials (2 slices of 512 columns) + row-norm and
+    # u + z + kbar + edge partials (4 slices of 256 columns) + row-norm and
     # key-norm partials + rowmask, each rounded to 256 bytes
-    S = 2
+    S = 4
     parts = [2 * 1024 * 8, 2 * 576 * 8, 3 * 1024 * 8, 2 * S * 96 * 2 * 8, 2 * S * 96 * 8,
              2 * S * 2 * 8, 192 * 8]
     assert n == sum((x + 255) // 256 * 256 for x in parts)
@@ -173,6 +173,28 @@ def test_xattn_rejects_bad_arguments(b):
         assert _xattn(b, q) == b.SKIP_ERR_INVALID_ARG, beta
     q = _problem(b, edge_rule="question", edge_beta=0.0)    # beta unused: accepted
     assert _xattn(b, q, ws_bytes=0) == b.SKIP_ERR_WORKSPACE
+
+
+def test_misaligned_element_arrays_are_rejected(b):
+    """Element arrays are read with 16-byte vector and direct-to-LDS loads:
+    each one shifted by 8 bytes is an argument error, found before anything
+    is enqueued."""
+    MIS = FAKE + 8
+    p = _problem(b)
+    for name in ("V", "Qtok", "w", "vk"):
+        assert _prune(b, p, **{name: MIS}) == b.SKIP_ERR_INVALID_ARG, name
+    for name in ("Qh", "Kh", "Vh", "O"):
+        assert _xattn(b, p, **{name: MIS}) == b.SKIP_ERR_INVALID_ARG, name
+
+    def fused(V=FAKE, Qtok=FAKE, w=None, Kh=FAKE, Vh=FAKE, O=FAKE):
+        return b.LIB.skip_route_fused(ctypes.byref(p), V, Qtok, FAKE, w, FAKE, Kh, Vh, FAKE,
+                                      FAKE, None, FAKE, O, None, FAKE, 1 << 30, None)
+    for name in ("V", "Qtok", "w", "Kh", "Vh", "O"):
+        assert fused(**{name: MIS}) == b.SKIP_ERR_INVALID_ARG, name
+    m = b.SkipQvsMlp(512, 0, MIS, None, FAKE, 0.5)
+    assert b.LIB.skip_prune_topk_mlp(ctypes.byref(p), ctypes.byref(m), FAKE, FAKE, FAKE, FAKE,
+                                     FAKE, None, None, FAKE, 1 << 30, None) \
+        == b.SKIP_ERR_INVALID_ARG                                          # W1
 
 
 def test_fused_requires_matching_head_split(b):
