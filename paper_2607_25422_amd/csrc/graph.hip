@@ -22,14 +22,6 @@
 
 namespace skip {
 
-template <typename T> __device__ __forceinline__ float elem_f32(const T* p, size_t i);
-template <> __device__ __forceinline__ float elem_f32<float>(const float* p, size_t i) {
-  return p[i];
-}
-template <> __device__ __forceinline__ float elem_f32<bf16_t>(const bf16_t* p, size_t i) {
-  return bf16_to_f32(p[i]);
-}
-
 // ---------------------------------------------------------------------------
 // Edge dot products on the float64 matrix cores, split over d.
 // Workgroup = (256-column slice, question), one workgroup per CU over the

@@ -14,9 +14,8 @@
 // In a step the slice workgroups of a question write their partial dot
 // products v_i . c_r and squared norms |c_r|^2 over their columns (coherent
 // stores); the last of them to finish (a counter) sums the partials in slice
-// order and assigns
-// every row by argmin_r |c_r|^2 - 2 v_i . c_r, which is |v_i - c_r|^2 less the
-// row's own |v_i|^2.
+// order and assigns every row by argmin_r |c_r|^2 - 2 v_i . c_r, which is
+// |v_i - c_r|^2 less the row's own |v_i|^2.
 #include "skip_common.h"
 #include "skip_internal.h"
 
