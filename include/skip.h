@@ -68,7 +68,7 @@
 extern "C" {
 #endif
 
-#define SKIP_ABI_VERSION 2
+#define SKIP_ABI_VERSION 3
 
 typedef enum skip_status {
   SKIP_OK = 0,
@@ -301,6 +301,23 @@ skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
                                   const int32_t* kept_offsets, const int32_t* kept_idx,
                                   const void* W, int32_t d_out, void* Y, int32_t out_f32,
                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The same projection in two calls, for callers that apply one W to many
+ * batches: skip_pack_projection writes W repacked for the matrix cores into a
+ * caller buffer of skip_workspace_bytes_project bytes (16-byte aligned), and
+ * skip_gather_project_packed multiplies with it, Y bitwise equal to what
+ * skip_gather_project gives.  The packed copy is an opaque layout of this
+ * ABI version, valid for the d of the problem and the d_out it was packed
+ * for; the caller owns it and may reuse it until it changes W.  Errors as for
+ * skip_gather_project (a short packed buffer: SKIP_ERR_WORKSPACE).
+ */
+skip_status_t skip_pack_projection(const skip_problem_t* p, const void* W, int32_t d_out,
+                                   void* packed, size_t packed_bytes, void* stream);
+skip_status_t skip_gather_project_packed(const skip_problem_t* p, const void* rows,
+                                         const int32_t* kept_offsets, const int32_t* kept_idx,
+                                         const void* packed, int32_t d_out, void* Y,
+                                         int32_t out_f32, void* stream);
 
 /*
  * Regions of the kept tokens (Sec. 3.4: the approximate k-means with which

@@ -33,7 +33,8 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_bipartite_xattn_masked", "skip_route_fused_gated",
                 "skip_workspace_bytes_regions", "skip_region_kmeans",
                 "skip_workspace_bytes_project", "skip_gather_project",
-                "skip_bipartite_xattn_proj")
+                "skip_bipartite_xattn_proj", "skip_pack_projection",
+                "skip_gather_project_packed")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -134,6 +135,11 @@ def _load() -> ctypes.CDLL:
     lib.skip_gather_project.restype = ctypes.c_int
     lib.skip_gather_project.argtypes = [P, vp, i32p, i32p, vp, ctypes.c_int32, vp,
                                         ctypes.c_int32, vp, ctypes.c_size_t, vp]
+    lib.skip_pack_projection.restype = ctypes.c_int
+    lib.skip_pack_projection.argtypes = [P, vp, ctypes.c_int32, vp, ctypes.c_size_t, vp]
+    lib.skip_gather_project_packed.restype = ctypes.c_int
+    lib.skip_gather_project_packed.argtypes = [P, vp, i32p, i32p, vp, ctypes.c_int32, vp,
+                                               ctypes.c_int32, vp]
     lib.skip_bipartite_xattn_proj.restype = ctypes.c_int
     lib.skip_bipartite_xattn_proj.argtypes = [P, vp, vp, i32p, vp, vp, i32p, i32p, vp, vp, vp,
                                               vp, i32p, i32p, vp, ctypes.c_size_t, vp]
@@ -456,6 +462,26 @@ def skip_gather_project(p: SkipProblem, rows, kept_offsets, kept_idx, W, Y, out_
     _check(st, "skip_gather_project")
 
 
+def skip_pack_projection(p: SkipProblem, W, packed, stream=None):
+    d_out = int(W.shape[0])
+    st = LIB.skip_pack_projection(ctypes.byref(p), _ptr(W, "W", _elem_dtype(p), d_out * p.d),
+                                  d_out, packed.data_ptr(), packed.numel(), _stream(stream))
+    _check(st, "skip_pack_projection")
+
+
+def skip_gather_project_packed(p: SkipProblem, rows, kept_offsets, kept_idx, packed, d_out, Y,
+                               out_f32=False, stream=None):
+    et = _elem_dtype(p)
+    n_rows = p.B * p.N if kept_idx is not None else p.total_kept
+    st = LIB.skip_gather_project_packed(
+        ctypes.byref(p), _ptr(rows, "rows", et, n_rows * p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept), packed.data_ptr(), int(d_out),
+        _ptr(Y, "Y", torch.float32 if out_f32 else et, p.total_kept * d_out),
+        1 if out_f32 else 0, _stream(stream))
+    _check(st, "skip_gather_project_packed")
+
+
 def skip_bipartite_xattn_proj(p: SkipProblem, Qh, edge_rows, kept_offsets, Kh, Vh,
                               passage_offsets, query_passages, passage_keys, O, lse=None,
                               passage_keep=None, edge_rowptr_out=None, edge_col_out=None,
@@ -737,6 +763,26 @@ def gather_project(db: DeviceBatch, rows: torch.Tensor, W: torch.Tensor, kept_id
                     dtype=torch.float32 if out_f32 else db.V.dtype, device=db.V.device)
     skip_gather_project(p, rows if p.total_kept else None, db.kept_offsets, kept_idx, W,
                         Y if p.total_kept else None, out_f32, workspace)
+    return Y[:p.total_kept]
+
+
+def pack_projection(db: DeviceBatch, W: torch.Tensor) -> torch.Tensor:
+    """W [d_out, d] bf16 repacked for the matrix cores, for
+    ``gather_project_packed`` (a uint8 tensor owned by the caller)."""
+    packed = torch.empty(workspace_bytes_project(db.p, int(W.shape[0])), dtype=torch.uint8,
+                         device=W.device)
+    skip_pack_projection(db.p, W, packed)
+    return packed
+
+
+def gather_project_packed(db: DeviceBatch, rows: torch.Tensor, packed: torch.Tensor, d_out: int,
+                          kept_idx=None, out_f32=False):
+    """``gather_project`` with weights packed once by ``pack_projection``."""
+    p = db.p
+    Y = torch.empty((max(p.total_kept, 1), int(d_out)),
+                    dtype=torch.float32 if out_f32 else db.V.dtype, device=db.V.device)
+    skip_gather_project_packed(p, rows if p.total_kept else None, db.kept_offsets, kept_idx,
+                               packed, d_out, Y if p.total_kept else None, out_f32)
     return Y[:p.total_kept]
 
 

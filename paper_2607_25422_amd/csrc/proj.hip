@@ -231,18 +231,21 @@ size_t proj_scratch_bytes(int d, int d_out) {
   return ((size_t)d_out * d * sizeof(bf16_t) + 255) & ~(size_t)255;
 }
 
-hipError_t launch_project(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
-                          const int32_t* kept_idx, const void* W, int d_out, void* Y,
-                          int out_f32, void* scratch, hipStream_t s) {
+hipError_t launch_proj_pack(int d, int d_out, const void* W, void* packed, hipStream_t s) {
+  hipLaunchKernelGGL(proj_pack_kernel, dim3(kProjPackBlocks), dim3(256), 0, s,
+                     (const bf16_t*)W, d, d_out, static_cast<u32x4*>(packed));
+  return hipGetLastError();
+}
+
+hipError_t launch_proj_gemm(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
+                            const int32_t* kept_idx, const void* packed, int d_out, void* Y,
+                            int out_f32, hipStream_t s) {
   const int M = p.total_kept;
   if (M <= 0) return hipSuccess;
-  u32x4* Wp = static_cast<u32x4*>(scratch);
-  hipLaunchKernelGGL(proj_pack_kernel, dim3(kProjPackBlocks), dim3(256), 0, s,
-                     (const bf16_t*)W, p.d, d_out, Wp);
   const int n_items = ((M + kProjMT - 1) / kProjMT) * (d_out / kProjNT);
   const int grid = ((n_items + 7) / 8) * 8;
   const bf16_t* R = static_cast<const bf16_t*>(rows);
-  const u32x4* Wc = Wp;
+  const u32x4* Wc = static_cast<const u32x4*>(packed);
   if (kept_idx) {
     if (out_f32)
       hipLaunchKernelGGL((proj_gemm_kernel<true, true>), dim3(grid), dim3(kProjThreads), 0, s,
@@ -259,6 +262,15 @@ hipError_t launch_project(const skip_problem_t& p, const void* rows, const int32
                          R, kept_offsets, kept_idx, p.B, p.N, M, p.d, d_out, Wc, Y, n_items);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_project(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
+                          const int32_t* kept_idx, const void* W, int d_out, void* Y,
+                          int out_f32, void* scratch, hipStream_t s) {
+  if (p.total_kept <= 0) return hipSuccess;
+  hipError_t e = launch_proj_pack(p.d, d_out, W, scratch, s);
+  if (e != hipSuccess) return e;
+  return launch_proj_gemm(p, rows, kept_offsets, kept_idx, scratch, d_out, Y, out_f32, s);
 }
 
 }  // namespace skip

@@ -320,27 +320,60 @@ skip_status_t skip_workspace_bytes_project(const skip_problem_t* p, int32_t d_ou
   return SKIP_OK;
 }
 
-skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
-                                  const int32_t* kept_offsets, const int32_t* kept_idx,
-                                  const void* W, int32_t d_out, void* Y, int32_t out_f32,
-                                  void* workspace, size_t workspace_bytes, void* stream) {
+// Shared argument checks of the projection calls (W: the weights, or their
+// packed copy).
+static skip_status_t check_project(const skip_problem_t* p, const void* rows,
+                                   const int32_t* kept_offsets, const int32_t* kept_idx,
+                                   const void* W, int32_t d_out, const void* Y,
+                                   int32_t out_f32) {
   skip_status_t st = check_common(p);
   if (st != SKIP_OK) return st;
-  if (!W || !workspace || (out_f32 != 0 && out_f32 != 1) || d_out <= 0)
-    return SKIP_ERR_INVALID_ARG;
+  if (!W || (out_f32 != 0 && out_f32 != 1) || d_out <= 0) return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && (!rows || !Y)) return SKIP_ERR_INVALID_ARG;
   if (kept_idx && !kept_offsets) return SKIP_ERR_INVALID_ARG;
-  if (reinterpret_cast<uintptr_t>(W) % 16 != 0 || reinterpret_cast<uintptr_t>(rows) % 16 != 0)
-    return SKIP_ERR_INVALID_ARG;
+  if (!al16(W) || !al16(rows) || !al16(Y)) return SKIP_ERR_INVALID_ARG;
   if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || d_out % 256 != 0 || d_out > 65536)
     return SKIP_ERR_UNSUPPORTED;
   if (kept_idx) {
     if (p->N < 1 || p->k_max > p->N) return SKIP_ERR_INVALID_ARG;
     if ((int64_t)p->B * p->N > INT32_MAX) return SKIP_ERR_UNSUPPORTED;
   }
+  return SKIP_OK;
+}
+
+skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
+                                  const int32_t* kept_offsets, const int32_t* kept_idx,
+                                  const void* W, int32_t d_out, void* Y, int32_t out_f32,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  skip_status_t st = check_project(p, rows, kept_offsets, kept_idx, W, d_out, Y, out_f32);
+  if (st != SKIP_OK) return st;
+  if (!workspace || !al16(workspace)) return SKIP_ERR_INVALID_ARG;
   if (workspace_bytes < proj_scratch_bytes(p->d, d_out)) return SKIP_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   SKIP_TRY(launch_project(*p, rows, kept_offsets, kept_idx, W, d_out, Y, out_f32, workspace, s));
+  return SKIP_OK;
+}
+
+skip_status_t skip_pack_projection(const skip_problem_t* p, const void* W, int32_t d_out,
+                                   void* packed, size_t packed_bytes, void* stream) {
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (!W || !packed || d_out <= 0 || !al16(W) || !al16(packed)) return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || d_out % 256 != 0 || d_out > 65536)
+    return SKIP_ERR_UNSUPPORTED;
+  if (packed_bytes < proj_scratch_bytes(p->d, d_out)) return SKIP_ERR_WORKSPACE;
+  SKIP_TRY(launch_proj_pack(p->d, d_out, W, packed, static_cast<hipStream_t>(stream)));
+  return SKIP_OK;
+}
+
+skip_status_t skip_gather_project_packed(const skip_problem_t* p, const void* rows,
+                                         const int32_t* kept_offsets, const int32_t* kept_idx,
+                                         const void* packed, int32_t d_out, void* Y,
+                                         int32_t out_f32, void* stream) {
+  skip_status_t st = check_project(p, rows, kept_offsets, kept_idx, packed, d_out, Y, out_f32);
+  if (st != SKIP_OK) return st;
+  SKIP_TRY(launch_proj_gemm(*p, rows, kept_offsets, kept_idx, packed, d_out, Y, out_f32,
+                            static_cast<hipStream_t>(stream)));
   return SKIP_OK;
 }
 

@@ -75,6 +75,10 @@ hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const
 
 // Learned projection of the kept rows --------------------------------------
 size_t proj_scratch_bytes(int d, int d_out);
+hipError_t launch_proj_pack(int d, int d_out, const void* W, void* packed, hipStream_t s);
+hipError_t launch_proj_gemm(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
+                            const int32_t* kept_idx, const void* packed, int d_out, void* Y,
+                            int out_f32, hipStream_t s);
 hipError_t launch_project(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
                           const int32_t* kept_idx, const void* W, int d_out, void* Y,
                           int out_f32, void* scratch, hipStream_t s);

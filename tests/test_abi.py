@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol(b):
 
 
 def test_version_and_status_strings(b):
-    assert b.abi_version() == 2
+    assert b.abi_version() == 3
     for s in range(5):
         assert b.status_string(s).startswith("SKIP_")
     assert "UNKNOWN" in b.status_string(99)
@@ -320,6 +320,25 @@ def test_projection_and_edge_rows_validation(b):
     q = b.make_problem("f32", B=2, N=576, d=1024, q_offsets=[0, 3, 7], kept_offsets=[0, 96, 192])
     assert proj(q) == b.SKIP_ERR_UNSUPPORTED
     assert proj(p, ws_bytes=n - 1) == b.SKIP_ERR_WORKSPACE
+
+    # packing once and multiplying with the packed copy
+    def pack(q, W=FAKE, d_out=256, packed=FAKE, nbytes=1 << 30):
+        return b.LIB.skip_pack_projection(ctypes.byref(q), W, d_out, packed, nbytes, None)
+    assert pack(p, W=None) == b.SKIP_ERR_INVALID_ARG
+    assert pack(p, packed=None) == b.SKIP_ERR_INVALID_ARG
+    assert pack(p, packed=FAKE + 8) == b.SKIP_ERR_INVALID_ARG
+    assert pack(p, d_out=300) == b.SKIP_ERR_UNSUPPORTED
+    assert pack(q) == b.SKIP_ERR_UNSUPPORTED
+    assert pack(p, nbytes=n - 1) == b.SKIP_ERR_WORKSPACE
+
+    def packed_call(q, rows=FAKE, packed=FAKE, d_out=256, Y=FAKE, f32=0):
+        return b.LIB.skip_gather_project_packed(ctypes.byref(q), rows, FAKE, None, packed, d_out,
+                                                Y, f32, None)
+    assert packed_call(p, packed=None) == b.SKIP_ERR_INVALID_ARG
+    assert packed_call(p, rows=None) == b.SKIP_ERR_INVALID_ARG
+    assert packed_call(p, Y=FAKE + 2) == b.SKIP_ERR_INVALID_ARG
+    assert packed_call(p, f32=3) == b.SKIP_ERR_INVALID_ARG
+    assert packed_call(p, d_out=512 + 128) == b.SKIP_ERR_UNSUPPORTED
 
     def xp(q, edge=FAKE, keys=FAKE, ws_bytes=0):
         return b.LIB.skip_bipartite_xattn_proj(ctypes.byref(q), FAKE, edge, FAKE, FAKE, FAKE,

@@ -81,6 +81,29 @@ def test_project_small_ragged(B, seed, d_out):
     assert torch.equal(y32.to(torch.bfloat16), y_idx)
 
 
+@pytest.mark.parametrize("d_out", [256, 768])
+def test_project_packed_matches_one_call(B, d_out):
+    """Weights packed once and reused: every output bitwise equal to the
+    one-call projection (bf16 and float outputs, rows in place and through
+    the kept indices), on two batches in a row."""
+    W = wls.make_projection(d_out, 256, 3)
+    Wd = W.cuda()
+    for seed, k in ((3, (0, 5, 64, 130)), (4, (1, 33))):
+        batch = wls.make_batch("llava_bf16", seed, B=len(k), N=300, H=4, d_h=64, T=(1, 3), k=k)
+        say(f"projection packed seed={seed} d_out={d_out} k={batch.k.tolist()}")
+        kept = kept_oracle(batch)
+        db = B.to_device(batch)
+        packed = B.pack_projection(db, Wd)
+        idx = torch.from_numpy(np.concatenate(kept).astype(np.int32)).cuda()
+        rows = kept_rows(batch, kept).cuda()
+        for out_f32 in (False, True):
+            one = B.gather_project(db, db.V, Wd, kept_idx=idx, out_f32=out_f32)
+            two = B.gather_project_packed(db, db.V, packed, d_out, kept_idx=idx, out_f32=out_f32)
+            three = B.gather_project_packed(db, rows, packed, d_out, out_f32=out_f32)
+            torch.cuda.synchronize()
+            assert torch.equal(one, two) and torch.equal(one, three), (seed, out_f32)
+
+
 def test_project_full_size(B):
     """highres_bf16: 3072 kept rows read in place through the kept indices,
     W 4096 x 4096; 64 sampled rows checked against the oracle, all columns."""
