@@ -39,7 +39,8 @@
  *     workspaces.  Calls sharing a workspace must be ordered on one stream.
  *   - Element arrays (V, Qtok, w_bias, Qh, Kh, Vh, O, V_kept) have the element
  *     type given by p->dtype and must be 16-byte aligned; row widths are
- *     multiples of 8 elements.
+ *     multiples of 8 elements.  The float passage_keys table, where given,
+ *     must be 16-byte aligned as well (it is read with 16-byte loads).
  *   - Offsets are int32, ascending, starting at 0; offsets arrays are device
  *     arrays whose last entry must equal the matching total in `p`.
  *     Kernels clamp every offset into its declared total, so inconsistent

@@ -281,9 +281,34 @@ def _stream(stream) -> int:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _ws(p, workspace):
+def _torch_stream(stream):
+    """The torch stream object of a stream argument (None: the current one)."""
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
+def _fresh_workspace(nbytes: int, device, stream=None) -> torch.Tensor:
+    """A workspace allocated for one call on ``stream`` (see _ws)."""
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    s = _torch_stream(stream)
+    if s != torch.cuda.current_stream():
+        ws.record_stream(s)
+    return ws
+
+
+def _ws(p, workspace, stream=None):
+    """The workspace of a call: the caller's, or a fresh one.  A fresh one is
+    released when the call returns, while the kernels may still run on
+    ``stream``; recording that stream on it keeps the caching allocator from
+    handing the memory to other work before they finish."""
     if workspace is None:
         workspace = new_workspace(p)
+        s = _torch_stream(stream)
+        if s != torch.cuda.current_stream():
+            workspace.record_stream(s)
     return workspace, workspace.data_ptr(), workspace.numel()
 
 
@@ -293,7 +318,7 @@ def _ws(p, workspace):
 def skip_prune_topk(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, kept_idx,
                     scores=None, V_kept=None, workspace=None, stream=None):
     et = _elem_dtype(p)
-    ws, wsp, wsn = _ws(p, workspace)
+    ws, wsp, wsn = _ws(p, workspace, stream)
     st = LIB.skip_prune_topk(
         ctypes.byref(p), _ptr(V, "V", et, p.B * p.N * p.d), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
         _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1), _ptr(w_bias, "w_bias", et, p.d),
@@ -309,7 +334,7 @@ def skip_prune_topk_mlp(p: SkipProblem, mlp: "QvsMlp", V, Qtok, q_offsets, kept_
     et = _elem_dtype(p)
     h = mlp.hidden
     if workspace is None:
-        workspace = torch.empty(workspace_bytes_mlp(p, h), dtype=torch.uint8, device=V.device)
+        workspace = _fresh_workspace(workspace_bytes_mlp(p, h), V.device, stream)
     m = SkipQvsMlp(h, 0, _ptr(mlp.W1, "W1", et, h * 3 * p.d), _ptr(mlp.b1, "b1", torch.float32, h),
                    _ptr(mlp.w2, "w2", torch.float32, h), float(mlp.b2))
     st = LIB.skip_prune_topk_mlp(
@@ -329,7 +354,7 @@ def skip_bipartite_xattn(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passage_offse
                          edge_col=None, edge_rowptr_out=None, edge_col_out=None,
                          workspace=None, stream=None):
     et = _elem_dtype(p)
-    ws, wsp, wsn = _ws(p, workspace)
+    ws, wsp, wsn = _ws(p, workspace, stream)
     st = LIB.skip_bipartite_xattn(
         ctypes.byref(p), _ptr(Qh, "Qh", et, p.total_kept * p.d),
         _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
@@ -353,8 +378,7 @@ def skip_skv_gate(p: SkipProblem, gate: "SkvGate", Qtok, q_offsets, V_kept, kept
     et = _elem_dtype(p)
     h = gate.hidden
     if workspace is None:
-        workspace = torch.empty(workspace_bytes_gate(p, h), dtype=torch.uint8,
-                                device=Qtok.device)
+        workspace = _fresh_workspace(workspace_bytes_gate(p, h), Qtok.device, stream)
     g = _gate_struct(p, gate)
     st = LIB.skip_skv_gate(
         ctypes.byref(p), ctypes.byref(g), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
@@ -376,7 +400,7 @@ def skip_bipartite_xattn_masked(p: SkipProblem, Qh, kept_offsets, Kh, Vh, passag
                                 edge_rowptr_out=None, edge_col_out=None, workspace=None,
                                 stream=None):
     et = _elem_dtype(p)
-    ws, wsp, wsn = _ws(p, workspace)
+    ws, wsp, wsn = _ws(p, workspace, stream)
     st = LIB.skip_bipartite_xattn_masked(
         ctypes.byref(p), _ptr(Qh, "Qh", et, p.total_kept * p.d),
         _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
@@ -406,8 +430,7 @@ def skip_route_fused_gated(p: SkipProblem, gate: "SkvGate", V, Qtok, q_offsets, 
                            workspace=None, stream=None):
     et = _elem_dtype(p)
     if workspace is None:
-        workspace = torch.empty(workspace_bytes_gate(p, gate.hidden), dtype=torch.uint8,
-                                device=V.device)
+        workspace = _fresh_workspace(workspace_bytes_gate(p, gate.hidden), V.device, stream)
     g = _gate_struct(p, gate)
     st = LIB.skip_route_fused_gated(
         ctypes.byref(p), ctypes.byref(g), _ptr(V, "V", et, p.B * p.N * p.d),
@@ -431,8 +454,8 @@ def skip_region_kmeans(p: SkipProblem, rows, kept_offsets, kept_idx, r_max, n_it
                        centroids, sizes=None, workspace=None, stream=None):
     et = _elem_dtype(p)
     if workspace is None:
-        workspace = torch.empty(max(workspace_bytes_regions(p, r_max), 256), dtype=torch.uint8,
-                                device=centroids.device)
+        workspace = _fresh_workspace(workspace_bytes_regions(p, r_max), centroids.device,
+                                     stream)
     n_rows = p.B * p.N if kept_idx is not None else p.total_kept
     st = LIB.skip_region_kmeans(
         ctypes.byref(p), _ptr(rows, "rows", et, n_rows * p.d),
@@ -450,8 +473,7 @@ def skip_gather_project(p: SkipProblem, rows, kept_offsets, kept_idx, W, Y, out_
     et = _elem_dtype(p)
     d_out = int(W.shape[0])
     if workspace is None:
-        workspace = torch.empty(workspace_bytes_project(p, d_out), dtype=torch.uint8,
-                                device=W.device)
+        workspace = _fresh_workspace(workspace_bytes_project(p, d_out), W.device, stream)
     n_rows = p.B * p.N if kept_idx is not None else p.total_kept
     st = LIB.skip_gather_project(
         ctypes.byref(p), _ptr(rows, "rows", et, n_rows * p.d),
@@ -487,7 +509,7 @@ def skip_bipartite_xattn_proj(p: SkipProblem, Qh, edge_rows, kept_offsets, Kh, V
                               passage_keep=None, edge_rowptr_out=None, edge_col_out=None,
                               workspace=None, stream=None):
     et = _elem_dtype(p)
-    ws, wsp, wsn = _ws(p, workspace)
+    ws, wsp, wsn = _ws(p, workspace, stream)
     st = LIB.skip_bipartite_xattn_proj(
         ctypes.byref(p), _ptr(Qh, "Qh", et, p.total_kept * p.d),
         _ptr(edge_rows, "edge_rows", et, p.total_kept * p.d),
@@ -511,7 +533,7 @@ def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, K
     """``stage_events``: a StageEvents set to time each kernel stage (calls
     skip_route_fused_profiled)."""
     et = _elem_dtype(p)
-    ws, wsp, wsn = _ws(p, workspace)
+    ws, wsp, wsn = _ws(p, workspace, stream)
     if stage_events is None:
         fn, extra = LIB.skip_route_fused, ()
     else:

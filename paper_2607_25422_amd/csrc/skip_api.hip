@@ -230,7 +230,8 @@ static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh, const v
     return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && (!Qh || !O)) return SKIP_ERR_INVALID_ARG;
   if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
-  if (!al16(Qh) || !al16(edge_rows) || !al16(Kh) || !al16(Vh) || !al16(O))
+  if (!al16(Qh) || !al16(edge_rows) || !al16(Kh) || !al16(Vh) || !al16(O) ||
+      !al16(passage_keys))
     return SKIP_ERR_INVALID_ARG;
   const bool given = edge_rowptr || edge_col;
   if (given && (!edge_rowptr || (!edge_col && p->total_edges > 0))) return SKIP_ERR_INVALID_ARG;
@@ -422,7 +423,8 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
   if (p->total_qtok < p->B) return SKIP_ERR_INVALID_ARG;
   if (p->total_kept > 0 && !V_kept) return SKIP_ERR_INVALID_ARG;
   if (p->total_passages > 0 && !keep) return SKIP_ERR_INVALID_ARG;
-  if (!al16(Qtok) || !al16(V_kept) || !al16(Kh)) return SKIP_ERR_INVALID_ARG;
+  if (!al16(Qtok) || !al16(V_kept) || !al16(Kh) || !al16(passage_keys))
+    return SKIP_ERR_INVALID_ARG;
   if (!passage_keys && p->total_passages > 0 && (!Kh || !passage_offsets))
     return SKIP_ERR_INVALID_ARG;
   st = check_gate(p, gate);
@@ -440,6 +442,26 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
   return SKIP_OK;
 }
 
+// Arguments of the fused route other than the workspace (host-side only).
+static skip_status_t check_fused_args(const skip_problem_t* p, const void* V, const void* Qtok,
+                                      const int32_t* q_offsets, const void* w_bias,
+                                      const int32_t* kept_offsets, const void* Kh,
+                                      const void* Vh, const int32_t* passage_offsets,
+                                      const int32_t* query_passages,
+                                      const float* passage_keys, const int32_t* kept_idx,
+                                      const void* O) {
+  skip_status_t st = check(p, kPrune | kGraph);
+  if (st != SKIP_OK) return st;
+  if (!V || !Qtok || !q_offsets || !kept_offsets || !query_passages || !passage_offsets)
+    return SKIP_ERR_INVALID_ARG;
+  if (p->total_kept > 0 && (!kept_idx || !O)) return SKIP_ERR_INVALID_ARG;
+  if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
+  if (!al16(V) || !al16(Qtok) || !al16(w_bias) || !al16(Kh) || !al16(Vh) || !al16(O) ||
+      !al16(passage_keys))
+    return SKIP_ERR_INVALID_ARG;
+  return SKIP_OK;
+}
+
 static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
                                       const void* Qtok, const int32_t* q_offsets,
                                       const void* w_bias, const int32_t* kept_offsets,
@@ -452,15 +474,11 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
                                       const skip_skv_gate_t* gate = nullptr,
                                       uint8_t* passage_keep = nullptr,
                                       float* gate_logits = nullptr) {
-  skip_status_t st = check(p, kPrune | kGraph);
+  skip_status_t st = check_fused_args(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                                      passage_offsets, query_passages, passage_keys, kept_idx,
+                                      O);
   if (st != SKIP_OK) return st;
-  if (!V || !Qtok || !q_offsets || !kept_offsets || !query_passages || !passage_offsets ||
-      !workspace)
-    return SKIP_ERR_INVALID_ARG;
-  if (p->total_kept > 0 && (!kept_idx || !O)) return SKIP_ERR_INVALID_ARG;
-  if (p->total_tokens > 0 && (!Kh || !Vh)) return SKIP_ERR_INVALID_ARG;
-  if (!al16(V) || !al16(Qtok) || !al16(w_bias) || !al16(Kh) || !al16(Vh) || !al16(O))
-    return SKIP_ERR_INVALID_ARG;
+  if (!workspace) return SKIP_ERR_INVALID_ARG;
   size_t need = workspace_size(*p);
   if (gate) {
     st = check_gate(p, gate);

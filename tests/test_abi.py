@@ -186,11 +186,14 @@ def test_misaligned_element_arrays_are_rejected(b):
     for name in ("Qh", "Kh", "Vh", "O"):
         assert _xattn(b, p, **{name: MIS}) == b.SKIP_ERR_INVALID_ARG, name
 
-    def fused(V=FAKE, Qtok=FAKE, w=None, Kh=FAKE, Vh=FAKE, O=FAKE):
+    def fused(V=FAKE, Qtok=FAKE, w=None, Kh=FAKE, Vh=FAKE, pk=None, O=FAKE):
         return b.LIB.skip_route_fused(ctypes.byref(p), V, Qtok, FAKE, w, FAKE, Kh, Vh, FAKE,
-                                      FAKE, None, FAKE, O, None, FAKE, 1 << 30, None)
-    for name in ("V", "Qtok", "w", "Kh", "Vh", "O"):
+                                      FAKE, pk, FAKE, O, None, FAKE, 1 << 30, None)
+    for name in ("V", "Qtok", "w", "Kh", "Vh", "pk", "O"):
         assert fused(**{name: MIS}) == b.SKIP_ERR_INVALID_ARG, name
+    # the float passage-key table is read with 16-byte loads too
+    assert _xattn(b, p, pk=MIS) == b.SKIP_ERR_INVALID_ARG
+    assert _xattn(b, p, pk=FAKE, ws_bytes=0) == b.SKIP_ERR_WORKSPACE     # aligned: passes
     m = b.SkipQvsMlp(512, 0, MIS, None, FAKE, 0.5)
     assert b.LIB.skip_prune_topk_mlp(ctypes.byref(p), ctypes.byref(m), FAKE, FAKE, FAKE, FAKE,
                                      FAKE, None, None, FAKE, 1 << 30, None) \
@@ -251,6 +254,7 @@ def test_gate_struct_and_validation(b):
     assert call(q) == b.SKIP_ERR_UNSUPPORTED                              # bf16 only
     assert call(p, ws_bytes=b.workspace_bytes_gate(p, 256) - 1) == b.SKIP_ERR_WORKSPACE
     assert call(p, Kh=None, pk=FAKE, ws_bytes=0) == b.SKIP_ERR_WORKSPACE  # given keys: no Kh
+    assert call(p, Kh=None, pk=FAKE + 4, ws_bytes=0) == b.SKIP_ERR_INVALID_ARG  # misaligned
     with pytest.raises(b.SkipError):
         b.workspace_bytes_gate(p, 100)
 
