@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define SKIP_ABI_VERSION 3
+#define SKIP_ABI_VERSION 4
 
 typedef enum skip_status {
   SKIP_OK = 0,
@@ -444,6 +444,41 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V,
                                const float* passage_keys, int32_t* kept_idx,
                                void* O, float* lse, void* workspace,
                                size_t workspace_bytes, void* stream);
+
+/*
+ * Largest scratch (in bytes) that skip_route_fused_noalloc can use: problems
+ * whose skip_workspace_bytes() exceeds it are rejected.
+ */
+#define SKIP_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/*
+ * skip_route_fused for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops, harnesses that forbid hipMalloc): the
+ * same route, results bitwise equal to skip_route_fused, with the workspace
+ * taken from a buffer of SKIP_NOALLOC_SCRATCH_BYTES bytes that the library
+ * holds in device memory on every GPU it is loaded on, until the process
+ * ends.  The call allocates and frees nothing.
+ *   - The problem's skip_workspace_bytes() must not exceed
+ *     SKIP_NOALLOC_SCRATCH_BYTES, else SKIP_ERR_WORKSPACE (nothing enqueued).
+ *   - The buffer is per GPU and shared by every call on that GPU: calls on
+ *     one GPU whose executions overlap (different streams, or host threads
+ *     with no ordering between them) race on it and give unspecified
+ *     results.  Order them, e.g. on one stream.  The buffer keeps what the
+ *     last call left; every value the route reads is written by the same
+ *     call first, so nothing needs clearing between calls.
+ *   - `stream` must belong to the current device (SKIP_ERR_INVALID_ARG
+ *     otherwise); the first call on a device looks up the buffer's address
+ *     there (SKIP_ERR_HIP if that fails).
+ * Other arguments and results as in skip_route_fused.
+ */
+skip_status_t skip_route_fused_noalloc(const skip_problem_t* p, const void* V,
+                                       const void* Qtok, const int32_t* q_offsets,
+                                       const void* w_bias, const int32_t* kept_offsets,
+                                       const void* Kh, const void* Vh,
+                                       const int32_t* passage_offsets,
+                                       const int32_t* query_passages,
+                                       const float* passage_keys, int32_t* kept_idx,
+                                       void* O, float* lse, void* stream);
 
 /* Kernel stages of skip_route_fused, in launch order: pooling (questions
  * and passage keys), salience scoring, top-k, edge compatibilities, edge

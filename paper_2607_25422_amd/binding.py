@@ -34,7 +34,7 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_workspace_bytes_regions", "skip_region_kmeans",
                 "skip_workspace_bytes_project", "skip_gather_project",
                 "skip_bipartite_xattn_proj", "skip_pack_projection",
-                "skip_gather_project_packed")
+                "skip_gather_project_packed", "skip_route_fused_noalloc")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
 
 
@@ -143,6 +143,9 @@ def _load() -> ctypes.CDLL:
     lib.skip_bipartite_xattn_proj.restype = ctypes.c_int
     lib.skip_bipartite_xattn_proj.argtypes = [P, vp, vp, i32p, vp, vp, i32p, i32p, vp, vp, vp,
                                               vp, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.skip_route_fused_noalloc.restype = ctypes.c_int
+    lib.skip_route_fused_noalloc.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p, vp,
+                                             i32p, vp, vp, vp]
     lib.skip_route_fused_profiled.restype = ctypes.c_int
     lib.skip_route_fused_profiled.argtypes = [P, vp, vp, i32p, vp, i32p, vp, vp, i32p, i32p,
                                               vp, i32p, vp, vp, vp, ctypes.c_size_t, vp,
@@ -550,6 +553,29 @@ def skip_route_fused(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, K
         _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
         _ptr(lse, "lse", torch.float32, p.total_kept * p.H), wsp, wsn, _stream(stream), *extra)
     _check(st, "skip_route_fused")
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20     # SKIP_NOALLOC_SCRATCH_BYTES
+
+
+def skip_route_fused_noalloc(p: SkipProblem, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                             passage_offsets, query_passages, kept_idx, O, lse=None,
+                             passage_keys=None, stream=None):
+    """skip_route_fused with the library's own device scratch (no workspace
+    argument, nothing allocated by the call)."""
+    et = _elem_dtype(p)
+    st = LIB.skip_route_fused_noalloc(
+        ctypes.byref(p), _ptr(V, "V", et, p.B * p.N * p.d), _ptr(Qtok, "Qtok", et, p.total_qtok * p.d),
+        _ptr(q_offsets, "q_offsets", torch.int32, p.B + 1), _ptr(w_bias, "w_bias", et, p.d),
+        _ptr(kept_offsets, "kept_offsets", torch.int32, p.B + 1),
+        _ptr(Kh, "Kh", et, p.total_tokens * p.d), _ptr(Vh, "Vh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(query_passages, "query_passages", torch.int32, p.B + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(kept_idx, "kept_idx", torch.int32, p.total_kept),
+        _ptr(O, "O", _out_dtype(p), p.total_kept * p.d),
+        _ptr(lse, "lse", torch.float32, p.total_kept * p.H), _stream(stream))
+    _check(st, "skip_route_fused_noalloc")
 
 
 class StageEvents:

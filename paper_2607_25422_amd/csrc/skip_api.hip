@@ -3,6 +3,7 @@
 // include/skip.h.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "skip.h"
 #include "skip_internal.h"
@@ -543,6 +544,69 @@ skip_status_t skip_route_fused(const skip_problem_t* p, const void* V, const voi
   return route_fused_impl(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
                           passage_offsets, query_passages, passage_keys, kept_idx, O, lse,
                           workspace, workspace_bytes, stream, nullptr);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Route without allocation: the workspace is a file-scope device array.  In
+// host code `scratch` names a host-side stand-in, not the device array; its
+// device address is looked up once per device (hipGetSymbolAddress, with that
+// device current) and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[SKIP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];   // device address of `scratch` on each device
+
+// The scratch address on the current device, looked up on first use there.
+hipError_t scratch_address(int dev, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+skip_status_t skip_route_fused_noalloc(const skip_problem_t* p, const void* V, const void* Qtok,
+                                       const int32_t* q_offsets, const void* w_bias,
+                                       const int32_t* kept_offsets, const void* Kh,
+                                       const void* Vh, const int32_t* passage_offsets,
+                                       const int32_t* query_passages,
+                                       const float* passage_keys, int32_t* kept_idx, void* O,
+                                       float* lse, void* stream) {
+  // host-side checks first: a problem that does not fit is rejected before
+  // any HIP call
+  skip_status_t st = check_fused_args(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                                      passage_offsets, query_passages, passage_keys, kept_idx,
+                                      O);
+  if (st != SKIP_OK) return st;
+  if (workspace_size(*p) > (size_t)SKIP_NOALLOC_SCRATCH_BYTES) return SKIP_ERR_WORKSPACE;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SKIP_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SKIP_ERR_UNSUPPORTED;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (s) {
+    int sdev = -1;
+    if (hipStreamGetDevice(s, &sdev) != hipSuccess) return SKIP_ERR_INVALID_ARG;
+    if (sdev != dev) return SKIP_ERR_INVALID_ARG;
+  }
+  void* ws = nullptr;
+  if (scratch_address(dev, &ws) != hipSuccess) return SKIP_ERR_HIP;
+  return route_fused_impl(p, V, Qtok, q_offsets, w_bias, kept_offsets, Kh, Vh,
+                          passage_offsets, query_passages, passage_keys, kept_idx, O, lse, ws,
+                          (size_t)SKIP_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 skip_status_t skip_workspace_bytes_regions(const skip_problem_t* p, int32_t r_max,

@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol(b):
 
 
 def test_version_and_status_strings(b):
-    assert b.abi_version() == 3
+    assert b.abi_version() == 4
     for s in range(5):
         assert b.status_string(s).startswith("SKIP_")
     assert "UNKNOWN" in b.status_string(99)
@@ -351,3 +351,27 @@ def test_projection_and_edge_rows_validation(b):
     assert xp(p, edge=None) == b.SKIP_ERR_INVALID_ARG
     assert xp(p, keys=None) == b.SKIP_ERR_INVALID_ARG
     assert xp(p) == b.SKIP_ERR_WORKSPACE
+
+
+def test_noalloc_route_validation(b):
+    """The route without allocation checks everything on the host first: bad
+    arguments and problems whose workspace exceeds the library's scratch are
+    rejected before any HIP call (no GPU here)."""
+    def call(q, V=FAKE, O=FAKE, pk=None):
+        return b.LIB.skip_route_fused_noalloc(ctypes.byref(q), V, FAKE, FAKE, None, FAKE, FAKE,
+                                              FAKE, FAKE, FAKE, pk, FAKE, O, None, None)
+    p = _problem(b)
+    assert b.workspace_bytes(p) <= b.NOALLOC_SCRATCH_BYTES
+    assert call(p, V=None) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, O=FAKE + 8) == b.SKIP_ERR_INVALID_ARG
+    assert call(p, pk=FAKE + 4) == b.SKIP_ERR_INVALID_ARG
+    assert call(_problem(b, H=8)) == b.SKIP_ERR_INVALID_ARG
+    # 8 questions x 40 passages of width 8192: the float64 passage keys alone
+    # take 21 MB, above the 16 MiB scratch
+    big = b.make_problem("bf16", B=8, N=576, d=8192, H=64, d_h=128,
+                         q_offsets=list(range(0, 9 * 4, 4)),
+                         kept_offsets=list(range(0, 9 * 96, 96)),
+                         passage_offsets=list(range(0, 321 * 16, 16)),
+                         query_passages=list(range(0, 321, 40)), sm_scale=0.125)
+    assert b.workspace_bytes(big) > b.NOALLOC_SCRATCH_BYTES
+    assert call(big) == b.SKIP_ERR_WORKSPACE
