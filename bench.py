@@ -86,7 +86,7 @@ def parse():
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel.highres_bf16.traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_sparse_kernel.highres_bf16.traffic.json")
 ATTN_SOURCE = os.path.join(ROOT, "paper_2607_25422_amd", "csrc", "attn.hip")
 
 
@@ -603,7 +603,7 @@ def main():
                         "p90": round(pct(0.9), 5), "steps": n_prof,
                         "what": "profiled pass: stage events on the stream, after the timed steps"},
         "roofline": {
-            "kernel": "attn_bf16_kernel" if wl.dtype == "bf16" else "attn_f32_kernel",
+            "kernel": "attn_sparse_kernel" if wl.dtype == "bf16" else "attn_f32_kernel",
             "bound": "hbm",
             "achieved": round(attn_gbs, 1),
             "peak": HBM_PEAK_GBS,

@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define SKIP_ABI_VERSION 4
+#define SKIP_ABI_VERSION 5
 
 typedef enum skip_status {
   SKIP_OK = 0,
@@ -482,8 +482,8 @@ skip_status_t skip_route_fused_noalloc(const skip_problem_t* p, const void* V,
 
 /* Kernel stages of skip_route_fused, in launch order: pooling (questions
  * and passage keys), salience scoring, top-k, edge compatibilities, edge
- * selection, attention. */
-#define SKIP_FUSED_STAGES 6
+ * selection, the attention work list (bf16; empty for float32), attention. */
+#define SKIP_FUSED_STAGES 7
 
 /*
  * skip_route_fused with per-stage timing, for profiling harnesses.

@@ -35,7 +35,8 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_workspace_bytes_project", "skip_gather_project",
                 "skip_bipartite_xattn_proj", "skip_pack_projection",
                 "skip_gather_project_packed", "skip_route_fused_noalloc")
-FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attention")
+FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attn_plan",
+                "attention")
 
 
 class SkipError(RuntimeError):

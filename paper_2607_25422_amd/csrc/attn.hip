@@ -5,23 +5,8 @@
 // every passage adjacent to i (one 64-bit neighbour mask per row):
 //   e_m = sm_scale * <Qh[i,h], Kh[m,h]>,  O = softmax(e) . Vh,  LSE = log sum exp e.
 //
-// bf16 path (MFMA).  Work item = (question b, head h, block of <= 256 kept
-// rows), eight waves.  The item walks the passages adjacent to any of its
-// rows, 64 tokens at a time; K and V tiles of head h are staged once per item
-// in an LDS ring and shared by all rows.  Per wave and tile:
-//   S^T (tokens x 32 rows) = K_tile (tokens x d_h) . Q^T   v_mfma_f32_32x32x16_bf16
-//   rows not adjacent to the passage are masked to -inf, online softmax in
-//   fp32 (base-2 exponent), P rounded to bf16,
-//   O^T (d_h x 32 rows) += V_tile^T . P^T                  v_mfma_f32_32x32x16_bf16
-// Computing the transposed products keeps each query row in one lane column,
-// so row statistics need no cross-lane traffic except between the two half
-// waves, and the S^T accumulator is already the P^T operand of the second
-// product.  The V^T operand comes from transposing LDS reads in the token
-// order of the S^T accumulator layout.
-//
-// Work items are laid out so that the row blocks of one (b, h) land on the
-// same XCD (workgroups are dealt round-robin over the 8 XCDs), which keeps
-// re-reads of a K/V tile within one L2.
+// bf16 path (MFMA): passage-major, only the graph's edges are computed (the
+// kernel comment below); a device-built work list orders the items by cost.
 //
 // fp32 path: one wave per (kept row, head); 64 tokens per step, lane = token
 // for the logits, lane = feature for the PV product.
@@ -38,11 +23,6 @@ struct IntC {                     // a compile-time count passed to a generic la
   static constexpr int value = N;
 };
 
-constexpr int kWaves = 8;                 // waves per work item
-constexpr int kThreads = 64 * kWaves;
-constexpr int kMaxRows = 32 * kWaves;     // kept rows per work item
-constexpr int kTile = 64;                 // tokens per K/V tile
-constexpr int kStages = 4;                // K/V tiles resident in LDS
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -59,25 +39,12 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// Wait until at most N of this wave's vector-memory operations are pending
-// (expcnt and lgkmcnt left unconstrained).
-template <int N>
-__device__ __forceinline__ void wait_vmem() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-// Workgroup barrier without a memory fence: LDS in the loop is written only
-// by direct global->LDS loads, whose completion is awaited explicitly.
+// Workgroup barrier without a memory fence: the waves that write LDS in the
+// loop wait for their own writes (lgkmcnt) before it.
 __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-}
-
-// LDS byte address of a shared-memory pointer, as a wave-uniform value.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
 }
 
 // A wave-uniform 64-bit value moved to scalar registers.
@@ -87,18 +54,11 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Direct global->LDS load of 16 bytes per lane (global_load_lds_dwordx4):
-// lane l's bytes land at LDS byte address lds + 16 * l (lds wave-uniform).
-// Issued through inline assembly so that the compiler's wait-count pass does
-// not treat it as a write that may alias every later LDS read (it would put
-// a full vmcnt(0) before them and drain the prefetch ring); completion is
-// awaited explicitly with wait_vmem<> before the barrier that publishes a
-// tile.
-__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(g), "s"(lds)
-               : "memory", "m0");
+// Sum of the two bf16 halves of a packed pair, added to c (v_dot2c_f32_bf16
+// against (1, 1): the products are exact, the sum is taken in float32).
+__device__ __forceinline__ float add_bf16_pair(uint32_t w, float c) {
+  const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), one, c, false);
 }
 
 // Value of lane l ^ 32 (v_permlane32_swap: the two half-waves trade places).
@@ -117,490 +77,651 @@ __device__ __forceinline__ u32x2 ds_read_tr16(const bf16_t* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
-// bf16 path.  Work item = (question b, head h, block of <= 256 kept rows);
-// eight waves, 32 rows each.  K and V tiles of 64 tokens of head h stream
-// through a 4-stage LDS ring filled by direct global->LDS loads (16 bytes a
-// lane), three tiles ahead of the tile being consumed, one barrier per tile.
-// Tiles are stored in natural token-major layout with 16-byte chunks XOR-
-// swizzled by row (conflict-free MFMA operand reads).  Per wave and tile:
-//   S^T (64 tokens x 32 rows) = K_tile . Q^T     (A: K rows, 16-byte LDS reads)
-//   mask rows without an edge to the passage and tokens past its end, online
-//   softmax in fp32 (base-2), P rounded to bf16,
-//   O^T (d_h x 32 rows) += V_tile^T . P^T        (A: V^T via transposing LDS reads)
-// The S^T accumulator layout gives lane half hh, element e of a 16-token
-// block the token 8*(e/4) + 4*hh + e%4; the V^T operand is read in that same
-// token order, so P^T needs no data movement.
+// ---------------------------------------------------------------------------
+// bf16 path, passage-major.  Attention is computed only on the graph's edges:
+// for each passage j, only the kept rows adjacent to j (Def. B.3: a row's
+// softmax runs over the tokens of its neighbour passages, and no other pair
+// is touched), so the work grows with the number of edges and a passage
+// adjacent to none of an item's rows is never read.
+//
+// Work item = (question b, head h, chunk of <= kSpRows kept rows).  The item
+// walks the passages with at least one adjacent row in the chunk, in
+// ascending order, 32 tokens at a time.  K and V tiles of head h stream
+// through two LDS rings of three tiles, one barrier per tile; two loader
+// waves (one for K, one for V) keep four more tiles in flight in registers
+// and write each into the ring when its slot frees.  For each passage the
+// adjacent rows (a 192-bit row mask per passage) form blocks of 32 in row
+// order; compute wave w takes block w.  Per tile and block:
+//   S^T (32 tokens x 32 rows) = K_tile . Q^T        v_mfma_f32_32x32x16_bf16
+//   online softmax in fp32 (base 2), P rounded to bf16,
+//   O^T (d_h x 32 rows)     += V_tile^T . P^T       v_mfma_f32_32x32x16_bf16
+// Computing the transposed products keeps each query row in one lane column
+// (row statistics need only an exchange between the two half waves) and
+// makes the S^T accumulator the P^T operand; V^T comes from transposing LDS
+// reads in the token order of that layout.  Q of the block's rows sits in
+// registers, loaded one busy passage ahead.  After a passage's last tile
+// each block's partial (O, max, sums) is merged into the item's
+// accumulators, fp32 in LDS for every row of the chunk, by log-sum-exp
+// rescaling; one passage's blocks hold disjoint rows and passages merge in
+// ascending order (a barrier at least between two), so the result is
+// deterministic.  The item ends by writing O = acc / sum and LSE for every
+// row of the chunk (0 and -inf for a row without neighbours).
+constexpr int kSpRows = 192;              // kept rows per work item
+constexpr int kSpTile = 32;               // tokens per K/V tile
+constexpr int kSpStages = 3;              // K (and V) tiles resident in LDS
+constexpr int kSpRegTiles = 4;            // K (and V) tiles in flight in loader registers
+constexpr int kSpCompute = kSpRows / 32;  // compute waves (one 32-row block each)
+constexpr int kSpWaves = kSpCompute + 2;  // + a K loader and a V loader
+constexpr int kSpThreads = 64 * kSpWaves;
+constexpr int kSpMaxP = 64;
+constexpr float kLazy = 8.f;              // log2 slack of the softmax reference maximum
+static_assert(kSpRows <= 3 * 64, "row masks have three 64-bit words");
+
+// Position of the n-th (from 0) set bit of x; n < popcount(x).
+__device__ __forceinline__ int nth_bit64(uint64_t x, int n) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    const int c = __popcll(x & ((1ull << w) - 1ull));
+    if (n >= c) {
+      n -= c;
+      x >>= w;
+      pos += w;
+    }
+  }
+  return pos;
+}
+
+// Work item record: {question, first kept row (global), first passage,
+// head | rows << 8 | passages << 16}; question -1: no item.
 template <int D, bool SPLIT_P>
-__global__ void __launch_bounds__(kThreads)
-attn_bf16_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
-                 int N, int qstride, const int32_t* __restrict__ kept_offsets,
-                 const bf16_t* __restrict__ Kh, const bf16_t* __restrict__ Vh,
-                 const int32_t* __restrict__ passage_offsets,
-                 const int32_t* __restrict__ query_passages,
-                 const uint64_t* __restrict__ rowmask, int H, int total_kept,
-                 int total_passages, int total_tokens, int k_max, int P_max, int RB,
-                 int n_items, float scale_log2, void* __restrict__ O, int o_f32,
-                 float* __restrict__ lse) {
+__global__ void __launch_bounds__(kSpThreads)
+attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
+                   int N, int qstride, const bf16_t* __restrict__ Kh,
+                   const bf16_t* __restrict__ Vh, const int32_t* __restrict__ passage_offsets,
+                   const uint64_t* __restrict__ rowmask, const int4* __restrict__ items, int H,
+                   int total_tokens, float scale_log2, void* __restrict__ O, int o_f32,
+                   float* __restrict__ lse) {
   constexpr int NCH = D / 8;               // 16-byte chunks per token row
+  constexpr int NC4 = D / 4;               // 4-float chunks per accumulator row
   constexpr int KB = D / 16;               // k-blocks of QK^T
   constexpr int DT = D / 32;               // 32-wide feature tiles of O
-  constexpr int TILE = kTile * D;          // elements per K (or V) tile
-  constexpr int NI = kTile * NCH / 64;     // 1 KiB load instructions per K (or V) tile
-  // direct loads per lane per tile (waves >= NI issue none when NI < kWaves)
-  constexpr int kLoaders = kWaves / 2;    // group A issues every tile load
-  constexpr int LPT = 2 * ((NI + kLoaders - 1) / kLoaders);
-  // V chunk swizzle: depends on row % 4 only; keeps the transposing reads of
-  // four consecutive tokens on distinct banks.
+  constexpr int TILE = kSpTile * D;        // elements per K (or V) tile
+  constexpr int NI = kSpTile * NCH / 64;   // 1 KiB direct loads per K (or V) tile
   auto vswz = [](int row) { return (NCH >= 16 ? 4 : 2) * (row & 3); };
-  static_assert(NI % kLoaders == 0, "tile loads must divide over the loading waves");
-  static_assert(2 * (DT * 16 + 2) * 64 * 4 <= kStages * TILE * 2,
-                "the merge of split blocks reuses the K ring");
-  __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kStages * TILE];
-  __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kStages * TILE];
-  __shared__ uint64_t wave_union[kWaves];
-  __shared__ int p_ts[64], p_te[64];
+  __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kSpStages * TILE];
+  __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kSpStages * TILE];
+  __shared__ __attribute__((aligned(16))) float Oacc[kSpRows * D];
+  __shared__ float m_acc[kSpRows], l_acc[kSpRows], lx_acc[kSpRows];
+  __shared__ uint64_t rmask[3][kSpMaxP];   // rows 64w..64w+63 adjacent to each passage
+  __shared__ int p_ts[kSpMaxP], p_te[kSpMaxP], p_cnt[kSpMaxP];
+  __shared__ int32_t qsrc[kSpRows];        // visual-token index of each row (fused route)
 
-  // XCD-aware decode: consecutive items on one XCD share (b, h).
-  const int per_xcd = gridDim.x / 8;
-  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (item >= n_items) return;
-  const int rb = item % RB;
-  const int h = (item / RB) % H;
-  const int b = item / (RB * H);
-
-  int k0, k1, p0, p1;
-  range_of(kept_offsets, b, total_kept, k0, k1);
-  range_of(query_passages, b, total_passages, p0, p1);
-  const int kq = min(k1 - k0, k_max);
-  const int P = min(min(p1 - p0, P_max), 64);
-  const int nblk = (kq + kMaxRows - 1) / kMaxRows;
-  if (rb >= nblk) return;
-  const int rpb = ((kq + nblk - 1) / nblk + 31) / 32 * 32;   // rows per block
-  const int row0 = rb * rpb;
-  const int row_end = min(kq, row0 + rpb);
+  const int4 item = items[blockIdx.x];
+  const int b = item.x;
+  if (b < 0) return;
+  const int row0 = item.y, p0 = item.z;
+  const int h = item.w & 0xff;
+  const int nrows = (item.w >> 8) & 0xff;
+  const int P = (item.w >> 16) & 0xff;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int col = lane & 31;         // query row within the wave
-  const int hh = lane >> 5;          // half wave
-  // Waves w and w+4 share a SIMD.  A wave takes one 32-row block over whole
-  // tiles, or one 32-token half of every tile of a block (its partner, wave
-  // w^1, takes the other half; the two merge once at the end).  Halves are
-  // used where they even out the rows per SIMD: 5-6 blocks (waves 4-7 split
-  // blocks 4 and 5: 48 rows per SIMD instead of 64) and 1-2 blocks (one
-  // block over two SIMDs).
-  const int nrb = (row_end - row0 + 31) / 32;
-  int wb = wave, half = -1;          // wave's row block; half < 0: whole tiles
-  if (nrb <= 2) {
-    wb = wave >> 1;
-    half = wave & 1;
-  } else if ((nrb == 5 || nrb == 6) && wave >= 4) {
-    wb = 4 + ((wave - 4) >> 1);
-    half = wave & 1;
-  }
-  const bool any_split = nrb <= 2 || nrb == 5 || nrb == 6;   // uniform over the item
-  const bool split = half >= 0;
-  const int sub0 = split ? half : 0;                           // first 32-token sub-tile
-  const int r = row0 + wb * 32 + col;
-  const bool row_ok = wb < nrb && r < row_end;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
+  const int col = lane & 31;
+  const int hh = lane >> 5;
 
+  // accumulators, passage ranges, row sources, row masks per passage
+  const uint64_t pm = (P >= 64) ? ~0ull : ((1ull << P) - 1ull);
+  const uint64_t mk = (tid < nrows) ? (rowmask[row0 + tid] & pm) : 0ull;
+  const int src = (kept_idx && tid < nrows) ? kept_idx[row0 + tid] : 0;
+  int ts = 0, te = 0;
+  if (tid < P) range_of(passage_offsets, p0 + tid, total_tokens, ts, te);
+  for (int i = tid; i < nrows * NC4; i += kSpThreads)
+    reinterpret_cast<float4*>(Oacc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (tid < nrows) {
+    m_acc[tid] = -INFINITY;
+    l_acc[tid] = 0.f;
+    lx_acc[tid] = 0.f;
+    qsrc[tid] = clampi(src, 0, N - 1);
+  }
   if (tid < P) {
-    int ts, te;
-    range_of(passage_offsets, p0 + tid, total_tokens, ts, te);
     p_ts[tid] = ts;
     p_te[tid] = te;
   }
-  uint64_t mrow = row_ok ? rowmask[k0 + r] : 0ull;
-  if (P < 64) mrow &= (1ull << P) - 1ull;
-  uint64_t wmask = mrow;
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) wmask |= __shfl_xor(wmask, s, 64);
-  if (lane == 0) wave_union[wave] = wmask;
-
-  // Q^T fragments (B operand): row `col`, features kb*16 + 8*hh .. +7.
-  u32x4 qf[KB];
-  {
-    // A lane past the block's rows reads the question's first kept row (the
-    // item has at least one) and zeroes it, so all loads issue together.
-    const int rr = row_ok ? r : 0;
-    const bf16_t* qrow;
-    if (kept_idx) {
-      const int src = clampi(kept_idx[k0 + rr], 0, N - 1);
-      qrow = qbase + ((size_t)b * N + src) * qstride + (size_t)h * D;
-    } else {
-      qrow = qbase + (size_t)(k0 + rr) * qstride + (size_t)h * D;
+  if (wave < 3) {
+    for (int j = 0; j < P; ++j) {
+      const uint64_t bal = __ballot((mk >> j) & 1ull);
+      if (lane == 0) rmask[wave][j] = bal;
     }
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-      qf[kb] = *reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh);
-    // a negative scale is folded in here (bf16 sign flips), so the logits
-    // below are always scaled by |scale|
-    const uint32_t neg = (scale_log2 < 0.f) ? 0x80008000u : 0u;
-    const uint32_t keep = row_ok ? 0xffffffffu : 0u;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) qf[kb] = (qf[kb] ^ neg) & keep;
-    // Settle the query loads here: left pending, the compiler would wait for
-    // them (vmcnt(0)) inside the tile loop, draining the prefetch ring.
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) asm volatile("" ::"v"(qf[kb]));
   }
   __syncthreads();
-  uint64_t U = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) U |= wave_union[w];
-  U = uniform64(U);
-  wmask = uniform64(wmask);
+  if (tid < P) p_cnt[tid] = __popcll(rmask[0][tid]) + __popcll(rmask[1][tid]) +
+                            __popcll(rmask[2][tid]);
+  __syncthreads();
+  // passages with at least one adjacent row of the chunk (and some tokens)
+  const bool touched = lane < P && p_cnt[lane] > 0 && p_te[lane] > p_ts[lane];
+  const uint64_t U = uniform64(__ballot(touched));
 
-  // Tile cursors over (adjacent passage, 64-token block): one for issuing
-  // loads, one for computing.
+  // Tile cursor over (touched passage, 32-token block).
   struct Cursor {
     uint64_t rem;
-    int j, t, te;
+    int j, t, ts, te;
   };
-  auto advance = [&](Cursor& c) -> bool {
-    if (c.j >= 0 && c.t + kTile < c.te) {
-      c.t += kTile;
+  auto advance = [&](Cursor& cu) -> bool {
+    if (cu.j >= 0 && cu.t + kSpTile < cu.te) {
+      cu.t += kSpTile;
       return true;
     }
-    while (c.rem) {
-      const int j = __builtin_ctzll(c.rem);
-      c.rem &= c.rem - 1ull;
-      const int ts = __builtin_amdgcn_readfirstlane(p_ts[j]);
-      const int te = __builtin_amdgcn_readfirstlane(p_te[j]);
-      if (te > ts) {
-        c.j = j; c.t = ts; c.te = te;
-        return true;
-      }
-    }
-    return false;
-  };
-  // Direct loads of one tile: instruction q fills LDS bytes [q*1024, +1024)
-  // of the stage; lane l's 16 bytes are slot o = q*64 + l = (row, physical
-  // chunk p).  K holds logical chunk p ^ (row % NCH) there, V holds logical
-  // chunk p ^ vswz(row) (a key of row % 4 only, so the transposing reads of
-  // tokens t, t+8, t+16, t+32 differ by constant offsets).  Rows past the
-  // passage end re-read its last token (finite values, masked in the
-  // softmax).
-  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  auto issue = [&](int stage, int t, int te) {
-    bf16_t* Ks = Kbuf + stage * TILE;
-    bf16_t* Vs = Vbuf + stage * TILE;
-#pragma unroll
-    for (int q = wave_s; q < NI; q += kLoaders) {
-      const int o = q * 64 + lane;
-      const int row = o / NCH, pch = o % NCH;
-      const int ck = pch ^ (row & (NCH - 1));
-      const int cv = pch ^ vswz(row);
-      const int tok = min(t + row, te - 1);
-      const size_t rowoff = ((size_t)tok * H + h) * D;
-      lds_dma16(Kh + rowoff + ck * 8, lds_addr(Ks + q * 512));
-      lds_dma16(Vh + rowoff + cv * 8, lds_addr(Vs + q * 512));
-    }
+    if (!cu.rem) return false;
+    const int j = __builtin_ctzll(cu.rem);
+    cu.rem &= cu.rem - 1ull;
+    cu.j = j;
+    cu.ts = __builtin_amdgcn_readfirstlane(p_ts[j]);
+    cu.te = __builtin_amdgcn_readfirstlane(p_te[j]);
+    cu.t = cu.ts;
+    return true;
   };
 
-  f32x16_t acc[DT];
-#pragma unroll
-  for (int t = 0; t < DT; ++t)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-
-  // per-lane constants of the MFMA operand reads: K rows st*32 + col share
-  // the swizzle key col % NCH; V^T reads follow the transposing-read layout
-  const int g16 = lane >> 4, s16 = lane & 15;
-  int koff[KB];                                       // K row col, chunk 2kb+hh
-#pragma unroll
-  for (int kb = 0; kb < KB; ++kb)
-    koff[kb] = col * D + (((2 * kb + hh) ^ (col & (NCH - 1))) << 3);
-  // V^T operand: token 4*hh + (s16 >> 2) (+ 16 per k-block, + 8 for the upper
-  // half), feature 32*dt + 16*(g16 & 1) + 4*(s16 & 3)
-  const int tr_tok = 4 * hh + (s16 >> 2);
-  int voff[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) {
-    const int d = 32 * dt + 16 * (g16 & 1) + 4 * (s16 & 3);
-    voff[dt] = tr_tok * D + (((d >> 3) ^ vswz(tr_tok)) << 3) + (d & 7);
+  // One barrier per tile publishes it; the loads run two tiles ahead.
+  int n_tiles = 0;
+  for (uint64_t r = U; r; r &= r - 1ull) {
+    const int j = __builtin_ctzll(r);
+    n_tiles += (__builtin_amdgcn_readfirstlane(p_te[j]) - __builtin_amdgcn_readfirstlane(p_ts[j]) +
+                kSpTile - 1) / kSpTile;
   }
 
-  // Matrix phase: O^T += V^T . P^T for the previous tile (weights pb/pl,
-  // V tile in stage pv_stage), then S^T = K . Q^T for the tile in stage
-  // s_stage into sacc.  NST (1 or 2) is the number of 32-token sub-tiles the
-  // wave computes, starting at sub-tile sub0.
-  f32x16_t sacc[2];
-  u32x4 pb[4], pl[4];
-  float acc_scale = 1.f;             // rescale of acc owed by the last softmax
-  auto pv_product = [&](auto nst, int pv_stage) {
-    constexpr int NST = decltype(nst)::value;
-    __builtin_amdgcn_sched_barrier(0);
-    if (__any(acc_scale != 1.f)) {   // some row's maximum moved
+  if (wave >= kSpCompute) {
+    // ---- loader waves: the first streams K, the second V --------------------
+    const bool isV = wave == kSpCompute + 1;
+    const bf16_t* gsrc = isV ? Vh : Kh;
+    bf16_t* buf = isV ? Vbuf : Kbuf;
+    // lane offsets of the tile's 16-byte chunks from the tile's first token:
+    // instruction q fills LDS bytes [q*1024, +1024) of the stage, lane l's
+    // slot o = q*64 + l being (token row, physical chunk); K holds logical
+    // chunk p ^ (row % NCH) there, V logical chunk p ^ vswz(row)
+    uint32_t voff[NI];
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[dt][v] *= acc_scale;
+    for (int q = 0; q < NI; ++q) {
+      const int o = q * 64 + lane;
+      const int row = o / NCH, pch = o % NCH;
+      const int ch = isV ? (pch ^ vswz(row)) : (pch ^ (row & (NCH - 1)));
+      voff[q] = (uint32_t)((row * H * D + ch * 8) * 2);
     }
-    const bf16_t* Vs = Vbuf + pv_stage * TILE + sub0 * 32 * D;
+    const bf16_t* hsrc = gsrc + (size_t)h * D;
+    // Tiles travel through registers: global loads run kSpRegTiles tiles
+    // ahead of the LDS ring (which holds the tile being consumed and the next
+    // one), so the loads keep streaming while the compute waves merge or
+    // start a passage.  Slot n % kSpRegTiles holds tile n; the register
+    // layout is the LDS layout (lane l writes bytes 16 l of each 1 KiB).
+    u32x4 rg[kSpRegTiles][NI];
+    auto gload = [&](auto slot, int t, int te_) {
+      const bf16_t* tbase = hsrc + (size_t)t * H * D;
+      const int over_base = t - (te_ - 1);
 #pragma unroll
-    for (int hf = 0; hf < NST; ++hf) {
+      for (int q = 0; q < NI; ++q) {
+        // rows past the passage's end read its last token (finite values,
+        // masked in the softmax)
+        const int row = (q * 64 + lane) / NCH;
+        const uint32_t o = voff[q] - (uint32_t)(max(over_base + row, 0) * H * D * 2);
+        rg[decltype(slot)::value][q] = *reinterpret_cast<const u32x4*>(
+            reinterpret_cast<const char*>(tbase) + o);
+      }
+      // tiles issue in order (the wait counts assume it)
+      asm volatile("" ::: "memory");
+    };
+    auto swrite = [&](auto slot, int n) {
+      bf16_t* dst = buf + (n % kSpStages) * TILE;
+#pragma unroll
+      for (int q = 0; q < NI; ++q)
+        *reinterpret_cast<u32x4*>(dst + q * 512 + lane * 8) = rg[decltype(slot)::value][q];
+    };
+    // Every step issues one tile's loads, unconditionally (past the last
+    // tile the cursor stays put and the last tile is read again), so that
+    // the compiler's wait counts before each register slot's LDS write are
+    // exact: the slot's loads are the oldest of the four in flight.
+    Cursor ci{U, -1, 0, 0, 0};
+    auto issue = [&](auto slot) {
+      advance(ci);
+      gload(slot, ci.t, ci.te);
+    };
+    static_assert(kSpRegTiles == 4 && kSpStages == 3, "slot arithmetic below");
+    if (n_tiles > 0) {
+      // prologue: loads of tiles 0 .. 3, tiles 0 and 1 into LDS, loads of
+      // tiles 4 and 5
+      issue(IntC<0>{});
+      issue(IntC<1>{});
+      issue(IntC<2>{});
+      issue(IntC<3>{});
+      swrite(IntC<0>{}, 0);
+      issue(IntC<0>{});
+      swrite(IntC<1>{}, 1);            // (a repeat of tile 0 if there is one tile)
+      issue(IntC<1>{});
+      // step i: after its barrier the LDS slot of tile i-1, which every wave
+      // finished in step i-1, is free; tile i+2 goes there from register slot
+      // (i+2) % 4, which then takes tile i+6
+      auto step = [&](auto u, int i) {
+        constexpr int sl = (decltype(u)::value + 2) % kSpRegTiles;
+        if (i < n_tiles) {
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // tiles <= i+1 written
+          barrier_nofence();                                     // tile i is published
+          // (past the last tile a repeat, into a slot that is not read again)
+          swrite(IntC<sl>{}, i + 2);
+        }
+        issue(IntC<sl>{});
+      };
+      // whole groups of four steps, one exit: the loads of every step are
+      // unconditional, so each slot's wait count is the same on every path
+      for (int i = 0; i < n_tiles; i += kSpRegTiles) {
+        step(IntC<0>{}, i);
+        step(IntC<1>{}, i + 1);
+        step(IntC<2>{}, i + 2);
+        step(IntC<3>{}, i + 3);
+      }
+    }
+  } else {
+    // ---- compute waves ------------------------------------------------------
+    const int g16 = lane >> 4, s16 = lane & 15;
+    int koff[KB];                                   // K row col, chunk 2kb+hh
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+      koff[kb] = col * D + (((2 * kb + hh) ^ (col & (NCH - 1))) << 3);
+    const int tr_tok = 4 * hh + (s16 >> 2);        // V^T operand, transposing reads
+    int voff[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int d = 32 * dt + 16 * (g16 & 1) + 4 * (s16 & 3);
+      voff[dt] = tr_tok * D + (((d >> 3) ^ vswz(tr_tok)) << 3) + (d & 7);
+    }
+    // a negative scale is folded into the queries (bf16 sign flips), so the
+    // logits are scaled by |scale| and their maximum is a plain maximum
+    const uint32_t neg = (scale_log2 < 0.f) ? 0x80008000u : 0u;
+    const float sc = fabsf(scale_log2);
+    // touched passages in which this wave has a block
+    const uint64_t bmask =
+        uniform64(__ballot(lane < P && ((U >> lane) & 1ull) && p_cnt[lane] > 32 * wave));
+    // Queries of the block's rows.  For the wave's busy passages in order:
+    // at the first tile of busy passage k, qf takes passage k's queries from
+    // qn, and qn is refilled (unconditionally, so the loads land in qn's own
+    // registers and stay in flight) with passage k+1's, whose rows were looked
+    // up during passage k-1; the lookup of passage k+2 then runs in phases,
+    // one per step, each LDS read consumed a step after it is issued: (1) the
+    // passage's row masks, (2) this lane's row (the n-th adjacent row, n = 32
+    // * wave + col) and its visual-token index.  A lane past the block's rows
+    // loads a placeholder row, whose scores land in a column that is never
+    // merged.
+    u32x4 qn[KB], qf[KB];
+    int lk_j = -1, lk_phase = 2;       // passage being looked up; phases done (2: done)
+    uint64_t lkw0 = 0, lkw1 = 0, lkw2 = 0;
+    int lk_row = -1, lk_src = 0;       // result of the lookup
+    int qn_row = -1;                   // row of the queries in qn
+    auto lookup_phase = [&]() {
+      if (lk_phase == 0) {
+        lkw0 = uniform64(rmask[0][lk_j]);
+        lkw1 = uniform64(rmask[1][lk_j]);
+        lkw2 = uniform64(rmask[2][lk_j]);
+      } else {
+        const int n = 32 * wave + col;
+        const int c0 = __popcll(lkw0), c1 = __popcll(lkw1), c2 = __popcll(lkw2);
+        if (n >= c0 + c1 + c2) lk_row = -1;
+        else if (n < c0) lk_row = nth_bit64(lkw0, n);
+        else if (n < c0 + c1) lk_row = 64 + nth_bit64(lkw1, n - c0);
+        else lk_row = 128 + nth_bit64(lkw2, n - c0 - c1);
+        lk_src = kept_idx ? qsrc[lk_row >= 0 ? lk_row : 0] : 0;
+      }
+      ++lk_phase;
+    };
+    auto start_lookup = [&](int j) {   // j < 0: nothing (placeholder row)
+      lk_j = j;
+      lk_phase = 0;
+      lk_row = -1;
+      lk_src = 0;
+      if (j < 0) lk_phase = 2;
+    };
+    auto load_q = [&]() {              // qn <- the looked-up rows' queries
+      qn_row = lk_row;
+      const int rr = lk_row >= 0 ? lk_row : 0;
+      const bf16_t* qrow = kept_idx
+          ? qbase + ((size_t)b * N + lk_src) * qstride + (size_t)h * D
+          : qbase + (size_t)(row0 + rr) * qstride + (size_t)h * D;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        qn[kb] = *reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh);
+    };
+    // first and second busy passages
+    const int busy0 = bmask ? __builtin_ctzll(bmask) : -1;
+    const uint64_t after0 = busy0 >= 0 ? (bmask & (bmask - 1ull)) : 0ull;
+    start_lookup(busy0);
+    while (lk_phase < 2) lookup_phase();
+    load_q();
+    start_lookup(after0 ? __builtin_ctzll(after0) : -1);
+
+    int acc_row = -1;                  // row of this lane's column in the current block
+    f32x16_t acc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[dt][v] = 0.f;
+    // row sums: of the weights as rounded for the PV product (normalises O)
+    // and of the exact weights (the log-sum-exp)
+    float m_run = -INFINITY, l_run = 0.f, lx_run = 0.f;
+
+    // acc's block partial into the item's accumulators: the row's sixteen
+    // 16-byte pieces read in two batches of eight, rescaled, written back
+    auto merge = [&]() {
+      const float l_tot = l_run + swap_halves(l_run);
+      const float lx_tot = lx_run + swap_halves(lx_run);
+      if (acc_row < 0) return;
+      const int ri = acc_row;
+      const float mo = m_acc[ri], lo = l_acc[ri], lxo = lx_acc[ri];
+      float4* orow = reinterpret_cast<float4*>(Oacc + ri * D);
+      const float mn = fmaxf(mo, m_run);
+      const float a = __builtin_amdgcn_exp2f(mo - mn);    // 0 while the row is empty
+      const float cb = __builtin_amdgcn_exp2f(m_run - mn);
+#pragma unroll
+      for (int half = 0; half < DT; half += 2) {
+        float4 ov[2][4];                  // features 4q .. 4q+3, q = 8dt + 2g4 + hh
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4)
+            ov[u][g4] = orow[((half + u) * 8 + 2 * g4 + hh) ^ (ri & (NC4 - 1))];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int dt = half + u;
+            float4 o = ov[u][g4];
+            o.x = fmaf(o.x, a, acc[dt][4 * g4 + 0] * cb);
+            o.y = fmaf(o.y, a, acc[dt][4 * g4 + 1] * cb);
+            o.z = fmaf(o.z, a, acc[dt][4 * g4 + 2] * cb);
+            o.w = fmaf(o.w, a, acc[dt][4 * g4 + 3] * cb);
+            orow[(dt * 8 + 2 * g4 + hh) ^ (ri & (NC4 - 1))] = o;
+          }
+      }
+      if (hh == 0) {
+        m_acc[ri] = mn;
+        l_acc[ri] = fmaf(lo, a, l_tot * cb);
+        lx_acc[ri] = fmaf(lxo, a, lx_tot * cb);
+      }
+    };
+
+    Cursor cc{U, -1, 0, 0, 0};
+    for (int i = 0; i < n_tiles; ++i) {
+      advance(cc);
+      const bool busy = (bmask >> cc.j) & 1ull;
+      const bool first = cc.t == cc.ts;
+      if (busy && first) {
+        // this passage's queries (sign of a negative scale folded in), then
+        // the next busy passage's loads into qn (its lookup finishes here if
+        // the previous passage was too short for it), then the lookup of the
+        // one after
+        acc_row = qn_row;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) qf[kb] = qn[kb] ^ neg;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) asm volatile("" ::"v"(qf[kb]) : "memory");
+        while (lk_phase < 2) lookup_phase();
+        load_q();
+        const uint64_t rest = bmask & cc.rem;
+        const uint64_t after = rest ? (rest & (rest - 1ull)) : 0ull;
+        start_lookup(after ? __builtin_ctzll(after) : -1);
+      } else if (lk_phase < 2) {
+        lookup_phase();
+      }
+      barrier_nofence();               // tile i has landed
+      if (!busy) continue;
+      const int stage = i % kSpStages;
+      if (first) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[dt][v] = 0.f;
+        m_run = -INFINITY;
+        l_run = 0.f;
+        lx_run = 0.f;
+      }
+      // S^T = K . Q^T
+      const bf16_t* Ks = Kbuf + stage * TILE;
+      u32x4 ka[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) ka[kb] = *reinterpret_cast<const u32x4*>(Ks + koff[kb]);
+      f32x16_t sacc;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) sacc = mfma32(ka[kb], qf[kb], sacc);
+      // Online softmax of this lane's row: accumulator element v holds token
+      // 8*(v/4) + 4*hh + v%4 of the tile.  The weights are taken against a
+      // reference maximum m_run that moves only when a tile's maximum exceeds
+      // it by more than 2^kLazy (the weights then stay <= 2^kLazy and acc is
+      // rescaled only then, not on every tile); the row sum l adds the
+      // weights as the PV product sees them (rounded to bf16), so numerator
+      // and denominator carry the same weights, and lx the exact weights
+      // (for the LSE).
+      if (cc.t + kSpTile > cc.te) {
+        const int rem = cc.te - cc.t - 4 * hh;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (8 * (v >> 2) + (v & 3) >= rem) sacc[v] = -INFINITY;
+      }
+      float sm = fmaxf(fmaxf(fmaxf(sacc[0], sacc[1]), fmaxf(sacc[2], sacc[3])),
+                       fmaxf(fmaxf(sacc[4], sacc[5]), fmaxf(sacc[6], sacc[7])));
+      sm = fmaxf(sm, fmaxf(fmaxf(fmaxf(sacc[8], sacc[9]), fmaxf(sacc[10], sacc[11])),
+                           fmaxf(fmaxf(sacc[12], sacc[13]), fmaxf(sacc[14], sacc[15]))));
+      sm = fmaxf(sm, swap_halves(sm));
+      const float tmax = sm * sc;                          // the tile has a valid token
+      const bool moved = tmax > m_run + kLazy;             // always on a block's first tile
+      const float m_new = moved ? tmax : m_run;
+      // acc and the sums are 0 before a block's first tile: nothing to rescale
+      const float alpha =
+          (moved && m_run != -INFINITY) ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+      m_run = m_new;
+      u32x4 pb[2], pl[2];
+      float ls = 0.f, lx = 0.f;
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        uint32_t w[4], wl[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[8 * kb2 + 2 * q], sc, -m_new));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[8 * kb2 + 2 * q + 1], sc, -m_new));
+          lx += p0 + p1;
+          w[q] = pack2_bf16(p0, p1);
+          if (SPLIT_P) {
+            wl[q] = pack2_bf16(p0 - __uint_as_float(w[q] << 16),
+                               p1 - __uint_as_float(w[q] & 0xffff0000u));
+          } else {
+            ls = add_bf16_pair(w[q], ls);
+          }
+        }
+        pb[kb2] = u32x4{w[0], w[1], w[2], w[3]};
+        if (SPLIT_P) pl[kb2] = u32x4{wl[0], wl[1], wl[2], wl[3]};
+      }
+      l_run = fmaf(l_run, alpha, SPLIT_P ? lx : ls);
+      lx_run = fmaf(lx_run, alpha, lx);
+      if (__any(alpha != 1.f)) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[dt][v] *= alpha;
+      }
+      // O^T += V^T . P^T (V^T by transposing reads in the token order of S^T)
+      const bf16_t* Vs = Vbuf + stage * TILE;
       u32x4 va[DT][2];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
-          const bf16_t* vp = Vs + (32 * hf + 16 * g) * D + voff[dt];
+          const bf16_t* vp = Vs + 16 * g * D + voff[dt];
           va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
                                               0, 1, 2, 3);
         }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        acc[dt] = mfma32(va[dt][0], pb[2 * hf], acc[dt]);
-        acc[dt] = mfma32(va[dt][1], pb[2 * hf + 1], acc[dt]);
+        acc[dt] = mfma32(va[dt][0], pb[0], acc[dt]);
+        acc[dt] = mfma32(va[dt][1], pb[1], acc[dt]);
         if (SPLIT_P) {
-          acc[dt] = mfma32(va[dt][0], pl[2 * hf], acc[dt]);
-          acc[dt] = mfma32(va[dt][1], pl[2 * hf + 1], acc[dt]);
+          acc[dt] = mfma32(va[dt][0], pl[0], acc[dt]);
+          acc[dt] = mfma32(va[dt][1], pl[1], acc[dt]);
         }
       }
+      if (cc.t + kSpTile >= cc.te) merge();    // the passage's last tile
     }
-    // Schedule: sixteen V^T reads ahead, then one MFMA (two with the split
-    // weights) per two reads, so the read latency hides behind the matrix
-    // pipe (left alone, the compiler waits for every operand pair in turn).
-    {
-      constexpr int R = NST * 4 * DT;
-      constexpr int MPS = SPLIT_P ? 2 : 1;
-      constexpr int M = NST * 2 * DT * MPS;
-      constexpr int PRE = R < 16 ? R : 16;
-      constexpr int STEPS = (R - PRE) / 2;
-      __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);   // LDS reads
-#pragma unroll
-      for (int i = 0; i < STEPS; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, MPS, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, M - STEPS * MPS, 0);
-    }
-  };
-  auto s_product = [&](auto nst, int s_stage) {
-    constexpr int NST = decltype(nst)::value;
-    __builtin_amdgcn_sched_barrier(0);
-    const bf16_t* Ks = Kbuf + s_stage * TILE + sub0 * 32 * D;
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      u32x4 ka[KB];
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        ka[kb] = *reinterpret_cast<const u32x4*>(Ks + st * 32 * D + koff[kb]);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) sacc[st] = mfma32(ka[kb], qf[kb], sacc[st]);
-    }
-    // Schedule: eight K reads ahead (all of them for one sub-tile at d_h 64),
-    // then one MFMA per read.
-    {
-      constexpr int R = NST * KB;
-      constexpr int PRE = R < 8 ? R : 8;
-      __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);
-#pragma unroll
-      for (int i = 0; i < R - PRE; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, PRE, 0);
-    }
-  };
-  // Vector phase: online softmax over the scores of this lane's row in sacc
-  // (sub-tiles with `full`, `rem`, adjacency bias `mbias`); rescales acc and
-  // leaves the bf16 weights in pb (and their remainders in pl).
-  auto softmax = [&](auto nst, bool full, int rem, float mbias) {
-    constexpr int NST = decltype(nst)::value;
-    __builtin_amdgcn_sched_barrier(0);
-    // (a negative scale was folded into the query fragments: c > 0)
-    const float c = fabsf(scale_log2);
-    if (!full) {                     // tokens past the passage end
-      // kept as a branch: selecting on every tile would cost 64 VALU ops
-      asm volatile("");
-#pragma unroll
-      for (int st = 0; st < NST; ++st)
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (32 * st + 8 * (v >> 2) + (v & 3) >= rem) sacc[st][v] = -INFINITY;
-    }
-    float sm = sacc[0][0];
-#pragma unroll
-    for (int st = 0; st < NST; ++st)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sm = fmaxf(sm, sacc[st][v]);
-    sm = fmaxf(sm, swap_halves(sm));
-    const float mt = (sm == -INFINITY) ? -INFINITY : fmaf(sm, c, mbias);
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    const float bias = mbias - ((m_new == -INFINITY) ? 0.f : m_new);
-    m_run = m_new;
-    float ls = 0.f;
-#pragma unroll
-    for (int kb2 = 0; kb2 < 2 * NST; ++kb2) {
-      float pv[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        // scores are finite on a full tile (a row not adjacent to the
-        // passage has bias -inf); past the passage end the weight is 0
-        const float x = sacc[kb2 >> 1][8 * (kb2 & 1) + e];
-        pv[e] = __builtin_amdgcn_exp2f(fmaf(x, c, bias));   // 0 for a masked token
-        ls += pv[e];
-      }
-      uint32_t w[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = pack2_bf16(pv[2 * q], pv[2 * q + 1]);
-      pb[kb2] = u32x4{w[0], w[1], w[2], w[3]};
-      if (SPLIT_P) {
-        uint32_t wl[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          wl[q] = pack2_bf16(pv[2 * q] - __uint_as_float(w[q] << 16),
-                             pv[2 * q + 1] - __uint_as_float(w[q] & 0xffff0000u));
-        pl[kb2] = u32x4{wl[0], wl[1], wl[2], wl[3]};
-      }
-    }
-    l_run = l_run * alpha + ls;
-    acc_scale = alpha;               // applied before the next PV product
-  };
-
-  // Tile loop, two half-steps per tile separated by barriers: the matrix
-  // phase of tile i (PV of tile i-1, S of tile i), then its softmax.  Group B
-  // (waves 4-7) takes one extra barrier first, so it runs half a step behind
-  // group A (waves 0-3): on each SIMD one wave's matrix work overlaps the
-  // other's vector work.  Group A issues and awaits every tile load; a tile
-  // is awaited before the barrier that precedes its first use by either
-  // group.  Tiles i-1 and i stay in use until group B's step i ends, so loads
-  // run STAGES-2 tiles ahead.
-  const bool group_b = wave >= 4;
-  const bool busy = wmask != 0;
-  Cursor ci{U, -1, 0, 0}, cc{U, -1, 0, 0};
-  int issued = 0;
-  if (!group_b) {
-#pragma unroll
-    for (int s = 0; s < kStages - 2; ++s)
-      if (advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
-  } else {
-    barrier_nofence();
   }
-  // tile i's loads have landed once at most `ahead` later tiles are pending
-  auto wait_tile = [&](int ahead) {
-    if (ahead >= 2) wait_vmem<2 * LPT>();
-    else if (ahead == 1) wait_vmem<LPT>();
-    else wait_vmem<0>();
-  };
-  // Step i: PV of tile i-1 (zero weights at i = 0), S and softmax of tile i;
-  // a final step past the last tile does only the PV.
-  auto busy_loop = [&](auto nst) {
-    // The first matrix phase adds tile 0's V with zero weights (exactly 0).
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      pb[q] = u32x4{0u, 0u, 0u, 0u};
-      pl[q] = u32x4{0u, 0u, 0u, 0u};
-    }
-    int prev_stage = 0;
-    for (int i = 0;; ++i) {
-      const bool more = advance(cc);
-      if (!more && i == 0) break;
-      if (more) {
-        if (!group_b) wait_tile(issued - i - 1);
-        barrier_nofence();
-        if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
-      }
-      pv_product(nst, prev_stage);
-      if (!more) break;
-      const int stage = i % kStages;
-      s_product(nst, stage);
-      barrier_nofence();
-      // accumulator element v of sub-tile st is token 32*st + 8*(v/4) + v%4
-      // + 4*hh of the wave's first sub-tile; it exists if that is below rem
-      const int t0 = cc.t + 32 * sub0;
-      softmax(nst, t0 + 32 * decltype(nst)::value <= cc.te, cc.te - t0 - 4 * hh,
-              ((mrow >> cc.j) & 1ull) ? 0.f : -INFINITY);
-      prev_stage = stage;
-    }
-  };
-  if (!busy) {
-    // A wave without kept rows only keeps step with the barriers (and, in
-    // group A, streams its share of the tiles).
-    for (int i = 0; advance(cc); ++i) {
-      if (!group_b) wait_tile(issued - i - 1);
-      barrier_nofence();
-      if (!group_b && advance(ci)) { issue(issued % kStages, ci.t, ci.te); ++issued; }
-      barrier_nofence();
-    }
-  } else if (split) {
-    busy_loop(IntC<1>{});
-  } else {
-    busy_loop(IntC<2>{});
-  }
-  if (!group_b) barrier_nofence();
+  __syncthreads();
 
-  // Merge the two halves of a split block (online-softmax combination):
-  // the upper half's wave hands (acc, m, l) over through the LDS ring.
-  if (any_split) {
-    __syncthreads();                 // every wave is done with the ring
-    // a pair's slot: blocks 0/1 (1-2 blocks) or 4/5 (5-6 blocks) use slots 0/1
-    float* xb = reinterpret_cast<float*>(Kbuf) + (wb & 1) * (DT * 16 + 2) * 64;
-    const bool paired = split && wb < nrb;   // waves past the last block hold no rows
-    if (paired && half == 1) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) xb[(dt * 16 + v) * 64 + lane] = acc[dt][v];
-      xb[(DT * 16) * 64 + lane] = m_run;
-      xb[(DT * 16 + 1) * 64 + lane] = l_run;
+  // O = acc / sum for every row of the chunk; LSE (natural log)
+  const size_t obase = (size_t)row0 * H * D + (size_t)h * D;
+  for (int e = tid; e < nrows * NC4; e += kSpThreads) {
+    const int ri = e / NC4, q = e % NC4;
+    const float4 v = reinterpret_cast<const float4*>(Oacc + ri * D)[q ^ (ri & (NC4 - 1))];
+    const float l = l_acc[ri];
+    const float inv = (l > 0.f) ? 1.f / l : 0.f;
+    const size_t off = obase + (size_t)ri * H * D + q * 4;
+    if (o_f32) {
+      *reinterpret_cast<float4*>(static_cast<float*>(O) + off) =
+          make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
+    } else {
+      uint2 w;
+      w.x = pack2_bf16(v.x * inv, v.y * inv);
+      w.y = pack2_bf16(v.z * inv, v.w * inv);
+      *reinterpret_cast<uint2*>(static_cast<bf16_t*>(O) + off) = w;
+    }
+  }
+  if (lse && tid < nrows) {
+    const float l = lx_acc[tid];
+    lse[(size_t)(row0 + tid) * H + h] = (l > 0.f) ? (m_acc[tid] + log2f(l)) * kLn2 : -INFINITY;
+  }
+}
+
+// Work list of the passage-major attention, built on the device from the
+// offsets (one workgroup).  Questions are ordered by decreasing cost (chunks x
+// passage tokens, ties to the lower index; natural order above kPlanMaxB
+// questions), so that the longest items start first.  The (question, head)
+// groups of that order are dealt in runs of eight; a run whose groups have at
+// most n chunks takes 8n consecutive workgroup ids, chunk c of the run's group
+// i at id base + 8c + i.  Workgroups are dealt round-robin over the 8 XCDs,
+// so the chunks of one (question, head), which read the same K/V tiles, run
+// side by side on one XCD and share its L2.  Unused ids get no item.
+constexpr int kPlanMaxB = 4096;
+constexpr int kPlanThreads = 1024;
+
+__global__ void __launch_bounds__(kPlanThreads)
+attn_plan_kernel(const int32_t* __restrict__ kept_offsets,
+                 const int32_t* __restrict__ query_passages,
+                 const int32_t* __restrict__ passage_offsets, int B, int H, int total_kept,
+                 int total_passages, int total_tokens, int k_max, int P_max, int n_ids,
+                 int4* __restrict__ items) {
+  // per question (when B <= kPlanMaxB): sort key, first kept row, rows,
+  // first passage, passages (<= 64), chunks
+  __shared__ uint64_t key[kPlanMaxB];
+  __shared__ int32_t q_k0[kPlanMaxB], q_p0[kPlanMaxB];
+  __shared__ int16_t q_kq[kPlanMaxB];
+  __shared__ uint8_t q_P[kPlanMaxB], q_nch[kPlanMaxB];
+  __shared__ uint32_t scan_sh[kPlanThreads / 64 + 1];
+  const int tid = threadIdx.x;
+  struct Q {
+    int k0, kq, p0, P, nch;
+  };
+  auto question = [&](int b) {
+    Q q;
+    int k1, p1;
+    range_of(kept_offsets, b, total_kept, q.k0, k1);
+    range_of(query_passages, b, total_passages, q.p0, p1);
+    q.kq = min(k1 - q.k0, k_max);
+    q.P = min(min(p1 - q.p0, P_max), kSpMaxP);
+    q.nch = (q.kq + kSpRows - 1) / kSpRows;
+    return q;
+  };
+  const bool cached = B <= kPlanMaxB;   // question data and the cost order in LDS
+  if (cached) {
+    int n = 1;
+    while (n < B) n <<= 1;
+    for (int b = tid; b < n; b += kPlanThreads) {
+      uint64_t kk = 0ull;
+      if (b < B) {
+        const Q q = question(b);
+        const int t0 = q.P > 0 ? clampi(passage_offsets[q.p0], 0, total_tokens) : 0;
+        const int t1 = q.P > 0 ? clampi(passage_offsets[q.p0 + q.P], t0, total_tokens) : 0;
+        const uint64_t cost = (uint64_t)q.nch * (uint64_t)(t1 - t0 + 1);
+        kk = (cost << 12) | (uint64_t)(kPlanMaxB - 1 - b);
+        q_k0[b] = q.k0;
+        q_p0[b] = q.p0;
+        q_kq[b] = (int16_t)q.kq;
+        q_P[b] = (uint8_t)q.P;
+        q_nch[b] = (uint8_t)q.nch;
+      }
+      key[b] = kk;
     }
     __syncthreads();
-    if (paired && half == 1) return;
-    if (paired) {
-      const float m1 = xb[(DT * 16) * 64 + lane];
-      const float l1 = xb[(DT * 16 + 1) * 64 + lane];
-      const float M = fmaxf(m_run, m1);
-      const float a0 = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - M);
-      const float a1 = (m1 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          acc[dt][v] = acc[dt][v] * a0 + xb[(dt * 16 + v) * 64 + lane] * a1;
-      l_run = l_run * a0 + l1 * a1;
-      m_run = M;
+    // bitonic sort, descending
+    for (int size = 2; size <= n; size <<= 1)
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int i = tid; i < n; i += kPlanThreads) {
+          const int jx = i ^ stride;
+          if (jx > i) {
+            const bool desc = (i & size) == 0;
+            const uint64_t x = key[i], y = key[jx];
+            if (desc ? (x < y) : (x > y)) {
+              key[i] = y;
+              key[jx] = x;
+            }
+          }
+        }
+        __syncthreads();
+      }
+  }
+  // question of rank r, and its data
+  auto at = [&](int r, int& b) -> Q {
+    if (!cached) {
+      b = r;
+      return question(r);
     }
-  }
-
-  // finalize
-  const float l_tot = l_run + swap_halves(l_run);
-  if (!row_ok) return;
-  const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
-  const size_t obase = ((size_t)(k0 + r) * H + h) * D;
-  if (o_f32) {
-    float* orow = static_cast<float*>(O) + obase;
+    b = kPlanMaxB - 1 - (int)(key[r] & (kPlanMaxB - 1));
+    return Q{q_k0[b], (int)q_kq[b], q_p0[b], (int)q_P[b], (int)q_nch[b]};
+  };
+  const int groups = B * H;   // B * H * k rows fit in int32 (k_max * P_max bounded)
+  const int runs = (groups + 7) / 8;
+  int carry = 0;
+  for (int m0 = 0; m0 < runs; m0 += kPlanThreads) {
+    const int m = m0 + tid;
+    int ncr = 0;
+    int qb[8];
+    Q qq[8];
 #pragma unroll
-    for (int t = 0; t < DT; ++t)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int f = t * 32 + 8 * g + 4 * hh;
-        float4 w = make_float4(acc[t][4 * g + 0] * inv, acc[t][4 * g + 1] * inv,
-                               acc[t][4 * g + 2] * inv, acc[t][4 * g + 3] * inv);
-        *reinterpret_cast<float4*>(orow + f) = w;
+    for (int i = 0; i < 8; ++i) {
+      const int g = m * 8 + i;
+      qb[i] = -1;
+      qq[i] = Q{0, 0, 0, 0, 0};
+      if (m < runs && g < groups) {
+        qq[i] = at(g / H, qb[i]);
+        ncr = max(ncr, qq[i].nch);
       }
-  } else {
-    bf16_t* orow = static_cast<bf16_t*>(O) + obase;
+    }
+    uint32_t total;
+    const uint32_t pre = block_exclusive_scan((uint32_t)ncr, scan_sh, &total);
+    const int base = 8 * (carry + (int)pre);
+    if (m < runs)
+      for (int c = 0; c < ncr; ++c)
 #pragma unroll
-    for (int t = 0; t < DT; ++t)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int f = t * 32 + 8 * g + 4 * hh;
-        uint2 w;
-        w.x = pack2_bf16(acc[t][4 * g + 0] * inv, acc[t][4 * g + 1] * inv);
-        w.y = pack2_bf16(acc[t][4 * g + 2] * inv, acc[t][4 * g + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + f) = w;
-      }
+        for (int i = 0; i < 8; ++i) {
+          const int id = base + 8 * c + i;
+          if (id >= n_ids) continue;
+          int4 it = make_int4(-1, 0, 0, 0);
+          if (qb[i] >= 0 && c < qq[i].nch) {
+            const Q& q = qq[i];
+            const int rpc = (q.kq + q.nch - 1) / q.nch;
+            const int r0 = c * rpc;
+            const int nrows = min(q.kq, r0 + rpc) - r0;
+            const int h = (m * 8 + i) % H;
+            it = make_int4(qb[i], q.k0 + r0, q.p0, h | (nrows << 8) | (q.P << 16));
+          }
+          items[id] = it;
+        }
+    carry += (int)total;
   }
-  if (lse && hh == 0)
-    lse[(size_t)(k0 + r) * H + h] = (l_tot > 0.f) ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
+  for (int id = 8 * carry + tid; id < n_ids; id += kPlanThreads) items[id] = make_int4(-1, 0, 0, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -688,32 +809,54 @@ attn_f32_kernel(const float* __restrict__ qbase, const int32_t* __restrict__ kep
 }
 
 // ---------------------------------------------------------------------------
+long long attn_plan_ids(const skip_problem_t& p) {
+  if (p.dtype != SKIP_BF16 || p.k_max <= 0 || p.B <= 0 || p.H <= 0) return 0;
+  const long long runs = ((long long)p.B * p.H + 7) / 8;
+  const long long nch = (p.k_max + kSpRows - 1) / kSpRows;
+  return 8 * runs * nch;
+}
+
+hipError_t launch_attention_plan(const skip_problem_t& p, const int32_t* kept_offsets,
+                                 const int32_t* query_passages,
+                                 const int32_t* passage_offsets, int32_t* plan, hipStream_t s) {
+  const long long n_ids = attn_plan_ids(p);
+  if (n_ids == 0) return hipSuccess;
+  if (n_ids > INT32_MAX / 16 || (long long)p.B * p.H > INT32_MAX / 16)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, kept_offsets,
+                     query_passages, passage_offsets, p.B, p.H, p.total_kept,
+                     p.total_passages, p.total_tokens, p.k_max, p.P_max, (int)n_ids,
+                     reinterpret_cast<int4*>(plan));
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const skip_problem_t& p, QuerySource q,
                             const int32_t* kept_offsets, const void* Kh, const void* Vh,
                             const int32_t* passage_offsets, const int32_t* query_passages,
-                            const uint64_t* rowmask, void* O, float* lse, hipStream_t s) {
+                            const uint64_t* rowmask, const int32_t* plan, void* O, float* lse,
+                            hipStream_t s) {
   if (p.k_max <= 0) return hipSuccess;
   const int qstride = p.d;
   if (p.dtype == SKIP_BF16) {
-    const int RB = (p.k_max + kMaxRows - 1) / kMaxRows;
-    const int n_items = p.B * p.H * RB;
-    const int grid = ((n_items + 7) / 8) * 8;
+    const long long n_ids = attn_plan_ids(p);
+    if (n_ids > INT32_MAX / 16 || (long long)p.B * p.H > INT32_MAX / 16)
+      return hipErrorInvalidValue;
+    const int4* items = reinterpret_cast<const int4*>(plan);
     const float sl2 = p.sm_scale * kLog2e;
-#define SKIP_ATTN_BF16(DD, SP)                                                               \
-  hipLaunchKernelGGL((attn_bf16_kernel<DD, SP>), dim3(grid), dim3(kThreads), 0, s,           \
-                     (const bf16_t*)q.base, q.kept_idx, q.N, qstride, kept_offsets,          \
-                     (const bf16_t*)Kh, (const bf16_t*)Vh, passage_offsets, query_passages,  \
-                     rowmask, p.H, p.total_kept, p.total_passages, p.total_tokens, p.k_max,  \
-                     p.P_max, RB, n_items, sl2, O, p.o_f32, lse)
+#define SKIP_ATTN_SPARSE(DD, SP)                                                             \
+  hipLaunchKernelGGL((attn_sparse_kernel<DD, SP>), dim3((unsigned)n_ids), dim3(kSpThreads), \
+                     0, s, (const bf16_t*)q.base, q.kept_idx, q.N, qstride, (const bf16_t*)Kh, \
+                     (const bf16_t*)Vh, passage_offsets, rowmask, items, p.H, p.total_tokens, \
+                     sl2, O, p.o_f32, lse)
     // float32 output: split softmax weights (bf16 hi + lo) for near-fp32 accuracy
     if (p.d_h == 64) {
-      if (p.o_f32) SKIP_ATTN_BF16(64, true);
-      else SKIP_ATTN_BF16(64, false);
+      if (p.o_f32) SKIP_ATTN_SPARSE(64, true);
+      else SKIP_ATTN_SPARSE(64, false);
     } else {
-      if (p.o_f32) SKIP_ATTN_BF16(128, true);
-      else SKIP_ATTN_BF16(128, false);
+      if (p.o_f32) SKIP_ATTN_SPARSE(128, true);
+      else SKIP_ATTN_SPARSE(128, false);
     }
-#undef SKIP_ATTN_BF16
+#undef SKIP_ATTN_SPARSE
   } else {
     dim3 grid((p.k_max * p.H + 3) / 4, p.B);
 #define SKIP_ATTN_F32(DD)                                                                    \

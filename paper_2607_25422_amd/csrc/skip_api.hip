@@ -86,6 +86,7 @@ size_t workspace_size(const skip_problem_t& p) {
   n += align_up((size_t)p.B * S * p.k_max * sizeof(double));            // row norms
   n += align_up((size_t)p.B * S * p.P_max * sizeof(double));            // key norms
   n += align_up((size_t)p.total_kept * sizeof(uint64_t));             // rowmask
+  n += align_up((size_t)attn_plan_ids(p) * 4 * sizeof(int32_t));      // attention work list
   return n;
 }
 
@@ -114,6 +115,7 @@ Workspace carve_workspace(const skip_problem_t& p, void* base) {
   w.qn2 = reinterpret_cast<double*>(take((size_t)p.B * S * p.k_max * sizeof(double)));
   w.kn2 = reinterpret_cast<double*>(take((size_t)p.B * S * p.P_max * sizeof(double)));
   w.rowmask = reinterpret_cast<uint64_t*>(take((size_t)p.total_kept * sizeof(uint64_t)));
+  w.plan = reinterpret_cast<int32_t*>(take((size_t)attn_plan_ids(p) * 4 * sizeof(int32_t)));
   w.bytes = off;
   return w;
 }
@@ -260,8 +262,9 @@ static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh, const v
     SKIP_TRY(launch_edge_select(*p, ep, kept_offsets, query_passages, w.rowmask,
                                 edge_rowptr_out, edge_col_out, s, passage_keep));
   }
+  SKIP_TRY(launch_attention_plan(*p, kept_offsets, query_passages, passage_offsets, w.plan, s));
   SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
-                            w.rowmask, O, lse, s));
+                            w.rowmask, w.plan, O, lse, s));
   return SKIP_OK;
 }
 
@@ -528,8 +531,11 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
                                 gate ? passage_keep : nullptr));
   SKIP_TRY(mark());
   if (work)
+    SKIP_TRY(launch_attention_plan(*p, kept_offsets, query_passages, passage_offsets, w.plan, s));
+  SKIP_TRY(mark());
+  if (work)
     SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
-                              w.rowmask, O, lse, s));
+                              w.rowmask, w.plan, O, lse, s));
   SKIP_TRY(mark());
   return SKIP_OK;
 }

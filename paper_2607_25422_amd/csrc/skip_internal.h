@@ -19,6 +19,7 @@ struct Workspace {
   double* qn2;        // [B][S][k_max] partial squared row norms
   double* kn2;        // [B][S][P_max] partial squared passage-key norms
   uint64_t* rowmask;  // [total_kept]  neighbour passages of each kept row
+  int32_t* plan;      // [attn_plan_ids][4] attention work list
   size_t bytes;
 };
 
@@ -122,11 +123,18 @@ hipError_t launch_csr_to_mask(const skip_problem_t& p, const int32_t* kept_offse
                               const int32_t* query_passages,
                               const int32_t* edge_rowptr, const int32_t* edge_col,
                               uint64_t* rowmask, hipStream_t s);
+// Workgroup ids of the bf16 attention launch (0 for fp32): the work list
+// takes one 16-byte record per id.
+long long attn_plan_ids(const skip_problem_t& p);
+// Work list of the bf16 attention launch (depends on the offsets only).
+hipError_t launch_attention_plan(const skip_problem_t& p, const int32_t* kept_offsets,
+                                 const int32_t* query_passages,
+                                 const int32_t* passage_offsets, int32_t* plan, hipStream_t s);
 hipError_t launch_attention(const skip_problem_t& p, QuerySource q,
                             const int32_t* kept_offsets, const void* Kh,
                             const void* Vh, const int32_t* passage_offsets,
                             const int32_t* query_passages,
-                            const uint64_t* rowmask, void* O, float* lse,
+                            const uint64_t* rowmask, const int32_t* plan, void* O, float* lse,
                             hipStream_t s);
 
 }  // namespace skip
