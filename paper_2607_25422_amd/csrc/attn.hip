@@ -16,18 +16,28 @@
 namespace skip {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 template <int N>
 struct IntC {                     // a compile-time count passed to a generic lambda
   static constexpr int value = N;
 };
+// f(IntC<0>), .., f(IntC<N-1>)
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IntC<I>{});
+    static_for<N, I + 1>(f);
+  }
+}
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-__device__ __forceinline__ f32x16_t mfma32(const u32x4& a, const u32x4& b, f32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+// D (16 x 16, fp32) += A (16 x 32) . B (32 x 16), bf16 operands: lane l holds
+// A[l % 16][8(l / 16) .. +7], B[8(l / 16) .. +7][l % 16] and D[4(l / 16) .. +3][l % 16].
+__device__ __forceinline__ f32x4_t mfma16(const u32x4& a, const u32x4& b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
@@ -68,13 +78,48 @@ __device__ __forceinline__ float swap_halves(float x) {
   return __uint_as_float(__lane_id() < 32 ? r[1] : r[0]);
 }
 
-// Transposing LDS read: in each group of 16 lanes, lane j receives element
-// j & 3 of the 8-byte pieces addressed by lanes (j >> 2) + 4e, e = 0..3.
+// Value of lane l ^ 16 (v_permlane16_swap: odd and even 16-lane rows trade).
+__device__ __forceinline__ float swap16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return __uint_as_float((__lane_id() & 16) ? r[0] : r[1]);
+}
+
+// Transposing LDS read (ds_read_b64_tr_b16) at byte address lds + OFF: in
+// each group of 16 lanes, lane j receives element j & 3 of the 8-byte pieces
+// addressed by lanes (j >> 2) + 4e, e = 0..3.  Issued through inline
+// assembly so that the constant offset sits in the instruction (the builtin
+// takes a full address per read); the compiler does not track its
+// completion, so the results pass through lds_wait_all before any use.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ u32x2 ds_read_tr16(const bf16_t* p) {
-  s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) s16x4_t*)(p));
-  return __builtin_bit_cast(u32x2, v);
+template <int OFF>
+__device__ __forceinline__ u32x2 ds_read_tr16_at(uint32_t lds) {
+  static_assert(OFF >= 0 && OFF < 65536 && OFF % 8 == 0, "DS offset field");
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(lds), "i"(OFF));
+  return r;
+}
+
+// Waits for every outstanding LDS read of the wave; the registers passed
+// through it are the values after the wait (a true dependency for the
+// compiler, so no use of them is scheduled above it).
+template <int N>
+__device__ __forceinline__ void lds_wait_all(u32x2 (&v)[N]) {
+  static_assert(N == 16 || N == 8, "operand count");
+  if constexpr (N == 16) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]),
+                   "+v"(v[6]), "+v"(v[7]), "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]),
+                   "+v"(v[12]), "+v"(v[13]), "+v"(v[14]), "+v"(v[15])
+                 :
+                 : "memory");
+  } else {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]),
+                   "+v"(v[6]), "+v"(v[7])
+                 :
+                 : "memory");
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -110,7 +155,7 @@ constexpr int kSpRows = 192;              // kept rows per work item
 constexpr int kSpTile = 32;               // tokens per K/V tile
 constexpr int kSpStages = 3;              // K (and V) tiles resident in LDS
 constexpr int kSpRegTiles = 4;            // K (and V) tiles in flight in loader registers
-constexpr int kSpCompute = kSpRows / 32;  // compute waves (one 32-row block each)
+constexpr int kSpCompute = kSpRows / 32;  // compute waves (two 16-row blocks each)
 constexpr int kSpWaves = kSpCompute + 2;  // + a K loader and a V loader
 constexpr int kSpThreads = 64 * kSpWaves;
 constexpr int kSpMaxP = 64;
@@ -144,13 +189,17 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
                    float* __restrict__ lse) {
   constexpr int NCH = D / 8;               // 16-byte chunks per token row
   constexpr int NC4 = D / 4;               // 4-float chunks per accumulator row
-  constexpr int KB = D / 16;               // k-blocks of QK^T
-  constexpr int DT = D / 32;               // 32-wide feature tiles of O
-  constexpr int TILE = kSpTile * D;        // elements per K (or V) tile
-  constexpr int NI = kSpTile * NCH / 64;   // 1 KiB direct loads per K (or V) tile
-  auto vswz = [](int row) { return (NCH >= 16 ? 4 : 2) * (row & 3); };
-  __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kSpStages * TILE];
-  __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kSpStages * TILE];
+  constexpr int KB = D / 32;               // k-blocks of QK^T (32 features each)
+  constexpr int DB = D / 16;               // 16-wide feature blocks of O
+  // Tiles are token-major with padded rows: K rows of D + 8 elements put the
+  // sixteen tokens of one S^T operand read on distinct banks, V rows of D +
+  // 16 the sixteen tokens of one transposing read (two 8-byte pieces each);
+  // every operand read is then a register base plus an immediate offset.
+  constexpr int SK = D + 8, SV = D + 16;   // row strides (elements)
+  constexpr int TK = kSpTile * SK, TV = kSpTile * SV;
+  constexpr int NI = kSpTile * NCH / 64;   // 16-byte loads per lane per K (or V) tile
+  __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kSpStages * TK];
+  __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kSpStages * TV];
   __shared__ __attribute__((aligned(16))) float Oacc[kSpRows * D];
   __shared__ float m_acc[kSpRows], l_acc[kSpRows], lx_acc[kSpRows];
   __shared__ uint64_t rmask[3][kSpMaxP];   // rows 64w..64w+63 adjacent to each passage
@@ -168,8 +217,6 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
-  const int col = lane & 31;
-  const int hh = lane >> 5;
 
   // accumulators, passage ranges, row sources, row masks per passage
   const uint64_t pm = (P >= 64) ? ~0ull : ((1ull << P) - 1ull);
@@ -236,24 +283,21 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
     const bool isV = wave == kSpCompute + 1;
     const bf16_t* gsrc = isV ? Vh : Kh;
     bf16_t* buf = isV ? Vbuf : Kbuf;
-    // lane offsets of the tile's 16-byte chunks from the tile's first token:
-    // instruction q fills LDS bytes [q*1024, +1024) of the stage, lane l's
-    // slot o = q*64 + l being (token row, physical chunk); K holds logical
-    // chunk p ^ (row % NCH) there, V logical chunk p ^ vswz(row)
+    const int S = isV ? SV : SK, T = isV ? TV : TK;
+    // load q of a tile: lane l takes 16-byte chunk (q*64 + l) % NCH of token
+    // row (q*64 + l) / NCH; byte offsets from the tile's first token
     uint32_t voff[NI];
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
       const int o = q * 64 + lane;
-      const int row = o / NCH, pch = o % NCH;
-      const int ch = isV ? (pch ^ vswz(row)) : (pch ^ (row & (NCH - 1)));
-      voff[q] = (uint32_t)((row * H * D + ch * 8) * 2);
+      voff[q] = (uint32_t)(((o / NCH) * H * D + (o % NCH) * 8) * 2);
     }
+    const int lds_lane = (lane / NCH) * S + (lane % NCH) * 8;
     const bf16_t* hsrc = gsrc + (size_t)h * D;
     // Tiles travel through registers: global loads run kSpRegTiles tiles
     // ahead of the LDS ring (which holds the tile being consumed and the next
     // one), so the loads keep streaming while the compute waves merge or
-    // start a passage.  Slot n % kSpRegTiles holds tile n; the register
-    // layout is the LDS layout (lane l writes bytes 16 l of each 1 KiB).
+    // start a passage.  Slot n % kSpRegTiles holds tile n.
     u32x4 rg[kSpRegTiles][NI];
     auto gload = [&](auto slot, int t, int te_) {
       const bf16_t* tbase = hsrc + (size_t)t * H * D;
@@ -271,10 +315,10 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
       asm volatile("" ::: "memory");
     };
     auto swrite = [&](auto slot, int n) {
-      bf16_t* dst = buf + (n % kSpStages) * TILE;
+      bf16_t* dst = buf + (n % kSpStages) * T + lds_lane;
 #pragma unroll
       for (int q = 0; q < NI; ++q)
-        *reinterpret_cast<u32x4*>(dst + q * 512 + lane * 8) = rg[decltype(slot)::value][q];
+        *reinterpret_cast<u32x4*>(dst + q * (64 / NCH) * S) = rg[decltype(slot)::value][q];
     };
     // Every step issues one tile's loads, unconditionally (past the last
     // tile the cursor stays put and the last tile is read again), so that
@@ -321,128 +365,245 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
     }
   } else {
     // ---- compute waves ------------------------------------------------------
-    const int g16 = lane >> 4, s16 = lane & 15;
-    int koff[KB];                                   // K row col, chunk 2kb+hh
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-      koff[kb] = col * D + (((2 * kb + hh) ^ (col & (NCH - 1))) << 3);
-    const int tr_tok = 4 * hh + (s16 >> 2);        // V^T operand, transposing reads
-    int voff[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const int d = 32 * dt + 16 * (g16 & 1) + 4 * (s16 & 3);
-      voff[dt] = tr_tok * D + (((d >> 3) ^ vswz(tr_tok)) << 3) + (d & 7);
-    }
+    // Lane layout of every product (16 x 16 blocks): r16 = lane & 15 is the
+    // lane's row within a block (the column of S^T, P^T and O^T); g = lane
+    // >> 4 picks tokens 4g..4g+3 of each 16-token half of S^T, the k-slice
+    // 8g..8g+7 of P^T (those same eight tokens, halves in order) and
+    // features 16db + 4g..4g+3 of O^T.
+    const int g = lane >> 4;
+    const int r16 = lane & 15;
+    // K (A of S^T): token r16 (+16), features 32kb + 8g .. +7
+    const int koff = r16 * SK + 8 * g;
+    // V^T (A of O^T) by transposing reads: lane (e = r16 >> 2, q = r16 & 3)
+    // addresses token 4g + e (+16), features 16db + 4q .. +3; lane r16 then
+    // holds feature 16db + r16 of tokens 4g .. 4g+3
+    const uint32_t vlds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(
+        Vbuf + (4 * g + (r16 >> 2)) * SV + 4 * (r16 & 3));
     // a negative scale is folded into the queries (bf16 sign flips), so the
     // logits are scaled by |scale| and their maximum is a plain maximum
     const uint32_t neg = (scale_log2 < 0.f) ? 0x80008000u : 0u;
     const float sc = fabsf(scale_log2);
-    // touched passages in which this wave has a block
-    const uint64_t bmask =
-        uniform64(__ballot(lane < P && ((U >> lane) & 1ull) && p_cnt[lane] > 32 * wave));
-    // Queries of the block's rows.  For the wave's busy passages in order:
-    // at the first tile of busy passage k, qf takes passage k's queries from
-    // qn, and qn is refilled (unconditionally, so the loads land in qn's own
-    // registers and stay in flight) with passage k+1's, whose rows were looked
-    // up during passage k-1; the lookup of passage k+2 then runs in phases,
-    // one per step, each LDS read consumed a step after it is issued: (1) the
-    // passage's row masks, (2) this lane's row (the n-th adjacent row, n = 32
-    // * wave + col) and its visual-token index.  A lane past the block's rows
-    // loads a placeholder row, whose scores land in a column that is never
-    // merged.
-    u32x4 qn[KB], qf[KB];
+    // Touched passages in which this wave has its first block (block `wave`)
+    // and its second (block wave + kSpCompute).
+    const uint64_t bmask = uniform64(
+        __ballot(lane < P && ((U >> lane) & 1ull) && p_cnt[lane] > 16 * wave));
+    const uint64_t bmask2 = uniform64(__ballot(
+        lane < P && ((U >> lane) & 1ull) && p_cnt[lane] > 16 * (wave + kSpCompute)));
+    // Queries of the blocks' rows go straight into qf.  For the wave's busy
+    // passages in order: at the first tile of busy passage k the lookup of
+    // busy passage k+1 starts and runs in phases, one per step: (1) the
+    // passage's row masks, (2) this lane's rows (the n-th adjacent row, n =
+    // 16 * block + r16) and their visual-token indices.  At passage k's last
+    // tile, once its S^T products have read qf, the lookup is finished and
+    // the loads of passage k+1's queries are issued into qf; they land while
+    // that tile's softmax, PV product and merge run.  A lane past a block's
+    // rows loads a placeholder row, whose scores land in a column that is
+    // never merged.
+    u32x4 qf[2][KB];
     int lk_j = -1, lk_phase = 2;       // passage being looked up; phases done (2: done)
     uint64_t lkw0 = 0, lkw1 = 0, lkw2 = 0;
-    int lk_row = -1, lk_src = 0;       // result of the lookup
-    int qn_row = -1;                   // row of the queries in qn
+    int lk_row[2] = {-1, -1}, lk_src[2] = {0, 0};   // result of the lookup
+    int nx_row[2] = {-1, -1};          // rows of the queries in qf for the next passage
+    auto nth_row = [&](int n) -> int {
+      const int c0 = __popcll(lkw0), c1 = __popcll(lkw1), c2 = __popcll(lkw2);
+      if (n >= c0 + c1 + c2) return -1;
+      if (n < c0) return nth_bit64(lkw0, n);
+      if (n < c0 + c1) return 64 + nth_bit64(lkw1, n - c0);
+      return 128 + nth_bit64(lkw2, n - c0 - c1);
+    };
     auto lookup_phase = [&]() {
       if (lk_phase == 0) {
         lkw0 = uniform64(rmask[0][lk_j]);
         lkw1 = uniform64(rmask[1][lk_j]);
         lkw2 = uniform64(rmask[2][lk_j]);
       } else {
-        const int n = 32 * wave + col;
-        const int c0 = __popcll(lkw0), c1 = __popcll(lkw1), c2 = __popcll(lkw2);
-        if (n >= c0 + c1 + c2) lk_row = -1;
-        else if (n < c0) lk_row = nth_bit64(lkw0, n);
-        else if (n < c0 + c1) lk_row = 64 + nth_bit64(lkw1, n - c0);
-        else lk_row = 128 + nth_bit64(lkw2, n - c0 - c1);
-        lk_src = kept_idx ? qsrc[lk_row >= 0 ? lk_row : 0] : 0;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          lk_row[k] = nth_row(16 * (wave + k * kSpCompute) + r16);
+          lk_src[k] = kept_idx ? qsrc[lk_row[k] >= 0 ? lk_row[k] : 0] : 0;
+        }
       }
       ++lk_phase;
     };
-    auto start_lookup = [&](int j) {   // j < 0: nothing (placeholder row)
+    auto start_lookup = [&](int j) {   // j < 0: nothing
       lk_j = j;
-      lk_phase = 0;
-      lk_row = -1;
-      lk_src = 0;
-      if (j < 0) lk_phase = 2;
+      lk_phase = j < 0 ? 2 : 0;
     };
-    auto load_q = [&]() {              // qn <- the looked-up rows' queries
-      qn_row = lk_row;
-      const int rr = lk_row >= 0 ? lk_row : 0;
-      const bf16_t* qrow = kept_idx
-          ? qbase + ((size_t)b * N + lk_src) * qstride + (size_t)h * D
-          : qbase + (size_t)(row0 + rr) * qstride + (size_t)h * D;
+    // qf <- the queries of the looked-up passage's rows (its second block
+    // only where this wave has one)
+    auto load_q = [&]() {
+      if (lk_j < 0) return;
+      while (lk_phase < 2) lookup_phase();
+      const bool two_next = (bmask2 >> lk_j) & 1ull;
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        qn[kb] = *reinterpret_cast<const u32x4*>(qrow + kb * 16 + 8 * hh);
+      for (int k = 0; k < 2; ++k) {
+        if (k == 1 && !two_next) break;
+        nx_row[k] = lk_row[k];
+        const int rr = lk_row[k] >= 0 ? lk_row[k] : 0;
+        const bf16_t* qrow = kept_idx
+            ? qbase + ((size_t)b * N + lk_src[k]) * qstride + (size_t)h * D
+            : qbase + (size_t)(row0 + rr) * qstride + (size_t)h * D;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          qf[k][kb] = *reinterpret_cast<const u32x4*>(qrow + 32 * kb + 8 * g);
+      }
     };
-    // first and second busy passages
-    const int busy0 = bmask ? __builtin_ctzll(bmask) : -1;
-    const uint64_t after0 = busy0 >= 0 ? (bmask & (bmask - 1ull)) : 0ull;
-    start_lookup(busy0);
-    while (lk_phase < 2) lookup_phase();
+    start_lookup(bmask ? __builtin_ctzll(bmask) : -1);
     load_q();
-    start_lookup(after0 ? __builtin_ctzll(after0) : -1);
 
-    int acc_row = -1;                  // row of this lane's column in the current block
-    f32x16_t acc[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[dt][v] = 0.f;
-    // row sums: of the weights as rounded for the PV product (normalises O)
-    // and of the exact weights (the log-sum-exp)
-    float m_run = -INFINITY, l_run = 0.f, lx_run = 0.f;
+    // per block: row of this lane's column, O^T partial, running maximum and
+    // row sums (of the weights as rounded for the PV product, which
+    // normalises O, and of the exact weights, for the LSE; both per lane
+    // until the merge)
+    int acc_row[2] = {-1, -1};
+    f32x4_t acc[2][DB];
+    float m_run[2], l_run[2], lx_run[2];
 
-    // acc's block partial into the item's accumulators: the row's sixteen
-    // 16-byte pieces read in two batches of eight, rescaled, written back
-    auto merge = [&]() {
-      const float l_tot = l_run + swap_halves(l_run);
-      const float lx_tot = lx_run + swap_halves(lx_run);
-      if (acc_row < 0) return;
-      const int ri = acc_row;
+    // a block's partial into the item's accumulators
+    auto merge = [&](auto kk) {
+      constexpr int k = decltype(kk)::value;
+      float l_tot = l_run[k] + swap16(l_run[k]);
+      float lx_tot = lx_run[k] + swap16(lx_run[k]);
+      l_tot += swap_halves(l_tot);
+      lx_tot += swap_halves(lx_tot);
+      const int ri = acc_row[k];
+      if (ri < 0) return;
       const float mo = m_acc[ri], lo = l_acc[ri], lxo = lx_acc[ri];
       float4* orow = reinterpret_cast<float4*>(Oacc + ri * D);
-      const float mn = fmaxf(mo, m_run);
+      const float mn = fmaxf(mo, m_run[k]);
       const float a = __builtin_amdgcn_exp2f(mo - mn);    // 0 while the row is empty
-      const float cb = __builtin_amdgcn_exp2f(m_run - mn);
+      const float cb = __builtin_amdgcn_exp2f(m_run[k] - mn);
+      float4 ov[DB];                    // features 16db + 4g .. +3
 #pragma unroll
-      for (int half = 0; half < DT; half += 2) {
-        float4 ov[2][4];                  // features 4q .. 4q+3, q = 8dt + 2g4 + hh
+      for (int db = 0; db < DB; ++db) ov[db] = orow[(4 * db + g) ^ (ri & (NC4 - 1))];
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4)
-            ov[u][g4] = orow[((half + u) * 8 + 2 * g4 + hh) ^ (ri & (NC4 - 1))];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4) {
-            const int dt = half + u;
-            float4 o = ov[u][g4];
-            o.x = fmaf(o.x, a, acc[dt][4 * g4 + 0] * cb);
-            o.y = fmaf(o.y, a, acc[dt][4 * g4 + 1] * cb);
-            o.z = fmaf(o.z, a, acc[dt][4 * g4 + 2] * cb);
-            o.w = fmaf(o.w, a, acc[dt][4 * g4 + 3] * cb);
-            orow[(dt * 8 + 2 * g4 + hh) ^ (ri & (NC4 - 1))] = o;
-          }
+      for (int db = 0; db < DB; ++db) {
+        float4 o = ov[db];
+        o.x = fmaf(o.x, a, acc[k][db][0] * cb);
+        o.y = fmaf(o.y, a, acc[k][db][1] * cb);
+        o.z = fmaf(o.z, a, acc[k][db][2] * cb);
+        o.w = fmaf(o.w, a, acc[k][db][3] * cb);
+        orow[(4 * db + g) ^ (ri & (NC4 - 1))] = o;
       }
-      if (hh == 0) {
+      if (g == 0) {
         m_acc[ri] = mn;
         l_acc[ri] = fmaf(lo, a, l_tot * cb);
         lx_acc[ri] = fmaf(lxo, a, lx_tot * cb);
+      }
+    };
+
+    // One tile for block K0: S^T = K . Q^T (two 16-token halves), online
+    // softmax of each row, O^T += V^T . P^T.  All of a phase's LDS reads are
+    // issued before its products (the V reads before the softmax, which
+    // hides them).  A wave with two blocks in the passage runs them one
+    // after the other.
+    auto tile = [&](auto k0, int stage, int t, int te_, bool first) {
+      constexpr int K0 = decltype(k0)::value;
+      constexpr int NBK = 1;
+      if (first) {
+#pragma unroll
+        for (int k = 0; k < NBK; ++k) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) acc[K0 + k][db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          m_run[K0 + k] = -INFINITY;
+          l_run[K0 + k] = 0.f;
+          lx_run[K0 + k] = 0.f;
+        }
+      }
+      const bf16_t* Ks = Kbuf + stage * TK + koff;
+      u32x4 ka[2][KB];
+#pragma unroll
+      for (int th = 0; th < 2; ++th)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          ka[th][kb] = *reinterpret_cast<const u32x4*>(Ks + th * 16 * SK + 32 * kb);
+      __builtin_amdgcn_sched_barrier(0);
+      f32x4_t s[NBK][2];
+#pragma unroll
+      for (int k = 0; k < NBK; ++k)
+#pragma unroll
+        for (int th = 0; th < 2; ++th) {
+          s[k][th] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) s[k][th] = mfma16(ka[th][kb], qf[K0 + k][kb], s[k][th]);
+        }
+      __builtin_amdgcn_sched_barrier(0);
+      // V reads (DB feature blocks x two 16-token halves) at constant offsets
+      // from one address
+      const uint32_t vaddr = vlds + (uint32_t)(stage * TV * 2);
+      u32x2 vr[2 * DB];
+      static_for<2 * DB>([&](auto c) {
+        constexpr int th = decltype(c)::value & 1, db = decltype(c)::value >> 1;
+        vr[2 * db + th] = ds_read_tr16_at<(th * 16 * SV + 16 * db) * 2>(vaddr);
+      });
+      __builtin_amdgcn_sched_barrier(0);
+      // Online softmax of this lane's row: s[k][th][j] is token 16th + 4g + j
+      // of the tile.  The weights are taken against a reference maximum m_run
+      // that moves only when a tile's maximum exceeds it by more than 2^kLazy
+      // (the weights then stay <= 2^kLazy and acc is rescaled only then, not
+      // on every tile); the row sum l adds the weights as the PV product sees
+      // them (rounded to bf16), so numerator and denominator carry the same
+      // weights, and lx the exact weights (for the LSE).
+      u32x4 pb[NBK], pl[NBK];
+#pragma unroll
+      for (int k = 0; k < NBK; ++k) {
+        if (t + kSpTile > te_) {
+          const int rem = te_ - t - 4 * g;        // tokens 4g + j < rem are valid
+#pragma unroll
+          for (int th = 0; th < 2; ++th)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (16 * th + j >= rem) s[k][th][j] = -INFINITY;
+        }
+        float sm = fmaxf(fmaxf(fmaxf(s[k][0][0], s[k][0][1]), fmaxf(s[k][0][2], s[k][0][3])),
+                         fmaxf(fmaxf(s[k][1][0], s[k][1][1]), fmaxf(s[k][1][2], s[k][1][3])));
+        sm = fmaxf(sm, swap16(sm));
+        sm = fmaxf(sm, swap_halves(sm));
+        const float tmax = sm * sc;                         // the tile has a valid token
+        const bool moved = tmax > m_run[K0 + k] + kLazy;         // always on a block's first tile
+        const float m_new = moved ? tmax : m_run[K0 + k];
+        // acc and the sums are 0 before a block's first tile: nothing to rescale
+        const float alpha =
+            (moved && m_run[K0 + k] != -INFINITY) ? __builtin_amdgcn_exp2f(m_run[K0 + k] - m_new) : 1.f;
+        m_run[K0 + k] = m_new;
+        uint32_t w[4], wl[4];
+        float ls = 0.f, lx = 0.f;
+#pragma unroll
+        for (int th = 0; th < 2; ++th)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(s[k][th][2 * q], sc, -m_new));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(s[k][th][2 * q + 1], sc, -m_new));
+            lx += p0 + p1;
+            const uint32_t pw = pack2_bf16(p0, p1);
+            w[2 * th + q] = pw;
+            if (SPLIT_P) {
+              wl[2 * th + q] = pack2_bf16(p0 - __uint_as_float(pw << 16),
+                                          p1 - __uint_as_float(pw & 0xffff0000u));
+            } else {
+              ls = add_bf16_pair(pw, ls);
+            }
+          }
+        pb[k] = u32x4{w[0], w[1], w[2], w[3]};
+        pl[k] = u32x4{wl[0], wl[1], wl[2], wl[3]};
+        l_run[K0 + k] = fmaf(l_run[K0 + k], alpha, SPLIT_P ? lx : ls);
+        lx_run[K0 + k] = fmaf(lx_run[K0 + k], alpha, lx);
+        if (__any(alpha != 1.f)) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) acc[K0 + k][db] *= alpha;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // O^T += V^T . P^T
+      lds_wait_all(vr);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const u32x4 va = __builtin_shufflevector(vr[2 * db], vr[2 * db + 1], 0, 1, 2, 3);
+#pragma unroll
+        for (int k = 0; k < NBK; ++k) {
+          acc[K0 + k][db] = mfma16(va, pb[k], acc[K0 + k][db]);
+          if (SPLIT_P) acc[K0 + k][db] = mfma16(va, pl[k], acc[K0 + k][db]);
+        }
       }
     };
 
@@ -450,123 +611,35 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
     for (int i = 0; i < n_tiles; ++i) {
       advance(cc);
       const bool busy = (bmask >> cc.j) & 1ull;
+      const bool two = (bmask2 >> cc.j) & 1ull;
       const bool first = cc.t == cc.ts;
+      const bool last = cc.t + kSpTile >= cc.te;   // the passage's last tile
       if (busy && first) {
-        // this passage's queries (sign of a negative scale folded in), then
-        // the next busy passage's loads into qn (its lookup finishes here if
-        // the previous passage was too short for it), then the lookup of the
-        // one after
-        acc_row = qn_row;
+        // this passage's queries are in qf (a negative scale's sign folded
+        // in here); the lookup of the next busy passage starts
+        acc_row[0] = nx_row[0];
+        acc_row[1] = nx_row[1];
+        if (neg) {
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) qf[kb] = qn[kb] ^ neg;
+          for (int k = 0; k < 2; ++k)
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) asm volatile("" ::"v"(qf[kb]) : "memory");
-        while (lk_phase < 2) lookup_phase();
-        load_q();
+            for (int kb = 0; kb < KB; ++kb) qf[k][kb] ^= neg;
+        }
         const uint64_t rest = bmask & cc.rem;
-        const uint64_t after = rest ? (rest & (rest - 1ull)) : 0ull;
-        start_lookup(after ? __builtin_ctzll(after) : -1);
+        start_lookup(rest ? __builtin_ctzll(rest) : -1);
       } else if (lk_phase < 2) {
         lookup_phase();
       }
       barrier_nofence();               // tile i has landed
       if (!busy) continue;
       const int stage = i % kSpStages;
-      if (first) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[dt][v] = 0.f;
-        m_run = -INFINITY;
-        l_run = 0.f;
-        lx_run = 0.f;
+      tile(IntC<0>{}, stage, cc.t, cc.te, first);
+      if (two) tile(IntC<1>{}, stage, cc.t, cc.te, first);
+      if (last) {
+        load_q();                      // the next busy passage's queries
+        merge(IntC<0>{});
+        if (two) merge(IntC<1>{});
       }
-      // S^T = K . Q^T
-      const bf16_t* Ks = Kbuf + stage * TILE;
-      u32x4 ka[KB];
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) ka[kb] = *reinterpret_cast<const u32x4*>(Ks + koff[kb]);
-      f32x16_t sacc;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) sacc = mfma32(ka[kb], qf[kb], sacc);
-      // Online softmax of this lane's row: accumulator element v holds token
-      // 8*(v/4) + 4*hh + v%4 of the tile.  The weights are taken against a
-      // reference maximum m_run that moves only when a tile's maximum exceeds
-      // it by more than 2^kLazy (the weights then stay <= 2^kLazy and acc is
-      // rescaled only then, not on every tile); the row sum l adds the
-      // weights as the PV product sees them (rounded to bf16), so numerator
-      // and denominator carry the same weights, and lx the exact weights
-      // (for the LSE).
-      if (cc.t + kSpTile > cc.te) {
-        const int rem = cc.te - cc.t - 4 * hh;
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (8 * (v >> 2) + (v & 3) >= rem) sacc[v] = -INFINITY;
-      }
-      float sm = fmaxf(fmaxf(fmaxf(sacc[0], sacc[1]), fmaxf(sacc[2], sacc[3])),
-                       fmaxf(fmaxf(sacc[4], sacc[5]), fmaxf(sacc[6], sacc[7])));
-      sm = fmaxf(sm, fmaxf(fmaxf(fmaxf(sacc[8], sacc[9]), fmaxf(sacc[10], sacc[11])),
-                           fmaxf(fmaxf(sacc[12], sacc[13]), fmaxf(sacc[14], sacc[15]))));
-      sm = fmaxf(sm, swap_halves(sm));
-      const float tmax = sm * sc;                          // the tile has a valid token
-      const bool moved = tmax > m_run + kLazy;             // always on a block's first tile
-      const float m_new = moved ? tmax : m_run;
-      // acc and the sums are 0 before a block's first tile: nothing to rescale
-      const float alpha =
-          (moved && m_run != -INFINITY) ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
-      m_run = m_new;
-      u32x4 pb[2], pl[2];
-      float ls = 0.f, lx = 0.f;
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
-        uint32_t w[4], wl[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[8 * kb2 + 2 * q], sc, -m_new));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[8 * kb2 + 2 * q + 1], sc, -m_new));
-          lx += p0 + p1;
-          w[q] = pack2_bf16(p0, p1);
-          if (SPLIT_P) {
-            wl[q] = pack2_bf16(p0 - __uint_as_float(w[q] << 16),
-                               p1 - __uint_as_float(w[q] & 0xffff0000u));
-          } else {
-            ls = add_bf16_pair(w[q], ls);
-          }
-        }
-        pb[kb2] = u32x4{w[0], w[1], w[2], w[3]};
-        if (SPLIT_P) pl[kb2] = u32x4{wl[0], wl[1], wl[2], wl[3]};
-      }
-      l_run = fmaf(l_run, alpha, SPLIT_P ? lx : ls);
-      lx_run = fmaf(lx_run, alpha, lx);
-      if (__any(alpha != 1.f)) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[dt][v] *= alpha;
-      }
-      // O^T += V^T . P^T (V^T by transposing reads in the token order of S^T)
-      const bf16_t* Vs = Vbuf + stage * TILE;
-      u32x4 va[DT][2];
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-          const bf16_t* vp = Vs + 16 * g * D + voff[dt];
-          va[dt][g] = __builtin_shufflevector(ds_read_tr16(vp), ds_read_tr16(vp + 8 * D),
-                                              0, 1, 2, 3);
-        }
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        acc[dt] = mfma32(va[dt][0], pb[0], acc[dt]);
-        acc[dt] = mfma32(va[dt][1], pb[1], acc[dt]);
-        if (SPLIT_P) {
-          acc[dt] = mfma32(va[dt][0], pl[0], acc[dt]);
-          acc[dt] = mfma32(va[dt][1], pl[1], acc[dt]);
-        }
-      }
-      if (cc.t + kSpTile >= cc.te) merge();    // the passage's last tile
     }
   }
   __syncthreads();
