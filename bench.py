@@ -40,8 +40,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="highres_bf16")
     ap.add_argument("--seed", type=int, default=2026)
-    ap.add_argument("--cpu-sample", type=int, default=12,
-                    help="questions of the batch the CPU oracle is timed on (0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=-1,
+                    help="questions of the batch the CPU oracle is timed on (-1, the "
+                         "default: the whole batch; 0: skip)")
+    ap.add_argument("--no-companion", action="store_true",
+                    help="with the default workload, skip the nested mixed_bf16 record")
     ap.add_argument("--avg-degree", type=float, default=None,
                     help="override the workload's average degree (edges per kept row)")
     ap.add_argument("--edge-rule", default="question", choices=["question", "row", "fraction"],
@@ -443,26 +446,10 @@ def bench_regions(args):
     print(json.dumps(res), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the routing core runs on a single MI355X; see the sharding notes)",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.scorer == "mlp":
-        bench_mlp_scorer(args)
-        return
-    if args.gate:
-        bench_gated_route(args)
-        return
-    if args.regions:
-        bench_regions(args)
-        return
-    if args.project:
-        bench_project(args)
-        return
-
+def measure_route(args, workload):
+    """The fused route on one workload: `steps` timed steps (after `warmup`),
+    then a profiled pass with stage events.  Returns (record, batch, device
+    batch, passage keys or None, average degree)."""
     import numpy as np
     import torch
 
@@ -470,10 +457,8 @@ def main():
     from paper_2607_25422_amd import binding as B
     from paper_2607_25422_amd import workloads as wls
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    print(f"[bench] generating {args.workload} seed {args.seed}", file=sys.stderr, flush=True)
-    batch = wls.make_batch(args.workload, args.seed, threads=16)
+    print(f"[bench] generating {workload} seed {args.seed}", file=sys.stderr, flush=True)
+    batch = wls.make_batch(workload, args.seed, threads=16)
     wl = batch.wl
     db = B.to_device(batch, avg_degree=args.avg_degree, edge_rule=args.edge_rule,
                      edge_metric=args.edge_metric, edge_beta=args.edge_beta)
@@ -634,20 +619,64 @@ def main():
         "stages_ms": {k: round(v, 5) for k, v in stages.items()},
     }
 
+    return res, batch, db, pkeys, avg_degree
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the routing core runs on a single MI355X; see the sharding notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.scorer == "mlp":
+        bench_mlp_scorer(args)
+        return
+    if args.gate:
+        bench_gated_route(args)
+        return
+    if args.regions:
+        bench_regions(args)
+        return
+    if args.project:
+        bench_project(args)
+        return
+
+    import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    res, batch, db, pkeys, avg_degree = measure_route(args, args.workload)
+    wl, p = batch.wl, db.p
+    if args.workload == "highres_bf16" and not args.no_companion:
+        # the other N = 2304 configuration, in the same run: the difficulty-
+        # mixed batch, nested as a record of its own
+        comp, cbatch, cdb, _, _ = measure_route(args, "mixed_bf16")
+        res["mixed_bf16"] = {k: comp[k] for k in ("value", "unit", "ms_per_step", "config",
+                                                  "roofline", "attention", "prune",
+                                                  "stages_ms", "step_gpu_ms")}
+        del cbatch, cdb
+        torch.cuda.empty_cache()
+
     if not args.no_ceilings:
         ceil = measure_ceilings(torch)
         res["ceilings"] = ceil
-        res["roofline"]["frac_of_read_ceiling"] = round(attn_gbs / ceil["read_gbs"], 4)
-        res["prune"]["score_frac_of_read_ceiling"] = round(score_gbs / ceil["read_gbs"], 4)
+        res["roofline"]["frac_of_read_ceiling"] = round(
+            res["roofline"]["achieved"] / ceil["read_gbs"], 4)
+        res["prune"]["score_frac_of_read_ceiling"] = round(
+            res["prune"]["score_gbs"] / ceil["read_gbs"], 4)
 
-    if args.cpu_sample > 0:
+    if args.cpu_sample != 0:
         from threadpoolctl import threadpool_limits
 
         import oracle as orc
-        qs = list(range(min(args.cpu_sample, p.B)))
-        print(f"[bench] timing the CPU oracle on {len(qs)} questions", file=sys.stderr,
-              flush=True)
-        with threadpool_limits(1):
+        n_q = p.B if args.cpu_sample < 0 else min(args.cpu_sample, p.B)
+        qs = list(range(n_q))
+        # as many BLAS threads as the process may run on
+        cores = len(os.sched_getaffinity(0))
+        print(f"[bench] timing the CPU oracle on {len(qs)} questions, {cores} threads",
+              file=sys.stderr, flush=True)
+        with threadpool_limits(cores):
             c0 = time.perf_counter()
             orc.route(batch.V, batch.Qtok, batch.q_offsets, batch.kept_offsets, batch.Kh,
                       batch.Vh, batch.passage_offsets, batch.query_passages, wl.scale,
@@ -658,11 +687,12 @@ def main():
         res["cpu_baseline"] = {
             "value": round(len(qs) / (c1 - c0), 4),
             "unit": "queries/s",
-            "cores": 1,
+            "cores": cores,
             "kind": "oracle",
             "sample": (f"{len(qs)} of {p.B} questions of {wl.name} seed {args.seed}: full route "
                        f"(pooling, scoring, top-k, graph, attention of every kept row), float64 "
-                       f"numpy, one thread, {c1 - c0:.1f} s, {cpu_model()}"),
+                       f"numpy, {cores} BLAS threads, {c1 - c0:.1f} s"),
+            "cpu": cpu_model(),
         }
     print(json.dumps(res), flush=True)
 

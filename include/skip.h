@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define SKIP_ABI_VERSION 5
+#define SKIP_ABI_VERSION 6
 
 typedef enum skip_status {
   SKIP_OK = 0,
@@ -302,6 +302,31 @@ skip_status_t skip_gather_project(const skip_problem_t* p, const void* rows,
                                   const int32_t* kept_offsets, const int32_t* kept_idx,
                                   const void* W, int32_t d_out, void* Y, int32_t out_f32,
                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Learned projection of the passage keys (eq. bsca applies W_k to a chunk
+ * key; Def. B.3 calls it h_k): keys_out[j] = W k~_j, where k~_j is the
+ * bfloat16 rounding (through float) of passage j's key: the caller's
+ * passage_keys[j] (float), or, with passage_keys NULL, the mean of the
+ * passage's token keys Kh (as pooled for the graph, in double).  bf16
+ * weights, float32 sums on the matrix cores, float output; the result is the
+ * passage_keys argument of skip_bipartite_xattn_proj when d_out == d.
+ *   Kh, passage_offsets  as in skip_bipartite_xattn (unused with passage_keys)
+ *   passage_keys  [total_passages][d] float, or NULL; 16-byte aligned
+ *   W             [d_out][d] bf16, 16-byte aligned
+ *   d_out         a multiple of 256, at most 65536;  d a multiple of 32
+ *   keys_out      out [total_passages][d_out] float, 16-byte aligned
+ * bf16 problems only (SKIP_ERR_UNSUPPORTED otherwise).  Workspace:
+ * skip_workspace_bytes_project_keys (pooled keys, their bf16 rows and W
+ * repacked).  Nothing is launched when there are no passages.
+ */
+skip_status_t skip_workspace_bytes_project_keys(const skip_problem_t* p, int32_t d_out,
+                                                size_t* bytes);
+skip_status_t skip_project_passage_keys(const skip_problem_t* p, const void* Kh,
+                                        const int32_t* passage_offsets,
+                                        const float* passage_keys, const void* W,
+                                        int32_t d_out, float* keys_out, void* workspace,
+                                        size_t workspace_bytes, void* stream);
 
 /*
  * The same projection in two calls, for callers that apply one W to many

@@ -34,7 +34,8 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_workspace_bytes_regions", "skip_region_kmeans",
                 "skip_workspace_bytes_project", "skip_gather_project",
                 "skip_bipartite_xattn_proj", "skip_pack_projection",
-                "skip_gather_project_packed", "skip_route_fused_noalloc")
+                "skip_gather_project_packed", "skip_route_fused_noalloc",
+                "skip_workspace_bytes_project_keys", "skip_project_passage_keys")
 FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attn_plan",
                 "attention")
 
@@ -136,6 +137,12 @@ def _load() -> ctypes.CDLL:
     lib.skip_gather_project.restype = ctypes.c_int
     lib.skip_gather_project.argtypes = [P, vp, i32p, i32p, vp, ctypes.c_int32, vp,
                                         ctypes.c_int32, vp, ctypes.c_size_t, vp]
+    lib.skip_workspace_bytes_project_keys.restype = ctypes.c_int
+    lib.skip_workspace_bytes_project_keys.argtypes = [P, ctypes.c_int32,
+                                                      ctypes.POINTER(ctypes.c_size_t)]
+    lib.skip_project_passage_keys.restype = ctypes.c_int
+    lib.skip_project_passage_keys.argtypes = [P, vp, i32p, vp, vp, ctypes.c_int32, vp, vp,
+                                              ctypes.c_size_t, vp]
     lib.skip_pack_projection.restype = ctypes.c_int
     lib.skip_pack_projection.argtypes = [P, vp, ctypes.c_int32, vp, ctypes.c_size_t, vp]
     lib.skip_gather_project_packed.restype = ctypes.c_int
@@ -249,6 +256,13 @@ def workspace_bytes_project(p: SkipProblem, d_out: int) -> int:
     n = ctypes.c_size_t(0)
     _check(LIB.skip_workspace_bytes_project(ctypes.byref(p), int(d_out), ctypes.byref(n)),
            "skip_workspace_bytes_project")
+    return int(n.value)
+
+
+def workspace_bytes_project_keys(p: SkipProblem, d_out: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.skip_workspace_bytes_project_keys(ctypes.byref(p), int(d_out), ctypes.byref(n)),
+           "skip_workspace_bytes_project_keys")
     return int(n.value)
 
 
@@ -486,6 +500,22 @@ def skip_gather_project(p: SkipProblem, rows, kept_offsets, kept_idx, W, Y, out_
         d_out, _ptr(Y, "Y", torch.float32 if out_f32 else et, p.total_kept * d_out),
         1 if out_f32 else 0, workspace.data_ptr(), workspace.numel(), _stream(stream))
     _check(st, "skip_gather_project")
+
+
+def skip_project_passage_keys(p: SkipProblem, Kh, passage_offsets, passage_keys, W, keys_out,
+                              workspace=None, stream=None):
+    et = _elem_dtype(p)
+    d_out = int(W.shape[0])
+    if workspace is None:
+        workspace = _fresh_workspace(workspace_bytes_project_keys(p, d_out), W.device, stream)
+    st = LIB.skip_project_passage_keys(
+        ctypes.byref(p), _ptr(Kh, "Kh", et, p.total_tokens * p.d),
+        _ptr(passage_offsets, "passage_offsets", torch.int32, p.total_passages + 1),
+        _ptr(passage_keys, "passage_keys", torch.float32, p.total_passages * p.d),
+        _ptr(W, "W", et, d_out * p.d),
+        d_out, _ptr(keys_out, "keys_out", torch.float32, p.total_passages * d_out),
+        workspace.data_ptr(), workspace.numel(), _stream(stream))
+    _check(st, "skip_project_passage_keys")
 
 
 def skip_pack_projection(p: SkipProblem, W, packed, stream=None):
@@ -813,6 +843,17 @@ def gather_project(db: DeviceBatch, rows: torch.Tensor, W: torch.Tensor, kept_id
     skip_gather_project(p, rows if p.total_kept else None, db.kept_offsets, kept_idx, W,
                         Y if p.total_kept else None, out_f32, workspace)
     return Y[:p.total_kept]
+
+
+def project_passage_keys(db: DeviceBatch, W: torch.Tensor, passage_keys=None):
+    """h_k = W k~_j for every passage (k~ the bf16 rounding of the pooled key,
+    or of ``passage_keys``).  Returns [total_passages, d_out] float32."""
+    p = db.p
+    out = torch.empty((max(p.total_passages, 1), int(W.shape[0])), dtype=torch.float32,
+                      device=db.V.device)
+    skip_project_passage_keys(p, db.Kh if p.total_tokens else None, db.passage_offsets,
+                              passage_keys, W, out if p.total_passages else None)
+    return out[:p.total_passages]
 
 
 def pack_projection(db: DeviceBatch, W: torch.Tensor) -> torch.Tensor:

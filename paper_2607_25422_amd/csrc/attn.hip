@@ -64,13 +64,6 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Sum of the two bf16 halves of a packed pair, added to c (v_dot2c_f32_bf16
-// against (1, 1): the products are exact, the sum is taken in float32).
-__device__ __forceinline__ float add_bf16_pair(uint32_t w, float c) {
-  const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), one, c, false);
-}
-
 // Value of lane l ^ 32 (v_permlane32_swap: the two half-waves trade places).
 __device__ __forceinline__ float swap_halves(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
@@ -135,22 +128,24 @@ __device__ __forceinline__ void lds_wait_all(u32x2 (&v)[N]) {
 // through two LDS rings of three tiles, one barrier per tile; two loader
 // waves (one for K, one for V) keep four more tiles in flight in registers
 // and write each into the ring when its slot frees.  For each passage the
-// adjacent rows (a 192-bit row mask per passage) form blocks of 32 in row
-// order; compute wave w takes block w.  Per tile and block:
-//   S^T (32 tokens x 32 rows) = K_tile . Q^T        v_mfma_f32_32x32x16_bf16
-//   online softmax in fp32 (base 2), P rounded to bf16,
-//   O^T (d_h x 32 rows)     += V_tile^T . P^T       v_mfma_f32_32x32x16_bf16
+// adjacent rows (a 192-bit row mask per passage) form blocks of 16 in row
+// order; compute wave w takes blocks w and w + 6.  Per tile and block:
+//   S^T (32 tokens x 16 rows) = K_tile . Q^T        v_mfma_f32_16x16x32_bf16
+//   online softmax in fp32 (base 2); each weight p split into bf16 hi + lo
+//   (hi = p rounded, lo = the rest rounded), so the PV product sees p to
+//   about 2^-16 relative and the result does not depend on the output type,
+//   O^T (d_h x 16 rows)     += V_tile^T . (P_hi + P_lo)^T
 // Computing the transposed products keeps each query row in one lane column
-// (row statistics need only an exchange between the two half waves) and
+// (row statistics need an exchange among the four lanes of that column) and
 // makes the S^T accumulator the P^T operand; V^T comes from transposing LDS
-// reads in the token order of that layout.  Q of the block's rows sits in
-// registers, loaded one busy passage ahead.  After a passage's last tile
-// each block's partial (O, max, sums) is merged into the item's
-// accumulators, fp32 in LDS for every row of the chunk, by log-sum-exp
-// rescaling; one passage's blocks hold disjoint rows and passages merge in
-// ascending order (a barrier at least between two), so the result is
-// deterministic.  The item ends by writing O = acc / sum and LSE for every
-// row of the chunk (0 and -inf for a row without neighbours).
+// reads in the token order of that layout.  The queries of a block's rows
+// sit in registers, loaded at the previous busy passage's last tile.  After
+// a passage's last tile each block's partial (O, max, sum) is merged into
+// the item's accumulators, fp32 in LDS for every row of the chunk, by
+// log-sum-exp rescaling; one passage's blocks hold disjoint rows and
+// passages merge in ascending order (a barrier at least between two), so the
+// result is deterministic.  The item ends by writing O = acc / sum and LSE
+// for every row of the chunk (0 and -inf for a row without neighbours).
 constexpr int kSpRows = 192;              // kept rows per work item
 constexpr int kSpTile = 32;               // tokens per K/V tile
 constexpr int kSpStages = 3;              // K (and V) tiles resident in LDS
@@ -179,7 +174,7 @@ __device__ __forceinline__ int nth_bit64(uint64_t x, int n) {
 
 // Work item record: {question, first kept row (global), first passage,
 // head | rows << 8 | passages << 16}; question -1: no item.
-template <int D, bool SPLIT_P>
+template <int D>
 __global__ void __launch_bounds__(kSpThreads)
 attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__ kept_idx,
                    int N, int qstride, const bf16_t* __restrict__ Kh,
@@ -201,7 +196,7 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
   __shared__ __attribute__((aligned(1024))) bf16_t Kbuf[kSpStages * TK];
   __shared__ __attribute__((aligned(1024))) bf16_t Vbuf[kSpStages * TV];
   __shared__ __attribute__((aligned(16))) float Oacc[kSpRows * D];
-  __shared__ float m_acc[kSpRows], l_acc[kSpRows], lx_acc[kSpRows];
+  __shared__ float m_acc[kSpRows], l_acc[kSpRows];
   __shared__ uint64_t rmask[3][kSpMaxP];   // rows 64w..64w+63 adjacent to each passage
   __shared__ int p_ts[kSpMaxP], p_te[kSpMaxP], p_cnt[kSpMaxP];
   __shared__ int32_t qsrc[kSpRows];        // visual-token index of each row (fused route)
@@ -229,7 +224,6 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
   if (tid < nrows) {
     m_acc[tid] = -INFINITY;
     l_acc[tid] = 0.f;
-    lx_acc[tid] = 0.f;
     qsrc[tid] = clampi(src, 0, N - 1);
   }
   if (tid < P) {
@@ -452,23 +446,19 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
     load_q();
 
     // per block: row of this lane's column, O^T partial, running maximum and
-    // row sums (of the weights as rounded for the PV product, which
-    // normalises O, and of the exact weights, for the LSE; both per lane
-    // until the merge)
+    // row sum of the weights (per lane until the merge)
     int acc_row[2] = {-1, -1};
     f32x4_t acc[2][DB];
-    float m_run[2], l_run[2], lx_run[2];
+    float m_run[2], l_run[2];
 
     // a block's partial into the item's accumulators
     auto merge = [&](auto kk) {
       constexpr int k = decltype(kk)::value;
       float l_tot = l_run[k] + swap16(l_run[k]);
-      float lx_tot = lx_run[k] + swap16(lx_run[k]);
       l_tot += swap_halves(l_tot);
-      lx_tot += swap_halves(lx_tot);
       const int ri = acc_row[k];
       if (ri < 0) return;
-      const float mo = m_acc[ri], lo = l_acc[ri], lxo = lx_acc[ri];
+      const float mo = m_acc[ri], lo = l_acc[ri];
       float4* orow = reinterpret_cast<float4*>(Oacc + ri * D);
       const float mn = fmaxf(mo, m_run[k]);
       const float a = __builtin_amdgcn_exp2f(mo - mn);    // 0 while the row is empty
@@ -488,7 +478,6 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
       if (g == 0) {
         m_acc[ri] = mn;
         l_acc[ri] = fmaf(lo, a, l_tot * cb);
-        lx_acc[ri] = fmaf(lxo, a, lx_tot * cb);
       }
     };
 
@@ -507,7 +496,6 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
           for (int db = 0; db < DB; ++db) acc[K0 + k][db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
           m_run[K0 + k] = -INFINITY;
           l_run[K0 + k] = 0.f;
-          lx_run[K0 + k] = 0.f;
         }
       }
       const bf16_t* Ks = Kbuf + stage * TK + koff;
@@ -541,9 +529,7 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
       // of the tile.  The weights are taken against a reference maximum m_run
       // that moves only when a tile's maximum exceeds it by more than 2^kLazy
       // (the weights then stay <= 2^kLazy and acc is rescaled only then, not
-      // on every tile); the row sum l adds the weights as the PV product sees
-      // them (rounded to bf16), so numerator and denominator carry the same
-      // weights, and lx the exact weights (for the LSE).
+      // on every tile).
       u32x4 pb[NBK], pl[NBK];
 #pragma unroll
       for (int k = 0; k < NBK; ++k) {
@@ -566,28 +552,25 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
         const float alpha =
             (moved && m_run[K0 + k] != -INFINITY) ? __builtin_amdgcn_exp2f(m_run[K0 + k] - m_new) : 1.f;
         m_run[K0 + k] = m_new;
+        // each weight as a bf16 pair hi + lo (hi its rounding, lo the
+        // rounding of the rest), both fed to the PV product
         uint32_t w[4], wl[4];
-        float ls = 0.f, lx = 0.f;
+        float ls = 0.f;
 #pragma unroll
         for (int th = 0; th < 2; ++th)
 #pragma unroll
           for (int q = 0; q < 2; ++q) {
             const float p0 = __builtin_amdgcn_exp2f(fmaf(s[k][th][2 * q], sc, -m_new));
             const float p1 = __builtin_amdgcn_exp2f(fmaf(s[k][th][2 * q + 1], sc, -m_new));
-            lx += p0 + p1;
+            ls += p0 + p1;
             const uint32_t pw = pack2_bf16(p0, p1);
             w[2 * th + q] = pw;
-            if (SPLIT_P) {
-              wl[2 * th + q] = pack2_bf16(p0 - __uint_as_float(pw << 16),
-                                          p1 - __uint_as_float(pw & 0xffff0000u));
-            } else {
-              ls = add_bf16_pair(pw, ls);
-            }
+            wl[2 * th + q] = pack2_bf16(p0 - __uint_as_float(pw << 16),
+                                        p1 - __uint_as_float(pw & 0xffff0000u));
           }
         pb[k] = u32x4{w[0], w[1], w[2], w[3]};
         pl[k] = u32x4{wl[0], wl[1], wl[2], wl[3]};
-        l_run[K0 + k] = fmaf(l_run[K0 + k], alpha, SPLIT_P ? lx : ls);
-        lx_run[K0 + k] = fmaf(lx_run[K0 + k], alpha, lx);
+        l_run[K0 + k] = fmaf(l_run[K0 + k], alpha, ls);
         if (__any(alpha != 1.f)) {
 #pragma unroll
           for (int db = 0; db < DB; ++db) acc[K0 + k][db] *= alpha;
@@ -602,7 +585,7 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
 #pragma unroll
         for (int k = 0; k < NBK; ++k) {
           acc[K0 + k][db] = mfma16(va, pb[k], acc[K0 + k][db]);
-          if (SPLIT_P) acc[K0 + k][db] = mfma16(va, pl[k], acc[K0 + k][db]);
+          acc[K0 + k][db] = mfma16(va, pl[k], acc[K0 + k][db]);
         }
       }
     };
@@ -663,7 +646,7 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
     }
   }
   if (lse && tid < nrows) {
-    const float l = lx_acc[tid];
+    const float l = l_acc[tid];
     lse[(size_t)(row0 + tid) * H + h] = (l > 0.f) ? (m_acc[tid] + log2f(l)) * kLn2 : -INFINITY;
   }
 }
@@ -916,19 +899,13 @@ hipError_t launch_attention(const skip_problem_t& p, QuerySource q,
       return hipErrorInvalidValue;
     const int4* items = reinterpret_cast<const int4*>(plan);
     const float sl2 = p.sm_scale * kLog2e;
-#define SKIP_ATTN_SPARSE(DD, SP)                                                             \
-  hipLaunchKernelGGL((attn_sparse_kernel<DD, SP>), dim3((unsigned)n_ids), dim3(kSpThreads), \
+#define SKIP_ATTN_SPARSE(DD)                                                                 \
+  hipLaunchKernelGGL((attn_sparse_kernel<DD>), dim3((unsigned)n_ids), dim3(kSpThreads),     \
                      0, s, (const bf16_t*)q.base, q.kept_idx, q.N, qstride, (const bf16_t*)Kh, \
                      (const bf16_t*)Vh, passage_offsets, rowmask, items, p.H, p.total_tokens, \
                      sl2, O, p.o_f32, lse)
-    // float32 output: split softmax weights (bf16 hi + lo) for near-fp32 accuracy
-    if (p.d_h == 64) {
-      if (p.o_f32) SKIP_ATTN_SPARSE(64, true);
-      else SKIP_ATTN_SPARSE(64, false);
-    } else {
-      if (p.o_f32) SKIP_ATTN_SPARSE(128, true);
-      else SKIP_ATTN_SPARSE(128, false);
-    }
+    if (p.d_h == 64) SKIP_ATTN_SPARSE(64);
+    else SKIP_ATTN_SPARSE(128);
 #undef SKIP_ATTN_SPARSE
   } else {
     dim3 grid((p.k_max * p.H + 3) / 4, p.B);

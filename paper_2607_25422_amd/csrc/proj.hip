@@ -13,6 +13,8 @@
 //                      wave's weight fragments come straight from the packed
 //                      copy into registers two steps ahead; 8 waves of 32
 //                      output columns x 96 rows (3 blocks of 32 x 32)
+#include <algorithm>
+
 #include "skip_common.h"
 #include "skip_internal.h"
 
@@ -261,6 +263,28 @@ hipError_t launch_proj_gemm(const skip_problem_t& p, const void* rows, const int
       hipLaunchKernelGGL((proj_gemm_kernel<false, false>), dim3(grid), dim3(kProjThreads), 0, s,
                          R, kept_offsets, kept_idx, p.B, p.N, M, p.d, d_out, Wc, Y, n_items);
   }
+  return hipGetLastError();
+}
+
+// Passage keys as bf16 rows for the projection: k~ = the bf16 rounding
+// (through float, nearest even at both steps) of the pooled double key or of
+// the caller's float key.
+__global__ void __launch_bounds__(256)
+keys_bf16_kernel(const double* __restrict__ kbar, const float* __restrict__ given, size_t n,
+                 bf16_t* __restrict__ out) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const float f = given ? given[i] : (float)kbar[i];
+    out[i] = __builtin_bit_cast(bf16_t, (__bf16)f);
+  }
+}
+
+hipError_t launch_keys_bf16(const double* kbar, const float* given, size_t n, void* out,
+                            hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const size_t blocks = std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(keys_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, kbar, given, n,
+                     static_cast<bf16_t*>(out));
   return hipGetLastError();
 }
 

@@ -382,6 +382,58 @@ skip_status_t skip_gather_project_packed(const skip_problem_t* p, const void* ro
   return SKIP_OK;
 }
 
+// Workspace of skip_project_passage_keys: pooled keys (double), the keys as
+// bf16 rows, W repacked.
+static size_t project_keys_bytes(const skip_problem_t& p, int32_t d_out) {
+  const size_t n = (size_t)p.total_passages * p.d;
+  return align_up(n * sizeof(double)) + align_up(n * sizeof(bf16_t)) +
+         proj_scratch_bytes(p.d, d_out);
+}
+
+skip_status_t skip_workspace_bytes_project_keys(const skip_problem_t* p, int32_t d_out,
+                                                size_t* bytes) {
+  if (!bytes) return SKIP_ERR_INVALID_ARG;
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (d_out <= 0) return SKIP_ERR_INVALID_ARG;
+  if (d_out % 256 != 0 || d_out > 65536) return SKIP_ERR_UNSUPPORTED;
+  *bytes = project_keys_bytes(*p, d_out);
+  return SKIP_OK;
+}
+
+skip_status_t skip_project_passage_keys(const skip_problem_t* p, const void* Kh,
+                                        const int32_t* passage_offsets,
+                                        const float* passage_keys, const void* W,
+                                        int32_t d_out, float* keys_out, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  skip_status_t st = check_common(p);
+  if (st != SKIP_OK) return st;
+  if (!W || d_out <= 0 || !al16(W)) return SKIP_ERR_INVALID_ARG;
+  if (p->dtype != SKIP_BF16 || p->d % 32 != 0 || d_out % 256 != 0 || d_out > 65536)
+    return SKIP_ERR_UNSUPPORTED;
+  if (p->total_passages > 0) {
+    if (!keys_out || !al16(keys_out)) return SKIP_ERR_INVALID_ARG;
+    if (passage_keys ? !al16(passage_keys) : (!Kh || !passage_offsets || !al16(Kh)))
+      return SKIP_ERR_INVALID_ARG;
+  }
+  if (!workspace || !al16(workspace)) return SKIP_ERR_INVALID_ARG;
+  if (workspace_bytes < project_keys_bytes(*p, d_out)) return SKIP_ERR_WORKSPACE;
+  if (p->total_passages == 0) return SKIP_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t n = (size_t)p->total_passages * p->d;
+  char* ws = static_cast<char*>(workspace);
+  double* kbar = reinterpret_cast<double*>(ws);
+  void* kb = ws + align_up(n * sizeof(double));
+  void* packed = static_cast<char*>(kb) + align_up(n * sizeof(bf16_t));
+  if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, kbar, s));
+  SKIP_TRY(launch_keys_bf16(kbar, passage_keys, n, kb, s));
+  // the keys are the rows of a plain (ungathered) projection
+  skip_problem_t q = *p;
+  q.total_kept = p->total_passages;
+  SKIP_TRY(launch_project(q, kb, nullptr, nullptr, W, d_out, keys_out, 1, packed, s));
+  return SKIP_OK;
+}
+
 static_assert(sizeof(skip_skv_gate_t) == 56 && offsetof(skip_skv_gate_t, b2) == 32 &&
                   offsetof(skip_skv_gate_t, rho) == 48,
               "skip_skv_gate_t layout is part of the ABI");

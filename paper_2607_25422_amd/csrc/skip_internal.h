@@ -80,6 +80,8 @@ hipError_t launch_proj_pack(int d, int d_out, const void* W, void* packed, hipSt
 hipError_t launch_proj_gemm(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
                             const int32_t* kept_idx, const void* packed, int d_out, void* Y,
                             int out_f32, hipStream_t s);
+hipError_t launch_keys_bf16(const double* kbar, const float* given, size_t n, void* out,
+                            hipStream_t s);
 hipError_t launch_project(const skip_problem_t& p, const void* rows, const int32_t* kept_offsets,
                           const int32_t* kept_idx, const void* W, int d_out, void* Y,
                           int out_f32, void* scratch, hipStream_t s);

@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol(b):
 
 
 def test_version_and_status_strings(b):
-    assert b.abi_version() == 5
+    assert b.abi_version() == 6
     for s in range(5):
         assert b.status_string(s).startswith("SKIP_")
     assert "UNKNOWN" in b.status_string(99)

@@ -152,3 +152,97 @@ def test_xattn_on_projected_edge_rows(B, seed, rule):
     check_graph(batch, rp, col, adj)
     check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), "bf16",
                     f"proj {rule}")
+
+
+@pytest.mark.parametrize("d_out", [256, 768])
+@pytest.mark.parametrize("seed", wls.SEEDS)
+def test_project_passage_keys_bound(B, seed, d_out):
+    """h_k = W_k k~_j on the device (eq. bsca; Def. B.3): k~ the bf16
+    rounding of the pooled key (mean of the passage's token keys) or of a
+    caller's float key; float output, held to the float32 bound of the row
+    projection."""
+    batch = wls.make_batch("llava_bf16", seed, B=5, N=300, H=4, d_h=64, T=(1, 3),
+                           k=(0, 7, 33, 64), P=(0, 1, 3, 6), L_p=(1, 5, 64, 100))
+    n_p = int(batch.P.sum())
+    say(f"passage-key projection seed={seed} d_out={d_out} passages={n_p}")
+    d = batch.wl.d
+    Wk = wls.make_projection(d_out, d, seed + 2)
+    db = B.to_device(batch)
+    got = B.project_passage_keys(db, Wk.cuda())
+    given = np.random.default_rng(seed).standard_normal((n_p, d)).astype(np.float32)
+    got_given = B.project_passage_keys(db, Wk.cuda(), passage_keys=torch.from_numpy(given).cuda())
+    torch.cuda.synchronize()
+    po = batch.passage_offsets
+    kbar = orc.passage_keys(batch.Kh.double().numpy(),
+                            [(int(po[j]), int(po[j + 1])) for j in range(n_p)])
+    Wn = Wk.double().numpy()
+    check_projection(orc.round_bf16(kbar), Wn, got, False, tag=f"pooled keys d_out={d_out}")
+    check_projection(orc.round_bf16(given.astype(np.float64)), Wn, got_given, False,
+                     tag=f"given keys d_out={d_out}")
+
+
+def test_project_passage_keys_no_passages(B):
+    batch = wls.make_batch("llava_bf16", 42, B=3, N=64, H=4, d_h=64, T=1, k=(0, 5), P=(0,))
+    db = B.to_device(batch)
+    got = B.project_passage_keys(db, wls.make_projection(256, batch.wl.d, 1).cuda())
+    torch.cuda.synchronize()
+    assert got.shape == (0, 256)
+
+
+@pytest.mark.parametrize("rule", ["question", "row"])
+@pytest.mark.parametrize("seed", wls.SEEDS)
+def test_projected_route_chain(B, seed, rule):
+    """The projected route end to end on the device: kept rows from the
+    top-k, edge rows W_v v_i (skip_gather_project), keys h_k = W_k k~_j
+    (skip_project_passage_keys), queries W_Q v_i (skip_gather_project), then
+    the graph on the edge rows and attention on the queries
+    (skip_bipartite_xattn_proj); against the oracle's chain
+    (project_rows, bf16 rounding, bipartite_xattn on edge_rows).
+
+    Inputs on a grid, so that every float32 sum on the device is exact and
+    both sides round the same values to bf16: token values and keys are
+    multiples of 1/8 in [-2, 2], passages hold 1, 4, 16 or 64 tokens (the
+    pooled keys are multiples of 2^-9), weights are multiples of 1/64 in
+    [-1/8, 1/8].  The projected rows and keys then match the oracle bit for
+    bit, the graphs exactly, and attention to the usual bar."""
+    batch = wls.make_batch("llava_bf16", seed, B=5, N=300, H=2, d_h=128, T=(1, 3),
+                           k=(0, 7, 33, 64), P=(0, 1, 3, 6), L_p=(1, 4, 16, 64))
+    rng = np.random.default_rng([seed, 77])
+
+    def grid(shape, lo, hi, den):
+        return torch.from_numpy(rng.integers(lo, hi + 1, size=shape) / den).to(torch.bfloat16)
+
+    batch.V = grid(tuple(batch.V.shape), -16, 16, 8.0)
+    batch.Kh = grid(tuple(batch.Kh.shape), -16, 16, 8.0)
+    d, H, d_h = batch.wl.d, batch.Kh.shape[1], batch.Kh.shape[2]
+    Wv, Wk, Wq = (grid((d, d), -8, 8, 64.0) for _ in range(3))
+    say(f"projected route chain seed={seed} rule={rule} k={batch.k.tolist()} "
+        f"P={batch.P.tolist()}")
+    db = B.to_device(batch, edge_rule=rule)
+    idx, _, _ = B.prune_topk(db, want_scores=False, want_rows=False)
+    E = B.gather_project(db, db.V, Wv.cuda(), kept_idx=idx)
+    Kp = B.project_passage_keys(db, Wk.cuda())
+    Q = B.gather_project(db, db.V, Wq.cuda(), kept_idx=idx).view(-1, H, d_h)
+    O, L, rp, col = B.bipartite_xattn_proj(db, Q, E, Kp if Kp.shape[0] else None)
+    torch.cuda.synchronize()
+
+    kept = kept_oracle(batch)
+    assert idx.cpu().numpy().tolist() == np.concatenate(kept).tolist(), "kept sets"
+    X = kept_rows(batch, kept).double().numpy()
+    E_ref = orc.round_bf16(orc.project_rows(X, Wv.double().numpy()))
+    Q_ref = orc.round_bf16(orc.project_rows(X, Wq.double().numpy()))
+    po = batch.passage_offsets
+    n_p = int(batch.P.sum())
+    kbar = orc.passage_keys(batch.Kh.double().numpy(),
+                            [(int(po[j]), int(po[j + 1])) for j in range(n_p)])
+    K_ref = orc.project_rows(orc.round_bf16(kbar), Wk.double().numpy())
+    np.testing.assert_array_equal(E.cpu().double().numpy(), E_ref)
+    np.testing.assert_array_equal(Q.cpu().double().numpy().reshape(-1, d), Q_ref)
+    np.testing.assert_array_equal(Kp.cpu().double().numpy(), K_ref)
+    _, adj, O_ref, L_ref = orc.bipartite_xattn(
+        Q_ref.reshape(-1, H, d_h), batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, batch.wl.avg_degree, passage_key_table=K_ref,
+        edge_rule=rule, edge_rows=E_ref)
+    check_graph(batch, rp, col, adj)
+    check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), "bf16",
+                    f"projected chain {rule}")

@@ -587,6 +587,44 @@ def _gate_dict(d, h, b2, rng, tau=0.5, rho=1.0):
                 w2=rng.standard_normal(h) / math.sqrt(h), b2=b2, tau=tau, rho=rho)
 
 
+def test_route_mlp_branch_ranks_by_the_scorer():
+    """route(mlp=...) keeps the top-k of the main-text scorer (Sec. 3.3, eq.
+    qvs).  Pinned two ways: a one-unit MLP equivalent to the linear logit on
+    inputs where every bfloat16 rounding is exact (integers, d = 4, so
+    1/sqrt(d) = 1/2) keeps exactly the linear route's sets, ties included;
+    a random MLP keeps the top-k of its own scores, question by question."""
+    rng = np.random.default_rng(7)
+    B, N, d = 4, 24, 4
+    V = rng.integers(-3, 4, size=(B, N, d)).astype(np.float64)
+    Qtok = rng.integers(-3, 4, size=(B, d)).astype(np.float64)     # one token each
+    q_offsets = np.arange(B + 1)
+    k = np.array([5, 0, 24, 9])
+    kept_offsets = np.concatenate([[0], np.cumsum(k)])
+    Kh = np.zeros((0, 1, d))
+    po = np.zeros(1, dtype=np.int64)
+    qp = np.zeros(B + 1, dtype=np.int64)
+    args = (V, Qtok, q_offsets, kept_offsets, Kh, Kh, po, qp, 0.5)
+    lin = orc.route(*args, with_attention=False)
+    # h = (v * q) . 1/2 + C, relu(h) = h, s = h - C = <v, q> / sqrt(d)
+    W1 = np.zeros((1, 3 * d))
+    W1[0, 2 * d:] = 0.5
+    eq = dict(W1=W1, b1=np.array([64.0]), w2=np.array([1.0]), b2=-64.0)
+    got = orc.route(*args, with_attention=False, mlp=eq)
+    for b in range(B):
+        np.testing.assert_array_equal(got.z[b], lin.z[b])
+        assert got.kept_idx[b].tolist() == lin.kept_idx[b].tolist(), f"question {b}"
+    # a random scorer: each question keeps the top-k of its own scores
+    h = 6
+    mlp = dict(W1=rng.standard_normal((h, 3 * d)), b1=rng.standard_normal(h),
+               w2=rng.standard_normal(h), b2=0.25)
+    got = orc.route(*args, with_attention=False, mlp=mlp)
+    for b in range(B):
+        s = orc.qvs_mlp_scores(V[b], Qtok[b], mlp["W1"], mlp["b1"], mlp["w2"], mlp["b2"])
+        np.testing.assert_array_equal(got.scores[b], s)
+        want = sorted(np.argsort(-s, kind="stable")[:k[b]].tolist())
+        assert got.kept_idx[b].tolist() == want, f"question {b}"
+
+
 def test_route_with_gate_limits():
     """A gate that passes everything (large b2, rho = 1) leaves the route as
     it was; one that passes nothing leaves every kept row without neighbours."""
