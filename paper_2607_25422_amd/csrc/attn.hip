@@ -15,8 +15,6 @@
 
 namespace skip {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 template <int N>
 struct IntC {                     // a compile-time count passed to a generic lambda
@@ -33,36 +31,6 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-
-// D (16 x 16, fp32) += A (16 x 32) . B (32 x 16), bf16 operands: lane l holds
-// A[l % 16][8(l / 16) .. +7], B[8(l / 16) .. +7][l % 16] and D[4(l / 16) .. +3][l % 16].
-__device__ __forceinline__ f32x4_t mfma16(const u32x4& a, const u32x4& b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-}
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-
-// Two floats -> packed bf16 pair, round-to-nearest-even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
-  bf16x2_t v = {(__bf16)lo, (__bf16)hi};
-  return __builtin_bit_cast(uint32_t, v);
-}
-
-// Workgroup barrier without a memory fence: the waves that write LDS in the
-// loop wait for their own writes (lgkmcnt) before it.
-__device__ __forceinline__ void barrier_nofence() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// A wave-uniform 64-bit value moved to scalar registers.
-__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
-  return ((uint64_t)hi << 32) | lo;
-}
 
 // Value of lane l ^ 32 (v_permlane32_swap: the two half-waves trade places).
 __device__ __forceinline__ float swap_halves(float x) {
@@ -513,7 +481,7 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
         for (int th = 0; th < 2; ++th) {
           s[k][th] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int kb = 0; kb < KB; ++kb) s[k][th] = mfma16(ka[th][kb], qf[K0 + k][kb], s[k][th]);
+          for (int kb = 0; kb < KB; ++kb) s[k][th] = mfma16_bf16(ka[th][kb], qf[K0 + k][kb], s[k][th]);
         }
       __builtin_amdgcn_sched_barrier(0);
       // V reads (DB feature blocks x two 16-token halves) at constant offsets
@@ -584,8 +552,8 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
         const u32x4 va = __builtin_shufflevector(vr[2 * db], vr[2 * db + 1], 0, 1, 2, 3);
 #pragma unroll
         for (int k = 0; k < NBK; ++k) {
-          acc[K0 + k][db] = mfma16(va, pb[k], acc[K0 + k][db]);
-          acc[K0 + k][db] = mfma16(va, pl[k], acc[K0 + k][db]);
+          acc[K0 + k][db] = mfma16_bf16(va, pb[k], acc[K0 + k][db]);
+          acc[K0 + k][db] = mfma16_bf16(va, pl[k], acc[K0 + k][db]);
         }
       }
     };

@@ -27,26 +27,6 @@ namespace skip {
 
 namespace {
 
-typedef __bf16 gbf16x8_t __attribute__((ext_vector_type(8)));
-typedef float gf32x16_t __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ gf32x16_t gmfma(const u32x4& a, const u32x4& b, gf32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(gbf16x8_t, a),
-                                                 __builtin_bit_cast(gbf16x8_t, b), c, 0, 0, 0);
-}
-
-__device__ __forceinline__ void gunpack8(const u32x4& x, float* out) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    out[2 * w] = __uint_as_float(x[w] << 16);
-    out[2 * w + 1] = __uint_as_float(x[w] & 0xffff0000u);
-  }
-}
-
-__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
-}
-
 // question of global passage index j (query_passages ascending)
 __device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, int j) {
   int lo = 0, hi = B;                      // answer in [0, B)
@@ -121,7 +101,7 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       float f[8];
-      gunpack8(x[u], f);
+      unpack8_bf16(x[u], f);
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
     }
@@ -129,7 +109,7 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
   for (; r < r1; r += kGateMeanWaves) {
     if (r >= base_r + kGateMeanWaves * 64) fetch_idx(r);
     float f[8];
-    gunpack8(load_row(r), f);
+    unpack8_bf16(load_row(r), f);
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
   }
@@ -197,11 +177,11 @@ gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
       const float e1 = bf16_to_f32(f32_to_bf16(e[2 * t + 1]));
       const float q0 = bf16_to_f32(f32_to_bf16(q[2 * t]));
       const float q1 = bf16_to_f32(f32_to_bf16(q[2 * t + 1]));
-      oq[t] = bf16_pair(q0, q1);
-      ov[t] = bf16_pair(v[2 * t], v[2 * t + 1]);
-      oe[t] = bf16_pair(e0, e1);
-      oh[t] = bf16_pair(e0 * q0, e1 * q1);              // exact product, one rounding
-      od[t] = bf16_pair(fabsf(e0 - q0), fabsf(e1 - q1)); // float32 difference, one rounding
+      oq[t] = pack2_bf16(q0, q1);
+      ov[t] = pack2_bf16(v[2 * t], v[2 * t + 1]);
+      oe[t] = pack2_bf16(e0, e1);
+      oh[t] = pack2_bf16(e0 * q0, e1 * q1);              // exact product, one rounding
+      od[t] = pack2_bf16(fabsf(e0 - q0), fabsf(e1 - q1)); // float32 difference, one rounding
     }
     *reinterpret_cast<u32x4*>(xr + c) = oq;
     *reinterpret_cast<u32x4*>(xr + d + c) = ov;
@@ -246,7 +226,7 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, in
   const bf16_t* xa = X + (size_t)prow * K + 32 * hh;
   const bf16_t* wb0 = W + (size_t)(ht * kGateNT + r32) * K + 32 * hh;
   const bf16_t* wb1 = wb0 + (size_t)32 * K;
-  gf32x16_t acc[2];
+  f32x16_t acc[2];
 #pragma unroll
   for (int v = 0; v < 16; ++v) { acc[0][v] = 0.f; acc[1][v] = 0.f; }
   const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -267,8 +247,8 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, in
     load_group(g + 4, a + 4, b0 + 4, b1 + 4);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      acc[0] = gmfma(a[u], b0[u], acc[0]);
-      acc[1] = gmfma(a[u], b1[u], acc[1]);
+      acc[0] = mfma32_bf16(a[u], b0[u], acc[0]);
+      acc[1] = mfma32_bf16(a[u], b1[u], acc[1]);
     }
   }
   if (g < g1) {
@@ -276,8 +256,8 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, in
     load_group(g, a, b0, b1);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      acc[0] = gmfma(a[u], b0[u], acc[0]);
-      acc[1] = gmfma(a[u], b1[u], acc[1]);
+      acc[0] = mfma32_bf16(a[u], b0[u], acc[0]);
+      acc[1] = mfma32_bf16(a[u], b1[u], acc[1]);
     }
   }
   // D layout: element v of block nb is passage 8*(v/4) + 4*hh + v%4, hidden

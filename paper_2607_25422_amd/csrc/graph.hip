@@ -50,20 +50,6 @@ constexpr int kEdKeyStride = kEdCols + 2;  // doubles per key row in LDS (bank s
 
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void ed_dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(g), "s"(lds)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void ed_wait_dma() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
-  asm volatile("" ::: "memory");
-}
-__device__ __forceinline__ uint32_t ed_lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
 struct EdgeDotArgs {
   const int32_t* kept_idx;     // NULL: rows are [total_kept][d]; else V [B][N][d]
   int N;
@@ -96,7 +82,7 @@ edge_dot_kernel(const T* __restrict__ rows, EdgeDotArgs a) {
   if (k <= 0 || P <= 0) return;                  // nothing of this question is read
   const int c0 = s * kEdCols, ncol = min(kEdCols, a.d - c0);
   const int w = tid >> 6, lane = tid & 63, l16 = lane & 15, kk = lane >> 4;
-  const uint32_t rlds = __builtin_amdgcn_readfirstlane(ed_lds_addr(rbuf));
+  const uint32_t rlds = lds_addr(rbuf);
   const size_t zs = (size_t)b * a.S + s;
 
   // Copy rows blk0 .. blk0 + 191, columns [pass·CPP, pass·CPP + CPP) of the
@@ -122,14 +108,14 @@ edge_dot_kernel(const T* __restrict__ rows, EdgeDotArgs a) {
       const int colc = col < ncol ? col : 0;
       const size_t row = a.kept_idx ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1)
                                     : (size_t)rid[j];
-      ed_dma16(rows + row * a.d + c0 + colc,
+      lds_dma16(rows + row * a.d + c0 + colc,
                __builtin_amdgcn_readfirstlane(rlds + (uint32_t)(48 * w + 2 * j) * 512u));
     }
   };
   // after the copies of a pass have landed: clear the chunks past the slice
   // (each wave its own rows; every wave waits for its copies first)
   auto finish_rows = [&](int pass) {
-    ed_wait_dma();
+    wait_vmcnt<0>();
     if (pass * CPP + CPP > ncol) {
       for (int t = lane; t < 48 * 32; t += 64) {
         const int r = 48 * w + (t >> 5), sl = t & 31;
@@ -212,7 +198,7 @@ edge_dot_kernel(const T* __restrict__ rows, EdgeDotArgs a) {
             const int r = 16 * (w + 4 * t) + l16;          // row within the block
             const u32x4 x = *reinterpret_cast<const u32x4*>(
                 rbuf + r * 512 + (((4 * g + kk) ^ (r & 7)) * 16));
-            unpack_f64<T>(x, qa[t]);
+            unpack16_f64<T>(x, qa[t]);
           }
 #pragma unroll
           for (int m = 0; m < E; ++m)

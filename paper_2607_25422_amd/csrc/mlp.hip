@@ -23,41 +23,6 @@ namespace skip {
 
 namespace {
 
-typedef __bf16 mbf16x8_t __attribute__((ext_vector_type(8)));
-typedef float mf32x16_t __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ mf32x16_t mfma_bf16(const u32x4& a, const u32x4& b, mf32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(mbf16x8_t, a),
-                                                 __builtin_bit_cast(mbf16x8_t, b), c, 0, 0, 0);
-}
-
-// Direct global->LDS load of 16 bytes per lane (lane l's bytes land at
-// lds + 16 * l); completion is awaited with an explicit vmcnt wait.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(g), "s"(lds)
-               : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_u32(const void* p) {
-  return __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-__device__ __forceinline__ void barrier_nf() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-typedef __bf16 mbf16x2_t __attribute__((ext_vector_type(2)));
-
 // bf16(a * q) for the 8 bf16 values of a (q: 8 floats); a product of two
 // bf16 values is exact in float32, so the pair conversion (round to nearest
 // even, v_cvt_pk_bf16_f32) is the one rounding of the model.
@@ -66,20 +31,13 @@ __device__ __forceinline__ u32x4 hadamard8(const u32x4& a, const float* q) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     const uint32_t x = a[w];
-    const mbf16x2_t p = {(__bf16)(__uint_as_float(x << 16) * q[2 * w]),
+    const bf16x2_t p = {(__bf16)(__uint_as_float(x << 16) * q[2 * w]),
                          (__bf16)(__uint_as_float(x & 0xffff0000u) * q[2 * w + 1])};
     r[w] = __builtin_bit_cast(uint32_t, p);
   }
   return r;
 }
 
-__device__ __forceinline__ void unpack8(const u32x4& x, float* out) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    out[2 * w] = __uint_as_float(x[w] << 16);
-    out[2 * w + 1] = __uint_as_float(x[w] & 0xffff0000u);
-  }
-}
 
 }  // namespace
 
@@ -135,13 +93,13 @@ mlp_prep_kernel(const bf16_t* __restrict__ qbf, const bf16_t* __restrict__ W1,
       const int c = g + (t * 64 + lane) * 8;
       if (c >= d) continue;
       float w0[8], w1[8];
-      unpack8(w[0][t], w0);
-      unpack8(w[1][t], w1);
+      unpack8_bf16(w[0][t], w0);
+      unpack8_bf16(w[1][t], w1);
 #pragma unroll
       for (int qq = 0; qq < kMlpPrepQ; ++qq) {
         if (qq >= nq) continue;
         float qv[8];
-        unpack8(*reinterpret_cast<const u32x4*>(&qs[qq][c]), qv);
+        unpack8_bf16(*reinterpret_cast<const u32x4*>(&qs[qq][c]), qv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           acc[0][qq] = fmaf(w0[e], qv[e], acc[0][qq]);
@@ -244,12 +202,12 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
   const int lc_t = (tid & 3) ^ ((trow >> 1) & 3);
   const bf16_t* vsrc = V + ((size_t)b * N + min(i0 + trow, N - 1)) * d + lc_t * 8;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t ar_lds = lds_u32(Ar) + (uint32_t)(wave_s * 1024);
+  const uint32_t ar_lds = lds_addr(Ar) + (uint32_t)(wave_s * 1024);
   // (waves past the tile's rows, 4 * kMlpMT threads and up, copy nothing)
   const bool v_loader = tid < 4 * kMlpMT;
   auto issue_v = [&](int s) {
     if (v_loader)
-      dma16(vsrc + s * kMlpKS, __builtin_amdgcn_readfirstlane(
+      lds_dma16(vsrc + s * kMlpKS, __builtin_amdgcn_readfirstlane(
                                    ar_lds + (uint32_t)((s % kMlpRing) * A_ELEMS * 2)));
   };
   // Hadamard tile of step s (this thread's 8 values, same swizzled position;
@@ -259,7 +217,7 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
     if (!v_loader) return;
     const u32x4 a = *reinterpret_cast<const u32x4*>(Ar + (s % kMlpRing) * A_ELEMS + tid * 8);
     float q[8];
-    unpack8(*reinterpret_cast<const u32x4*>(Qs + s * kMlpKS + lc_t * 8), q);
+    unpack8_bf16(*reinterpret_cast<const u32x4*>(Qs + s * kMlpKS + lc_t * 8), q);
     *reinterpret_cast<u32x4*>(Hd + (s & 1) * A_ELEMS + tid * 8) = hadamard8(a, q);
   };
   // W1 fragments of step s: [x][kk], x = 0 the v block, 1 the Hadamard block
@@ -271,7 +229,7 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
       for (int kk = 0; kk < 2; ++kk) w[x][kk] = wsrc[(size_t)s * 256 + (x * 2 + kk) * 64];
   };
 
-  mf32x16_t acc[kMlpMB];
+  f32x16_t acc[kMlpMB];
 #pragma unroll
   for (int mb = 0; mb < kMlpMB; ++mb)
 #pragma unroll
@@ -303,8 +261,8 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int mb = 0; mb < kMlpMB; ++mb) {
-        acc[mb] = mfma_bf16(a1[kk][mb], w[0][kk], acc[mb]);
-        acc[mb] = mfma_bf16(a3[kk][mb], w[1][kk], acc[mb]);
+        acc[mb] = mfma32_bf16(a1[kk][mb], w[0][kk], acc[mb]);
+        acc[mb] = mfma32_bf16(a3[kk][mb], w[1][kk], acc[mb]);
       }
     // Schedule: half the operand reads ahead, then one MFMA per read, so the
     // read latency hides behind the matrix pipe.
@@ -330,8 +288,8 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
   u32x4 wA[2][2], wB[2][2];
   load_w(0, wA);
   load_w(min(1, ksteps - 1), wB);
-  wait_vm<0>();
-  barrier_nf();
+  wait_vmcnt<0>();
+  barrier_nofence();
   hadamard_tile(0);
 
   // Step s: wait for the v tile of step s+1 (the Hadamard pass reads it),
@@ -341,9 +299,9 @@ mlp_score_kernel(const bf16_t* __restrict__ V, int N, int d, int B,
   auto step = [&](int s, u32x4 (&w)[2][2]) {
     // outstanding per wave after this wait: the v tile of step s+2 (one
     // load, while there is one) and the W1 fragments of step s+1 (four loads)
-    if (s + 2 < ksteps) wait_vm<5>();
-    else wait_vm<4>();
-    barrier_nf();
+    if (s + 2 < ksteps) wait_vmcnt<5>();
+    else wait_vmcnt<4>();
+    barrier_nofence();
     if (s + kMlpAhead < ksteps) issue_v(s + kMlpAhead);
     mma_step(s, w);
     if (s + 1 < ksteps) hadamard_tile(s + 1);

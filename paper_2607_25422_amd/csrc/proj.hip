@@ -20,43 +20,6 @@
 
 namespace skip {
 
-namespace {
-
-typedef __bf16 pbf16x8_t __attribute__((ext_vector_type(8)));
-typedef float pf32x16_t __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ pf32x16_t pmfma(const u32x4& a, const u32x4& b, pf32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(pbf16x8_t, a),
-                                                 __builtin_bit_cast(pbf16x8_t, b), c, 0, 0, 0);
-}
-
-// Direct global->LDS load of 16 bytes per lane (lane l's bytes land at
-// lds + 16 * l); completion is awaited with an explicit vmcnt wait.
-__device__ __forceinline__ void pdma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(g), "s"(lds)
-               : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t plds_u32(const void* p) {
-  return __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
-}
-
-template <int N>
-__device__ __forceinline__ void pwait_vm() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-__device__ __forceinline__ void pbarrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-}  // namespace
-
 // rows per tile: 3 blocks of 32 (3072 kept rows make 32 tiles, so with 16
 // column tiles 512 items fill 256 CUs twice over)
 constexpr int kProjMT = 96;
@@ -129,12 +92,12 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
   }
   const bf16_t* asrc = rows + rid * d + lc * 8;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t ar_lds = plds_u32(Ar) + (uint32_t)(wave_s * 1024);
+  const uint32_t ar_lds = lds_addr(Ar) + (uint32_t)(wave_s * 1024);
   // (waves past the tile's rows, 4 * kProjMT threads and up, copy nothing)
   const bool a_loader = tid < 4 * kProjMT;
   auto issue_a = [&](int s) {
     if (a_loader)
-      pdma16(asrc + s * kProjKS, __builtin_amdgcn_readfirstlane(
+      lds_dma16(asrc + s * kProjKS, __builtin_amdgcn_readfirstlane(
                                      ar_lds + (uint32_t)((s % kProjRing) * A_ELEMS * 2)));
   };
   const u32x4* wsrc = Wp + ((size_t)(nt * 8 + wave) * ksteps) * 128 + lane;
@@ -143,7 +106,7 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
     for (int kk = 0; kk < 2; ++kk) w[kk] = wsrc[(size_t)s * 128 + kk * 64];
   };
 
-  pf32x16_t acc[kProjMB];
+  f32x16_t acc[kProjMB];
 #pragma unroll
   for (int mb = 0; mb < kProjMB; ++mb)
 #pragma unroll
@@ -169,7 +132,7 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int mb = 0; mb < kProjMB; ++mb) acc[mb] = pmfma(a[kk][mb], w[kk], acc[mb]);
+      for (int mb = 0; mb < kProjMB; ++mb) acc[mb] = mfma32_bf16(a[kk][mb], w[kk], acc[mb]);
     // half the operand reads ahead, then one MFMA per read
     constexpr int NR = 2 * kProjMB;          // operand reads (= MFMAs)
     __builtin_amdgcn_sched_group_barrier(0x100, NR / 2, 0);
@@ -194,10 +157,10 @@ proj_gemm_kernel(const bf16_t* __restrict__ rows, const int32_t* __restrict__ ke
   // barrier (publishes it; the slot of step s-1 is free), load the tile of
   // step s+3, multiply step s, load the fragments of step s+2.
   auto step = [&](int s, u32x4 (&w)[2]) {
-    if (s + 2 < ksteps) pwait_vm<4>();
-    else if (s + 1 < ksteps) pwait_vm<3>();
-    else pwait_vm<2>();
-    pbarrier();
+    if (s + 2 < ksteps) wait_vmcnt<4>();
+    else if (s + 1 < ksteps) wait_vmcnt<3>();
+    else wait_vmcnt<2>();
+    barrier_nofence();
     if (s + kProjAhead < ksteps) issue_a(s + kProjAhead);
     mma_step(s, w);
     // unconditional (the last steps reload the final fragments): a

@@ -18,31 +18,6 @@
 
 namespace skip {
 
-template <typename T> struct Vec16;   // 16 bytes of T
-template <> struct Vec16<float> { static constexpr int n = 4; };
-template <> struct Vec16<bf16_t> { static constexpr int n = 8; };
-
-template <typename T>
-__device__ __forceinline__ void unpack16(const u32x4& x, double* out);
-template <>
-__device__ __forceinline__ void unpack16<float>(const u32x4& x, double* out) {
-  out[0] = (double)__uint_as_float(x.x);
-  out[1] = (double)__uint_as_float(x.y);
-  out[2] = (double)__uint_as_float(x.z);
-  out[3] = (double)__uint_as_float(x.w);
-}
-template <>
-__device__ __forceinline__ void unpack16<bf16_t>(const u32x4& x, double* out) {
-  out[0] = (double)bf16_to_f32(x.x & 0xffffu);
-  out[1] = (double)bf16_to_f32(x.x >> 16);
-  out[2] = (double)bf16_to_f32(x.y & 0xffffu);
-  out[3] = (double)bf16_to_f32(x.y >> 16);
-  out[4] = (double)bf16_to_f32(x.z & 0xffffu);
-  out[5] = (double)bf16_to_f32(x.z >> 16);
-  out[6] = (double)bf16_to_f32(x.w & 0xffffu);
-  out[7] = (double)bf16_to_f32(x.w >> 16);
-}
-
 // ---------------------------------------------------------------------------
 // Streaming GEMV in float64.  Workgroup = 4 waves = kScoreRows rows of one
 // question; each wave handles kRowsPerWave rows, R at a time, U column chunks
@@ -97,7 +72,7 @@ score_kernel(const T* __restrict__ V, const double* __restrict__ u, int N, int d
 #pragma unroll
           for (int rr = 0; rr < kScoreR; ++rr) {
             double v[VEC];
-            unpack16<T>(x[rr][uu], v);
+            unpack16_f64<T>(x[rr][uu], v);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[rr] = fma(v[e], w[e], acc[rr]);
           }

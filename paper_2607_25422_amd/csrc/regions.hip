@@ -35,23 +35,6 @@ template <> __device__ __forceinline__ double reg_load1<bf16_t>(const bf16_t* p)
   return (double)bf16_to_f32(*p);
 }
 
-// Direct global->LDS load of 16 bytes per lane (lane l's bytes land at
-// lds + 16 * l); completion is awaited with an explicit vmcnt wait, since the
-// compiler does not count these loads.
-__device__ __forceinline__ void reg_dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(g), "s"(lds)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void reg_wait_dma() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
-  asm volatile("" ::: "memory");
-}
-__device__ __forceinline__ uint32_t reg_lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
 // 16 bytes of a row held in LDS: 8 bf16 or 4 f32 elements, as doubles
 template <typename T> struct RegLds;
 template <> struct RegLds<bf16_t> {
@@ -182,7 +165,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
   static_assert(64 * RPL <= kRegResidentRows, "resident positions fit");
   const int w = tid >> 6, lane = tid & 63;
   uint8_t* wrows = pool + w * (WROWS * 128);        // this wave's rows
-  const uint32_t wlds = __builtin_amdgcn_readfirstlane(reg_lds_addr(wrows));
+  const uint32_t wlds = lds_addr(wrows);
   const bool resident = NP == 1 && k <= 64 * RPL;
   auto stage_rows = [&](int blk0, int pass) {
     // lane l fetches chunk (l & 7) ^ (l >> 3) of local row 8j + (l >> 3);
@@ -203,7 +186,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 #pragma unroll
     for (int j = 0; j < 8 * RPL; ++j) {
       const size_t row = IDX ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1) : (size_t)rid[j];
-      reg_dma16(rows + row * a.d + c0 + colc, wlds + j * 1024);
+      lds_dma16(rows + row * a.d + c0 + colc, wlds + j * 1024);
     }
   };
   // element (local row lr, slice column tid) of a resident block
@@ -215,7 +198,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
 
   // ---- centroids of this step, this slice's columns (thread = column)
   if (a.t == 0) {
-    if (resident) reg_wait_dma();                  // a wave reads only rows it copied
+    if (resident) wait_vmcnt<0>();                  // a wave reads only rows it copied
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
       if (r < R) {
@@ -287,7 +270,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
         }
         spos[p] = word;
       }
-      reg_wait_dma();
+      wait_vmcnt<0>();
       __syncthreads();
       const uint32_t lsw = (uint32_t)((lane >> 3) << 4);
       const uint8_t* wl = wrows + (lane & 7) * sizeof(T);
@@ -401,7 +384,7 @@ region_step_kernel(const T* __restrict__ rows, RegionArgs a) {
     for (int pass = 0; pass < NP; ++pass) {
       if (!resident) {
         stage_rows(blk0, pass);
-        reg_wait_dma();
+        wait_vmcnt<0>();
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {

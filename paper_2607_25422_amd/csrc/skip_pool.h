@@ -7,31 +7,6 @@
 
 namespace skip {
 
-template <typename T> struct GVec;
-template <> struct GVec<float> { static constexpr int n = 4; };
-template <> struct GVec<bf16_t> { static constexpr int n = 8; };
-
-template <typename T>
-__device__ __forceinline__ void unpack_f64(const u32x4& x, double* out);
-template <>
-__device__ __forceinline__ void unpack_f64<float>(const u32x4& x, double* out) {
-  out[0] = (double)__uint_as_float(x.x);
-  out[1] = (double)__uint_as_float(x.y);
-  out[2] = (double)__uint_as_float(x.z);
-  out[3] = (double)__uint_as_float(x.w);
-}
-template <>
-__device__ __forceinline__ void unpack_f64<bf16_t>(const u32x4& x, double* out) {
-  out[0] = (double)bf16_to_f32(x.x & 0xffffu);
-  out[1] = (double)bf16_to_f32(x.x >> 16);
-  out[2] = (double)bf16_to_f32(x.y & 0xffffu);
-  out[3] = (double)bf16_to_f32(x.y >> 16);
-  out[4] = (double)bf16_to_f32(x.z & 0xffffu);
-  out[5] = (double)bf16_to_f32(x.z >> 16);
-  out[6] = (double)bf16_to_f32(x.w & 0xffffu);
-  out[7] = (double)bf16_to_f32(x.w >> 16);
-}
-
 // Workgroup = (column slice of 64 lanes x kPoolChunks x 16 bytes, range);
 // wave w sums rows w, w+4, ... (four rows, two 16-byte chunks each, in flight
 // per lane); the four partial sums are combined in wave order through LDS.
@@ -53,7 +28,7 @@ struct PoolRanges {
 template <typename T>
 __global__ void __launch_bounds__(256)
 pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) {
-  constexpr int VEC = GVec<T>::n;
+  constexpr int VEC = Vec16<T>::n;
   constexpr int CH = kPoolChunks;
   __shared__ double part[4][64][CH * VEC];
   const bool question = (int)blockIdx.y < qr.n;
@@ -91,7 +66,7 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
 #pragma unroll
       for (int h = 0; h < CH; ++h) {
         double v[VEC];
-        unpack_f64<T>(x[q][h], v);
+        unpack16_f64<T>(x[q][h], v);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[h][e] += v[e];
       }
@@ -102,7 +77,7 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
       if (!ok[h]) continue;
       u32x4 x = *reinterpret_cast<const u32x4*>(src + (size_t)t * d + cc[h]);
       double v[VEC];
-      unpack_f64<T>(x, v);
+      unpack16_f64<T>(x, v);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) acc[h][e] += v[e];
     }
@@ -120,7 +95,7 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
     if (!ok[h]) continue;
     double wv[VEC];
     if (question && w) {
-      unpack_f64<T>(*reinterpret_cast<const u32x4*>(w + cc[h]), wv);
+      unpack16_f64<T>(*reinterpret_cast<const u32x4*>(w + cc[h]), wv);
     } else {
 #pragma unroll
       for (int e = 0; e < VEC; ++e) wv[e] = 0.0;
