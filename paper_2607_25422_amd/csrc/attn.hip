@@ -509,19 +509,30 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
             for (int j = 0; j < 4; ++j)
               if (16 * th + j >= rem) s[k][th][j] = -INFINITY;
         }
-        float sm = fmaxf(fmaxf(fmaxf(s[k][0][0], s[k][0][1]), fmaxf(s[k][0][2], s[k][0][3])),
-                         fmaxf(fmaxf(s[k][1][0], s[k][1][1]), fmaxf(s[k][1][2], s[k][1][3])));
-        sm = fmaxf(sm, swap16(sm));
-        sm = fmaxf(sm, swap_halves(sm));
-        const float tmax = sm * sc;                         // the tile has a valid token
-        const bool moved = tmax > m_run[K0 + k] + kLazy;         // always on a block's first tile
-        const float m_new = moved ? tmax : m_run[K0 + k];
-        // acc and the sums are 0 before a block's first tile: nothing to rescale
-        const float alpha =
-            (moved && m_run[K0 + k] != -INFINITY) ? __builtin_amdgcn_exp2f(m_run[K0 + k] - m_new) : 1.f;
-        m_run[K0 + k] = m_new;
-        // each weight as a bf16 pair hi + lo (hi its rounding, lo the
-        // rounding of the rest), both fed to the PV product
+        // this lane's 8 logits; the row maximum (over the four lanes of the
+        // row) is needed only when some row's reference has to move, which
+        // a lane can tell from its own logits
+        const float lm = fmaxf(fmaxf(fmaxf(s[k][0][0], s[k][0][1]), fmaxf(s[k][0][2], s[k][0][3])),
+                               fmaxf(fmaxf(s[k][1][0], s[k][1][1]), fmaxf(s[k][1][2], s[k][1][3])));
+        float m_new = m_run[K0 + k];                        // -inf on a block's first tile
+        if (__any(lm * sc > m_new + kLazy)) {
+          float sm = fmaxf(lm, swap16(lm));
+          sm = fmaxf(sm, swap_halves(sm));
+          const float tmax = sm * sc;                       // the tile has a valid token
+          if (tmax > m_new + kLazy) {
+            // acc and the sum are 0 before a block's first tile: nothing to
+            // rescale then
+            const float alpha = m_new != -INFINITY ? __builtin_amdgcn_exp2f(m_new - tmax) : 1.f;
+            m_new = tmax;
+            l_run[K0 + k] *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) acc[K0 + k][db] *= alpha;
+          }
+          m_run[K0 + k] = m_new;
+        }
+        // each weight p as a bf16 pair hi + lo: hi = p truncated to bf16 (its
+        // top 16 bits, v_perm_b32 packs two), lo = the rest p - hi (exact)
+        // rounded to bf16, so hi + lo is p to about 2^-16 relative
         uint32_t w[4], wl[4];
         float ls = 0.f;
 #pragma unroll
@@ -531,18 +542,14 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
             const float p0 = __builtin_amdgcn_exp2f(fmaf(s[k][th][2 * q], sc, -m_new));
             const float p1 = __builtin_amdgcn_exp2f(fmaf(s[k][th][2 * q + 1], sc, -m_new));
             ls += p0 + p1;
-            const uint32_t pw = pack2_bf16(p0, p1);
-            w[2 * th + q] = pw;
-            wl[2 * th + q] = pack2_bf16(p0 - __uint_as_float(pw << 16),
-                                        p1 - __uint_as_float(pw & 0xffff0000u));
+            const uint32_t b0 = __float_as_uint(p0), b1 = __float_as_uint(p1);
+            w[2 * th + q] = __builtin_amdgcn_perm(b1, b0, 0x07060302u);
+            wl[2 * th + q] = pack2_bf16(p0 - __uint_as_float(b0 & 0xffff0000u),
+                                        p1 - __uint_as_float(b1 & 0xffff0000u));
           }
         pb[k] = u32x4{w[0], w[1], w[2], w[3]};
         pl[k] = u32x4{wl[0], wl[1], wl[2], wl[3]};
-        l_run[K0 + k] = fmaf(l_run[K0 + k], alpha, ls);
-        if (__any(alpha != 1.f)) {
-#pragma unroll
-          for (int db = 0; db < DB; ++db) acc[K0 + k][db] *= alpha;
-        }
+        l_run[K0 + k] += ls;
       }
       __builtin_amdgcn_sched_barrier(0);
       // O^T += V^T . P^T
