@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define SKIP_ABI_VERSION 6
+#define SKIP_ABI_VERSION 7
 
 typedef enum skip_status {
   SKIP_OK = 0,
@@ -505,10 +505,11 @@ skip_status_t skip_route_fused_noalloc(const skip_problem_t* p, const void* V,
                                        const float* passage_keys, int32_t* kept_idx,
                                        void* O, float* lse, void* stream);
 
-/* Kernel stages of skip_route_fused, in launch order: pooling (questions
- * and passage keys), salience scoring, top-k, edge compatibilities, edge
- * selection, the attention work list (bf16; empty for float32), attention. */
-#define SKIP_FUSED_STAGES 7
+/* Kernel stages of skip_route_fused, in launch order: question pooling;
+ * salience scoring with the top-k (and the passage-key pooling unless the
+ * keys are given) in one launch; edge compatibilities; edge selection (with
+ * the attention's work list built beside it); attention. */
+#define SKIP_FUSED_STAGES 5
 
 /*
  * skip_route_fused with per-stage timing, for profiling harnesses.

@@ -36,8 +36,7 @@ ENTRY_POINTS = ("skip_abi_version", "skip_status_string", "skip_workspace_bytes"
                 "skip_bipartite_xattn_proj", "skip_pack_projection",
                 "skip_gather_project_packed", "skip_route_fused_noalloc",
                 "skip_workspace_bytes_project_keys", "skip_project_passage_keys")
-FUSED_STAGES = ("pool", "score", "topk", "edge_cos", "edge_select", "attn_plan",
-                "attention")
+FUSED_STAGES = ("pool", "score", "edge_cos", "edge_select", "attention")
 
 
 class SkipError(RuntimeError):

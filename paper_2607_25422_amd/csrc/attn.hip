@@ -12,6 +12,7 @@
 // for the logits, lane = feature for the PV product.
 #include "skip_common.h"
 #include "skip_internal.h"
+#include "skip_plan.h"
 
 namespace skip {
 
@@ -114,14 +115,12 @@ __device__ __forceinline__ void lds_wait_all(u32x2 (&v)[N]) {
 // passages merge in ascending order (a barrier at least between two), so the
 // result is deterministic.  The item ends by writing O = acc / sum and LSE
 // for every row of the chunk (0 and -inf for a row without neighbours).
-constexpr int kSpRows = 192;              // kept rows per work item
 constexpr int kSpTile = 32;               // tokens per K/V tile
 constexpr int kSpStages = 3;              // K (and V) tiles resident in LDS
 constexpr int kSpRegTiles = 4;            // K (and V) tiles in flight in loader registers
 constexpr int kSpCompute = kSpRows / 32;  // compute waves (two 16-row blocks each)
 constexpr int kSpWaves = kSpCompute + 2;  // + a K loader and a V loader
 constexpr int kSpThreads = 64 * kSpWaves;
-constexpr int kSpMaxP = 64;
 constexpr float kLazy = 8.f;              // log2 slack of the softmax reference maximum
 static_assert(kSpRows <= 3 * 64, "row masks have three 64-bit words");
 
@@ -626,16 +625,8 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
   }
 }
 
-// Work list of the passage-major attention, built on the device from the
-// offsets (one workgroup).  Questions are ordered by decreasing cost (chunks x
-// passage tokens, ties to the lower index; natural order above kPlanMaxB
-// questions), so that the longest items start first.  The (question, head)
-// groups of that order are dealt in runs of eight; a run whose groups have at
-// most n chunks takes 8n consecutive workgroup ids, chunk c of the run's group
-// i at id base + 8c + i.  Workgroups are dealt round-robin over the 8 XCDs,
-// so the chunks of one (question, head), which read the same K/V tiles, run
-// side by side on one XCD and share its L2.  Unused ids get no item.
-constexpr int kPlanMaxB = 4096;
+// Standalone work-list launch (calls whose graph is given; the fused route
+// builds the list in the edge-selection launch).
 constexpr int kPlanThreads = 1024;
 
 __global__ void __launch_bounds__(kPlanThreads)
@@ -644,115 +635,10 @@ attn_plan_kernel(const int32_t* __restrict__ kept_offsets,
                  const int32_t* __restrict__ passage_offsets, int B, int H, int total_kept,
                  int total_passages, int total_tokens, int k_max, int P_max, int n_ids,
                  int4* __restrict__ items) {
-  // per question (when B <= kPlanMaxB): sort key, first kept row, rows,
-  // first passage, passages (<= 64), chunks
-  __shared__ uint64_t key[kPlanMaxB];
-  __shared__ int32_t q_k0[kPlanMaxB], q_p0[kPlanMaxB];
-  __shared__ int16_t q_kq[kPlanMaxB];
-  __shared__ uint8_t q_P[kPlanMaxB], q_nch[kPlanMaxB];
+  __shared__ PlanLds L;
   __shared__ uint32_t scan_sh[kPlanThreads / 64 + 1];
-  const int tid = threadIdx.x;
-  struct Q {
-    int k0, kq, p0, P, nch;
-  };
-  auto question = [&](int b) {
-    Q q;
-    int k1, p1;
-    range_of(kept_offsets, b, total_kept, q.k0, k1);
-    range_of(query_passages, b, total_passages, q.p0, p1);
-    q.kq = min(k1 - q.k0, k_max);
-    q.P = min(min(p1 - q.p0, P_max), kSpMaxP);
-    q.nch = (q.kq + kSpRows - 1) / kSpRows;
-    return q;
-  };
-  const bool cached = B <= kPlanMaxB;   // question data and the cost order in LDS
-  if (cached) {
-    int n = 1;
-    while (n < B) n <<= 1;
-    for (int b = tid; b < n; b += kPlanThreads) {
-      uint64_t kk = 0ull;
-      if (b < B) {
-        const Q q = question(b);
-        const int t0 = q.P > 0 ? clampi(passage_offsets[q.p0], 0, total_tokens) : 0;
-        const int t1 = q.P > 0 ? clampi(passage_offsets[q.p0 + q.P], t0, total_tokens) : 0;
-        const uint64_t cost = (uint64_t)q.nch * (uint64_t)(t1 - t0 + 1);
-        kk = (cost << 12) | (uint64_t)(kPlanMaxB - 1 - b);
-        q_k0[b] = q.k0;
-        q_p0[b] = q.p0;
-        q_kq[b] = (int16_t)q.kq;
-        q_P[b] = (uint8_t)q.P;
-        q_nch[b] = (uint8_t)q.nch;
-      }
-      key[b] = kk;
-    }
-    __syncthreads();
-    // bitonic sort, descending
-    for (int size = 2; size <= n; size <<= 1)
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int i = tid; i < n; i += kPlanThreads) {
-          const int jx = i ^ stride;
-          if (jx > i) {
-            const bool desc = (i & size) == 0;
-            const uint64_t x = key[i], y = key[jx];
-            if (desc ? (x < y) : (x > y)) {
-              key[i] = y;
-              key[jx] = x;
-            }
-          }
-        }
-        __syncthreads();
-      }
-  }
-  // question of rank r, and its data
-  auto at = [&](int r, int& b) -> Q {
-    if (!cached) {
-      b = r;
-      return question(r);
-    }
-    b = kPlanMaxB - 1 - (int)(key[r] & (kPlanMaxB - 1));
-    return Q{q_k0[b], (int)q_kq[b], q_p0[b], (int)q_P[b], (int)q_nch[b]};
-  };
-  const int groups = B * H;   // B * H * k rows fit in int32 (k_max * P_max bounded)
-  const int runs = (groups + 7) / 8;
-  int carry = 0;
-  for (int m0 = 0; m0 < runs; m0 += kPlanThreads) {
-    const int m = m0 + tid;
-    int ncr = 0;
-    int qb[8];
-    Q qq[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int g = m * 8 + i;
-      qb[i] = -1;
-      qq[i] = Q{0, 0, 0, 0, 0};
-      if (m < runs && g < groups) {
-        qq[i] = at(g / H, qb[i]);
-        ncr = max(ncr, qq[i].nch);
-      }
-    }
-    uint32_t total;
-    const uint32_t pre = block_exclusive_scan((uint32_t)ncr, scan_sh, &total);
-    const int base = 8 * (carry + (int)pre);
-    if (m < runs)
-      for (int c = 0; c < ncr; ++c)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int id = base + 8 * c + i;
-          if (id >= n_ids) continue;
-          int4 it = make_int4(-1, 0, 0, 0);
-          if (qb[i] >= 0 && c < qq[i].nch) {
-            const Q& q = qq[i];
-            const int rpc = (q.kq + q.nch - 1) / q.nch;
-            const int r0 = c * rpc;
-            const int nrows = min(q.kq, r0 + rpc) - r0;
-            const int h = (m * 8 + i) % H;
-            it = make_int4(qb[i], q.k0 + r0, q.p0, h | (nrows << 8) | (q.P << 16));
-          }
-          items[id] = it;
-        }
-    carry += (int)total;
-  }
-  for (int id = 8 * carry + tid; id < n_ids; id += kPlanThreads) items[id] = make_int4(-1, 0, 0, 0);
+  build_attention_plan(L, scan_sh, kept_offsets, query_passages, passage_offsets, B, H,
+                       total_kept, total_passages, total_tokens, k_max, P_max, n_ids, items);
 }
 
 // ---------------------------------------------------------------------------

@@ -17,6 +17,7 @@
 //   csr_to_mask  : neighbour masks from a caller-given CSR graph
 #include "skip_common.h"
 #include "skip_internal.h"
+#include "skip_plan.h"
 #include "skip_pool.h"
 #include "skip_select.h"
 
@@ -238,6 +239,14 @@ edge_dot_kernel(const T* __restrict__ rows, EdgeDotArgs a) {
 // ---------------------------------------------------------------------------
 // Edge selection, one workgroup per question.
 constexpr int kGSelThreads = 1024;
+
+// The attention's work list, built by one extra workgroup of the selection
+// launch (items NULL: none).
+struct PlanArgs {
+  int4* items;
+  const int32_t* passage_offsets;
+  int H, total_tokens, n_ids;
+};
 constexpr int kGSelMaxPT = 16;     // k_b * P_b <= 16384
 
 // Edges a question keeps under each cut (the same arithmetic on every side).
@@ -259,13 +268,23 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
                    int total_passages, int k_max, int P_max, int d, double avg_degree,
                    int rule, int metric, double beta, const uint8_t* __restrict__ keep,
                    uint64_t* __restrict__ rowmask, int32_t* __restrict__ rowptr_out,
-                   int32_t* __restrict__ col_out) {
+                   int32_t* __restrict__ col_out, PlanArgs plan) {
   __shared__ SelectShared sh;
   __shared__ uint32_t scan_sh[20];
   __shared__ uint8_t flag[kGSelThreads * kGSelMaxPT];
   // row norms while the keys are formed, then the keys of the per-row cut
   __shared__ __align__(16) uint64_t rkeys[kGSelThreads * kGSelMaxPT];
   __shared__ double knorm[64];
+  static_assert(sizeof(PlanLds) <= sizeof(rkeys), "the work list builder reuses the key LDS");
+  if ((int)blockIdx.x == B) {
+    // the extra workgroup: the attention's work list (it depends on the
+    // offsets only)
+    build_attention_plan(*reinterpret_cast<PlanLds*>(rkeys), scan_sh, kept_offsets,
+                         query_passages, plan.passage_offsets, B, plan.H, total_kept,
+                         total_passages, plan.total_tokens, k_max, P_max, plan.n_ids,
+                         plan.items);
+    return;
+  }
   double* qnorm = reinterpret_cast<double*>(rkeys);
   const int b = blockIdx.x;
   int k0, k1, p0, p1;
@@ -504,12 +523,23 @@ hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
 hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
                               const int32_t* kept_offsets, const int32_t* query_passages,
                               uint64_t* rowmask, int32_t* rowptr_out, int32_t* col_out,
-                              hipStream_t s, const uint8_t* passage_keep) {
-  hipLaunchKernelGGL(edge_select_kernel, dim3(p.B), dim3(kGSelThreads), 0, s, ep.part,
-                     ep.qn2, ep.kn2, edge_slices(p), kept_offsets, query_passages, p.B,
-                     p.total_kept, p.total_passages, p.k_max, p.P_max, p.d, p.avg_degree,
-                     p.edge_rule, p.edge_metric, p.edge_beta, passage_keep, rowmask,
-                     rowptr_out, col_out);
+                              hipStream_t s, const uint8_t* passage_keep,
+                              const int32_t* passage_offsets, int32_t* plan) {
+  PlanArgs pa{};
+  const long long n_ids = plan ? attn_plan_ids(p) : 0;
+  if (n_ids > INT32_MAX / 16) return hipErrorInvalidValue;
+  if (n_ids > 0) {
+    pa.items = reinterpret_cast<int4*>(plan);
+    pa.passage_offsets = passage_offsets;
+    pa.H = p.H;
+    pa.total_tokens = p.total_tokens;
+    pa.n_ids = (int)n_ids;
+  }
+  hipLaunchKernelGGL(edge_select_kernel, dim3(p.B + (n_ids > 0 ? 1 : 0)), dim3(kGSelThreads),
+                     0, s, ep.part, ep.qn2, ep.kn2, edge_slices(p), kept_offsets,
+                     query_passages, p.B, p.total_kept, p.total_passages, p.k_max, p.P_max, p.d,
+                     p.avg_degree, p.edge_rule, p.edge_metric, p.edge_beta, passage_keep,
+                     rowmask, rowptr_out, col_out, pa);
   return hipGetLastError();
 }
 

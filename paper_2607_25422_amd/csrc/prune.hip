@@ -11,6 +11,9 @@
 // The score pass is the HBM stream of V: each wave streams rows with 16-byte
 // loads (a full 1 KiB per wave instruction), several rows and several column
 // chunks in flight per lane, against u_b staged once per workgroup in LDS.
+#include <algorithm>
+#include <type_traits>
+
 #include "skip_common.h"
 #include "skip_internal.h"
 #include "skip_pool.h"
@@ -26,20 +29,22 @@ constexpr int kScoreRows = 24;
 constexpr int kScoreR = 6;
 constexpr int kScoreU = 4;
 
+// Rows [24 rb, 24 rb + 24) of question b: z = <u_b, v_i> in float64 (and
+// sigma(z) if asked).  su: u_b in LDS (d doubles, filled here).  z is
+// written with device-coherent stores: the question's top-k may run on
+// another XCD.
 template <typename T>
-__global__ void __launch_bounds__(256)
-score_kernel(const T* __restrict__ V, const double* __restrict__ u, int N, int d,
-             double* __restrict__ z, float* __restrict__ scores) {
+__device__ __forceinline__ void score_rows(const T* __restrict__ V, const double* __restrict__ u,
+                                           int N, int d, int b, int rb, double* __restrict__ z,
+                                           float* __restrict__ scores, double* su) {
   constexpr int VEC = Vec16<T>::n;
-  extern __shared__ double su[];          // [d]
-  const int b = blockIdx.y;
   for (int c = threadIdx.x; c < d; c += blockDim.x) su[c] = u[(size_t)b * d + c];
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int rows_per_wave = kScoreRows / 4;
-  const int r_begin = blockIdx.x * kScoreRows + wave * rows_per_wave;
+  const int r_begin = rb * kScoreRows + wave * rows_per_wave;
   const int r_end = min(r_begin + rows_per_wave, N);
   const T* Vb = V + (size_t)b * N * d;
 
@@ -84,11 +89,73 @@ score_kernel(const T* __restrict__ V, const double* __restrict__ u, int N, int d
       const double t = wave_sum_f64(acc[rr]);
       const int r = r0 + rr;
       if (lane == 0 && r < r_end) {
-        z[(size_t)b * N + r] = t;
+        store_shared(&z[(size_t)b * N + r], t);
         if (scores) scores[(size_t)b * N + r] = (float)(1.0 / (1.0 + exp(-t)));
       }
     }
   }
+}
+
+// Exact top-k of question b's N logits by one workgroup (any size); the
+// logits are read device-coherently.  sh: LDS for the selection; scan_sh:
+// blockDim.x / 64 + 1 words.  Kept indices ascending.
+template <int MAXPT>
+__device__ __forceinline__ void topk_block(const double* __restrict__ z, int b, int N,
+                                           const int32_t* __restrict__ kept_offsets,
+                                           int total_kept, int32_t* __restrict__ kept_idx,
+                                           SelectShared* sh, uint32_t* scan_sh) {
+  int k0, k1;
+  range_of(kept_offsets, b, total_kept, k0, k1);
+  const int kk = min(k1 - k0, N);
+  const int C = (N + blockDim.x - 1) / blockDim.x;
+  const int e0 = threadIdx.x * C;
+  const int cnt = max(0, min(C, N - e0));
+  uint64_t keys[MAXPT];
+#pragma unroll
+  for (int j = 0; j < MAXPT; ++j)
+    keys[j] = (j < cnt) ? order_key(load_shared(&z[(size_t)b * N + e0 + j])) : 0ull;
+  const SelectMask<MAXPT> flags = block_select_top<MAXPT>(keys, cnt, N, kk, sh);
+  uint32_t total;
+  uint32_t pos = block_exclusive_scan((uint32_t)__popcll((uint64_t)flags), scan_sh, &total);
+#pragma unroll
+  for (int j = 0; j < MAXPT; ++j) {
+    if (flags & ((SelectMask<MAXPT>)1 << j)) {
+      if (pos < (uint32_t)kk) kept_idx[k0 + pos] = e0 + j;
+      ++pos;
+    }
+  }
+}
+
+// The prune stage in one launch: RB = ceil(N / kScoreRows) scoring
+// workgroups per question, question-major, then (optionally) the pooling
+// workgroups of the passage keys.  The last scoring workgroup of a question
+// to finish (a per-question counter, cleared by the question pooling before
+// the launch and again here after use) selects the question's top k, so the
+// top-k runs beside the scoring of later questions and the key pooling
+// instead of as a launch of its own.
+template <typename T, int MAXPT>
+__global__ void __launch_bounds__(256)
+prune_kernel(const T* __restrict__ V, const double* __restrict__ u, int N, int d, int B,
+             int RB, double* __restrict__ z, float* __restrict__ scores,
+             const int32_t* __restrict__ kept_offsets, int total_kept,
+             int32_t* __restrict__ kept_idx, int32_t* __restrict__ counters,
+             PoolRanges<T> keys, int key_slices) {
+  extern __shared__ __align__(16) double lds[];
+  __shared__ int last;
+  const int bid = blockIdx.x;
+  const int n_score = RB * B;
+  if (bid >= n_score) {
+    const int kb = bid - n_score;
+    pool_block<T>(keys, kb / key_slices, kb % key_slices, false, nullptr, d, lds);
+    return;
+  }
+  const int b = bid / RB, rb = bid % RB;
+  score_rows<T>(V, u, N, d, b, rb, z, scores, lds);
+  if (!finish_and_check_last(&counters[b], RB, &last)) return;
+  SelectShared* sh = reinterpret_cast<SelectShared*>(lds);
+  uint32_t* scan_sh = reinterpret_cast<uint32_t*>(sh + 1);
+  topk_block<MAXPT>(z, b, N, kept_offsets, total_kept, kept_idx, sh, scan_sh);
+  if (threadIdx.x == 0) store_shared(&counters[b], 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -161,22 +228,41 @@ gather_kernel(const T* __restrict__ V, const int32_t* __restrict__ kept_offsets,
 // Launchers.
 hipError_t launch_pool_question(const skip_problem_t& p, const void* Qtok,
                                 const int32_t* q_offsets, const void* w_bias,
-                                double* u, hipStream_t s) {
+                                double* u, int32_t* counters, hipStream_t s) {
   return launch_pools(p.dtype, p.d, Qtok, q_offsets, p.B, p.total_qtok, w_bias, u, nullptr,
-                      nullptr, 0, 0, nullptr, s);
+                      nullptr, 0, 0, nullptr, s, counters);
 }
 
-hipError_t launch_score(const skip_problem_t& p, const void* V, const double* u,
-                        double* z, float* scores, hipStream_t s) {
-  dim3 grid((p.N + kScoreRows - 1) / kScoreRows, p.B);
-  const size_t lds = (size_t)p.d * sizeof(double);
-  if (p.dtype == SKIP_F32)
-    hipLaunchKernelGGL(score_kernel<float>, grid, dim3(256), lds, s,
-                       (const float*)V, u, p.N, p.d, z, scores);
-  else
-    hipLaunchKernelGGL(score_kernel<bf16_t>, grid, dim3(256), lds, s,
-                       (const bf16_t*)V, u, p.N, p.d, z, scores);
-  return hipGetLastError();
+hipError_t launch_prune(const skip_problem_t& p, const void* V, const double* u, double* z,
+                        float* scores, const int32_t* kept_offsets, int32_t* kept_idx,
+                        int32_t* counters, const void* Kh, const int32_t* passage_offsets,
+                        int n_keys, double* kbar, hipStream_t s) {
+  if (p.B <= 0 || p.N <= 0) return hipSuccess;
+  const int RB = (p.N + kScoreRows - 1) / kScoreRows;
+  const int C = (p.N + 255) / 256;              // logits per thread in the top-k
+  if (C > 64) return hipErrorInvalidValue;
+  auto go = [&](auto tag, auto maxpt) -> hipError_t {
+    using T = decltype(tag);
+    constexpr int MAXPT = decltype(maxpt)::value;
+    const int slices = (p.d + 64 * kPoolChunks * Vec16<T>::n - 1) / (64 * kPoolChunks * Vec16<T>::n);
+    const size_t lds = std::max({(size_t)p.d * sizeof(double), pool_lds_bytes<T>(),
+                                 sizeof(SelectShared) + 20 * sizeof(uint32_t)});
+    const long long grid = (long long)RB * p.B + (long long)slices * n_keys;
+    if (grid > INT32_MAX) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((prune_kernel<T, MAXPT>), dim3((unsigned)grid), dim3(256), lds, s,
+                       (const T*)V, u, p.N, p.d, p.B, RB, z, scores, kept_offsets,
+                       p.total_kept, kept_idx, counters,
+                       PoolRanges<T>{(const T*)Kh, passage_offsets, n_keys, p.total_tokens, kbar},
+                       slices);
+    return hipGetLastError();
+  };
+  auto by_pt = [&](auto tag) -> hipError_t {
+    if (C <= 16) return go(tag, std::integral_constant<int, 16>{});
+    if (C <= 32) return go(tag, std::integral_constant<int, 32>{});
+    return go(tag, std::integral_constant<int, 64>{});
+  };
+  if (p.dtype == SKIP_F32) return by_pt(float{});
+  return by_pt(bf16_t{});
 }
 
 hipError_t launch_topk(const skip_problem_t& p, const double* z,

@@ -87,6 +87,7 @@ size_t workspace_size(const skip_problem_t& p) {
   n += align_up((size_t)p.B * S * p.P_max * sizeof(double));            // key norms
   n += align_up((size_t)p.total_kept * sizeof(uint64_t));             // rowmask
   n += align_up((size_t)attn_plan_ids(p) * 4 * sizeof(int32_t));      // attention work list
+  n += align_up((size_t)p.B * sizeof(int32_t));                       // prune counters
   return n;
 }
 
@@ -116,6 +117,7 @@ Workspace carve_workspace(const skip_problem_t& p, void* base) {
   w.kn2 = reinterpret_cast<double*>(take((size_t)p.B * S * p.P_max * sizeof(double)));
   w.rowmask = reinterpret_cast<uint64_t*>(take((size_t)p.total_kept * sizeof(uint64_t)));
   w.plan = reinterpret_cast<int32_t*>(take((size_t)attn_plan_ids(p) * 4 * sizeof(int32_t)));
+  w.counters = reinterpret_cast<int32_t*>(take((size_t)p.B * sizeof(int32_t)));
   w.bytes = off;
   return w;
 }
@@ -161,12 +163,11 @@ skip_status_t skip_prune_topk(const skip_problem_t* p, const void* V, const void
   if (workspace_bytes < workspace_size(*p)) return SKIP_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Workspace w = carve_workspace(*p, workspace);
-  SKIP_TRY(launch_pool_question(*p, Qtok, q_offsets, w_bias, w.u, s));
-  SKIP_TRY(launch_score(*p, V, w.u, w.z, scores, s));
-  if (p->total_kept > 0) {
-    SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
-    if (V_kept) SKIP_TRY(launch_gather(*p, V, kept_offsets, kept_idx, V_kept, s));
-  }
+  SKIP_TRY(launch_pool_question(*p, Qtok, q_offsets, w_bias, w.u, w.counters, s));
+  SKIP_TRY(launch_prune(*p, V, w.u, w.z, scores, kept_offsets, kept_idx, w.counters, nullptr,
+                        nullptr, 0, nullptr, s));
+  if (p->total_kept > 0 && V_kept)
+    SKIP_TRY(launch_gather(*p, V, kept_offsets, kept_idx, V_kept, s));
   return SKIP_OK;
 }
 
@@ -259,10 +260,13 @@ static skip_status_t xattn_impl(const skip_problem_t* p, const void* Qh, const v
     if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
     const QuerySource e{edge_rows ? edge_rows : Qh, nullptr, 0};
     SKIP_TRY(launch_edge_dot(*p, e, kept_offsets, query_passages, w.kbar, passage_keys, ep, s));
+    // the selection launch also builds the attention's work list
     SKIP_TRY(launch_edge_select(*p, ep, kept_offsets, query_passages, w.rowmask,
-                                edge_rowptr_out, edge_col_out, s, passage_keep));
+                                edge_rowptr_out, edge_col_out, s, passage_keep,
+                                passage_offsets, w.plan));
   }
-  SKIP_TRY(launch_attention_plan(*p, kept_offsets, query_passages, passage_offsets, w.plan, s));
+  if (given)
+    SKIP_TRY(launch_attention_plan(*p, kept_offsets, query_passages, passage_offsets, w.plan, s));
   SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,
                             w.rowmask, w.plan, O, lse, s));
   return SKIP_OK;
@@ -552,16 +556,13 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
   const bool work = p->total_kept > 0;
   QuerySource q{V, kept_idx, p->N};
   SKIP_TRY(mark());
-  // question pooling and (unless given) passage-key pooling in one launch
-  if (work) {
-    const int np = passage_keys ? 0 : p->total_passages;
-    SKIP_TRY(launch_pools(p->dtype, p->d, Qtok, q_offsets, p->B, p->total_qtok, w_bias, w.u,
-                          Kh, passage_offsets, np, p->total_tokens, w.kbar, s));
-  }
+  // question pooling (which also clears the prune launch's counters)
+  if (work) SKIP_TRY(launch_pool_question(*p, Qtok, q_offsets, w_bias, w.u, w.counters, s));
   SKIP_TRY(mark());
-  if (work) SKIP_TRY(launch_score(*p, V, w.u, w.z, nullptr, s));
-  SKIP_TRY(mark());
-  if (work) SKIP_TRY(launch_topk(*p, w.z, kept_offsets, kept_idx, s));
+  // scoring and top-k, with (unless given) the passage-key pooling beside them
+  if (work)
+    SKIP_TRY(launch_prune(*p, V, w.u, w.z, nullptr, kept_offsets, kept_idx, w.counters, Kh,
+                          passage_offsets, passage_keys ? 0 : p->total_passages, w.kbar, s));
   SKIP_TRY(mark());
   if (gate && p->total_passages > 0) {
     // verify step: question and kept-row means, then the gate on the passage
@@ -577,13 +578,11 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
     SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,
                              EdgePartials{w.part, w.qn2, w.kn2}, s));
   SKIP_TRY(mark());
+  // edge selection, with the attention's work list built beside it
   if (work)
     SKIP_TRY(launch_edge_select(*p, EdgePartials{w.part, w.qn2, w.kn2}, kept_offsets,
                                 query_passages, w.rowmask, nullptr, nullptr, s,
-                                gate ? passage_keep : nullptr));
-  SKIP_TRY(mark());
-  if (work)
-    SKIP_TRY(launch_attention_plan(*p, kept_offsets, query_passages, passage_offsets, w.plan, s));
+                                gate ? passage_keep : nullptr, passage_offsets, w.plan));
   SKIP_TRY(mark());
   if (work)
     SKIP_TRY(launch_attention(*p, q, kept_offsets, Kh, Vh, passage_offsets, query_passages,

@@ -20,6 +20,7 @@ struct Workspace {
   double* kn2;        // [B][S][P_max] partial squared passage-key norms
   uint64_t* rowmask;  // [total_kept]  neighbour passages of each kept row
   int32_t* plan;      // [attn_plan_ids][4] attention work list
+  int32_t* counters;  // [B] scoring workgroups finished per question
   size_t bytes;
 };
 
@@ -28,9 +29,14 @@ Workspace carve_workspace(const skip_problem_t& p, void* base);
 // Stage 1 ---------------------------------------------------------------
 hipError_t launch_pool_question(const skip_problem_t& p, const void* Qtok,
                                 const int32_t* q_offsets, const void* w_bias,
-                                double* u, hipStream_t s);
-hipError_t launch_score(const skip_problem_t& p, const void* V, const double* u,
-                        double* z, float* scores, hipStream_t s);
+                                double* u, int32_t* counters, hipStream_t s);
+// Scoring and top-k of every question in one launch (u and the cleared
+// counters from launch_pool_question), plus the pooling of n_keys passage
+// keys of Kh into kbar (0: none).
+hipError_t launch_prune(const skip_problem_t& p, const void* V, const double* u, double* z,
+                        float* scores, const int32_t* kept_offsets, int32_t* kept_idx,
+                        int32_t* counters, const void* Kh, const int32_t* passage_offsets,
+                        int n_keys, double* kbar, hipStream_t s);
 hipError_t launch_topk(const skip_problem_t& p, const double* z,
                        const int32_t* kept_offsets, int32_t* kept_idx,
                        hipStream_t s);
@@ -117,10 +123,11 @@ hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
                            const int32_t* query_passages, const double* kbar,
                            const float* passage_keys, EdgePartials ep, hipStream_t s);
 hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
-                              const int32_t* kept_offsets,
-                              const int32_t* query_passages, uint64_t* rowmask,
-                              int32_t* rowptr_out, int32_t* col_out,
-                              hipStream_t s, const uint8_t* passage_keep = nullptr);
+                              const int32_t* kept_offsets, const int32_t* query_passages,
+                              uint64_t* rowmask, int32_t* rowptr_out, int32_t* col_out,
+                              hipStream_t s, const uint8_t* passage_keep = nullptr,
+                              const int32_t* passage_offsets = nullptr,
+                              int32_t* plan = nullptr);
 hipError_t launch_csr_to_mask(const skip_problem_t& p, const int32_t* kept_offsets,
                               const int32_t* query_passages,
                               const int32_t* edge_rowptr, const int32_t* edge_col,

@@ -10,10 +10,9 @@ namespace skip {
 // Workgroup = (column slice of 64 lanes x kPoolChunks x 16 bytes, range);
 // wave w sums rows w, w+4, ... (four rows, two 16-byte chunks each, in flight
 // per lane); the four partial sums are combined in wave order through LDS.
-// One launch serves two independent sets of ranges: the questions (ranges
-// 0..nq-1 of Qtok, written as the scoring vector u = mean / sqrt(d) + w) and
-// the passages (the following ranges of Kh, written as their mean), so the
-// short question pooling runs alongside the passage stream.
+// Questions are written as the scoring vector u = mean / sqrt(d) + w, passage
+// keys as their mean.  The same workgroup body runs in the pooling launch and
+// in the prune launch (passage keys beside the scoring).
 constexpr int kPoolChunks = 2;
 
 template <typename T>
@@ -25,15 +24,21 @@ struct PoolRanges {
   double* out;      // [n][d]
 };
 
+// Bytes of LDS one pooling workgroup uses (four waves' partial sums).
 template <typename T>
-__global__ void __launch_bounds__(256)
-pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) {
+constexpr size_t pool_lds_bytes() {
+  return 4 * 64 * kPoolChunks * Vec16<T>::n * sizeof(double);
+}
+
+// One pooling workgroup (256 threads): range j of rg, column slice `slice`;
+// `question` ranges are written as the scoring vector (mean / sqrt(d) + w).
+// part: pool_lds_bytes<T>() of LDS.  Contains one __syncthreads().
+template <typename T>
+__device__ __forceinline__ void pool_block(const PoolRanges<T>& rg, int j, int slice,
+                                           bool question, const T* __restrict__ w, int d,
+                                           double* part) {
   constexpr int VEC = Vec16<T>::n;
   constexpr int CH = kPoolChunks;
-  __shared__ double part[4][64][CH * VEC];
-  const bool question = (int)blockIdx.y < qr.n;
-  const PoolRanges<T> rg = question ? qr : pr;
-  const int j = question ? (int)blockIdx.y : (int)blockIdx.y - qr.n;
   const T* __restrict__ src = rg.src;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -41,7 +46,7 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
   bool ok[CH];
 #pragma unroll
   for (int h = 0; h < CH; ++h) {
-    cc[h] = ((blockIdx.x * CH + h) * 64 + lane) * VEC;
+    cc[h] = ((slice * CH + h) * 64 + lane) * VEC;
     ok[h] = cc[h] < d;
   }
   int t0, t1;
@@ -82,14 +87,17 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
       for (int e = 0; e < VEC; ++e) acc[h][e] += v[e];
     }
   }
+  // part[wave][lane][CH * VEC]
+  double* mine = part + ((size_t)wave * 64 + lane) * (CH * VEC);
 #pragma unroll
   for (int h = 0; h < CH; ++h)
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) part[wave][lane][h * VEC + e] = acc[h][e];
+    for (int e = 0; e < VEC; ++e) mine[h * VEC + e] = acc[h][e];
   __syncthreads();
   if (wave != 0) return;
   const int L = t1 - t0;
   const double rsd = 1.0 / sqrt((double)d);
+  const size_t wstride = (size_t)64 * (CH * VEC);
 #pragma unroll
   for (int h = 0; h < CH; ++h) {
     if (!ok[h]) continue;
@@ -103,8 +111,8 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
       const int i = h * VEC + e;
-      const double s = ((part[0][lane][i] + part[1][lane][i]) + part[2][lane][i]) +
-                       part[3][lane][i];
+      const double s = ((mine[i] + mine[wstride + i]) + mine[2 * wstride + i]) +
+                       mine[3 * wstride + i];
       double m = (L > 0) ? s / (double)L : 0.0;
       if (question) m = m * rsd + wv[e];
       rg.out[(size_t)j * d + cc[h] + e] = m;
@@ -112,12 +120,28 @@ pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d) 
   }
 }
 
+// One launch serves two independent sets of ranges: the questions (ranges
+// 0..nq-1 of Qtok, written as the scoring vector) and the passages (the
+// following ranges of Kh, written as their mean).  counters (or NULL): the
+// per-question completion counters of the scoring launch, cleared here.
+template <typename T>
+__global__ void __launch_bounds__(256)
+pool_kernel(PoolRanges<T> qr, const T* __restrict__ w, PoolRanges<T> pr, int d,
+            int32_t* __restrict__ counters) {
+  __shared__ double part[4 * 64 * kPoolChunks * Vec16<T>::n];
+  const bool question = (int)blockIdx.y < qr.n;
+  const int j = question ? (int)blockIdx.y : (int)blockIdx.y - qr.n;
+  if (counters && question && blockIdx.x == 0 && threadIdx.x == 0) counters[j] = 0;
+  pool_block<T>(question ? qr : pr, j, blockIdx.x, question, w, d, part);
+}
+
 // Questions (Qtok by q_offsets -> u, nq ranges) and passages (Kh by
 // passage_offsets -> kbar, np ranges); either set may be empty.
 inline hipError_t launch_pools(int dtype, int d, const void* Qtok, const int32_t* q_offsets,
                                int nq, int total_qtok, const void* w, double* u,
                                const void* Kh, const int32_t* passage_offsets, int np,
-                               int total_tokens, double* kbar, hipStream_t s) {
+                               int total_tokens, double* kbar, hipStream_t s,
+                               int32_t* counters = nullptr) {
   if (nq + np <= 0) return hipSuccess;
   if (dtype == SKIP_F32) {
     dim3 grid((d + 256 * kPoolChunks - 1) / (256 * kPoolChunks), nq + np);
@@ -126,7 +150,7 @@ inline hipError_t launch_pools(int dtype, int d, const void* Qtok, const int32_t
                        (const float*)w,
                        PoolRanges<float>{(const float*)Kh, passage_offsets, np, total_tokens,
                                          kbar},
-                       d);
+                       d, counters);
   } else {
     dim3 grid((d + 512 * kPoolChunks - 1) / (512 * kPoolChunks), nq + np);
     hipLaunchKernelGGL(pool_kernel<bf16_t>, grid, dim3(256), 0, s,
@@ -134,7 +158,7 @@ inline hipError_t launch_pools(int dtype, int d, const void* Qtok, const int32_t
                        (const bf16_t*)w,
                        PoolRanges<bf16_t>{(const bf16_t*)Kh, passage_offsets, np,
                                           total_tokens, kbar},
-                       d);
+                       d, counters);
   }
   return hipGetLastError();
 }

@@ -17,6 +17,8 @@
 // registers (keys[0..cnt)), C = ceil(n / blockDim.x) <= MAXPT.
 #pragma once
 
+#include <type_traits>
+
 #include "skip_common.h"
 
 namespace skip {
@@ -31,13 +33,20 @@ struct SelectShared {
   uint32_t scan[20];
 };
 
+// Per-thread element masks: 32 bits, or 64 for more elements a thread.
+template <int MAXPT>
+using SelectMask = typename std::conditional<(MAXPT > 32), uint64_t, uint32_t>::type;
+
 // Returns a bitmask over the thread's elements (bit j = element t*C + j).
 template <int MAXPT>
-__device__ uint32_t block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int n,
-                                     int kk, SelectShared* sh) {
-  static_assert(MAXPT <= 32, "flags are a 32-bit mask");
-  const uint32_t all = (cnt >= 32) ? 0xffffffffu : ((1u << cnt) - 1u);
-  if (kk <= 0) return 0u;
+__device__ SelectMask<MAXPT> block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int n,
+                                              int kk, SelectShared* sh) {
+  static_assert(MAXPT <= 64, "flags are at most a 64-bit mask");
+  using M = SelectMask<MAXPT>;
+  constexpr int W = 8 * sizeof(M);
+  const M one = 1;
+  const M all = (cnt >= W) ? ~(M)0 : ((one << cnt) - one);
+  if (kk <= 0) return 0;
   if (kk >= n) return all;
 
   for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[0][i] = 0u;
@@ -93,23 +102,23 @@ __device__ uint32_t block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int
     if (inbin == need) { whole_bucket = true; break; }
   }
 
-  uint32_t flags = 0u, inb = 0u;
+  M flags = 0, inb = 0;
 #pragma unroll
   for (int j = 0; j < MAXPT; ++j) {
     if (j < cnt) {
       const uint64_t m = keys[j] & mask;
-      if (m > prefix) flags |= 1u << j;
-      else if (m == prefix) inb |= 1u << j;
+      if (m > prefix) flags |= one << j;
+      else if (m == prefix) inb |= one << j;
     }
   }
   if (whole_bucket) return flags | inb;
   // Exactly equal keys: admit the `need` lowest indices.
   uint32_t total;
-  uint32_t rank = block_exclusive_scan(__popc(inb), sh->scan, &total);
+  uint32_t rank = block_exclusive_scan((uint32_t)__popcll((uint64_t)inb), sh->scan, &total);
 #pragma unroll
   for (int j = 0; j < MAXPT; ++j) {
-    if (inb & (1u << j)) {
-      if (rank < need) flags |= 1u << j;
+    if (inb & (one << j)) {
+      if (rank < need) flags |= one << j;
       ++rank;
     }
   }

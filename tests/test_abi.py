@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol(b):
 
 
 def test_version_and_status_strings(b):
-    assert b.abi_version() == 6
+    assert b.abi_version() == 7
     for s in range(5):
         assert b.status_string(s).startswith("SKIP_")
     assert "UNKNOWN" in b.status_string(99)
@@ -66,10 +66,11 @@ def test_workspace_bytes(b):
     # u + z + kbar + edge partials (4 slices of 256 columns) + row-norm and
     # key-norm partials + rowmask + the attention work list (16 bytes per
     # workgroup id: 8 ids per run of 8 (question, head) groups, 2 * 16 groups,
-    # one chunk of <= 192 rows), each rounded to 256 bytes
+    # one chunk of <= 192 rows) + one prune counter per question, each rounded
+    # to 256 bytes
     S = 4
     parts = [2 * 1024 * 8, 2 * 576 * 8, 3 * 1024 * 8, 2 * S * 96 * 2 * 8, 2 * S * 96 * 8,
-             2 * S * 2 * 8, 192 * 8, 4 * 8 * 16]
+             2 * S * 2 * 8, 192 * 8, 4 * 8 * 16, 2 * 4]
     assert n == sum((x + 255) // 256 * 256 for x in parts)
     with pytest.raises(b.SkipError):
         b.workspace_bytes(_problem(b, B=0, q_offsets=[0], kept_offsets=[0], query_passages=[0]))
