@@ -135,6 +135,32 @@ def test_prune_ties_lowest_index(B):
     assert idx[k0:k1].tolist() == list(range(k1 - k0))
 
 
+@pytest.mark.parametrize("k", [100, 400])
+@pytest.mark.parametrize("n_equal", [30, 200, 600])
+def test_prune_tie_band_at_the_cut(B, n_equal, k):
+    # n_equal tokens are made copies of the token ranked k - n_equal/2 (or of
+    # the top token), so the k-th largest logit is shared by a band of equal
+    # values on both sides of the cut, from a few to more than k of them: the
+    # selection must take every logit above the band and the band's lowest
+    # indices, as the oracle does.
+    batch = wls.make_batch("llava_bf16", 11, B=3, N=1024, H=4, d_h=64, k=(k,))
+    V = batch.V.clone()
+    w = None if batch.w_bias is None else batch.w_bias.double().numpy()
+    for b in range(batch.B):
+        t0, t1 = int(batch.q_offsets[b]), int(batch.q_offsets[b + 1])
+        q_bar = orc.mean_pool_question(batch.Qtok[t0:t1].double().numpy())
+        z = orc.qvs_logits(V[b].double().numpy(), q_bar, w)
+        order = np.argsort(-z, kind="stable")
+        pivot = int(order[max(0, k - n_equal // 2)])
+        V[b, torch.from_numpy(order[-n_equal:].copy())] = V[b, pivot].clone()   # lowest ranks become copies
+    batch.V = V
+    db, idx, _, _ = run_prune(B, batch)
+    ref = oracle_route(batch, with_attention=False)
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist(), f"question {b}"
+
+
 @pytest.mark.parametrize("seed", wls.SEEDS)
 @pytest.mark.parametrize("name", wls.ORDER)
 def test_prune_named_full_size(B, name, seed):
