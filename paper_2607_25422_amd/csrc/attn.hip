@@ -241,6 +241,9 @@ attn_sparse_kernel(const bf16_t* __restrict__ qbase, const int32_t* __restrict__
 
   if (wave >= kSpCompute) {
     // ---- loader waves: the first streams K, the second V --------------------
+    // (their LDS writes must land before each barrier; issuing ahead of the
+    // compute waves' operand reads keeps them from queueing behind those)
+    __builtin_amdgcn_s_setprio(3);
     const bool isV = wave == kSpCompute + 1;
     const bf16_t* gsrc = isV ? Vh : Kh;
     bf16_t* buf = isV ? Vbuf : Kbuf;
