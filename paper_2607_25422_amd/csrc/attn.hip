@@ -101,7 +101,7 @@ __device__ __forceinline__ void lds_wait_all(u32x2 (&v)[N]) {
 // order; compute wave w takes blocks w and w + 6.  Per tile and block:
 //   S^T (32 tokens x 16 rows) = K_tile . Q^T        v_mfma_f32_16x16x32_bf16
 //   online softmax in fp32 (base 2); each weight p split into bf16 hi + lo
-//   (hi = p rounded, lo = the rest rounded), so the PV product sees p to
+//   (hi = p truncated, lo = the rest rounded), so the PV product sees p to
 //   about 2^-16 relative and the result does not depend on the output type,
 //   O^T (d_h x 16 rows)     += V_tile^T . (P_hi + P_lo)^T
 // Computing the transposed products keeps each query row in one lane column
