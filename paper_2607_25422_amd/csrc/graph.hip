@@ -5,8 +5,9 @@
 //                  heads flattened), float64 sums
 //   edge_dot     : float64 partial sums of <q_i, kbar_j>, |q_i|^2, |kbar_j|^2
 //                  over slices of d
-//   (cosine)       c_ij = <q_i, kbar_j> / (|q_i| |kbar_j|), 0 when a norm is 0,
-//                  formed from the partial sums by the selection kernel
+//   edge_keys    : c_ij = <q_i, kbar_j> / (|q_i| |kbar_j|) (0 when a norm is
+//                  0) from the partial sums in slice order, as an
+//                  order-preserving 64-bit key per candidate
 //   edge_select  : per question, the E_b = min(ceil(avg_degree * k_b),
 //                  k_b * P_b) largest cosines (lower flattened index i*P_b+j
 //                  on ties) -> one 64-bit neighbour mask per kept row, and
@@ -25,27 +26,28 @@ namespace skip {
 
 // ---------------------------------------------------------------------------
 // Edge dot products on the float64 matrix cores, split over d.
-// Workgroup = (256-column slice, question), one workgroup per CU over the
-// chip for the usual shapes; the slices of a question run on one XCD
-// (workgroup id L goes to XCD L % 8).  v_mfma_f64_16x16x4_f64 takes one
-// element of A (16 rows x 4 columns) and one of B (4 columns x 16 passages)
-// per lane: lane l supplies row/passage l % 16 and column slot l / 16.  The
-// contraction order over columns is free, so column slot kk of MFMA m within
-// a group of 4·E columns (E = 8 bf16 or 4 f32 per 16-byte chunk) is column
-// E*kk + m: a lane then reads one 16-byte chunk of its row and E consecutive
-// key values per group.
-//   * The kept rows come into LDS in blocks of 192 (16-row tiles; wave w
-//     takes tiles w, w + 4, w + 8) by direct loads of whole 512-byte row
-//     slices (f32 rows in two 128-column passes); chunk c of row r sits at
-//     slot c ^ (r & 7), so that the lanes' reads of one chunk group fall on
-//     distinct banks.  Chunks past the slice are cleared.
+// Workgroup = (question, 256-column slice, block of 64 kept rows); the slices
+// and row blocks of a question run on one XCD (workgroup id L goes to XCD
+// L % 8), where they share the keys in the L2.  v_mfma_f64_16x16x4_f64 takes
+// one element of A (16 rows x 4 columns) and one of B (4 columns x 16
+// passages) per lane: lane l supplies row/passage l % 16 and column slot
+// l / 16.  The contraction order over columns is free, so column slot kk of
+// MFMA m within a group of 4·E columns (E = 8 bf16 or 4 f32 per 16-byte
+// chunk) is column E*kk + m: a lane then reads one 16-byte chunk of its row
+// and E consecutive key values per group.
+//   * Wave w takes the 16-row tile w of the block and reads its rows' slice
+//     straight from memory, one 16-byte chunk per lane and group (bf16: all
+//     chunks loaded into registers before the keys are staged; f32, twice
+//     the chunks: each where it is used).
 //   * The passage keys of the slice sit in LDS as float64, 16 passages at a
-//     time, read by all four waves.
+//     time, read by all four waves.  With only the keys in LDS (33 KiB) four
+//     bf16 workgroups share a CU, so one wave's loads and conversions overlap
+//     another's matrix products.
 // Each lane also sums the squares of its row values (partial row norms); the
-// key norms come from the keys in LDS.  Results per slice are summed in slice
-// order by the selection kernel.
+// key norms come from the keys in LDS (row block 0).  Results per slice are
+// summed in slice order by the key launch.
 constexpr int kEdCols = 256;               // columns per slice
-constexpr int kEdBlockRows = 192;          // rows per LDS block (12 tiles)
+constexpr int kEdRows = 64;                // rows per workgroup (a 16-row tile per wave)
 constexpr int kEdPT = 16;                  // passages per tile
 constexpr int kEdKeyStride = kEdCols + 2;  // doubles per key row in LDS (bank spread)
 
@@ -58,182 +60,197 @@ struct EdgeDotArgs {
   const int32_t* query_passages;
   const double* kbar;          // [total_passages][d] float64 keys, or
   const float* pkeys;          // [total_passages][d] caller-given keys
-  int d, total_kept, total_passages, k_max, P_max, B, S;
+  int d, total_kept, total_passages, k_max, P_max, B, S, RB;
   double* part;                // [B][S][k_max][P_max] partial <q_i, k̄_j>
   double* qn2p;                // [B][S][k_max]        partial |q_i|^2
   double* kn2p;                // [B][S][P_max]        partial |k̄_j|^2
 };
 
 template <typename T>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2)   // waves per SIMD
 edge_dot_kernel(const T* __restrict__ rows, EdgeDotArgs a) {
   constexpr int E = 16 / (int)sizeof(T);          // columns per 16-byte chunk
-  constexpr int CPP = 32 * E;                      // columns per pass (512 bytes of a row)
-  constexpr int NP = kEdCols / CPP;                // passes per slice
-  __shared__ __align__(16) uint8_t rbuf[kEdBlockRows * 512];
+  constexpr int NG = kEdCols / (4 * E);            // groups of 4·E columns per slice
   __shared__ __align__(16) double ks[kEdPT * kEdKeyStride];
   const int L = blockIdx.x, xcd = L & 7, jl = L >> 3;
-  const int s = jl % a.S, b = xcd + 8 * (jl / a.S), tid = threadIdx.x;
+  const int per_q = a.S * a.RB;
+  const int b = xcd + 8 * (jl / per_q);
+  const int s = (jl % per_q) % a.S, rb = (jl % per_q) / a.S, tid = threadIdx.x;
   if (b >= a.B) return;
   int k0, k1, p0, p1;
   range_of(a.kept_offsets, b, a.total_kept, k0, k1);
   range_of(a.query_passages, b, a.total_passages, p0, p1);
   const int k = min(k1 - k0, a.k_max);
   const int P = min(min(p1 - p0, a.P_max), 64);
-  if (k <= 0 || P <= 0) return;                  // nothing of this question is read
+  // nothing of this question is read, or the block is past its rows
+  if (k <= 0 || P <= 0 || rb * kEdRows >= k) return;
   const int c0 = s * kEdCols, ncol = min(kEdCols, a.d - c0);
-  const int w = tid >> 6, lane = tid & 63, l16 = lane & 15, kk = lane >> 4;
-  const uint32_t rlds = lds_addr(rbuf);
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
+  const int lane = tid & 63, l16 = lane & 15, kk = lane >> 4;
   const size_t zs = (size_t)b * a.S + s;
+  const int tile0 = rb * kEdRows + 16 * w;         // first row of the wave's tile
 
-  // Copy rows blk0 .. blk0 + 191, columns [pass·CPP, pass·CPP + CPP) of the
-  // slice, into rbuf.  Wave w copies rows 48w .. 48w + 47, two per load
-  // instruction: lane l writes slot l % 32 of row 2j + l / 32, which holds
-  // chunk (l % 32) ^ (row & 7).  Rows past the question repeat its last row;
-  // chunks past the slice read its first chunk (cleared afterwards).  The
-  // row indices are all read before the first copy: the copies are opaque to
-  // the compiler, which would otherwise wait for each one before the next.
-  auto stage_rows = [&](int blk0, int pass) {
-    const int half = lane >> 5, slot = lane & 31;
-    int rid[24];
+  // The lane's row (rows past the question repeat its last row) and its
+  // chunk of each group; chunks past the slice are zero.
+  const int ri = min(tile0 + l16, k - 1);
+  const int rid = a.kept_idx ? a.kept_idx[k0 + ri] : k0 + ri;
+  const T* rsrc = rows + (a.kept_idx ? ((size_t)b * a.N + clampi(rid, 0, a.N - 1)) * a.d
+                                     : (size_t)rid * a.d) + c0;
+  // Keys of passages pt0 .. pt0 + 15 over the slice.  Float64 keys go
+  // straight into LDS (direct loads, half a key row of 128 values per wave
+  // instruction; wave w takes half rows w, w + 4, ...); caller-given f32 keys
+  // pass through registers and are widened.  Passages past P repeat the last
+  // one and columns past the slice repeat its last pair: their products
+  // meet zero row values or are not written, and the key norms skip them.
+  // The first keys (cached, shared by the question's workgroups) are
+  // requested before the rows, so that they arrive first: the products then
+  // start while the rows stream in, group by group.
+  constexpr int KPT = kEdPT * kEdCols / 256;   // f32 key values per thread
+  static_assert(KPT == kEdPT && kEdCols == 256, "thread t stages column t of each key");
+  static_assert((kEdKeyStride * 8) % 16 == 0, "key rows start on 16 bytes");
+  const bool dma = a.pkeys == nullptr;
+  const uint32_t ks_lds = lds_addr(ks);
+  float kf[KPT];
+  auto load_keys = [&](int pt0) {
+    if (dma) {
 #pragma unroll
-    for (int j = 0; j < 24; ++j) {
-      const int i = min(blk0 + 48 * w + 2 * j + half, k - 1);
-      rid[j] = a.kept_idx ? a.kept_idx[k0 + i] : k0 + i;
-    }
-    __builtin_amdgcn_sched_barrier(0);
+      for (int q = 0; q < 2 * kEdPT / 4; ++q) {
+        const int hr = 4 * q + w, n = hr >> 1, h = hr & 1;
+        const int col = min(h * 128 + 2 * lane, ncol - 2);
+        lds_dma16(a.kbar + (size_t)(p0 + min(pt0 + n, P - 1)) * a.d + c0 + col,
+                  __builtin_amdgcn_readfirstlane(ks_lds +
+                                                 (uint32_t)(n * kEdKeyStride * 8 + h * 1024)));
+      }
+    } else {
+      const int cc = min(tid, ncol - 1);
 #pragma unroll
-    for (int j = 0; j < 24; ++j) {
-      const int r = 48 * w + 2 * j + half;         // row within the block
-      const int col = pass * CPP + (slot ^ (r & 7)) * E;
-      const int colc = col < ncol ? col : 0;
-      const size_t row = a.kept_idx ? (size_t)b * a.N + clampi(rid[j], 0, a.N - 1)
-                                    : (size_t)rid[j];
-      lds_dma16(rows + row * a.d + c0 + colc,
-               __builtin_amdgcn_readfirstlane(rlds + (uint32_t)(48 * w + 2 * j) * 512u));
+      for (int u = 0; u < KPT; ++u)
+        kf[u] = a.pkeys[(size_t)(p0 + min(pt0 + u, P - 1)) * a.d + c0 + cc];
     }
   };
-  // after the copies of a pass have landed: clear the chunks past the slice
-  // (each wave its own rows; every wave waits for its copies first)
-  auto finish_rows = [&](int pass) {
-    wait_vmcnt<0>();
-    if (pass * CPP + CPP > ncol) {
-      for (int t = lane; t < 48 * 32; t += 64) {
-        const int r = 48 * w + (t >> 5), sl = t & 31;
-        if (pass * CPP + (sl ^ (r & 7)) * E >= ncol)
-          *reinterpret_cast<u32x4*>(rbuf + r * 512 + sl * 16) = u32x4{0u, 0u, 0u, 0u};
-      }
+  auto store_keys = [&]() {
+    if (!dma) {
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) ks[u * kEdKeyStride + tid] = (double)kf[u];
     }
-    __syncthreads();                               // rows of every wave are in
   };
-
-  for (int blk0 = 0; blk0 < k; blk0 += kEdBlockRows) {
-    for (int pt0 = 0; pt0 < P; pt0 += kEdPT) {
-      // two accumulators per tile (even and odd MFMA of a group), added at
-      // the end: six independent chains keep the matrix pipeline busy
-      double qq[3] = {0.0, 0.0, 0.0};
-      f64x4_t acc[3][2];
+  // (the row address first: waiting for its index later would also wait
+  // for the direct key loads, which the compiler does not count)
+  asm volatile("" : : "v"(rsrc) : "memory");
+  load_keys(0);
+  // bf16: every chunk of the slice in registers; f32 (twice the chunks):
+  // each group's chunk is loaded where it is used
+  constexpr bool kStage = sizeof(T) == 2;
+  u32x4 x[kStage ? NG : 1];
+  if (!kStage) {
+  } else if (ncol == kEdCols) {
+    // a whole slice: one base address, constant offsets
+    const T* rl = rsrc + kk * E;
 #pragma unroll
-      for (int t = 0; t < 3; ++t) acc[t][0] = acc[t][1] = f64x4_t{0.0, 0.0, 0.0, 0.0};
-      for (int pass = 0; pass < NP; ++pass) {
-        __syncthreads();                           // the previous rows and keys are read
-        stage_rows(blk0, pass);
-        // keys of passages pt0 .. pt0 + 15 over this pass's columns (0 past P
-        // or the slice), under the row copies
-        // (every load unconditional, passages and columns clamped into range
-        // and the value replaced by 0 afterwards, so that they all issue
-        // before the first wait)
-        {
-          constexpr int KPT = kEdPT * CPP / 256;   // key values per thread
-          double kvv[KPT];
+    for (int g = 0; g < NG; ++g) x[g] = *reinterpret_cast<const u32x4*>(rl + g * 4 * E);
+  } else {
 #pragma unroll
-          for (int u = 0; u < KPT; ++u) {
-            const int t = tid + 256 * u, n = t / CPP, c = pass * CPP + t % CPP;
-            const size_t o = (size_t)(p0 + min(pt0 + n, P - 1)) * a.d + c0 + min(c, ncol - 1);
-            kvv[u] = a.pkeys ? (double)a.pkeys[o] : a.kbar[o];
-          }
-#pragma unroll
-          for (int u = 0; u < KPT; ++u) {
-            const int t = tid + 256 * u, n = t / CPP, c = pass * CPP + t % CPP;
-            ks[n * kEdKeyStride + c] = (pt0 + n < P && c < ncol) ? kvv[u] : 0.0;
-          }
-        }
-        finish_rows(pass);
-        if (blk0 == 0) {
-          // |k̄_j|^2 over the pass's columns: wave w takes passages w, w + 4,
-          // w + 8, w + 12, lane l the columns l, l + 64, ... in order, then a
-          // fixed shuffle tree; added to the partial of the previous pass
-          double q2[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const double* kr = ks + (w + 4 * u) * kEdKeyStride + pass * CPP;
-            q2[u] = 0.0;
-            for (int c = lane; c < CPP; c += 64) q2[u] = fma(kr[c], kr[c], q2[u]);
-          }
-#pragma unroll
-          for (int sh = 32; sh >= 1; sh >>= 1)
-#pragma unroll
-            for (int u = 0; u < 4; ++u) q2[u] += __shfl_xor(q2[u], sh, kWave);
-          if (lane == 0) {
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int j = pt0 + w + 4 * u;
-              if (j < P) {
-                double* o = a.kn2p + zs * a.P_max + j;
-                *o = (pass == 0 ? 0.0 : *o) + q2[u];
-              }
-            }
-          }
-        }
-        // products: per group of 4 chunks, one key read (E values) feeds the
-        // three row tiles of the wave
-        const double* kp = ks + l16 * kEdKeyStride + pass * CPP + kk * E;
-#pragma unroll 2
-        for (int g = 0; g < 8; ++g) {
-          double kv[E];
-#pragma unroll
-          for (int m = 0; m < E; ++m) kv[m] = kp[g * 4 * E + m];
-          double qa[3][8];
-#pragma unroll
-          for (int t = 0; t < 3; ++t) {
-            const int r = 16 * (w + 4 * t) + l16;          // row within the block
-            const u32x4 x = *reinterpret_cast<const u32x4*>(
-                rbuf + r * 512 + (((4 * g + kk) ^ (r & 7)) * 16));
-            unpack16_f64<T>(x, qa[t]);
-          }
-#pragma unroll
-          for (int m = 0; m < E; ++m)
-#pragma unroll
-            for (int t = 0; t < 3; ++t)
-              acc[t][m & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[t][m], kv[m], acc[t][m & 1], 0, 0, 0);
-          if (pt0 == 0) {
-#pragma unroll
-            for (int t = 0; t < 3; ++t)
-#pragma unroll
-              for (int m = 0; m < E; ++m) qq[t] = fma(qa[t][m], qa[t][m], qq[t]);
-          }
-        }
-      }
-      // D[i][j]: register v of lane l holds row 4v + l/16 of the tile, passage l % 16
-#pragma unroll
-      for (int t = 0; t < 3; ++t) {
-        const int tile0 = blk0 + 16 * (w + 4 * t);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int i = tile0 + 4 * v + kk, j = pt0 + l16;
-          if (i < k && j < P) a.part[(zs * a.k_max + i) * a.P_max + j] = acc[t][0][v] + acc[t][1][v];
-        }
-        if (pt0 == 0) {
-          // lanes l16, l16 + 16, l16 + 32, l16 + 48 hold the four column slots of row l16
-          double q = qq[t];
-          q += __shfl_xor(q, 16, kWave);
-          q += __shfl_xor(q, 32, kWave);
-          const int i = tile0 + l16;
-          if (kk == 0 && i < k) a.qn2p[zs * a.k_max + i] = q;
-        }
-      }
+    for (int g = 0; g < NG; ++g) {
+      const int col = g * 4 * E + kk * E;
+      x[g] = *reinterpret_cast<const u32x4*>(rsrc + (col < ncol ? col : 0));
     }
   }
+  // the row loads stay above this point: the direct key loads, issued
+  // before them, are complete once at most their count is pending
+  asm volatile("" ::: "memory");
+  if (dma) wait_vmcnt<kStage ? NG : 0>();
+  store_keys();
+
+  double qq = 0.0;
+  for (int pt0 = 0; pt0 < P; pt0 += kEdPT) {
+    if (pt0 > 0) {
+      __syncthreads();                             // the previous keys are read
+      load_keys(pt0);
+      if (dma) wait_vmcnt<0>();
+      store_keys();
+    }
+    __syncthreads();
+    if (rb == 0) {
+      // |k̄_j|^2 over the slice: wave w takes passages w, w + 4, w + 8,
+      // w + 12, lane l the columns l, l + 64, ... in order, then a fixed
+      // shuffle tree
+      double q2[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const double* kr = ks + (w + 4 * u) * kEdKeyStride;
+        q2[u] = 0.0;
+#pragma unroll
+        for (int c = lane; c < kEdCols; c += 64)
+          if (c < ncol) q2[u] = fma(kr[c], kr[c], q2[u]);
+      }
+#pragma unroll
+      for (int sh = 32; sh >= 1; sh >>= 1)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q2[u] += __shfl_xor(q2[u], sh, kWave);
+      if (lane == 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = pt0 + w + 4 * u;
+          if (j < P) a.kn2p[zs * a.P_max + j] = q2[u];
+        }
+      }
+    }
+    // products: per group, E key values and the lane's chunk; four
+    // independent accumulators (MFMA m goes to m % 4), added in order
+    f64x4_t acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+    const double* kp = ks + l16 * kEdKeyStride + kk * E;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      double kv[E], qa[E];
+#pragma unroll
+      for (int m = 0; m < E; m += 2) {
+        const double2 k2 = *reinterpret_cast<const double2*>(kp + g * 4 * E + m);
+        kv[m] = k2.x;
+        kv[m + 1] = k2.y;
+      }
+      // a chunk past the slice holds 0 (its load read the first chunk); the
+      // conversion stays inside the passage loop (an empty asm redefines the
+      // chunk), so only one group's values are live at a time
+      const int col = g * 4 * E + kk * E;
+      u32x4 xg;
+      if constexpr (kStage) {
+        xg = x[g];
+      } else {
+        // (the base passes through an empty asm so that the compiler forms
+        // each address here instead of keeping all of them live)
+        const T* rp = rsrc;
+        int lim = ncol;
+        asm volatile("" : "+v"(rp), "+v"(lim));
+        xg = *reinterpret_cast<const u32x4*>(rp + (col < lim ? col : 0));
+      }
+      if (col >= ncol) xg = u32x4{0u, 0u, 0u, 0u};
+      asm volatile("" : "+v"(xg));
+      unpack16_f64<T>(xg, qa);
+#pragma unroll
+      for (int m = 0; m < E; ++m)
+        acc[m & 3] = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[m], kv[m], acc[m & 3], 0, 0, 0);
+      if (pt0 == 0) {
+#pragma unroll
+        for (int m = 0; m < E; ++m) qq = fma(qa[m], qa[m], qq);
+      }
+      // one group's key reads and conversions in flight at a time (keeps
+      // the register count at three waves per SIMD)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // D[i][j]: register v of lane l holds row 4v + l/16 of the tile, passage l % 16
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = tile0 + 4 * v + kk, j = pt0 + l16;
+      if (i < k && j < P)
+        a.part[(zs * a.k_max + i) * a.P_max + j] = ((acc[0][v] + acc[1][v]) + acc[2][v]) + acc[3][v];
+    }
+  }
+  // lanes l16, l16 + 16, l16 + 32, l16 + 48 hold the four column slots of row l16
+  qq += __shfl_xor(qq, 16, kWave);
+  qq += __shfl_xor(qq, 32, kWave);
+  if (kk == 0 && tile0 + l16 < k) a.qn2p[zs * a.k_max + tile0 + l16] = qq;
 }
 
 // ---------------------------------------------------------------------------
@@ -260,21 +277,71 @@ __device__ __forceinline__ long long edges_of_question(int k, int P, int rule,
   return (long long)fmin((double)n, fmax(0.0, want));
 }
 
+// Candidate keys, one thread per (row, passage) of a question: the slice
+// partials of the dot product (and of both squared norms) summed in slice
+// order, the cosine (or the scaled dot product) formed from them, and its
+// order-preserving key written over slice 0 of the partials; a passage the
+// verification gate dropped gets the lowest key.  Each candidate's partials
+// are read and its key written by one thread only.
+__global__ void __launch_bounds__(256)
+edge_keys_kernel(double* __restrict__ part, const double* __restrict__ qn2p,
+                 const double* __restrict__ kn2p, int S,
+                 const int32_t* __restrict__ kept_offsets,
+                 const int32_t* __restrict__ query_passages, int total_kept,
+                 int total_passages, int k_max, int P_max, int d, int metric,
+                 const uint8_t* __restrict__ keep) {
+  const int b = blockIdx.y;
+  int k0, k1, p0, p1;
+  range_of(kept_offsets, b, total_kept, k0, k1);
+  range_of(query_passages, b, total_passages, p0, p1);
+  const int k = min(k1 - k0, k_max);
+  const int P = min(min(p1 - p0, P_max), 64);
+  const int n = min(k * P, kGSelThreads * kGSelMaxPT);
+  const int f = blockIdx.x * blockDim.x + threadIdx.x;
+  if (f >= n) return;
+  const int i = f / P, j = f - i * P;
+  // sum of S values at base + s * stride, in slice order (slices clamped
+  // into range, so that every load of a batch is unconditional)
+  auto slice_sum = [&](const double* base, size_t stride) -> double {
+    double acc = 0.0;
+    for (int sl0 = 0; sl0 < S; sl0 += 16) {
+      double x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = base[(size_t)min(sl0 + u, S - 1) * stride];
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (sl0 + u < S) acc += x[u];
+    }
+    return acc;
+  };
+  double* cand = part + ((size_t)b * S * k_max + i) * P_max + j;
+  const double dot = slice_sum(cand, (size_t)k_max * P_max);
+  double c;
+  if (metric == SKIP_EDGE_DOT) {
+    c = dot * (1.0 / sqrt((double)d));
+  } else {
+    const double nq = sqrt(slice_sum(qn2p + (size_t)b * S * k_max + i, (size_t)k_max));
+    const double nk = sqrt(slice_sum(kn2p + (size_t)b * S * P_max + j, (size_t)P_max));
+    c = (nq > 0.0 && nk > 0.0) ? dot / (nq * nk) : 0.0;
+  }
+  const bool kept = keep ? keep[p0 + j] != 0 : true;
+  *reinterpret_cast<uint64_t*>(cand) = kept ? order_key(c) : 0ull;
+}
+
 __global__ void __launch_bounds__(kGSelThreads)
-edge_select_kernel(const double* __restrict__ part, const double* __restrict__ qn2p,
-                   const double* __restrict__ kn2p, int S,
+edge_select_kernel(const double* __restrict__ part, int S,
                    const int32_t* __restrict__ kept_offsets,
                    const int32_t* __restrict__ query_passages, int B, int total_kept,
-                   int total_passages, int k_max, int P_max, int d, double avg_degree,
-                   int rule, int metric, double beta, const uint8_t* __restrict__ keep,
+                   int total_passages, int k_max, int P_max, double avg_degree,
+                   int rule, double beta, const uint8_t* __restrict__ keep,
                    uint64_t* __restrict__ rowmask, int32_t* __restrict__ rowptr_out,
                    int32_t* __restrict__ col_out, PlanArgs plan) {
   __shared__ SelectShared sh;
   __shared__ uint32_t scan_sh[20];
   __shared__ uint8_t flag[kGSelThreads * kGSelMaxPT];
-  // row norms while the keys are formed, then the keys of the per-row cut
+  // the keys of the per-row cut (the work list builder's LDS in the extra
+  // workgroup)
   __shared__ __align__(16) uint64_t rkeys[kGSelThreads * kGSelMaxPT];
-  __shared__ double knorm[64];
   static_assert(sizeof(PlanLds) <= sizeof(rkeys), "the work list builder reuses the key LDS");
   if ((int)blockIdx.x == B) {
     // the extra workgroup: the attention's work list (it depends on the
@@ -285,7 +352,6 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
                          plan.items);
     return;
   }
-  double* qnorm = reinterpret_cast<double*>(rkeys);
   const int b = blockIdx.x;
   int k0, k1, p0, p1;
   range_of(kept_offsets, b, total_kept, k0, k1);
@@ -302,81 +368,22 @@ edge_select_kernel(const double* __restrict__ part, const double* __restrict__ q
   }
   const int Pk = __popcll(pkeep);
   const int E = (int)edges_of_question(k, Pk, rule, avg_degree, beta);
-  const double inv_sqrt_d = 1.0 / sqrt((double)d);
 
   const int C = (n + blockDim.x - 1) / blockDim.x;
   const int e0 = threadIdx.x * C;
   const int cnt = max(0, min(C, n - e0));
-  // Norms |q_i| and |k̄_j| first: square roots of the slice partials summed
-  // in slice order (slices clamped into range, so every load of a batch is
-  // unconditional), kept in LDS.
-  auto slice_sum = [&](const double* base, size_t stride) -> double {
-    double acc = 0.0;
-    for (int sl0 = 0; sl0 < S; sl0 += 16) {
-      double x[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) x[u] = base[(size_t)min(sl0 + u, S - 1) * stride];
-#pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (sl0 + u < S) acc += x[u];
-    }
-    return acc;
-  };
-  if (metric != SKIP_EDGE_DOT) {
-    const int kr = min(k, kGSelThreads * kGSelMaxPT);   // rows that have candidates
-    for (int t = threadIdx.x; t < kr + P; t += blockDim.x) {
-      if (t < kr) qnorm[t] = sqrt(slice_sum(qn2p + (size_t)b * S * k_max + t, (size_t)k_max));
-      else knorm[t - kr] = sqrt(slice_sum(kn2p + (size_t)b * S * P_max + (t - kr), (size_t)P_max));
-    }
-    __syncthreads();
-  }
-  // compatibility of (i, j) from the per-slice partial products, in slice
-  // order; two candidates at a time, sixteen slices of their loads in flight
+  // the candidates' keys, formed by the key launch over slice 0 of the
+  // partials
+  const uint64_t* ck = reinterpret_cast<const uint64_t*>(part) + (size_t)b * S * k_max * P_max;
   uint64_t keys[kGSelMaxPT];
 #pragma unroll
-  for (int jj = 0; jj < kGSelMaxPT; ++jj) keys[jj] = 0ull;
-#pragma unroll
-  for (int jj = 0; jj < kGSelMaxPT; jj += 2) {
+  for (int jj = 0; jj < kGSelMaxPT; ++jj) {
+    keys[jj] = 0ull;
     if (jj < cnt) {
-      int ii[2], pj[2];
-      double dot[2] = {0.0, 0.0};
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int f = min(e0 + jj + h, n - 1);
-        ii[h] = f / P;
-        pj[h] = f - ii[h] * P;
-      }
-      for (int sl0 = 0; sl0 < S; sl0 += 16) {
-        double pd[2][16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const size_t base = (size_t)b * S + min(sl0 + u, S - 1);
-#pragma unroll
-          for (int h = 0; h < 2; ++h) pd[h][u] = part[(base * k_max + ii[h]) * P_max + pj[h]];
-        }
-#pragma unroll
-        for (int u = 0; u < 16; ++u)
-          if (sl0 + u < S) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) dot[h] += pd[h][u];
-          }
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        if (jj + h < cnt) {
-          double c;
-          if (metric == SKIP_EDGE_DOT) {
-            c = dot[h] * inv_sqrt_d;
-          } else {
-            const double nq = qnorm[ii[h]], nk = knorm[pj[h]];
-            c = (nq > 0.0 && nk > 0.0) ? dot[h] / (nq * nk) : 0.0;
-          }
-          keys[jj + h] = ((pkeep >> pj[h]) & 1ull) ? order_key(c) : 0ull;
-        }
-      }
+      const int f = e0 + jj, ii = f / P;
+      keys[jj] = ck[(size_t)ii * P_max + (f - ii * P)];
     }
   }
-  __syncthreads();                 // the row norms are read before rkeys is written
   uint32_t flags;
   if (rule == SKIP_EDGE_ROW_TOP) {
     // every row keeps its D largest (lower passage first on ties)
@@ -509,10 +516,13 @@ hipError_t launch_edge_dot(const skip_problem_t& p, QuerySource q,
   a.P_max = p.P_max;
   a.B = p.B;
   a.S = edge_slices(p);
+  a.RB = (p.k_max + kEdRows - 1) / kEdRows;
   a.part = ep.part;
   a.qn2p = ep.qn2;
   a.kn2p = ep.kn2;
-  dim3 grid(8 * ((p.B + 7) / 8) * a.S);
+  const long long nwg = 8ll * ((p.B + 7) / 8) * a.S * a.RB;
+  if (nwg > INT32_MAX) return hipErrorInvalidValue;
+  dim3 grid((unsigned)nwg);
   if (p.dtype == SKIP_F32)
     hipLaunchKernelGGL(edge_dot_kernel<float>, grid, dim3(256), 0, s, (const float*)q.base, a);
   else
@@ -535,11 +545,21 @@ hipError_t launch_edge_select(const skip_problem_t& p, EdgePartials ep,
     pa.total_tokens = p.total_tokens;
     pa.n_ids = (int)n_ids;
   }
+  const int S = edge_slices(p);
+  if (p.total_kept > 0 && p.k_max > 0 && p.P_max > 0) {
+    // the candidates' keys from the partials of the dot-product launch
+    const int n = (int)std::min<long long>((long long)p.k_max * std::min(p.P_max, 64),
+                                           (long long)kGSelThreads * kGSelMaxPT);
+    hipLaunchKernelGGL(edge_keys_kernel, dim3((n + 255) / 256, p.B), dim3(256), 0, s, ep.part,
+                       ep.qn2, ep.kn2, S, kept_offsets, query_passages, p.total_kept,
+                       p.total_passages, p.k_max, p.P_max, p.d, p.edge_metric, passage_keep);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(edge_select_kernel, dim3(p.B + (n_ids > 0 ? 1 : 0)), dim3(kGSelThreads),
-                     0, s, ep.part, ep.qn2, ep.kn2, edge_slices(p), kept_offsets,
-                     query_passages, p.B, p.total_kept, p.total_passages, p.k_max, p.P_max, p.d,
-                     p.avg_degree, p.edge_rule, p.edge_metric, p.edge_beta, passage_keep,
-                     rowmask, rowptr_out, col_out, pa);
+                     0, s, ep.part, S, kept_offsets, query_passages, p.B, p.total_kept,
+                     p.total_passages, p.k_max, p.P_max, p.avg_degree, p.edge_rule,
+                     p.edge_beta, passage_keep, rowmask, rowptr_out, col_out, pa);
   return hipGetLastError();
 }
 

@@ -23,15 +23,28 @@
 
 namespace skip {
 
-// Histograms and pass results alternate between two copies, so that a pass
-// takes two barriers: the next pass's histogram is cleared while this one is
-// filled (its last reader, the previous pass's scan, is past a barrier), and
-// a pass's result is not overwritten until two passes later.
+// Histograms rotate over three copies, so that a pass takes one barrier:
+// every wave scans the pass's histogram itself (no result broadcast), and
+// the copy the next pass fills is cleared during this pass's counting, when
+// its last readers (the scans two passes back) are past a barrier.
 struct SelectShared {
-  uint32_t hist[2][256];
-  uint32_t misc[2][4];
+  alignas(16) uint32_t hist[3][256];
   uint32_t scan[20];
 };
+
+// Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of
+// 16 lanes, then the last lane of rows 0 and 2 added to rows 1 and 3, then
+// that of row 1 to rows 2 and 3 (DPP row_shr and row_bcast; a lane with no
+// source reads 0).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
 
 // Per-thread element masks: 32 bits, or 64 for more elements a thread.
 template <int MAXPT>
@@ -39,7 +52,7 @@ using SelectMask = typename std::conditional<(MAXPT > 32), uint64_t, uint32_t>::
 
 // Returns a bitmask over the thread's elements (bit j = element t*C + j).
 template <int MAXPT>
-__device__ SelectMask<MAXPT> block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int n,
+__device__ __forceinline__ SelectMask<MAXPT> block_select_top(const uint64_t (&keys)[MAXPT], int cnt, int n,
                                               int kk, SelectShared* sh) {
   static_assert(MAXPT <= 64, "flags are at most a 64-bit mask");
   using M = SelectMask<MAXPT>;
@@ -48,6 +61,8 @@ __device__ SelectMask<MAXPT> block_select_top(const uint64_t (&keys)[MAXPT], int
   const M all = (cnt >= W) ? ~(M)0 : ((one << cnt) - one);
   if (kk <= 0) return 0;
   if (kk >= n) return all;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int C = (n + (int)blockDim.x - 1) / (int)blockDim.x;   // element slots a thread
 
   for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[0][i] = 0u;
   __syncthreads();
@@ -56,47 +71,55 @@ __device__ SelectMask<MAXPT> block_select_top(const uint64_t (&keys)[MAXPT], int
   bool whole_bucket = false;
   for (int pass = 0; pass < 8; ++pass) {
     const int shift = 56 - 8 * pass;
-    uint32_t* hist = sh->hist[pass & 1];
-    uint32_t* misc = sh->misc[pass & 1];
+    uint32_t* hist = sh->hist[pass % 3];
+    // Count the digits of the keys that share the prefix (element slots up
+    // to C = ceil(n / blockDim.x), the same for every thread).  In the first
+    // pass, where most keys share the leading digits, the lanes of a wave
+    // with the digit of the first remaining lane are counted by one atomic
+    // (two rounds); every other count is one atomic.
 #pragma unroll
     for (int j = 0; j < MAXPT; ++j) {
-      if (j < cnt && (keys[j] & mask) == prefix)
-        atomicAdd(&hist[(uint32_t)(keys[j] >> shift) & 255u], 1u);
-    }
-    for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[(pass + 1) & 1][i] = 0u;
-    __syncthreads();
-    if (threadIdx.x < kWave) {
-      const int l = threadIdx.x;
-      const uint32_t h0 = hist[255 - 4 * l], h1 = hist[254 - 4 * l];
-      const uint32_t h2 = hist[253 - 4 * l], h3 = hist[252 - 4 * l];
-      const uint32_t s = h0 + h1 + h2 + h3;
-      uint32_t inc = s;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        uint32_t y = __shfl_up(inc, o, kWave);
-        if (l >= o) inc += y;
-      }
-      const uint32_t exc = inc - s;
-      if (exc < need && need <= inc) {       // exactly one lane
-        uint32_t c = exc;
-        uint32_t bin, inbin;
-        if (c + h0 >= need) {
-          bin = 255 - 4 * l; inbin = h0;
-        } else if (c + h0 + h1 >= need) {
-          c += h0; bin = 254 - 4 * l; inbin = h1;
-        } else if (c + h0 + h1 + h2 >= need) {
-          c += h0 + h1; bin = 253 - 4 * l; inbin = h2;
-        } else {
-          c += h0 + h1 + h2; bin = 252 - 4 * l; inbin = h3;
+      const bool act = j < cnt && (keys[j] & mask) == prefix;
+      const uint32_t dg = (uint32_t)(keys[j] >> shift) & 255u;
+      if (j >= C) {
+      } else if (pass == 0) {
+        uint64_t rem = __ballot(act);
+        for (int r = 0; r < 2 && rem; ++r) {
+          const int l0 = __builtin_ctzll(rem);
+          const uint32_t d0 = __builtin_amdgcn_readlane(dg, l0);
+          const uint64_t same = __ballot(act && dg == d0) & rem;
+          if (lane == l0) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+          rem &= ~same;
         }
-        misc[0] = bin;
-        misc[1] = c;        // candidates with a larger digit: all taken
-        misc[2] = inbin;    // candidates with exactly this digit
+        if ((rem >> lane) & 1ull) atomicAdd(&hist[dg], 1u);
+      } else if (act) {
+        atomicAdd(&hist[dg], 1u);
       }
     }
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) sh->hist[(pass + 1) % 3][i] = 0u;
     __syncthreads();
-    const uint32_t bin = misc[0], above = misc[1], inbin = misc[2];
-    need -= above;
+    // Every wave: lane l holds digits 255 - 4l .. 252 - 4l; the first lane
+    // whose running count from the top reaches `need` holds the digit.
+    const uint4 hv = *reinterpret_cast<const uint4*>(&hist[252 - 4 * lane]);
+    const uint32_t h0 = hv.w, h1 = hv.z, h2 = hv.y, h3 = hv.x;   // digits 255-4l, ..
+    const uint32_t s = h0 + h1 + h2 + h3;
+    const uint32_t inc = wave_incl_scan(s);
+    const uint64_t hit = __ballot(inc >= need);
+    const int L = hit ? __builtin_ctzll(hit) : kWave - 1;   // (need <= the prefix's count)
+    uint32_t c = __builtin_amdgcn_readlane(inc - s, L);
+    const uint32_t g0 = __builtin_amdgcn_readlane(h0, L), g1 = __builtin_amdgcn_readlane(h1, L);
+    const uint32_t g2 = __builtin_amdgcn_readlane(h2, L), g3 = __builtin_amdgcn_readlane(h3, L);
+    uint32_t bin, inbin;
+    if (c + g0 >= need) {
+      bin = 255 - 4 * L; inbin = g0;
+    } else if (c + g0 + g1 >= need) {
+      c += g0; bin = 254 - 4 * L; inbin = g1;
+    } else if (c + g0 + g1 + g2 >= need) {
+      c += g0 + g1; bin = 253 - 4 * L; inbin = g2;
+    } else {
+      c += g0 + g1 + g2; bin = 252 - 4 * L; inbin = g3;
+    }
+    need -= c;            // candidates with a larger digit: all taken
     prefix |= (uint64_t)bin << shift;
     mask |= 0xffull << shift;
     if (inbin == need) { whole_bucket = true; break; }
