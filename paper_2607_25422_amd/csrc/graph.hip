@@ -410,7 +410,7 @@ edge_select_kernel(const double* __restrict__ part, int S,
     for (int jj = 0; jj < kGSelMaxPT; ++jj)
       if (jj < cnt && flag[e0 + jj]) flags |= 1u << jj;
   } else {
-    flags = block_select_top<kGSelMaxPT>(keys, cnt, n, E, &sh);
+    flags = block_select_top_wide<kGSelMaxPT>(keys, cnt, n, E, &sh);
 #pragma unroll
     for (int j = 0; j < kGSelMaxPT; ++j)
       if (j < cnt) flag[e0 + j] = (flags >> j) & 1u;

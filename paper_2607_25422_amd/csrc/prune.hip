@@ -134,7 +134,7 @@ __device__ __forceinline__ void topk_block(const double* __restrict__ z, int b, 
 // top-k runs beside the scoring of later questions and the key pooling
 // instead of as a launch of its own.
 template <typename T, int MAXPT>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, 3)   // three waves per SIMD for the scoring stream
 prune_kernel(const T* __restrict__ V, const double* __restrict__ u, int N, int d, int B,
              int RB, double* __restrict__ z, float* __restrict__ scores,
              const int32_t* __restrict__ kept_offsets, int total_kept,
@@ -179,7 +179,7 @@ topk_kernel(const double* __restrict__ z, const int32_t* __restrict__ kept_offse
 #pragma unroll
   for (int j = 0; j < kSelMaxPT; ++j)
     keys[j] = (j < cnt) ? order_key(z[(size_t)b * N + e0 + j]) : 0ull;
-  const uint32_t flags = block_select_top<kSelMaxPT>(keys, cnt, N, kk, &sh);
+  const uint32_t flags = block_select_top_wide<kSelMaxPT>(keys, cnt, N, kk, &sh);
   uint32_t total;
   uint32_t pos = block_exclusive_scan(__popc(flags), scan_sh, &total);
 #pragma unroll
