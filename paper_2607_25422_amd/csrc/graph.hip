@@ -40,9 +40,10 @@ namespace skip {
 //     chunks loaded into registers before the keys are staged; f32, twice
 //     the chunks: each where it is used).
 //   * The passage keys of the slice sit in LDS as float64, 16 passages at a
-//     time, read by all four waves.  With only the keys in LDS (33 KiB) four
-//     bf16 workgroups share a CU, so one wave's loads and conversions overlap
-//     another's matrix products.
+//     time, read by all four waves (float64 keys by direct global->LDS loads
+//     issued before the rows).  With only the keys in LDS (33 KiB), three
+//     bf16 workgroups share a CU (registers allow three waves per SIMD), so
+//     one wave's loads and conversions overlap another's matrix products.
 // Each lane also sums the squares of its row values (partial row norms); the
 // key norms come from the keys in LDS (row block 0).  Results per slice are
 // summed in slice order by the key launch.
