@@ -507,8 +507,10 @@ skip_status_t skip_route_fused_noalloc(const skip_problem_t* p, const void* V,
 
 /* Kernel stages of skip_route_fused, in launch order: question pooling;
  * salience scoring with the top-k (and the passage-key pooling unless the
- * keys are given) in one launch; edge compatibilities; edge selection (with
- * the attention's work list built beside it); attention. */
+ * keys are given) in one launch; edge compatibilities (partial dot products
+ * over slices of d); edge selection (the candidates' keys from the slice
+ * sums, then the selection with the attention's work list built beside it);
+ * attention. */
 #define SKIP_FUSED_STAGES 5
 
 /*
@@ -517,9 +519,11 @@ skip_status_t skip_route_fused_noalloc(const skip_problem_t* p, const void* V,
  * created by the caller (host array of handles); event s is recorded on
  * `stream` just before stage s is enqueued and the last one after the final
  * stage, so hipEventElapsedTime(events[s], events[s+1]) is the duration of
- * stage s.  The stages, in order: pooling (the questions and, unless the
- * caller gives passage keys, the passages), scoring, top-k, edge cosines,
- * edge selection, attention.  Other arguments and results as in
+ * stage s.  The stages, in order, as listed for SKIP_FUSED_STAGES:
+ * question pooling; scoring with the top-k and (unless the caller gives
+ * passage keys) the passage-key pooling; edge compatibilities (in the gated
+ * route preceded by the gate); edge selection; attention.  Other arguments
+ * and results as in
  * skip_route_fused; SKIP_ERR_INVALID_ARG if stage_events is NULL or
  * n_events is wrong.
  */
