@@ -301,6 +301,40 @@ def test_xattn_edge_rules_and_metrics(B, rule, metric, beta, dtype):
     check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), dtype)
 
 
+@pytest.mark.parametrize("rule,metric", [("question", "cosine"), ("fraction", "dot")])
+def test_xattn_edge_tie_groups_at_the_cut(B, rule, metric):
+    """All kept rows of a question but its last three are copies of its first
+    row, so each passage's candidates form a group of equal compatibilities
+    (bit-equal on both sides: equal rows take the same arithmetic) and the
+    per-question cut falls inside one of them: the selection must take the
+    group's lowest flat indices i * P + j, as the oracle does."""
+    batch = small_batch("bf16", 7, H=2, d_h=128)
+    Qh = queries_from_batch(batch).clone()
+    for b in range(batch.B):
+        k0, k1 = int(batch.kept_offsets[b]), int(batch.kept_offsets[b + 1])
+        if k1 - k0 > 4:
+            Qh[k0:k1 - 3] = Qh[k0].clone()
+    say(f"xattn edge ties {rule}/{metric} P={batch.P.tolist()} k={batch.k.tolist()}")
+    db = B.to_device(batch, avg_degree=2.5, edge_rule=rule, edge_metric=metric, edge_beta=0.3)
+    O, L, rp, col = B.bipartite_xattn(db, Qh.cuda())
+    torch.cuda.synchronize()
+    _, adj, O_ref, L_ref = orc.bipartite_xattn(
+        Qh, batch.kept_offsets, batch.Kh, batch.Vh, batch.passage_offsets,
+        batch.query_passages, batch.wl.scale, 2.5, edge_rule=rule, edge_metric=metric,
+        edge_beta=0.3)
+    # the cut splits a tie group: some row of a group is kept and a later one
+    # of the same group is not
+    split = False
+    for a in adj:
+        if a.shape[0] > 4:
+            for j in range(a.shape[1]):
+                col_j = a[:-3, j]
+                split |= bool(col_j.any() and not col_j.all())
+    assert split, "no tie group straddles the cut; the test input needs changing"
+    check_graph(batch, rp, col, adj)
+    check_attention(f64(O), f64(L), np.concatenate(O_ref), np.concatenate(L_ref), "bf16")
+
+
 @pytest.mark.parametrize("dtype,H,d_h,P", [("bf16", 5, 64, (2, 9)), ("f32", 3, 128, (4, 7)),
                                           ("bf16", 2, 128, (17, 20)), ("f32", 4, 64, (18,))])
 def test_graph_ragged_slices_and_passage_groups(B, dtype, H, d_h, P):
