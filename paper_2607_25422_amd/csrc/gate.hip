@@ -9,13 +9,20 @@
 //   gate_mean_kernel  : q_bar (question tokens) and v_bar (kept rows, given as
 //                       rows or through kept_idx) in float64, 8 waves a
 //                       workgroup with four rows a wave in flight
-//   gate_x_kernel     : the bf16 gate input x_j of every passage, [T][5d]
-//   gate_score_kernel : W x_j on v_mfma_f32_32x32x16_bf16, tiles of 32
-//                       passages x 64 hidden units, the 5d columns split into
-//                       S chunks (split-K, so the launch fills the chip at a
-//                       few hundred passages); one float32 partial per chunk
-//   gate_fin_kernel   : one workgroup a passage: the chunk partials summed in
-//                       chunk order, + b1, relu, . w2, + b2 -> logit_j; the
+//   gate_x_kernel     : the bf16 gate inputs: the passage blocks
+//                       [e ; e*q_bar ; |e - q_bar|] of every passage, [T][3d],
+//                       and the question blocks [q_bar ; v_bar] of every
+//                       question, [B][2d]
+//   gate_score_kernel : W x on v_mfma_f32_32x32x16_bf16, split as
+//                       W[:, 2d:5d] . (passage blocks) per passage plus
+//                       W[:, 0:2d] . (question blocks) once per question (the
+//                       same for all its passages); tiles of 32 rows x 64
+//                       hidden units, the columns split into chunks (split-K,
+//                       so the launch fills the chip at a few hundred
+//                       passages); one float32 partial per chunk
+//   gate_fin_kernel   : one workgroup a passage: its chunk partials in chunk
+//                       order, then its question's in chunk order, + b1,
+//                       relu, . w2, + b2 -> logit_j; the
 //                       last workgroup of a question to finish (a counter in
 //                       the workspace) takes the question's cut
 #include <cmath>
@@ -43,7 +50,8 @@ __device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, 
 constexpr int kGateMT = 32;        // passages per score tile
 constexpr int kGateNT = 64;        // hidden units per score tile
 constexpr int kGateMeanWaves = 8;  // waves per mean workgroup (512 columns)
-constexpr int kGateTargetWG = 640; // score workgroups aimed for when choosing S
+constexpr int kGateTargetWG = 640; // passage-tile workgroups aimed for when choosing S
+constexpr int kGateInFlight = 3;   // 64-column groups whose loads a wave issues together
 
 // Workgroup (512-column slice, y): y < B is q_bar_y over the question tokens,
 // y >= B is v_bar_{y-B} over the kept rows (rows[kept_offsets range], or
@@ -128,24 +136,41 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
   }
 }
 
-// Block j (passage): X[j] = [q' ; v' ; e' ; (e' q')' ; |e' - q'|'] (x' the
-// bf16 rounding), pq[j] = its question; the first passage of a question also
-// clears that question's finish counter.  Thread t fills 8-column groups t,
-// t+256, ... of every block of X.
+// Block j < T (passage j of question b): X[j] = [e' ; (e' q')' ; |e' - q'|']
+// (x' the bf16 rounding), pq[j] = b.  Block T + b (question b): Xq[b] =
+// [q' ; v'], and the question's finish counter cleared.  Thread t fills
+// 8-column groups t, t+256, ... of every block of its row.
 __global__ void __launch_bounds__(256)
 gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
               const double* __restrict__ kbar, const float* __restrict__ pkeys,
               const int32_t* __restrict__ query_passages, int B, int T, int d,
-              bf16_t* __restrict__ X, int32_t* __restrict__ pq, int32_t* __restrict__ done) {
+              bf16_t* __restrict__ X, bf16_t* __restrict__ Xq, int32_t* __restrict__ pq,
+              int32_t* __restrict__ done) {
   const int j = blockIdx.x;
-  const int b = question_of(query_passages, B, T, j);
-  if (threadIdx.x == 0) {
-    pq[j] = b;
-    if (clampi(query_passages[b], 0, T) == j) done[b] = 0;
+  if (j >= T) {
+    const int b = j - T;
+    if (threadIdx.x == 0) done[b] = 0;
+    bf16_t* xr = Xq + (size_t)b * 2 * d;
+    for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+      const double2* qp2 = reinterpret_cast<const double2*>(qbar + (size_t)b * d + c);
+      const double2* vp2 = reinterpret_cast<const double2*>(vbar + (size_t)b * d + c);
+      u32x4 oq, ov;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const double2 x = qp2[t], y = vp2[t];
+        oq[t] = pack2_bf16((float)x.x, (float)x.y);
+        ov[t] = pack2_bf16((float)y.x, (float)y.y);
+      }
+      *reinterpret_cast<u32x4*>(xr + c) = oq;
+      *reinterpret_cast<u32x4*>(xr + d + c) = ov;
+    }
+    return;
   }
-  bf16_t* xr = X + (size_t)j * 5 * d;
+  const int b = question_of(query_passages, B, T, j);
+  if (threadIdx.x == 0) pq[j] = b;
+  bf16_t* xr = X + (size_t)j * 3 * d;
   for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
-    float e[8], q[8], v[8];
+    float e[8], q[8];
     if (pkeys) {
       const float4 a = *reinterpret_cast<const float4*>(pkeys + (size_t)j * d + c);
       const float4 a2 = *reinterpret_cast<const float4*>(pkeys + (size_t)j * d + c + 4);
@@ -161,78 +186,81 @@ gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
       }
     }
     const double2* qp2 = reinterpret_cast<const double2*>(qbar + (size_t)b * d + c);
-    const double2* vp2 = reinterpret_cast<const double2*>(vbar + (size_t)b * d + c);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const double2 x = qp2[t], y = vp2[t];
+      const double2 x = qp2[t];
       q[2 * t] = (float)x.x;
       q[2 * t + 1] = (float)x.y;
-      v[2 * t] = (float)y.x;
-      v[2 * t + 1] = (float)y.y;
     }
-    u32x4 oq, ov, oe, oh, od;
+    u32x4 oe, oh, od;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const float e0 = bf16_to_f32(f32_to_bf16(e[2 * t]));
       const float e1 = bf16_to_f32(f32_to_bf16(e[2 * t + 1]));
       const float q0 = bf16_to_f32(f32_to_bf16(q[2 * t]));
       const float q1 = bf16_to_f32(f32_to_bf16(q[2 * t + 1]));
-      oq[t] = pack2_bf16(q0, q1);
-      ov[t] = pack2_bf16(v[2 * t], v[2 * t + 1]);
       oe[t] = pack2_bf16(e0, e1);
       oh[t] = pack2_bf16(e0 * q0, e1 * q1);              // exact product, one rounding
       od[t] = pack2_bf16(fabsf(e0 - q0), fabsf(e1 - q1)); // float32 difference, one rounding
     }
-    *reinterpret_cast<u32x4*>(xr + c) = oq;
-    *reinterpret_cast<u32x4*>(xr + d + c) = ov;
-    *reinterpret_cast<u32x4*>(xr + 2 * d + c) = oe;
-    *reinterpret_cast<u32x4*>(xr + 3 * d + c) = oh;
-    *reinterpret_cast<u32x4*>(xr + 4 * d + c) = od;
+    *reinterpret_cast<u32x4*>(xr + c) = oe;
+    *reinterpret_cast<u32x4*>(xr + d + c) = oh;
+    *reinterpret_cast<u32x4*>(xr + 2 * d + c) = od;
   }
 }
 
-// Tile (32 passages from 32*blockIdx.x, 64 hidden units from 64*blockIdx.y),
-// chunk z of the 5d columns, in groups of 64 columns: groups [z*ch, min((z+1)*
-// ch, ceil(5d/64))), wave w taking the groups w, w+4, ...  In a group the lane
-// pair (passage or unit l%32, half hh) reads the row's 128 contiguous bytes,
-// 64 a lane as four 16-byte pieces, and piece u feeds MFMA step u: step u sums
-// the columns 8u..8u+7 and 32+8u..32+8u+7 of the group (A and B take the same
-// columns, so the product over the group is complete).  Two groups (eight
-// steps) are in flight per wave.  A half group at the end of the columns
-// (5d/32 odd) reads zeros for its second half.  The four waves' sums are added
-// in wave order and written as part[z][passage][unit].
+// Row tiles: 32 passages (tiles 0 .. n_pt-1: the rows of X, K = 3d columns,
+// against W's columns 2d .. 5d) or 32 questions (tiles n_pt ..: the rows of
+// Xq, K = 2d, against W's columns 0 .. 2d).  Tile (rows, 64 hidden units),
+// chunk z of its K columns, in groups of 64 columns: groups [z*ch, min((z+1)*
+// ch, ceil(K/64))), wave w taking the groups w, w+4, ...; a question tile
+// whose K ends before chunk z exits at once.  In a group the lane pair (row
+// or unit l%32, half hh) reads the row's 128 contiguous bytes, 64 a lane as
+// four 16-byte pieces, and piece u feeds MFMA step u: step u sums the columns
+// 8u..8u+7 and 32+8u..32+8u+7 of the group (A and B take the same columns,
+// so the product over the group is complete).  Three groups (twelve steps)
+// are in flight per wave, spare slots of the last round reading zeros.  A
+// half group at the end of the columns (K/32 odd)
+// reads zeros for its second half.  The four waves' sums are added in wave
+// order and written as part[z][passage][unit] or partq[z][question][unit].
 //
 // Tiles go to XCDs by chunk: the hardware deals workgroup ids round-robin over
-// the 8 XCDs, and id L takes chunk z = 8 * zl + L % 8 with (zl, ht, pt) the
-// (L / 8)-th entry of that XCD's list, pt fastest.  Every tile of a chunk then
-// runs on one XCD, whose L2 holds the chunk's columns of X and W (about 1.7 MB
-// at 160 passages x 512 units x 4096), so each is read from memory once.
-// Ids whose chunk is past the last one exit at once.
+// the 8 XCDs, and id L takes chunk z = 8 * zl + L % 8 with (zl, ht, rt) the
+// (L / 8)-th entry of that XCD's list, rt fastest.  Every tile of a chunk then
+// runs on one XCD, whose L2 holds the chunk's columns of X and W, so each is
+// read from memory once.  Ids whose chunk is past the last one exit at once.
 __global__ void __launch_bounds__(256)
-gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int T, int d,
-                  int h, int ch, int S, float* __restrict__ part) {
+gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Xq,
+                  const bf16_t* __restrict__ W, int T, int B, int d, int h, int ch, int S,
+                  float* __restrict__ part, float* __restrict__ partq) {
   __shared__ float red[4][kGateMT][kGateNT + 1];
   const int n_pt = (T + kGateMT - 1) / kGateMT, n_ht = h / kGateNT;
+  const int n_rt = n_pt + (B + kGateMT - 1) / kGateMT;
   const int L = blockIdx.x, xcd = L & 7, jl = L >> 3;
-  const int pt = jl % n_pt, ht = (jl / n_pt) % n_ht, zl = jl / (n_pt * n_ht);
+  const int rt = jl % n_rt, ht = (jl / n_rt) % n_ht, zl = jl / (n_rt * n_ht);
   const int z = zl * 8 + xcd;
   if (z >= S) return;
+  const bool qtile = rt >= n_pt;
+  const int K = qtile ? 2 * d : 3 * d;
+  const int ngroups = (K + 63) / 64;
+  if (z * ch >= ngroups) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int hh = lane >> 5, r32 = lane & 31;
-  const int K = 5 * d;
-  const int ngroups = (K + 63) / 64;
   const int g1 = min((z + 1) * ch, ngroups);
-  const int prow = min(pt * kGateMT + r32, T - 1);
-  const bf16_t* xa = X + (size_t)prow * K + 32 * hh;
-  const bf16_t* wb0 = W + (size_t)(ht * kGateNT + r32) * K + 32 * hh;
-  const bf16_t* wb1 = wb0 + (size_t)32 * K;
+  const int nrows = qtile ? B : T;
+  const int r0 = (qtile ? rt - n_pt : rt) * kGateMT;
+  const int prow = min(r0 + r32, nrows - 1);
+  const bf16_t* xa = (qtile ? Xq : X) + (size_t)prow * K + 32 * hh;
+  const bf16_t* wb0 = W + (size_t)(ht * kGateNT + r32) * (5 * d) + (qtile ? 0 : 2 * d) + 32 * hh;
+  const bf16_t* wb1 = wb0 + (size_t)32 * 5 * d;
   f32x16_t acc[2];
 #pragma unroll
   for (int v = 0; v < 16; ++v) { acc[0][v] = 0.f; acc[1][v] = 0.f; }
   const u32x4 zero = {0u, 0u, 0u, 0u};
-  auto load_group = [&](int g, u32x4* a, u32x4* b0, u32x4* b1) {
-    const int c = 64 * g;
-    const bool ok = c + 32 * hh < K;        // K is a multiple of 32
+  // group gg of the wave's rounds; past g1 (the last round's spare slots) zeros
+  auto load_group = [&](int gg, u32x4* a, u32x4* b0, u32x4* b1) {
+    const int c = 64 * gg;
+    const bool ok = gg < g1 && c + 32 * hh < K;   // K is a multiple of 32
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       a[u] = ok ? *reinterpret_cast<const u32x4*>(xa + c + 8 * u) : zero;
@@ -240,22 +268,13 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, in
       b1[u] = ok ? *reinterpret_cast<const u32x4*>(wb1 + c + 8 * u) : zero;
     }
   };
-  int g = z * ch + wave;
-  for (; g + 4 < g1; g += 8) {
-    u32x4 a[8], b0[8], b1[8];
-    load_group(g, a, b0, b1);
-    load_group(g + 4, a + 4, b0 + 4, b1 + 4);
+  for (int g = z * ch + wave; g < g1; g += 4 * kGateInFlight) {
+    u32x4 a[4 * kGateInFlight], b0[4 * kGateInFlight], b1[4 * kGateInFlight];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      acc[0] = mfma32_bf16(a[u], b0[u], acc[0]);
-      acc[1] = mfma32_bf16(a[u], b1[u], acc[1]);
-    }
-  }
-  if (g < g1) {
-    u32x4 a[4], b0[4], b1[4];
-    load_group(g, a, b0, b1);
+    for (int e = 0; e < kGateInFlight; ++e)
+      load_group(g + 4 * e, a + 4 * e, b0 + 4 * e, b1 + 4 * e);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 4 * kGateInFlight; ++u) {
       acc[0] = mfma32_bf16(a[u], b0[u], acc[0]);
       acc[1] = mfma32_bf16(a[u], b1[u], acc[1]);
     }
@@ -268,31 +287,33 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, in
     for (int v = 0; v < 16; ++v)
       red[wave][8 * (v >> 2) + 4 * hh + (v & 3)][nb * 32 + r32] = acc[nb][v];
   __syncthreads();
-  // thread t: passage t / 8, hidden units 8 * (t % 8) .. + 7
+  // thread t: row t / 8, hidden units 8 * (t % 8) .. + 7
   const int m = threadIdx.x >> 3, n0 = (threadIdx.x & 7) * 8;
-  const int p = pt * kGateMT + m;
-  if (p >= T) return;
+  const int p = r0 + m;
+  if (p >= nrows) return;
   float o[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int n = n0 + e;
     o[e] = ((red[0][m][n] + red[1][m][n]) + red[2][m][n]) + red[3][m][n];
   }
-  float4* dst = reinterpret_cast<float4*>(part + ((size_t)z * T + p) * h + ht * kGateNT + n0);
+  float4* dst = reinterpret_cast<float4*>((qtile ? partq : part) + ((size_t)z * nrows + p) * h +
+                                          ht * kGateNT + n0);
   dst[0] = make_float4(o[0], o[1], o[2], o[3]);
   dst[1] = make_float4(o[4], o[5], o[6], o[7]);
 }
 
-// Block p (passage, 256 threads): pre-activation of unit j = the S chunk
-// partials in chunk order + b1[j]; thread t sums relu(.) * w2[j] over its
+// Block p (passage of question b, 256 threads): pre-activation of unit j =
+// the S chunk partials of p in chunk order, then the Sq chunk partials of b
+// in chunk order, + b1[j]; thread t sums relu(.) * w2[j] over its
 // units j = t, t+256, ... in order; the four waves' sums (wave shuffles, then
 // wave order) plus b2, rounded to float32, are logit_p.  The block then bumps
 // its question's counter; the block that completes it (P_b blocks in all)
 // takes the cut: kept = logit >= t and among the cap largest verified logits
 // (ties: lower index), on the float32 logits.
 __global__ void __launch_bounds__(256)
-gate_fin_kernel(const float* __restrict__ part, int S, int T, int h,
-                const float* __restrict__ b1, const float* __restrict__ w2, double b2,
+gate_fin_kernel(const float* __restrict__ part, int S, const float* __restrict__ partq, int Sq,
+                int T, int B, int h, const float* __restrict__ b1, const float* __restrict__ w2, double b2,
                 const int32_t* __restrict__ pq, const int32_t* __restrict__ query_passages,
                 double t, double rho, float* __restrict__ zbuf, int32_t* __restrict__ done,
                 float* __restrict__ logits, uint8_t* __restrict__ keep) {
@@ -300,27 +321,30 @@ gate_fin_kernel(const float* __restrict__ part, int S, int T, int h,
   __shared__ int last;
   const int p = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float s = 0.f;
-  const size_t zs = (size_t)T * h;
-  for (int j = threadIdx.x; j < h; j += blockDim.x) {
-    const float* src = part + (size_t)p * h + j;
-    float a = 0.f;
-    int zc = 0;
-    for (; zc + 8 <= S; zc += 8) {
-      float v[8];
+  const int b = pq[p];
+  // a + src[0] + src[zs] + ... + src[(n-1) zs], in that order (loads issued
+  // 16 at a time)
+  auto chunk_sum = [](float a, const float* src, int n, size_t zs) {
+    for (int zc = 0; zc < n; zc += 16) {
+      float v[16];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = src[(size_t)(zc + e) * zs];
+      for (int e = 0; e < 16; ++e) v[e] = zc + e < n ? src[(size_t)(zc + e) * zs] : 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) a += v[e];
+      for (int e = 0; e < 16; ++e)
+        if (zc + e < n) a += v[e];
     }
-    for (; zc < S; ++zc) a += src[(size_t)zc * zs];
+    return a;
+  };
+  float s = 0.f;
+  for (int j = threadIdx.x; j < h; j += blockDim.x) {
+    float a = chunk_sum(0.f, part + (size_t)p * h + j, S, (size_t)T * h);
+    a = chunk_sum(a, partq + (size_t)b * h + j, Sq, (size_t)B * h);
     a += b1 ? b1[j] : 0.f;
     s = fmaf(fmaxf(a, 0.f), w2[j], s);
   }
   s = wave_sum_f32(s);
   if (lane == 0) wsum[wave] = s;
   __syncthreads();
-  const int b = pq[p];
   int p0, p1;
   range_of(query_passages, b, T, p0, p1);
   const int P = min(p1 - p0, 64);
@@ -349,25 +373,29 @@ gate_fin_kernel(const float* __restrict__ part, int S, int T, int h,
 
 static size_t galign(size_t n) { return (n + 255) & ~(size_t)255; }
 
-// chunk length (64-column groups) and count S of the split over the 5d columns
-static void gate_split(int T, int h, int d, int* ch, int* S) {
+// chunk length ch (64-column groups), chunk count S of the passage blocks'
+// 3d columns and Sq of the question blocks' 2d columns (Sq <= S)
+static void gate_split(int T, int h, int d, int* ch, int* S, int* Sq) {
   const int tiles = ((T + kGateMT - 1) / kGateMT) * (h / kGateNT);
-  const int groups = (5 * d + 63) / 64;
+  const int groups = (3 * d + 63) / 64;
   int s = (kGateTargetWG + tiles - 1) / tiles;
   const int smax = groups / 4 > 0 ? groups / 4 : 1;   // at least one group a wave
   s = s < 1 ? 1 : (s > smax ? smax : s);
   const int c = (groups + s - 1) / s;
   *ch = c;
   *S = (groups + c - 1) / c;
+  *Sq = ((2 * d + 63) / 64 + c - 1) / c;
 }
 
 size_t gate_scratch_bytes(const skip_problem_t& p, int hidden) {
   const size_t T = (size_t)p.total_passages;
-  int ch = 1, S = 1;
-  if (T > 0) gate_split((int)T, hidden, p.d, &ch, &S);
+  int ch = 1, S = 1, Sq = 1;
+  if (T > 0) gate_split((int)T, hidden, p.d, &ch, &S, &Sq);
   return 2 * galign((size_t)p.B * p.d * sizeof(double)) +          // qbar, vbar
-         galign(T * 5 * p.d * sizeof(bf16_t)) +                     // X
-         galign((size_t)S * T * hidden * sizeof(float)) +           // chunk partials
+         galign(T * 3 * p.d * sizeof(bf16_t)) +                     // X
+         galign((size_t)p.B * 2 * p.d * sizeof(bf16_t)) +           // Xq
+         galign((size_t)S * T * hidden * sizeof(float)) +           // passage chunk partials
+         galign((size_t)Sq * p.B * hidden * sizeof(float)) +        // question chunk partials
          galign(T * sizeof(float)) +                                // logits
          galign(T * sizeof(int32_t)) +                              // question of each passage
          galign((size_t)p.B * sizeof(int32_t));                     // finish counters
@@ -375,8 +403,8 @@ size_t gate_scratch_bytes(const skip_problem_t& p, int hidden) {
 
 GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base) {
   const size_t T = (size_t)p.total_passages;
-  int ch = 1, S = 1;
-  if (T > 0) gate_split((int)T, hidden, p.d, &ch, &S);
+  int ch = 1, S = 1, Sq = 1;
+  if (T > 0) gate_split((int)T, hidden, p.d, &ch, &S, &Sq);
   char* c = static_cast<char*>(base);
   GateScratch g;
   g.qbar = reinterpret_cast<double*>(c);
@@ -384,9 +412,13 @@ GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base) 
   g.vbar = reinterpret_cast<double*>(c);
   c += galign((size_t)p.B * p.d * sizeof(double));
   g.X = reinterpret_cast<bf16_t*>(c);
-  c += galign(T * 5 * p.d * sizeof(bf16_t));
+  c += galign(T * 3 * p.d * sizeof(bf16_t));
+  g.Xq = reinterpret_cast<bf16_t*>(c);
+  c += galign((size_t)p.B * 2 * p.d * sizeof(bf16_t));
   g.part = reinterpret_cast<float*>(c);
   c += galign((size_t)S * T * hidden * sizeof(float));
+  g.partq = reinterpret_cast<float*>(c);
+  c += galign((size_t)Sq * p.B * hidden * sizeof(float));
   g.z = reinterpret_cast<float*>(c);
   c += galign(T * sizeof(float));
   g.pq = reinterpret_cast<int32_t*>(c);
@@ -410,18 +442,20 @@ hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const
                        GateScratch g, float* logits, uint8_t* keep, hipStream_t s) {
   const int T = p.total_passages, h = gt.hidden;
   if (T <= 0) return hipSuccess;
-  int ch = 1, S = 1;
-  gate_split(T, h, p.d, &ch, &S);
-  hipLaunchKernelGGL(gate_x_kernel, dim3(T), dim3(256), 0, s, (const double*)g.qbar,
+  int ch = 1, S = 1, Sq = 1;
+  gate_split(T, h, p.d, &ch, &S, &Sq);
+  hipLaunchKernelGGL(gate_x_kernel, dim3(T + p.B), dim3(256), 0, s, (const double*)g.qbar,
                      (const double*)g.vbar, kbar, passage_keys, query_passages, p.B, T, p.d,
-                     g.X, g.pq, g.done);
-  const int n_tiles = ((T + kGateMT - 1) / kGateMT) * (h / kGateNT);
+                     g.X, g.Xq, g.pq, g.done);
+  const int n_rt = (T + kGateMT - 1) / kGateMT + (p.B + kGateMT - 1) / kGateMT;
+  const int n_tiles = n_rt * (h / kGateNT);
   hipLaunchKernelGGL(gate_score_kernel, dim3(8 * ((S + 7) / 8) * n_tiles), dim3(256), 0, s,
-                     (const bf16_t*)g.X, (const bf16_t*)gt.W, T, p.d, h, ch, S, g.part);
+                     (const bf16_t*)g.X, (const bf16_t*)g.Xq, (const bf16_t*)gt.W, T, p.B, p.d,
+                     h, ch, S, g.part, g.partq);
   const double t = std::log(gt.tau) - std::log1p(-gt.tau);
-  hipLaunchKernelGGL(gate_fin_kernel, dim3(T), dim3(256), 0, s, (const float*)g.part, S, T, h,
-                     gt.b1, gt.w2, gt.b2, (const int32_t*)g.pq, query_passages, t, gt.rho, g.z,
-                     g.done, logits, keep);
+  hipLaunchKernelGGL(gate_fin_kernel, dim3(T), dim3(256), 0, s, (const float*)g.part, S,
+                     (const float*)g.partq, Sq, T, p.B, h, gt.b1, gt.w2, gt.b2,
+                     (const int32_t*)g.pq, query_passages, t, gt.rho, g.z, g.done, logits, keep);
   return hipGetLastError();
 }
 

@@ -61,8 +61,10 @@ hipError_t launch_mlp_scores(const skip_problem_t& p, const skip_qvs_mlp_t& m, c
 struct GateScratch {
   double* qbar;      // [B][d]         mean of the question tokens
   double* vbar;      // [B][d]         mean of the kept visual rows
-  bf16_t* X;         // [T][5d]        gate inputs
-  float* part;       // [S][T][h]      chunk partials of W x
+  bf16_t* X;         // [T][3d]        passage blocks of the gate inputs
+  bf16_t* Xq;        // [B][2d]        question blocks of the gate inputs
+  float* part;       // [S][T][h]      chunk partials of the passage blocks' products
+  float* partq;      // [Sq][B][h]     chunk partials of the question blocks' products
   float* z;          // [T]            logits
   int32_t* pq;       // [T]            question of each passage
   int32_t* done;     // [B]            finished passages per question
