@@ -8,7 +8,7 @@
 // value; the difference rounded from its float32 value).
 //   gate_mean_kernel  : q_bar (question tokens) and v_bar (kept rows, given as
 //                       rows or through kept_idx) in float64, 8 waves a
-//                       workgroup with four rows a wave in flight
+//                       workgroup with eight rows a wave in flight
 //   gate_x_kernel     : the bf16 gate inputs: the passage blocks
 //                       [e ; e*q_bar ; |e - q_bar|] of every passage, [T][3d],
 //                       and the question blocks [q_bar ; v_bar] of every
@@ -56,7 +56,7 @@ constexpr int kGateInFlight = 3;   // 64-column groups whose loads a wave issues
 // Workgroup (512-column slice, y): y < B is q_bar_y over the question tokens,
 // y >= B is v_bar_{y-B} over the kept rows (rows[kept_offsets range], or
 // V[b][kept_idx[r]] when kept_idx is given).  Wave w sums the rows w, w+8, ...
-// in float64 (16 bytes a lane, four rows in flight); the eight partial sums
+// in float64 (16 bytes a lane, eight rows in flight); the eight partial sums
 // are added in wave order; an empty range gives 0.
 __global__ void __launch_bounds__(512)
 gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_offsets,
@@ -98,7 +98,7 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-  constexpr int U = 4;
+  constexpr int U = 8;
   int r = r0 + wave;
   fetch_idx(r);
   for (; r + kGateMeanWaves * (U - 1) < r1; r += kGateMeanWaves * U) {
@@ -303,21 +303,21 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Xq,
   dst[1] = make_float4(o[4], o[5], o[6], o[7]);
 }
 
-// Block p (passage of question b, 256 threads): pre-activation of unit j =
+// Block p (passage of question b, 512 threads): pre-activation of unit j =
 // the S chunk partials of p in chunk order, then the Sq chunk partials of b
 // in chunk order, + b1[j]; thread t sums relu(.) * w2[j] over its
-// units j = t, t+256, ... in order; the four waves' sums (wave shuffles, then
+// units j = t, t+512, ... in order; the eight waves' sums (wave shuffles, then
 // wave order) plus b2, rounded to float32, are logit_p.  The block then bumps
 // its question's counter; the block that completes it (P_b blocks in all)
 // takes the cut: kept = logit >= t and among the cap largest verified logits
 // (ties: lower index), on the float32 logits.
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(512)
 gate_fin_kernel(const float* __restrict__ part, int S, const float* __restrict__ partq, int Sq,
                 int T, int B, int h, const float* __restrict__ b1, const float* __restrict__ w2, double b2,
                 const int32_t* __restrict__ pq, const int32_t* __restrict__ query_passages,
                 double t, double rho, float* __restrict__ zbuf, int32_t* __restrict__ done,
                 float* __restrict__ logits, uint8_t* __restrict__ keep) {
-  __shared__ float wsum[4];
+  __shared__ float wsum[8];
   __shared__ int last;
   const int p = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -349,8 +349,9 @@ gate_fin_kernel(const float* __restrict__ part, int S, const float* __restrict__
   range_of(query_passages, b, T, p0, p1);
   const int P = min(p1 - p0, 64);
   if (threadIdx.x == 0) {
-    const double tot = (((double)wsum[0] + (double)wsum[1]) + (double)wsum[2]) +
-                       (double)wsum[3] + b2;
+    double tot = (double)wsum[0];
+    for (int w = 1; w < 8; ++w) tot += (double)wsum[w];
+    tot += b2;
     const float zl = (float)tot;
     store_shared(&zbuf[p], zl);                   // read by the question's last block
     if (logits) logits[p] = zl;
@@ -453,7 +454,7 @@ hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const
                      (const bf16_t*)g.X, (const bf16_t*)g.Xq, (const bf16_t*)gt.W, T, p.B, p.d,
                      h, ch, S, g.part, g.partq);
   const double t = std::log(gt.tau) - std::log1p(-gt.tau);
-  hipLaunchKernelGGL(gate_fin_kernel, dim3(T), dim3(256), 0, s, (const float*)g.part, S,
+  hipLaunchKernelGGL(gate_fin_kernel, dim3(T), dim3(512), 0, s, (const float*)g.part, S,
                      (const float*)g.partq, Sq, T, p.B, h, gt.b1, gt.w2, gt.b2,
                      (const int32_t*)g.pq, query_passages, t, gt.rho, g.z, g.done, logits, keep);
   return hipGetLastError();
