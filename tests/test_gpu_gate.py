@@ -129,6 +129,33 @@ def test_gate_small_ragged(B, hidden, seed):
         check_gate(batch, w, logits, keep, ref, tau, rho, tag=f"h{hidden} tau={tau} rho={rho}")
 
 
+@pytest.mark.parametrize("given_keys", [False, True])
+def test_gate_many_questions_odd_group_count(B, given_keys):
+    """40 questions (two 32-row tiles of question blocks), 275 passages (a
+    ragged last passage tile) and d = 192: the passage blocks' 3d columns
+    are an odd number of 64-column groups (a wave's last round has spare
+    slots), the question blocks' 2d columns fewer, so the two kinds of tile
+    take different group counts."""
+    batch = wls.make_batch("llava_bf16", 42, B=40, N=120, H=3, d_h=64, T=(1, 3, 8),
+                           k=(0, 7, 33, 64), P=(0, 1, 3, 6, 17), L_p=(1, 5, 40))
+    w = wls.make_gate_weights(batch.wl, 128, 42)
+    say(f"gate 40 questions d=192 given_keys={given_keys} P={batch.P.tolist()}")
+    assert batch.wl.d == 192 and batch.B == 40
+    db = B.to_device(batch)
+    Vk = kept_rows_oracle(batch)
+    keys = None
+    if given_keys:
+        rng = np.random.default_rng(42)
+        keys = torch.from_numpy((rng.standard_normal((int(batch.P.sum()), batch.wl.d)) * 0.5)
+                                .astype(np.float32))
+    ref = gate_oracle(batch, w, Vk, keys)
+    for tau, rho in ((0.5, 0.5), (0.3, 1.0)):
+        keep, logits = B.skv_gate(db, gate_device(B, w, tau, rho), Vk.cuda(),
+                                  passage_keys=None if keys is None else keys.cuda())
+        torch.cuda.synchronize()
+        check_gate(batch, w, logits, keep, ref, tau, rho, tag=f"d192 tau={tau} rho={rho}")
+
+
 def test_gate_given_keys_no_b1_repeatable(B):
     batch = wls.make_batch("llava_bf16", 7, B=4, N=200, H=2, d_h=128, T=(2, 9), k=(5, 40),
                            P=(2, 9, 64), L_p=(3, 20))
