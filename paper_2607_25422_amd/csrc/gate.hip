@@ -16,7 +16,7 @@
 //   gate_score_kernel : W x on v_mfma_f32_32x32x16_bf16, split as
 //                       W[:, 2d:5d] . (passage blocks) per passage plus
 //                       W[:, 0:2d] . (question blocks) once per question (the
-//                       same for all its passages); tiles of 32 rows x 64
+//                       same for all its passages); tiles of 64 rows x 64
 //                       hidden units, the columns split into chunks (split-K,
 //                       so the launch fills the chip at a few hundred
 //                       passages); one float32 partial per chunk
@@ -47,11 +47,12 @@ __device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, 
 
 }  // namespace
 
-constexpr int kGateMT = 32;        // passages per score tile
+constexpr int kGateRB = 2;         // 32-row MFMA blocks per score tile
+constexpr int kGateMT = 32 * kGateRB;  // rows (passages or questions) per score tile
 constexpr int kGateNT = 64;        // hidden units per score tile
 constexpr int kGateMeanWaves = 8;  // waves per mean workgroup (512 columns)
 constexpr int kGateTargetWG = 640; // passage-tile workgroups aimed for when choosing S
-constexpr int kGateInFlight = 3;   // 64-column groups whose loads a wave issues together
+constexpr int kGateInFlight = 2;   // 64-column groups whose loads a wave issues together
 
 // Workgroup (512-column slice, y): y < B is q_bar_y over the question tokens,
 // y >= B is v_bar_{y-B} over the kept rows (rows[kept_offsets range], or
@@ -209,19 +210,19 @@ gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
   }
 }
 
-// Row tiles: 32 passages (tiles 0 .. n_pt-1: the rows of X, K = 3d columns,
-// against W's columns 2d .. 5d) or 32 questions (tiles n_pt ..: the rows of
-// Xq, K = 2d, against W's columns 0 .. 2d).  Tile (rows, 64 hidden units),
-// chunk z of its K columns, in groups of 64 columns: groups [z*ch, min((z+1)*
-// ch, ceil(K/64))), wave w taking the groups w, w+4, ...; a question tile
-// whose K ends before chunk z exits at once.  In a group the lane pair (row
-// or unit l%32, half hh) reads the row's 128 contiguous bytes, 64 a lane as
-// four 16-byte pieces, and piece u feeds MFMA step u: step u sums the columns
-// 8u..8u+7 and 32+8u..32+8u+7 of the group (A and B take the same columns,
-// so the product over the group is complete).  Three groups (twelve steps)
-// are in flight per wave, spare slots of the last round reading zeros.  A
-// half group at the end of the columns (K/32 odd)
-// reads zeros for its second half.  The four waves' sums are added in wave
+// Row tiles: 64 passages (tiles 0 .. n_pt-1: the rows of X, K = 3d columns,
+// against W's columns 2d .. 5d) or 64 questions (tiles n_pt ..: the rows of
+// Xq, K = 2d, against W's columns 0 .. 2d), as two 32-row MFMA blocks that
+// share every W operand.  Tile (rows, 64 hidden units), chunk z of its K
+// columns, in groups of 64 columns: groups [z*ch, min((z+1)*ch, ceil(K/64))),
+// wave w taking the groups w, w+4, ...; a question tile whose K ends before
+// chunk z exits at once.  In a group the lane pair (row or unit l%32, half
+// hh) reads the row's 128 contiguous bytes, 64 a lane as four 16-byte pieces,
+// and piece u feeds MFMA step u: step u sums the columns 8u..8u+7 and
+// 32+8u..32+8u+7 of the group (A and B take the same columns, so the product
+// over the group is complete).  Two groups are in flight per wave, spare
+// slots of the last round reading zeros.  A half group at the end of the
+// columns (K/32 odd) reads zeros for its second half.  The four waves' sums are added in wave
 // order and written as part[z][passage][unit] or partq[z][question][unit].
 //
 // Tiles go to XCDs by chunk: the hardware deals workgroup ids round-robin over
@@ -249,58 +250,72 @@ gate_score_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Xq,
   const int g1 = min((z + 1) * ch, ngroups);
   const int nrows = qtile ? B : T;
   const int r0 = (qtile ? rt - n_pt : rt) * kGateMT;
-  const int prow = min(r0 + r32, nrows - 1);
-  const bf16_t* xa = (qtile ? Xq : X) + (size_t)prow * K + 32 * hh;
+  const bf16_t* xbase = qtile ? Xq : X;
+  const bf16_t* xa[kGateRB];
+#pragma unroll
+  for (int rb = 0; rb < kGateRB; ++rb)
+    xa[rb] = xbase + (size_t)min(r0 + 32 * rb + r32, nrows - 1) * K + 32 * hh;
   const bf16_t* wb0 = W + (size_t)(ht * kGateNT + r32) * (5 * d) + (qtile ? 0 : 2 * d) + 32 * hh;
   const bf16_t* wb1 = wb0 + (size_t)32 * 5 * d;
-  f32x16_t acc[2];
+  f32x16_t acc[kGateRB][2];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) { acc[0][v] = 0.f; acc[1][v] = 0.f; }
+  for (int rb = 0; rb < kGateRB; ++rb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) { acc[rb][0][v] = 0.f; acc[rb][1][v] = 0.f; }
   const u32x4 zero = {0u, 0u, 0u, 0u};
   // group gg of the wave's rounds; past g1 (the last round's spare slots) zeros
-  auto load_group = [&](int gg, u32x4* a, u32x4* b0, u32x4* b1) {
+  auto load_group = [&](int gg, u32x4 (*a)[4], u32x4* b0, u32x4* b1) {
     const int c = 64 * gg;
     const bool ok = gg < g1 && c + 32 * hh < K;   // K is a multiple of 32
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      a[u] = ok ? *reinterpret_cast<const u32x4*>(xa + c + 8 * u) : zero;
+#pragma unroll
+      for (int rb = 0; rb < kGateRB; ++rb)
+        a[rb][u] = ok ? *reinterpret_cast<const u32x4*>(xa[rb] + c + 8 * u) : zero;
       b0[u] = ok ? *reinterpret_cast<const u32x4*>(wb0 + c + 8 * u) : zero;
       b1[u] = ok ? *reinterpret_cast<const u32x4*>(wb1 + c + 8 * u) : zero;
     }
   };
   for (int g = z * ch + wave; g < g1; g += 4 * kGateInFlight) {
-    u32x4 a[4 * kGateInFlight], b0[4 * kGateInFlight], b1[4 * kGateInFlight];
+    u32x4 a[kGateInFlight][kGateRB][4], b0[kGateInFlight][4], b1[kGateInFlight][4];
+#pragma unroll
+    for (int e = 0; e < kGateInFlight; ++e) load_group(g + 4 * e, a[e], b0[e], b1[e]);
 #pragma unroll
     for (int e = 0; e < kGateInFlight; ++e)
-      load_group(g + 4 * e, a + 4 * e, b0 + 4 * e, b1 + 4 * e);
 #pragma unroll
-    for (int u = 0; u < 4 * kGateInFlight; ++u) {
-      acc[0] = mfma32_bf16(a[u], b0[u], acc[0]);
-      acc[1] = mfma32_bf16(a[u], b1[u], acc[1]);
-    }
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int rb = 0; rb < kGateRB; ++rb) {
+          acc[rb][0] = mfma32_bf16(a[e][rb][u], b0[e][u], acc[rb][0]);
+          acc[rb][1] = mfma32_bf16(a[e][rb][u], b1[e][u], acc[rb][1]);
+        }
   }
-  // D layout: element v of block nb is passage 8*(v/4) + 4*hh + v%4, hidden
-  // unit nb*32 + r32 of the tile
+  // D layout: element v of block (rb, nb) is row 32*rb + 8*(v/4) + 4*hh + v%4,
+  // hidden unit nb*32 + r32 of the tile
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
+  for (int rb = 0; rb < kGateRB; ++rb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      red[wave][8 * (v >> 2) + 4 * hh + (v & 3)][nb * 32 + r32] = acc[nb][v];
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        red[wave][32 * rb + 8 * (v >> 2) + 4 * hh + (v & 3)][nb * 32 + r32] = acc[rb][nb][v];
   __syncthreads();
-  // thread t: row t / 8, hidden units 8 * (t % 8) .. + 7
-  const int m = threadIdx.x >> 3, n0 = (threadIdx.x & 7) * 8;
+  // thread t: row t / (256 / MT), hidden units NPT * (t % (256 / MT)) .. + NPT-1
+  constexpr int TPR = 256 / kGateMT, NPT = kGateNT / TPR;
+  const int m = threadIdx.x / TPR, n0 = (threadIdx.x % TPR) * NPT;
   const int p = r0 + m;
   if (p >= nrows) return;
-  float o[8];
+  float o[NPT];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+  for (int e = 0; e < NPT; ++e) {
     const int n = n0 + e;
     o[e] = ((red[0][m][n] + red[1][m][n]) + red[2][m][n]) + red[3][m][n];
   }
   float4* dst = reinterpret_cast<float4*>((qtile ? partq : part) + ((size_t)z * nrows + p) * h +
                                           ht * kGateNT + n0);
-  dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-  dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+#pragma unroll
+  for (int e = 0; e < NPT / 4; ++e)
+    dst[e] = make_float4(o[4 * e], o[4 * e + 1], o[4 * e + 2], o[4 * e + 3]);
 }
 
 // Block p (passage of question b, 512 threads): pre-activation of unit j =
