@@ -8,7 +8,7 @@
 // value; the difference rounded from its float32 value).
 //   gate_mean_kernel  : q_bar (question tokens) and v_bar (kept rows, given as
 //                       rows or through kept_idx) in float64, 8 waves a
-//                       workgroup with eight rows a wave in flight
+//                       workgroup, sixteen rows a wave in flight
 //   gate_x_kernel     : the bf16 gate inputs: the passage blocks
 //                       [e ; e*q_bar ; |e - q_bar|] of every passage, [T][3d],
 //                       and the question blocks [q_bar ; v_bar] of every
@@ -50,15 +50,18 @@ __device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, 
 constexpr int kGateRB = 2;         // 32-row MFMA blocks per score tile
 constexpr int kGateMT = 32 * kGateRB;  // rows (passages or questions) per score tile
 constexpr int kGateNT = 64;        // hidden units per score tile
-constexpr int kGateMeanWaves = 8;  // waves per mean workgroup (512 columns)
+constexpr int kGateMeanWaves = 8;  // waves per mean workgroup (256 columns)
 constexpr int kGateTargetWG = 640; // passage-tile workgroups aimed for when choosing S
 constexpr int kGateInFlight = 2;   // 64-column groups whose loads a wave issues together
 
-// Workgroup (512-column slice, y): y < B is q_bar_y over the question tokens,
+// Workgroup (256-column slice, y): y < B is q_bar_y over the question tokens,
 // y >= B is v_bar_{y-B} over the kept rows (rows[kept_offsets range], or
-// V[b][kept_idx[r]] when kept_idx is given).  Wave w sums the rows w, w+8, ...
-// in float64 (16 bytes a lane, eight rows in flight); the eight partial sums
-// are added in wave order; an empty range gives 0.
+// V[b][kept_idx[r]] when kept_idx is given).  Row slot s of wave w is row
+// w + 8s of the range; the half-wave s % 2 takes it, each lane 16 bytes of
+// the row, so a half-wave covers the slice and a wave has two rows in each
+// load instruction.  Sums in float64, sixteen slots (eight rows a half-wave)
+// in flight; the sixteen partial sums are added in (wave, half) order; an
+// empty range gives 0.
 __global__ void __launch_bounds__(512)
 gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_offsets,
                  int total_qtok, const bf16_t* __restrict__ rows,
@@ -69,22 +72,23 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
   const bool isq = (int)blockIdx.y < B;
   const int b = isq ? (int)blockIdx.y : (int)blockIdx.y - B;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = (blockIdx.x * 64 + lane) * 8;
+  const int hf = lane >> 5, l32 = lane & 31;
+  const int c = (blockIdx.x * 32 + l32) * 8;
   int r0, r1;
   if (isq) range_of(q_offsets, b, total_qtok, r0, r1);
   else range_of(kept_offsets, b, total_kept, r0, r1);
   const bf16_t* src = isq ? Qtok : rows;
   const bool indexed = !isq && kept_idx != nullptr;
   // indexed rows: lane i holds the index of the wave's i-th row (rows w,
-  // w+8, ... up to 64 of them a pass), read once before the row loads
+  // w+8, ... up to 64 of them), read before the row loads that need it
   int my_idx = 0, base_r = r0 + wave;
   auto fetch_idx = [&](int rb) {
     const int r = rb + kGateMeanWaves * lane;
     my_idx = (indexed && r < r1) ? clampi(kept_idx[r], 0, N - 1) : 0;
     base_r = rb;
   };
-  // the row loop is wave-uniform (every lane shuffles); lanes past the last
-  // column load nothing
+  // every lane shuffles (the loop is wave-uniform); lanes past the last
+  // column or the last row load nothing
   const bool cok = c < d;
   const u32x4 zero = {0u, 0u, 0u, 0u};
   auto load_row = [&](int r) -> u32x4 {
@@ -93,46 +97,42 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
       const int i = __shfl(my_idx, (r - base_r) / kGateMeanWaves, kWave);
       off = ((size_t)b * N + i) * d;
     }
-    return cok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + off + c))
+    return (cok && r < r1)
+               ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + off + c))
                : zero;
   };
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-  constexpr int U = 8;
+  constexpr int U = 16;                       // row slots a wave per round
   int r = r0 + wave;
   fetch_idx(r);
-  for (; r + kGateMeanWaves * (U - 1) < r1; r += kGateMeanWaves * U) {
+  for (; r < r1; r += kGateMeanWaves * U) {
     if (r + kGateMeanWaves * (U - 1) >= base_r + kGateMeanWaves * 64) fetch_idx(r);
-    u32x4 x[U];
+    u32x4 x[U / 2];
 #pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = load_row(r + kGateMeanWaves * u);
+    for (int u = 0; u < U / 2; ++u) x[u] = load_row(r + kGateMeanWaves * (2 * u + hf));
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float f[8];
-      unpack8_bf16(x[u], f);
+    for (int u = 0; u < U / 2; ++u) {
+      if (r + kGateMeanWaves * (2 * u + hf) < r1) {
+        float f[8];
+        unpack8_bf16(x[u], f);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
+        for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
+      }
     }
-  }
-  for (; r < r1; r += kGateMeanWaves) {
-    if (r >= base_r + kGateMeanWaves * 64) fetch_idx(r);
-    float f[8];
-    unpack8_bf16(load_row(r), f);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += (double)f[e];
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) part[wave][lane][e] = acc[e];
   __syncthreads();
-  if (wave != 0 || c >= d) return;
+  if (wave != 0 || hf != 0 || c >= d) return;
   const int L = r1 - r0;
   double* out = (isq ? qbar : vbar) + (size_t)b * d + c;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    double s = part[0][lane][e];
+    double s = part[0][l32][e] + part[0][l32 + 32][e];
 #pragma unroll
-    for (int w = 1; w < kGateMeanWaves; ++w) s += part[w][lane][e];
+    for (int w = 1; w < kGateMeanWaves; ++w) s = (s + part[w][l32][e]) + part[w][l32 + 32][e];
     out[e] = L > 0 ? s / (double)L : 0.0;
   }
 }
@@ -447,7 +447,7 @@ hipError_t launch_gate_means(const skip_problem_t& p, const void* Qtok,
                              const int32_t* q_offsets, const void* rows,
                              const int32_t* kept_offsets, const int32_t* kept_idx,
                              GateScratch g, hipStream_t s) {
-  hipLaunchKernelGGL(gate_mean_kernel, dim3((p.d + 511) / 512, 2 * p.B), dim3(512), 0, s,
+  hipLaunchKernelGGL(gate_mean_kernel, dim3((p.d + 255) / 256, 2 * p.B), dim3(512), 0, s,
                      (const bf16_t*)Qtok, q_offsets, p.total_qtok, (const bf16_t*)rows,
                      kept_offsets, kept_idx, p.N, p.total_kept, p.B, p.d, g.qbar, g.vbar);
   return hipGetLastError();
