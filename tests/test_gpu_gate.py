@@ -366,3 +366,28 @@ def test_route_fused_gated_full_size_equals_staged(B):
             want_O.append(ref.O[b][r]); want_L.append(ref.LSE[b][r])
     check_attention(np.stack(got_O), np.stack(got_L), np.stack(want_O), np.stack(want_L),
                     "bf16", "fused gated highres")
+
+
+@pytest.mark.parametrize("workload,seed", [("llava_bf16", s) for s in wls.SEEDS] +
+                         [("highres_bf16", 2026)])
+def test_route_fused_gated_keeping_all_equals_plain(B, workload, seed):
+    """A gate that keeps every passage (threshold far below every logit,
+    rho = 1: Def. B.4's cut then drops nothing) leaves the route of Alg. 1
+    unchanged: kept sets, outputs and log-sum-exps bitwise equal to the
+    plain fused route on the same batch."""
+    if workload == "llava_bf16":
+        batch = wls.make_batch(workload, seed, B=6, N=300, H=4, d_h=64, T=(1, 3, 8),
+                               k=(0, 7, 33, 64), P=(0, 1, 3, 6, 17), L_p=(1, 5, 64),
+                               with_bias=True)
+    else:
+        batch = wls.make_batch(workload, seed, threads=16)
+    w = wls.make_gate_weights(batch.wl, 256, seed)
+    say(f"gated keeping all {workload} seed={seed} P={batch.P.tolist()}")
+    db = B.to_device(batch)
+    idx, keep, logits, O, L = B.route_fused_gated(db, gate_device(B, w, 1e-300, 1.0))
+    pidx, pO, pL = B.route_fused(db)
+    torch.cuda.synchronize()
+    assert bool((keep == 1).all()), "a passage was dropped"
+    assert bool(torch.isfinite(logits).all())
+    assert torch.equal(idx, pidx), "kept sets differ"
+    assert torch.equal(O, pO) and torch.equal(L, pL), "gated route != plain route"
