@@ -391,3 +391,35 @@ def test_route_fused_gated_keeping_all_equals_plain(B, workload, seed):
     assert bool(torch.isfinite(logits).all())
     assert torch.equal(idx, pidx), "kept sets differ"
     assert torch.equal(O, pO) and torch.equal(L, pL), "gated route != plain route"
+
+
+@pytest.mark.parametrize("rule,metric,beta", [("row", "cosine", 0.1), ("fraction", "dot", 0.3),
+                                               ("question", "dot", 0.1)])
+def test_route_fused_gated_edge_rules(B, rule, metric, beta):
+    """The fused gated route under the other edge cuts and compatibilities
+    (Sec. 3.5, eq. (bsca) and its quantile cut; per-row top-Δ): kept sets,
+    the gate and the attention of every kept row against the oracle's route
+    with the same gate and cut."""
+    seed = 42
+    batch = wls.make_batch("llava_bf16", seed, B=6, N=300, H=4, d_h=64, T=(1, 3, 8),
+                           k=(0, 7, 33, 64), P=(0, 1, 3, 6, 17), L_p=(1, 5, 64),
+                           with_bias=True)
+    w = wls.make_gate_weights(batch.wl, 256, seed)
+    say(f"fused gated {rule}/{metric} k={batch.k.tolist()} P={batch.P.tolist()}")
+    db = B.to_device(batch, avg_degree=4.0, edge_rule=rule, edge_metric=metric, edge_beta=beta)
+    idx, keep, logits, O, L = B.route_fused_gated(db, gate_device(B, w, 0.5, 0.5))
+    torch.cuda.synchronize()
+    ref = orc.route(batch.V, batch.Qtok, batch.q_offsets, batch.kept_offsets, batch.Kh,
+                    batch.Vh, batch.passage_offsets, batch.query_passages, batch.wl.scale, 4.0,
+                    w_bias=batch.w_bias, edge_rule=rule, edge_metric=metric, edge_beta=beta,
+                    gate=gate_dict(w, 0.5, 0.5))
+    idx = idx.cpu().numpy()
+    for b in range(batch.B):
+        k0, k1 = batch.kept_offsets[b], batch.kept_offsets[b + 1]
+        assert idx[k0:k1].tolist() == ref.kept_idx[b].tolist(), f"q{b} kept set"
+    check_gate(batch, w, logits, keep, ref.gate_logits, 0.5, 0.5, tag=f"fused {rule}/{metric}")
+    Of, Lf = f64(O), f64(L)
+    for b in matching_questions(batch, keep, ref.keep):
+        k0, k1 = int(batch.kept_offsets[b]), int(batch.kept_offsets[b + 1])
+        check_attention(Of[k0:k1], Lf[k0:k1], ref.O[b], ref.LSE[b], "bf16",
+                        f"fused gated {rule}/{metric} q{b}")
