@@ -81,6 +81,40 @@ def test_project_small_ragged(B, seed, d_out):
     assert torch.equal(y32.to(torch.bfloat16), y_idx)
 
 
+@pytest.mark.parametrize("d_out", [256, 512])
+def test_project_permutation_exact(B, d_out):
+    """W selecting one input column per output (a permutation of the d
+    columns, repeated and scaled by 2 past the first d outputs): every output
+    is one exact product, so Y equals the selected, scaled columns of the
+    kept rows bit for bit, through the one-call and the packed paths (eq.
+    (bsca)'s W_v x with a W whose product is known exactly)."""
+    batch = wls.make_batch("llava_bf16", 11, B=4, N=300, H=4, d_h=64, T=(1, 3),
+                           k=(0, 7, 64, 130))
+    d = batch.wl.d
+    rng = np.random.default_rng(11)
+    perm = rng.permutation(d)
+    W = torch.zeros((d_out, d), dtype=torch.float32)
+    for o in range(d_out):
+        W[o, perm[o % d]] = 1.0 if o < d else 2.0
+    W = W.to(torch.bfloat16)
+    say(f"projection permutation d_out={d_out} k={batch.k.tolist()}")
+    kept = kept_oracle(batch)
+    rows = kept_rows(batch, kept)
+    cols = torch.from_numpy(np.array([perm[o % d] for o in range(d_out)], dtype=np.int64))
+    scale = torch.tensor([1.0 if o < d else 2.0 for o in range(d_out)], dtype=torch.float32)
+    want = rows.float()[:, cols] * scale
+    db = B.to_device(batch)
+    Wd = W.cuda()
+    idx = torch.from_numpy(np.concatenate(kept).astype(np.int32)).cuda()
+    packed = B.pack_projection(db, Wd)
+    outs = [B.gather_project(db, db.V, Wd, kept_idx=idx, out_f32=True),
+            B.gather_project_packed(db, rows.cuda(), packed, d_out, out_f32=True),
+            B.gather_project(db, rows.cuda(), Wd).float()]
+    torch.cuda.synchronize()
+    for i, y in enumerate(outs):
+        assert torch.equal(y.cpu(), want), f"output {i} is not the selected columns"
+
+
 @pytest.mark.parametrize("d_out", [256, 768])
 def test_project_packed_matches_one_call(B, d_out):
     """Weights packed once and reused: every output bitwise equal to the
