@@ -290,7 +290,7 @@ def bench_gated_route(args):
         "gated_route_gpu_ms": {"p50": round(gated[n // 2], 5), "mean": round(mean(gated), 5)},
         "plain_route_gpu_ms": {"p50": round(plain[n // 2], 5), "mean": round(mean(plain), 5)},
         "passages_kept": kept, "passages": p.total_passages,
-        "roofline": {"kernel": "skip_skv_gate call (4 kernels, keys given)", "bound": "hbm",
+        "roofline": {"kernel": "skip_skv_gate call (3 kernels, keys given)", "bound": "hbm",
                      "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
                      "algorithmic_bytes": gate_bytes, "avg_ms": round(gms, 5),

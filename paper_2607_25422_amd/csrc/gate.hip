@@ -8,11 +8,11 @@
 // value; the difference rounded from its float32 value).
 //   gate_mean_kernel  : q_bar (question tokens) and v_bar (kept rows, given as
 //                       rows or through kept_idx) in float64, 8 waves a
-//                       workgroup, sixteen rows a wave in flight
-//   gate_x_kernel     : the bf16 gate inputs: the passage blocks
-//                       [e ; e*q_bar ; |e - q_bar|] of every passage, [T][3d],
-//                       and the question blocks [q_bar ; v_bar] of every
-//                       question, [B][2d]
+//                       workgroup, sixteen rows a wave in flight; then, per
+//                       column slice, the bf16 gate inputs: the question
+//                       blocks [q_bar ; v_bar] of every question, [B][2d],
+//                       and the passage blocks [e ; e*q_bar ; |e - q_bar|]
+//                       of every passage, [T][3d]
 //   gate_score_kernel : W x on v_mfma_f32_32x32x16_bf16, split as
 //                       W[:, 2d:5d] . (passage blocks) per passage plus
 //                       W[:, 0:2d] . (question blocks) once per question (the
@@ -62,13 +62,23 @@ constexpr int kGateInFlight = 2;   // 64-column groups whose loads a wave issues
 // load instruction.  Sums in float64, sixteen slots (eight rows a half-wave)
 // in flight; the sixteen partial sums are added in (wave, half) order; an
 // empty range gives 0.
+// The workgroup then writes its slice of the bf16 gate inputs: Xq[b] =
+// [q' ; v'] (x' the bf16 rounding of float32(x)); a question workgroup also
+// the slice of X[j] = [e' ; (e' q')' ; |e' - q'|'] for every passage j of
+// its question (half-wave h taking the passages h, h+16, ...: the keys e_j
+// are complete before this launch), pq[j] = b and, in slice 0, the
+// question's finish counter cleared.
 __global__ void __launch_bounds__(512)
 gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_offsets,
                  int total_qtok, const bf16_t* __restrict__ rows,
                  const int32_t* __restrict__ kept_offsets, const int32_t* __restrict__ kept_idx,
                  int N, int total_kept, int B, int d, double* __restrict__ qbar,
-                 double* __restrict__ vbar) {
+                 double* __restrict__ vbar, const double* __restrict__ kbar,
+                 const float* __restrict__ pkeys, const int32_t* __restrict__ query_passages,
+                 int T, bf16_t* __restrict__ X, bf16_t* __restrict__ Xq,
+                 int32_t* __restrict__ pq, int32_t* __restrict__ done) {
   __shared__ double part[kGateMeanWaves][64][8];
+  __shared__ float qsl[256];          // q' of the slice's columns (question workgroups)
   const bool isq = (int)blockIdx.y < B;
   const int b = isq ? (int)blockIdx.y : (int)blockIdx.y - B;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -125,53 +135,37 @@ gate_mean_kernel(const bf16_t* __restrict__ Qtok, const int32_t* __restrict__ q_
 #pragma unroll
   for (int e = 0; e < 8; ++e) part[wave][lane][e] = acc[e];
   __syncthreads();
-  if (wave != 0 || hf != 0 || c >= d) return;
   const int L = r1 - r0;
-  double* out = (isq ? qbar : vbar) + (size_t)b * d + c;
+  if (wave == 0 && hf == 0 && cok) {
+    double* out = (isq ? qbar : vbar) + (size_t)b * d + c;
+    float m[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    double s = part[0][l32][e] + part[0][l32 + 32][e];
+    for (int e = 0; e < 8; ++e) {
+      double s = part[0][l32][e] + part[0][l32 + 32][e];
 #pragma unroll
-    for (int w = 1; w < kGateMeanWaves; ++w) s = (s + part[w][l32][e]) + part[w][l32 + 32][e];
-    out[e] = L > 0 ? s / (double)L : 0.0;
-  }
-}
-
-// Block j < T (passage j of question b): X[j] = [e' ; (e' q')' ; |e' - q'|']
-// (x' the bf16 rounding), pq[j] = b.  Block T + b (question b): Xq[b] =
-// [q' ; v'], and the question's finish counter cleared.  Thread t fills
-// 8-column groups t, t+256, ... of every block of its row.
-__global__ void __launch_bounds__(256)
-gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
-              const double* __restrict__ kbar, const float* __restrict__ pkeys,
-              const int32_t* __restrict__ query_passages, int B, int T, int d,
-              bf16_t* __restrict__ X, bf16_t* __restrict__ Xq, int32_t* __restrict__ pq,
-              int32_t* __restrict__ done) {
-  const int j = blockIdx.x;
-  if (j >= T) {
-    const int b = j - T;
-    if (threadIdx.x == 0) done[b] = 0;
-    bf16_t* xr = Xq + (size_t)b * 2 * d;
-    for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
-      const double2* qp2 = reinterpret_cast<const double2*>(qbar + (size_t)b * d + c);
-      const double2* vp2 = reinterpret_cast<const double2*>(vbar + (size_t)b * d + c);
-      u32x4 oq, ov;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const double2 x = qp2[t], y = vp2[t];
-        oq[t] = pack2_bf16((float)x.x, (float)x.y);
-        ov[t] = pack2_bf16((float)y.x, (float)y.y);
-      }
-      *reinterpret_cast<u32x4*>(xr + c) = oq;
-      *reinterpret_cast<u32x4*>(xr + d + c) = ov;
+      for (int w = 1; w < kGateMeanWaves; ++w) s = (s + part[w][l32][e]) + part[w][l32 + 32][e];
+      const double mean = L > 0 ? s / (double)L : 0.0;
+      out[e] = mean;
+      m[e] = (float)mean;
     }
-    return;
+    u32x4 ob;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ob[t] = pack2_bf16(m[2 * t], m[2 * t + 1]);
+    *reinterpret_cast<u32x4*>(Xq + (size_t)b * 2 * d + (isq ? 0 : d) + c) = ob;
+    if (isq) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qsl[8 * l32 + e] = bf16_to_f32(f32_to_bf16(m[e]));
+    }
   }
-  const int b = question_of(query_passages, B, T, j);
-  if (threadIdx.x == 0) pq[j] = b;
-  bf16_t* xr = X + (size_t)j * 3 * d;
-  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
-    float e[8], q[8];
+  if (!isq) return;                   // uniform: the kind of workgroup
+  if (blockIdx.x == 0 && threadIdx.x == 0) done[b] = 0;
+  __syncthreads();
+  int p0, p1;
+  range_of(query_passages, b, T, p0, p1);
+  for (int j = p0 + (int)(threadIdx.x >> 5); j < p1; j += 16) {
+    if (blockIdx.x == 0 && l32 == 0) pq[j] = b;
+    if (!cok) continue;
+    float e[8];
     if (pkeys) {
       const float4 a = *reinterpret_cast<const float4*>(pkeys + (size_t)j * d + c);
       const float4 a2 = *reinterpret_cast<const float4*>(pkeys + (size_t)j * d + c + 4);
@@ -186,24 +180,17 @@ gate_x_kernel(const double* __restrict__ qbar, const double* __restrict__ vbar,
         e[2 * t + 1] = (float)x.y;
       }
     }
-    const double2* qp2 = reinterpret_cast<const double2*>(qbar + (size_t)b * d + c);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const double2 x = qp2[t];
-      q[2 * t] = (float)x.x;
-      q[2 * t + 1] = (float)x.y;
-    }
     u32x4 oe, oh, od;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const float e0 = bf16_to_f32(f32_to_bf16(e[2 * t]));
       const float e1 = bf16_to_f32(f32_to_bf16(e[2 * t + 1]));
-      const float q0 = bf16_to_f32(f32_to_bf16(q[2 * t]));
-      const float q1 = bf16_to_f32(f32_to_bf16(q[2 * t + 1]));
+      const float q0 = qsl[8 * l32 + 2 * t], q1 = qsl[8 * l32 + 2 * t + 1];
       oe[t] = pack2_bf16(e0, e1);
       oh[t] = pack2_bf16(e0 * q0, e1 * q1);              // exact product, one rounding
       od[t] = pack2_bf16(fabsf(e0 - q0), fabsf(e1 - q1)); // float32 difference, one rounding
     }
+    bf16_t* xr = X + (size_t)j * 3 * d;
     *reinterpret_cast<u32x4*>(xr + c) = oe;
     *reinterpret_cast<u32x4*>(xr + d + c) = oh;
     *reinterpret_cast<u32x4*>(xr + 2 * d + c) = od;
@@ -446,23 +433,22 @@ GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base) 
 hipError_t launch_gate_means(const skip_problem_t& p, const void* Qtok,
                              const int32_t* q_offsets, const void* rows,
                              const int32_t* kept_offsets, const int32_t* kept_idx,
-                             GateScratch g, hipStream_t s) {
+                             const double* kbar, const float* passage_keys,
+                             const int32_t* query_passages, GateScratch g, hipStream_t s) {
   hipLaunchKernelGGL(gate_mean_kernel, dim3((p.d + 255) / 256, 2 * p.B), dim3(512), 0, s,
                      (const bf16_t*)Qtok, q_offsets, p.total_qtok, (const bf16_t*)rows,
-                     kept_offsets, kept_idx, p.N, p.total_kept, p.B, p.d, g.qbar, g.vbar);
+                     kept_offsets, kept_idx, p.N, p.total_kept, p.B, p.d, g.qbar, g.vbar, kbar,
+                     passage_keys, query_passages, p.total_passages, g.X, g.Xq, g.pq, g.done);
   return hipGetLastError();
 }
 
-hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* kbar,
-                       const float* passage_keys, const int32_t* query_passages,
-                       GateScratch g, float* logits, uint8_t* keep, hipStream_t s) {
+hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt,
+                       const int32_t* query_passages, GateScratch g, float* logits,
+                       uint8_t* keep, hipStream_t s) {
   const int T = p.total_passages, h = gt.hidden;
   if (T <= 0) return hipSuccess;
   int ch = 1, S = 1, Sq = 1;
   gate_split(T, h, p.d, &ch, &S, &Sq);
-  hipLaunchKernelGGL(gate_x_kernel, dim3(T + p.B), dim3(256), 0, s, (const double*)g.qbar,
-                     (const double*)g.vbar, kbar, passage_keys, query_passages, p.B, T, p.d,
-                     g.X, g.Xq, g.pq, g.done);
   const int n_rt = (T + kGateMT - 1) / kGateMT + (p.B + kGateMT - 1) / kGateMT;
   const int n_tiles = n_rt * (h / kGateNT);
   hipLaunchKernelGGL(gate_score_kernel, dim3(8 * ((S + 7) / 8) * n_tiles), dim3(256), 0, s,

@@ -495,10 +495,12 @@ skip_status_t skip_skv_gate(const skip_problem_t* p, const skip_skv_gate_t* gate
   hipStream_t s = static_cast<hipStream_t>(stream);
   Workspace w = carve_workspace(*p, workspace);
   GateScratch g = carve_gate_scratch(*p, gate->hidden, static_cast<char*>(workspace) + w.bytes);
-  // q_bar and v_bar, the passage keys when they are not given, the gate
-  SKIP_TRY(launch_gate_means(*p, Qtok, q_offsets, V_kept, kept_offsets, nullptr, g, s));
+  // the passage keys when they are not given, then q_bar, v_bar and the
+  // gate inputs, then the gate
   if (!passage_keys) SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-  SKIP_TRY(launch_gate(*p, *gate, w.kbar, passage_keys, query_passages, g, logits, keep, s));
+  SKIP_TRY(launch_gate_means(*p, Qtok, q_offsets, V_kept, kept_offsets, nullptr, w.kbar,
+                             passage_keys, query_passages, g, s));
+  SKIP_TRY(launch_gate(*p, *gate, query_passages, g, logits, keep, s));
   return SKIP_OK;
 }
 
@@ -565,14 +567,14 @@ static skip_status_t route_fused_impl(const skip_problem_t* p, const void* V,
                           passage_offsets, passage_keys ? 0 : p->total_passages, w.kbar, s));
   SKIP_TRY(mark());
   if (gate && p->total_passages > 0) {
-    // verify step: question and kept-row means, then the gate on the passage
-    // keys pooled above
+    // verify step: question and kept-row means with the gate inputs (from
+    // the passage keys pooled above), then the gate
     GateScratch g = carve_gate_scratch(*p, gate->hidden, static_cast<char*>(workspace) + w.bytes);
-    SKIP_TRY(launch_gate_means(*p, Qtok, q_offsets, V, kept_offsets, kept_idx, g, s));
     if (!work && !passage_keys)
       SKIP_TRY(launch_passage_keys(*p, Kh, passage_offsets, w.kbar, s));
-    SKIP_TRY(launch_gate(*p, *gate, w.kbar, passage_keys, query_passages, g, gate_logits,
-                         passage_keep, s));
+    SKIP_TRY(launch_gate_means(*p, Qtok, q_offsets, V, kept_offsets, kept_idx, w.kbar,
+                               passage_keys, query_passages, g, s));
+    SKIP_TRY(launch_gate(*p, *gate, query_passages, g, gate_logits, passage_keep, s));
   }
   if (work)
     SKIP_TRY(launch_edge_dot(*p, q, kept_offsets, query_passages, w.kbar, passage_keys,

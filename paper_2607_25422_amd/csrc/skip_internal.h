@@ -71,16 +71,19 @@ struct GateScratch {
 };
 size_t gate_scratch_bytes(const skip_problem_t& p, int hidden);
 GateScratch carve_gate_scratch(const skip_problem_t& p, int hidden, void* base);
-// g.qbar, g.vbar from the question tokens and the kept rows: rows[kept
-// range] when kept_idx is NULL, else V[b][kept_idx[r]] (rows = V)
+// g.qbar, g.vbar from the question tokens and the kept rows (rows[kept
+// range] when kept_idx is NULL, else V[b][kept_idx[r]], rows = V), and the
+// gate inputs g.X, g.Xq from them and the passage keys (kbar, or
+// passage_keys if given; complete before this launch)
 hipError_t launch_gate_means(const skip_problem_t& p, const void* Qtok,
                              const int32_t* q_offsets, const void* rows,
                              const int32_t* kept_offsets, const int32_t* kept_idx,
-                             GateScratch g, hipStream_t s);
-// the gate on g's means and the passage keys (kbar, or passage_keys if given)
-hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt, const double* kbar,
-                       const float* passage_keys, const int32_t* query_passages,
-                       GateScratch g, float* logits, uint8_t* keep, hipStream_t s);
+                             const double* kbar, const float* passage_keys,
+                             const int32_t* query_passages, GateScratch g, hipStream_t s);
+// the gate on the inputs launch_gate_means wrote
+hipError_t launch_gate(const skip_problem_t& p, const skip_skv_gate_t& gt,
+                       const int32_t* query_passages, GateScratch g, float* logits,
+                       uint8_t* keep, hipStream_t s);
 
 // Learned projection of the kept rows --------------------------------------
 size_t proj_scratch_bytes(int d, int d_out);
