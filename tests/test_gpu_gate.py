@@ -129,17 +129,19 @@ def test_gate_small_ragged(B, hidden, seed):
         check_gate(batch, w, logits, keep, ref, tau, rho, tag=f"h{hidden} tau={tau} rho={rho}")
 
 
+@pytest.mark.parametrize("hidden", [128, 4096])
 @pytest.mark.parametrize("given_keys", [False, True])
-def test_gate_many_questions_odd_group_count(B, given_keys):
+def test_gate_many_questions_odd_group_count(B, given_keys, hidden):
     """40 questions (two 32-row tiles of question blocks), 275 passages (a
     ragged last passage tile) and d = 192: the passage blocks' 3d columns
     are an odd number of 64-column groups (a wave's last round has spare
     slots), the question blocks' 2d columns fewer, so the two kinds of tile
-    take different group counts."""
+    take different group counts.  At h = 4096 (the largest gate) every
+    thread of the final kernel sums eight hidden units."""
     batch = wls.make_batch("llava_bf16", 42, B=40, N=120, H=3, d_h=64, T=(1, 3, 8),
                            k=(0, 7, 33, 64), P=(0, 1, 3, 6, 17), L_p=(1, 5, 40))
-    w = wls.make_gate_weights(batch.wl, 128, 42)
-    say(f"gate 40 questions d=192 given_keys={given_keys} P={batch.P.tolist()}")
+    w = wls.make_gate_weights(batch.wl, hidden, 42)
+    say(f"gate 40 questions d=192 h={hidden} given_keys={given_keys} P={batch.P.tolist()}")
     assert batch.wl.d == 192 and batch.B == 40
     db = B.to_device(batch)
     Vk = kept_rows_oracle(batch)
