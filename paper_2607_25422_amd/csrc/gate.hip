@@ -32,21 +32,6 @@
 
 namespace skip {
 
-namespace {
-
-// question of global passage index j (query_passages ascending)
-__device__ __forceinline__ int question_of(const int32_t* qp, int B, int total, int j) {
-  int lo = 0, hi = B;                      // answer in [0, B)
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (clampi(qp[mid], 0, total) <= j) lo = mid;
-    else hi = mid;
-  }
-  return lo;
-}
-
-}  // namespace
-
 constexpr int kGateRB = 2;         // 32-row MFMA blocks per score tile
 constexpr int kGateMT = 32 * kGateRB;  // rows (passages or questions) per score tile
 constexpr int kGateNT = 64;        // hidden units per score tile
